@@ -1,0 +1,341 @@
+"""Oracle: sparse DeepCNet(ell, k) forward and backward on the CPU, NumPy float64.
+
+TEST INFRASTRUCTURE ONLY -- the product path never imports this module.
+
+What is computed (the paper's own description, restated):
+
+* DeepCNet(ell, k) (Section 2.1): ell + 1 convolutional layers separated by ell
+  layers of 2x2 max-pooling; the n-th convolution has n*k filters, 3x3 in the
+  first layer and 2x2 afterwards; the input grid is N = 3 * 2**ell so that the
+  last convolution leaves a 1x1 grid; ReLU on hidden layers and a softmax
+  output layer (Section 2.1, activation paragraph).
+* Spatial sparsity (Section 2.3): every hidden variable has a ground state,
+  the value it takes when its input region holds no meaningful input; only
+  sites whose value can differ from it are computed.  Each layer keeps a
+  feature matrix (row 0 the ground state, then one row per active site) and a
+  pointer matrix (one entry per spatial location of the layer, naming that
+  location's feature-matrix row).  Backpropagation runs over the same
+  structures in reverse (Section 2.3, last paragraph).
+
+Readings where the paper is silent (each is also listed in the design notes):
+
+* convolutions are "valid" with stride 1 and cross-correlation orientation;
+  the weight row index is ``(dy*F + dx)*C_in + c`` (forced by N = 3*2**ell
+  reaching exactly 1x1, Section 2.1);
+* a site is active when any site of its receptive window in the layer below
+  is active, whatever the values (Figure 2's caption); input sites are active
+  exactly when listed;
+* the input ground state is 0 (zero background, Sections 1 and 2.5);
+* feature-matrix rows are in ascending (b, y, x) order;
+* max-pool argmax is the first maximal window position in row-major order
+  (dy, dx) = (0,0), (0,1), (1,0), (1,1);
+* ReLU'(0) = 0; the loss is softmax cross-entropy averaged over the batch;
+* the ground row takes part in backpropagation as one virtual site standing
+  for all inactive sites together, so weight and bias gradients equal those
+  of the dense network (derivation in ``backward``);
+* storage rounding: in mode "f32" every stored matrix is rounded to float32;
+  in mode "bf16" activations, gradients fed to products and the softmax
+  layer's input/gradients are rounded to bfloat16 (round to nearest even)
+  while sums stay in float64 here (float32 on the GPU); weight and bias
+  gradients and logits are float32.  Mode "f64" rounds nothing and is what
+  the pins against the dense network use.
+"""
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+
+class OracleInputError(ValueError):
+    """Raised for inputs the method does not define: duplicate or out-of-range sites."""
+
+    def __init__(self, kind: str, msg: str):
+        super().__init__(f"{kind}: {msg}")
+        self.kind = kind
+
+
+# ---------------------------------------------------------------------------
+# storage rounding
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bfloat16 through float32, nearest-even at each step.
+
+    bfloat16 keeps the upper 16 bits of an IEEE float32.  Rounding adds 0x7FFF
+    plus the lowest kept bit to the 32-bit pattern before truncation, which is
+    round-to-nearest with ties to even.  (Finite inputs only.)
+    """
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def round_f32(x: np.ndarray) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def round_store(x: np.ndarray, mode: str) -> np.ndarray:
+    """Round to the storage type of ``mode`` ("f64": none, "f32", "bf16")."""
+    if mode == "f64":
+        return np.asarray(x, dtype=np.float64)
+    if mode == "f32":
+        return round_f32(x)
+    if mode == "bf16":
+        return round_bf16(x)
+    raise ValueError(mode)
+
+
+# ---------------------------------------------------------------------------
+# architecture
+
+
+@dataclass(frozen=True)
+class Stage:
+    kind: str  # "conv" or "pool"
+    F: int  # window side: 3 or 2 for convolutions, 2 for pooling
+    S_in: int  # spatial side of the layer below
+    S: int  # spatial side of this layer
+    c_in: int
+    c_out: int
+
+    @property
+    def A(self) -> int:
+        return self.F * self.F
+
+
+def stage_plan(ell: int, k: int, c_in: int) -> List[Stage]:
+    """The 2*ell + 1 stages of DeepCNet(ell, k) on an N = 3*2**ell input (Section 2.1).
+
+    A valid FxF convolution shrinks the side by F - 1; a 2x2 stride-2 pool halves it.
+    """
+    if ell < 1 or k < 1 or c_in < 1:
+        raise ValueError("ell, k and c_in must be positive")
+    N = 3 * 2 ** ell
+    stages = [Stage("conv", 3, N, N - 2, c_in, k)]
+    S, C = N - 2, k
+    for n in range(2, ell + 2):
+        stages.append(Stage("pool", 2, S, S // 2, C, C))
+        S //= 2
+        stages.append(Stage("conv", 2, S, S - 1, C, n * k))
+        S, C = S - 1, n * k
+    assert S == 1
+    return stages
+
+
+# ---------------------------------------------------------------------------
+# the sparse network
+
+
+@dataclass
+class Layer:
+    """One layer's structures (Section 2.3).
+
+    ``P``: pointer matrix [B, S, S]; 0 means "inactive, use the ground row".
+    ``sites``: [n, 3] (b, y, x) of rows 1..n, in ascending order.
+    ``R``: [n + 1, A] rows of the layer below read by each row's window (row 0 all 0).
+    ``X``: feature matrix [n + 1, C], row 0 the ground state.
+    """
+
+    S: int
+    P: np.ndarray
+    sites: np.ndarray
+    R: Optional[np.ndarray] = None
+    X: Optional[np.ndarray] = None
+    argmax: Optional[np.ndarray] = None  # pooling layers: [n + 1, C] window position of the max
+    grad: Optional[np.ndarray] = None  # conv: dL/dZ (pre-activation); pool and input: dL/dX
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def n(self) -> int:
+        return int(self.sites.shape[0])
+
+
+def _pointer_from_active(active: np.ndarray):
+    """Number the active locations 1..n in ascending (b, y, x) order."""
+    b, y, x = np.nonzero(active)
+    P = np.zeros(active.shape, dtype=np.int64)
+    P[b, y, x] = np.arange(1, b.size + 1)
+    return P, np.stack([b, y, x], axis=1).astype(np.int64)
+
+
+class SparseDeepCNet:
+    """Sparse DeepCNet(ell, k) with a softmax head; calls mirror the C interface.
+
+    ``build`` makes every layer's pointer matrix and window lists, ``forward``
+    fills the feature matrices and the loss, ``backward`` returns parameter
+    gradients and, per layer, the gradient matrices.
+    """
+
+    def __init__(self, ell: int, k: int, c_in: int, n_classes: int, mode: str = "f64"):
+        if mode not in ("f64", "f32", "bf16"):
+            raise ValueError(mode)
+        self.ell, self.k, self.c_in, self.n_classes, self.mode = ell, k, c_in, n_classes, mode
+        self.N = 3 * 2 ** ell
+        self.stages = stage_plan(ell, k, c_in)
+        self.layers: List[Layer] = []
+
+    # -- parameters ---------------------------------------------------------
+    def param_shapes(self):
+        """Weight shapes: convolutions ``[F*F*C_in, C_out]``, then the softmax layer ``[C_last, classes]``."""
+        shapes = [(s.A * s.c_in, s.c_out) for s in self.stages if s.kind == "conv"]
+        shapes.append((self.stages[-1].c_out, self.n_classes))
+        return shapes
+
+    # -- structure ----------------------------------------------------------
+    def build(self, coords: np.ndarray, batch: int):
+        """Pointer matrices and window lists for every layer (Section 2.3).
+
+        Input layer: the listed sites are active, numbered in ascending order.
+        Convolution layer: a location is active when some location of its FxF
+        window in the layer below is active; its window list names the rows of
+        those F*F locations (0 for the inactive ones).  Pooling layer: the same
+        with the 2x2 stride-2 window.
+        """
+        coords = np.asarray(coords, dtype=np.int64).reshape(-1, 3)
+        N = self.N
+        if batch < 0:
+            raise OracleInputError("invalid_argument", "negative batch")
+        if coords.size:
+            b, y, x = coords[:, 0], coords[:, 1], coords[:, 2]
+            bad = (b < 0) | (b >= batch) | (y < 0) | (y >= N) | (x < 0) | (x >= N)
+            if bad.any():
+                raise OracleInputError("out_of_range", f"site {coords[np.argmax(bad)].tolist()} outside batch/grid")
+            keys = (b * N + y) * N + x
+            if np.unique(keys).size != keys.size:
+                raise OracleInputError("duplicate", "a site is listed twice")
+        self.batch = batch
+        n_in = coords.shape[0]
+        P0 = np.zeros((batch, N, N), dtype=np.int64)
+        if n_in:
+            keys = (coords[:, 0] * N + coords[:, 1]) * N + coords[:, 2]
+            order = np.argsort(keys, kind="stable")  # row r+1 holds caller site order[r]
+            P0[coords[order, 0], coords[order, 1], coords[order, 2]] = np.arange(1, n_in + 1)
+        else:
+            order = np.zeros(0, dtype=np.int64)
+        self.input_order = order
+        self.layers = [Layer(S=N, P=P0, sites=coords[order] if n_in else np.zeros((0, 3), np.int64))]
+
+        for st in self.stages:
+            below = self.layers[-1]
+            step = 1 if st.kind == "conv" else 2
+            # window location (dy, dx) of output (Y, X) is (step*Y + dy, step*X + dx) below
+            win = np.zeros((batch, st.S, st.S, st.A), dtype=np.int64)
+            for dy in range(st.F):
+                for dx in range(st.F):
+                    win[..., dy * st.F + dx] = below.P[:, dy: dy + step * st.S: step, dx: dx + step * st.S: step]
+            active = (win != 0).any(axis=-1)
+            P, sites = _pointer_from_active(active)
+            R = np.zeros((sites.shape[0] + 1, st.A), dtype=np.int64)
+            R[1:] = win[sites[:, 0], sites[:, 1], sites[:, 2]]
+            self.layers.append(Layer(S=st.S, P=P, sites=sites, R=R))
+        return self.layer_sizes()
+
+    def layer_sizes(self):
+        """Active-site counts n_0 .. n_{2 ell + 1} (ground rows not counted)."""
+        return [L.n for L in self.layers]
+
+    def head_rows(self) -> np.ndarray:
+        """Row of each sample's single top-layer site (0, the ground row, for an empty sample)."""
+        return self.layers[-1].P[:, 0, 0].copy()
+
+    # -- forward ------------------------------------------------------------
+    def forward(self, feats, Ws, bs, labels):
+        """Feature matrices of every layer, logits and mean softmax cross-entropy.
+
+        Convolution: row o of the output is ReLU(b + sum_f W_f^T x_{R[o][f]}),
+        row 0 included -- its window is all ground rows, which makes it the
+        layer's ground state.  Pooling: channel-wise max over the window's rows
+        (row 0 passes the ground state through).  Head: each sample's top-layer
+        row (the ground row if the sample is empty) feeds the softmax layer.
+        """
+        m = self.mode
+        L0 = self.layers[0]
+        feats = np.asarray(feats, dtype=np.float64).reshape(-1, self.c_in)
+        X = np.zeros((L0.n + 1, self.c_in))
+        X[1:] = feats[self.input_order]
+        L0.X = round_store(X, m)
+        self.Ws = [round_store(np.asarray(W, dtype=np.float64), m) for W in Ws]
+        self.bs = [np.asarray(b, dtype=np.float64) for b in bs]
+        ci = 0
+        for si, st in enumerate(self.stages):
+            L, below = self.layers[si + 1], self.layers[si]
+            V = below.X[L.R]  # [n + 1, A, C_in]: the gathered windows
+            if st.kind == "conv":
+                Z = V.reshape(V.shape[0], -1) @ self.Ws[ci] + self.bs[ci]
+                L.X = round_store(np.maximum(Z, 0.0), m)
+                ci += 1
+            else:
+                L.argmax = np.argmax(V, axis=1)  # first maximal window position
+                L.X = V.max(axis=1)
+        rows = self.head_rows()
+        self.h = self.layers[-1].X[rows]
+        logits = self.h @ self.Ws[-1] + self.bs[-1]
+        self.logits = logits if m == "f64" else round_f32(logits)
+        labels = np.asarray(labels, dtype=np.int64)
+        self.labels = labels
+        z = self.logits - self.logits.max(axis=1, keepdims=True)
+        lse = np.log(np.exp(z).sum(axis=1))
+        self.loss = float(np.mean(lse - z[np.arange(self.batch), labels])) if self.batch else 0.0
+        return self.logits, self.loss
+
+    # -- backward -----------------------------------------------------------
+    def backward(self):
+        """Gradients of the mean loss with respect to every parameter and layer.
+
+        Each layer's gradient matrix has the feature matrix's rows; row 0 holds
+        the sum of the dense network's gradients over all of that layer's
+        inactive sites.  Because an inactive output's window is entirely
+        inactive, its contribution to a weight gradient is (ground row) x
+        (its gradient), so summing those gradients into row 0 first and then
+        treating row 0 as one more site gives the dense weight and bias
+        gradients exactly; the same argument gives row 0 of the layer below.
+        """
+        m = self.mode
+        B = self.batch
+        p = np.exp(self.logits - self.logits.max(axis=1, keepdims=True))
+        p /= p.sum(axis=1, keepdims=True)
+        onehot = np.zeros_like(p)
+        onehot[np.arange(B), self.labels] = 1.0
+        dlogits = round_store((p - onehot) / max(B, 1), m)
+        self.dlogits = dlogits
+        dW = [None] * len(self.Ws)
+        db = [None] * len(self.Ws)
+        dW[-1] = self.h.T @ dlogits
+        db[-1] = dlogits.sum(axis=0)
+        dh = dlogits @ self.Ws[-1].T
+        top = self.layers[-1]
+        dY = np.zeros_like(top.X)
+        np.add.at(dY, self.head_rows(), dh)
+        top.grad = round_store(dY * (top.X > 0), m)  # dL/dZ of the last convolution
+
+        ci = len(self.Ws) - 2
+        for si in range(len(self.stages) - 1, -1, -1):
+            st, L, below = self.stages[si], self.layers[si + 1], self.layers[si]
+            if st.kind == "conv":
+                delta = L.grad  # [n + 1, C_out]
+                V = below.X[L.R].reshape(L.R.shape[0], -1)
+                dW[ci] = V.T @ delta
+                db[ci] = delta.sum(axis=0)
+                dV = (delta @ self.Ws[ci].T).reshape(L.R.shape[0], st.A, st.c_in)
+                dX = np.zeros((below.n + 1, st.c_in))
+                np.add.at(dX, L.R.ravel(), dV.reshape(-1, st.c_in))
+                below.grad = round_store(dX, m)  # pooling layer (or input): dL/dX
+                ci -= 1
+            else:
+                dYp = L.grad  # dL/dY of the pooling layer
+                rows = L.R[np.arange(L.R.shape[0])[:, None], L.argmax]  # [n + 1, C] row of each max
+                dX = np.zeros((below.n + 1, st.c_in))
+                np.add.at(dX, (rows, np.broadcast_to(np.arange(st.c_in), rows.shape)), dYp)
+                below.grad = round_store(dX * (below.X > 0), m)  # the convolution below: dL/dZ
+        self.dW, self.db = dW, db
+        dfeats = np.zeros((self.layers[0].n, self.c_in))
+        dfeats[self.input_order] = self.layers[0].grad[1:]
+        self.dfeats = dfeats
+        return dW, db, dfeats
+
+    # -- inspection ---------------------------------------------------------
+    def layer_view(self, i: int) -> Layer:
+        """Layer i: 0 is the input, 1 .. 2 ell + 1 follow the stages."""
+        return self.layers[i]

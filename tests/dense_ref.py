@@ -1,0 +1,85 @@
+"""Dense brute force for pinning the oracle: the ordinary (non-sparse) DeepCNet.
+
+The sparse method is an exact memoisation of the dense network evaluated on a
+zero-filled N x N input grid (Section 2.3), so the dense network computed with
+library routines -- torch's conv2d / max_pool2d / relu / cross_entropy and
+autograd, on the CPU in float64 -- is an independent statement of the result.
+It shares nothing with the oracle beyond the weight layout convention
+(row ``(dy*F + dx)*C_in + c`` of a ``[F*F*C_in, C_out]`` matrix).
+"""
+
+import numpy as np
+import torch
+import torch.nn.functional as Fn
+
+
+def conv_weight(W: np.ndarray, F: int, c_in: int) -> torch.Tensor:
+    """[F*F*C_in, C_out] -> torch's [C_out, C_in, F, F] (cross-correlation)."""
+    c_out = W.shape[1]
+    w = torch.tensor(W, dtype=torch.float64).reshape(F, F, c_in, c_out)
+    return w.permute(3, 2, 0, 1).contiguous()
+
+
+def dense_grid(coords, feats, batch, N, c_in):
+    x = torch.zeros(batch, c_in, N, N, dtype=torch.float64)
+    coords = np.asarray(coords).reshape(-1, 3)
+    if coords.shape[0]:
+        x[coords[:, 0], :, coords[:, 1], coords[:, 2]] = torch.tensor(np.asarray(feats), dtype=torch.float64)
+    return x
+
+
+class DenseDeepCNet:
+    """Dense DeepCNet(ell, k): 3x3 conv, then (2x2/2 max-pool, 2x2 conv) x ell, ReLU, softmax head."""
+
+    def __init__(self, ell, k, c_in, n_classes):
+        self.ell, self.k, self.c_in, self.n_classes = ell, k, c_in, n_classes
+        self.N = 3 * 2 ** ell
+
+    def run(self, coords, feats, batch, Ws, bs, labels):
+        x = dense_grid(coords, feats, batch, self.N, self.c_in).requires_grad_(True)
+        params = []
+        for W, b in zip(Ws, bs):
+            params.append(torch.tensor(np.asarray(W), dtype=torch.float64, requires_grad=True))
+            params.append(torch.tensor(np.asarray(b), dtype=torch.float64, requires_grad=True))
+        Zs, Ys = [], []  # per stage: pre-activation (conv) and output
+        h = x
+        c = self.c_in
+        for li in range(self.ell + 1):
+            if li > 0:
+                h = Fn.max_pool2d(h, 2)
+                h.retain_grad()
+                Zs.append(None)
+                Ys.append(h)
+            F = 3 if li == 0 else 2
+            W, b = params[2 * li], params[2 * li + 1]
+            wt = W.reshape(F, F, c, W.shape[1]).permute(3, 2, 0, 1)
+            z = Fn.conv2d(h, wt) + b.view(1, -1, 1, 1)
+            z.retain_grad()
+            h = torch.relu(z)
+            Zs.append(z)
+            Ys.append(h)
+            c = W.shape[1]
+        assert h.shape[-1] == 1 and h.shape[-2] == 1
+        feat = h[:, :, 0, 0]
+        logits = feat @ params[-2] + params[-1]
+        loss = Fn.cross_entropy(logits, torch.tensor(np.asarray(labels), dtype=torch.int64))
+        loss.backward()
+        self.x, self.params, self.Zs, self.Ys = x, params, Zs, Ys
+        self.logits, self.loss = logits.detach().numpy(), float(loss)
+        self.dW = [p.grad.numpy() for p in params[0::2]]
+        self.db = [p.grad.numpy() for p in params[1::2]]
+        return self
+
+
+def dilate_reference(active: np.ndarray, kind: str, F: int) -> np.ndarray:
+    """Active set of the next layer from a boolean [B, S, S] grid, via library routines.
+
+    Convolution: conv2d of the indicator with an all-ones FxF kernel is non-zero.
+    Pooling: max_pool2d(2) of the indicator.
+    """
+    t = torch.tensor(active.astype(np.float64))[:, None]
+    if kind == "conv":
+        out = Fn.conv2d(t, torch.ones(1, 1, F, F, dtype=torch.float64)) > 0
+    else:
+        out = Fn.max_pool2d(t, 2) > 0
+    return out[:, 0].numpy()
