@@ -67,9 +67,13 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     round-to-nearest with ties to even.  (Finite inputs only.)
     """
     f = np.asarray(x, dtype=np.float64).astype(np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+    u = f.view(np.uint32)
+    lsb = u >> 16
+    lsb &= 1
+    u += np.uint32(0x7FFF)  # cannot overflow: finite patterns are <= 0xFF7FFFFF
+    u += lsb
+    u &= np.uint32(0xFFFF0000)
+    return f.astype(np.float64)
 
 
 def round_f32(x: np.ndarray) -> np.ndarray:
@@ -144,6 +148,7 @@ class Layer:
     R: Optional[np.ndarray] = None
     X: Optional[np.ndarray] = None
     argmax: Optional[np.ndarray] = None  # pooling layers: [n + 1, C] window position of the max
+    relu_on: Optional[np.ndarray] = None  # convolution layers: [n + 1, C] ReLU derivative, 1 where X > 0
     grad: Optional[np.ndarray] = None  # conv: dL/dZ (pre-activation); pool and input: dL/dX
     extra: dict = field(default_factory=dict)
 
@@ -265,6 +270,7 @@ class SparseDeepCNet:
             if st.kind == "conv":
                 Z = V.reshape(V.shape[0], -1) @ self.Ws[ci] + self.bs[ci]
                 L.X = round_store(np.maximum(Z, 0.0), m)
+                L.relu_on = L.X > 0  # ReLU'(Z): 1 where the stored output is positive, 0 at Z <= 0
                 ci += 1
             else:
                 L.argmax = np.argmax(V, axis=1)  # first maximal window position
@@ -308,7 +314,7 @@ class SparseDeepCNet:
         top = self.layers[-1]
         dY = np.zeros_like(top.X)
         np.add.at(dY, self.head_rows(), dh)
-        top.grad = round_store(dY * (top.X > 0), m)  # dL/dZ of the last convolution
+        top.grad = round_store(dY * top.relu_on, m)  # dL/dZ of the last convolution
 
         ci = len(self.Ws) - 2
         for si in range(len(self.stages) - 1, -1, -1):
@@ -328,7 +334,7 @@ class SparseDeepCNet:
                 rows = L.R[np.arange(L.R.shape[0])[:, None], L.argmax]  # [n + 1, C] row of each max
                 dX = np.zeros((below.n + 1, st.c_in))
                 np.add.at(dX, (rows, np.broadcast_to(np.arange(st.c_in), rows.shape)), dYp)
-                below.grad = round_store(dX * (below.X > 0), m)  # the convolution below: dL/dZ
+                below.grad = round_store(dX * below.relu_on, m)  # the convolution below: dL/dZ
         self.dW, self.db = dW, db
         dfeats = np.zeros((self.layers[0].n, self.c_in))
         dfeats[self.input_order] = self.layers[0].grad[1:]
