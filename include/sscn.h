@@ -1,0 +1,168 @@
+/*
+ * sscn.h -- spatially-sparse DeepCNet forward and backward pass on one AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The calls follow the statement of the problem in Graham, "Spatially-sparse
+ * convolutional neural networks" (arXiv:1409.6070): a batch of active sites,
+ * each with a feature vector, on an N x N grid (Sections 1, 2.4, 2.5), fed to
+ * the layer list of a DeepCNet(ell, k) (Section 2.1):
+ *
+ *     input - kC3 - MP2 - 2kC2 - MP2 - ... - (ell+1)kC2 - softmax output
+ *
+ * with N = 3 * 2^ell, valid stride-1 convolutions, 2x2 stride-2 max-pooling,
+ * ReLU on hidden layers.  Only active sites are computed; every inactive site
+ * of a layer shares that layer's ground state (Section 2.3), kept as row 0 of
+ * the layer's feature matrix.
+ *
+ * Memory ownership.  The caller owns every device buffer: inputs, parameters,
+ * gradients, logits, loss and one workspace.  The library never allocates or
+ * frees device memory and never synchronises, except in sscn_layer_sizes().
+ * All work is enqueued on the stream passed in (a hipStream_t, NULL for the
+ * null stream).  A net is used from one host thread and one stream at a time.
+ *
+ * Layouts.  Row-major throughout.  Convolution weight n (n = 0 .. ell) is a
+ * [F*F*C_in, C_out] matrix whose row index is (dy*F + dx)*C_in + c
+ * (cross-correlation: output (y, x) reads input (y+dy, x+dx)); F = 3 for
+ * n = 0, else 2.  The softmax layer (index ell+1) is [C_last, n_classes].
+ * Weights and input features are in the net's storage dtype; biases, weight
+ * and bias gradients, logits and the loss are float32.
+ *
+ * Errors.  Argument errors are returned at once.  Data errors found on the
+ * device (a site outside the grid or batch, a site listed twice) are latched
+ * in the workspace and returned by the next sscn_layer_sizes(); results
+ * computed from such input are undefined but every kernel stays within its
+ * buffers.  No C++ exception crosses this interface and nothing exits the
+ * process.
+ */
+#ifndef SSCN_H
+#define SSCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define SSCN_API __attribute__((visibility("default")))
+#else
+#define SSCN_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SSCN_OK = 0,
+  SSCN_ERR_INVALID_ARGUMENT = 1, /* null pointer, bad size or index          */
+  SSCN_ERR_OUT_OF_RANGE = 2,     /* a site outside [0,batch) x [0,N)^2        */
+  SSCN_ERR_DUPLICATE_SITE = 3,   /* the same (b, y, x) listed twice           */
+  SSCN_ERR_CAPACITY = 4,         /* n > max_active or batch > batch_max       */
+  SSCN_ERR_BAD_STATE = 5,        /* call out of order (e.g. forward before build) */
+  SSCN_ERR_HIP = 6,              /* a HIP runtime call failed                 */
+  SSCN_ERR_WORKSPACE = 7         /* workspace null, too small or misaligned   */
+} sscn_status;
+
+typedef enum { SSCN_F32 = 0, SSCN_BF16 = 1 } sscn_dtype;
+
+/* DeepCNet(ell, k) with c_in input features per site and an n_classes softmax
+ * output (Section 2.1).  batch_max and max_active bound the batches that
+ * sscn_rulebook_build accepts and size the workspace.  dtype is the storage
+ * type of features, weights and stored activations/gradients; products and
+ * sums accumulate in float32. */
+typedef struct {
+  int32_t ell;
+  int32_t k;
+  int32_t c_in;
+  int32_t n_classes;
+  int32_t batch_max;
+  int32_t max_active;
+  int32_t dtype; /* sscn_dtype */
+} sscn_net_desc;
+
+typedef struct sscn_net sscn_net; /* opaque host-side plan */
+
+/* One layer of the network as stored in the workspace (for tests and
+ * inspection).  Layer 0 is the input; layer s = 1 .. 2*ell+1 is the output of
+ * stage s (odd s: convolution, even s: pooling).  All pointers are device
+ * pointers into the workspace bound by the last sscn_rulebook_build. */
+typedef struct {
+  int32_t kind;       /* 0 input, 1 convolution, 2 max-pooling                  */
+  int32_t side;       /* spatial side S of the layer                            */
+  int32_t channels;   /* C: features per site                                   */
+  int32_t row_stride; /* elements per feature/gradient row (C rounded up)       */
+  int32_t window;     /* A = F*F positions per window (0 for the input layer)   */
+  int32_t capacity;   /* rows available for active sites (ground row excluded)  */
+  const int32_t* count;  /* [1] number n of active sites, set by rulebook_build  */
+  const int32_t* sites;  /* [capacity] rows 1..n: key (b*S + y)*S + x, ascending */
+  const int32_t* rules;  /* [(capacity+1) * A]: row of the layer below read by
+                            window position (dy*F + dx) of each row; 0 = ground;
+                            row 0 is all 0                                      */
+  const int32_t* rules_t;/* convolution: [(capacity_below+1) * A]: for each row
+                            i of the layer below, the row whose window holds i at
+                            position f, -1 if none.  Pooling: [capacity_below+1]
+                            parent row * 4 + position, -1 if none.              */
+  void* features;        /* [(capacity+1) * row_stride] storage dtype, row 0 = ground */
+  void* grad;            /* same shape: convolution dL/dZ (pre-activation),
+                            pooling and input dL/dX; row 0 = sum over inactive sites */
+  uint8_t* argmax;       /* pooling: [(capacity+1) * row_stride] window position
+                            (0..3, first maximum in (dy, dx) order) of each max  */
+} sscn_layer_view;
+
+/* Host only.  Validates desc (ell in 1..8, k, c_in, n_classes, batch_max,
+ * max_active >= 1, dtype known) and builds the plan. */
+SSCN_API sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out);
+SSCN_API void sscn_net_destroy(sscn_net* net);
+SSCN_API const char* sscn_status_string(int32_t status);
+
+/* Number of parameter matrices (ell + 2) and the shape of matrix `layer`
+ * (0 .. ell convolutions, ell+1 softmax layer); the bias has `cols` entries.
+ * Section 2.1 gives the weight count 3^2*M*k + sum_n 2^2*(n k)*((n+1) k). */
+SSCN_API int32_t sscn_net_num_params(const sscn_net* net);
+SSCN_API sscn_status sscn_net_param_shape(const sscn_net* net, int32_t layer, int64_t* rows, int64_t* cols);
+
+/* Bytes of device workspace the net needs (an upper bound for any batch
+ * within batch_max / max_active).  The workspace must be 256-byte aligned
+ * and left untouched from sscn_rulebook_build through sscn_backward. */
+SSCN_API sscn_status sscn_net_workspace_bytes(const sscn_net* net, size_t* bytes);
+
+/* Builds every layer's active-site set and window lists (Section 2.3: the
+ * pointer matrix, here a rank-indexed occupancy bitmap per layer) for
+ * d_coords[n][3] = (b, y, x), int32, any order, 0 <= b < batch, 0 <= y,x < N.
+ * Rows are numbered in ascending (b, y, x) order.  Asynchronous; device-side
+ * input errors are reported by sscn_layer_sizes. */
+SSCN_API sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t n, int32_t batch,
+                                void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* Synchronises `stream`, copies the 2*ell+2 active-site counts (layer 0 =
+ * input, then each stage) to h_counts, and returns any latched input error
+ * (SSCN_ERR_OUT_OF_RANGE / SSCN_ERR_DUPLICATE_SITE). */
+SSCN_API sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream);
+
+/* Forward pass (Sections 2.1, 2.3): d_feats[n][c_in] (storage dtype, in the
+ * order given to sscn_rulebook_build); h_W / h_b host arrays of ell+2 device
+ * pointers (weights in storage dtype, biases float32); d_labels[batch] int32
+ * in [0, n_classes).  Writes d_logits[batch][n_classes] and *d_loss (mean
+ * softmax cross-entropy), both float32. */
+SSCN_API sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
+                         const int32_t* d_labels, float* d_logits, float* d_loss, void* stream);
+
+/* Backward pass of the last sscn_forward (Section 2.3: the same structures in
+ * reverse).  h_dW / h_db: host arrays of ell+2 device float32 pointers shaped
+ * like the parameters; they are overwritten (not accumulated).  d_dfeats
+ * (nullable): [n][c_in] storage dtype, gradient of the loss with respect to
+ * the input features, in the caller's site order. */
+SSCN_API sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db, void* d_dfeats, void* stream);
+
+/* Runs only stage s (1 .. 2*ell+1) of the forward or backward pass on the
+ * current workspace contents, with the parameters of the last sscn_forward /
+ * sscn_backward.  For checking one kernel group against known inputs. */
+SSCN_API sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream);
+SSCN_API sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream);
+
+/* Describes layer `layer` (0 .. 2*ell+1) of the bound workspace. */
+SSCN_API sscn_status sscn_layer_view_get(const sscn_net* net, int32_t layer, sscn_layer_view* out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSCN_H */

@@ -1,0 +1,67 @@
+"""Builds libsscn.so (the HIP kernels and the C interface) in-tree for gfx950.
+
+    python -m paper_1409_6070_amd.build
+
+Every source is compiled with hipcc for gfx950 only; packed-fp32 instructions
+are disabled (``-Xclang -target-feature -Xclang -packed-fp32-ops``) so the
+compiler never emits v_pk_{add,mul,fma}_f32.
+"""
+
+import os
+import subprocess
+import sys
+from concurrent.futures import ThreadPoolExecutor
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "csrc")
+BUILD = os.path.join(HERE, "_build")
+LIB = os.path.join(HERE, "libsscn.so")
+SOURCES = ["rulebook.hip", "gemm.hip", "pool.hip", "head.hip", "api.hip"]
+ARCH = "gfx950"
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+CFLAGS = [
+    f"--offload-arch={ARCH}",
+    "-O3",
+    "-std=c++17",
+    "-fPIC",
+    "-fvisibility=hidden",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall",
+    "-Wno-unused-result",
+]
+
+
+def _run(cmd):
+    p = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    out = "\n".join(l for l in p.stdout.splitlines() if "unknown target feature" not in l and "packed-fp32-ops" not in l)
+    return p.returncode, out
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    jobs = []
+    for src in SOURCES:
+        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        jobs.append((src, [HIPCC, *CFLAGS, "-I", os.path.join(HERE, "..", "include"), "-c",
+                           os.path.join(CSRC, src), "-o", obj], obj))
+    with ThreadPoolExecutor(max_workers=min(len(jobs), 8)) as ex:
+        results = list(ex.map(lambda j: (j[0], *_run(j[1])), jobs))
+    failed = [(s, out) for s, rc, out in results if rc != 0]
+    for s, rc, out in results:
+        if verbose and out.strip():
+            print(f"[{s}]\n{out}")
+    if failed:
+        msg = "\n".join(f"--- {s}\n{out}" for s, out in failed)
+        raise RuntimeError(f"hipcc failed:\n{msg}")
+    tmp = LIB + ".tmp"
+    rc, out = _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *[j[2] for j in jobs]])
+    if rc != 0:
+        raise RuntimeError(f"link failed:\n{out}")
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    path = build(verbose="-v" in sys.argv)
+    print(path)

@@ -1,0 +1,586 @@
+// C interface of libsscn: plan, workspace layout and launch sequencing for the
+// spatially-sparse DeepCNet forward and backward pass (arXiv:1409.6070,
+// Sections 2.1 and 2.3).  Host code only; every kernel is enqueued on the
+// caller's stream and no call synchronises except sscn_layer_sizes().
+
+#include <cstring>
+#include <new>
+
+#include "../../include/sscn.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace sscn;
+
+namespace {
+
+struct LayerPlan {
+  int kind;  // 0 input, 1 conv, 2 pool
+  int S, C, Cp, F, A, Wd;
+  int64_t cap;
+  int conv_index;  // convolution layers: parameter index
+  // workspace pointers
+  uint64_t* bits;
+  int32_t* wpre;
+  int32_t* scount;
+  int32_t* soff;
+  int32_t* sites;
+  void* X;
+  void* grad;
+  int32_t* rules;
+  int32_t* rules_t;
+  uint8_t* argmax;
+};
+
+struct ParamPlan {
+  int A, c_in, c_out, cp_in, cp_out;  // FC: A = 1, cp_in = Cp_last, cp_out = dlogits stride
+  int NpadF, KpadF, NpadD, KpadD;
+  int Mpad_w, Npad_w, nchunks, m_ones, m_ind;
+  void* WpF;
+  void* WpD;
+};
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    off = (off + 255) / 256 * 256;
+    void* p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+}  // namespace
+
+struct sscn_net {
+  sscn_net_desc d;
+  bool bf16;
+  int esz, VE;
+  int nlayers;
+  int nparams;
+  LayerPlan L[MAX_LAYERS];
+  ParamPlan P[MAX_LAYERS];
+  int dl_stride;  // dlogits row stride (elements)
+  int pool_parts;
+  // global workspace pointers
+  int32_t* counts;
+  int32_t* err;
+  int32_t* perm;
+  int32_t* head_rows;
+  void* dlogits;
+  float* dh;
+  float* loss_part;
+  float* wpart;
+  float* D0;
+  float* ppart;
+  size_t ws_bytes;
+  int32_t max_words;
+  // bound state
+  void* ws;
+  int batch;
+  int n;
+  bool built, forwarded;
+  const void* W[MAX_LAYERS];
+  const float* b[MAX_LAYERS];
+  float* dW[MAX_LAYERS];
+  float* db[MAX_LAYERS];
+  bool want_dfeats;
+  float* logits;
+  const int32_t* labels;
+};
+
+static void carve(sscn_net* net, void* base) {
+  Carver cv(base);
+  const int B = net->d.batch_max;
+  net->counts = (int32_t*)cv.take(sizeof(int32_t) * net->nlayers);
+  net->err = (int32_t*)cv.take(sizeof(int32_t) * 4);
+  net->perm = (int32_t*)cv.take(sizeof(int32_t) * (size_t)net->d.max_active);
+  net->head_rows = (int32_t*)cv.take(sizeof(int32_t) * (size_t)B);
+  size_t max_part = 0, max_d0 = 0;
+  int max_cp = 0;
+  for (int s = 0; s < net->nlayers; ++s) {
+    LayerPlan& L = net->L[s];
+    const size_t words = (size_t)B * L.S * L.Wd;
+    L.bits = (uint64_t*)cv.take(words * 8);
+    L.wpre = (int32_t*)cv.take(words * 4);
+    L.scount = (int32_t*)cv.take((size_t)B * 4);
+    L.soff = (int32_t*)cv.take((size_t)B * 4);
+    L.sites = (int32_t*)cv.take((size_t)L.cap * 4);
+    L.X = cv.take((size_t)(L.cap + 1) * L.Cp * net->esz);
+    L.grad = cv.take((size_t)(L.cap + 1) * L.Cp * net->esz);
+    max_cp = std::max(max_cp, L.Cp);
+    if (s >= 1) {
+      const LayerPlan& Lb = net->L[s - 1];
+      L.rules = (int32_t*)cv.take((size_t)(L.cap + 1) * L.A * 4);
+      if (L.kind == 1)
+        L.rules_t = (int32_t*)cv.take((size_t)(Lb.cap + 1) * L.A * 4);
+      else
+        L.rules_t = (int32_t*)cv.take((size_t)(Lb.cap + 1) * 4);
+      L.argmax = (L.kind == 2) ? (uint8_t*)cv.take((size_t)(L.cap + 1) * L.Cp) : nullptr;
+    } else {
+      L.rules = L.rules_t = nullptr;
+      L.argmax = nullptr;
+    }
+  }
+  for (int p = 0; p < net->nparams; ++p) {
+    ParamPlan& P = net->P[p];
+    P.WpF = cv.take((size_t)P.NpadF * P.KpadF * net->esz);
+    P.WpD = cv.take((size_t)P.NpadD * P.KpadD * net->esz);
+    max_part = std::max(max_part, (size_t)P.nchunks * P.Mpad_w * P.Npad_w);
+    max_d0 = std::max(max_d0, (size_t)P.A * P.c_out);
+  }
+  const LayerPlan& Lt = net->L[net->nlayers - 1];
+  net->dlogits = cv.take((size_t)B * net->dl_stride * net->esz);
+  net->dh = (float*)cv.take((size_t)B * Lt.Cp * 4);
+  net->loss_part = (float*)cv.take((size_t)B * 4);
+  net->wpart = (float*)cv.take(max_part * 4);
+  net->D0 = (float*)cv.take(max_d0 * 4);
+  net->ppart = (float*)cv.take((size_t)net->pool_parts * max_cp * 4);
+  net->ws_bytes = cv.off + 256;
+}
+
+static int wgrad_chunks(int64_t rows_cap, int tiles_mn, int BK) {
+  int64_t max_chunks = std::max<int64_t>(1, (rows_cap + 4 * BK - 1) / (4 * BK));
+  int64_t want = std::max<int64_t>(1, (512 + tiles_mn - 1) / tiles_mn);
+  return (int)std::min<int64_t>(want, max_chunks);
+}
+
+extern "C" {
+
+const char* sscn_status_string(int32_t s) {
+  switch (s) {
+    case SSCN_OK: return "ok";
+    case SSCN_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case SSCN_ERR_OUT_OF_RANGE: return "site outside the grid or batch";
+    case SSCN_ERR_DUPLICATE_SITE: return "site listed twice";
+    case SSCN_ERR_CAPACITY: return "batch or site count above the net's limits";
+    case SSCN_ERR_BAD_STATE: return "call out of order";
+    case SSCN_ERR_HIP: return "HIP runtime error";
+    case SSCN_ERR_WORKSPACE: return "workspace null, too small or misaligned";
+    default: return "unknown status";
+  }
+}
+
+sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
+  if (!desc || !out) return SSCN_ERR_INVALID_ARGUMENT;
+  *out = nullptr;
+  const sscn_net_desc& d = *desc;
+  if (d.ell < 1 || d.ell > 8 || d.k < 1 || d.c_in < 1 || d.n_classes < 1 || d.batch_max < 1 || d.max_active < 1)
+    return SSCN_ERR_INVALID_ARGUMENT;
+  if (d.dtype != SSCN_F32 && d.dtype != SSCN_BF16) return SSCN_ERR_INVALID_ARGUMENT;
+  const int64_t N = 3ll << d.ell;
+  if ((int64_t)d.batch_max * N * N >= (1ll << 31)) return SSCN_ERR_INVALID_ARGUMENT;
+  if ((int64_t)(d.ell + 1) * d.k > (1 << 20) || d.n_classes > (1 << 24) || d.c_in > (1 << 16))
+    return SSCN_ERR_INVALID_ARGUMENT;
+  sscn_net* net = new (std::nothrow) sscn_net();
+  if (!net) return SSCN_ERR_INVALID_ARGUMENT;
+  net->d = d;
+  net->bf16 = d.dtype == SSCN_BF16;
+  net->esz = net->bf16 ? 2 : 4;
+  net->VE = 16 / net->esz;
+  net->nlayers = 2 * d.ell + 2;
+  net->nparams = d.ell + 2;
+  net->pool_parts = 64;
+  const GemmTile gt = gemm_tile(net->bf16);
+  const int VE = net->VE;
+  auto cp = [VE](int c) { return (int)round_up(c, VE); };
+  // layers (Section 2.1): input N; conv3 N-2; then (pool S/2, conv2 S-1) x ell
+  LayerPlan* L = net->L;
+  L[0] = LayerPlan{};
+  L[0].kind = 0;
+  L[0].S = (int)N;
+  L[0].C = d.c_in;
+  L[0].cap = d.max_active;
+  int S = (int)N, C = d.c_in, ci = 0;
+  for (int s = 1; s < net->nlayers; ++s) {
+    LayerPlan& l = L[s];
+    l = LayerPlan{};
+    const int64_t below = L[s - 1].cap;
+    if (s % 2 == 1) {
+      l.kind = 1;
+      l.F = (s == 1) ? 3 : 2;
+      l.S = S - (l.F - 1);
+      l.C = ((s + 1) / 2) * d.k;
+      l.conv_index = ci++;
+    } else {
+      l.kind = 2;
+      l.F = 2;
+      l.S = S / 2;
+      l.C = C;
+      l.conv_index = -1;
+    }
+    l.A = l.F * l.F;
+    const int64_t grid_cap = (int64_t)d.batch_max * l.S * l.S;
+    l.cap = std::min<int64_t>(grid_cap, (l.kind == 1 ? l.A : 1) * below);
+    S = l.S;
+    C = l.C;
+  }
+  for (int s = 0; s < net->nlayers; ++s) {
+    L[s].Cp = cp(L[s].C);
+    L[s].Wd = (L[s].S + 63) / 64;
+    if ((L[s].cap + 1) * (int64_t)std::max(L[s].Cp, std::max(L[s].A, 1)) >= (1ll << 31)) {
+      delete net;
+      return SSCN_ERR_INVALID_ARGUMENT;
+    }
+  }
+  net->max_words = L[0].S * L[0].Wd;
+  net->dl_stride = cp(d.n_classes);
+  // parameters
+  for (int s = 1; s < net->nlayers; ++s) {
+    if (L[s].kind != 1) continue;
+    ParamPlan& P = net->P[L[s].conv_index];
+    P.A = L[s].A;
+    P.c_in = L[s - 1].C;
+    P.c_out = L[s].C;
+    P.cp_in = L[s - 1].Cp;
+    P.cp_out = L[s].Cp;
+    P.NpadF = (int)round_up(P.c_out, gt.BN);
+    P.KpadF = (int)round_up((int64_t)P.A * P.cp_in, gt.BK);
+    P.NpadD = (int)round_up(P.c_in, gt.BN);
+    P.KpadD = (int)round_up((int64_t)P.A * P.cp_out, gt.BK);
+    P.m_ones = P.A * P.cp_in;
+    P.m_ind = P.m_ones + 1;
+    P.Mpad_w = (int)round_up(P.m_ind + P.A, gt.BM);
+    P.Npad_w = (int)round_up(P.c_out, gt.BN);
+    P.nchunks = wgrad_chunks(L[s].cap + 1, (P.Mpad_w / gt.BM) * (P.Npad_w / gt.BN), gt.BK);
+  }
+  {
+    ParamPlan& P = net->P[d.ell + 1];
+    const LayerPlan& Lt = L[net->nlayers - 1];
+    P.A = 1;
+    P.c_in = Lt.C;
+    P.c_out = d.n_classes;
+    P.cp_in = Lt.Cp;
+    P.cp_out = net->dl_stride;
+    P.NpadF = (int)round_up(P.c_out, gt.BN);
+    P.KpadF = (int)round_up(P.cp_in, gt.BK);
+    P.NpadD = (int)round_up(P.c_in, gt.BN);
+    P.KpadD = (int)round_up(P.cp_out, gt.BK);
+    P.m_ones = P.cp_in;
+    P.m_ind = -1;
+    P.Mpad_w = (int)round_up(P.m_ones + 1, gt.BM);
+    P.Npad_w = (int)round_up(P.c_out, gt.BN);
+    P.nchunks = 1;
+  }
+  carve(net, nullptr);
+  *out = net;
+  return SSCN_OK;
+}
+
+void sscn_net_destroy(sscn_net* net) { delete net; }
+
+int32_t sscn_net_num_params(const sscn_net* net) { return net ? net->nparams : 0; }
+
+sscn_status sscn_net_param_shape(const sscn_net* net, int32_t layer, int64_t* rows, int64_t* cols) {
+  if (!net || !rows || !cols || layer < 0 || layer >= net->nparams) return SSCN_ERR_INVALID_ARGUMENT;
+  const ParamPlan& P = net->P[layer];
+  *rows = (int64_t)P.A * P.c_in;
+  *cols = P.c_out;
+  return SSCN_OK;
+}
+
+sscn_status sscn_net_workspace_bytes(const sscn_net* net, size_t* bytes) {
+  if (!net || !bytes) return SSCN_ERR_INVALID_ARGUMENT;
+  *bytes = net->ws_bytes;
+  return SSCN_OK;
+}
+
+sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t n, int32_t batch, void* d_ws,
+                                size_t ws_bytes, void* stream) {
+  if (!net || n < 0 || batch < 0) return SSCN_ERR_INVALID_ARGUMENT;
+  if (n > 0 && !d_coords) return SSCN_ERR_INVALID_ARGUMENT;
+  if (n > net->d.max_active || batch > net->d.batch_max) return SSCN_ERR_CAPACITY;
+  if (!d_ws || ws_bytes < net->ws_bytes || ((uintptr_t)d_ws & 255u)) return SSCN_ERR_WORKSPACE;
+  net->built = net->forwarded = false;
+  if (net->ws != d_ws) {
+    carve(net, d_ws);
+    net->ws = d_ws;
+  }
+  net->batch = batch;
+  net->n = n;
+  hipStream_t st = (hipStream_t)stream;
+  RulebookArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.nlayers = net->nlayers;
+  a.batch = batch;
+  SitesWork wk;
+  std::memset(&wk, 0, sizeof(wk));
+  int64_t acc = 0;
+  for (int s = 0; s < net->nlayers; ++s) {
+    const LayerPlan& L = net->L[s];
+    a.L[s] = LayerBits{L.bits, L.wpre, L.scount, L.soff, L.sites, L.S, L.Wd};
+    a.kind[s] = L.kind;
+    a.F[s] = L.F;
+    a.rules[s] = L.rules;
+    a.rules_t[s] = L.rules_t;
+    wk.base[s] = acc;
+    acc += (int64_t)batch * L.S * L.Wd;
+  }
+  wk.base[net->nlayers] = acc;
+  wk.total = acc;
+  a.counts = net->counts;
+  a.err = net->err;
+  a.perm = net->perm;
+  a.head_rows = net->head_rows;
+  a.coords = d_coords;
+  a.n = n;
+  if (launch_rulebook(a, wk, net->max_words, st) != hipSuccess) return SSCN_ERR_HIP;
+  net->built = true;
+  return SSCN_OK;
+}
+
+sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream) {
+  if (!net || !h_counts) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net->built) return SSCN_ERR_BAD_STATE;
+  hipStream_t st = (hipStream_t)stream;
+  int32_t err = 0;
+  if (hipMemcpyAsync(h_counts, net->counts, sizeof(int32_t) * net->nlayers, hipMemcpyDeviceToHost, st) != hipSuccess)
+    return SSCN_ERR_HIP;
+  if (hipMemcpyAsync(&err, net->err, sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return SSCN_ERR_HIP;
+  if (err & ERRBIT_RANGE) return SSCN_ERR_OUT_OF_RANGE;
+  if (err & ERRBIT_DUP) return SSCN_ERR_DUPLICATE_SITE;
+  return SSCN_OK;
+}
+
+static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lb = net->L[s - 1];
+  if (L.kind == 1) {
+    const ParamPlan& P = net->P[L.conv_index];
+    GemmArgs g{};
+    g.src = Lb.X;
+    g.src_stride = Lb.Cp;
+    g.rmap = L.rules;
+    g.A = L.A;
+    g.cseg = Lb.Cp;
+    g.K = L.A * Lb.Cp;
+    g.Kpad = P.KpadF;
+    g.Bt = P.WpF;
+    g.Npad = P.NpadF;
+    g.bias = net->b[L.conv_index];
+    g.N = L.C;
+    g.out_cols = L.Cp;
+    g.out = L.X;
+    g.out_stride = L.Cp;
+    g.epi = EPI_BIAS_RELU;
+    g.rows_dev = net->counts + s;
+    g.rows_add = 1;
+    g.row_begin = 0;
+    return launch_gemm(net->bf16, g, L.cap + 1, st);
+  }
+  return launch_pool_fwd(net->bf16, Lb.X, Lb.Cp, L.rules, L.X, L.Cp, L.argmax, L.Cp, net->counts + s, L.cap, st);
+}
+
+static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lb = net->L[s - 1];
+  hipError_t e;
+  if (L.kind == 2)
+    return launch_pool_bwd(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, L.rules, Lb.X, Lb.grad, L.Cp,
+                           net->counts + s, net->counts + s - 1, Lb.cap, L.cap, net->ppart, net->pool_parts, st);
+  const int ci = L.conv_index;
+  const ParamPlan& P = net->P[ci];
+  WGradArgs w{};
+  w.src = Lb.X;
+  w.src_stride = Lb.Cp;
+  w.rmap = L.rules;
+  w.A = L.A;
+  w.cseg = Lb.Cp;
+  w.m_ones = P.m_ones;
+  w.m_ind = P.m_ind;
+  w.Mpad = P.Mpad_w;
+  w.dsrc = L.grad;
+  w.dsrc_stride = L.Cp;
+  w.dsrc_cols = L.Cp;
+  w.Npad = P.Npad_w;
+  w.rows_dev = net->counts + s;
+  w.rows_add = 1;
+  w.nchunks = P.nchunks;
+  w.part = net->wpart;
+  if ((e = launch_wgrad(net->bf16, w, st)) != hipSuccess) return e;
+  if ((e = launch_wgrad_reduce(net->wpart, P.nchunks, P.Mpad_w, P.Npad_w, P.A, P.cp_in, P.c_in, P.c_out, P.m_ones,
+                               P.m_ind, net->dW[ci], net->db[ci], net->D0, st)) != hipSuccess)
+    return e;
+  if (s == 1 && !net->want_dfeats) return hipSuccess;
+  GemmArgs g{};
+  g.src = L.grad;
+  g.src_stride = L.Cp;
+  g.rmap = L.rules_t;
+  g.A = L.A;
+  g.cseg = L.Cp;
+  g.K = L.A * L.Cp;
+  g.Kpad = P.KpadD;
+  g.Bt = P.WpD;
+  g.Npad = P.NpadD;
+  g.bias = nullptr;
+  g.N = Lb.C;
+  g.out_cols = Lb.Cp;
+  g.out = Lb.grad;
+  g.out_stride = Lb.Cp;
+  g.epi = EPI_STORE;
+  g.rows_dev = net->counts + s - 1;
+  g.rows_add = 1;
+  g.row_begin = 1;
+  if ((e = launch_gemm(net->bf16, g, Lb.cap + 1, st)) != hipSuccess) return e;
+  return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, st);
+}
+
+sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
+                         const int32_t* d_labels, float* d_logits, float* d_loss, void* stream) {
+  if (!net || !h_W || !h_b || !d_labels || !d_logits || !d_loss) return SSCN_ERR_INVALID_ARGUMENT;
+  if (net->n > 0 && !d_feats) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net->built) return SSCN_ERR_BAD_STATE;
+  for (int p = 0; p < net->nparams; ++p)
+    if (!h_W[p] || !h_b[p]) return SSCN_ERR_INVALID_ARGUMENT;
+  hipStream_t st = (hipStream_t)stream;
+  for (int p = 0; p < net->nparams; ++p) {
+    net->W[p] = h_W[p];
+    net->b[p] = h_b[p];
+  }
+  net->logits = d_logits;
+  net->labels = d_labels;
+  const LayerPlan& L0 = net->L[0];
+  if (launch_scatter_input(net->bf16, d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, st) != hipSuccess)
+    return SSCN_ERR_HIP;
+  for (int p = 0; p < net->nparams; ++p) {
+    const ParamPlan& P = net->P[p];
+    if (launch_pack(net->bf16, 0, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpF, P.NpadF, P.KpadF, st) !=
+            hipSuccess ||
+        launch_pack(net->bf16, 1, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpD, P.NpadD, P.KpadD, st) !=
+            hipSuccess)
+      return SSCN_ERR_HIP;
+  }
+  for (int s = 1; s < net->nlayers; ++s)
+    if (forward_stage(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
+  // softmax layer on each sample's top-layer row
+  const LayerPlan& Lt = net->L[net->nlayers - 1];
+  const ParamPlan& P = net->P[net->d.ell + 1];
+  GemmArgs g{};
+  g.src = Lt.X;
+  g.src_stride = Lt.Cp;
+  g.rmap = net->head_rows;
+  g.A = 1;
+  g.cseg = Lt.Cp;
+  g.K = Lt.Cp;
+  g.Kpad = P.KpadF;
+  g.Bt = P.WpF;
+  g.Npad = P.NpadF;
+  g.bias = h_b[net->d.ell + 1];
+  g.N = net->d.n_classes;
+  g.out_cols = net->d.n_classes;
+  g.out = d_logits;
+  g.out_stride = net->d.n_classes;
+  g.epi = EPI_BIAS_F32;
+  g.rows_host = net->batch;
+  g.row_begin = 0;
+  if (launch_gemm(net->bf16, g, net->batch, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (launch_softmax_xent(net->bf16, d_logits, d_labels, net->batch, net->d.n_classes, net->dlogits, net->dl_stride,
+                          net->loss_part, d_loss, st) != hipSuccess)
+    return SSCN_ERR_HIP;
+  net->forwarded = true;
+  return SSCN_OK;
+}
+
+sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db, void* d_dfeats, void* stream) {
+  if (!net || !h_dW || !h_db) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net->forwarded) return SSCN_ERR_BAD_STATE;
+  for (int p = 0; p < net->nparams; ++p) {
+    if (!h_dW[p] || !h_db[p]) return SSCN_ERR_INVALID_ARGUMENT;
+    net->dW[p] = h_dW[p];
+    net->db[p] = h_db[p];
+  }
+  hipStream_t st = (hipStream_t)stream;
+  net->want_dfeats = d_dfeats != nullptr;
+  const int top = net->nlayers - 1;
+  const LayerPlan& Lt = net->L[top];
+  const int fc = net->d.ell + 1;
+  const ParamPlan& P = net->P[fc];
+  // softmax layer: dW, db from (h, dlogits); dh = dlogits W^T
+  WGradArgs w{};
+  w.src = Lt.X;
+  w.src_stride = Lt.Cp;
+  w.rmap = net->head_rows;
+  w.A = 1;
+  w.cseg = Lt.Cp;
+  w.m_ones = P.m_ones;
+  w.m_ind = -1;
+  w.Mpad = P.Mpad_w;
+  w.dsrc = net->dlogits;
+  w.dsrc_stride = net->dl_stride;
+  w.dsrc_cols = net->dl_stride;
+  w.Npad = P.Npad_w;
+  w.rows_host = net->batch;
+  w.nchunks = 1;
+  w.part = net->wpart;
+  if (launch_wgrad(net->bf16, w, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (launch_wgrad_reduce(net->wpart, 1, P.Mpad_w, P.Npad_w, 1, P.cp_in, P.c_in, P.c_out, P.m_ones, -1, h_dW[fc],
+                          h_db[fc], nullptr, st) != hipSuccess)
+    return SSCN_ERR_HIP;
+  GemmArgs g{};
+  g.src = net->dlogits;
+  g.src_stride = net->dl_stride;
+  g.rmap = nullptr;
+  g.A = 1;
+  g.cseg = net->dl_stride;
+  g.K = net->dl_stride;
+  g.Kpad = P.KpadD;
+  g.Bt = P.WpD;
+  g.Npad = P.NpadD;
+  g.bias = nullptr;
+  g.N = Lt.C;
+  g.out_cols = Lt.Cp;
+  g.out = net->dh;
+  g.out_stride = Lt.Cp;
+  g.epi = EPI_F32;
+  g.rows_host = net->batch;
+  g.row_begin = 0;
+  if (launch_gemm(net->bf16, g, net->batch, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp, st) !=
+      hipSuccess)
+    return SSCN_ERR_HIP;
+  for (int s = top; s >= 1; --s)
+    if (backward_stage(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (d_dfeats) {
+    const LayerPlan& L0 = net->L[0];
+    if (launch_gather_dfeats(net->bf16, L0.grad, L0.Cp, net->perm, net->n, net->d.c_in, d_dfeats, st) != hipSuccess)
+      return SSCN_ERR_HIP;
+  }
+  return SSCN_OK;
+}
+
+sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream) {
+  if (!net || stage < 1 || stage >= net->nlayers) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net->forwarded) return SSCN_ERR_BAD_STATE;
+  return forward_stage(net, stage, (hipStream_t)stream) == hipSuccess ? SSCN_OK : SSCN_ERR_HIP;
+}
+
+sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream) {
+  if (!net || stage < 1 || stage >= net->nlayers) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net->forwarded || !net->dW[0]) return SSCN_ERR_BAD_STATE;
+  return backward_stage(net, stage, (hipStream_t)stream) == hipSuccess ? SSCN_OK : SSCN_ERR_HIP;
+}
+
+sscn_status sscn_layer_view_get(const sscn_net* net, int32_t layer, sscn_layer_view* out) {
+  if (!net || !out || layer < 0 || layer >= net->nlayers) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net->ws) return SSCN_ERR_BAD_STATE;
+  const LayerPlan& L = net->L[layer];
+  out->kind = L.kind;
+  out->side = L.S;
+  out->channels = L.C;
+  out->row_stride = L.Cp;
+  out->window = layer ? L.A : 0;
+  out->capacity = (int32_t)L.cap;
+  out->count = net->counts + layer;
+  out->sites = L.sites;
+  out->rules = L.rules;
+  out->rules_t = L.rules_t;
+  out->features = L.X;
+  out->grad = L.grad;
+  out->argmax = L.argmax;
+  return SSCN_OK;
+}
+
+}  // extern "C"

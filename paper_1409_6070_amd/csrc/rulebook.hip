@@ -1,0 +1,314 @@
+// Active-site sets and window lists for every layer (the paper's pointer
+// matrices, Section 2.3), built on the GPU.
+//
+// Each layer's pointer matrix is held as an occupancy bitmap with one bit per
+// grid location, rows aligned to 64-bit words, plus the exclusive popcount
+// prefix of every word within its sample.  The row of an active location is
+// then 1 + (sites in earlier samples) + (prefix of its word) + (set bits below
+// it in the word): an order-preserving perfect hash of (b, y, x) onto rows
+// 1..n, giving ascending (b, y, x) order with no sort.  Duplicates are found
+// from the previous value returned by the atomic OR that inserts a site.
+//
+// Active sets follow Section 2.3 and Figure 2: a convolution output is active
+// when any location of its FxF window below is active, a pooling output when
+// any of its 2x2 stride-2 window is.  Both are computed bit-parallel on whole
+// 64-bit words, one workgroup per sample with the sample's bitmaps in LDS.
+
+#include "common.h"
+#include "kernels.h"
+
+namespace sscn {
+
+static constexpr int RB_THREADS = 256;
+
+__global__ void __launch_bounds__(256) k_rb_clear(uint64_t* bits0, int64_t nwords, int32_t* err) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < nwords; i += stride) bits0[i] = 0ull;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *err = 0;
+}
+
+__global__ void __launch_bounds__(256) k_rb_insert(const int32_t* __restrict__ coords, int32_t n, int32_t batch,
+                                                   int32_t N, int32_t Wd, uint64_t* bits0, int32_t* err) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int b = coords[3 * i], y = coords[3 * i + 1], x = coords[3 * i + 2];
+  if (b < 0 || b >= batch || y < 0 || y >= N || x < 0 || x >= N) {
+    atomicOr(err, ERRBIT_RANGE);
+    return;
+  }
+  unsigned long long bit = 1ull << (x & 63);
+  unsigned long long* w = (unsigned long long*)&bits0[((int64_t)b * N + y) * Wd + (x >> 6)];
+  unsigned long long old = atomicOr(w, bit);
+  if (old & bit) atomicOr(err, ERRBIT_DUP);
+}
+
+// Keep the even-numbered bits of a 64-bit word, packed into the low 32 bits.
+__device__ inline uint64_t compress_even_bits(uint64_t v) {
+  v &= 0x5555555555555555ull;
+  v = (v | (v >> 1)) & 0x3333333333333333ull;
+  v = (v | (v >> 2)) & 0x0F0F0F0F0F0F0F0Full;
+  v = (v | (v >> 4)) & 0x00FF00FF00FF00FFull;
+  v = (v | (v >> 8)) & 0x0000FFFF0000FFFFull;
+  v = (v | (v >> 16)) & 0x00000000FFFFFFFFull;
+  return v;
+}
+
+__device__ inline uint64_t row_mask_word(int w, int S) {
+  int lo = w * 64;
+  int nb = S - lo;
+  if (nb >= 64) return ~0ull;
+  if (nb <= 0) return 0ull;
+  return (1ull << nb) - 1ull;
+}
+
+// Block-wide exclusive prefix of popcounts over nw words held in LDS.
+// Writes wpre[0..nw) (global) and returns the total.
+__device__ int block_popcount_scan(const uint64_t* words, int nw, int32_t* wpre, int* scratch) {
+  const int t = threadIdx.x;
+  const int per = (nw + RB_THREADS - 1) / RB_THREADS;
+  const int beg = t * per;
+  int local = 0;
+  for (int j = 0; j < per; ++j) {
+    int w = beg + j;
+    if (w < nw) local += __popcll(words[w]);
+  }
+  scratch[t] = local;
+  __syncthreads();
+  // Hillis-Steele inclusive scan over RB_THREADS values
+  for (int off = 1; off < RB_THREADS; off <<= 1) {
+    int v = (t >= off) ? scratch[t - off] : 0;
+    __syncthreads();
+    scratch[t] += v;
+    __syncthreads();
+  }
+  int run = scratch[t] - local;
+  for (int j = 0; j < per; ++j) {
+    int w = beg + j;
+    if (w < nw) {
+      wpre[w] = run;
+      run += __popcll(words[w]);
+    }
+  }
+  int total = scratch[RB_THREADS - 1];
+  __syncthreads();
+  return total;
+}
+
+// One workgroup per sample: every layer's bitmap from the input bitmap.
+__global__ void __launch_bounds__(RB_THREADS) k_rb_bitmaps(RulebookArgs a, int32_t max_words) {
+  extern __shared__ uint64_t lds[];
+  uint64_t* cur = lds;
+  uint64_t* nxt = lds + max_words;
+  int* scratch = (int*)(lds + 2 * max_words);
+  const int b = blockIdx.x;
+  const int t = threadIdx.x;
+
+  {  // layer 0
+    const LayerBits& L = a.L[0];
+    const int nw = L.S * L.Wd;
+    const uint64_t* src = L.bits + (int64_t)b * nw;
+    for (int w = t; w < nw; w += RB_THREADS) cur[w] = src[w];
+    __syncthreads();
+    int tot = block_popcount_scan(cur, nw, L.wpre + (int64_t)b * nw, scratch);
+    if (t == 0) L.scount[b] = tot;
+  }
+  for (int s = 1; s < a.nlayers; ++s) {
+    const LayerBits& Li = a.L[s - 1];
+    const LayerBits& Lo = a.L[s];
+    const int nwo = Lo.S * Lo.Wd;
+    if (a.kind[s] == 1) {  // convolution, F x F valid window
+      const int F = a.F[s];
+      for (int idx = t; idx < nwo; idx += RB_THREADS) {
+        const int Y = idx / Lo.Wd, w = idx - Y * Lo.Wd;
+        uint64_t acc = 0;
+        for (int dy = 0; dy < F; ++dy) {
+          const uint64_t* row = cur + (Y + dy) * Li.Wd;
+          const uint64_t lo = row[w];
+          const uint64_t hi = (w + 1 < Li.Wd) ? row[w + 1] : 0ull;
+          acc |= lo;
+          for (int dx = 1; dx < F; ++dx) acc |= (lo >> dx) | (hi << (64 - dx));
+        }
+        nxt[idx] = acc & row_mask_word(w, Lo.S);
+      }
+    } else {  // 2x2 stride-2 pooling
+      for (int idx = t; idx < nwo; idx += RB_THREADS) {
+        const int Y = idx / Lo.Wd, w = idx - Y * Lo.Wd;
+        const uint64_t* r0 = cur + (2 * Y) * Li.Wd;
+        const uint64_t* r1 = r0 + Li.Wd;
+        uint64_t p0 = 0, p1 = 0;
+        if (2 * w < Li.Wd) {
+          uint64_t r = r0[2 * w] | r1[2 * w];
+          p0 = compress_even_bits(r | (r >> 1));
+        }
+        if (2 * w + 1 < Li.Wd) {
+          uint64_t r = r0[2 * w + 1] | r1[2 * w + 1];
+          p1 = compress_even_bits(r | (r >> 1));
+        }
+        nxt[idx] = (p0 | (p1 << 32)) & row_mask_word(w, Lo.S);
+      }
+    }
+    __syncthreads();
+    uint64_t* dst = Lo.bits + (int64_t)b * nwo;
+    for (int w = t; w < nwo; w += RB_THREADS) dst[w] = nxt[w];
+    int tot = block_popcount_scan(nxt, nwo, Lo.wpre + (int64_t)b * nwo, scratch);
+    if (t == 0) Lo.scount[b] = tot;
+    uint64_t* tmp = cur;
+    cur = nxt;
+    nxt = tmp;
+    __syncthreads();
+  }
+}
+
+// Sample offsets and layer totals (one thread per layer, samples in order).
+__global__ void k_rb_offsets(RulebookArgs a) {
+  int s = threadIdx.x;
+  if (s >= a.nlayers) return;
+  int acc = 0;
+  for (int b = 0; b < a.batch; ++b) {
+    a.L[s].soff[b] = acc;
+    acc += a.L[s].scount[b];
+  }
+  a.counts[s] = acc;
+}
+
+// Site keys of every layer, in row order: one thread per bitmap word.
+__global__ void __launch_bounds__(256) k_rb_sites(RulebookArgs a, SitesWork wk) {
+  int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; g < wk.total; g += stride) {
+    int s = 0;
+    while (s + 1 < a.nlayers && g >= wk.base[s + 1]) ++s;
+    const LayerBits& L = a.L[s];
+    int64_t idx = g - wk.base[s];
+    uint64_t word = L.bits[idx];
+    if (!word) continue;
+    int64_t per_sample = (int64_t)L.S * L.Wd;
+    int b = (int)(idx / per_sample);
+    int rem = (int)(idx - (int64_t)b * per_sample);
+    int y = rem / L.Wd, w = rem - y * L.Wd;
+    int row = L.soff[b] + L.wpre[idx];
+    while (word) {
+      int bit = __ffsll((long long)word) - 1;
+      word &= word - 1;
+      int x = w * 64 + bit;
+      L.sites[row++] = (b * L.S + y) * L.S + x;
+    }
+  }
+}
+
+__device__ inline int32_t rank_row(const LayerBits& L, int b, int y, int x) {
+  int64_t idx = ((int64_t)b * L.S + y) * L.Wd + (x >> 6);
+  uint64_t w = L.bits[idx];
+  int bit = x & 63;
+  if (!((w >> bit) & 1ull)) return 0;
+  return 1 + L.soff[b] + L.wpre[idx] + __popcll(w & ((1ull << bit) - 1ull));
+}
+
+// Window lists (rules), their transposes, the caller-site -> row map and the
+// head rows.  Segments run one after another; each is grid-strided over its
+// device-side count.
+__global__ void __launch_bounds__(256) k_rb_rules(RulebookArgs a) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int s = 1; s < a.nlayers; ++s) {
+    const LayerBits& Lo = a.L[s];
+    const LayerBits& Li = a.L[s - 1];
+    const int F = a.F[s];
+    const int A = F * F;
+    const int step = (a.kind[s] == 1) ? 1 : 2;
+    const int n_out = a.counts[s];
+    const int n_in = a.counts[s - 1];
+    int32_t* R = a.rules[s];
+    for (int64_t o = tid; o <= n_out; o += stride) {
+      if (o == 0) {
+        for (int f = 0; f < A; ++f) R[f] = 0;
+        continue;
+      }
+      int key = Lo.sites[o - 1];
+      int X = key % Lo.S;
+      int tq = key / Lo.S;
+      int Y = tq % Lo.S;
+      int b = tq / Lo.S;
+      for (int dy = 0; dy < F; ++dy)
+        for (int dx = 0; dx < F; ++dx)
+          R[o * A + dy * F + dx] = rank_row(Li, b, step * Y + dy, step * X + dx);
+    }
+    int32_t* Rt = a.rules_t[s];
+    if (a.kind[s] == 1) {
+      for (int64_t i = tid; i <= n_in; i += stride) {
+        if (i == 0) {
+          for (int f = 0; f < A; ++f) Rt[f] = -1;
+          continue;
+        }
+        int key = Li.sites[i - 1];
+        int x = key % Li.S;
+        int tq = key / Li.S;
+        int y = tq % Li.S;
+        int b = tq / Li.S;
+        for (int dy = 0; dy < F; ++dy)
+          for (int dx = 0; dx < F; ++dx) {
+            int Y = y - dy, X = x - dx;
+            int r = -1;
+            if (Y >= 0 && X >= 0 && Y < Lo.S && X < Lo.S) r = rank_row(Lo, b, Y, X);
+            Rt[i * A + dy * F + dx] = r;
+          }
+      }
+    } else {
+      for (int64_t i = tid; i <= n_in; i += stride) {
+        if (i == 0) {
+          Rt[0] = -1;
+          continue;
+        }
+        int key = Li.sites[i - 1];
+        int x = key % Li.S;
+        int tq = key / Li.S;
+        int y = tq % Li.S;
+        int b = tq / Li.S;
+        int Y = y >> 1, X = x >> 1;
+        int r = -1;
+        if (Y < Lo.S && X < Lo.S) {
+          int p = rank_row(Lo, b, Y, X);
+          r = p * 4 + (y & 1) * 2 + (x & 1);
+        }
+        Rt[i] = r;
+      }
+    }
+  }
+  {  // caller site -> input row
+    const LayerBits& L0 = a.L[0];
+    for (int64_t i = tid; i < a.n; i += stride) {
+      int b = a.coords[3 * i], y = a.coords[3 * i + 1], x = a.coords[3 * i + 2];
+      int r = -1;
+      if (b >= 0 && b < a.batch && y >= 0 && y < L0.S && x >= 0 && x < L0.S) r = rank_row(L0, b, y, x);
+      a.perm[i] = r;
+    }
+  }
+  {  // each sample's single top-layer site (row 0 when the sample is empty)
+    const LayerBits& Lt = a.L[a.nlayers - 1];
+    for (int64_t b = tid; b < a.batch; b += stride) a.head_rows[b] = rank_row(Lt, (int)b, 0, 0);
+  }
+}
+
+hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, int32_t max_words, hipStream_t st) {
+  const LayerBits& L0 = a.L[0];
+  int64_t nw0 = (int64_t)a.batch * L0.S * L0.Wd;
+  int g = (int)std::min<int64_t>((nw0 + 255) / 256, 1024);
+  if (g < 1) g = 1;
+  hipLaunchKernelGGL(k_rb_clear, dim3(g), dim3(256), 0, st, L0.bits, nw0, a.err);
+  if (a.n > 0)
+    hipLaunchKernelGGL(k_rb_insert, dim3((a.n + 255) / 256), dim3(256), 0, st, a.coords, a.n, a.batch, L0.S, L0.Wd,
+                       L0.bits, a.err);
+  if (a.batch > 0) {
+    size_t lds = (size_t)2 * max_words * sizeof(uint64_t) + RB_THREADS * sizeof(int);
+    hipLaunchKernelGGL(k_rb_bitmaps, dim3(a.batch), dim3(RB_THREADS), lds, st, a, max_words);
+  }
+  hipLaunchKernelGGL(k_rb_offsets, dim3(1), dim3(64), 0, st, a);
+  int gs = (int)std::min<int64_t>((wk.total + 255) / 256, 2048);
+  if (gs < 1) gs = 1;
+  hipLaunchKernelGGL(k_rb_sites, dim3(gs), dim3(256), 0, st, a, wk);
+  hipLaunchKernelGGL(k_rb_rules, dim3(1024), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace sscn

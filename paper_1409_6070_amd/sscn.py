@@ -1,0 +1,282 @@
+"""ctypes binding of libsscn (include/sscn.h): argument marshalling only.
+
+The functions ``sscn_*`` below carry the C names and signatures one to one.
+``SparseDeepCNet`` is a convenience wrapper that allocates the caller-owned
+device buffers with torch (workspace, gradients, logits) and passes raw
+pointers plus torch's current HIP stream; every step of the computation runs
+in the HIP kernels of the library.  If the library is not built, loading
+fails with an error -- there is no fallback path.
+"""
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsscn.so")
+
+SSCN_F32, SSCN_BF16 = 0, 1
+STATUS = {
+    0: "SSCN_OK",
+    1: "SSCN_ERR_INVALID_ARGUMENT",
+    2: "SSCN_ERR_OUT_OF_RANGE",
+    3: "SSCN_ERR_DUPLICATE_SITE",
+    4: "SSCN_ERR_CAPACITY",
+    5: "SSCN_ERR_BAD_STATE",
+    6: "SSCN_ERR_HIP",
+    7: "SSCN_ERR_WORKSPACE",
+}
+EXPORTED = [
+    "sscn_net_create", "sscn_net_destroy", "sscn_status_string", "sscn_net_num_params", "sscn_net_param_shape",
+    "sscn_net_workspace_bytes", "sscn_rulebook_build", "sscn_layer_sizes", "sscn_forward", "sscn_backward",
+    "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get",
+]
+
+
+class SSCNError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+        super().__init__(f"{where}: {self.name}")
+
+
+class NetDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("ell", "k", "c_in", "n_classes", "batch_max", "max_active", "dtype")]
+
+
+class LayerView(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int32), ("side", ctypes.c_int32), ("channels", ctypes.c_int32),
+        ("row_stride", ctypes.c_int32), ("window", ctypes.c_int32), ("capacity", ctypes.c_int32),
+        ("count", ctypes.c_void_p), ("sites", ctypes.c_void_p), ("rules", ctypes.c_void_p),
+        ("rules_t", ctypes.c_void_p), ("features", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+        ("argmax", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libsscn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_1409_6070_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, I32, VP, SZ = ctypes.POINTER, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+    sig = {
+        "sscn_net_create": (I32, [P(NetDesc), P(VP)]),
+        "sscn_net_destroy": (None, [VP]),
+        "sscn_status_string": (ctypes.c_char_p, [I32]),
+        "sscn_net_num_params": (I32, [VP]),
+        "sscn_net_param_shape": (I32, [VP, I32, P(ctypes.c_int64), P(ctypes.c_int64)]),
+        "sscn_net_workspace_bytes": (I32, [VP, P(SZ)]),
+        "sscn_rulebook_build": (I32, [VP, VP, I32, I32, VP, SZ, VP]),
+        "sscn_layer_sizes": (I32, [VP, P(I32), VP]),
+        "sscn_forward": (I32, [VP, VP, P(VP), P(VP), VP, VP, VP, VP]),
+        "sscn_backward": (I32, [VP, P(VP), P(VP), VP, VP]),
+        "sscn_forward_stage": (I32, [VP, I32, VP]),
+        "sscn_backward_stage": (I32, [VP, I32, VP]),
+        "sscn_layer_view_get": (I32, [VP, I32, P(LayerView)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise SSCNError(status, where)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# the C calls, same names
+
+
+def sscn_net_create(desc: NetDesc) -> int:
+    h = ctypes.c_void_p()
+    _check(load_library().sscn_net_create(ctypes.byref(desc), ctypes.byref(h)), "sscn_net_create")
+    return h.value
+
+
+def sscn_net_destroy(net: int) -> None:
+    load_library().sscn_net_destroy(net)
+
+
+def sscn_status_string(status: int) -> str:
+    return load_library().sscn_status_string(status).decode()
+
+
+def sscn_net_num_params(net: int) -> int:
+    return load_library().sscn_net_num_params(net)
+
+
+def sscn_net_param_shape(net: int, layer: int):
+    r, c = ctypes.c_int64(), ctypes.c_int64()
+    _check(load_library().sscn_net_param_shape(net, layer, ctypes.byref(r), ctypes.byref(c)), "sscn_net_param_shape")
+    return r.value, c.value
+
+
+def sscn_net_workspace_bytes(net: int) -> int:
+    b = ctypes.c_size_t()
+    _check(load_library().sscn_net_workspace_bytes(net, ctypes.byref(b)), "sscn_net_workspace_bytes")
+    return b.value
+
+
+def sscn_rulebook_build(net: int, d_coords: int, n: int, batch: int, d_ws: int, ws_bytes: int, stream: int) -> None:
+    _check(load_library().sscn_rulebook_build(net, d_coords, n, batch, d_ws, ws_bytes, stream), "sscn_rulebook_build")
+
+
+def sscn_layer_sizes(net: int, nlayers: int, stream: int) -> List[int]:
+    arr = (ctypes.c_int32 * nlayers)()
+    _check(load_library().sscn_layer_sizes(net, arr, stream), "sscn_layer_sizes")
+    return list(arr)
+
+
+def _ptr_array(ptrs: Sequence[int]):
+    return (ctypes.c_void_p * len(ptrs))(*ptrs)
+
+
+def sscn_forward(net, d_feats, W_ptrs, b_ptrs, d_labels, d_logits, d_loss, stream) -> None:
+    _check(load_library().sscn_forward(net, d_feats, _ptr_array(W_ptrs), _ptr_array(b_ptrs), d_labels, d_logits,
+                                       d_loss, stream), "sscn_forward")
+
+
+def sscn_backward(net, dW_ptrs, db_ptrs, d_dfeats, stream) -> None:
+    _check(load_library().sscn_backward(net, _ptr_array(dW_ptrs), _ptr_array(db_ptrs), d_dfeats, stream),
+           "sscn_backward")
+
+
+def sscn_forward_stage(net, stage, stream) -> None:
+    _check(load_library().sscn_forward_stage(net, stage, stream), "sscn_forward_stage")
+
+
+def sscn_backward_stage(net, stage, stream) -> None:
+    _check(load_library().sscn_backward_stage(net, stage, stream), "sscn_backward_stage")
+
+
+def sscn_layer_view_get(net, layer) -> LayerView:
+    v = LayerView()
+    _check(load_library().sscn_layer_view_get(net, layer, ctypes.byref(v)), "sscn_layer_view_get")
+    return v
+
+
+# ---------------------------------------------------------------------------
+# convenience wrapper
+
+
+class SparseDeepCNet:
+    """DeepCNet(ell, k) on the GPU through libsscn; torch supplies memory and the stream."""
+
+    def __init__(self, ell: int, k: int, c_in: int, n_classes: int, batch_max: int, max_active: int,
+                 dtype: str = "bf16", device: str = "cuda"):
+        if dtype not in ("f32", "bf16"):
+            raise ValueError(dtype)
+        self.ell, self.k, self.c_in, self.n_classes = ell, k, c_in, n_classes
+        self.dtype = dtype
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.device = torch.device(device)
+        self.nlayers = 2 * ell + 2
+        desc = NetDesc(ell, k, c_in, n_classes, batch_max, max_active, SSCN_BF16 if dtype == "bf16" else SSCN_F32)
+        self.handle = sscn_net_create(desc)
+        self.ws_bytes = sscn_net_workspace_bytes(self.handle)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        self.param_shapes = [sscn_net_param_shape(self.handle, i) for i in range(sscn_net_num_params(self.handle))]
+        self.dW = [torch.empty(r, c, dtype=torch.float32, device=self.device) for r, c in self.param_shapes]
+        self.db = [torch.empty(c, dtype=torch.float32, device=self.device) for _, c in self.param_shapes]
+        self.loss = torch.empty(1, dtype=torch.float32, device=self.device)
+        self.logits = None
+        self._keep = []
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h:
+            try:
+                sscn_net_destroy(h)
+            except Exception:
+                pass
+            self.handle = None
+
+    # -- calls ---------------------------------------------------------------
+    def rulebook_build(self, coords: torch.Tensor, batch: int) -> None:
+        assert coords.dtype == torch.int32 and coords.is_contiguous() and coords.device.type == "cuda"
+        self.batch = batch
+        self.n = int(coords.shape[0])
+        self._coords = coords
+        sscn_rulebook_build(self.handle, coords.data_ptr() if self.n else None, self.n, batch, self.ws.data_ptr(),
+                            self.ws_bytes, _stream())
+
+    def layer_sizes(self) -> List[int]:
+        return sscn_layer_sizes(self.handle, self.nlayers, _stream())
+
+    def forward(self, feats: torch.Tensor, Ws: Sequence[torch.Tensor], bs: Sequence[torch.Tensor],
+                labels: torch.Tensor):
+        assert feats.dtype == self.tdtype and feats.is_contiguous()
+        assert labels.dtype == torch.int32
+        for W in Ws:
+            assert W.dtype == self.tdtype and W.is_contiguous()
+        for b in bs:
+            assert b.dtype == torch.float32 and b.is_contiguous()
+        if self.logits is None or self.logits.shape[0] != self.batch:
+            self.logits = torch.empty(self.batch, self.n_classes, dtype=torch.float32, device=self.device)
+        self._keep = [feats, list(Ws), list(bs), labels]
+        sscn_forward(self.handle, feats.data_ptr() if feats.numel() else None, [W.data_ptr() for W in Ws],
+                     [b.data_ptr() for b in bs], labels.data_ptr(), self.logits.data_ptr(), self.loss.data_ptr(),
+                     _stream())
+        return self.logits, self.loss
+
+    def backward(self, want_dfeats: bool = False):
+        dfeats = None
+        if want_dfeats:
+            dfeats = torch.empty(self.n, self.c_in, dtype=self.tdtype, device=self.device)
+        sscn_backward(self.handle, [t.data_ptr() for t in self.dW], [t.data_ptr() for t in self.db],
+                      dfeats.data_ptr() if (dfeats is not None and self.n) else None, _stream())
+        return self.dW, self.db, dfeats
+
+    def forward_stage(self, stage: int) -> None:
+        sscn_forward_stage(self.handle, stage, _stream())
+
+    def backward_stage(self, stage: int) -> None:
+        sscn_backward_stage(self.handle, stage, _stream())
+
+    # -- inspection ----------------------------------------------------------
+    def _slice(self, ptr: int, nbytes: int, dtype) -> torch.Tensor:
+        off = ptr - self.ws.data_ptr()
+        assert 0 <= off and off + nbytes <= self.ws_bytes
+        return self.ws[off: off + nbytes].view(dtype)
+
+    def layer_view(self, layer: int, n: Optional[int] = None) -> dict:
+        """Tensors viewing layer `layer` in the workspace, trimmed to n active rows (+ the ground row)."""
+        v = sscn_layer_view_get(self.handle, layer)
+        if n is None:
+            n = self.layer_sizes()[layer]
+        es = 2 if self.dtype == "bf16" else 4
+        out = dict(kind=v.kind, side=v.side, channels=v.channels, row_stride=v.row_stride, window=v.window,
+                   capacity=v.capacity, n=n)
+        rs = v.row_stride
+        out["features"] = self._slice(v.features, (n + 1) * rs * es, self.tdtype).view(n + 1, rs)
+        out["grad"] = self._slice(v.grad, (n + 1) * rs * es, self.tdtype).view(n + 1, rs)
+        out["sites"] = self._slice(v.sites, max(n, 0) * 4, torch.int32) if n else torch.zeros(0, dtype=torch.int32)
+        if layer > 0:
+            A = v.window
+            out["rules"] = self._slice(v.rules, (n + 1) * A * 4, torch.int32).view(n + 1, A)
+            if v.argmax:
+                out["argmax"] = self._slice(v.argmax, (n + 1) * rs, torch.uint8).view(n + 1, rs)
+        return out
+
+    def rules_t(self, layer: int, n_below: int) -> torch.Tensor:
+        v = sscn_layer_view_get(self.handle, layer)
+        if v.kind == 1:
+            return self._slice(v.rules_t, (n_below + 1) * v.window * 4, torch.int32).view(n_below + 1, v.window)
+        return self._slice(v.rules_t, (n_below + 1) * 4, torch.int32)

@@ -1,0 +1,219 @@
+"""HIP path vs the CPU oracle, through the C interface, on the GPU.
+
+Every case prints its name, seed and shape before touching the GPU.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from tests.gpu_harness import Pair, TOL, check_structure, check_values, log, rel_err, to_dtype
+from workloads import CONFIGS, circle_sites, get_config, he_params, make_batch, random_labels
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1409_6070_amd import sscn
+    sscn.load_library()
+
+
+def _sparse_case(seed, ell, batch, p, c_in, empty=(), full=()):
+    rng = np.random.default_rng(seed)
+    N = 3 * 2 ** ell
+    coords = []
+    for b in range(batch):
+        if b in empty:
+            continue
+        m = np.ones((N, N), bool) if b in full else rng.random((N, N)) < p
+        ys, xs = np.nonzero(m)
+        coords.append(np.stack([np.full(ys.size, b), ys, xs], 1))
+    coords = np.concatenate(coords) if coords else np.zeros((0, 3), np.int64)
+    coords = coords[rng.permutation(len(coords))]
+    feats = rng.normal(size=(len(coords), c_in))
+    return coords, feats
+
+
+SMALL = [
+    # name, ell, k, c_in, classes, batch, p, empty, full, seed
+    ("l1k3_m1_b2", 1, 3, 1, 4, 2, 0.3, (), (), 1),
+    ("l2k5_m3_b3_empty", 2, 5, 3, 7, 3, 0.08, (1,), (), 2),
+    ("l2k12_m1_b2_full", 2, 12, 1, 5, 2, 0.1, (), (0,), 3),
+    ("l3k20_m2_b4", 3, 20, 2, 33, 4, 0.05, (), (), 4),
+    ("l3k33_m9_b3", 3, 33, 9, 70, 3, 0.04, (2,), (), 5),
+    ("l4k24_m1_b5", 4, 24, 1, 129, 5, 0.02, (), (), 6),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_small_networks(case, dtype):
+    name, ell, k, c_in, ncls, batch, p, empty, full, seed = case
+    coords, feats = _sparse_case(seed, ell, batch, p, c_in, empty, full)
+    log(f"[small] {name} {dtype} n={len(coords)} seed={seed}")
+    Ws, bs = he_params(ell, k, c_in, ncls, 100 + seed)
+    labels = random_labels(batch, ncls, 200 + seed)
+    pair = Pair(ell, k, c_in, ncls, batch, coords, feats, Ws, bs, labels, dtype).run_gpu()
+    check_structure(pair)
+    rep = check_values(pair)
+    log(f"  worst rel err {max(v for k_, v in rep.items() if not k_.startswith(('argmax', 'relu'))):.3g}")
+
+
+def _config_case(cfg, dtype, index=0):
+    b = make_batch(cfg, index)
+    Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed)
+    labels = random_labels(cfg.batch, cfg.n_classes, cfg.label_seed)
+    return b, Ws, bs, labels
+
+
+CFG_CASES = [(c.name, d) for c in CONFIGS for d in c.dtypes]
+
+
+@pytest.mark.parametrize("name,dtype", CFG_CASES, ids=[f"{n}-{d}" for n, d in CFG_CASES])
+def test_workload_parity_full_size(name, dtype):
+    """The full workloads, every layer, every gradient, against the whole oracle."""
+    cfg = get_config(name)
+    b, Ws, bs, labels = _config_case(cfg, dtype)
+    log(f"[workload] {name} {dtype} n={b.n} batch={cfg.batch}")
+    pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, dtype,
+                max_active=int(b.n * 1.25)).run_gpu()
+    check_structure(pair)
+    rep = check_values(pair)
+    worst = {k_: v for k_, v in rep.items() if not k_.startswith(("argmax", "relu"))}
+    log(f"  worst rel err {max(worst.values()):.3g} ({max(worst, key=worst.get)}); "
+        f"near-tie flips: argmax {sum(v for k_, v in rep.items() if k_.startswith('argmax'))}, "
+        f"relu {sum(v for k_, v in rep.items() if k_.startswith('relu'))}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stage_kernels_on_oracle_inputs(dtype):
+    """Each stage fed the oracle's exact input: pools bit-exact (values and argmax), convs to tolerance."""
+    cfg = get_config("deepcnet4_20_strokes_b8")
+    b, Ws, bs, labels = _config_case(cfg, dtype)
+    log(f"[stage] {cfg.name} {dtype}")
+    pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, dtype).run_gpu()
+    o = pair.o
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    for s in range(1, len(o.layers)):
+        below = pair.net.layer_view(s - 1, pair.counts[s - 1])
+        C = below["channels"]
+        inp = torch.zeros_like(below["features"])
+        inp[:, :C] = torch.tensor(o.layers[s - 1].X, dtype=torch.float64).to(tdt).cuda()
+        below["features"].copy_(inp)
+        pair.net.forward_stage(s)
+        torch.cuda.synchronize()
+        v = pair.view(s)
+        L = o.layers[s]
+        if o.stages[s - 1].kind == "pool":
+            np.testing.assert_array_equal(v["X"], L.X, err_msg=f"pool values stage {s}")
+            np.testing.assert_array_equal(v["argmax"], L.argmax, err_msg=f"pool argmax stage {s}")
+        else:
+            e = rel_err(v["X"], L.X)
+            assert e <= TOL[dtype] / 10, f"conv stage {s}: {e}"
+    # backward, stage by stage from the oracle's gradients
+    for s in range(len(o.layers) - 1, 0, -1):
+        L = o.layers[s]
+        v = pair.net.layer_view(s, pair.counts[s])
+        C = v["channels"]
+        g = torch.zeros_like(v["grad"])
+        g[:, :C] = torch.tensor(L.grad, dtype=torch.float64).to(tdt).cuda()
+        v["grad"].copy_(g)
+        X = torch.zeros_like(v["features"])
+        X[:, :C] = torch.tensor(L.X, dtype=torch.float64).to(tdt).cuda()
+        v["features"].copy_(X)
+        below = pair.net.layer_view(s - 1, pair.counts[s - 1])
+        Xb = torch.zeros_like(below["features"])
+        Xb[:, :below["channels"]] = torch.tensor(o.layers[s - 1].X, dtype=torch.float64).to(tdt).cuda()
+        below["features"].copy_(Xb)
+        pair.net.backward_stage(s)
+        torch.cuda.synchronize()
+        vb = pair.view(s - 1)
+        e = rel_err(vb["G"], o.layers[s - 1].grad)
+        if o.stages[s - 1].kind == "pool":
+            # rows >= 1 are routed copies: exact; row 0 is a sum
+            np.testing.assert_array_equal(vb["G"][1:], o.layers[s - 1].grad[1:], err_msg=f"pool bwd stage {s}")
+        assert e <= TOL[dtype], f"backward stage {s}: {e}"
+
+
+def test_rulebook_path_counts_full_grid():
+    """Fully active 96x96 input of DeepCNet(5,.): routes through the GPU window lists (Section 2.6)."""
+    ell, N = 5, 96
+    ys, xs = np.meshgrid(np.arange(N), np.arange(N), indexing="ij")
+    coords = np.stack([np.zeros(N * N, int), ys.ravel(), xs.ravel()], 1)
+    log("[paths] ell=5 full grid")
+    Ws, bs = he_params(ell, 1, 1, 2, 7)
+    pair = Pair(ell, 1, 1, 2, 1, coords, np.ones((N * N, 1)), Ws, bs, [0], "f32", run_oracle=False).run_gpu()
+    cnt = np.ones(pair.counts[-1] + 1)
+    cnt[0] = 0
+    for s in range(len(pair.counts) - 1, 0, -1):
+        R = pair.view(s)["rules"]
+        nxt = np.zeros(pair.counts[s - 1] + 1)
+        np.add.at(nxt, R[1:].ravel(), np.repeat(cnt[1:], R.shape[1]))
+        nxt[0] = 0
+        cnt = nxt
+    sites = pair.view(0)["sites"]
+    grid = np.zeros((N, N))
+    grid[sites // N, sites % N] = cnt[1:]
+    assert grid[0, 0] == grid[0, N - 1] == grid[N - 1, 0] == grid[N - 1, N - 1] == 1
+    assert np.all(grid[32:64, 32:64] == 9 * 4 ** (ell - 1)) and grid.max() == 9 * 4 ** (ell - 1)
+
+
+def test_circle_fixture_counts():
+    c = circle_sites(96, 32)
+    log("[circle] diameter 32 in 96x96")
+    Ws, bs = he_params(5, 4, 1, 3, 8)
+    pair = Pair(5, 4, 1, 3, 1, c.coords, c.feats, Ws, bs, [1], "f32").run_gpu()
+    check_structure(pair)
+    check_values(pair)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_empty_inputs(dtype):
+    """No active site at all: every layer is its ground row; gradients flow through row 0 only."""
+    log(f"[empty] {dtype}")
+    Ws, bs = he_params(3, 6, 2, 5, 9)
+    pair = Pair(3, 6, 2, 5, 3, np.zeros((0, 3), np.int64), np.zeros((0, 2)), Ws, bs, [0, 4, 2], dtype,
+                want_dfeats=False).run_gpu()
+    assert pair.counts == [0] * 8
+    check_values(pair)
+
+
+def test_repeat_runs_are_bitwise_identical():
+    cfg = get_config("deepcnet5_50_strokes_b100")
+    b, Ws, bs, labels = _config_case(cfg, "bf16", index=1)
+    log("[determinism] deepcnet5_50 bf16 batch 1")
+    pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, "bf16",
+                run_oracle=False)
+    outs = []
+    for _ in range(2):
+        pair.run_gpu()
+        outs.append([pair.logits.copy(), *[w.copy() for w in pair.dW], *[x.copy() for x in pair.db],
+                     pair.dfeats.copy(), pair.view(3)["X"].copy(), pair.view(4)["G"].copy()])
+    for a, c in zip(*outs):
+        np.testing.assert_array_equal(a, c)
+
+
+@pytest.mark.parametrize("bad,status", [("dup", "SSCN_ERR_DUPLICATE_SITE"), ("range", "SSCN_ERR_OUT_OF_RANGE"),
+                                        ("batch", "SSCN_ERR_OUT_OF_RANGE")])
+def test_invalid_sites_are_reported(bad, status):
+    from paper_1409_6070_amd import sscn
+    log(f"[errors] {bad}")
+    net = sscn.SparseDeepCNet(2, 3, 1, 4, batch_max=2, max_active=16, dtype="f32")
+    coords = np.array([[0, 1, 1], [0, 2, 3], [1, 5, 5]], np.int32)
+    if bad == "dup":
+        coords[2] = coords[0]
+    elif bad == "range":
+        coords[1] = (0, 12, 0)
+    else:
+        coords[2] = (2, 0, 0)
+    net.rulebook_build(torch.tensor(coords).cuda(), 2)
+    with pytest.raises(sscn.SSCNError) as e:
+        net.layer_sizes()
+    assert e.value.name == status
+    # a clean build afterwards succeeds
+    ok = np.array([[0, 1, 1], [1, 2, 2]], np.int32)
+    net.rulebook_build(torch.tensor(ok).cuda(), 2)
+    assert net.layer_sizes()[0] == 2

@@ -1,0 +1,91 @@
+"""libsscn without a GPU: it loads, exports every declared symbol, and its host-only calls behave.
+
+No kernel is launched here; calls that reach the GPU are covered by the ``gpu`` tests.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import SparseDeepCNet as Oracle
+from paper_1409_6070_amd import sscn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sscn.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"SSCN_API[^;(]*?\b(sscn_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = sscn.load_library()
+    names = _declared()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(sscn.EXPORTED) == names
+
+
+def test_status_strings():
+    for code in range(8):
+        assert sscn.sscn_status_string(code)
+    assert "twice" in sscn.sscn_status_string(3)
+
+
+@pytest.mark.parametrize("ell,k,c_in,ncls", [(4, 20, 1, 10), (5, 50, 1, 3755), (5, 50, 8, 3755), (5, 100, 3, 10),
+                                             (6, 100, 1, 3755)])
+def test_param_shapes_match_oracle(ell, k, c_in, ncls):
+    h = sscn.sscn_net_create(sscn.NetDesc(ell, k, c_in, ncls, 8, 1000, sscn.SSCN_BF16))
+    try:
+        got = [sscn.sscn_net_param_shape(h, i) for i in range(sscn.sscn_net_num_params(h))]
+        assert got == Oracle(ell, k, c_in, ncls).param_shapes()
+        assert sscn.sscn_net_workspace_bytes(h) > 0
+    finally:
+        sscn.sscn_net_destroy(h)
+
+
+@pytest.mark.parametrize("desc", [
+    (0, 10, 1, 10, 8, 100, 0),       # ell out of range
+    (9, 10, 1, 10, 8, 100, 0),
+    (4, 0, 1, 10, 8, 100, 0),        # k
+    (4, 10, 0, 10, 8, 100, 0),       # c_in
+    (4, 10, 1, 0, 8, 100, 0),        # classes
+    (4, 10, 1, 10, 0, 100, 0),       # batch_max
+    (4, 10, 1, 10, 8, 0, 0),         # max_active
+    (4, 10, 1, 10, 8, 100, 7),       # dtype
+    (7, 10, 1, 10, 100000, 100, 0),  # batch_max * N^2 beyond int32 keys
+])
+def test_create_rejects_bad_descriptions(desc):
+    with pytest.raises(sscn.SSCNError) as e:
+        sscn.sscn_net_create(sscn.NetDesc(*desc))
+    assert e.value.name == "SSCN_ERR_INVALID_ARGUMENT"
+
+
+def test_host_checked_errors_need_no_gpu():
+    lib = sscn.load_library()
+    h = sscn.sscn_net_create(sscn.NetDesc(3, 4, 1, 5, 4, 100, sscn.SSCN_F32))
+    try:
+        ws = sscn.sscn_net_workspace_bytes(h)
+        fake = 1 << 20  # never dereferenced: each call below fails its host checks first
+        assert lib.sscn_rulebook_build(h, fake, 101, 4, fake, ws, None) == 4  # n > max_active
+        assert lib.sscn_rulebook_build(h, fake, 10, 5, fake, ws, None) == 4  # batch > batch_max
+        assert lib.sscn_rulebook_build(h, fake, 10, 4, None, ws, None) == 7  # no workspace
+        assert lib.sscn_rulebook_build(h, fake, 10, 4, fake, ws - 1, None) == 7  # too small
+        assert lib.sscn_rulebook_build(h, fake + 8, 10, 4, fake + 8, ws, None) == 7  # misaligned
+        assert lib.sscn_rulebook_build(h, None, 10, 4, fake, ws, None) == 1  # null coords
+        arr = (ctypes.c_int32 * 8)()
+        assert lib.sscn_layer_sizes(h, arr, None) == 5  # before any build
+        ptrs = (ctypes.c_void_p * 5)(*([fake] * 5))
+        assert lib.sscn_forward(h, fake, ptrs, ptrs, fake, fake, fake, None) == 5  # before build
+        assert lib.sscn_backward(h, ptrs, ptrs, None, None) == 5  # before forward
+        assert lib.sscn_forward_stage(h, 1, None) == 5
+        assert lib.sscn_forward_stage(h, 0, None) == 1
+        assert lib.sscn_net_param_shape(h, 5, ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_int64())) == 1
+        v = sscn.LayerView()
+        assert lib.sscn_layer_view_get(h, 0, ctypes.byref(v)) == 5  # no workspace bound yet
+    finally:
+        sscn.sscn_net_destroy(h)

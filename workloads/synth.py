@@ -150,7 +150,11 @@ def _layer_shapes(ell: int, k: int, c_in: int):
 
 
 def he_params(ell: int, k: int, c_in: int, n_classes: int, seed: int):
-    """Random parameters for DeepCNet(ell, k): He-normal weights, U[-0.1, 0.1] biases.
+    """Random parameters for DeepCNet(ell, k): U[-0.1, 0.1] biases; He-normal
+    convolution weights (N(0, 2/fan_in), the usual choice before a ReLU) and a
+    Glorot-normal softmax layer (N(0, 2/(fan_in + fan_out)), the usual choice for
+    a linear output layer; it keeps fresh logits O(1) instead of saturating the
+    softmax).
 
     Returns ``(Ws, bs)``: ``ell + 2`` matrices, the convolutions' ``[F*F*C_in, C_out]``
     (rows ordered ``(dy*F + dx)*C_in + c``) followed by the softmax layer's
@@ -160,8 +164,9 @@ def he_params(ell: int, k: int, c_in: int, n_classes: int, seed: int):
     rng = np.random.default_rng(seed)
     shapes = _layer_shapes(ell, k, c_in) + [((ell + 1) * k, n_classes)]
     Ws, bs = [], []
-    for rows, cols in shapes:
-        Ws.append(rng.normal(0.0, np.sqrt(2.0 / rows), size=(rows, cols)))
+    for i, (rows, cols) in enumerate(shapes):
+        var = 2.0 / rows if i < len(shapes) - 1 else 2.0 / (rows + cols)
+        Ws.append(rng.normal(0.0, np.sqrt(var), size=(rows, cols)))
         bs.append(rng.uniform(-0.1, 0.1, size=cols))
     return Ws, bs
 
