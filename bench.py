@@ -1,0 +1,279 @@
+"""Benchmark: DeepCNet(5,50) sparse-convolution forward + backward, samples/s on one MI355X.
+
+One step = rulebook build + forward + backward (every stage, the softmax layer
+and its loss, all parameter gradients) for one batch of 100 synthetic
+pen-stroke samples on a 96x96 grid; the inputs of 8 pre-generated batches are
+resident in HBM before timing starts.  Prints one JSON line on stdout.
+
+    python bench.py [--steps K] [--warmup W] [--dtype bf16|f32] [--workload NAME]
+    python bench.py --calibrate-copy      # plain device copy, for counter scaling
+
+Measurement: W untimed steps, then K steps between two device synchronisations.
+During the timed steps the library brackets every launch of the gather-GEMM
+kernel class with HIP events on the stream it runs on; the roofline object
+divides that class's algorithmic FLOPs by its event-measured time.  A second,
+shorter pass times every kernel class for the breakdown.  The CPU baseline is
+the oracle (test infrastructure) timed on this host on batch 0.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+from workloads import get_config, he_params, make_batches, random_labels  # noqa: E402
+
+DEFAULT_WORKLOAD = "deepcnet5_50_strokes_b100"
+MFMA_PEAK = {"bf16": 2.5e15, "f32": 157.3e12}  # dense MFMA FLOP/s, MI355X
+HBM_PEAK = 8.0e12  # bytes/s
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def layer_shapes(cfg):
+    """(kind, A, C_in, C_out) per stage of DeepCNet(ell, k) (Section 2.1)."""
+    st = [("conv", 9, cfg.c_in, cfg.k)]
+    c = cfg.k
+    for n in range(2, cfg.ell + 2):
+        st.append(("pool", 4, c, c))
+        st.append(("conv", 4, c, n * cfg.k))
+        c = n * cfg.k
+    return st
+
+
+def gemm_work(cfg, sizes):
+    """Algorithmic FLOPs of one step, per kernel class.
+
+    gather_gemm: convolution forward 2(n_s+1)A C_in C_out per stage, convolution
+    input gradient 2 n_{s-1} A C_out C_in per stage s > 1 (the first layer's
+    input gradient is not part of a training step), softmax layer forward and
+    dh, 2 B C_last classes each.
+    wgrad: 2(n_s+1)A C_in C_out per stage plus 2 B C_last classes.
+    """
+    fwd = dgrad = 0.0
+    for s, (kind, A, ci, co) in enumerate(layer_shapes(cfg), start=1):
+        if kind != "conv":
+            continue
+        fwd += 2.0 * (sizes[s] + 1) * A * ci * co
+        if s > 1:
+            dgrad += 2.0 * sizes[s - 1] * A * co * ci
+    head = 2.0 * cfg.batch * (cfg.ell + 1) * cfg.k * cfg.n_classes
+    return {"gather_gemm": fwd + dgrad + 2 * head, "wgrad": fwd + head, "conv_total": 2 * fwd + dgrad}
+
+
+def read_traffic(kernel, dtype):
+    """HBM bytes per launch from the committed counter summary, if it matches the current kernel source."""
+    path = os.path.join(PROFILES, f"{kernel}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_1409_6070_amd", "csrc", kv.get("source", "gemm.hip"))
+    if not os.path.exists(src):
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if kv.get("source_sha256_16") != sha or kv.get("dtype") != dtype:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0):
+    """The oracle, as it stands, on batch 0: build + forward + backward, repeated for ~budget_s."""
+    from oracle import SparseDeepCNet as Oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = 1
+    feats = torch.tensor(batch.feats, dtype=torch.float32)
+    Wt = [torch.tensor(W, dtype=torch.float32) for W in Ws]
+    if dtype == "bf16":
+        feats = feats.to(torch.bfloat16)
+        Wt = [w.to(torch.bfloat16) for w in Wt]
+    feats = feats.double().numpy()
+    Wn = [w.double().numpy() for w in Wt]
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        o = Oracle(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, dtype)
+        o.build(batch.coords, batch.batch)
+        o.forward(feats, Wn, bs, labels)
+        o.backward()
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 50:
+            break
+    cpu = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(reps * cfg.batch / el, 3), "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "sample": f"batch 0 of {cfg.name} ({cfg.batch} samples), {reps} x (build + forward + backward), "
+                      f"mode {dtype}, {el:.1f} s; NumPy float64, BLAS threads {threads}; host CPU: {cpu}"}
+
+
+def calibrate_copy():
+    """A plain device-to-device copy of known size (for scaling FETCH_SIZE / WRITE_SIZE)."""
+    n = 256 << 20  # bytes
+    a = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--batches", type=int, default=8)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported here "
+              "(the path would shard over samples with one all-reduce of dW/db per step)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+
+    from paper_1409_6070_amd.sscn import SparseDeepCNet
+
+    cfg = get_config(args.workload)
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if args.dtype == "bf16" else torch.float32
+    log(f"[bench] generating {args.batches} batches of {cfg.name}")
+    batches = make_batches(cfg, args.batches)
+    Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed)
+    labels = random_labels(cfg.batch, cfg.n_classes, cfg.label_seed)
+    Ws_d = [torch.tensor(W, dtype=torch.float32).to(tdt).to(dev).contiguous() for W in Ws]
+    bs_d = [torch.tensor(b, dtype=torch.float32).to(dev).contiguous() for b in bs]
+    lab_d = torch.tensor(labels, dtype=torch.int32, device=dev)
+    inputs = []
+    for b in batches:
+        inputs.append((torch.tensor(b.coords, dtype=torch.int32, device=dev).contiguous(),
+                       torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous()))
+    max_active = max(b.n for b in batches)
+    net = SparseDeepCNet(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, batch_max=cfg.batch, max_active=max_active,
+                         dtype=args.dtype)
+    sizes = []
+    for c, _ in inputs:
+        net.rulebook_build(c, cfg.batch)
+        sizes.append(net.layer_sizes())
+    torch.cuda.synchronize()
+
+    def step(i):
+        c, f = inputs[i % len(inputs)]
+        net.rulebook_build(c, cfg.batch)
+        net.forward(f, Ws_d, bs_d, lab_d)
+        net.backward()
+
+    log(f"[bench] warmup {args.warmup} steps")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    net.timing_collect("gather_gemm")  # drop anything recorded so far
+    net.timing(["gather_gemm"])
+    log(f"[bench] timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    g_launches, g_ms = net.timing_collect("gather_gemm")
+    net.timing([])
+    sec = (t1 - t0) / args.steps
+    value = cfg.batch / sec
+    log(f"[bench] {sec * 1e3:.3f} ms/step, {value:.1f} samples/s")
+
+    # algorithmic work of the timed steps (batches cycle in order)
+    step_sizes = [sizes[i % len(sizes)] for i in range(args.steps)]
+    work = [gemm_work(cfg, s) for s in step_sizes]
+    g_flops = sum(w["gather_gemm"] for w in work)
+    avg_launch_s = g_ms / 1e3 / max(g_launches, 1)
+    achieved = g_flops / max(g_launches, 1) / avg_launch_s if g_launches else 0.0
+    peak = MFMA_PEAK[args.dtype]
+    traffic = read_traffic("gather_gemm", args.dtype)
+    roofline = {
+        "kernel": "k_gemm_gather (implicit-gather MFMA GEMM: conv forward, conv input gradient, softmax layer)",
+        "bound": "mfma", "achieved": round(achieved / 1e12, 3), "peak": peak / 1e12, "unit": "TFLOP/s",
+        "frac": round(achieved / peak, 5), "traffic": traffic,
+        "launches_per_step": g_launches / args.steps, "avg_launch_us": round(avg_launch_s * 1e6, 3),
+        "algorithmic_gflop_per_launch": round(g_flops / max(g_launches, 1) / 1e9, 4),
+    }
+
+    # breakdown of one pass over a few steps with every class timed
+    from paper_1409_6070_amd.sscn import KERNEL_CLASSES
+
+    net.timing(KERNEL_CLASSES)
+    nb = min(5, args.steps)
+    for i in range(nb):
+        step(i)
+    breakdown = {}
+    for kc in KERNEL_CLASSES:
+        n, ms = net.timing_collect(kc)
+        breakdown[kc] = {"launches_per_step": n / nb, "us_per_step": round(ms * 1e3 / nb, 2)}
+    net.timing([])
+
+    mean_sizes = np.mean(np.array(sizes, dtype=np.float64), axis=0)
+    conv_flops = float(np.mean([w["conv_total"] for w in work]))
+    out = {
+        "metric": "DeepCNet(5,50) sparse-conv fwd+bwd samples/sec; GEMM % MFMA peak",
+        "value": round(value, 2),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "net": f"DeepCNet({cfg.ell},{cfg.k})", "grid": cfg.grid,
+                   "c_in": cfg.c_in, "classes": cfg.n_classes, "batch": cfg.batch,
+                   "input_active_fraction": round(float(mean_sizes[0]) / (cfg.batch * cfg.grid ** 2), 4),
+                   "step": "rulebook build + forward + backward"},
+        "conv_gemm_gflop_per_step": round(conv_flops / 1e9, 3),
+        "roofline": roofline,
+        "kernel_breakdown": breakdown,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(cfg, batches[0], Ws, bs, labels, args.dtype)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

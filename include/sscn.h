@@ -158,6 +158,32 @@ SSCN_API sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* con
 SSCN_API sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream);
 SSCN_API sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream);
 
+/* Kernel timing with HIP events, for measurement tools.  Kernel classes: */
+typedef enum {
+  SSCN_KC_RULEBOOK = 0,   /* active sets, window lists, transposes            */
+  SSCN_KC_GATHER_GEMM = 1,/* implicit-gather MFMA GEMM: conv forward, conv input
+                             gradient, softmax layer forward and dh          */
+  SSCN_KC_WGRAD = 2,      /* split-K MFMA weight gradient                      */
+  SSCN_KC_WGRAD_REDUCE = 3,/* partial sums -> dW, db, ground-row sums; row-0 dX */
+  SSCN_KC_POOL_FWD = 4,
+  SSCN_KC_POOL_BWD = 5,   /* routing gather + ground-row reduction            */
+  SSCN_KC_HEAD = 6,       /* input scatter, weight packing, softmax, loss, scatter of dh */
+  SSCN_KC_COUNT = 7
+} sscn_kernel_class;
+
+/* While enabled, every launch of a kernel whose class bit (1 << class) is set
+ * in class_mask is bracketed by a pair of HIP events recorded on the caller's
+ * stream.  A mask of 0 disables timing.  Events are created on first use and
+ * destroyed with the net; at most 65536 launches are recorded between two
+ * sscn_timing_collect calls (further launches are not timed). */
+SSCN_API sscn_status sscn_timing_enable(sscn_net* net, uint32_t class_mask);
+
+/* Synchronises `stream`, then for kernel class `kernel_class` returns the
+ * number of timed launches and the sum of their event-measured durations
+ * (milliseconds) since the previous collect, and forgets those records. */
+SSCN_API sscn_status sscn_timing_collect(sscn_net* net, int32_t kernel_class, int32_t* launches, float* total_ms,
+                                         void* stream);
+
 /* Describes layer `layer` (0 .. 2*ell+1) of the bound workspace. */
 SSCN_API sscn_status sscn_layer_view_get(const sscn_net* net, int32_t layer, sscn_layer_view* out);
 

@@ -5,6 +5,7 @@
 
 #include <cstring>
 #include <new>
+#include <vector>
 
 #include "../../include/sscn.h"
 #include "common.h"
@@ -89,7 +90,43 @@ struct sscn_net {
   bool want_dfeats;
   float* logits;
   const int32_t* labels;
+  // kernel timing (HIP events around launcher calls of the selected classes)
+  uint32_t tmask = 0;
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_next = 0;
+  struct Rec {
+    int cls;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  ~sscn_net() {
+    for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+  }
 };
+
+static constexpr size_t MAX_TIMED = 65536;
+
+static hipEvent_t next_event(sscn_net* net) {
+  if (net->ev_next == net->ev_pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    net->ev_pool.push_back(e);
+  }
+  return net->ev_pool[net->ev_next++];
+}
+
+// Runs one launcher call; when its class is being timed, brackets it with two events.
+template <class F>
+static hipError_t timed(sscn_net* net, int cls, hipStream_t st, F&& launch) {
+  if (!(net->tmask & (1u << cls)) || net->recs.size() >= MAX_TIMED) return launch();
+  hipEvent_t a = next_event(net), b = next_event(net);
+  if (!a || !b) return launch();
+  if (hipEventRecord(a, st) != hipSuccess) return hipErrorUnknown;
+  hipError_t e = launch();
+  if (hipEventRecord(b, st) != hipSuccess) return hipErrorUnknown;
+  net->recs.push_back({cls, a, b});
+  return e;
+}
 
 static void carve(sscn_net* net, void* base) {
   Carver cv(base);
@@ -326,7 +363,8 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   a.head_rows = net->head_rows;
   a.coords = d_coords;
   a.n = n;
-  if (launch_rulebook(a, wk, net->max_words, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (timed(net, SSCN_KC_RULEBOOK, st, [&] { return launch_rulebook(a, wk, net->max_words, st); }) != hipSuccess)
+    return SSCN_ERR_HIP;
   net->built = true;
   return SSCN_OK;
 }
@@ -369,9 +407,11 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
     g.rows_dev = net->counts + s;
     g.rows_add = 1;
     g.row_begin = 0;
-    return launch_gemm(net->bf16, g, L.cap + 1, st);
+    return timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, L.cap + 1, st); });
   }
-  return launch_pool_fwd(net->bf16, Lb.X, Lb.Cp, L.rules, L.X, L.Cp, L.argmax, L.Cp, net->counts + s, L.cap, st);
+  return timed(net, SSCN_KC_POOL_FWD, st, [&] {
+    return launch_pool_fwd(net->bf16, Lb.X, Lb.Cp, L.rules, L.X, L.Cp, L.argmax, L.Cp, net->counts + s, L.cap, st);
+  });
 }
 
 static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
@@ -379,8 +419,10 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
   const LayerPlan& Lb = net->L[s - 1];
   hipError_t e;
   if (L.kind == 2)
-    return launch_pool_bwd(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, L.rules, Lb.X, Lb.grad, L.Cp,
-                           net->counts + s, net->counts + s - 1, Lb.cap, L.cap, net->ppart, net->pool_parts, st);
+    return timed(net, SSCN_KC_POOL_BWD, st, [&] {
+      return launch_pool_bwd(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, L.rules, Lb.X, Lb.grad, L.Cp,
+                             net->counts + s, net->counts + s - 1, Lb.cap, L.cap, net->ppart, net->pool_parts, st);
+    });
   const int ci = L.conv_index;
   const ParamPlan& P = net->P[ci];
   WGradArgs w{};
@@ -400,9 +442,11 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
   w.rows_add = 1;
   w.nchunks = P.nchunks;
   w.part = net->wpart;
-  if ((e = launch_wgrad(net->bf16, w, st)) != hipSuccess) return e;
-  if ((e = launch_wgrad_reduce(net->wpart, P.nchunks, P.Mpad_w, P.Npad_w, P.A, P.cp_in, P.c_in, P.c_out, P.m_ones,
-                               P.m_ind, net->dW[ci], net->db[ci], net->D0, st)) != hipSuccess)
+  if ((e = timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, w, st); })) != hipSuccess) return e;
+  if ((e = timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
+         return launch_wgrad_reduce(net->wpart, P.nchunks, P.Mpad_w, P.Npad_w, P.A, P.cp_in, P.c_in, P.c_out,
+                                    P.m_ones, P.m_ind, net->dW[ci], net->db[ci], net->D0, st);
+       })) != hipSuccess)
     return e;
   if (s == 1 && !net->want_dfeats) return hipSuccess;
   GemmArgs g{};
@@ -424,8 +468,12 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
   g.rows_dev = net->counts + s - 1;
   g.rows_add = 1;
   g.row_begin = 1;
-  if ((e = launch_gemm(net->bf16, g, Lb.cap + 1, st)) != hipSuccess) return e;
-  return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, st);
+  if ((e = timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, Lb.cap + 1, st); })) !=
+      hipSuccess)
+    return e;
+  return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
+    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, st);
+  });
 }
 
 sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
@@ -443,14 +491,19 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   net->logits = d_logits;
   net->labels = d_labels;
   const LayerPlan& L0 = net->L[0];
-  if (launch_scatter_input(net->bf16, d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, st) != hipSuccess)
+  if (timed(net, SSCN_KC_HEAD, st, [&] {
+        return launch_scatter_input(net->bf16, d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, st);
+      }) != hipSuccess)
     return SSCN_ERR_HIP;
   for (int p = 0; p < net->nparams; ++p) {
     const ParamPlan& P = net->P[p];
-    if (launch_pack(net->bf16, 0, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpF, P.NpadF, P.KpadF, st) !=
-            hipSuccess ||
-        launch_pack(net->bf16, 1, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpD, P.NpadD, P.KpadD, st) !=
-            hipSuccess)
+    if (timed(net, SSCN_KC_HEAD, st, [&] {
+          hipError_t e = launch_pack(net->bf16, 0, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpF, P.NpadF,
+                                     P.KpadF, st);
+          if (e != hipSuccess) return e;
+          return launch_pack(net->bf16, 1, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpD, P.NpadD,
+                             P.KpadD, st);
+        }) != hipSuccess)
       return SSCN_ERR_HIP;
   }
   for (int s = 1; s < net->nlayers; ++s)
@@ -476,9 +529,12 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   g.epi = EPI_BIAS_F32;
   g.rows_host = net->batch;
   g.row_begin = 0;
-  if (launch_gemm(net->bf16, g, net->batch, st) != hipSuccess) return SSCN_ERR_HIP;
-  if (launch_softmax_xent(net->bf16, d_logits, d_labels, net->batch, net->d.n_classes, net->dlogits, net->dl_stride,
-                          net->loss_part, d_loss, st) != hipSuccess)
+  if (timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, net->batch, st); }) != hipSuccess)
+    return SSCN_ERR_HIP;
+  if (timed(net, SSCN_KC_HEAD, st, [&] {
+        return launch_softmax_xent(net->bf16, d_logits, d_labels, net->batch, net->d.n_classes, net->dlogits,
+                                   net->dl_stride, net->loss_part, d_loss, st);
+      }) != hipSuccess)
     return SSCN_ERR_HIP;
   net->forwarded = true;
   return SSCN_OK;
@@ -515,9 +571,12 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   w.rows_host = net->batch;
   w.nchunks = 1;
   w.part = net->wpart;
-  if (launch_wgrad(net->bf16, w, st) != hipSuccess) return SSCN_ERR_HIP;
-  if (launch_wgrad_reduce(net->wpart, 1, P.Mpad_w, P.Npad_w, 1, P.cp_in, P.c_in, P.c_out, P.m_ones, -1, h_dW[fc],
-                          h_db[fc], nullptr, st) != hipSuccess)
+  if (timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, w, st); }) != hipSuccess)
+    return SSCN_ERR_HIP;
+  if (timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
+        return launch_wgrad_reduce(net->wpart, 1, P.Mpad_w, P.Npad_w, 1, P.cp_in, P.c_in, P.c_out, P.m_ones, -1,
+                                   h_dW[fc], h_db[fc], nullptr, st);
+      }) != hipSuccess)
     return SSCN_ERR_HIP;
   GemmArgs g{};
   g.src = net->dlogits;
@@ -537,15 +596,19 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   g.epi = EPI_F32;
   g.rows_host = net->batch;
   g.row_begin = 0;
-  if (launch_gemm(net->bf16, g, net->batch, st) != hipSuccess) return SSCN_ERR_HIP;
-  if (launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp, st) !=
-      hipSuccess)
+  if (timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, net->batch, st); }) != hipSuccess)
+    return SSCN_ERR_HIP;
+  if (timed(net, SSCN_KC_HEAD, st, [&] {
+        return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp, st);
+      }) != hipSuccess)
     return SSCN_ERR_HIP;
   for (int s = top; s >= 1; --s)
     if (backward_stage(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
   if (d_dfeats) {
     const LayerPlan& L0 = net->L[0];
-    if (launch_gather_dfeats(net->bf16, L0.grad, L0.Cp, net->perm, net->n, net->d.c_in, d_dfeats, st) != hipSuccess)
+    if (timed(net, SSCN_KC_HEAD, st, [&] {
+          return launch_gather_dfeats(net->bf16, L0.grad, L0.Cp, net->perm, net->n, net->d.c_in, d_dfeats, st);
+        }) != hipSuccess)
       return SSCN_ERR_HIP;
   }
   return SSCN_OK;
@@ -561,6 +624,37 @@ sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream) {
   if (!net || stage < 1 || stage >= net->nlayers) return SSCN_ERR_INVALID_ARGUMENT;
   if (!net->forwarded || !net->dW[0]) return SSCN_ERR_BAD_STATE;
   return backward_stage(net, stage, (hipStream_t)stream) == hipSuccess ? SSCN_OK : SSCN_ERR_HIP;
+}
+
+sscn_status sscn_timing_enable(sscn_net* net, uint32_t class_mask) {
+  if (!net) return SSCN_ERR_INVALID_ARGUMENT;
+  net->tmask = class_mask & ((1u << SSCN_KC_COUNT) - 1u);
+  return SSCN_OK;
+}
+
+sscn_status sscn_timing_collect(sscn_net* net, int32_t kernel_class, int32_t* launches, float* total_ms,
+                                void* stream) {
+  if (!net || !launches || !total_ms || kernel_class < 0 || kernel_class >= SSCN_KC_COUNT)
+    return SSCN_ERR_INVALID_ARGUMENT;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return SSCN_ERR_HIP;
+  int32_t n = 0;
+  float tot = 0.f;
+  std::vector<sscn_net::Rec> keep;
+  for (const auto& r : net->recs) {
+    if (r.cls != kernel_class) {
+      keep.push_back(r);
+      continue;
+    }
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return SSCN_ERR_HIP;
+    tot += ms;
+    ++n;
+  }
+  net->recs.swap(keep);
+  if (net->recs.empty()) net->ev_next = 0;
+  *launches = n;
+  *total_ms = tot;
+  return SSCN_OK;
 }
 
 sscn_status sscn_layer_view_get(const sscn_net* net, int32_t layer, sscn_layer_view* out) {

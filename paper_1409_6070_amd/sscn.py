@@ -31,8 +31,9 @@ STATUS = {
 EXPORTED = [
     "sscn_net_create", "sscn_net_destroy", "sscn_status_string", "sscn_net_num_params", "sscn_net_param_shape",
     "sscn_net_workspace_bytes", "sscn_rulebook_build", "sscn_layer_sizes", "sscn_forward", "sscn_backward",
-    "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get",
+    "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get", "sscn_timing_enable", "sscn_timing_collect",
 ]
+KERNEL_CLASSES = ["rulebook", "gather_gemm", "wgrad", "wgrad_reduce", "pool_fwd", "pool_bwd", "head"]
 
 
 class SSCNError(RuntimeError):
@@ -82,6 +83,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sscn_forward_stage": (I32, [VP, I32, VP]),
         "sscn_backward_stage": (I32, [VP, I32, VP]),
         "sscn_layer_view_get": (I32, [VP, I32, P(LayerView)]),
+        "sscn_timing_enable": (I32, [VP, ctypes.c_uint32]),
+        "sscn_timing_collect": (I32, [VP, I32, P(I32), P(ctypes.c_float), VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -172,6 +175,17 @@ def sscn_layer_view_get(net, layer) -> LayerView:
     return v
 
 
+def sscn_timing_enable(net, class_mask: int) -> None:
+    _check(load_library().sscn_timing_enable(net, class_mask), "sscn_timing_enable")
+
+
+def sscn_timing_collect(net, kernel_class: int, stream):
+    n, ms = ctypes.c_int32(), ctypes.c_float()
+    _check(load_library().sscn_timing_collect(net, kernel_class, ctypes.byref(n), ctypes.byref(ms), stream),
+           "sscn_timing_collect")
+    return n.value, ms.value
+
+
 # ---------------------------------------------------------------------------
 # convenience wrapper
 
@@ -243,6 +257,17 @@ class SparseDeepCNet:
         sscn_backward(self.handle, [t.data_ptr() for t in self.dW], [t.data_ptr() for t in self.db],
                       dfeats.data_ptr() if (dfeats is not None and self.n) else None, _stream())
         return self.dW, self.db, dfeats
+
+    def timing(self, classes: Sequence[str]) -> None:
+        """Bracket launches of the named kernel classes with HIP events (empty: off)."""
+        mask = 0
+        for c in classes:
+            mask |= 1 << KERNEL_CLASSES.index(c)
+        sscn_timing_enable(self.handle, mask)
+
+    def timing_collect(self, kernel_class: str):
+        """(launches, total milliseconds) of a class since the last collect."""
+        return sscn_timing_collect(self.handle, KERNEL_CLASSES.index(kernel_class), _stream())
 
     def forward_stage(self, stage: int) -> None:
         sscn_forward_stage(self.handle, stage, _stream())
