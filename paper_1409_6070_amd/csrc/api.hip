@@ -35,8 +35,10 @@ struct LayerPlan {
 
 struct ParamPlan {
   int A, c_in, c_out, cp_in, cp_out;  // FC: A = 1, cp_in = Cp_last, cp_out = dlogits stride
+  GemmPlan pf, pd;                    // forward (logits) and input-gradient (dh) GEMMs
+  int64_t rows_f, rows_d;             // their row bounds
   int NpadF, KpadF, NpadD, KpadD;
-  int Mpad_w, Npad_w, nchunks, m_ones, m_ind;
+  int Mpad_w, Npad_w, bn_w, nchunks, m_ones, m_ind;
   void* WpF;
   void* WpD;
 };
@@ -74,6 +76,7 @@ struct sscn_net {
   float* dh;
   float* loss_part;
   float* wpart;
+  float* gpart;  // split-K partials of the gather GEMMs
   float* D0;
   float* ppart;
   size_t ws_bytes;
@@ -99,10 +102,35 @@ struct sscn_net {
     hipEvent_t a, b;
   };
   std::vector<Rec> recs;
+  // second stream of the backward pass: weight gradients run beside the
+  // input-gradient chain; ev_fork[s] / ev_join[s] order the two per stage
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork[MAX_LAYERS + 1] = {};
+  hipEvent_t ev_join[MAX_LAYERS + 1] = {};
   ~sscn_net() {
     for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+    for (int i = 0; i <= MAX_LAYERS; ++i) {
+      if (ev_fork[i]) (void)hipEventDestroy(ev_fork[i]);
+      if (ev_join[i]) (void)hipEventDestroy(ev_join[i]);
+    }
+    if (side) (void)hipStreamDestroy(side);
   }
 };
+
+static bool ensure_side_stream(sscn_net* net) {
+  if (net->side) return true;
+  hipStream_t s = nullptr;
+  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return false;
+  for (int i = 0; i <= MAX_LAYERS; ++i) {
+    if (hipEventCreateWithFlags(&net->ev_fork[i], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&net->ev_join[i], hipEventDisableTiming) != hipSuccess) {
+      (void)hipStreamDestroy(s);
+      return false;
+    }
+  }
+  net->side = s;
+  return true;
+}
 
 static constexpr size_t MAX_TIMED = 65536;
 
@@ -135,7 +163,7 @@ static void carve(sscn_net* net, void* base) {
   net->err = (int32_t*)cv.take(sizeof(int32_t) * 4);
   net->perm = (int32_t*)cv.take(sizeof(int32_t) * (size_t)net->d.max_active);
   net->head_rows = (int32_t*)cv.take(sizeof(int32_t) * (size_t)B);
-  size_t max_part = 0, max_d0 = 0;
+  size_t max_part = 0, max_d0 = 0, max_gpart = 0;
   int max_cp = 0;
   for (int s = 0; s < net->nlayers; ++s) {
     LayerPlan& L = net->L[s];
@@ -167,20 +195,32 @@ static void carve(sscn_net* net, void* base) {
     P.WpD = cv.take((size_t)P.NpadD * P.KpadD * net->esz);
     max_part = std::max(max_part, (size_t)P.nchunks * P.Mpad_w * P.Npad_w);
     max_d0 = std::max(max_d0, (size_t)P.A * P.c_out);
+    if (P.pf.ksplit > 1) max_gpart = std::max(max_gpart, (size_t)P.pf.ksplit * P.rows_f * P.pf.Npad);
+    if (P.pd.ksplit > 1) max_gpart = std::max(max_gpart, (size_t)P.pd.ksplit * P.rows_d * P.pd.Npad);
   }
   const LayerPlan& Lt = net->L[net->nlayers - 1];
   net->dlogits = cv.take((size_t)B * net->dl_stride * net->esz);
   net->dh = (float*)cv.take((size_t)B * Lt.Cp * 4);
   net->loss_part = (float*)cv.take((size_t)B * 4);
   net->wpart = (float*)cv.take(max_part * 4);
+  net->gpart = (float*)cv.take(std::max<size_t>(max_gpart, 1) * 4);
   net->D0 = (float*)cv.take(max_d0 * 4);
   net->ppart = (float*)cv.take((size_t)net->pool_parts * max_cp * 4);
   net->ws_bytes = cv.off + 256;
 }
 
+static void set_plan(GemmArgs& g, const GemmPlan& p, int64_t rows_cap, float* gpart) {
+  g.cfg = p.cfg;
+  g.ksplit = p.ksplit;
+  g.part = gpart;
+  g.part_rows = (int32_t)rows_cap;
+}
+
 static int wgrad_chunks(int64_t rows_cap, int tiles_mn, int BK) {
-  int64_t max_chunks = std::max<int64_t>(1, (rows_cap + 4 * BK - 1) / (4 * BK));
-  int64_t want = std::max<int64_t>(1, (512 + tiles_mn - 1) / tiles_mn);
+  // about 1024 workgroups (at most 512 chunks), each summing at least 4 slabs of sites:
+  // the kernel is latency-bound, so workgroups in flight matter more than partial-sum bytes
+  int64_t max_chunks = std::max<int64_t>(1, std::min<int64_t>(512, (rows_cap + 4 * BK - 1) / (4 * BK)));
+  int64_t want = std::max<int64_t>(1, (1024 + tiles_mn - 1) / tiles_mn);
   return (int)std::min<int64_t>(want, max_chunks);
 }
 
@@ -219,8 +259,8 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   net->VE = 16 / net->esz;
   net->nlayers = 2 * d.ell + 2;
   net->nparams = d.ell + 2;
-  net->pool_parts = 64;
-  const GemmTile gt = gemm_tile(net->bf16);
+  net->pool_parts = 128;  // most row blocks of a ground-row reduction
+  const int BK = net->bf16 ? 64 : 32;
   const int VE = net->VE;
   auto cp = [VE](int c) { return (int)round_up(c, VE); };
   // layers (Section 2.1): input N; conv3 N-2; then (pool S/2, conv2 S-1) x ell
@@ -256,6 +296,10 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   }
   for (int s = 0; s < net->nlayers; ++s) {
     L[s].Cp = cp(L[s].C);
+    if (L[s].Cp / VE > 256) {  // one channel vector per thread of a 256-thread block
+      delete net;
+      return SSCN_ERR_INVALID_ARGUMENT;
+    }
     L[s].Wd = (L[s].S + 63) / 64;
     if ((L[s].cap + 1) * (int64_t)std::max(L[s].Cp, std::max(L[s].A, 1)) >= (1ll << 31)) {
       delete net;
@@ -273,15 +317,20 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.c_out = L[s].C;
     P.cp_in = L[s - 1].Cp;
     P.cp_out = L[s].Cp;
-    P.NpadF = (int)round_up(P.c_out, gt.BN);
-    P.KpadF = (int)round_up((int64_t)P.A * P.cp_in, gt.BK);
-    P.NpadD = (int)round_up(P.c_in, gt.BN);
-    P.KpadD = (int)round_up((int64_t)P.A * P.cp_out, gt.BK);
+    P.rows_f = L[s].cap + 1;
+    P.rows_d = L[s - 1].cap + 1;
+    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.A * P.cp_in);
+    P.pd = plan_gemm(net->bf16, P.rows_d, P.c_in, P.A * P.cp_out);
+    P.NpadF = P.pf.Npad;
+    P.KpadF = P.pf.Kpad;
+    P.NpadD = P.pd.Npad;
+    P.KpadD = P.pd.Kpad;
     P.m_ones = P.A * P.cp_in;
     P.m_ind = P.m_ones + 1;
-    P.Mpad_w = (int)round_up(P.m_ind + P.A, gt.BM);
-    P.Npad_w = (int)round_up(P.c_out, gt.BN);
-    P.nchunks = wgrad_chunks(L[s].cap + 1, (P.Mpad_w / gt.BM) * (P.Npad_w / gt.BN), gt.BK);
+    P.Mpad_w = (int)round_up(P.m_ind + P.A, WG_BM);
+    P.bn_w = wgrad_bn(P.c_out);
+    P.Npad_w = (int)round_up(P.c_out, P.bn_w);
+    P.nchunks = wgrad_chunks(L[s].cap + 1, (P.Mpad_w / WG_BM) * (P.Npad_w / P.bn_w), BK);
   }
   {
     ParamPlan& P = net->P[d.ell + 1];
@@ -291,14 +340,19 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.c_out = d.n_classes;
     P.cp_in = Lt.Cp;
     P.cp_out = net->dl_stride;
-    P.NpadF = (int)round_up(P.c_out, gt.BN);
-    P.KpadF = (int)round_up(P.cp_in, gt.BK);
-    P.NpadD = (int)round_up(P.c_in, gt.BN);
-    P.KpadD = (int)round_up(P.cp_out, gt.BK);
+    P.rows_f = d.batch_max;
+    P.rows_d = d.batch_max;
+    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.cp_in);
+    P.pd = plan_gemm(net->bf16, P.rows_d, P.c_in, P.cp_out);
+    P.NpadF = P.pf.Npad;
+    P.KpadF = P.pf.Kpad;
+    P.NpadD = P.pd.Npad;
+    P.KpadD = P.pd.Kpad;
     P.m_ones = P.cp_in;
     P.m_ind = -1;
-    P.Mpad_w = (int)round_up(P.m_ones + 1, gt.BM);
-    P.Npad_w = (int)round_up(P.c_out, gt.BN);
+    P.Mpad_w = (int)round_up(P.m_ones + 1, WG_BM);
+    P.bn_w = wgrad_bn(P.c_out);
+    P.Npad_w = (int)round_up(P.c_out, P.bn_w);
     P.nchunks = 1;
   }
   carve(net, nullptr);
@@ -363,7 +417,23 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   a.head_rows = net->head_rows;
   a.coords = d_coords;
   a.n = n;
-  if (timed(net, SSCN_KC_RULEBOOK, st, [&] { return launch_rulebook(a, wk, net->max_words, st); }) != hipSuccess)
+  // window-list segments, each with workgroups for about two rows per thread at capacity
+  RulesWork rw;
+  std::memset(&rw, 0, sizeof(rw));
+  auto add_seg = [&](int kind, int layer, int64_t rows) {
+    const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>(2048, (rows + 511) / 512));
+    rw.kind[rw.nseg] = kind;
+    rw.layer[rw.nseg] = layer;
+    rw.blk[rw.nseg + 1] = rw.blk[rw.nseg] + blocks;
+    ++rw.nseg;
+  };
+  for (int s = 1; s < net->nlayers; ++s) {
+    add_seg(0, s, net->L[s].cap + 1);
+    add_seg(1, s, net->L[s - 1].cap + 1);
+  }
+  add_seg(2, 0, n);
+  add_seg(3, 0, batch);
+  if (timed(net, SSCN_KC_RULEBOOK, st, [&] { return launch_rulebook(a, wk, rw, net->max_words, st); }) != hipSuccess)
     return SSCN_ERR_HIP;
   net->built = true;
   return SSCN_OK;
@@ -407,6 +477,7 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
     g.rows_dev = net->counts + s;
     g.rows_add = 1;
     g.row_begin = 0;
+    set_plan(g, P.pf, P.rows_f, net->gpart);
     return timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, L.cap + 1, st); });
   }
   return timed(net, SSCN_KC_POOL_FWD, st, [&] {
@@ -414,17 +485,34 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
   });
 }
 
-static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
+// Backward of stage s.  With side != st the weight gradient (and the ground-row
+// term of the input gradient, which needs its column sums) runs on `side`, the
+// rest of the input gradient on `st`; a pooling stage waits for the side
+// stream of the convolution above only before its ground-row step.
+static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st, hipStream_t side) {
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
+  const bool split = side != st;
   hipError_t e;
-  if (L.kind == 2)
+  if (L.kind == 2) {
+    const int nparts = (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (L.cap + 255) / 256));
+    if ((e = timed(net, SSCN_KC_POOL_BWD, st, [&] {
+           return launch_pool_bwd_rows(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, L.rules, Lb.X, Lb.grad, L.Cp,
+                                       net->counts + s, net->counts + s - 1, Lb.cap, net->ppart, nparts, st);
+         })) != hipSuccess)
+      return e;
+    if (split && (e = hipStreamWaitEvent(st, net->ev_join[s + 1], 0)) != hipSuccess) return e;
     return timed(net, SSCN_KC_POOL_BWD, st, [&] {
-      return launch_pool_bwd(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, L.rules, Lb.X, Lb.grad, L.Cp,
-                             net->counts + s, net->counts + s - 1, Lb.cap, L.cap, net->ppart, net->pool_parts, st);
+      return launch_pool_row0_final(net->bf16, L.grad, net->ppart, nparts, Lb.X, Lb.grad, L.Cp, st);
     });
+  }
   const int ci = L.conv_index;
   const ParamPlan& P = net->P[ci];
+  const bool need_dx = s > 1 || net->want_dfeats;
+  if (split) {
+    if ((e = hipEventRecord(net->ev_fork[s], st)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side, net->ev_fork[s], 0)) != hipSuccess) return e;
+  }
   WGradArgs w{};
   w.src = Lb.X;
   w.src_stride = Lb.Cp;
@@ -442,13 +530,24 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
   w.rows_add = 1;
   w.nchunks = P.nchunks;
   w.part = net->wpart;
-  if ((e = timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, w, st); })) != hipSuccess) return e;
-  if ((e = timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
+  w.cfg = P.bn_w == 128 ? 0 : 1;
+  w.dW = net->dW[ci];
+  w.db = net->db[ci];
+  w.D0 = net->D0;
+  w.c_in = P.c_in;
+  w.c_out = P.c_out;
+  if ((e = timed(net, SSCN_KC_WGRAD, side, [&] { return launch_wgrad(net->bf16, w, side); })) != hipSuccess) return e;
+  if ((e = timed(net, SSCN_KC_WGRAD_REDUCE, side, [&] {
          return launch_wgrad_reduce(net->wpart, P.nchunks, P.Mpad_w, P.Npad_w, P.A, P.cp_in, P.c_in, P.c_out,
-                                    P.m_ones, P.m_ind, net->dW[ci], net->db[ci], net->D0, st);
+                                    P.m_ones, P.m_ind, net->dW[ci], net->db[ci], net->D0, side);
        })) != hipSuccess)
     return e;
-  if (s == 1 && !net->want_dfeats) return hipSuccess;
+  if (need_dx && (e = timed(net, SSCN_KC_WGRAD_REDUCE, side, [&] {
+                    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, side);
+                  })) != hipSuccess)
+    return e;
+  if (split && (e = hipEventRecord(net->ev_join[s], side)) != hipSuccess) return e;
+  if (!need_dx) return hipSuccess;
   GemmArgs g{};
   g.src = L.grad;
   g.src_stride = L.Cp;
@@ -468,12 +567,8 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st) {
   g.rows_dev = net->counts + s - 1;
   g.rows_add = 1;
   g.row_begin = 1;
-  if ((e = timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, Lb.cap + 1, st); })) !=
-      hipSuccess)
-    return e;
-  return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
-    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, st);
-  });
+  set_plan(g, P.pd, P.rows_d, net->gpart);
+  return timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, Lb.cap + 1, st); });
 }
 
 sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
@@ -495,17 +590,15 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
         return launch_scatter_input(net->bf16, d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
+  PackArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
   for (int p = 0; p < net->nparams; ++p) {
     const ParamPlan& P = net->P[p];
-    if (timed(net, SSCN_KC_HEAD, st, [&] {
-          hipError_t e = launch_pack(net->bf16, 0, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpF, P.NpadF,
-                                     P.KpadF, st);
-          if (e != hipSuccess) return e;
-          return launch_pack(net->bf16, 1, h_W[p], P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.WpD, P.NpadD,
-                             P.KpadD, st);
-        }) != hipSuccess)
-      return SSCN_ERR_HIP;
+    pa.job[pa.njobs++] = PackJob{h_W[p], P.WpF, 0, P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.NpadF, P.KpadF};
+    pa.job[pa.njobs++] = PackJob{h_W[p], P.WpD, 1, P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.NpadD, P.KpadD};
   }
+  if (timed(net, SSCN_KC_HEAD, st, [&] { return launch_pack_all(net->bf16, pa, st); }) != hipSuccess)
+    return SSCN_ERR_HIP;
   for (int s = 1; s < net->nlayers; ++s)
     if (forward_stage(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
   // softmax layer on each sample's top-layer row
@@ -529,6 +622,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   g.epi = EPI_BIAS_F32;
   g.rows_host = net->batch;
   g.row_begin = 0;
+  set_plan(g, P.pf, P.rows_f, net->gpart);
   if (timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, net->batch, st); }) != hipSuccess)
     return SSCN_ERR_HIP;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
@@ -550,11 +644,16 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   }
   hipStream_t st = (hipStream_t)stream;
   net->want_dfeats = d_dfeats != nullptr;
+  if (!ensure_side_stream(net)) return SSCN_ERR_HIP;
+  hipStream_t side = net->side;
   const int top = net->nlayers - 1;
   const LayerPlan& Lt = net->L[top];
   const int fc = net->d.ell + 1;
   const ParamPlan& P = net->P[fc];
-  // softmax layer: dW, db from (h, dlogits); dh = dlogits W^T
+  // softmax layer: dW, db from (h, dlogits) on the side stream; dh = dlogits W^T on st
+  if (hipEventRecord(net->ev_fork[MAX_LAYERS], st) != hipSuccess ||
+      hipStreamWaitEvent(side, net->ev_fork[MAX_LAYERS], 0) != hipSuccess)
+    return SSCN_ERR_HIP;
   WGradArgs w{};
   w.src = Lt.X;
   w.src_stride = Lt.Cp;
@@ -571,11 +670,17 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   w.rows_host = net->batch;
   w.nchunks = 1;
   w.part = net->wpart;
-  if (timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, w, st); }) != hipSuccess)
+  w.cfg = P.bn_w == 128 ? 0 : 1;
+  w.dW = h_dW[fc];
+  w.db = h_db[fc];
+  w.D0 = nullptr;
+  w.c_in = P.c_in;
+  w.c_out = P.c_out;
+  if (timed(net, SSCN_KC_WGRAD, side, [&] { return launch_wgrad(net->bf16, w, side); }) != hipSuccess)
     return SSCN_ERR_HIP;
-  if (timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
+  if (timed(net, SSCN_KC_WGRAD_REDUCE, side, [&] {
         return launch_wgrad_reduce(net->wpart, 1, P.Mpad_w, P.Npad_w, 1, P.cp_in, P.c_in, P.c_out, P.m_ones, -1,
-                                   h_dW[fc], h_db[fc], nullptr, st);
+                                   h_dW[fc], h_db[fc], nullptr, side);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
   GemmArgs g{};
@@ -596,6 +701,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   g.epi = EPI_F32;
   g.rows_host = net->batch;
   g.row_begin = 0;
+  set_plan(g, P.pd, P.rows_d, net->gpart);
   if (timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, net->batch, st); }) != hipSuccess)
     return SSCN_ERR_HIP;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
@@ -603,7 +709,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
       }) != hipSuccess)
     return SSCN_ERR_HIP;
   for (int s = top; s >= 1; --s)
-    if (backward_stage(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
+    if (backward_stage(net, s, st, side) != hipSuccess) return SSCN_ERR_HIP;
   if (d_dfeats) {
     const LayerPlan& L0 = net->L[0];
     if (timed(net, SSCN_KC_HEAD, st, [&] {
@@ -611,6 +717,9 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
         }) != hipSuccess)
       return SSCN_ERR_HIP;
   }
+  // everything on the side stream completes before the caller's stream moves on
+  if (hipEventRecord(net->ev_join[0], side) != hipSuccess || hipStreamWaitEvent(st, net->ev_join[0], 0) != hipSuccess)
+    return SSCN_ERR_HIP;
   return SSCN_OK;
 }
 
@@ -623,7 +732,8 @@ sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream) {
 sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream) {
   if (!net || stage < 1 || stage >= net->nlayers) return SSCN_ERR_INVALID_ARGUMENT;
   if (!net->forwarded || !net->dW[0]) return SSCN_ERR_BAD_STATE;
-  return backward_stage(net, stage, (hipStream_t)stream) == hipSuccess ? SSCN_OK : SSCN_ERR_HIP;
+  hipStream_t st = (hipStream_t)stream;
+  return backward_stage(net, stage, st, st) == hipSuccess ? SSCN_OK : SSCN_ERR_HIP;
 }
 
 sscn_status sscn_timing_enable(sscn_net* net, uint32_t class_mask) {

@@ -48,240 +48,438 @@ struct MfmaCore<float> {
   }
 };
 
-// Tile shape: WM x WN waves, each TM x TN 16x16 MFMA tiles.
-constexpr int G_WM = 2, G_WN = 2, G_TM = 2, G_TN = 2;
-constexpr int G_THREADS = 64 * G_WM * G_WN;
-constexpr int G_BM = G_WM * G_TM * 16;
-constexpr int G_BN = G_WN * G_TN * 16;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <typename T>
-struct Tiles {
+// Tile configuration: WM x WN waves, each computing TM x TN 16x16 MFMA tiles;
+// K advances in slabs of 128 bytes per row (64 bf16 / 32 fp32 elements).
+template <typename T, int WM_, int WN_, int TM_, int TN_>
+struct GCfg {
+  static constexpr int WM = WM_, WN = WN_, TM = TM_, TN = TN_;
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int BM = WM * TM * 16, BN = WN * TN * 16;
   static constexpr int VE = Elem<T>::VE;
   static constexpr int KB = MfmaCore<T>::KB;
-  static constexpr int BK = 2 * KB;  // 128 bytes of k per LDS row
-  static constexpr int LDK = BK + VE;  // padded LDS row (elements)
+  static constexpr int BK = 2 * KB;
+  static constexpr int KV = BK / VE;       // 16-byte vectors per row and slab
+  static constexpr int LDK = BK + VE;      // LDS row pitch (elements), padded against bank conflicts
+  static constexpr int AV = BM * KV / NT;  // A vectors per thread and slab
+  static constexpr int BV = BN * KV / NT;
+  static_assert(AV * NT == BM * KV && BV * NT == BN * KV, "tile must split evenly over the threads");
 };
 
-GemmTile gemm_tile(bool bf16) {
-  return bf16 ? GemmTile{G_BM, G_BN, Tiles<__bf16>::BK} : GemmTile{G_BM, G_BN, Tiles<float>::BK};
+constexpr int AMAX = 9;  // largest window (3x3)
+
+// the four tile shapes (index = GemmArgs::cfg)
+template <typename T> using C128x128 = GCfg<T, 2, 2, 4, 4>;
+template <typename T> using C128x64 = GCfg<T, 4, 1, 2, 4>;
+template <typename T> using C64x64 = GCfg<T, 2, 2, 2, 2>;
+template <typename T> using C32x64 = GCfg<T, 2, 2, 1, 2>;
+
+GemmTile gemm_tile(bool bf16, int cfg) {
+  const int BK = bf16 ? 64 : 32;
+  switch (cfg) {
+    case 0: return GemmTile{128, 128, BK};
+    case 1: return GemmTile{128, 64, BK};
+    case 2: return GemmTile{64, 64, BK};
+    default: return GemmTile{32, 64, BK};
+  }
 }
 
-// acc[i][j] += A_tile(wave rows i) * B_tile(wave cols j) over one BK slab in LDS
-template <typename T>
-__device__ inline void mma_slab(const T* As, const T* Bs, f32x4 (&acc)[G_TM][G_TN], int wm, int wn, int lane) {
-  constexpr int LDK = Tiles<T>::LDK;
-  constexpr int KB = Tiles<T>::KB;
-  constexpr int VE = Tiles<T>::VE;
+// acc[i][j] += A_tile(wave rows i) * B_tile(wave cols j) over one slab in LDS
+template <typename T, class C>
+__device__ inline void mma_slab(const T* As, const T* Bs, f32x4 (&acc)[C::TM][C::TN], int wm, int wn, int lane) {
   const int r16 = lane & 15, g = lane >> 4;
 #pragma unroll
-  for (int kb = 0; kb < Tiles<T>::BK; kb += KB) {
+  for (int kb = 0; kb < C::BK; kb += C::KB) {
 #pragma unroll
-    for (int i = 0; i < G_TM; ++i)
+    for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-      for (int j = 0; j < G_TN; ++j)
-        MfmaCore<T>::step(As + (wm * G_TM * 16 + i * 16 + r16) * LDK + kb + g * VE,
-                          Bs + (wn * G_TN * 16 + j * 16 + r16) * LDK + kb + g * VE, acc[i][j]);
+      for (int j = 0; j < C::TN; ++j)
+        MfmaCore<T>::step(As + (wm * C::TM * 16 + i * 16 + r16) * C::LDK + kb + g * C::VE,
+                          Bs + (wn * C::TN * 16 + j * 16 + r16) * C::LDK + kb + g * C::VE, acc[i][j]);
   }
 }
 
 template <typename T>
-__global__ void __launch_bounds__(G_THREADS) k_gemm_gather(GemmArgs a) {
-  constexpr int VE = Tiles<T>::VE;
-  constexpr int BK = Tiles<T>::BK;
-  constexpr int LDK = Tiles<T>::LDK;
-  constexpr int KV = BK / VE;  // vectors per LDS row
-  __shared__ __attribute__((aligned(16))) T As[G_BM * LDK];
-  __shared__ __attribute__((aligned(16))) T Bs[G_BN * LDK];
+__device__ inline float epi_value(const GemmArgs& a, float v, int n) {
+  if (a.bias && n < a.N) v += a.bias[n];
+  if (a.epi == EPI_BIAS_RELU) v = fmaxf(v, 0.f);
+  return v;
+}
+
+template <typename T>
+__device__ inline void store_out(const GemmArgs& a, int64_t m, int n, float v) {
+  const int64_t o = m * a.out_stride + n;
+  if (a.epi == EPI_BIAS_RELU || a.epi == EPI_STORE)
+    ((T*)a.out)[o] = Elem<T>::from_f32(v);
+  else
+    ((float*)a.out)[o] = v;
+}
+
+// Implicit-gather GEMM.  Per tile: the tile's window rows go to LDS once; the
+// next K slab's global loads are issued before the current slab's MFMAs
+// (register prefetch); the output tile is staged in LDS for 16-byte stores.
+// With ksplit > 1 each workgroup covers one K range and writes fp32 partial
+// sums, reduced (with the epilogue) by k_gemm_splitk_reduce.
+template <typename T, class C>
+__global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
+  constexpr int VE = C::VE, BK = C::BK, KV = C::KV, LDK = C::LDK, BM = C::BM, BN = C::BN, NT = C::NT;
+  constexpr int SMEM = (BM + BN) * LDK;
+  constexpr int CS = BN + VE;  // staging pitch
+  constexpr bool STAGE = BM * CS <= SMEM;
+  __shared__ __attribute__((aligned(16))) T smem[SMEM];
+  __shared__ int32_t Rs[BM * AMAX];
+  T* As = smem;
+  T* Bs = smem + BM * LDK;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / G_WN, wn = wave % G_WN;
+  const int wm = wave / C::WN, wn = wave % C::WN;
   const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
   const int span = rows - a.row_begin;
   if (span <= 0) return;
-  const int tiles_m = (span + G_BM - 1) / G_BM;
-  const int tiles_n = a.Npad / G_BN;
+  const int tiles_m = (span + BM - 1) / BM;
+  const int tiles_n = a.Npad / BN;
+  const int kslabs = a.Kpad / BK;
+  const int kper = (kslabs + a.ksplit - 1) / a.ksplit * BK;
+  const int ntiles = tiles_m * tiles_n * a.ksplit;
   const T* src = (const T*)a.src;
   const T* Bt = (const T*)a.Bt;
+  const int A = a.A;
 
-  for (int tile = blockIdx.x; tile < tiles_m * tiles_n; tile += gridDim.x) {
-    const int tn = tile % tiles_n, tm = tile / tiles_n;
-    const int m0 = a.row_begin + tm * G_BM, n0 = tn * G_BN;
-    f32x4 acc[G_TM][G_TN];
-#pragma unroll
-    for (int i = 0; i < G_TM; ++i)
-#pragma unroll
-      for (int j = 0; j < G_TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int tn = tile % tiles_n;
+    const int t2 = tile / tiles_n;
+    const int tm = t2 % tiles_m;
+    const int ks = t2 / tiles_m;
+    const int m0 = a.row_begin + tm * BM, n0 = tn * BN;
+    const int kbeg = ks * kper;
+    const int kend = min(a.Kpad, kbeg + kper);
 
-    for (int k0 = 0; k0 < a.Kpad; k0 += BK) {
-      for (int v = tid; v < G_BM * KV; v += G_THREADS) {
+    for (int i = tid; i < BM * A; i += NT) {
+      const int r = i / A, f = i - r * A, m = m0 + r;
+      int v = -1;
+      if (m < rows) v = a.rmap ? a.rmap[(int64_t)m * A + f] : (f == 0 ? m : -1);
+      Rs[i] = v;
+    }
+    __syncthreads();
+
+    f32x4 acc[C::TM][C::TN];
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    u32x4 ra[C::AV], rb[C::BV];
+    auto load = [&](int k0) {
+#pragma unroll
+      for (int j = 0; j < C::AV; ++j) {
+        const int v = tid + j * NT;
         const int r = v / KV, kv = v - r * KV;
-        const int m = m0 + r, k = k0 + kv * VE;
-        Vec16 val = {{0u, 0u, 0u, 0u}};
-        if (m < rows && k < a.K) {
+        const int k = k0 + kv * VE;
+        u32x4 val = {0u, 0u, 0u, 0u};
+        if (k < a.K) {
           const int f = k / a.cseg, c = k - f * a.cseg;
-          const int srow = a.rmap ? a.rmap[(int64_t)m * a.A + f] : m;
-          if (srow >= 0) val = *(const Vec16*)(src + (int64_t)srow * a.src_stride + c);
+          const int srow = Rs[r * A + f];
+          if (srow >= 0) val = *(const u32x4*)(src + (int64_t)srow * a.src_stride + c);
         }
-        *(Vec16*)(As + r * LDK + kv * VE) = val;
+        ra[j] = val;
       }
-      for (int v = tid; v < G_BN * KV; v += G_THREADS) {
+#pragma unroll
+      for (int j = 0; j < C::BV; ++j) {
+        const int v = tid + j * NT;
         const int r = v / KV, kv = v - r * KV;
-        *(Vec16*)(Bs + r * LDK + kv * VE) = *(const Vec16*)(Bt + (int64_t)(n0 + r) * a.Kpad + k0 + kv * VE);
+        rb[j] = *(const u32x4*)(Bt + (int64_t)(n0 + r) * a.Kpad + k0 + kv * VE);
+      }
+    };
+    if (kbeg < kend) load(kbeg);
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+#pragma unroll
+      for (int j = 0; j < C::AV; ++j) {
+        const int v = tid + j * NT;
+        const int r = v / KV, kv = v - r * KV;
+        *(u32x4*)(As + r * LDK + kv * VE) = ra[j];
+      }
+#pragma unroll
+      for (int j = 0; j < C::BV; ++j) {
+        const int v = tid + j * NT;
+        const int r = v / KV, kv = v - r * KV;
+        *(u32x4*)(Bs + r * LDK + kv * VE) = rb[j];
       }
       __syncthreads();
-      mma_slab<T>(As, Bs, acc, wm, wn, lane);
+      if (k0 + BK < kend) load(k0 + BK);
+      mma_slab<T, C>(As, Bs, acc, wm, wn, lane);
       __syncthreads();
     }
 
     const int g = lane >> 4, c16 = lane & 15;
+    if (a.ksplit > 1) {
+      float* part = a.part + (int64_t)ks * a.part_rows * a.Npad;
 #pragma unroll
-    for (int i = 0; i < G_TM; ++i)
+      for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-      for (int j = 0; j < G_TN; ++j) {
-        const int n = n0 + wn * G_TN * 16 + j * 16 + c16;
-        if (n >= a.out_cols) continue;
-        const float bias = (a.bias && n < a.N) ? a.bias[n] : 0.f;
+        for (int j = 0; j < C::TN; ++j) {
+          const int n = n0 + wn * C::TN * 16 + j * 16 + c16;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m0 + wm * G_TM * 16 + i * 16 + g * 4 + r;
-          if (m >= rows) continue;
-          float v = acc[i][j][r] + bias;
-          const int64_t o = (int64_t)m * a.out_stride + n;
-          switch (a.epi) {
-            case EPI_BIAS_RELU:
-              ((T*)a.out)[o] = Elem<T>::from_f32(fmaxf(v, 0.f));
-              break;
-            case EPI_STORE:
-              ((T*)a.out)[o] = Elem<T>::from_f32(v);
-              break;
-            default:
-              ((float*)a.out)[o] = v;
-              break;
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
+            if (m < rows) part[(int64_t)m * a.Npad + n] = acc[i][j][r];
           }
         }
+    } else if (STAGE && (a.epi == EPI_BIAS_RELU || a.epi == EPI_STORE)) {
+      T* Cs = smem;
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j) {
+          const int nl = wn * C::TN * 16 + j * 16 + c16;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int ml = wm * C::TM * 16 + i * 16 + g * 4 + r;
+            Cs[ml * CS + nl] = Elem<T>::from_f32(epi_value<T>(a, acc[i][j][r], n0 + nl));
+          }
+        }
+      __syncthreads();
+      for (int v = tid; v < BM * (BN / VE); v += NT) {
+        const int r = v / (BN / VE), nv = v - r * (BN / VE);
+        const int m = m0 + r, n = n0 + nv * VE;
+        if (m < rows && n < a.out_cols)
+          *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = *(const u32x4*)(Cs + r * CS + nv * VE);
       }
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j) {
+          const int n = n0 + wn * C::TN * 16 + j * 16 + c16;
+          if (n >= a.out_cols) continue;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
+            if (m < rows) store_out<T>(a, m, n, epi_value<T>(a, acc[i][j][r], n));
+          }
+        }
+    }
+    __syncthreads();
   }
 }
 
+// Sum of the split-K partials plus the epilogue.
 template <typename T>
-__global__ void __launch_bounds__(G_THREADS) k_wgrad(WGradArgs a) {
-  constexpr int VE = Tiles<T>::VE;
-  constexpr int BK = Tiles<T>::BK;
-  constexpr int LDK = Tiles<T>::LDK;
-  __shared__ __attribute__((aligned(16))) T As[G_BM * LDK];  // [m][site]
-  __shared__ __attribute__((aligned(16))) T Bs[G_BN * LDK];  // [n][site]
+__global__ void __launch_bounds__(256) k_gemm_splitk_reduce(GemmArgs a) {
+  const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
+  const int64_t span = rows - a.row_begin;
+  if (span <= 0) return;
+  const int64_t total = span * a.out_cols;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t m = a.row_begin + t / a.out_cols;
+    const int n = (int)(t % a.out_cols);
+    float s = 0.f;
+    for (int ks = 0; ks < a.ksplit; ++ks) s += a.part[((int64_t)ks * a.part_rows + m) * a.Npad + n];
+    store_out<T>(a, m, n, epi_value<T>(a, s, n));
+  }
+}
+
+// Packs 4 consecutive-site values of one element into one LDS store.
+template <typename T>
+struct Quad;
+template <>
+struct Quad<__bf16> {
+  typedef uint64_t W;
+  __device__ static inline W pack(__bf16 a, __bf16 b, __bf16 c, __bf16 d) {
+    return (uint64_t)__builtin_bit_cast(uint16_t, a) | ((uint64_t)__builtin_bit_cast(uint16_t, b) << 16) |
+           ((uint64_t)__builtin_bit_cast(uint16_t, c) << 32) | ((uint64_t)__builtin_bit_cast(uint16_t, d) << 48);
+  }
+};
+template <>
+struct Quad<float> {
+  typedef u32x4 W;
+  __device__ static inline W pack(float a, float b, float c, float d) {
+    return u32x4{__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b), __builtin_bit_cast(uint32_t, c),
+                 __builtin_bit_cast(uint32_t, d)};
+  }
+};
+
+// Weight-gradient GEMM, split over sites (the K dimension).  A^T and delta^T
+// slabs are staged in LDS as [row of dW / col of dW][site]: each thread loads
+// 16-byte vectors (VE consecutive channels) of 4 consecutive sites and stores
+// them transposed, 4 sites per LDS write.  Loads of the next slab are issued
+// before the current slab's MFMAs.
+template <typename T, class C>
+__global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
+  constexpr int VE = C::VE, BK = C::BK, LDK = C::LDK, BM = C::BM, BN = C::BN, NT = C::NT;
+  constexpr int MV = BM / VE, NV = BN / VE;  // vectors across a slab row
+  static_assert(MV * (BK / 4) == NT && NV * (BK / 4) <= NT, "one quad of sites per thread");
+  typedef typename Quad<T>::W QW;
+  __shared__ __attribute__((aligned(16))) T As[BM * LDK];  // [m][site]
+  __shared__ __attribute__((aligned(16))) T Bs[BN * LDK];  // [n][site]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / G_WN, wn = wave % G_WN;
+  const int wm = wave / C::WN, wn = wave % C::WN;
   const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
-  const int tiles_m = a.Mpad / G_BM, tiles_n = a.Npad / G_BN;
+  const int tiles_m = a.Mpad / BM, tiles_n = a.Npad / BN;
   const int ntiles = tiles_m * tiles_n * a.nchunks;
   const int per = ((rows + a.nchunks - 1) / a.nchunks + BK - 1) / BK * BK;
   const int m_gather = a.A * a.cseg;
+  const int m_rows = a.m_ind >= 0 ? a.m_ind + a.A : a.m_ones + 1;  // rows of dW / db / D0 that are read back
   const T* src = (const T*)a.src;
   const T* dsrc = (const T*)a.dsrc;
   const T one = Elem<T>::from_f32(1.f), zero = Elem<T>::from_f32(0.f);
+  // this thread's quad: sites 4*q .. 4*q+3 of a slab, vector mv / nv
+  const int qa = tid / MV, mv = tid - qa * MV;
+  const int qb = tid / NV, nvv = tid - qb * NV;
+  const bool b_active = tid < NV * (BK / 4);
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int tn = tile % tiles_n;
     const int tq = tile / tiles_n;
     const int tm = tq % tiles_m;
     const int chunk = tq / tiles_m;
-    const int m0 = tm * G_BM, n0 = tn * G_BN;
+    const int m0 = tm * BM, n0 = tn * BN;
     const int o_beg = chunk * per;
     const int o_end = min(rows, o_beg + per);
-    f32x4 acc[G_TM][G_TN];
+    f32x4 acc[C::TM][C::TN];
 #pragma unroll
-    for (int i = 0; i < G_TM; ++i)
+    for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-      for (int j = 0; j < G_TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int ob = o_beg; ob < o_end; ob += BK) {
-      // A^T slab: As[m][o - ob], gathered along m (contiguous channels of one row)
-      for (int v = tid; v < BK * (G_BM / VE); v += G_THREADS) {
-        const int ol = v / (G_BM / VE), mv = v - ol * (G_BM / VE);
-        const int o = ob + ol, m = m0 + mv * VE;
-        T vals[VE];
+    u32x4 ra[4], rb[4];
+    const int m = m0 + mv * VE;
+    const int f_of_m = m < m_gather ? m / a.cseg : 0;
+    const int c_of_m = m < m_gather ? m - f_of_m * a.cseg : 0;
+    const int n = n0 + nvv * VE;
+    // source rows of this thread's 4 sites, fetched one slab ahead of their use
+    int rnext[4];
+    auto load_rows = [&](int ob) {
 #pragma unroll
-        for (int j = 0; j < VE; ++j) vals[j] = zero;
+      for (int i = 0; i < 4; ++i) {
+        const int o = ob + 4 * qa + i;
+        int r = -1;
+        if (o < o_end && m < m_gather) r = a.rmap ? a.rmap[(int64_t)o * a.A + f_of_m] : o;
+        rnext[i] = r;
+      }
+    };
+    auto load = [&](int ob) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int o = ob + 4 * qa + i;
+        u32x4 val = {0u, 0u, 0u, 0u};
         if (o < o_end) {
           if (m < m_gather) {
-            const int f = m / a.cseg, c = m - f * a.cseg;
-            const int srow = a.rmap ? a.rmap[(int64_t)o * a.A + f] : o;
-            Vec16 raw = *(const Vec16*)(src + (int64_t)srow * a.src_stride + c);
-            const T* rv = (const T*)&raw;
-#pragma unroll
-            for (int j = 0; j < VE; ++j) vals[j] = rv[j];
+            val = *(const u32x4*)(src + (int64_t)rnext[i] * a.src_stride + c_of_m);
           } else {
+            T* vv = (T*)&val;
 #pragma unroll
             for (int j = 0; j < VE; ++j) {
               const int mm = m + j;
-              if (mm == a.m_ones) vals[j] = one;
+              T x = zero;
+              if (mm == a.m_ones)
+                x = one;
               else if (a.m_ind >= 0 && mm >= a.m_ind && mm < a.m_ind + a.A)
-                vals[j] = (a.rmap[(int64_t)o * a.A + (mm - a.m_ind)] == 0) ? one : zero;
+                x = (a.rmap[(int64_t)o * a.A + (mm - a.m_ind)] == 0) ? one : zero;
+              vv[j] = x;
             }
           }
         }
-#pragma unroll
-        for (int j = 0; j < VE; ++j) As[(mv * VE + j) * LDK + ol] = vals[j];
+        ra[i] = val;
       }
-      // B^T slab: Bs[n][o - ob]
-      for (int v = tid; v < BK * (G_BN / VE); v += G_THREADS) {
-        const int ol = v / (G_BN / VE), nv = v - ol * (G_BN / VE);
-        const int o = ob + ol, n = n0 + nv * VE;
-        T vals[VE];
 #pragma unroll
-        for (int j = 0; j < VE; ++j) vals[j] = zero;
-        if (o < o_end && n < a.dsrc_cols) {
-          Vec16 raw = *(const Vec16*)(dsrc + (int64_t)o * a.dsrc_stride + n);
-          const T* rv = (const T*)&raw;
+      for (int i = 0; i < 4; ++i) {
+        const int o = ob + 4 * qb + i;
+        u32x4 val = {0u, 0u, 0u, 0u};
+        if (b_active && o < o_end && n < a.dsrc_cols) val = *(const u32x4*)(dsrc + (int64_t)o * a.dsrc_stride + n);
+        rb[i] = val;
+      }
+    };
+    load_rows(o_beg);
+    if (o_beg < o_end) {
+      load(o_beg);
+      load_rows(o_beg + BK);
+    }
+    for (int ob = o_beg; ob < o_end; ob += BK) {
 #pragma unroll
-          for (int j = 0; j < VE; ++j) vals[j] = rv[j];
-        }
+      for (int j = 0; j < VE; ++j)
+        *(QW*)(As + (mv * VE + j) * LDK + 4 * qa) =
+            Quad<T>::pack(((const T*)&ra[0])[j], ((const T*)&ra[1])[j], ((const T*)&ra[2])[j], ((const T*)&ra[3])[j]);
+      if (b_active) {
 #pragma unroll
-        for (int j = 0; j < VE; ++j) Bs[(nv * VE + j) * LDK + ol] = vals[j];
+        for (int j = 0; j < VE; ++j)
+          *(QW*)(Bs + (nvv * VE + j) * LDK + 4 * qb) = Quad<T>::pack(((const T*)&rb[0])[j], ((const T*)&rb[1])[j],
+                                                                      ((const T*)&rb[2])[j], ((const T*)&rb[3])[j]);
       }
       __syncthreads();
-      mma_slab<T>(As, Bs, acc, wm, wn, lane);
+      if (ob + BK < o_end) {
+        load(ob + BK);
+        load_rows(ob + 2 * BK);
+      }
+      mma_slab<T, C>(As, Bs, acc, wm, wn, lane);
       __syncthreads();
     }
 
     float* part = a.part + (int64_t)chunk * a.Mpad * a.Npad;
     const int g = lane >> 4, c16 = lane & 15;
 #pragma unroll
-    for (int i = 0; i < G_TM; ++i)
+    for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-      for (int j = 0; j < G_TN; ++j) {
-        const int n = n0 + wn * G_TN * 16 + j * 16 + c16;
+      for (int j = 0; j < C::TN; ++j) {
+        const int nn = n0 + wn * C::TN * 16 + j * 16 + c16;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int m = m0 + wm * G_TM * 16 + i * 16 + g * 4 + r;
-          part[(int64_t)m * a.Npad + n] = acc[i][j][r];
+          const int mm = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
+          if (mm >= m_rows) continue;
+          if (a.nchunks > 1) {
+            part[(int64_t)mm * a.Npad + nn] = acc[i][j][r];
+          } else if (nn < a.c_out) {  // single chunk: the sum is final
+            if (mm < m_gather) {
+              const int f = mm / a.cseg, c = mm - f * a.cseg;
+              if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + nn] = acc[i][j][r];
+            } else if (mm == a.m_ones) {
+              a.db[nn] = acc[i][j][r];
+            } else if (a.D0) {
+              a.D0[(int64_t)(mm - a.m_ind) * a.c_out + nn] = acc[i][j][r];
+            }
+          }
         }
       }
   }
 }
 
+// dW, db and the ground-row sums D0 from the split-K partials.  A block has G
+// thread groups (G = 16, or fewer when there are fewer chunks) of 256/G threads,
+// one output per thread of a group; group g sums chunks g, g+G, ...; the G group
+// sums are added in a fixed order.
 __global__ void __launch_bounds__(256) k_wgrad_reduce(const float* __restrict__ part, int32_t nchunks, int32_t Mpad,
                                                       int32_t Npad, int32_t A, int32_t cseg, int32_t c_in,
                                                       int32_t c_out, int32_t m_ones, int32_t m_ind, float* dW,
-                                                      float* db, float* D0) {
+                                                      float* db, float* D0, int32_t G) {
+  __shared__ float red[256];
+  const int E = 256 / G;  // outputs per block
   const int m_gather = A * cseg;
-  const int64_t total = (int64_t)Mpad * c_out;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
-    const int m = (int)(t / c_out), n = (int)(t - (int64_t)m * c_out);
-    float s = 0.f;
-    for (int ch = 0; ch < nchunks; ++ch) s += part[((int64_t)ch * Mpad + m) * Npad + n];
-    if (m < m_gather) {
-      const int f = m / cseg, c = m - f * cseg;
-      if (c < c_in) dW[((int64_t)f * c_in + c) * c_out + n] = s;
-    } else if (m == m_ones) {
-      if (db) db[n] = s;
-    } else if (m_ind >= 0 && m >= m_ind && m < m_ind + A) {
-      if (D0) D0[(int64_t)(m - m_ind) * c_out + n] = s;
-    }
+  const int m_rows = m_ind >= 0 ? m_ind + A : m_ones + 1;
+  const int64_t total = (int64_t)m_rows * c_out;
+  const int el = threadIdx.x % E, grp = threadIdx.x / E;
+  const int64_t t = (int64_t)blockIdx.x * E + el;
+  int m = 0, n = 0;
+  float s = 0.f;
+  if (t < total) {
+    m = (int)(t / c_out);
+    n = (int)(t - (int64_t)m * c_out);
+    for (int ch = grp; ch < nchunks; ch += G) s += part[((int64_t)ch * Mpad + m) * Npad + n];
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  if (grp != 0 || t >= total) return;
+  s = 0.f;
+  for (int g = 0; g < G; ++g) s += red[g * E + el];
+  if (m < m_gather) {
+    const int f = m / cseg, c = m - f * cseg;
+    if (c < c_in) dW[((int64_t)f * c_in + c) * c_out + n] = s;
+  } else if (m == m_ones) {
+    if (db) db[n] = s;
+  } else if (m_ind >= 0 && m >= m_ind && m < m_ind + A) {
+    if (D0) D0[(int64_t)(m - m_ind) * c_out + n] = s;
   }
 }
 
@@ -309,35 +507,95 @@ __global__ void __launch_bounds__(256) k_row0_dx(const T* __restrict__ W, const 
 
 static int device_grid_limit() { return 256 * 8; }
 
+template <typename T, class C>
+static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
+  const int64_t span = max_rows - a.row_begin;
+  const int64_t tiles = ((span + C::BM - 1) / C::BM) * (a.Npad / C::BN) * a.ksplit;
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit());
+  hipLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a);
+  if (a.ksplit > 1) {
+    const int64_t total = span * a.out_cols;
+    const int g2 = (int)std::min<int64_t>(std::max<int64_t>((total + 255) / 256, 1), 4096);
+    hipLaunchKernelGGL(k_gemm_splitk_reduce<T>, dim3(g2), dim3(256), 0, st, a);
+  }
+}
+
+template <typename T>
+static void launch_gemm_t(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
+  switch (a.cfg) {
+    case 0: launch_cfg<T, C128x128<T>>(a, max_rows, st); break;
+    case 1: launch_cfg<T, C128x64<T>>(a, max_rows, st); break;
+    case 2: launch_cfg<T, C64x64<T>>(a, max_rows, st); break;
+    default: launch_cfg<T, C32x64<T>>(a, max_rows, st); break;
+  }
+}
+
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st) {
-  int64_t span = max_rows - a.row_begin;
-  if (span <= 0) return hipSuccess;
-  int64_t tiles = ((span + G_BM - 1) / G_BM) * (a.Npad / G_BN);
-  int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit());
+  if (max_rows - a.row_begin <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(k_gemm_gather<__bf16>, dim3(grid), dim3(G_THREADS), 0, st, a);
+    launch_gemm_t<__bf16>(a, max_rows, st);
   else
-    hipLaunchKernelGGL(k_gemm_gather<float>, dim3(grid), dim3(G_THREADS), 0, st, a);
+    launch_gemm_t<float>(a, max_rows, st);
   return hipGetLastError();
 }
 
-hipError_t launch_wgrad(bool bf16, const WGradArgs& a, hipStream_t st) {
-  int64_t tiles = (int64_t)(a.Mpad / G_BM) * (a.Npad / G_BN) * a.nchunks;
-  int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit());
-  if (bf16)
-    hipLaunchKernelGGL(k_wgrad<__bf16>, dim3(grid), dim3(G_THREADS), 0, st, a);
+GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K) {
+  // Tile width: 128 when that pads N no more than 64 does and still gives >= 256
+  // tiles; otherwise 64-wide tiles with the tallest of 128/64/32 rows that gives
+  // >= 256 tiles.  K is split when even 32-row tiles leave the GPU mostly idle.
+  const int BK = bf16 ? 64 : 32;
+  const int64_t n128 = (N + 127) / 128 * 128, n64 = (N + 63) / 64 * 64;
+  auto tiles = [&](int bm, int64_t npad, int bn) { return ((max_rows + bm - 1) / bm) * (npad / bn); };
+  GemmPlan p;
+  if (n128 <= n64 && tiles(128, n128, 128) >= 256)
+    p.cfg = 0;
+  else if (tiles(128, n64, 64) >= 256)
+    p.cfg = 1;
+  else if (tiles(64, n64, 64) >= 256)
+    p.cfg = 2;
   else
-    hipLaunchKernelGGL(k_wgrad<float>, dim3(grid), dim3(G_THREADS), 0, st, a);
+    p.cfg = 3;
+  const GemmTile t = gemm_tile(bf16, p.cfg);
+  p.BN = t.BN;
+  p.Npad = (int)round_up(N, t.BN);
+  p.Kpad = (int)round_up(K, BK);
+  const int64_t tl = tiles(t.BM, p.Npad, t.BN);
+  const int kslabs = p.Kpad / BK;
+  p.ksplit = 1;
+  if (tl < 128 && kslabs >= 4) p.ksplit = (int)std::max<int64_t>(1, std::min<int64_t>(kslabs / 2, (256 + tl - 1) / tl));
+  return p;
+}
+
+hipError_t launch_wgrad(bool bf16, const WGradArgs& a, hipStream_t st) {
+  // a.cfg: 0 = 128 x 128 tiles, 1 = 128 x 64
+  const int BN = a.cfg == 0 ? 128 : 64;
+  const int64_t tiles = (int64_t)(a.Mpad / 128) * (a.Npad / BN) * a.nchunks;
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit());
+  if (bf16) {
+    if (a.cfg == 0)
+      hipLaunchKernelGGL((k_wgrad<__bf16, C128x128<__bf16>>), dim3(grid), dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_wgrad<__bf16, C128x64<__bf16>>), dim3(grid), dim3(256), 0, st, a);
+  } else {
+    if (a.cfg == 0)
+      hipLaunchKernelGGL((k_wgrad<float, C128x128<float>>), dim3(grid), dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_wgrad<float, C128x64<float>>), dim3(grid), dim3(256), 0, st, a);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_wgrad_reduce(const float* part, int32_t nchunks, int32_t Mpad, int32_t Npad, int32_t A, int32_t cseg,
                                int32_t c_in, int32_t c_out, int32_t m_ones, int32_t m_ind, float* dW, float* db,
                                float* D0, hipStream_t st) {
-  int64_t total = (int64_t)Mpad * c_out;
-  int grid = (int)std::min<int64_t>((total + 255) / 256, 2048);
-  hipLaunchKernelGGL(k_wgrad_reduce, dim3(std::max(grid, 1)), dim3(256), 0, st, part, nchunks, Mpad, Npad, A, cseg,
-                     c_in, c_out, m_ones, m_ind, dW, db, D0);
+  if (nchunks <= 1) return hipSuccess;  // the weight-gradient kernel wrote the results
+  const int m_rows = m_ind >= 0 ? m_ind + A : m_ones + 1;
+  const int64_t total = (int64_t)m_rows * c_out;
+  const int G = nchunks >= 16 ? 16 : (nchunks >= 8 ? 8 : (nchunks >= 4 ? 4 : 2));
+  const int E = 256 / G;
+  const int grid = (int)std::max<int64_t>(1, (total + E - 1) / E);
+  hipLaunchKernelGGL(k_wgrad_reduce, dim3(grid), dim3(256), 0, st, part, nchunks, Mpad, Npad, A, cseg, c_in, c_out,
+                     m_ones, m_ind, dW, db, D0, G);
   return hipGetLastError();
 }
 

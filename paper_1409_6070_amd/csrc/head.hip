@@ -37,62 +37,85 @@ __global__ void __launch_bounds__(256) k_gather_dfeats(const T* __restrict__ gra
   }
 }
 
+// All weight packings of a step in one launch: blockIdx.y selects the job.
+//   mode 0 (forward):   Bt[n][f*cp_in + c]  = W[(f*c_in + c)*c_out + n]
+//   mode 1 (backward):  Bt[c][f*cp_out + n] = W[(f*c_in + c)*c_out + n]
 template <typename T>
-__global__ void __launch_bounds__(256) k_pack(int mode, const T* __restrict__ W, int32_t A, int32_t c_in,
-                                              int32_t c_out, int32_t cp_in, int32_t cp_out, T* Bt, int32_t Npad,
-                                              int32_t Kpad) {
-  const int64_t total = (int64_t)Npad * Kpad;
+__global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
+  const PackJob& j = pa.job[blockIdx.y];
+  const T* W = (const T*)j.W;
+  T* Bt = (T*)j.Bt;
+  const int64_t total = (int64_t)j.Npad * j.Kpad;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
-    const int n = (int)(t / Kpad), k = (int)(t - (int64_t)n * Kpad);
+    const int n = (int)(t / j.Kpad), k = (int)(t - (int64_t)n * j.Kpad);
     T v = Elem<T>::from_f32(0.f);
-    if (mode == 0) {  // Bt[n = out channel][k = f*cp_in + c]
-      const int f = k / cp_in, c = k - f * cp_in;
-      if (n < c_out && f < A && c < c_in) v = W[((int64_t)f * c_in + c) * c_out + n];
-    } else {  // Bt[n = in channel c][k = f*cp_out + o]
-      const int f = k / cp_out, o = k - f * cp_out;
-      if (n < c_in && f < A && o < c_out) v = W[((int64_t)f * c_in + n) * c_out + o];
+    if (j.mode == 0) {
+      const int f = k / j.cp_in, c = k - f * j.cp_in;
+      if (n < j.c_out && f < j.A && c < j.c_in) v = W[((int64_t)f * j.c_in + c) * j.c_out + n];
+    } else {
+      const int f = k / j.cp_out, o = k - f * j.cp_out;
+      if (n < j.c_in && f < j.A && o < j.c_out) v = W[((int64_t)f * j.c_in + n) * j.c_out + o];
     }
     Bt[t] = v;
   }
 }
 
+__device__ inline float wave_max(float v) {
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+__device__ inline float wave_sum(float v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
 // One workgroup per sample: softmax over the logits, the sample's loss term and
-// dL/dlogits = (softmax - onehot) / batch.
+// dL/dlogits = (softmax - onehot) / batch.  Up to 4096 logits stay in registers.
 template <typename T>
 __global__ void __launch_bounds__(256) k_softmax_xent(const float* __restrict__ logits,
                                                       const int32_t* __restrict__ labels, int32_t batch,
                                                       int32_t classes, T* dlogits, int32_t dl_stride,
                                                       float* loss_part) {
-  __shared__ float red[256];
-  const int b = blockIdx.x;
+  constexpr int CACHE = 16;
+  __shared__ float red[4];
+  const int b = blockIdx.x, t = threadIdx.x, w = t >> 6;
   const float* z = logits + (int64_t)b * classes;
+  float v[CACHE];
   float mx = -INFINITY;
-  for (int c = threadIdx.x; c < classes; c += blockDim.x) mx = fmaxf(mx, z[c]);
-  red[threadIdx.x] = mx;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (threadIdx.x < off) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + off]);
-    __syncthreads();
+#pragma unroll
+  for (int i = 0; i < CACHE; ++i) {
+    const int c = t + i * 256;
+    v[i] = c < classes ? z[c] : -INFINITY;
+    mx = fmaxf(mx, v[i]);
   }
-  mx = red[0];
+  for (int c = t + CACHE * 256; c < classes; c += 256) mx = fmaxf(mx, z[c]);
+  mx = wave_max(mx);
+  if ((t & 63) == 0) red[w] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   __syncthreads();
   float s = 0.f;
-  for (int c = threadIdx.x; c < classes; c += blockDim.x) s += expf(z[c] - mx);
-  red[threadIdx.x] = s;
+#pragma unroll
+  for (int i = 0; i < CACHE; ++i) {
+    v[i] = (t + i * 256 < classes) ? expf(v[i] - mx) : 0.f;
+    s += v[i];
+  }
+  for (int c = t + CACHE * 256; c < classes; c += 256) s += expf(z[c] - mx);
+  s = wave_sum(s);
+  if ((t & 63) == 0) red[w] = s;
   __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
-    __syncthreads();
-  }
-  const float sum = red[0];
+  const float sum = (red[0] + red[1]) + (red[2] + red[3]);
   const int label = labels[b];
-  const float inv_b = 1.f / (float)batch;
-  for (int c = threadIdx.x; c < dl_stride; c += blockDim.x) {
-    float g = 0.f;
-    if (c < classes) g = (expf(z[c] - mx) / sum - (c == label ? 1.f : 0.f)) * inv_b;
-    dlogits[(int64_t)b * dl_stride + c] = Elem<T>::from_f32(g);
+  const float inv_b = 1.f / (float)batch, inv_s = 1.f / sum;
+  T* dl = dlogits + (int64_t)b * dl_stride;
+#pragma unroll
+  for (int i = 0; i < CACHE; ++i) {
+    const int c = t + i * 256;
+    if (c < dl_stride) dl[c] = Elem<T>::from_f32(c < classes ? (v[i] * inv_s - (c == label ? 1.f : 0.f)) * inv_b : 0.f);
   }
-  if (threadIdx.x == 0) {
+  for (int c = t + CACHE * 256; c < dl_stride; c += 256)
+    dl[c] = Elem<T>::from_f32(c < classes ? (expf(z[c] - mx) * inv_s - (c == label ? 1.f : 0.f)) * inv_b : 0.f);
+  if (t == 0) {
     const bool ok = label >= 0 && label < classes;
     loss_part[b] = ok ? (logf(sum) + mx - z[label]) : 0.f;
   }
@@ -106,25 +129,26 @@ __global__ void k_loss_final(const float* __restrict__ loss_part, int32_t batch,
   }
 }
 
-// grad_top[row(b)] = mask * dh[b] for non-empty samples; grad_top[0] = mask0 * sum of dh over empty samples.
+// grad_top[row(b)] = mask * dh[b] for non-empty samples (blockIdx.y = b < batch);
+// grad_top[0] = mask0 * sum of dh over empty samples (blockIdx.y = batch).
 template <typename T>
 __global__ void __launch_bounds__(256) k_head_scatter(const float* __restrict__ dh, int32_t dh_stride,
                                                       const int32_t* __restrict__ head_rows, int32_t batch,
                                                       const T* __restrict__ Y_top, T* grad_top, int32_t cp) {
-  for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < cp; c += gridDim.x * blockDim.x) {
-    float g0 = 0.f;
-    for (int b = 0; b < batch; ++b) {
-      const int r = head_rows[b];
-      const float g = dh[(int64_t)b * dh_stride + c];
-      if (r == 0) {
-        g0 += g;
-      } else {
-        const bool on = Elem<T>::to_f32(Y_top[(int64_t)r * cp + c]) > 0.f;
-        grad_top[(int64_t)r * cp + c] = on ? Elem<T>::from_f32(g) : Elem<T>::from_f32(0.f);
-      }
-    }
-    grad_top[c] = (Elem<T>::to_f32(Y_top[c]) > 0.f) ? Elem<T>::from_f32(g0) : Elem<T>::from_f32(0.f);
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cp) return;
+  const int b = blockIdx.y;
+  if (b < batch) {
+    const int r = head_rows[b];
+    if (r == 0) return;
+    const bool on = Elem<T>::to_f32(Y_top[(int64_t)r * cp + c]) > 0.f;
+    grad_top[(int64_t)r * cp + c] = on ? Elem<T>::from_f32(dh[(int64_t)b * dh_stride + c]) : Elem<T>::from_f32(0.f);
+    return;
   }
+  float g0 = 0.f;
+  for (int bb = 0; bb < batch; ++bb)
+    if (head_rows[bb] == 0) g0 += dh[(int64_t)bb * dh_stride + c];
+  grad_top[c] = (Elem<T>::to_f32(Y_top[c]) > 0.f) ? Elem<T>::from_f32(g0) : Elem<T>::from_f32(0.f);
 }
 
 __global__ void __launch_bounds__(256) k_fill_zero(uint32_t* p, int64_t words) {
@@ -167,15 +191,15 @@ hipError_t launch_gather_dfeats(bool bf16, const void* grad0, int32_t cp0, const
   return hipGetLastError();
 }
 
-hipError_t launch_pack(bool bf16, int mode, const void* W, int32_t A, int32_t c_in, int32_t c_out, int32_t cp_in,
-                       int32_t cp_out, void* Bt, int32_t Npad, int32_t Kpad, hipStream_t st) {
-  int grid = grid_for((int64_t)Npad * Kpad);
+hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st) {
+  int64_t most = 0;
+  for (int i = 0; i < pa.njobs; ++i) most = std::max<int64_t>(most, (int64_t)pa.job[i].Npad * pa.job[i].Kpad);
+  if (pa.njobs <= 0 || most <= 0) return hipSuccess;
+  const int gx = (int)std::max<int64_t>(1, std::min<int64_t>((most + 255) / 256, 512));
   if (bf16)
-    hipLaunchKernelGGL(k_pack<__bf16>, dim3(grid), dim3(256), 0, st, mode, (const __bf16*)W, A, c_in, c_out, cp_in,
-                       cp_out, (__bf16*)Bt, Npad, Kpad);
+    hipLaunchKernelGGL(k_pack_all<__bf16>, dim3(gx, pa.njobs), dim3(256), 0, st, pa);
   else
-    hipLaunchKernelGGL(k_pack<float>, dim3(grid), dim3(256), 0, st, mode, (const float*)W, A, c_in, c_out, cp_in,
-                       cp_out, (float*)Bt, Npad, Kpad);
+    hipLaunchKernelGGL(k_pack_all<float>, dim3(gx, pa.njobs), dim3(256), 0, st, pa);
   return hipGetLastError();
 }
 
@@ -195,12 +219,12 @@ hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* la
 
 hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
                                int32_t batch, const void* Y_top, void* grad_top, int32_t cp, hipStream_t st) {
-  int grid = (cp + 255) / 256;
+  dim3 grid((cp + 255) / 256, batch + 1);
   if (bf16)
-    hipLaunchKernelGGL(k_head_scatter<__bf16>, dim3(grid), dim3(256), 0, st, dh, dh_stride, head_rows, batch,
+    hipLaunchKernelGGL(k_head_scatter<__bf16>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
                        (const __bf16*)Y_top, (__bf16*)grad_top, cp);
   else
-    hipLaunchKernelGGL(k_head_scatter<float>, dim3(grid), dim3(256), 0, st, dh, dh_stride, head_rows, batch,
+    hipLaunchKernelGGL(k_head_scatter<float>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
                        (const float*)Y_top, (float*)grad_top, cp);
   return hipGetLastError();
 }

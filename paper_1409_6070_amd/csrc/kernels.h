@@ -12,7 +12,18 @@ struct SitesWork {
   int64_t base[MAX_LAYERS + 1];
 };
 
-hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, int32_t max_words, hipStream_t st);
+// Segments of the window-list kernel: kind 0 = R of layer s, 1 = transposes of
+// layer s, 2 = caller-site rows, 3 = head rows; segment i owns workgroups
+// [blk[i], blk[i+1]).
+struct RulesWork {
+  int32_t nseg;
+  int32_t kind[2 * MAX_LAYERS + 2];
+  int32_t layer[2 * MAX_LAYERS + 2];
+  int32_t blk[2 * MAX_LAYERS + 3];
+};
+
+hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const RulesWork& rw, int32_t max_words,
+                           hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // gather GEMM: out[m][n] = epi( sum_k A(m,k) * Bt[n][k] ),
@@ -46,6 +57,19 @@ struct GemmArgs {
   int32_t rows_add;
   int32_t rows_host;
   int32_t row_begin;
+  int32_t cfg;        // tile shape (see plan_gemm)
+  int32_t ksplit;     // > 1: K split over workgroups, fp32 partials in part
+  float* part;        // [ksplit][part_rows][Npad]
+  int32_t part_rows;  // row capacity of part
+};
+
+// Tile shape and padding of one GEMM, chosen on the host from its row bound.
+struct GemmPlan {
+  int cfg = 3;
+  int BN = 64;
+  int Npad = 0;
+  int Kpad = 0;
+  int ksplit = 1;
 };
 
 // weight-gradient GEMM, split over sites:
@@ -70,12 +94,22 @@ struct WGradArgs {
   int32_t rows_host;
   int32_t nchunks;
   float* part;
+  int32_t cfg;  // 0: 128 x 128 tiles, 1: 128 x 64 tiles
+  // with nchunks == 1 the kernel writes the results itself (no partials):
+  float* dW;    // [A*c_in x c_out]
+  float* db;    // [c_out]
+  float* D0;    // [A x c_out] or null
+  int32_t c_in, c_out;
 };
 
 struct GemmTile {
   int BM, BN, BK;
 };
-GemmTile gemm_tile(bool bf16);
+GemmTile gemm_tile(bool bf16, int cfg);
+GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K);
+// weight-gradient tiles: 128 rows of dW, 128 or 64 columns
+constexpr int WG_BM = 128;
+inline int wgrad_bn(int c_out) { return (c_out + 127) / 128 * 128 <= (c_out + 63) / 64 * 64 ? 128 : 64; }
 
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st);
 hipError_t launch_wgrad(bool bf16, const WGradArgs& a, hipStream_t st);
@@ -94,11 +128,15 @@ hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, 
 hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const int32_t* R, void* X_out,
                            int32_t stride_out, uint8_t* argmax, int32_t cp, const int32_t* n_out, int64_t cap_out,
                            hipStream_t st);
-// routes dY back to the rows below and applies the ReLU mask of the convolution below
-hipError_t launch_pool_bwd(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
-                           const int32_t* R, const void* Y_below, void* grad_below, int32_t cp, const int32_t* n_out,
-                           const int32_t* n_in, int64_t cap_in, int64_t cap_out, float* part, int32_t nparts,
-                           hipStream_t st);
+// Routes dY back to the rows >= 1 below, applying the ReLU mask of the convolution
+// below, and writes the per-block partial sums of the ground-row term.
+hipError_t launch_pool_bwd_rows(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
+                                const int32_t* R, const void* Y_below, void* grad_below, int32_t cp,
+                                const int32_t* n_out, const int32_t* n_in, int64_t cap_in, float* part, int32_t nparts,
+                                hipStream_t st);
+// grad_below[0] = mask(Y_below[0]) * (dY[0] + sum of the partials)
+hipError_t launch_pool_row0_final(bool bf16, const void* dY, const float* part, int32_t nparts, const void* Y_below,
+                                  void* grad_below, int32_t cp, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // input, parameters, head
@@ -107,11 +145,19 @@ hipError_t launch_scatter_input(bool bf16, const void* feats, int32_t n, int32_t
                                 int32_t cp0, hipStream_t st);
 hipError_t launch_gather_dfeats(bool bf16, const void* grad0, int32_t cp0, const int32_t* perm, int32_t n,
                                 int32_t c_in, void* dfeats, hipStream_t st);
-// Bt[n][k] = (n < rows_n && k-map valid) ? W[...] : 0, for the two packings
+// One packing of a weight matrix into a GEMM's [N][K] operand (zero padded):
 //   mode 0 (forward):   Bt[n][f*cp_in + c]  = W[(f*c_in + c)*c_out + n]
 //   mode 1 (backward):  Bt[c][f*cp_out + n] = W[(f*c_in + c)*c_out + n]
-hipError_t launch_pack(bool bf16, int mode, const void* W, int32_t A, int32_t c_in, int32_t c_out, int32_t cp_in,
-                       int32_t cp_out, void* Bt, int32_t Npad, int32_t Kpad, hipStream_t st);
+struct PackJob {
+  const void* W;
+  void* Bt;
+  int32_t mode, A, c_in, c_out, cp_in, cp_out, Npad, Kpad;
+};
+struct PackArgs {
+  int32_t njobs;
+  PackJob job[2 * MAX_LAYERS];
+};
+hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st);
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
                                void* dlogits, int32_t dl_stride, float* loss_part, float* loss, hipStream_t st);
 hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,

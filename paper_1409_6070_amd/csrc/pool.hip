@@ -17,41 +17,59 @@
 
 namespace sscn {
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// Packs VE argmax bytes (VE = 8 or 4) into one integer store/load.
+template <int VE>
+struct ArgPack;
+template <>
+struct ArgPack<8> {
+  typedef uint64_t W;
+};
+template <>
+struct ArgPack<4> {
+  typedef uint32_t W;
+};
+
 template <typename T>
 __global__ void __launch_bounds__(256) k_pool_fwd(const T* __restrict__ X_in, int32_t stride_in,
                                                   const int32_t* __restrict__ R, T* X_out, int32_t stride_out,
                                                   uint8_t* argmax, int32_t cp, const int32_t* n_out_p) {
   constexpr int VE = Elem<T>::VE;
+  typedef typename ArgPack<VE>::W AW;
   const int nv = cp / VE;
   const int64_t total = (int64_t)(*n_out_p + 1) * nv;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
     const int64_t o = t / nv;
     const int c = (int)(t - o * nv) * VE;
-    Vec16 in[4];
-#pragma unroll
-    for (int f = 0; f < 4; ++f) in[f] = *(const Vec16*)(X_in + (int64_t)R[o * 4 + f] * stride_in + c);
-    Vec16 out;
+    const i32x4 r = *(const i32x4*)(R + o * 4);
+    u32x4 in[4];
+    in[0] = *(const u32x4*)(X_in + (int64_t)r[0] * stride_in + c);
+    in[1] = *(const u32x4*)(X_in + (int64_t)r[1] * stride_in + c);
+    in[2] = *(const u32x4*)(X_in + (int64_t)r[2] * stride_in + c);
+    in[3] = *(const u32x4*)(X_in + (int64_t)r[3] * stride_in + c);
+    u32x4 out;
     T* ov = (T*)&out;
-    uint8_t am[VE];
+    AW am = 0;
+    // every index below is a compile-time constant, so in[] stays in registers;
+    // the maximum converts back exactly (bf16 and fp32 values are exact in fp32)
 #pragma unroll
     for (int j = 0; j < VE; ++j) {
       float best = Elem<T>::to_f32(((const T*)&in[0])[j]);
-      int arg = 0;
+      AW arg = 0;
 #pragma unroll
       for (int f = 1; f < 4; ++f) {
-        float v = Elem<T>::to_f32(((const T*)&in[f])[j]);
-        if (v > best) {
-          best = v;
-          arg = f;
-        }
+        const float v = Elem<T>::to_f32(((const T*)&in[f])[j]);
+        const bool gt = v > best;
+        best = gt ? v : best;
+        arg = gt ? (AW)f : arg;
       }
-      ov[j] = ((const T*)&in[arg])[j];
-      am[j] = (uint8_t)arg;
+      ov[j] = Elem<T>::from_f32(best);
+      am |= arg << (8 * j);
     }
-    *(Vec16*)(X_out + o * stride_out + c) = out;
-    uint8_t* ap = argmax + o * stride_out + c;
-#pragma unroll
-    for (int j = 0; j < VE; ++j) ap[j] = am[j];
+    *(u32x4*)(X_out + o * stride_out + c) = out;
+    *(AW*)(argmax + o * stride_out + c) = am;
   }
 }
 
@@ -61,58 +79,97 @@ __global__ void __launch_bounds__(256) k_pool_bwd(const T* __restrict__ dY, int3
                                                   const T* __restrict__ Y_below, T* grad_below, int32_t cp,
                                                   const int32_t* n_in_p) {
   constexpr int VE = Elem<T>::VE;
+  typedef typename ArgPack<VE>::W AW;
   const int nv = cp / VE;
   const int64_t total = (int64_t)(*n_in_p) * nv;  // rows 1..n_in
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
     const int64_t i = 1 + t / nv;
     const int c = (int)(t - (i - 1) * nv) * VE;
     const int p = Pt[i];
-    Vec16 y = *(const Vec16*)(Y_below + i * stride + c);
-    Vec16 out = {{0u, 0u, 0u, 0u}};
+    const u32x4 y = *(const u32x4*)(Y_below + i * stride + c);
+    u32x4 out = {0u, 0u, 0u, 0u};
     if (p >= 0) {
       const int64_t o = p >> 2;
       const int f = p & 3;
-      Vec16 g = *(const Vec16*)(dY + o * stride + c);
-      const uint8_t* ap = argmax + o * stride + c;
+      const u32x4 g = *(const u32x4*)(dY + o * stride + c);
+      const AW am = *(const AW*)(argmax + o * stride + c);
 #pragma unroll
       for (int j = 0; j < VE; ++j) {
-        const bool take = (ap[j] == f) && (Elem<T>::to_f32(((const T*)&y)[j]) > 0.f);
+        const bool take = ((int)((am >> (8 * j)) & 0xff) == f) && (Elem<T>::to_f32(((const T*)&y)[j]) > 0.f);
         ((T*)&out)[j] = take ? ((const T*)&g)[j] : Elem<T>::from_f32(0.f);
       }
     }
-    *(Vec16*)(grad_below + i * stride + c) = out;
+    *(u32x4*)(grad_below + i * stride + c) = out;
   }
 }
 
-// Pass 1: block b sums, per channel, dY[o][c] over its rows o >= 1 whose max came from row 0.
+// Ground-row reduction, pass 1.  Block b takes a contiguous range of output
+// rows o >= 1; thread t owns channel vector t % nv and every (256/nv)-th row of
+// the range, summing dY[o][c] where the max of (o, c) was read from row 0.
+// The row lanes are then combined in LDS in a fixed order: deterministic.
 template <typename T>
 __global__ void __launch_bounds__(256) k_pool_row0_part(const T* __restrict__ dY, int32_t stride,
                                                         const uint8_t* __restrict__ argmax,
                                                         const int32_t* __restrict__ R, int32_t cp,
                                                         const int32_t* n_out_p, float* part) {
+  constexpr int VE = Elem<T>::VE;
+  typedef typename ArgPack<VE>::W AW;
+  __shared__ float red[256 * VE];
+  const int nv = cp / VE;
+  const int lanes = 256 / nv;  // row lanes (nv <= 256)
+  const int t = threadIdx.x;
+  const int v = t % nv, rl = t / nv;
   const int n_out = *n_out_p;
   const int per = (n_out + gridDim.x - 1) / gridDim.x;
   const int o_beg = 1 + blockIdx.x * per;
   const int o_end = min(n_out + 1, o_beg + per);
-  for (int c = threadIdx.x; c < cp; c += blockDim.x) {
-    float s = 0.f;
-    for (int o = o_beg; o < o_end; ++o) {
-      const int f = argmax[(int64_t)o * stride + c];
-      if (R[(int64_t)o * 4 + f] == 0) s += Elem<T>::to_f32(dY[(int64_t)o * stride + c]);
+  float acc[VE];
+#pragma unroll
+  for (int j = 0; j < VE; ++j) acc[j] = 0.f;
+  if (rl < lanes) {
+    for (int o = o_beg + rl; o < o_end; o += lanes) {
+      const i32x4 r = *(const i32x4*)(R + (int64_t)o * 4);
+      const AW am = *(const AW*)(argmax + (int64_t)o * stride + v * VE);
+      const u32x4 g = *(const u32x4*)(dY + (int64_t)o * stride + v * VE);
+#pragma unroll
+      for (int j = 0; j < VE; ++j) {
+        const int f = (int)((am >> (8 * j)) & 3);
+        const int rf = f == 0 ? r.x : (f == 1 ? r.y : (f == 2 ? r.z : r.w));
+        if (rf == 0) acc[j] += Elem<T>::to_f32(((const T*)&g)[j]);
+      }
     }
-    part[(int64_t)blockIdx.x * cp + c] = s;
+  }
+#pragma unroll
+  for (int j = 0; j < VE; ++j) red[t * VE + j] = acc[j];
+  __syncthreads();
+  for (int e = t; e < cp; e += 256) {  // channel e = vector e / VE, element e % VE
+    const int vv = e / VE, jj = e - vv * VE;
+    float s = 0.f;
+    for (int l = 0; l < lanes; ++l) s += red[(l * nv + vv) * VE + jj];
+    part[(int64_t)blockIdx.x * cp + e] = s;
   }
 }
 
-// Pass 2: grad_below[0][c] = mask(Y_below[0][c]) * (dY[0][c] + sum of pass-1 partials).
+// Pass 2: a block covers 16 channels with 16 groups of 16 threads; group g sums
+// partials g, g+16, ...; the 16 group sums are added in a fixed order.
+// grad_below[0][c] = mask(Y_below[0][c]) * (dY[0][c] + sum of partials).
 template <typename T>
 __global__ void __launch_bounds__(256) k_pool_row0_final(const T* __restrict__ dY, const float* __restrict__ part,
                                                          int32_t nparts, const T* __restrict__ Y_below,
                                                          T* grad_below, int32_t cp) {
-  for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < cp; c += gridDim.x * blockDim.x) {
-    float s = Elem<T>::to_f32(dY[c]);
-    for (int p = 0; p < nparts; ++p) s += part[(int64_t)p * cp + c];
-    grad_below[c] = (Elem<T>::to_f32(Y_below[c]) > 0.f) ? Elem<T>::from_f32(s) : Elem<T>::from_f32(0.f);
+  __shared__ float red[16][16];
+  const int cl = threadIdx.x & 15, grp = threadIdx.x >> 4;
+  const int c = blockIdx.x * 16 + cl;
+  float s = 0.f;
+  if (c < cp)
+    for (int p = grp; p < nparts; p += 16) s += part[(int64_t)p * cp + c];
+  red[grp][cl] = s;
+  __syncthreads();
+  if (grp == 0 && c < cp) {
+    float tot = 0.f;
+    for (int g = 0; g < 16; ++g) tot += red[g][cl];
+    tot += Elem<T>::to_f32(dY[c]);
+    grad_below[c] = (Elem<T>::to_f32(Y_below[c]) > 0.f) ? Elem<T>::from_f32(tot) : Elem<T>::from_f32(0.f);
   }
 }
 
@@ -132,10 +189,10 @@ hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const
   return hipGetLastError();
 }
 
-hipError_t launch_pool_bwd(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
-                           const int32_t* R, const void* Y_below, void* grad_below, int32_t cp, const int32_t* n_out,
-                           const int32_t* n_in, int64_t cap_in, int64_t cap_out, float* part, int32_t nparts,
-                           hipStream_t st) {
+hipError_t launch_pool_bwd_rows(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
+                                const int32_t* R, const void* Y_below, void* grad_below, int32_t cp,
+                                const int32_t* n_out, const int32_t* n_in, int64_t cap_in, float* part, int32_t nparts,
+                                hipStream_t st) {
   const int VE = bf16 ? 8 : 4;
   int grid = grid_for(cap_in * (cp / VE));
   if (bf16) {
@@ -143,17 +200,23 @@ hipError_t launch_pool_bwd(bool bf16, const void* dY, int32_t stride, const uint
                        (const __bf16*)Y_below, (__bf16*)grad_below, cp, n_in);
     hipLaunchKernelGGL(k_pool_row0_part<__bf16>, dim3(nparts), dim3(256), 0, st, (const __bf16*)dY, stride, argmax, R,
                        cp, n_out, part);
-    hipLaunchKernelGGL(k_pool_row0_final<__bf16>, dim3((cp + 255) / 256), dim3(256), 0, st, (const __bf16*)dY, part,
-                       nparts, (const __bf16*)Y_below, (__bf16*)grad_below, cp);
   } else {
     hipLaunchKernelGGL(k_pool_bwd<float>, dim3(grid), dim3(256), 0, st, (const float*)dY, stride, argmax, Pt,
                        (const float*)Y_below, (float*)grad_below, cp, n_in);
     hipLaunchKernelGGL(k_pool_row0_part<float>, dim3(nparts), dim3(256), 0, st, (const float*)dY, stride, argmax, R, cp,
                        n_out, part);
-    hipLaunchKernelGGL(k_pool_row0_final<float>, dim3((cp + 255) / 256), dim3(256), 0, st, (const float*)dY, part,
-                       nparts, (const float*)Y_below, (float*)grad_below, cp);
   }
-  (void)cap_out;
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_row0_final(bool bf16, const void* dY, const float* part, int32_t nparts, const void* Y_below,
+                                  void* grad_below, int32_t cp, hipStream_t st) {
+  if (bf16)
+    hipLaunchKernelGGL(k_pool_row0_final<__bf16>, dim3((cp + 15) / 16), dim3(256), 0, st, (const __bf16*)dY, part,
+                       nparts, (const __bf16*)Y_below, (__bf16*)grad_below, cp);
+  else
+    hipLaunchKernelGGL(k_pool_row0_final<float>, dim3((cp + 15) / 16), dim3(256), 0, st, (const float*)dY, part,
+                       nparts, (const float*)Y_below, (float*)grad_below, cp);
   return hipGetLastError();
 }
 

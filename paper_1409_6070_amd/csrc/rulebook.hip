@@ -160,16 +160,33 @@ __global__ void __launch_bounds__(RB_THREADS) k_rb_bitmaps(RulebookArgs a, int32
   }
 }
 
-// Sample offsets and layer totals (one thread per layer, samples in order).
-__global__ void k_rb_offsets(RulebookArgs a) {
-  int s = threadIdx.x;
-  if (s >= a.nlayers) return;
-  int acc = 0;
-  for (int b = 0; b < a.batch; ++b) {
-    a.L[s].soff[b] = acc;
-    acc += a.L[s].scount[b];
+// Sample offsets and layer totals: one workgroup per layer, a block-wide
+// exclusive scan of the per-sample counts.
+__global__ void __launch_bounds__(RB_THREADS) k_rb_offsets(RulebookArgs a) {
+  __shared__ int scratch[RB_THREADS];
+  const int s = blockIdx.x;
+  const int t = threadIdx.x;
+  const LayerBits& L = a.L[s];
+  const int per = (a.batch + RB_THREADS - 1) / RB_THREADS;
+  const int beg = t * per;
+  int local = 0;
+  for (int j = 0; j < per; ++j)
+    if (beg + j < a.batch) local += L.scount[beg + j];
+  scratch[t] = local;
+  __syncthreads();
+  for (int off = 1; off < RB_THREADS; off <<= 1) {
+    const int v = (t >= off) ? scratch[t - off] : 0;
+    __syncthreads();
+    scratch[t] += v;
+    __syncthreads();
   }
-  a.counts[s] = acc;
+  int run = scratch[t] - local;
+  for (int j = 0; j < per; ++j)
+    if (beg + j < a.batch) {
+      L.soff[beg + j] = run;
+      run += L.scount[beg + j];
+    }
+  if (t == RB_THREADS - 1) a.counts[s] = scratch[RB_THREADS - 1];
 }
 
 // Site keys of every layer, in row order: one thread per bitmap word.
@@ -206,91 +223,91 @@ __device__ inline int32_t rank_row(const LayerBits& L, int b, int y, int x) {
 }
 
 // Window lists (rules), their transposes, the caller-site -> row map and the
-// head rows.  Segments run one after another; each is grid-strided over its
-// device-side count.
-__global__ void __launch_bounds__(256) k_rb_rules(RulebookArgs a) {
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int s = 1; s < a.nlayers; ++s) {
+// head rows.  Each list is a segment with its own range of workgroups
+// (RulesWork), grid-strided over its device-side count.
+__global__ void __launch_bounds__(256) k_rb_rules(RulebookArgs a, RulesWork rw) {
+  int seg = 0;
+  while (seg + 1 < rw.nseg && (int)blockIdx.x >= rw.blk[seg + 1]) ++seg;
+  const int kind = rw.kind[seg], s = rw.layer[seg];
+  const int nblk = rw.blk[seg + 1] - rw.blk[seg];
+  const int64_t tid = (int64_t)((int)blockIdx.x - rw.blk[seg]) * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)nblk * blockDim.x;
+  if (kind == 0 || kind == 1) {
     const LayerBits& Lo = a.L[s];
     const LayerBits& Li = a.L[s - 1];
     const int F = a.F[s];
     const int A = F * F;
-    const int step = (a.kind[s] == 1) ? 1 : 2;
-    const int n_out = a.counts[s];
-    const int n_in = a.counts[s - 1];
-    int32_t* R = a.rules[s];
-    for (int64_t o = tid; o <= n_out; o += stride) {
-      if (o == 0) {
-        for (int f = 0; f < A; ++f) R[f] = 0;
-        continue;
-      }
-      int key = Lo.sites[o - 1];
-      int X = key % Lo.S;
-      int tq = key / Lo.S;
-      int Y = tq % Lo.S;
-      int b = tq / Lo.S;
-      for (int dy = 0; dy < F; ++dy)
-        for (int dx = 0; dx < F; ++dx)
-          R[o * A + dy * F + dx] = rank_row(Li, b, step * Y + dy, step * X + dx);
-    }
-    int32_t* Rt = a.rules_t[s];
-    if (a.kind[s] == 1) {
-      for (int64_t i = tid; i <= n_in; i += stride) {
-        if (i == 0) {
-          for (int f = 0; f < A; ++f) Rt[f] = -1;
+    if (kind == 0) {  // R_s: the window of every row of layer s
+      const int step = (a.kind[s] == 1) ? 1 : 2;
+      const int n_out = a.counts[s];
+      int32_t* R = a.rules[s];
+      for (int64_t o = tid; o <= n_out; o += stride) {
+        if (o == 0) {
+          for (int f = 0; f < A; ++f) R[f] = 0;
           continue;
         }
-        int key = Li.sites[i - 1];
-        int x = key % Li.S;
-        int tq = key / Li.S;
-        int y = tq % Li.S;
-        int b = tq / Li.S;
+        const int key = Lo.sites[o - 1];
+        const int X = key % Lo.S;
+        const int tq = key / Lo.S;
+        const int Y = tq % Lo.S;
+        const int b = tq / Lo.S;
         for (int dy = 0; dy < F; ++dy)
-          for (int dx = 0; dx < F; ++dx) {
-            int Y = y - dy, X = x - dx;
-            int r = -1;
-            if (Y >= 0 && X >= 0 && Y < Lo.S && X < Lo.S) r = rank_row(Lo, b, Y, X);
-            Rt[i * A + dy * F + dx] = r;
-          }
+          for (int dx = 0; dx < F; ++dx) R[o * A + dy * F + dx] = rank_row(Li, b, step * Y + dy, step * X + dx);
       }
-    } else {
+    } else {  // transposes: for every row of layer s-1, the rows of layer s whose window holds it
+      const int n_in = a.counts[s - 1];
+      int32_t* Rt = a.rules_t[s];
       for (int64_t i = tid; i <= n_in; i += stride) {
-        if (i == 0) {
-          Rt[0] = -1;
-          continue;
+        if (a.kind[s] == 1) {
+          if (i == 0) {
+            for (int f = 0; f < A; ++f) Rt[f] = -1;
+            continue;
+          }
+          const int key = Li.sites[i - 1];
+          const int x = key % Li.S;
+          const int tq = key / Li.S;
+          const int y = tq % Li.S;
+          const int b = tq / Li.S;
+          for (int dy = 0; dy < F; ++dy)
+            for (int dx = 0; dx < F; ++dx) {
+              const int Y = y - dy, X = x - dx;
+              int r = -1;
+              if (Y >= 0 && X >= 0 && Y < Lo.S && X < Lo.S) r = rank_row(Lo, b, Y, X);
+              Rt[i * A + dy * F + dx] = r;
+            }
+        } else {
+          if (i == 0) {
+            Rt[0] = -1;
+            continue;
+          }
+          const int key = Li.sites[i - 1];
+          const int x = key % Li.S;
+          const int tq = key / Li.S;
+          const int y = tq % Li.S;
+          const int b = tq / Li.S;
+          const int Y = y >> 1, X = x >> 1;
+          int r = -1;
+          if (Y < Lo.S && X < Lo.S) r = rank_row(Lo, b, Y, X) * 4 + (y & 1) * 2 + (x & 1);
+          Rt[i] = r;
         }
-        int key = Li.sites[i - 1];
-        int x = key % Li.S;
-        int tq = key / Li.S;
-        int y = tq % Li.S;
-        int b = tq / Li.S;
-        int Y = y >> 1, X = x >> 1;
-        int r = -1;
-        if (Y < Lo.S && X < Lo.S) {
-          int p = rank_row(Lo, b, Y, X);
-          r = p * 4 + (y & 1) * 2 + (x & 1);
-        }
-        Rt[i] = r;
       }
     }
-  }
-  {  // caller site -> input row
+  } else if (kind == 2) {  // caller site -> input row
     const LayerBits& L0 = a.L[0];
     for (int64_t i = tid; i < a.n; i += stride) {
-      int b = a.coords[3 * i], y = a.coords[3 * i + 1], x = a.coords[3 * i + 2];
+      const int b = a.coords[3 * i], y = a.coords[3 * i + 1], x = a.coords[3 * i + 2];
       int r = -1;
       if (b >= 0 && b < a.batch && y >= 0 && y < L0.S && x >= 0 && x < L0.S) r = rank_row(L0, b, y, x);
       a.perm[i] = r;
     }
-  }
-  {  // each sample's single top-layer site (row 0 when the sample is empty)
+  } else {  // each sample's single top-layer site (row 0 when the sample is empty)
     const LayerBits& Lt = a.L[a.nlayers - 1];
     for (int64_t b = tid; b < a.batch; b += stride) a.head_rows[b] = rank_row(Lt, (int)b, 0, 0);
   }
 }
 
-hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, int32_t max_words, hipStream_t st) {
+hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const RulesWork& rw, int32_t max_words,
+                           hipStream_t st) {
   const LayerBits& L0 = a.L[0];
   int64_t nw0 = (int64_t)a.batch * L0.S * L0.Wd;
   int g = (int)std::min<int64_t>((nw0 + 255) / 256, 1024);
@@ -303,11 +320,11 @@ hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, int32_t m
     size_t lds = (size_t)2 * max_words * sizeof(uint64_t) + RB_THREADS * sizeof(int);
     hipLaunchKernelGGL(k_rb_bitmaps, dim3(a.batch), dim3(RB_THREADS), lds, st, a, max_words);
   }
-  hipLaunchKernelGGL(k_rb_offsets, dim3(1), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(RB_THREADS), 0, st, a);
   int gs = (int)std::min<int64_t>((wk.total + 255) / 256, 2048);
   if (gs < 1) gs = 1;
   hipLaunchKernelGGL(k_rb_sites, dim3(gs), dim3(256), 0, st, a, wk);
-  hipLaunchKernelGGL(k_rb_rules, dim3(1024), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(k_rb_rules, dim3(rw.blk[rw.nseg]), dim3(256), 0, st, a, rw);
   return hipGetLastError();
 }
 
