@@ -7,7 +7,7 @@
 #include <new>
 #include <vector>
 
-#include "../../include/sscn.h"
+#include "sscn.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -216,10 +216,12 @@ static void set_plan(GemmArgs& g, const GemmPlan& p, int64_t rows_cap, float* gp
   g.part_rows = (int32_t)rows_cap;
 }
 
-static int wgrad_chunks(int64_t rows_cap, int tiles_mn, int BK) {
-  // about 1024 workgroups (at most 512 chunks), each summing at least 4 slabs of sites:
-  // the kernel is latency-bound, so workgroups in flight matter more than partial-sum bytes
+// Site chunks of a split-K weight gradient: about 1024 workgroups, at least 4
+// slabs of sites each, and partial sums (chunks x |dW| fp32) of at most twice the
+// bytes the kernel reads (rows x row_bytes).
+static int wgrad_chunks(int64_t rows_cap, int tiles_mn, int BK, int64_t row_bytes, int64_t part_bytes) {
   int64_t max_chunks = std::max<int64_t>(1, std::min<int64_t>(512, (rows_cap + 4 * BK - 1) / (4 * BK)));
+  max_chunks = std::min<int64_t>(max_chunks, std::max<int64_t>(1, 2 * rows_cap * row_bytes / std::max<int64_t>(part_bytes, 1)));
   int64_t want = std::max<int64_t>(1, (1024 + tiles_mn - 1) / tiles_mn);
   return (int)std::min<int64_t>(want, max_chunks);
 }
@@ -259,7 +261,7 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   net->VE = 16 / net->esz;
   net->nlayers = 2 * d.ell + 2;
   net->nparams = d.ell + 2;
-  net->pool_parts = 128;  // most row blocks of a ground-row reduction
+  net->pool_parts = 512;  // most row blocks of a ground-row reduction
   const int BK = net->bf16 ? 64 : 32;
   const int VE = net->VE;
   auto cp = [VE](int c) { return (int)round_up(c, VE); };
@@ -330,7 +332,12 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.Mpad_w = (int)round_up(P.m_ind + P.A, WG_BM);
     P.bn_w = wgrad_bn(P.c_out);
     P.Npad_w = (int)round_up(P.c_out, P.bn_w);
-    P.nchunks = wgrad_chunks(L[s].cap + 1, (P.Mpad_w / WG_BM) * (P.Npad_w / P.bn_w), BK);
+    {
+      const int m_rows = P.m_ind + P.A;
+      const int64_t row_bytes = (int64_t)(P.A * P.cp_in + P.cp_out) * net->esz;
+      const int64_t part_bytes = (int64_t)m_rows * P.Npad_w * 4;
+      P.nchunks = wgrad_chunks(L[s].cap + 1, (P.Mpad_w / WG_BM) * (P.Npad_w / P.bn_w), BK, row_bytes, part_bytes);
+    }
   }
   {
     ParamPlan& P = net->P[d.ell + 1];
@@ -495,7 +502,7 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st, hipStream
   const bool split = side != st;
   hipError_t e;
   if (L.kind == 2) {
-    const int nparts = (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (L.cap + 255) / 256));
+    const int nparts = (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (L.cap + 63) / 64));
     if ((e = timed(net, SSCN_KC_POOL_BWD, st, [&] {
            return launch_pool_bwd_rows(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, L.rules, Lb.X, Lb.grad, L.Cp,
                                        net->counts + s, net->counts + s - 1, Lb.cap, net->ppart, nparts, st);

@@ -101,10 +101,18 @@ __device__ inline void mma_slab(const T* As, const T* Bs, f32x4 (&acc)[C::TM][C:
 }
 
 template <typename T>
-__device__ inline float epi_value(const GemmArgs& a, float v, int n) {
-  if (a.bias && n < a.N) v += a.bias[n];
+__device__ inline float epi_value(const GemmArgs& a, float v, float bias) {
+  v += bias;
   if (a.epi == EPI_BIAS_RELU) v = fmaxf(v, 0.f);
   return v;
+}
+
+// q = k / d for 0 <= k < 2^20, 1 <= d < 2^16: float estimate, then exact correction.
+__device__ inline int div_small(int k, int d, float rcp) {
+  int q = (int)((float)k * rcp);
+  q += (q + 1) * d <= k ? 1 : 0;
+  q -= q * d > k ? 1 : 0;
+  return q;
 }
 
 template <typename T>
@@ -156,11 +164,17 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
     const int kbeg = ks * kper;
     const int kend = min(a.Kpad, kbeg + kper);
 
-    for (int i = tid; i < BM * A; i += NT) {
-      const int r = i / A, f = i - r * A, m = m0 + r;
-      int v = -1;
-      if (m < rows) v = a.rmap ? a.rmap[(int64_t)m * A + f] : (f == 0 ? m : -1);
-      Rs[i] = v;
+    if (tid < BM) {  // the tile's window rows: one row per thread, independent loads
+      const int m = m0 + tid;
+      const int32_t* rp = a.rmap ? a.rmap + (int64_t)m * A : nullptr;
+#pragma unroll
+      for (int f = 0; f < AMAX; ++f) {
+        if (f < A) {
+          int v = -1;
+          if (m < rows) v = rp ? rp[f] : (f == 0 ? m : -1);
+          Rs[tid * A + f] = v;
+        }
+      }
     }
     __syncthreads();
 
@@ -171,19 +185,23 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
       for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     u32x4 ra[C::AV], rb[C::BV];
+    const float rcp_cseg = 1.f / (float)a.cseg;
     auto load = [&](int k0) {
+      int srow[C::AV], col[C::AV];
 #pragma unroll
-      for (int j = 0; j < C::AV; ++j) {
+      for (int j = 0; j < C::AV; ++j) {  // window row and channel of each vector, then all loads at once
         const int v = tid + j * NT;
         const int r = v / KV, kv = v - r * KV;
         const int k = k0 + kv * VE;
-        u32x4 val = {0u, 0u, 0u, 0u};
-        if (k < a.K) {
-          const int f = k / a.cseg, c = k - f * a.cseg;
-          const int srow = Rs[r * A + f];
-          if (srow >= 0) val = *(const u32x4*)(src + (int64_t)srow * a.src_stride + c);
-        }
-        ra[j] = val;
+        const bool in_k = k < a.K;
+        const int f = in_k ? div_small(k, a.cseg, rcp_cseg) : 0;
+        srow[j] = in_k ? Rs[r * A + f] : -1;
+        col[j] = in_k ? k - f * a.cseg : 0;
+      }
+#pragma unroll
+      for (int j = 0; j < C::AV; ++j) {
+        const u32x4 val = *(const u32x4*)(src + (int64_t)max(srow[j], 0) * a.src_stride + col[j]);
+        ra[j] = srow[j] >= 0 ? val : u32x4{0u, 0u, 0u, 0u};
       }
 #pragma unroll
       for (int j = 0; j < C::BV; ++j) {
@@ -213,6 +231,12 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
     }
 
     const int g = lane >> 4, c16 = lane & 15;
+    float bias[C::TN];
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int n = n0 + wn * C::TN * 16 + j * 16 + c16;
+      bias[j] = (a.bias && n < a.N) ? a.bias[n] : 0.f;
+    }
     if (a.ksplit > 1) {
       float* part = a.part + (int64_t)ks * a.part_rows * a.Npad;
 #pragma unroll
@@ -236,7 +260,7 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int ml = wm * C::TM * 16 + i * 16 + g * 4 + r;
-            Cs[ml * CS + nl] = Elem<T>::from_f32(epi_value<T>(a, acc[i][j][r], n0 + nl));
+            Cs[ml * CS + nl] = Elem<T>::from_f32(epi_value<T>(a, acc[i][j][r], bias[j]));
           }
         }
       __syncthreads();
@@ -256,7 +280,7 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int m = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
-            if (m < rows) store_out<T>(a, m, n, epi_value<T>(a, acc[i][j][r], n));
+            if (m < rows) store_out<T>(a, m, n, epi_value<T>(a, acc[i][j][r], bias[j]));
           }
         }
     }
@@ -276,7 +300,7 @@ __global__ void __launch_bounds__(256) k_gemm_splitk_reduce(GemmArgs a) {
     const int n = (int)(t % a.out_cols);
     float s = 0.f;
     for (int ks = 0; ks < a.ksplit; ++ks) s += a.part[((int64_t)ks * a.part_rows + m) * a.Npad + n];
-    store_out<T>(a, m, n, epi_value<T>(a, s, n));
+    store_out<T>(a, m, n, epi_value<T>(a, s, (a.bias && n < a.N) ? a.bias[n] : 0.f));
   }
 }
 
