@@ -154,7 +154,12 @@ SSCN_API sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* con
 
 /* Runs only stage s (1 .. 2*ell+1) of the forward or backward pass on the
  * current workspace contents, with the parameters of the last sscn_forward /
- * sscn_backward.  For checking one kernel group against known inputs. */
+ * sscn_backward.  For checking one kernel group against known inputs.  A
+ * backward convolution stage takes its output gradient (all rows) as it
+ * stands and writes its parameter gradients and the whole gradient below; a
+ * backward pooling stage writes the whole gradient below (and, as a side
+ * effect, the bias gradient of the convolution below it and row 0 of that
+ * convolution's input gradient). */
 SSCN_API sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream);
 SSCN_API sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream);
 
@@ -164,11 +169,14 @@ typedef enum {
   SSCN_KC_GATHER_GEMM = 1,/* implicit-gather MFMA GEMM: conv forward, conv input
                              gradient, softmax layer forward and dh          */
   SSCN_KC_WGRAD = 2,      /* split-K MFMA weight gradient                      */
-  SSCN_KC_WGRAD_REDUCE = 3,/* partial sums -> dW, db, ground-row sums; row-0 dX */
+  SSCN_KC_WGRAD_REDUCE = 3,/* split-K partial sums -> dW (and the softmax db)  */
   SSCN_KC_POOL_FWD = 4,
-  SSCN_KC_POOL_BWD = 5,   /* routing gather + ground-row reduction            */
+  SSCN_KC_POOL_BWD = 5,   /* routing through the windows, with the ground-row,
+                             bias and ground-window sums of the conv below    */
   SSCN_KC_HEAD = 6,       /* input scatter, weight packing, softmax, loss, scatter of dh */
-  SSCN_KC_COUNT = 7
+  SSCN_KC_GROUND = 7,     /* bias and ground-window sums of a conv not under a
+                             pooling layer; ground-row input gradient        */
+  SSCN_KC_COUNT = 8
 } sscn_kernel_class;
 
 /* While enabled, every launch of a kernel whose class bit (1 << class) is set

@@ -38,7 +38,7 @@ struct ParamPlan {
   GemmPlan pf, pd;                    // forward (logits) and input-gradient (dh) GEMMs
   int64_t rows_f, rows_d;             // their row bounds
   int NpadF, KpadF, NpadD, KpadD;
-  int Mpad_w, Npad_w, bn_w, nchunks, m_ones, m_ind;
+  int Mpad_w, Npad_w, bn_w, nchunks, m_ones;
   void* WpF;
   void* WpD;
 };
@@ -102,34 +102,36 @@ struct sscn_net {
     hipEvent_t a, b;
   };
   std::vector<Rec> recs;
-  // second stream of the backward pass: weight gradients run beside the
-  // input-gradient chain; ev_fork[s] / ev_join[s] order the two per stage
-  hipStream_t side = nullptr;
+  // Backward streams beside the caller's: `side` runs the weight gradients,
+  // `side2` the row-0 chain (bias and ground-row sums, row 0 of each input
+  // gradient).  ev_fork[s]: delta of layer s complete in rows >= 1 (caller's
+  // stream); ev_full[s]: delta complete with row 0 (side2); ev_join[0..1]: the
+  // two side streams done, joined at the end of the backward pass.
+  hipStream_t side = nullptr, side2 = nullptr;
   hipEvent_t ev_fork[MAX_LAYERS + 1] = {};
-  hipEvent_t ev_join[MAX_LAYERS + 1] = {};
+  hipEvent_t ev_full[MAX_LAYERS + 1] = {};
+  hipEvent_t ev_join[2] = {};
   ~sscn_net() {
     for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
     for (int i = 0; i <= MAX_LAYERS; ++i) {
       if (ev_fork[i]) (void)hipEventDestroy(ev_fork[i]);
-      if (ev_join[i]) (void)hipEventDestroy(ev_join[i]);
+      if (ev_full[i]) (void)hipEventDestroy(ev_full[i]);
     }
+    for (hipEvent_t e : ev_join)
+      if (e) (void)hipEventDestroy(e);
     if (side) (void)hipStreamDestroy(side);
+    if (side2) (void)hipStreamDestroy(side2);
   }
 };
 
 static bool ensure_side_stream(sscn_net* net) {
-  if (net->side) return true;
-  hipStream_t s = nullptr;
-  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return false;
-  for (int i = 0; i <= MAX_LAYERS; ++i) {
-    if (hipEventCreateWithFlags(&net->ev_fork[i], hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&net->ev_join[i], hipEventDisableTiming) != hipSuccess) {
-      (void)hipStreamDestroy(s);
-      return false;
-    }
-  }
-  net->side = s;
-  return true;
+  if (net->side2) return true;
+  auto ev = [](hipEvent_t* e) { return *e || hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess; };
+  for (int i = 0; i <= MAX_LAYERS; ++i)
+    if (!ev(&net->ev_fork[i]) || !ev(&net->ev_full[i])) return false;
+  if (!ev(&net->ev_join[0]) || !ev(&net->ev_join[1])) return false;
+  if (!net->side && hipStreamCreateWithFlags(&net->side, hipStreamNonBlocking) != hipSuccess) return false;
+  return hipStreamCreateWithFlags(&net->side2, hipStreamNonBlocking) == hipSuccess;
 }
 
 static constexpr size_t MAX_TIMED = 65536;
@@ -205,7 +207,7 @@ static void carve(sscn_net* net, void* base) {
   net->wpart = (float*)cv.take(max_part * 4);
   net->gpart = (float*)cv.take(std::max<size_t>(max_gpart, 1) * 4);
   net->D0 = (float*)cv.take(max_d0 * 4);
-  net->ppart = (float*)cv.take((size_t)net->pool_parts * max_cp * 4);
+  net->ppart = (float*)cv.take((size_t)net->pool_parts * (2 + 9) * max_cp * 4);
   net->ws_bytes = cv.off + 256;
 }
 
@@ -261,7 +263,7 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   net->VE = 16 / net->esz;
   net->nlayers = 2 * d.ell + 2;
   net->nparams = d.ell + 2;
-  net->pool_parts = 512;  // most row blocks of a ground-row reduction
+  net->pool_parts = 1024;  // most row blocks per slot of a bias / ground-row reduction
   const int BK = net->bf16 ? 64 : 32;
   const int VE = net->VE;
   auto cp = [VE](int c) { return (int)round_up(c, VE); };
@@ -284,6 +286,12 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
       l.C = ((s + 1) / 2) * d.k;
       l.conv_index = ci++;
     } else {
+      // with N = 3 * 2^ell every pooling input side is even, so each site below
+      // lies in exactly one window (the pooling backward relies on it)
+      if (S % 2 != 0) {
+        delete net;
+        return SSCN_ERR_INVALID_ARGUMENT;
+      }
       l.kind = 2;
       l.F = 2;
       l.S = S / 2;
@@ -327,13 +335,12 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.KpadF = P.pf.Kpad;
     P.NpadD = P.pd.Npad;
     P.KpadD = P.pd.Kpad;
-    P.m_ones = P.A * P.cp_in;
-    P.m_ind = P.m_ones + 1;
-    P.Mpad_w = (int)round_up(P.m_ind + P.A, WG_BM);
+    P.m_ones = -1;  // db comes from the bias / ground-row sums
+    P.Mpad_w = (int)round_up(P.A * P.cp_in, WG_BM);
     P.bn_w = wgrad_bn(P.c_out);
     P.Npad_w = (int)round_up(P.c_out, P.bn_w);
     {
-      const int m_rows = P.m_ind + P.A;
+      const int m_rows = P.A * P.cp_in;
       const int64_t row_bytes = (int64_t)(P.A * P.cp_in + P.cp_out) * net->esz;
       const int64_t part_bytes = (int64_t)m_rows * P.Npad_w * 4;
       P.nchunks = wgrad_chunks(L[s].cap + 1, (P.Mpad_w / WG_BM) * (P.Npad_w / P.bn_w), BK, row_bytes, part_bytes);
@@ -356,7 +363,6 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.NpadD = P.pd.Npad;
     P.KpadD = P.pd.Kpad;
     P.m_ones = P.cp_in;
-    P.m_ind = -1;
     P.Mpad_w = (int)round_up(P.m_ones + 1, WG_BM);
     P.bn_w = wgrad_bn(P.c_out);
     P.Npad_w = (int)round_up(P.c_out, P.bn_w);
@@ -492,34 +498,66 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
   });
 }
 
-// Backward of stage s.  With side != st the weight gradient (and the ground-row
-// term of the input gradient, which needs its column sums) runs on `side`, the
-// rest of the input gradient on `st`; a pooling stage waits for the side
-// stream of the convolution above only before its ground-row step.
-static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st, hipStream_t side) {
+// Row blocks of a bias / ground-row reduction over `rows` rows: about 2 rows
+// per thread.
+static int ground_parts(const sscn_net* net, int64_t rows, int cp) {
+  const int lanes = 256 / (cp / (net->bf16 ? 8 : 4));
+  return (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (rows + 2 * lanes - 1) / (2 * lanes)));
+}
+
+// Whether the backward pass needs row 0 of the gradient below convolution s
+// (the ground row of its input): always above the first layer; for the first,
+// only when the caller asks for the input-feature gradient, which its
+// layer view then holds in full.
+static bool needs_row0(const sscn_net* net, int s) { return s > 1 || net->want_dfeats; }
+
+// Row 0 of convolution s's output gradient delta (when pooling layer s+1 sits
+// above it: pool_above), its bias gradient and ground-row sums, then row 0 of
+// the gradient below it.  Needs delta rows >= 1 and, with pool_above, layer
+// s+1's gradient in full.
+static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_t st) {
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
-  const bool split = side != st;
-  hipError_t e;
-  if (L.kind == 2) {
-    const int nparts = (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (L.cap + 63) / 64));
-    if ((e = timed(net, SSCN_KC_POOL_BWD, st, [&] {
-           return launch_pool_bwd_rows(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, L.rules, Lb.X, Lb.grad, L.Cp,
-                                       net->counts + s, net->counts + s - 1, Lb.cap, net->ppart, nparts, st);
-         })) != hipSuccess)
-      return e;
-    if (split && (e = hipStreamWaitEvent(st, net->ev_join[s + 1], 0)) != hipSuccess) return e;
-    return timed(net, SSCN_KC_POOL_BWD, st, [&] {
-      return launch_pool_row0_final(net->bf16, L.grad, net->ppart, nparts, Lb.X, Lb.grad, L.Cp, st);
-    });
-  }
   const int ci = L.conv_index;
   const ParamPlan& P = net->P[ci];
-  const bool need_dx = s > 1 || net->want_dfeats;
-  if (split) {
-    if ((e = hipEventRecord(net->ev_fork[s], st)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(side, net->ev_fork[s], 0)) != hipSuccess) return e;
+  const bool row0 = needs_row0(net, s);
+  GroundArgs g{};
+  if (pool_above) {
+    const LayerPlan& Lp = net->L[s + 1];
+    g.dY = Lp.grad;
+    g.argmax = Lp.argmax;
+    g.Rp = Lp.rules;
+    g.n_pool = net->counts + s + 1;
+    g.B1 = ground_parts(net, Lp.cap, Lp.Cp);
+    g.Y_below = L.X;
   }
+  g.dZ = L.grad;
+  g.R = L.rules;
+  g.n_rows = net->counts + s;
+  g.B2 = ground_parts(net, L.cap, L.Cp);
+  g.stride = L.Cp;
+  g.cp = L.Cp;
+  g.c_out = L.C;
+  g.part = net->ppart;
+  g.PM = net->pool_parts;
+  g.db = net->db[ci];
+  g.D0 = net->D0;
+  hipError_t e;
+  if ((e = timed(net, SSCN_KC_GROUND, st, [&] { return launch_ground(net->bf16, g, row0 ? L.A : 0, st); })) !=
+      hipSuccess)
+    return e;
+  if (!row0) return hipSuccess;
+  return timed(net, SSCN_KC_GROUND, st, [&] {
+    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, st);
+  });
+}
+
+// Weight gradient of convolution s (its delta complete).
+static hipError_t conv_wgrad(sscn_net* net, int s, hipStream_t st) {
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lb = net->L[s - 1];
+  const int ci = L.conv_index;
+  const ParamPlan& P = net->P[ci];
   WGradArgs w{};
   w.src = Lb.X;
   w.src_stride = Lb.Cp;
@@ -527,7 +565,6 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st, hipStream
   w.A = L.A;
   w.cseg = Lb.Cp;
   w.m_ones = P.m_ones;
-  w.m_ind = P.m_ind;
   w.Mpad = P.Mpad_w;
   w.dsrc = L.grad;
   w.dsrc_stride = L.Cp;
@@ -540,21 +577,29 @@ static hipError_t backward_stage(sscn_net* net, int s, hipStream_t st, hipStream
   w.cfg = P.bn_w == 128 ? 0 : 1;
   w.dW = net->dW[ci];
   w.db = net->db[ci];
-  w.D0 = net->D0;
   w.c_in = P.c_in;
   w.c_out = P.c_out;
-  if ((e = timed(net, SSCN_KC_WGRAD, side, [&] { return launch_wgrad(net->bf16, w, side); })) != hipSuccess) return e;
-  if ((e = timed(net, SSCN_KC_WGRAD_REDUCE, side, [&] {
-         return launch_wgrad_reduce(net->wpart, P.nchunks, P.Mpad_w, P.Npad_w, P.A, P.cp_in, P.c_in, P.c_out,
-                                    P.m_ones, P.m_ind, net->dW[ci], net->db[ci], net->D0, side);
-       })) != hipSuccess)
-    return e;
-  if (need_dx && (e = timed(net, SSCN_KC_WGRAD_REDUCE, side, [&] {
-                    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, side);
-                  })) != hipSuccess)
-    return e;
-  if (split && (e = hipEventRecord(net->ev_join[s], side)) != hipSuccess) return e;
-  if (!need_dx) return hipSuccess;
+  hipError_t e;
+  if ((e = timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, w, st); })) != hipSuccess) return e;
+  return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
+    return launch_wgrad_reduce(net->wpart, P.nchunks, P.Mpad_w, P.Npad_w, P.A, P.cp_in, P.c_in, P.c_out, P.m_ones,
+                               net->dW[ci], net->db[ci], st);
+  });
+}
+
+// Rows >= 1 of the gradient below stage s: pooling routing, or the input-gradient
+// GEMM of a convolution.  (The GEMM reads delta rows >= 1 only: a window list
+// entry of -1 selects zero, whatever its load of row 0 returned.)
+static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lb = net->L[s - 1];
+  if (L.kind == 2)
+    return timed(net, SSCN_KC_POOL_BWD, st, [&] {
+      return launch_pool_route(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, Lb.X, Lb.grad, L.Cp,
+                               net->counts + s - 1, Lb.cap, st);
+    });
+  if (!(s > 1 || net->want_dfeats)) return hipSuccess;
+  const ParamPlan& P = net->P[L.conv_index];
   GemmArgs g{};
   g.src = L.grad;
   g.src_stride = L.Cp;
@@ -668,7 +713,6 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   w.A = 1;
   w.cseg = Lt.Cp;
   w.m_ones = P.m_ones;
-  w.m_ind = -1;
   w.Mpad = P.Mpad_w;
   w.dsrc = net->dlogits;
   w.dsrc_stride = net->dl_stride;
@@ -680,14 +724,13 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   w.cfg = P.bn_w == 128 ? 0 : 1;
   w.dW = h_dW[fc];
   w.db = h_db[fc];
-  w.D0 = nullptr;
   w.c_in = P.c_in;
   w.c_out = P.c_out;
   if (timed(net, SSCN_KC_WGRAD, side, [&] { return launch_wgrad(net->bf16, w, side); }) != hipSuccess)
     return SSCN_ERR_HIP;
   if (timed(net, SSCN_KC_WGRAD_REDUCE, side, [&] {
-        return launch_wgrad_reduce(net->wpart, 1, P.Mpad_w, P.Npad_w, 1, P.cp_in, P.c_in, P.c_out, P.m_ones, -1,
-                                   h_dW[fc], h_db[fc], nullptr, side);
+        return launch_wgrad_reduce(net->wpart, 1, P.Mpad_w, P.Npad_w, 1, P.cp_in, P.c_in, P.c_out, P.m_ones,
+                                   h_dW[fc], h_db[fc], side);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
   GemmArgs g{};
@@ -715,8 +758,27 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
         return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp, st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
-  for (int s = top; s >= 1; --s)
-    if (backward_stage(net, s, st, side) != hipSuccess) return SSCN_ERR_HIP;
+  // Stages from the top down.  The caller's stream carries rows >= 1 of every
+  // gradient (pooling routing, input-gradient GEMMs), which never read row 0;
+  // side2 completes each convolution's delta with row 0 and its bias and
+  // ground-row sums and writes row 0 of the gradient below; side takes each
+  // weight gradient once its delta is complete.
+  hipStream_t side2 = net->side2;
+  for (int s = top; s >= 1; --s) {
+    if (net->L[s].kind == 1) {
+      if (hipEventRecord(net->ev_fork[s], st) != hipSuccess || hipStreamWaitEvent(side2, net->ev_fork[s], 0) != hipSuccess)
+        return SSCN_ERR_HIP;
+      if (ground_level(net, s, s < top && net->L[s + 1].kind == 2, side2) != hipSuccess) return SSCN_ERR_HIP;
+      // ground_level wrote delta row 0 before its row-0 input gradient: fork after it
+      if (hipEventRecord(net->ev_full[s], side2) != hipSuccess || hipStreamWaitEvent(side, net->ev_full[s], 0) != hipSuccess)
+        return SSCN_ERR_HIP;
+      if (conv_wgrad(net, s, side) != hipSuccess) return SSCN_ERR_HIP;
+    }
+    if (rows_below(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
+  }
+  // row 0 of the input-layer gradient comes from side2
+  if (hipEventRecord(net->ev_join[1], side2) != hipSuccess || hipStreamWaitEvent(st, net->ev_join[1], 0) != hipSuccess)
+    return SSCN_ERR_HIP;
   if (d_dfeats) {
     const LayerPlan& L0 = net->L[0];
     if (timed(net, SSCN_KC_HEAD, st, [&] {
@@ -740,7 +802,16 @@ sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream) {
   if (!net || stage < 1 || stage >= net->nlayers) return SSCN_ERR_INVALID_ARGUMENT;
   if (!net->forwarded || !net->dW[0]) return SSCN_ERR_BAD_STATE;
   hipStream_t st = (hipStream_t)stream;
-  return backward_stage(net, stage, st, st) == hipSuccess ? SSCN_OK : SSCN_ERR_HIP;
+  hipError_t e;
+  if (net->L[stage].kind == 1) {
+    // delta of this layer as it stands: its own sums, weight gradient, gradient below
+    if ((e = ground_level(net, stage, false, st)) == hipSuccess && (e = conv_wgrad(net, stage, st)) == hipSuccess)
+      e = rows_below(net, stage, st);
+  } else {
+    // rows >= 1 below, then row 0 below with the sums of the convolution below
+    if ((e = rows_below(net, stage, st)) == hipSuccess) e = ground_level(net, stage - 1, true, st);
+  }
+  return e == hipSuccess ? SSCN_OK : SSCN_ERR_HIP;
 }
 
 sscn_status sscn_timing_enable(sscn_net* net, uint32_t class_mask) {

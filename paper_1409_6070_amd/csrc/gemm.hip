@@ -9,9 +9,8 @@
 //  * forward      out = ReLU(G W + b)        rows: output sites + ground row
 //  * input grad   dX  = sum_f delta[Rt[.][f]] W_f^T   rows: sites below
 //  * softmax head logits = h W + b, dh = dlogits W^T  (window of one)
-//  * weight grad  dW = G^T delta, split over sites; extra A rows produce
-//                 db = sum delta and the ground-row sums D0[f] = sum over
-//                 rows whose window position f reads the ground row.
+//  * weight grad  dW = G^T delta, split over sites (for the softmax layer one
+//                 extra A row of ones also gives db = sum delta).
 //
 // bf16: v_mfma_f32_16x16x32_bf16 (one per 32-wide k block);
 // fp32: v_mfma_f32_16x16x4f32 (four per 16-wide k block).  Accumulation is
@@ -346,7 +345,7 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
   const int ntiles = tiles_m * tiles_n * a.nchunks;
   const int per = ((rows + a.nchunks - 1) / a.nchunks + BK - 1) / BK * BK;
   const int m_gather = a.A * a.cseg;
-  const int m_rows = a.m_ind >= 0 ? a.m_ind + a.A : a.m_ones + 1;  // rows of dW / db / D0 that are read back
+  const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;  // rows of dW / db that are read back
   const T* src = (const T*)a.src;
   const T* dsrc = (const T*)a.dsrc;
   const T one = Elem<T>::from_f32(1.f), zero = Elem<T>::from_f32(0.f);
@@ -396,15 +395,7 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
           } else {
             T* vv = (T*)&val;
 #pragma unroll
-            for (int j = 0; j < VE; ++j) {
-              const int mm = m + j;
-              T x = zero;
-              if (mm == a.m_ones)
-                x = one;
-              else if (a.m_ind >= 0 && mm >= a.m_ind && mm < a.m_ind + a.A)
-                x = (a.rmap[(int64_t)o * a.A + (mm - a.m_ind)] == 0) ? one : zero;
-              vv[j] = x;
-            }
+            for (int j = 0; j < VE; ++j) vv[j] = (m + j == a.m_ones) ? one : zero;
           }
         }
         ra[i] = val;
@@ -461,8 +452,6 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
               if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + nn] = acc[i][j][r];
             } else if (mm == a.m_ones) {
               a.db[nn] = acc[i][j][r];
-            } else if (a.D0) {
-              a.D0[(int64_t)(mm - a.m_ind) * a.c_out + nn] = acc[i][j][r];
             }
           }
         }
@@ -470,18 +459,18 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
   }
 }
 
-// dW, db and the ground-row sums D0 from the split-K partials.  A block has G
+// dW (and db) from the split-K partials.  A block has G
 // thread groups (G = 16, or fewer when there are fewer chunks) of 256/G threads,
 // one output per thread of a group; group g sums chunks g, g+G, ...; the G group
 // sums are added in a fixed order.
 __global__ void __launch_bounds__(256) k_wgrad_reduce(const float* __restrict__ part, int32_t nchunks, int32_t Mpad,
                                                       int32_t Npad, int32_t A, int32_t cseg, int32_t c_in,
-                                                      int32_t c_out, int32_t m_ones, int32_t m_ind, float* dW,
-                                                      float* db, float* D0, int32_t G) {
+                                                      int32_t c_out, int32_t m_ones, float* dW, float* db,
+                                                      int32_t G) {
   __shared__ float red[256];
   const int E = 256 / G;  // outputs per block
   const int m_gather = A * cseg;
-  const int m_rows = m_ind >= 0 ? m_ind + A : m_ones + 1;
+  const int m_rows = m_ones >= 0 ? m_ones + 1 : m_gather;
   const int64_t total = (int64_t)m_rows * c_out;
   const int el = threadIdx.x % E, grp = threadIdx.x / E;
   const int64_t t = (int64_t)blockIdx.x * E + el;
@@ -502,8 +491,6 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(const float* __restrict__ 
     if (c < c_in) dW[((int64_t)f * c_in + c) * c_out + n] = s;
   } else if (m == m_ones) {
     if (db) db[n] = s;
-  } else if (m_ind >= 0 && m >= m_ind && m < m_ind + A) {
-    if (D0) D0[(int64_t)(m - m_ind) * c_out + n] = s;
   }
 }
 
@@ -610,16 +597,15 @@ hipError_t launch_wgrad(bool bf16, const WGradArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_wgrad_reduce(const float* part, int32_t nchunks, int32_t Mpad, int32_t Npad, int32_t A, int32_t cseg,
-                               int32_t c_in, int32_t c_out, int32_t m_ones, int32_t m_ind, float* dW, float* db,
-                               float* D0, hipStream_t st) {
+                               int32_t c_in, int32_t c_out, int32_t m_ones, float* dW, float* db, hipStream_t st) {
   if (nchunks <= 1) return hipSuccess;  // the weight-gradient kernel wrote the results
-  const int m_rows = m_ind >= 0 ? m_ind + A : m_ones + 1;
+  const int m_rows = m_ones >= 0 ? m_ones + 1 : A * cseg;
   const int64_t total = (int64_t)m_rows * c_out;
   const int G = nchunks >= 16 ? 16 : (nchunks >= 8 ? 8 : (nchunks >= 4 ? 4 : 2));
   const int E = 256 / G;
   const int grid = (int)std::max<int64_t>(1, (total + E - 1) / E);
   hipLaunchKernelGGL(k_wgrad_reduce, dim3(grid), dim3(256), 0, st, part, nchunks, Mpad, Npad, A, cseg, c_in, c_out,
-                     m_ones, m_ind, dW, db, D0, G);
+                     m_ones, dW, db, G);
   return hipGetLastError();
 }
 

@@ -75,7 +75,7 @@ struct GemmPlan {
 // weight-gradient GEMM, split over sites:
 //   part[chunk][m][n] = sum_{o in chunk} A(o, m) * dsrc[o][n]
 //   A(o, m) = src[rmap[o*A + f]][c] for m = f*cseg + c < A*cseg;
-//   A(o, m_ones) = 1;  A(o, m_ind + f) = [rmap[o*A + f] == 0]
+//   A(o, m_ones) = 1 when m_ones >= 0 (row m_ones of the result is then db)
 struct WGradArgs {
   const void* src;
   int32_t src_stride;
@@ -83,7 +83,6 @@ struct WGradArgs {
   int32_t A;
   int32_t cseg;
   int32_t m_ones;
-  int32_t m_ind;
   int32_t Mpad;
   const void* dsrc;
   int32_t dsrc_stride;
@@ -96,9 +95,8 @@ struct WGradArgs {
   float* part;
   int32_t cfg;  // 0: 128 x 128 tiles, 1: 128 x 64 tiles
   // with nchunks == 1 the kernel writes the results itself (no partials):
-  float* dW;    // [A*c_in x c_out]
-  float* db;    // [c_out]
-  float* D0;    // [A x c_out] or null
+  float* dW;  // [A*c_in x c_out]
+  float* db;  // [c_out]
   int32_t c_in, c_out;
 };
 
@@ -114,10 +112,9 @@ inline int wgrad_bn(int c_out) { return (c_out + 127) / 128 * 128 <= (c_out + 63
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st);
 hipError_t launch_wgrad(bool bf16, const WGradArgs& a, hipStream_t st);
 
-// part -> dW [A*c_in x c_out], db [c_out], D0 [A x c_out] (ground-row sums)
+// part -> dW [A*c_in x c_out] (and db [c_out] when m_ones >= 0)
 hipError_t launch_wgrad_reduce(const float* part, int32_t nchunks, int32_t Mpad, int32_t Npad, int32_t A, int32_t cseg,
-                               int32_t c_in, int32_t c_out, int32_t m_ones, int32_t m_ind, float* dW, float* db,
-                               float* D0, hipStream_t st);
+                               int32_t c_in, int32_t c_out, int32_t m_ones, float* dW, float* db, hipStream_t st);
 // grad_in[0][c] = sum_f sum_n W[(f*c_in + c)*c_out + n] * D0[f][n]
 hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, int32_t c_in, int32_t c_out,
                           int32_t cp_in, void* grad_in, hipStream_t st);
@@ -128,15 +125,36 @@ hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, 
 hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const int32_t* R, void* X_out,
                            int32_t stride_out, uint8_t* argmax, int32_t cp, const int32_t* n_out, int64_t cap_out,
                            hipStream_t st);
-// Routes dY back to the rows >= 1 below, applying the ReLU mask of the convolution
-// below, and writes the per-block partial sums of the ground-row term.
-hipError_t launch_pool_bwd_rows(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
-                                const int32_t* R, const void* Y_below, void* grad_below, int32_t cp,
-                                const int32_t* n_out, const int32_t* n_in, int64_t cap_in, float* part, int32_t nparts,
-                                hipStream_t st);
-// grad_below[0] = mask(Y_below[0]) * (dY[0] + sum of the partials)
-hipError_t launch_pool_row0_final(bool bf16, const void* dY, const float* part, int32_t nparts, const void* Y_below,
-                                  void* grad_below, int32_t cp, hipStream_t st);
+// Pooling backward, rows >= 1 below: grad_below[i] = dY[Pt[i] / 4] where the
+// window's maximum came from position Pt[i] % 4 and Y_below[i] > 0, else 0.
+hipError_t launch_pool_route(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
+                             const void* Y_below, void* grad_below, int32_t cp, const int32_t* n_in, int64_t cap_in,
+                             hipStream_t st);
+
+// Bias gradient db [c_out] and ground-row sums D0 [AC x c_out] (AC in {0, 1, 4,
+// 9}) of a convolution with output gradient delta = dZ, and, with a pooling
+// layer above (B1 > 0), row 0 of delta itself.  Needs delta rows >= 1 and, with
+// a pooling layer, that layer's dY (rows 0..n_pool), argmax and windows Rp.
+struct GroundArgs {
+  // pooling layer above (B1 = 0: none)
+  const void* dY;
+  const uint8_t* argmax;
+  const int32_t* Rp;
+  const int32_t* n_pool;
+  int32_t B1;
+  const void* Y_below;  // the convolution's output (ReLU mask of row 0)
+  // the convolution
+  void* dZ;            // delta, rows 0..n; row 0 written when B1 > 0
+  const int32_t* R;    // its window list [rows][AC]
+  const int32_t* n_rows;
+  int32_t B2;
+  int32_t stride, cp, c_out;
+  float* part;  // [(2 + AC) * cp * PM]
+  int32_t PM;   // partial stride, >= B1, B2
+  float* db;
+  float* D0;
+};
+hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // input, parameters, head

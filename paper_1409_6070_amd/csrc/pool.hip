@@ -6,11 +6,13 @@
 // state through.
 //
 // Backward: windows do not overlap, so each active row below has exactly one
-// parent; its gradient is a gather through the parent link (no atomics).  The
-// ReLU mask of the convolution below is applied in the same pass, so the
-// stored result is dL/dZ of that convolution.  Row 0 (the ground row) sums
-// the ground row above and every maximum an active window took from a ground
-// location: a two-pass deterministic reduction.
+// window above and takes its gradient through that link (a gather, no
+// atomics), with the ReLU mask of the convolution below applied in the same
+// pass: the stored result is that convolution's output gradient delta.  Row 0
+// (the ground row) sums the ground row above and every maximum an active
+// window took from a ground location; it is reduced together with the
+// convolution below's bias gradient and ground-row sums (block partials, then
+// a fixed-order final pass: deterministic).
 
 #include "common.h"
 #include "kernels.h"
@@ -73,11 +75,17 @@ __global__ void __launch_bounds__(256) k_pool_fwd(const T* __restrict__ X_in, in
   }
 }
 
+// Routing of the output gradient dY of a pooling layer to the rows below: row
+// i >= 1 has one window above, p = Pt[i] = 4 * (row above) + (position of i),
+// and takes dY[p / 4] where that window's maximum came from position p % 4 and
+// the value below passed the ReLU (Y_below[i] > 0); else 0.  The stored
+// result is the output gradient delta of the convolution below, rows >= 1.
+// Row 0 of it needs a reduction (k_ground_sums / k_ground_final).
 template <typename T>
-__global__ void __launch_bounds__(256) k_pool_bwd(const T* __restrict__ dY, int32_t stride,
-                                                  const uint8_t* __restrict__ argmax, const int32_t* __restrict__ Pt,
-                                                  const T* __restrict__ Y_below, T* grad_below, int32_t cp,
-                                                  const int32_t* n_in_p) {
+__global__ void __launch_bounds__(256) k_pool_route(const T* __restrict__ dY, int32_t stride,
+                                                    const uint8_t* __restrict__ argmax, const int32_t* __restrict__ Pt,
+                                                    const T* __restrict__ Y_below, T* grad_below, int32_t cp,
+                                                    const int32_t* n_in_p) {
   constexpr int VE = Elem<T>::VE;
   typedef typename ArgPack<VE>::W AW;
   const int nv = cp / VE;
@@ -103,42 +111,13 @@ __global__ void __launch_bounds__(256) k_pool_bwd(const T* __restrict__ dY, int3
   }
 }
 
-// Ground-row reduction, pass 1.  Block b takes a contiguous range of output
-// rows o >= 1; thread t owns channel vector t % nv and every (256/nv)-th row of
-// the range, summing dY[o][c] where the max of (o, c) was read from row 0.
-// The row lanes are then combined in LDS in a fixed order: deterministic.
-template <typename T>
-__global__ void __launch_bounds__(256) k_pool_row0_part(const T* __restrict__ dY, int32_t stride,
-                                                        const uint8_t* __restrict__ argmax,
-                                                        const int32_t* __restrict__ R, int32_t cp,
-                                                        const int32_t* n_out_p, float* part) {
-  constexpr int VE = Elem<T>::VE;
-  typedef typename ArgPack<VE>::W AW;
-  __shared__ float red[256 * VE];
-  const int nv = cp / VE;
-  const int lanes = 256 / nv;  // row lanes (nv <= 256)
+// Sum over one block's rows, per channel: thread t holds VE channels of vector
+// t % nv; the 256/nv row lanes are combined in LDS in a fixed order; the sum of
+// channel e goes to out[e * PM].
+template <int VE>
+__device__ inline void block_channel_sums(const float (&acc)[VE], float* red, int nv, int cp, float* out, int PM) {
   const int t = threadIdx.x;
-  const int v = t % nv, rl = t / nv;
-  const int n_out = *n_out_p;
-  const int per = (n_out + gridDim.x - 1) / gridDim.x;
-  const int o_beg = 1 + blockIdx.x * per;
-  const int o_end = min(n_out + 1, o_beg + per);
-  float acc[VE];
-#pragma unroll
-  for (int j = 0; j < VE; ++j) acc[j] = 0.f;
-  if (rl < lanes) {
-    for (int o = o_beg + rl; o < o_end; o += lanes) {
-      const i32x4 r = *(const i32x4*)(R + (int64_t)o * 4);
-      const AW am = *(const AW*)(argmax + (int64_t)o * stride + v * VE);
-      const u32x4 g = *(const u32x4*)(dY + (int64_t)o * stride + v * VE);
-#pragma unroll
-      for (int j = 0; j < VE; ++j) {
-        const int f = (int)((am >> (8 * j)) & 3);
-        const int rf = f == 0 ? r.x : (f == 1 ? r.y : (f == 2 ? r.z : r.w));
-        if (rf == 0) acc[j] += Elem<T>::to_f32(((const T*)&g)[j]);
-      }
-    }
-  }
+  const int lanes = 256 / nv;
 #pragma unroll
   for (int j = 0; j < VE; ++j) red[t * VE + j] = acc[j];
   __syncthreads();
@@ -146,31 +125,143 @@ __global__ void __launch_bounds__(256) k_pool_row0_part(const T* __restrict__ dY
     const int vv = e / VE, jj = e - vv * VE;
     float s = 0.f;
     for (int l = 0; l < lanes; ++l) s += red[(l * nv + vv) * VE + jj];
-    part[(int64_t)blockIdx.x * cp + e] = s;
+    out[(int64_t)e * PM] = s;
+  }
+  __syncthreads();
+}
+
+// gnd[k] = (R[i][k] == 0): window position k of row i reads the ground row.
+template <int AC>
+__device__ inline void ground_flags(const int32_t* __restrict__ R, int64_t i, int (&gnd)[AC > 0 ? AC : 1]) {
+  if constexpr (AC == 4) {
+    const i32x4 r = *(const i32x4*)(R + i * 4);
+    gnd[0] = r.x == 0;
+    gnd[1] = r.y == 0;
+    gnd[2] = r.z == 0;
+    gnd[3] = r.w == 0;
+  } else {
+#pragma unroll
+    for (int k = 0; k < AC; ++k) gnd[k] = R[i * AC + k] == 0;
   }
 }
 
-// Pass 2: a block covers 16 channels with 16 groups of 16 threads; group g sums
-// partials g, g+16, ...; the 16 group sums are added in a fixed order.
-// grad_below[0][c] = mask(Y_below[0][c]) * (dY[0][c] + sum of partials).
-template <typename T>
-__global__ void __launch_bounds__(256) k_pool_row0_final(const T* __restrict__ dY, const float* __restrict__ part,
-                                                         int32_t nparts, const T* __restrict__ Y_below,
-                                                         T* grad_below, int32_t cp) {
-  __shared__ float red[16][16];
-  const int cl = threadIdx.x & 15, grp = threadIdx.x >> 4;
-  const int c = blockIdx.x * 16 + cl;
-  float s = 0.f;
-  if (c < cp)
-    for (int p = grp; p < nparts; p += 16) s += part[(int64_t)p * cp + c];
-  red[grp][cl] = s;
-  __syncthreads();
-  if (grp == 0 && c < cp) {
-    float tot = 0.f;
-    for (int g = 0; g < 16; ++g) tot += red[g][cl];
-    tot += Elem<T>::to_f32(dY[c]);
-    grad_below[c] = (Elem<T>::to_f32(Y_below[c]) > 0.f) ? Elem<T>::from_f32(tot) : Elem<T>::from_f32(0.f);
+// Partial sums behind a convolution's bias gradient and ground-row sums, and
+// behind the ground row of a pooling layer above it.  Slots (per channel):
+//   0       sum over pooling rows o >= 1 of dY[o] where the maximum came from a
+//           ground location (blocks [0, B1), only with a pooling layer above);
+//   1       sum over delta rows i >= 1 (bias gradient);
+//   2 + f   sum over delta rows i >= 1 whose window position f reads the
+//           ground row (D0[f]), f < AC.
+// Row 0 of delta enters in the final pass.  A block takes a contiguous range of
+// rows; partial p of slot k, channel c is part[(k * cp + c) * PM + p].
+template <typename T, int AC>
+__global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
+  constexpr int VE = Elem<T>::VE;
+  typedef typename ArgPack<VE>::W AW;
+  __shared__ float red[256 * VE];
+  const int nv = g.cp / VE;
+  const int lanes = 256 / nv;
+  const int t = threadIdx.x;
+  const int v = t % nv, rl = t / nv;
+  const int c = v * VE;
+  const bool active = rl < lanes;
+  if ((int)blockIdx.x < g.B1) {
+    const T* dY = (const T*)g.dY;
+    const int n = *g.n_pool;
+    const int per = (n + g.B1 - 1) / g.B1;
+    const int o_beg = 1 + blockIdx.x * per, o_end = min(n + 1, o_beg + per);
+    float acc[VE];
+#pragma unroll
+    for (int j = 0; j < VE; ++j) acc[j] = 0.f;
+    if (active) {
+#pragma unroll 2
+      for (int o = o_beg + rl; o < o_end; o += lanes) {
+        const i32x4 r = *(const i32x4*)(g.Rp + (int64_t)o * 4);
+        const AW am = *(const AW*)(g.argmax + (int64_t)o * g.stride + c);
+        const u32x4 gv = *(const u32x4*)(dY + (int64_t)o * g.stride + c);
+#pragma unroll
+        for (int j = 0; j < VE; ++j) {
+          const int f = (int)((am >> (8 * j)) & 3);
+          const int rf = f == 0 ? r.x : (f == 1 ? r.y : (f == 2 ? r.z : r.w));
+          acc[j] += rf == 0 ? Elem<T>::to_f32(((const T*)&gv)[j]) : 0.f;
+        }
+      }
+    }
+    block_channel_sums<VE>(acc, red, nv, g.cp, g.part + blockIdx.x, g.PM);
+    return;
   }
+  const int b = blockIdx.x - g.B1;
+  const T* dZ = (const T*)g.dZ;
+  const int n = *g.n_rows;
+  const int per = (n + g.B2 - 1) / g.B2;
+  const int i_beg = 1 + b * per, i_end = min(n + 1, i_beg + per);
+  float acc[1 + AC][VE];
+#pragma unroll
+  for (int k = 0; k <= AC; ++k)
+#pragma unroll
+    for (int j = 0; j < VE; ++j) acc[k][j] = 0.f;
+  if (active) {
+#pragma unroll 2
+    for (int i = i_beg + rl; i < i_end; i += lanes) {
+      const u32x4 gv = *(const u32x4*)(dZ + (int64_t)i * g.stride + c);
+      int gnd[AC > 0 ? AC : 1];
+      ground_flags<AC>(g.R, i, gnd);
+#pragma unroll
+      for (int j = 0; j < VE; ++j) {
+        const float d = Elem<T>::to_f32(((const T*)&gv)[j]);
+        acc[0][j] += d;
+#pragma unroll
+        for (int k = 0; k < AC; ++k) acc[1 + k][j] += gnd[k] ? d : 0.f;
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k <= AC; ++k)
+    block_channel_sums<VE>(acc[k], red, nv, g.cp, g.part + (int64_t)(1 + k) * g.cp * g.PM + b, g.PM);
+}
+
+// Final pass: one wavefront per channel c sums each slot's partials (lane l
+// takes partials l, l+64, ...; then a butterfly over the 64 lanes, the same
+// order every run), and lane 0 finishes:
+//   with a pooling layer above, row 0 of delta is
+//     z0 = mask(Y_below[0][c]) * (dY[0][c] + slot 0), written to delta[0][c];
+//   without one, z0 = delta[0][c] as stored;
+//   db[c] = slot 1 + z0,  D0[f][c] = slot 2+f + z0  (row 0 reads the ground row
+//   at every window position), for c < c_out.
+template <typename T, int AC>
+__global__ void __launch_bounds__(256) k_ground_final(GroundArgs g) {
+  const int lane = threadIdx.x & 63;
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (c >= g.cp) return;
+  const bool pool = g.B1 > 0;
+  float tot[2 + AC];
+#pragma unroll
+  for (int k = 0; k < 2 + AC; ++k) {
+    const int np = k == 0 ? g.B1 : g.B2;
+    const float* pp = g.part + ((int64_t)k * g.cp + c) * g.PM;
+    float s = 0.f;
+#pragma unroll 4
+    for (int p = lane; p < np; p += 64) s += pp[p];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+    tot[k] = s;
+  }
+  if (lane != 0) return;
+  T* dZ = (T*)g.dZ;
+  float z0;
+  if (pool) {
+    const T g0 = (Elem<T>::to_f32(((const T*)g.Y_below)[c]) > 0.f)
+                     ? Elem<T>::from_f32(tot[0] + Elem<T>::to_f32(((const T*)g.dY)[c]))
+                     : Elem<T>::from_f32(0.f);
+    dZ[c] = g0;
+    z0 = Elem<T>::to_f32(g0);
+  } else {
+    z0 = Elem<T>::to_f32(dZ[c]);
+  }
+  if (c >= g.c_out) return;
+  g.db[c] = tot[1] + z0;
+#pragma unroll
+  for (int k = 0; k < AC; ++k) g.D0[(int64_t)k * g.c_out + c] = tot[2 + k] + z0;
 }
 
 static int grid_for(int64_t items) { return (int)std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 4096)); }
@@ -189,34 +280,47 @@ hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const
   return hipGetLastError();
 }
 
-hipError_t launch_pool_bwd_rows(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
-                                const int32_t* R, const void* Y_below, void* grad_below, int32_t cp,
-                                const int32_t* n_out, const int32_t* n_in, int64_t cap_in, float* part, int32_t nparts,
-                                hipStream_t st) {
+hipError_t launch_pool_route(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
+                             const void* Y_below, void* grad_below, int32_t cp, const int32_t* n_in, int64_t cap_in,
+                             hipStream_t st) {
   const int VE = bf16 ? 8 : 4;
-  int grid = grid_for(cap_in * (cp / VE));
-  if (bf16) {
-    hipLaunchKernelGGL(k_pool_bwd<__bf16>, dim3(grid), dim3(256), 0, st, (const __bf16*)dY, stride, argmax, Pt,
+  const int grid = grid_for(cap_in * (cp / VE));
+  if (bf16)
+    hipLaunchKernelGGL(k_pool_route<__bf16>, dim3(grid), dim3(256), 0, st, (const __bf16*)dY, stride, argmax, Pt,
                        (const __bf16*)Y_below, (__bf16*)grad_below, cp, n_in);
-    hipLaunchKernelGGL(k_pool_row0_part<__bf16>, dim3(nparts), dim3(256), 0, st, (const __bf16*)dY, stride, argmax, R,
-                       cp, n_out, part);
-  } else {
-    hipLaunchKernelGGL(k_pool_bwd<float>, dim3(grid), dim3(256), 0, st, (const float*)dY, stride, argmax, Pt,
+  else
+    hipLaunchKernelGGL(k_pool_route<float>, dim3(grid), dim3(256), 0, st, (const float*)dY, stride, argmax, Pt,
                        (const float*)Y_below, (float*)grad_below, cp, n_in);
-    hipLaunchKernelGGL(k_pool_row0_part<float>, dim3(nparts), dim3(256), 0, st, (const float*)dY, stride, argmax, R, cp,
-                       n_out, part);
-  }
   return hipGetLastError();
 }
 
-hipError_t launch_pool_row0_final(bool bf16, const void* dY, const float* part, int32_t nparts, const void* Y_below,
-                                  void* grad_below, int32_t cp, hipStream_t st) {
-  if (bf16)
-    hipLaunchKernelGGL(k_pool_row0_final<__bf16>, dim3((cp + 15) / 16), dim3(256), 0, st, (const __bf16*)dY, part,
-                       nparts, (const __bf16*)Y_below, (__bf16*)grad_below, cp);
-  else
-    hipLaunchKernelGGL(k_pool_row0_final<float>, dim3((cp + 15) / 16), dim3(256), 0, st, (const float*)dY, part,
-                       nparts, (const float*)Y_below, (float*)grad_below, cp);
+template <typename T, int AC>
+static void launch_ground_t(const GroundArgs& g, hipStream_t st) {
+  hipLaunchKernelGGL((k_ground_sums<T, AC>), dim3(g.B1 + g.B2), dim3(256), 0, st, g);
+  hipLaunchKernelGGL((k_ground_final<T, AC>), dim3((g.cp + 3) / 4), dim3(256), 0, st, g);
+}
+
+hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, hipStream_t st) {
+  if (g.B2 < 1 || g.B1 < 0 || g.B1 > g.PM || g.B2 > g.PM) return hipErrorInvalidValue;
+#define SSCN_GROUND(T, A) launch_ground_t<T, A>(g, st)
+  if (bf16) {
+    switch (AC) {
+      case 0: SSCN_GROUND(__bf16, 0); break;
+      case 1: SSCN_GROUND(__bf16, 1); break;
+      case 4: SSCN_GROUND(__bf16, 4); break;
+      case 9: SSCN_GROUND(__bf16, 9); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (AC) {
+      case 0: SSCN_GROUND(float, 0); break;
+      case 1: SSCN_GROUND(float, 1); break;
+      case 4: SSCN_GROUND(float, 4); break;
+      case 9: SSCN_GROUND(float, 9); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
+#undef SSCN_GROUND
   return hipGetLastError();
 }
 
