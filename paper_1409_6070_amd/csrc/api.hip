@@ -39,6 +39,7 @@ struct ParamPlan {
   int64_t rows_f, rows_d;             // their row bounds
   int NpadF, KpadF, NpadD, KpadD;
   int Mpad_w, Npad_w, bn_w, nchunks, m_ones;
+  size_t part_off;  // this layer's split-K partials in wpart (floats)
   void* WpF;
   void* WpD;
 };
@@ -102,37 +103,10 @@ struct sscn_net {
     hipEvent_t a, b;
   };
   std::vector<Rec> recs;
-  // Backward streams beside the caller's: `side` runs the weight gradients,
-  // `side2` the row-0 chain (bias and ground-row sums, row 0 of each input
-  // gradient).  ev_fork[s]: delta of layer s complete in rows >= 1 (caller's
-  // stream); ev_full[s]: delta complete with row 0 (side2); ev_join[0..1]: the
-  // two side streams done, joined at the end of the backward pass.
-  hipStream_t side = nullptr, side2 = nullptr;
-  hipEvent_t ev_fork[MAX_LAYERS + 1] = {};
-  hipEvent_t ev_full[MAX_LAYERS + 1] = {};
-  hipEvent_t ev_join[2] = {};
   ~sscn_net() {
     for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
-    for (int i = 0; i <= MAX_LAYERS; ++i) {
-      if (ev_fork[i]) (void)hipEventDestroy(ev_fork[i]);
-      if (ev_full[i]) (void)hipEventDestroy(ev_full[i]);
-    }
-    for (hipEvent_t e : ev_join)
-      if (e) (void)hipEventDestroy(e);
-    if (side) (void)hipStreamDestroy(side);
-    if (side2) (void)hipStreamDestroy(side2);
   }
 };
-
-static bool ensure_side_stream(sscn_net* net) {
-  if (net->side2) return true;
-  auto ev = [](hipEvent_t* e) { return *e || hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess; };
-  for (int i = 0; i <= MAX_LAYERS; ++i)
-    if (!ev(&net->ev_fork[i]) || !ev(&net->ev_full[i])) return false;
-  if (!ev(&net->ev_join[0]) || !ev(&net->ev_join[1])) return false;
-  if (!net->side && hipStreamCreateWithFlags(&net->side, hipStreamNonBlocking) != hipSuccess) return false;
-  return hipStreamCreateWithFlags(&net->side2, hipStreamNonBlocking) == hipSuccess;
-}
 
 static constexpr size_t MAX_TIMED = 65536;
 
@@ -195,7 +169,9 @@ static void carve(sscn_net* net, void* base) {
     ParamPlan& P = net->P[p];
     P.WpF = cv.take((size_t)P.NpadF * P.KpadF * net->esz);
     P.WpD = cv.take((size_t)P.NpadD * P.KpadD * net->esz);
-    max_part = std::max(max_part, (size_t)P.nchunks * P.Mpad_w * P.Npad_w);
+    // every layer's partials coexist: the weight gradients run as one group
+    P.part_off = max_part;
+    if (P.nchunks > 1) max_part += (size_t)P.nchunks * P.Mpad_w * P.Npad_w;
     max_d0 = std::max(max_d0, (size_t)P.A * P.c_out);
     if (P.pf.ksplit > 1) max_gpart = std::max(max_gpart, (size_t)P.pf.ksplit * P.rows_f * P.pf.Npad);
     if (P.pd.ksplit > 1) max_gpart = std::max(max_gpart, (size_t)P.pd.ksplit * P.rows_d * P.pd.Npad);
@@ -204,7 +180,7 @@ static void carve(sscn_net* net, void* base) {
   net->dlogits = cv.take((size_t)B * net->dl_stride * net->esz);
   net->dh = (float*)cv.take((size_t)B * Lt.Cp * 4);
   net->loss_part = (float*)cv.take((size_t)B * 4);
-  net->wpart = (float*)cv.take(max_part * 4);
+  net->wpart = (float*)cv.take(std::max<size_t>(max_part, 1) * 4);
   net->gpart = (float*)cv.take(std::max<size_t>(max_gpart, 1) * 4);
   net->D0 = (float*)cv.take(max_d0 * 4);
   net->ppart = (float*)cv.take((size_t)net->pool_parts * (2 + 9) * max_cp * 4);
@@ -218,13 +194,14 @@ static void set_plan(GemmArgs& g, const GemmPlan& p, int64_t rows_cap, float* gp
   g.part_rows = (int32_t)rows_cap;
 }
 
-// Site chunks of a split-K weight gradient: about 1024 workgroups, at least 4
+// Site chunks of a split-K weight gradient: about 256 workgroups per layer (the
+// layers of a step share one launch), at least 4
 // slabs of sites each, and partial sums (chunks x |dW| fp32) of at most twice the
 // bytes the kernel reads (rows x row_bytes).
 static int wgrad_chunks(int64_t rows_cap, int tiles_mn, int BK, int64_t row_bytes, int64_t part_bytes) {
   int64_t max_chunks = std::max<int64_t>(1, std::min<int64_t>(512, (rows_cap + 4 * BK - 1) / (4 * BK)));
   max_chunks = std::min<int64_t>(max_chunks, std::max<int64_t>(1, 2 * rows_cap * row_bytes / std::max<int64_t>(part_bytes, 1)));
-  int64_t want = std::max<int64_t>(1, (1024 + tiles_mn - 1) / tiles_mn);
+  int64_t want = std::max<int64_t>(1, (256 + tiles_mn - 1) / tiles_mn);
   return (int)std::min<int64_t>(want, max_chunks);
 }
 
@@ -498,11 +475,11 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
   });
 }
 
-// Row blocks of a bias / ground-row reduction over `rows` rows: about 2 rows
+// Row blocks of a bias / ground-row reduction over `rows` rows: about 8 rows
 // per thread.
 static int ground_parts(const sscn_net* net, int64_t rows, int cp) {
   const int lanes = 256 / (cp / (net->bf16 ? 8 : 4));
-  return (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (rows + 2 * lanes - 1) / (2 * lanes)));
+  return (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (rows + 8 * lanes - 1) / (8 * lanes)));
 }
 
 // Whether the backward pass needs row 0 of the gradient below convolution s
@@ -552,8 +529,8 @@ static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_
   });
 }
 
-// Weight gradient of convolution s (its delta complete).
-static hipError_t conv_wgrad(sscn_net* net, int s, hipStream_t st) {
+// Weight-gradient arguments of convolution s (run once its delta is complete).
+static WGradArgs conv_wgrad_args(const sscn_net* net, int s) {
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
   const int ci = L.conv_index;
@@ -573,18 +550,29 @@ static hipError_t conv_wgrad(sscn_net* net, int s, hipStream_t st) {
   w.rows_dev = net->counts + s;
   w.rows_add = 1;
   w.nchunks = P.nchunks;
-  w.part = net->wpart;
+  w.part = net->wpart + P.part_off;
   w.cfg = P.bn_w == 128 ? 0 : 1;
   w.dW = net->dW[ci];
   w.db = net->db[ci];
   w.c_in = P.c_in;
   w.c_out = P.c_out;
+  return w;
+}
+
+// Weight gradients of a list of layers: one launch per tile shape, then one
+// launch reducing every split-K layer.
+static hipError_t run_wgrads(sscn_net* net, const WGradArgs* w, int n, hipStream_t st) {
   hipError_t e;
-  if ((e = timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, w, st); })) != hipSuccess) return e;
-  return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] {
-    return launch_wgrad_reduce(net->wpart, P.nchunks, P.Mpad_w, P.Npad_w, P.A, P.cp_in, P.c_in, P.c_out, P.m_ones,
-                               net->dW[ci], net->db[ci], st);
-  });
+  for (int cfg = 0; cfg < 2; ++cfg) {
+    WGradArgs sel[MAX_WG_LAYERS];
+    int k = 0;
+    for (int i = 0; i < n; ++i)
+      if (w[i].cfg == cfg) sel[k++] = w[i];
+    if (k && (e = timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, cfg, sel, k, st); })) !=
+                 hipSuccess)
+      return e;
+  }
+  return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] { return launch_wgrad_reduce(w, n, st); });
 }
 
 // Rows >= 1 of the gradient below stage s: pooling routing, or the input-gradient
@@ -696,43 +684,11 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   }
   hipStream_t st = (hipStream_t)stream;
   net->want_dfeats = d_dfeats != nullptr;
-  if (!ensure_side_stream(net)) return SSCN_ERR_HIP;
-  hipStream_t side = net->side;
   const int top = net->nlayers - 1;
   const LayerPlan& Lt = net->L[top];
   const int fc = net->d.ell + 1;
   const ParamPlan& P = net->P[fc];
-  // softmax layer: dW, db from (h, dlogits) on the side stream; dh = dlogits W^T on st
-  if (hipEventRecord(net->ev_fork[MAX_LAYERS], st) != hipSuccess ||
-      hipStreamWaitEvent(side, net->ev_fork[MAX_LAYERS], 0) != hipSuccess)
-    return SSCN_ERR_HIP;
-  WGradArgs w{};
-  w.src = Lt.X;
-  w.src_stride = Lt.Cp;
-  w.rmap = net->head_rows;
-  w.A = 1;
-  w.cseg = Lt.Cp;
-  w.m_ones = P.m_ones;
-  w.Mpad = P.Mpad_w;
-  w.dsrc = net->dlogits;
-  w.dsrc_stride = net->dl_stride;
-  w.dsrc_cols = net->dl_stride;
-  w.Npad = P.Npad_w;
-  w.rows_host = net->batch;
-  w.nchunks = 1;
-  w.part = net->wpart;
-  w.cfg = P.bn_w == 128 ? 0 : 1;
-  w.dW = h_dW[fc];
-  w.db = h_db[fc];
-  w.c_in = P.c_in;
-  w.c_out = P.c_out;
-  if (timed(net, SSCN_KC_WGRAD, side, [&] { return launch_wgrad(net->bf16, w, side); }) != hipSuccess)
-    return SSCN_ERR_HIP;
-  if (timed(net, SSCN_KC_WGRAD_REDUCE, side, [&] {
-        return launch_wgrad_reduce(net->wpart, 1, P.Mpad_w, P.Npad_w, 1, P.cp_in, P.c_in, P.c_out, P.m_ones,
-                                   h_dW[fc], h_db[fc], side);
-      }) != hipSuccess)
-    return SSCN_ERR_HIP;
+  // softmax layer: dh = dlogits W^T, scattered to the top layer's rows
   GemmArgs g{};
   g.src = net->dlogits;
   g.src_stride = net->dl_stride;
@@ -758,27 +714,14 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
         return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp, st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
-  // Stages from the top down.  The caller's stream carries rows >= 1 of every
-  // gradient (pooling routing, input-gradient GEMMs), which never read row 0;
-  // side2 completes each convolution's delta with row 0 and its bias and
-  // ground-row sums and writes row 0 of the gradient below; side takes each
-  // weight gradient once its delta is complete.
-  hipStream_t side2 = net->side2;
+  // Stages from the top down, all on the caller's stream: each convolution's
+  // delta is completed (row 0, bias and ground-row sums, row 0 of the
+  // gradient below), then rows >= 1 of the gradient below it.
   for (int s = top; s >= 1; --s) {
-    if (net->L[s].kind == 1) {
-      if (hipEventRecord(net->ev_fork[s], st) != hipSuccess || hipStreamWaitEvent(side2, net->ev_fork[s], 0) != hipSuccess)
-        return SSCN_ERR_HIP;
-      if (ground_level(net, s, s < top && net->L[s + 1].kind == 2, side2) != hipSuccess) return SSCN_ERR_HIP;
-      // ground_level wrote delta row 0 before its row-0 input gradient: fork after it
-      if (hipEventRecord(net->ev_full[s], side2) != hipSuccess || hipStreamWaitEvent(side, net->ev_full[s], 0) != hipSuccess)
-        return SSCN_ERR_HIP;
-      if (conv_wgrad(net, s, side) != hipSuccess) return SSCN_ERR_HIP;
-    }
+    if (net->L[s].kind == 1 && ground_level(net, s, s < top && net->L[s + 1].kind == 2, st) != hipSuccess)
+      return SSCN_ERR_HIP;
     if (rows_below(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
   }
-  // row 0 of the input-layer gradient comes from side2
-  if (hipEventRecord(net->ev_join[1], side2) != hipSuccess || hipStreamWaitEvent(st, net->ev_join[1], 0) != hipSuccess)
-    return SSCN_ERR_HIP;
   if (d_dfeats) {
     const LayerPlan& L0 = net->L[0];
     if (timed(net, SSCN_KC_HEAD, st, [&] {
@@ -786,9 +729,35 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
         }) != hipSuccess)
       return SSCN_ERR_HIP;
   }
-  // everything on the side stream completes before the caller's stream moves on
-  if (hipEventRecord(net->ev_join[0], side) != hipSuccess || hipStreamWaitEvent(st, net->ev_join[0], 0) != hipSuccess)
-    return SSCN_ERR_HIP;
+  // every weight gradient, the softmax layer's included, as one group
+  WGradArgs w[MAX_WG_LAYERS];
+  int nw = 0;
+  for (int s = 1; s <= top; ++s)
+    if (net->L[s].kind == 1) w[nw++] = conv_wgrad_args(net, s);
+  {
+    WGradArgs& f = w[nw++];
+    f = WGradArgs{};
+    f.src = Lt.X;
+    f.src_stride = Lt.Cp;
+    f.rmap = net->head_rows;
+    f.A = 1;
+    f.cseg = Lt.Cp;
+    f.m_ones = P.m_ones;
+    f.Mpad = P.Mpad_w;
+    f.dsrc = net->dlogits;
+    f.dsrc_stride = net->dl_stride;
+    f.dsrc_cols = net->dl_stride;
+    f.Npad = P.Npad_w;
+    f.rows_host = net->batch;
+    f.nchunks = 1;
+    f.part = net->wpart;
+    f.cfg = P.bn_w == 128 ? 0 : 1;
+    f.dW = h_dW[fc];
+    f.db = h_db[fc];
+    f.c_in = P.c_in;
+    f.c_out = P.c_out;
+  }
+  if (run_wgrads(net, w, nw, st) != hipSuccess) return SSCN_ERR_HIP;
   return SSCN_OK;
 }
 
@@ -805,7 +774,8 @@ sscn_status sscn_backward_stage(sscn_net* net, int32_t stage, void* stream) {
   hipError_t e;
   if (net->L[stage].kind == 1) {
     // delta of this layer as it stands: its own sums, weight gradient, gradient below
-    if ((e = ground_level(net, stage, false, st)) == hipSuccess && (e = conv_wgrad(net, stage, st)) == hipSuccess)
+    const WGradArgs w = conv_wgrad_args(net, stage);
+    if ((e = ground_level(net, stage, false, st)) == hipSuccess && (e = run_wgrads(net, &w, 1, st)) == hipSuccess)
       e = rows_below(net, stage, st);
   } else {
     // rows >= 1 below, then row 0 below with the sums of the convolution below

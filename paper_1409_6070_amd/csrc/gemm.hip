@@ -328,8 +328,11 @@ struct Quad<float> {
 // 16-byte vectors (VE consecutive channels) of 4 consecutive sites and stores
 // them transposed, 4 sites per LDS write.  Loads of the next slab are issued
 // before the current slab's MFMAs.
+//
+// One launch serves a group of layers: workgroup tile t belongs to the layer l
+// with tile_beg[l] <= t < tile_beg[l + 1].
 template <typename T, class C>
-__global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
+__global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp) {
   constexpr int VE = C::VE, BK = C::BK, LDK = C::LDK, BM = C::BM, BN = C::BN, NT = C::NT;
   constexpr int MV = BM / VE, NV = BN / VE;  // vectors across a slab row
   static_assert(MV * (BK / 4) == NT && NV * (BK / 4) <= NT, "one quad of sites per thread");
@@ -340,21 +343,27 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave / C::WN, wn = wave % C::WN;
-  const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
-  const int tiles_m = a.Mpad / BM, tiles_n = a.Npad / BN;
-  const int ntiles = tiles_m * tiles_n * a.nchunks;
-  const int per = ((rows + a.nchunks - 1) / a.nchunks + BK - 1) / BK * BK;
-  const int m_gather = a.A * a.cseg;
-  const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;  // rows of dW / db that are read back
-  const T* src = (const T*)a.src;
-  const T* dsrc = (const T*)a.dsrc;
   const T one = Elem<T>::from_f32(1.f), zero = Elem<T>::from_f32(0.f);
-  // this thread's quad: sites 4*q .. 4*q+3 of a slab, vector mv / nv
-  const int qa = tid / MV, mv = tid - qa * MV;
-  const int qb = tid / NV, nvv = tid - qb * NV;
-  const bool b_active = tid < NV * (BK / 4);
+  // this thread's quad: sites 4*q .. 4*q+3 of a slab, vector mv / nv.  The quad
+  // index runs fastest so that a wavefront's transposed LDS writes spread over
+  // all banks (vector-fastest puts every vector of a quad on the same bank).
+  constexpr int NQ = BK / 4;
+  const int qa = tid % NQ, mv = tid / NQ;
+  const int qb = tid % NQ, nvv = tid / NQ;
+  const bool b_active = tid < NV * NQ;
 
-  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+  for (int t = blockIdx.x; t < grp.tile_beg[grp.n]; t += gridDim.x) {
+    int l = 0;
+    while (l + 1 < grp.n && t >= grp.tile_beg[l + 1]) ++l;
+    const WGradArgs& a = grp.L[l];
+    const int tile = t - grp.tile_beg[l];
+    const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
+    const int tiles_m = a.Mpad / BM, tiles_n = a.Npad / BN;
+    const int per = ((rows + a.nchunks - 1) / a.nchunks + BK - 1) / BK * BK;
+    const int m_gather = a.A * a.cseg;
+    const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;  // rows of dW / db that are read back
+    const T* src = (const T*)a.src;
+    const T* dsrc = (const T*)a.dsrc;
     const int tn = tile % tiles_n;
     const int tq = tile / tiles_n;
     const int tm = tq % tiles_m;
@@ -459,38 +468,41 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradArgs a) {
   }
 }
 
-// dW (and db) from the split-K partials.  A block has G
-// thread groups (G = 16, or fewer when there are fewer chunks) of 256/G threads,
-// one output per thread of a group; group g sums chunks g, g+G, ...; the G group
-// sums are added in a fixed order.
-__global__ void __launch_bounds__(256) k_wgrad_reduce(const float* __restrict__ part, int32_t nchunks, int32_t Mpad,
-                                                      int32_t Npad, int32_t A, int32_t cseg, int32_t c_in,
-                                                      int32_t c_out, int32_t m_ones, float* dW, float* db,
-                                                      int32_t G) {
+// dW (and db) from the split-K partials, for a group of layers (block b
+// belongs to layer l with blk_beg[l] <= b < blk_beg[l + 1]).  A block has G
+// thread groups (G = 16, or fewer when there are fewer chunks) of 256/G
+// threads, one output per thread of a group; group g sums chunks g, g+G, ...;
+// the G group sums are added in a fixed order.
+__global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
   __shared__ float red[256];
+  int l = 0;
+  while (l + 1 < grp.n && (int)blockIdx.x >= grp.blk_beg[l + 1]) ++l;
+  const WGradArgs& a = grp.L[l];
+  const int G = grp.G[l];
   const int E = 256 / G;  // outputs per block
-  const int m_gather = A * cseg;
-  const int m_rows = m_ones >= 0 ? m_ones + 1 : m_gather;
-  const int64_t total = (int64_t)m_rows * c_out;
-  const int el = threadIdx.x % E, grp = threadIdx.x / E;
-  const int64_t t = (int64_t)blockIdx.x * E + el;
+  const int m_gather = a.A * a.cseg;
+  const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;
+  const int64_t total = (int64_t)m_rows * a.c_out;
+  const int el = threadIdx.x % E, grpi = threadIdx.x / E;
+  const int64_t t = (int64_t)((int)blockIdx.x - grp.blk_beg[l]) * E + el;
   int m = 0, n = 0;
   float s = 0.f;
   if (t < total) {
-    m = (int)(t / c_out);
-    n = (int)(t - (int64_t)m * c_out);
-    for (int ch = grp; ch < nchunks; ch += G) s += part[((int64_t)ch * Mpad + m) * Npad + n];
+    m = (int)(t / a.c_out);
+    n = (int)(t - (int64_t)m * a.c_out);
+    const float* part = a.part;
+    for (int ch = grpi; ch < a.nchunks; ch += G) s += part[((int64_t)ch * a.Mpad + m) * a.Npad + n];
   }
   red[threadIdx.x] = s;
   __syncthreads();
-  if (grp != 0 || t >= total) return;
+  if (grpi != 0 || t >= total) return;
   s = 0.f;
   for (int g = 0; g < G; ++g) s += red[g * E + el];
   if (m < m_gather) {
-    const int f = m / cseg, c = m - f * cseg;
-    if (c < c_in) dW[((int64_t)f * c_in + c) * c_out + n] = s;
-  } else if (m == m_ones) {
-    if (db) db[n] = s;
+    const int f = m / a.cseg, c = m - f * a.cseg;
+    if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + n] = s;
+  } else if (m == a.m_ones) {
+    if (a.db) a.db[n] = s;
   }
 }
 
@@ -577,35 +589,49 @@ GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K) {
   return p;
 }
 
-hipError_t launch_wgrad(bool bf16, const WGradArgs& a, hipStream_t st) {
-  // a.cfg: 0 = 128 x 128 tiles, 1 = 128 x 64
-  const int BN = a.cfg == 0 ? 128 : 64;
-  const int64_t tiles = (int64_t)(a.Mpad / 128) * (a.Npad / BN) * a.nchunks;
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit());
+hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st) {
+  // cfg: 0 = 128 x 128 tiles, 1 = 128 x 64
+  if (n < 1 || n > MAX_WG_LAYERS) return hipErrorInvalidValue;
+  const int BN = cfg == 0 ? 128 : 64;
+  WGradGroup g{};
+  g.n = n;
+  g.tile_beg[0] = 0;
+  for (int l = 0; l < n; ++l) {
+    g.L[l] = layers[l];
+    g.tile_beg[l + 1] = g.tile_beg[l] + (layers[l].Mpad / 128) * (layers[l].Npad / BN) * layers[l].nchunks;
+  }
+  const int grid = std::min(std::max(g.tile_beg[n], 1), device_grid_limit());
   if (bf16) {
-    if (a.cfg == 0)
-      hipLaunchKernelGGL((k_wgrad<__bf16, C128x128<__bf16>>), dim3(grid), dim3(256), 0, st, a);
+    if (cfg == 0)
+      hipLaunchKernelGGL((k_wgrad<__bf16, C128x128<__bf16>>), dim3(grid), dim3(256), 0, st, g);
     else
-      hipLaunchKernelGGL((k_wgrad<__bf16, C128x64<__bf16>>), dim3(grid), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((k_wgrad<__bf16, C128x64<__bf16>>), dim3(grid), dim3(256), 0, st, g);
   } else {
-    if (a.cfg == 0)
-      hipLaunchKernelGGL((k_wgrad<float, C128x128<float>>), dim3(grid), dim3(256), 0, st, a);
+    if (cfg == 0)
+      hipLaunchKernelGGL((k_wgrad<float, C128x128<float>>), dim3(grid), dim3(256), 0, st, g);
     else
-      hipLaunchKernelGGL((k_wgrad<float, C128x64<float>>), dim3(grid), dim3(256), 0, st, a);
+      hipLaunchKernelGGL((k_wgrad<float, C128x64<float>>), dim3(grid), dim3(256), 0, st, g);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_wgrad_reduce(const float* part, int32_t nchunks, int32_t Mpad, int32_t Npad, int32_t A, int32_t cseg,
-                               int32_t c_in, int32_t c_out, int32_t m_ones, float* dW, float* db, hipStream_t st) {
-  if (nchunks <= 1) return hipSuccess;  // the weight-gradient kernel wrote the results
-  const int m_rows = m_ones >= 0 ? m_ones + 1 : A * cseg;
-  const int64_t total = (int64_t)m_rows * c_out;
-  const int G = nchunks >= 16 ? 16 : (nchunks >= 8 ? 8 : (nchunks >= 4 ? 4 : 2));
-  const int E = 256 / G;
-  const int grid = (int)std::max<int64_t>(1, (total + E - 1) / E);
-  hipLaunchKernelGGL(k_wgrad_reduce, dim3(grid), dim3(256), 0, st, part, nchunks, Mpad, Npad, A, cseg, c_in, c_out,
-                     m_ones, dW, db, G);
+hipError_t launch_wgrad_reduce(const WGradArgs* layers, int n, hipStream_t st) {
+  WGradGroup g{};
+  g.blk_beg[0] = 0;
+  for (int l = 0; l < n; ++l) {
+    const WGradArgs& a = layers[l];
+    if (a.nchunks <= 1) continue;  // the weight-gradient kernel wrote the results
+    const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : a.A * a.cseg;
+    const int64_t total = (int64_t)m_rows * a.c_out;
+    const int G = a.nchunks >= 16 ? 16 : (a.nchunks >= 8 ? 8 : (a.nchunks >= 4 ? 4 : 2));
+    const int E = 256 / G;
+    g.L[g.n] = a;
+    g.G[g.n] = G;
+    g.blk_beg[g.n + 1] = g.blk_beg[g.n] + (int)((total + E - 1) / E);
+    ++g.n;
+  }
+  if (g.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_wgrad_reduce, dim3(g.blk_beg[g.n]), dim3(256), 0, st, g);
   return hipGetLastError();
 }
 

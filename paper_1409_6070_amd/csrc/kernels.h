@@ -100,6 +100,16 @@ struct WGradArgs {
   int32_t c_in, c_out;
 };
 
+// Weight gradients of several layers in one launch (all with the same tile).
+constexpr int MAX_WG_LAYERS = MAX_LAYERS / 2 + 2;  // convolutions + softmax layer
+struct WGradGroup {
+  int32_t n;
+  int32_t tile_beg[MAX_WG_LAYERS + 1];  // workgroup tiles of layer l: [tile_beg[l], tile_beg[l+1])
+  int32_t blk_beg[MAX_WG_LAYERS + 1];   // reduce blocks of layer l
+  int32_t G[MAX_WG_LAYERS];             // reduce thread groups of layer l
+  WGradArgs L[MAX_WG_LAYERS];
+};
+
 struct GemmTile {
   int BM, BN, BK;
 };
@@ -110,11 +120,13 @@ constexpr int WG_BM = 128;
 inline int wgrad_bn(int c_out) { return (c_out + 127) / 128 * 128 <= (c_out + 63) / 64 * 64 ? 128 : 64; }
 
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st);
-hipError_t launch_wgrad(bool bf16, const WGradArgs& a, hipStream_t st);
+// Weight gradients of n layers that all use tile shape cfg (0: 128 x 128,
+// 1: 128 x 64) in one launch.
+hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st);
 
-// part -> dW [A*c_in x c_out] (and db [c_out] when m_ones >= 0)
-hipError_t launch_wgrad_reduce(const float* part, int32_t nchunks, int32_t Mpad, int32_t Npad, int32_t A, int32_t cseg,
-                               int32_t c_in, int32_t c_out, int32_t m_ones, float* dW, float* db, hipStream_t st);
+// part -> dW [A*c_in x c_out] (and db [c_out] when m_ones >= 0) for every layer
+// of the list with nchunks > 1, in one launch.
+hipError_t launch_wgrad_reduce(const WGradArgs* layers, int n, hipStream_t st);
 // grad_in[0][c] = sum_f sum_n W[(f*c_in + c)*c_out + n] * D0[f][n]
 hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, int32_t c_in, int32_t c_out,
                           int32_t cp_in, void* grad_in, hipStream_t st);

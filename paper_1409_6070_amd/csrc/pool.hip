@@ -174,7 +174,7 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
 #pragma unroll
     for (int j = 0; j < VE; ++j) acc[j] = 0.f;
     if (active) {
-#pragma unroll 2
+#pragma unroll 4
       for (int o = o_beg + rl; o < o_end; o += lanes) {
         const i32x4 r = *(const i32x4*)(g.Rp + (int64_t)o * 4);
         const AW am = *(const AW*)(g.argmax + (int64_t)o * g.stride + c);
@@ -201,7 +201,7 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
 #pragma unroll
     for (int j = 0; j < VE; ++j) acc[k][j] = 0.f;
   if (active) {
-#pragma unroll 2
+#pragma unroll 4
     for (int i = i_beg + rl; i < i_end; i += lanes) {
       const u32x4 gv = *(const u32x4*)(dZ + (int64_t)i * g.stride + c);
       int gnd[AC > 0 ? AC : 1];
@@ -234,18 +234,26 @@ __global__ void __launch_bounds__(256) k_ground_final(GroundArgs g) {
   const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (c >= g.cp) return;
   const bool pool = g.B1 > 0;
+  // every slot's loads of one step issued together (slot 0 has B1 partials,
+  // the others B2)
   float tot[2 + AC];
 #pragma unroll
-  for (int k = 0; k < 2 + AC; ++k) {
-    const int np = k == 0 ? g.B1 : g.B2;
-    const float* pp = g.part + ((int64_t)k * g.cp + c) * g.PM;
-    float s = 0.f;
-#pragma unroll 4
-    for (int p = lane; p < np; p += 64) s += pp[p];
+  for (int k = 0; k < 2 + AC; ++k) tot[k] = 0.f;
+  const float* pc = g.part + (int64_t)c * g.PM;
+  const int64_t slot = (int64_t)g.cp * g.PM;
+  const int npm = max(g.B1, g.B2);
+#pragma unroll 2
+  for (int p = lane; p < npm; p += 64) {
+    if (p < g.B1) tot[0] += pc[p];
+    if (p < g.B2) {
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-    tot[k] = s;
+      for (int k = 1; k < 2 + AC; ++k) tot[k] += pc[k * slot + p];
+    }
   }
+#pragma unroll
+  for (int k = 0; k < 2 + AC; ++k)
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) tot[k] += __shfl_xor(tot[k], off);
   if (lane != 0) return;
   T* dZ = (T*)g.dZ;
   float z0;
