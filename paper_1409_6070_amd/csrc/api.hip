@@ -482,22 +482,24 @@ static int ground_parts(const sscn_net* net, int64_t rows, int cp) {
   return (int)std::min<int64_t>(net->pool_parts, std::max<int64_t>(1, (rows + 8 * lanes - 1) / (8 * lanes)));
 }
 
+// Blocks of the fused pooling backward over `rows` pooling rows: one row per
+// thread and at most 512 blocks (more rows per thread beyond that).
+static int pool_bwd_blocks(const sscn_net* net, int64_t rows, int cp) {
+  const int lanes = 256 / (cp / (net->bf16 ? 8 : 4));
+  return (int)std::min<int64_t>(std::min(512, net->pool_parts), std::max<int64_t>(1, (rows + lanes - 1) / lanes));
+}
+
 // Whether the backward pass needs row 0 of the gradient below convolution s
 // (the ground row of its input): always above the first layer; for the first,
 // only when the caller asks for the input-feature gradient, which its
 // layer view then holds in full.
 static bool needs_row0(const sscn_net* net, int s) { return s > 1 || net->want_dfeats; }
 
-// Row 0 of convolution s's output gradient delta (when pooling layer s+1 sits
-// above it: pool_above), its bias gradient and ground-row sums, then row 0 of
-// the gradient below it.  Needs delta rows >= 1 and, with pool_above, layer
-// s+1's gradient in full.
-static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_t st) {
+// Bias / ground-row reduction arguments of convolution s (pool_above: pooling
+// layer s+1 sits on it and routes its gradient; its windows give slot 0).
+static GroundArgs ground_args(const sscn_net* net, int s, bool pool_above) {
   const LayerPlan& L = net->L[s];
-  const LayerPlan& Lb = net->L[s - 1];
   const int ci = L.conv_index;
-  const ParamPlan& P = net->P[ci];
-  const bool row0 = needs_row0(net, s);
   GroundArgs g{};
   if (pool_above) {
     const LayerPlan& Lp = net->L[s + 1];
@@ -505,13 +507,15 @@ static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_
     g.argmax = Lp.argmax;
     g.Rp = Lp.rules;
     g.n_pool = net->counts + s + 1;
-    g.B1 = ground_parts(net, Lp.cap, Lp.Cp);
+    g.B1 = pool_bwd_blocks(net, Lp.cap, Lp.Cp);
+    g.B2 = g.B1;  // one pass: the fused pooling backward
     g.Y_below = L.X;
+  } else {
+    g.B2 = ground_parts(net, L.cap, L.Cp);
   }
   g.dZ = L.grad;
   g.R = L.rules;
   g.n_rows = net->counts + s;
-  g.B2 = ground_parts(net, L.cap, L.Cp);
   g.stride = L.Cp;
   g.cp = L.Cp;
   g.c_out = L.C;
@@ -519,9 +523,23 @@ static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_
   g.PM = net->pool_parts;
   g.db = net->db[ci];
   g.D0 = net->D0;
+  return g;
+}
+
+// Row 0 of convolution s's output gradient delta (with a pooling layer above:
+// its fused backward has written the partial sums), the bias gradient and the
+// ground-row sums, then row 0 of the gradient below.
+static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_t st) {
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lb = net->L[s - 1];
+  const int ci = L.conv_index;
+  const ParamPlan& P = net->P[ci];
+  const bool row0 = needs_row0(net, s);
+  const GroundArgs g = ground_args(net, s, pool_above);
   hipError_t e;
-  if ((e = timed(net, SSCN_KC_GROUND, st, [&] { return launch_ground(net->bf16, g, row0 ? L.A : 0, st); })) !=
-      hipSuccess)
+  if ((e = timed(net, SSCN_KC_GROUND, st, [&] {
+         return launch_ground(net->bf16, g, row0 ? L.A : 0, pool_above ? 2 : 0, st);
+       })) != hipSuccess)
     return e;
   if (!row0) return hipSuccess;
   return timed(net, SSCN_KC_GROUND, st, [&] {
@@ -575,17 +593,20 @@ static hipError_t run_wgrads(sscn_net* net, const WGradArgs* w, int n, hipStream
   return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] { return launch_wgrad_reduce(w, n, st); });
 }
 
-// Rows >= 1 of the gradient below stage s: pooling routing, or the input-gradient
-// GEMM of a convolution.  (The GEMM reads delta rows >= 1 only: a window list
-// entry of -1 selects zero, whatever its load of row 0 returned.)
+// Rows >= 1 of the gradient below stage s: the pooling backward (with the
+// partial sums of the convolution below), or the input-gradient GEMM of a
+// convolution.  (The GEMM reads delta rows >= 1 only: a window list entry of -1
+// selects zero, whatever its load of row 0 returned.)
 static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
-  if (L.kind == 2)
-    return timed(net, SSCN_KC_POOL_BWD, st, [&] {
-      return launch_pool_route(net->bf16, L.grad, L.Cp, L.argmax, L.rules_t, Lb.X, Lb.grad, L.Cp,
-                               net->counts + s - 1, Lb.cap, st);
-    });
+  if (L.kind == 2) {
+    // rows >= 1 below with the partial sums of the convolution below
+    if (Lb.kind != 1) return hipErrorInvalidValue;  // a pooling layer sits on a convolution
+    const GroundArgs g = ground_args(net, s - 1, true);
+    const int Ac = needs_row0(net, s - 1) ? Lb.A : 0;
+    return timed(net, SSCN_KC_POOL_BWD, st, [&] { return launch_ground(net->bf16, g, Ac, 1, st); });
+  }
   if (!(s > 1 || net->want_dfeats)) return hipSuccess;
   const ParamPlan& P = net->P[L.conv_index];
   GemmArgs g{};

@@ -37,26 +37,48 @@ __global__ void __launch_bounds__(256) k_gather_dfeats(const T* __restrict__ gra
   }
 }
 
-// All weight packings of a step in one launch: blockIdx.y selects the job.
+// All weight packings of a step in one launch: blockIdx.y selects the job,
+// blockIdx.x a tile of 64 n x 32 k of its output.
 //   mode 0 (forward):   Bt[n][f*cp_in + c]  = W[(f*c_in + c)*c_out + n]
+//     a transpose: the tile's 32 source rows are read along n (coalesced) into
+//     LDS and written out along k;
 //   mode 1 (backward):  Bt[c][f*cp_out + n] = W[(f*c_in + c)*c_out + n]
+//     row segments: read and written along n.
+// Entries outside the weight (padding) are zero.
+constexpr int PACK_N = 64, PACK_K = 32;
 template <typename T>
 __global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
+  __shared__ T tile[PACK_K][PACK_N + 2];
   const PackJob& j = pa.job[blockIdx.y];
   const T* W = (const T*)j.W;
   T* Bt = (T*)j.Bt;
-  const int64_t total = (int64_t)j.Npad * j.Kpad;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
-    const int n = (int)(t / j.Kpad), k = (int)(t - (int64_t)n * j.Kpad);
-    T v = Elem<T>::from_f32(0.f);
+  const int tiles_k = j.Kpad / PACK_K;
+  const int ntiles = (j.Npad / PACK_N) * tiles_k;
+  const T zero = Elem<T>::from_f32(0.f);
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int n0 = (t / tiles_k) * PACK_N, k0 = (t % tiles_k) * PACK_K;
     if (j.mode == 0) {
-      const int f = k / j.cp_in, c = k - f * j.cp_in;
-      if (n < j.c_out && f < j.A && c < j.c_in) v = W[((int64_t)f * j.c_in + c) * j.c_out + n];
+      for (int i = threadIdx.x; i < PACK_K * PACK_N; i += 256) {
+        const int kk = i / PACK_N, nn = i % PACK_N;
+        const int k = k0 + kk, n = n0 + nn;
+        const int f = k / j.cp_in, c = k - f * j.cp_in;
+        tile[kk][nn] = (f < j.A && c < j.c_in && n < j.c_out) ? W[((int64_t)f * j.c_in + c) * j.c_out + n] : zero;
+      }
+      __syncthreads();
+      for (int i = threadIdx.x; i < PACK_N * PACK_K; i += 256) {
+        const int nn = i / PACK_K, kk = i % PACK_K;
+        Bt[(int64_t)(n0 + nn) * j.Kpad + k0 + kk] = tile[kk][nn];
+      }
+      __syncthreads();
     } else {
-      const int f = k / j.cp_out, o = k - f * j.cp_out;
-      if (n < j.c_in && f < j.A && o < j.c_out) v = W[((int64_t)f * j.c_in + n) * j.c_out + o];
+      for (int i = threadIdx.x; i < PACK_N * PACK_K; i += 256) {
+        const int nn = i / PACK_K, kk = i % PACK_K;
+        const int c = n0 + nn, k = k0 + kk;
+        const int f = k / j.cp_out, o = k - f * j.cp_out;
+        Bt[(int64_t)c * j.Kpad + k] =
+            (f < j.A && o < j.c_out && c < j.c_in) ? W[((int64_t)f * j.c_in + c) * j.c_out + o] : zero;
+      }
     }
-    Bt[t] = v;
   }
 }
 
@@ -193,9 +215,14 @@ hipError_t launch_gather_dfeats(bool bf16, const void* grad0, int32_t cp0, const
 
 hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st) {
   int64_t most = 0;
-  for (int i = 0; i < pa.njobs; ++i) most = std::max<int64_t>(most, (int64_t)pa.job[i].Npad * pa.job[i].Kpad);
+  for (int i = 0; i < pa.njobs; ++i) {
+    const PackJob& j = pa.job[i];
+    // GEMM padding: N to a multiple of 64, K to a multiple of 32
+    if (j.Npad % PACK_N || j.Kpad % PACK_K) return hipErrorInvalidValue;
+    most = std::max<int64_t>(most, (int64_t)(j.Npad / PACK_N) * (j.Kpad / PACK_K));
+  }
   if (pa.njobs <= 0 || most <= 0) return hipSuccess;
-  const int gx = (int)std::max<int64_t>(1, std::min<int64_t>((most + 255) / 256, 512));
+  const int gx = (int)std::max<int64_t>(1, std::min<int64_t>(most, 256));
   if (bf16)
     hipLaunchKernelGGL(k_pack_all<__bf16>, dim3(gx, pa.njobs), dim3(256), 0, st, pa);
   else

@@ -137,12 +137,6 @@ hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, 
 hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const int32_t* R, void* X_out,
                            int32_t stride_out, uint8_t* argmax, int32_t cp, const int32_t* n_out, int64_t cap_out,
                            hipStream_t st);
-// Pooling backward, rows >= 1 below: grad_below[i] = dY[Pt[i] / 4] where the
-// window's maximum came from position Pt[i] % 4 and Y_below[i] > 0, else 0.
-hipError_t launch_pool_route(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
-                             const void* Y_below, void* grad_below, int32_t cp, const int32_t* n_in, int64_t cap_in,
-                             hipStream_t st);
-
 // Bias gradient db [c_out] and ground-row sums D0 [AC x c_out] (AC in {0, 1, 4,
 // 9}) of a convolution with output gradient delta = dZ, and, with a pooling
 // layer above (B1 > 0), row 0 of delta itself.  Needs delta rows >= 1 and, with
@@ -166,7 +160,12 @@ struct GroundArgs {
   float* db;
   float* D0;
 };
-hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, hipStream_t st);
+// kind 0: partial sums over delta rows >= 1 (and, with B1 > 0, over the pooling
+//         rows), then the final pass;
+// kind 1: pooling backward fused with those partial sums (writes delta rows >= 1;
+//         needs B1 == B2);
+// kind 2: the final pass alone, over partials written by kind 1.
+hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // input, parameters, head

@@ -75,42 +75,6 @@ __global__ void __launch_bounds__(256) k_pool_fwd(const T* __restrict__ X_in, in
   }
 }
 
-// Routing of the output gradient dY of a pooling layer to the rows below: row
-// i >= 1 has one window above, p = Pt[i] = 4 * (row above) + (position of i),
-// and takes dY[p / 4] where that window's maximum came from position p % 4 and
-// the value below passed the ReLU (Y_below[i] > 0); else 0.  The stored
-// result is the output gradient delta of the convolution below, rows >= 1.
-// Row 0 of it needs a reduction (k_ground_sums / k_ground_final).
-template <typename T>
-__global__ void __launch_bounds__(256) k_pool_route(const T* __restrict__ dY, int32_t stride,
-                                                    const uint8_t* __restrict__ argmax, const int32_t* __restrict__ Pt,
-                                                    const T* __restrict__ Y_below, T* grad_below, int32_t cp,
-                                                    const int32_t* n_in_p) {
-  constexpr int VE = Elem<T>::VE;
-  typedef typename ArgPack<VE>::W AW;
-  const int nv = cp / VE;
-  const int64_t total = (int64_t)(*n_in_p) * nv;  // rows 1..n_in
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t i = 1 + t / nv;
-    const int c = (int)(t - (i - 1) * nv) * VE;
-    const int p = Pt[i];
-    const u32x4 y = *(const u32x4*)(Y_below + i * stride + c);
-    u32x4 out = {0u, 0u, 0u, 0u};
-    if (p >= 0) {
-      const int64_t o = p >> 2;
-      const int f = p & 3;
-      const u32x4 g = *(const u32x4*)(dY + o * stride + c);
-      const AW am = *(const AW*)(argmax + o * stride + c);
-#pragma unroll
-      for (int j = 0; j < VE; ++j) {
-        const bool take = ((int)((am >> (8 * j)) & 0xff) == f) && (Elem<T>::to_f32(((const T*)&y)[j]) > 0.f);
-        ((T*)&out)[j] = take ? ((const T*)&g)[j] : Elem<T>::from_f32(0.f);
-      }
-    }
-    *(u32x4*)(grad_below + i * stride + c) = out;
-  }
-}
-
 // Sum over one block's rows, per channel: thread t holds VE channels of vector
 // t % nv; the 256/nv row lanes are combined in LDS in a fixed order; the sum of
 // channel e goes to out[e * PM].
@@ -143,6 +107,77 @@ __device__ inline void ground_flags(const int32_t* __restrict__ R, int64_t i, in
 #pragma unroll
     for (int k = 0; k < AC; ++k) gnd[k] = R[i * AC + k] == 0;
   }
+}
+
+// Pooling backward fused with the sums of the convolution below, one pass over
+// the pooling layer's rows o >= 1 (thread (lane l, channel vector v) of block b
+// takes rows 1 + b*lanes + l, then every gridDim*lanes-th).  For each window
+// position f of row o, with child row i = Rp[o][f]:
+//   i >= 1:  delta[i] = dY[o] where argmax[o] == f and Y_below[i] > 0, else 0
+//            (each row >= 1 below lies in exactly one window: written once),
+//            summed into slot 1 and, where the convolution's window position f'
+//            of row i reads the ground row, into slot 2 + f';
+//   i == 0:  dY[o] where argmax[o] == f is summed into slot 0 (maxima taken from
+//            the ground state).
+// Partial p = block b of slot k, channel c: part[(k * cp + c) * PM + b].
+template <typename T, int AC>
+__global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g) {
+  constexpr int VE = Elem<T>::VE;
+  constexpr int J = 2 + AC;
+  typedef typename ArgPack<VE>::W AW;
+  __shared__ float red[256 * VE];
+  const int nv = g.cp / VE;
+  const int lanes = 256 / nv;
+  const int t = threadIdx.x;
+  const int v = t % nv, rl = t / nv;
+  const int c = v * VE;
+  const T* dY = (const T*)g.dY;
+  const T* Yb = (const T*)g.Y_below;
+  T* dZ = (T*)g.dZ;
+  const int n = *g.n_pool;
+  float acc[J][VE];
+#pragma unroll
+  for (int k = 0; k < J; ++k)
+#pragma unroll
+    for (int j = 0; j < VE; ++j) acc[k][j] = 0.f;
+  if (rl < lanes) {
+#pragma unroll 2
+    for (int o = 1 + blockIdx.x * lanes + rl; o <= n; o += gridDim.x * lanes) {
+      const i32x4 r = *(const i32x4*)(g.Rp + (int64_t)o * 4);
+      const AW am = *(const AW*)(g.argmax + (int64_t)o * g.stride + c);
+      const u32x4 gv = *(const u32x4*)(dY + (int64_t)o * g.stride + c);
+#pragma unroll
+      for (int f = 0; f < 4; ++f) {
+        const int i = r[f];
+        if (i == 0) {
+#pragma unroll
+          for (int j = 0; j < VE; ++j)
+            acc[0][j] += ((int)((am >> (8 * j)) & 0xff) == f) ? Elem<T>::to_f32(((const T*)&gv)[j]) : 0.f;
+        } else {
+          const u32x4 y = *(const u32x4*)(Yb + (int64_t)i * g.stride + c);
+          int gnd[AC > 0 ? AC : 1];
+          ground_flags<AC>(g.R, i, gnd);
+          u32x4 out;
+#pragma unroll
+          for (int j = 0; j < VE; ++j) {
+            const bool take = ((int)((am >> (8 * j)) & 0xff) == f) && (Elem<T>::to_f32(((const T*)&y)[j]) > 0.f);
+            ((T*)&out)[j] = take ? ((const T*)&gv)[j] : Elem<T>::from_f32(0.f);
+          }
+          *(u32x4*)(dZ + (int64_t)i * g.stride + c) = out;
+#pragma unroll
+          for (int j = 0; j < VE; ++j) {
+            const float d = Elem<T>::to_f32(((const T*)&out)[j]);
+            acc[1][j] += d;
+#pragma unroll
+            for (int k = 0; k < AC; ++k) acc[2 + k][j] += gnd[k] ? d : 0.f;
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < J; ++k)
+    block_channel_sums<VE>(acc[k], red, nv, g.cp, g.part + (int64_t)k * g.cp * g.PM + blockIdx.x, g.PM);
 }
 
 // Partial sums behind a convolution's bias gradient and ground-row sums, and
@@ -220,9 +255,10 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
     block_channel_sums<VE>(acc[k], red, nv, g.cp, g.part + (int64_t)(1 + k) * g.cp * g.PM + b, g.PM);
 }
 
-// Final pass: one wavefront per channel c sums each slot's partials (lane l
-// takes partials l, l+64, ...; then a butterfly over the 64 lanes, the same
-// order every run), and lane 0 finishes:
+// Final pass: one block per channel c; its 4 wavefronts sum each slot's
+// partials (lane l of wave w takes partials 64w + l, then every 256th), each
+// wave reduces with a butterfly over its 64 lanes and the 4 wave sums are added
+// in a fixed order (the same every run); thread 0 finishes:
 //   with a pooling layer above, row 0 of delta is
 //     z0 = mask(Y_below[0][c]) * (dY[0][c] + slot 0), written to delta[0][c];
 //   without one, z0 = delta[0][c] as stored;
@@ -230,12 +266,10 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
 //   at every window position), for c < c_out.
 template <typename T, int AC>
 __global__ void __launch_bounds__(256) k_ground_final(GroundArgs g) {
-  const int lane = threadIdx.x & 63;
-  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (c >= g.cp) return;
+  __shared__ float wsum[4][2 + AC];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x;
   const bool pool = g.B1 > 0;
-  // every slot's loads of one step issued together (slot 0 has B1 partials,
-  // the others B2)
   float tot[2 + AC];
 #pragma unroll
   for (int k = 0; k < 2 + AC; ++k) tot[k] = 0.f;
@@ -243,7 +277,7 @@ __global__ void __launch_bounds__(256) k_ground_final(GroundArgs g) {
   const int64_t slot = (int64_t)g.cp * g.PM;
   const int npm = max(g.B1, g.B2);
 #pragma unroll 2
-  for (int p = lane; p < npm; p += 64) {
+  for (int p = threadIdx.x; p < npm; p += 256) {
     if (p < g.B1) tot[0] += pc[p];
     if (p < g.B2) {
 #pragma unroll
@@ -251,10 +285,15 @@ __global__ void __launch_bounds__(256) k_ground_final(GroundArgs g) {
     }
   }
 #pragma unroll
-  for (int k = 0; k < 2 + AC; ++k)
+  for (int k = 0; k < 2 + AC; ++k) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) tot[k] += __shfl_xor(tot[k], off);
-  if (lane != 0) return;
+    if (lane == 0) wsum[w][k] = tot[k];
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+#pragma unroll
+  for (int k = 0; k < 2 + AC; ++k) tot[k] = ((wsum[0][k] + wsum[1][k]) + wsum[2][k]) + wsum[3][k];
   T* dZ = (T*)g.dZ;
   float z0;
   if (pool) {
@@ -288,29 +327,20 @@ hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const
   return hipGetLastError();
 }
 
-hipError_t launch_pool_route(bool bf16, const void* dY, int32_t stride, const uint8_t* argmax, const int32_t* Pt,
-                             const void* Y_below, void* grad_below, int32_t cp, const int32_t* n_in, int64_t cap_in,
-                             hipStream_t st) {
-  const int VE = bf16 ? 8 : 4;
-  const int grid = grid_for(cap_in * (cp / VE));
-  if (bf16)
-    hipLaunchKernelGGL(k_pool_route<__bf16>, dim3(grid), dim3(256), 0, st, (const __bf16*)dY, stride, argmax, Pt,
-                       (const __bf16*)Y_below, (__bf16*)grad_below, cp, n_in);
-  else
-    hipLaunchKernelGGL(k_pool_route<float>, dim3(grid), dim3(256), 0, st, (const float*)dY, stride, argmax, Pt,
-                       (const float*)Y_below, (float*)grad_below, cp, n_in);
-  return hipGetLastError();
-}
-
+// kind 0: sums over delta rows (and pooling rows), then the final pass;
+// kind 1: the fused pooling backward (B1 == B2 blocks), then the final pass;
+// kind 2: the final pass alone (partials already written).
 template <typename T, int AC>
-static void launch_ground_t(const GroundArgs& g, hipStream_t st) {
-  hipLaunchKernelGGL((k_ground_sums<T, AC>), dim3(g.B1 + g.B2), dim3(256), 0, st, g);
-  hipLaunchKernelGGL((k_ground_final<T, AC>), dim3((g.cp + 3) / 4), dim3(256), 0, st, g);
+static void launch_ground_t(const GroundArgs& g, int kind, hipStream_t st) {
+  if (kind == 0) hipLaunchKernelGGL((k_ground_sums<T, AC>), dim3(g.B1 + g.B2), dim3(256), 0, st, g);
+  if (kind == 1) hipLaunchKernelGGL((k_pool_bwd<T, AC>), dim3(g.B2), dim3(256), 0, st, g);
+  if (kind != 1) hipLaunchKernelGGL((k_ground_final<T, AC>), dim3(g.cp), dim3(256), 0, st, g);
 }
 
-hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, hipStream_t st) {
+hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, hipStream_t st) {
   if (g.B2 < 1 || g.B1 < 0 || g.B1 > g.PM || g.B2 > g.PM) return hipErrorInvalidValue;
-#define SSCN_GROUND(T, A) launch_ground_t<T, A>(g, st)
+  if (kind == 1 && g.B1 != g.B2) return hipErrorInvalidValue;
+#define SSCN_GROUND(T, A) launch_ground_t<T, A>(g, kind, st)
   if (bf16) {
     switch (AC) {
       case 0: SSCN_GROUND(__bf16, 0); break;
