@@ -68,6 +68,7 @@ struct sscn_net {
   ParamPlan P[MAX_LAYERS];
   int dl_stride;  // dlogits row stride (elements)
   int pool_parts;
+  int wgrad_slabs;
   // global workspace pointers
   int32_t* counts;
   int32_t* err;
@@ -194,15 +195,14 @@ static void set_plan(GemmArgs& g, const GemmPlan& p, int64_t rows_cap, float* gp
   g.part_rows = (int32_t)rows_cap;
 }
 
-// Site chunks of a split-K weight gradient: about 256 workgroups per layer (the
-// layers of a step share one launch), at least 4
-// slabs of sites each, and partial sums (chunks x |dW| fp32) of at most twice the
-// bytes the kernel reads (rows x row_bytes).
-static int wgrad_chunks(int64_t rows_cap, int tiles_mn, int BK, int64_t row_bytes, int64_t part_bytes) {
-  int64_t max_chunks = std::max<int64_t>(1, std::min<int64_t>(512, (rows_cap + 4 * BK - 1) / (4 * BK)));
-  max_chunks = std::min<int64_t>(max_chunks, std::max<int64_t>(1, 2 * rows_cap * row_bytes / std::max<int64_t>(part_bytes, 1)));
-  int64_t want = std::max<int64_t>(1, (256 + tiles_mn - 1) / tiles_mn);
-  return (int)std::min<int64_t>(want, max_chunks);
+// Most site chunks of a split-K weight gradient (the partial buffers hold that
+// many): slabs x BK sites per chunk at the row capacity, at most 512, and
+// partial sums (chunks x |dW| fp32) of at most twice the bytes the kernel reads
+// (rows x row_bytes).  The kernel takes min(this, rows / (slabs x BK)) from the
+// device-side row count.
+static int wgrad_chunks(int64_t rows_cap, int slabs, int BK, int64_t row_bytes, int64_t part_bytes) {
+  int64_t n = std::max<int64_t>(1, std::min<int64_t>(512, (rows_cap + slabs * BK - 1) / (slabs * BK)));
+  return (int)std::min<int64_t>(n, std::max<int64_t>(1, 2 * rows_cap * row_bytes / std::max<int64_t>(part_bytes, 1)));
 }
 
 extern "C" {
@@ -241,6 +241,7 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   net->nlayers = 2 * d.ell + 2;
   net->nparams = d.ell + 2;
   net->pool_parts = 1024;  // most row blocks per slot of a bias / ground-row reduction
+  net->wgrad_slabs = 8;    // slabs of sites per weight-gradient workgroup
   const int BK = net->bf16 ? 64 : 32;
   const int VE = net->VE;
   auto cp = [VE](int c) { return (int)round_up(c, VE); };
@@ -320,7 +321,7 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
       const int m_rows = P.A * P.cp_in;
       const int64_t row_bytes = (int64_t)(P.A * P.cp_in + P.cp_out) * net->esz;
       const int64_t part_bytes = (int64_t)m_rows * P.Npad_w * 4;
-      P.nchunks = wgrad_chunks(L[s].cap + 1, (P.Mpad_w / WG_BM) * (P.Npad_w / P.bn_w), BK, row_bytes, part_bytes);
+      P.nchunks = wgrad_chunks(L[s].cap + 1, net->wgrad_slabs, BK, row_bytes, part_bytes);
     }
   }
   {
@@ -568,6 +569,7 @@ static WGradArgs conv_wgrad_args(const sscn_net* net, int s) {
   w.rows_dev = net->counts + s;
   w.rows_add = 1;
   w.nchunks = P.nchunks;
+  w.slabs = net->wgrad_slabs;
   w.part = net->wpart + P.part_off;
   w.cfg = P.bn_w == 128 ? 0 : 1;
   w.dW = net->dW[ci];
@@ -590,7 +592,7 @@ static hipError_t run_wgrads(sscn_net* net, const WGradArgs* w, int n, hipStream
                  hipSuccess)
       return e;
   }
-  return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] { return launch_wgrad_reduce(w, n, st); });
+  return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] { return launch_wgrad_reduce(net->bf16, w, n, st); });
 }
 
 // Rows >= 1 of the gradient below stage s: the pooling backward (with the
@@ -771,6 +773,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
     f.Npad = P.Npad_w;
     f.rows_host = net->batch;
     f.nchunks = 1;
+    f.slabs = 1;
     f.part = net->wpart;
     f.cfg = P.bn_w == 128 ? 0 : 1;
     f.dW = h_dW[fc];

@@ -323,6 +323,13 @@ struct Quad<float> {
   }
 };
 
+// Site chunks actually used: slabs of BK sites per chunk as planned, at most
+// the planned (capacity) chunk count, from the device-side row count.
+__device__ inline int wgrad_chunks_dev(const WGradArgs& a, int rows, int BK) {
+  const int want = (rows + a.slabs * BK - 1) / (a.slabs * BK);
+  return max(1, min(a.nchunks, want));
+}
+
 // Weight-gradient GEMM, split over sites (the K dimension).  A^T and delta^T
 // slabs are staged in LDS as [row of dW / col of dW][site]: each thread loads
 // 16-byte vectors (VE consecutive channels) of 4 consecutive sites and stores
@@ -359,7 +366,8 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp) {
     const int tile = t - grp.tile_beg[l];
     const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
     const int tiles_m = a.Mpad / BM, tiles_n = a.Npad / BN;
-    const int per = ((rows + a.nchunks - 1) / a.nchunks + BK - 1) / BK * BK;
+    const int nch = wgrad_chunks_dev(a, rows, BK);
+    const int per = ((rows + nch - 1) / nch + BK - 1) / BK * BK;
     const int m_gather = a.A * a.cseg;
     const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;  // rows of dW / db that are read back
     const T* src = (const T*)a.src;
@@ -368,6 +376,7 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp) {
     const int tq = tile / tiles_n;
     const int tm = tq % tiles_m;
     const int chunk = tq / tiles_m;
+    if (chunk >= nch) continue;  // fewer rows than the plan allowed for
     const int m0 = tm * BM, n0 = tn * BN;
     const int o_beg = chunk * per;
     const int o_end = min(rows, o_beg + per);
@@ -453,7 +462,7 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp) {
         for (int r = 0; r < 4; ++r) {
           const int mm = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
           if (mm >= m_rows) continue;
-          if (a.nchunks > 1) {
+          if (nch > 1) {
             part[(int64_t)mm * a.Npad + nn] = acc[i][j][r];
           } else if (nn < a.c_out) {  // single chunk: the sum is final
             if (mm < m_gather) {
@@ -478,6 +487,8 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
   int l = 0;
   while (l + 1 < grp.n && (int)blockIdx.x >= grp.blk_beg[l + 1]) ++l;
   const WGradArgs& a = grp.L[l];
+  const int nch = wgrad_chunks_dev(a, a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host, grp.BK);
+  if (nch <= 1) return;  // the weight-gradient kernel wrote the results
   const int G = grp.G[l];
   const int E = 256 / G;  // outputs per block
   const int m_gather = a.A * a.cseg;
@@ -491,7 +502,7 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
     m = (int)(t / a.c_out);
     n = (int)(t - (int64_t)m * a.c_out);
     const float* part = a.part;
-    for (int ch = grpi; ch < a.nchunks; ch += G) s += part[((int64_t)ch * a.Mpad + m) * a.Npad + n];
+    for (int ch = grpi; ch < nch; ch += G) s += part[((int64_t)ch * a.Mpad + m) * a.Npad + n];
   }
   red[threadIdx.x] = s;
   __syncthreads();
@@ -615,8 +626,9 @@ hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipS
   return hipGetLastError();
 }
 
-hipError_t launch_wgrad_reduce(const WGradArgs* layers, int n, hipStream_t st) {
+hipError_t launch_wgrad_reduce(bool bf16, const WGradArgs* layers, int n, hipStream_t st) {
   WGradGroup g{};
+  g.BK = bf16 ? 64 : 32;
   g.blk_beg[0] = 0;
   for (int l = 0; l < n; ++l) {
     const WGradArgs& a = layers[l];

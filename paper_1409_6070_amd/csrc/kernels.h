@@ -91,7 +91,8 @@ struct WGradArgs {
   const int32_t* rows_dev;
   int32_t rows_add;
   int32_t rows_host;
-  int32_t nchunks;
+  int32_t nchunks;  // planned (most) site chunks; partials hold that many
+  int32_t slabs;    // slabs of sites per chunk: chunks = min(nchunks, rows / (slabs * BK))
   float* part;
   int32_t cfg;  // 0: 128 x 128 tiles, 1: 128 x 64 tiles
   // with nchunks == 1 the kernel writes the results itself (no partials):
@@ -107,6 +108,7 @@ struct WGradGroup {
   int32_t tile_beg[MAX_WG_LAYERS + 1];  // workgroup tiles of layer l: [tile_beg[l], tile_beg[l+1])
   int32_t blk_beg[MAX_WG_LAYERS + 1];   // reduce blocks of layer l
   int32_t G[MAX_WG_LAYERS];             // reduce thread groups of layer l
+  int32_t BK;                           // sites per slab
   WGradArgs L[MAX_WG_LAYERS];
 };
 
@@ -126,7 +128,7 @@ hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipS
 
 // part -> dW [A*c_in x c_out] (and db [c_out] when m_ones >= 0) for every layer
 // of the list with nchunks > 1, in one launch.
-hipError_t launch_wgrad_reduce(const WGradArgs* layers, int n, hipStream_t st);
+hipError_t launch_wgrad_reduce(bool bf16, const WGradArgs* layers, int n, hipStream_t st);
 // grad_in[0][c] = sum_f sum_n W[(f*c_in + c)*c_out + n] * D0[f][n]
 hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, int32_t c_in, int32_t c_out,
                           int32_t cp_in, void* grad_in, hipStream_t st);
