@@ -121,6 +121,25 @@ static hipEvent_t next_event(sscn_net* net) {
 }
 
 // Runs one launcher call; when its class is being timed, brackets it with two events.
+// A gather-GEMM launch; while its class is timed, the kernels themselves record
+// the start and end events (the span of the GEMM kernel and its split-K reduce,
+// without the dispatch latency that events recorded around the launch include).
+static hipError_t timed_gemm(sscn_net* net, GemmArgs g, int64_t max_rows, hipStream_t st) {
+  g.t_start = g.t_stop = nullptr;
+  hipEvent_t a = nullptr, b = nullptr;
+  if ((net->tmask & (1u << SSCN_KC_GATHER_GEMM)) && net->recs.size() < MAX_TIMED && max_rows - g.row_begin > 0) {
+    a = next_event(net);
+    b = next_event(net);
+    if (a && b) {
+      g.t_start = a;
+      g.t_stop = b;
+    }
+  }
+  const hipError_t e = launch_gemm(net->bf16, g, max_rows, st);
+  if (g.t_start && e == hipSuccess) net->recs.push_back({SSCN_KC_GATHER_GEMM, a, b});
+  return e;
+}
+
 template <class F>
 static hipError_t timed(sscn_net* net, int cls, hipStream_t st, F&& launch) {
   if (!(net->tmask & (1u << cls)) || net->recs.size() >= MAX_TIMED) return launch();
@@ -469,7 +488,7 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
     g.rows_add = 1;
     g.row_begin = 0;
     set_plan(g, P.pf, P.rows_f, net->gpart);
-    return timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, L.cap + 1, st); });
+    return timed_gemm(net, g, L.cap + 1, st);
   }
   return timed(net, SSCN_KC_POOL_FWD, st, [&] {
     return launch_pool_fwd(net->bf16, Lb.X, Lb.Cp, L.rules, L.X, L.Cp, L.argmax, L.Cp, net->counts + s, L.cap, st);
@@ -631,7 +650,7 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
   g.rows_add = 1;
   g.row_begin = 1;
   set_plan(g, P.pd, P.rows_d, net->gpart);
-  return timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, Lb.cap + 1, st); });
+  return timed_gemm(net, g, Lb.cap + 1, st);
 }
 
 sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
@@ -686,7 +705,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   g.rows_host = net->batch;
   g.row_begin = 0;
   set_plan(g, P.pf, P.rows_f, net->gpart);
-  if (timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, net->batch, st); }) != hipSuccess)
+  if (timed_gemm(net, g, net->batch, st) != hipSuccess)
     return SSCN_ERR_HIP;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_softmax_xent(net->bf16, d_logits, d_labels, net->batch, net->d.n_classes, net->dlogits,
@@ -731,7 +750,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   g.rows_host = net->batch;
   g.row_begin = 0;
   set_plan(g, P.pd, P.rows_d, net->gpart);
-  if (timed(net, SSCN_KC_GATHER_GEMM, st, [&] { return launch_gemm(net->bf16, g, net->batch, st); }) != hipSuccess)
+  if (timed_gemm(net, g, net->batch, st) != hipSuccess)
     return SSCN_ERR_HIP;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp, st);

@@ -19,6 +19,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 namespace sscn {
 
 template <typename T>
@@ -546,11 +548,19 @@ static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   const int64_t span = max_rows - a.row_begin;
   const int64_t tiles = ((span + C::BM - 1) / C::BM) * (a.Npad / C::BN) * a.ksplit;
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit());
-  hipLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a);
+  const bool timed = a.t_start || a.t_stop;
+  if (timed)
+    hipExtLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a.t_start,
+                          a.ksplit > 1 ? nullptr : a.t_stop, 0, a);
+  else
+    hipLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a);
   if (a.ksplit > 1) {
     const int64_t total = span * a.out_cols;
     const int g2 = (int)std::min<int64_t>(std::max<int64_t>((total + 255) / 256, 1), 4096);
-    hipLaunchKernelGGL(k_gemm_splitk_reduce<T>, dim3(g2), dim3(256), 0, st, a);
+    if (timed)
+      hipExtLaunchKernelGGL(k_gemm_splitk_reduce<T>, dim3(g2), dim3(256), 0, st, nullptr, a.t_stop, 0, a);
+    else
+      hipLaunchKernelGGL(k_gemm_splitk_reduce<T>, dim3(g2), dim3(256), 0, st, a);
   }
 }
 

@@ -61,6 +61,10 @@ struct GemmArgs {
   int32_t ksplit;     // > 1: K split over workgroups, fp32 partials in part
   float* part;        // [ksplit][part_rows][Npad]
   int32_t part_rows;  // row capacity of part
+  // optional timing events (timing-enabled events, or null): t_start is recorded
+  // when the GEMM kernel starts, t_stop when the last kernel of the launch
+  // (the GEMM, or its split-K reduce) ends
+  hipEvent_t t_start, t_stop;
 };
 
 // Tile shape and padding of one GEMM, chosen on the host from its row bound.
