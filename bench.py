@@ -6,6 +6,7 @@ pen-stroke samples on a 96x96 grid; the inputs of 8 pre-generated batches are
 resident in HBM before timing starts.  Prints one JSON line on stdout.
 
     python bench.py [--steps K] [--warmup W] [--dtype bf16|f32] [--workload NAME]
+    python bench.py --workload deepcnet5_10_digits_b1000   # forward-only inference, characters/s
     python bench.py --calibrate-copy      # plain device copy, for counter scaling
 
 Measurement: W untimed steps, then K steps between two device synchronisations
@@ -35,6 +36,7 @@ from workloads import get_config, he_params, make_batches, random_labels  # noqa
 DEFAULT_WORKLOAD = "deepcnet5_50_strokes_b100"
 MFMA_PEAK = {"bf16": 2.5e15, "f32": 157.3e12}  # dense MFMA FLOP/s, MI355X
 HBM_PEAK = 8.0e12  # bytes/s
+PAPER_DIGITS_PER_S = 3000.0  # Section 3.2: DeepCNet(5,10) test-time classification rate, GTX 680
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -53,7 +55,7 @@ def layer_shapes(cfg):
     return st
 
 
-def gemm_work(cfg, sizes):
+def gemm_work(cfg, sizes, infer=False):
     """Algorithmic FLOPs of one step, per kernel class.
 
     gather_gemm: convolution forward 2(n_s+1)A C_in C_out per stage, convolution
@@ -70,11 +72,14 @@ def gemm_work(cfg, sizes):
         if s > 1:
             dgrad += 2.0 * sizes[s - 1] * A * co * ci
     head = 2.0 * cfg.batch * (cfg.ell + 1) * cfg.k * cfg.n_classes
+    if infer:  # forward only: conv forward and the logits
+        return {"gather_gemm": fwd + head, "wgrad": 0.0, "conv_total": fwd}
     return {"gather_gemm": fwd + dgrad + 2 * head, "wgrad": fwd + head, "conv_total": 2 * fwd + dgrad}
 
 
-def read_traffic(kernel, dtype):
-    """HBM bytes per launch from the committed counter summary, if it matches the current kernel source."""
+def read_traffic(kernel, dtype, workload):
+    """HBM bytes per launch from the committed counter summary, if it matches the current kernel source,
+    the dtype and the workload."""
     path = os.path.join(PROFILES, f"{kernel}_traffic.txt")
     if not os.path.exists(path):
         return None
@@ -87,7 +92,7 @@ def read_traffic(kernel, dtype):
     if not os.path.exists(src):
         return None
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if kv.get("source_sha256_16") != sha or kv.get("dtype") != dtype:
+    if kv.get("source_sha256_16") != sha or kv.get("dtype") != dtype or kv.get("workload") != workload:
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -95,8 +100,8 @@ def read_traffic(kernel, dtype):
         return None
 
 
-def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0):
-    """The oracle, as it stands, on batch 0: build + forward + backward, repeated for ~budget_s."""
+def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False):
+    """The oracle, as it stands, on batch 0: build + forward (+ backward unless infer), repeated for ~budget_s."""
     from oracle import SparseDeepCNet as Oracle
 
     try:
@@ -117,7 +122,8 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0):
         o = Oracle(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, dtype)
         o.build(batch.coords, batch.batch)
         o.forward(feats, Wn, bs, labels)
-        o.backward()
+        if not infer:
+            o.backward()
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 50:
@@ -130,8 +136,10 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0):
                 break
     except OSError:
         pass
-    return {"value": round(reps * cfg.batch / el, 3), "unit": "samples/s", "cores": threads, "kind": "oracle",
-            "sample": f"batch 0 of {cfg.name} ({cfg.batch} samples), {reps} x (build + forward + backward), "
+    what = "build + forward" if infer else "build + forward + backward"
+    return {"value": round(reps * cfg.batch / el, 3), "unit": "characters/s" if infer else "samples/s",
+            "cores": threads, "kind": "oracle",
+            "sample": f"batch 0 of {cfg.name} ({cfg.batch} samples), {reps} x ({what}), "
                       f"mode {dtype}, {el:.1f} s; NumPy float64, BLAS threads {threads}; host CPU: {cpu}"}
 
 
@@ -193,11 +201,16 @@ def main():
         sizes.append(net.layer_sizes())
     torch.cuda.synchronize()
 
+    infer = cfg.mode == "infer"
+
     def step(i):
         c, f = inputs[i % len(inputs)]
         net.rulebook_build(c, cfg.batch)
-        net.forward(f, Ws_d, bs_d, lab_d)
-        net.backward()
+        if infer:
+            net.forward(f, Ws_d, bs_d, None)
+        else:
+            net.forward(f, Ws_d, bs_d, lab_d)
+            net.backward()
 
     log(f"[bench] warmup {args.warmup} steps")
     for i in range(args.warmup):
@@ -226,14 +239,15 @@ def main():
 
     # algorithmic work of the timed steps (batches cycle in order)
     step_sizes = [sizes[i % len(sizes)] for i in range(args.steps)]
-    work = [gemm_work(cfg, s) for s in step_sizes]
+    work = [gemm_work(cfg, s, infer) for s in step_sizes]
     g_flops = sum(w["gather_gemm"] for w in work)
     avg_launch_s = g_ms / 1e3 / max(g_launches, 1)
     achieved = g_flops / max(g_launches, 1) / avg_launch_s if g_launches else 0.0
     peak = MFMA_PEAK[args.dtype]
-    traffic = read_traffic("gather_gemm", args.dtype)
+    traffic = read_traffic("gather_gemm", args.dtype, cfg.name)
     roofline = {
-        "kernel": "k_gemm_gather (implicit-gather MFMA GEMM: conv forward, conv input gradient, softmax layer)",
+        "kernel": ("k_gemm_gather (implicit-gather MFMA GEMM: conv forward, softmax layer logits)" if infer else
+                   "k_gemm_gather (implicit-gather MFMA GEMM: conv forward, conv input gradient, softmax layer)"),
         "bound": "mfma", "achieved": round(achieved / 1e12, 3), "peak": peak / 1e12, "unit": "TFLOP/s",
         "frac": round(achieved / peak, 5), "traffic": traffic,
         "launches_per_step": g_launches / args.steps, "avg_launch_us": round(avg_launch_s * 1e6, 3),
@@ -255,10 +269,16 @@ def main():
 
     mean_sizes = np.mean(np.array(sizes, dtype=np.float64), axis=0)
     conv_flops = float(np.mean([w["conv_total"] for w in work]))
+    if infer:
+        metric = f"DeepCNet({cfg.ell},{cfg.k}) forward-only characters/sec (digit pictures in a {cfg.grid}x{cfg.grid} grid)"
+        unit = "characters/s"
+    else:
+        metric = "DeepCNet(5,50) sparse-conv fwd+bwd samples/sec; GEMM % MFMA peak"
+        unit = "samples/s"
     out = {
-        "metric": "DeepCNet(5,50) sparse-conv fwd+bwd samples/sec; GEMM % MFMA peak",
+        "metric": metric,
         "value": round(value, 2),
-        "unit": "samples/s",
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -271,15 +291,20 @@ def main():
         "config": {"workload": cfg.name, "net": f"DeepCNet({cfg.ell},{cfg.k})", "grid": cfg.grid,
                    "c_in": cfg.c_in, "classes": cfg.n_classes, "batch": cfg.batch,
                    "input_active_fraction": round(float(mean_sizes[0]) / (cfg.batch * cfg.grid ** 2), 4),
-                   "step": "rulebook build + forward + backward"},
+                   "step": "rulebook build + forward (logits)" if infer else "rulebook build + forward + backward"},
         "conv_gemm_gflop_per_step": round(conv_flops / 1e9, 3),
         "roofline": roofline,
         "kernel_breakdown": breakdown,
         "cpu_baseline": None,
     }
+    if infer and cfg.ell == 5 and cfg.k == 10:
+        # the paper's one speed figure is this workload: 3000 characters/s classified
+        # by DeepCNet(5,10) on a GTX 680 (Section 3.2) -- another machine, context only
+        out["vs_baseline"] = round(value / PAPER_DIGITS_PER_S, 2)
+        out["baseline_context"] = "paper: 3000 characters/s, DeepCNet(5,10) forward on digit pictures, GTX 680 (Section 3.2)"
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(cfg, batches[0], Ws, bs, labels, args.dtype)
+        out["cpu_baseline"] = cpu_baseline(cfg, batches[0], Ws, bs, labels, args.dtype, infer=infer)
     print(json.dumps(out), flush=True)
 
 

@@ -141,7 +141,10 @@ SSCN_API sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* st
  * order given to sscn_rulebook_build); h_W / h_b host arrays of ell+2 device
  * pointers (weights in storage dtype, biases float32); d_labels[batch] int32
  * in [0, n_classes).  Writes d_logits[batch][n_classes] and *d_loss (mean
- * softmax cross-entropy), both float32. */
+ * softmax cross-entropy), both float32.  With d_labels and d_loss both null
+ * the pass is inference only: it writes the logits, skips the loss and the
+ * backward-only work, and a following sscn_backward returns
+ * SSCN_ERR_BAD_STATE.  Exactly one of them null: SSCN_ERR_INVALID_ARGUMENT. */
 SSCN_API sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
                          const int32_t* d_labels, float* d_logits, float* d_loss, void* stream);
 

@@ -655,7 +655,9 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
 
 sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
                          const int32_t* d_labels, float* d_logits, float* d_loss, void* stream) {
-  if (!net || !h_W || !h_b || !d_labels || !d_logits || !d_loss) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net || !h_W || !h_b || !d_logits) return SSCN_ERR_INVALID_ARGUMENT;
+  if ((d_labels == nullptr) != (d_loss == nullptr)) return SSCN_ERR_INVALID_ARGUMENT;
+  const bool train = d_labels != nullptr;  // else inference: logits only
   if (net->n > 0 && !d_feats) return SSCN_ERR_INVALID_ARGUMENT;
   if (!net->built) return SSCN_ERR_BAD_STATE;
   for (int p = 0; p < net->nparams; ++p)
@@ -677,7 +679,8 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   for (int p = 0; p < net->nparams; ++p) {
     const ParamPlan& P = net->P[p];
     pa.job[pa.njobs++] = PackJob{h_W[p], P.WpF, 0, P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.NpadF, P.KpadF};
-    pa.job[pa.njobs++] = PackJob{h_W[p], P.WpD, 1, P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.NpadD, P.KpadD};
+    if (train)  // the input-gradient layout is only read by the backward pass
+      pa.job[pa.njobs++] = PackJob{h_W[p], P.WpD, 1, P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.NpadD, P.KpadD};
   }
   if (timed(net, SSCN_KC_HEAD, st, [&] { return launch_pack_all(net->bf16, pa, st); }) != hipSuccess)
     return SSCN_ERR_HIP;
@@ -705,8 +708,10 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   g.rows_host = net->batch;
   g.row_begin = 0;
   set_plan(g, P.pf, P.rows_f, net->gpart);
+  net->forwarded = false;
   if (timed_gemm(net, g, net->batch, st) != hipSuccess)
     return SSCN_ERR_HIP;
+  if (!train) return SSCN_OK;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_softmax_xent(net->bf16, d_logits, d_labels, net->batch, net->d.n_classes, net->dlogits,
                                    net->dl_stride, net->loss_part, d_loss, st);

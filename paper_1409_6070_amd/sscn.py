@@ -235,9 +235,10 @@ class SparseDeepCNet:
         return sscn_layer_sizes(self.handle, self.nlayers, _stream())
 
     def forward(self, feats: torch.Tensor, Ws: Sequence[torch.Tensor], bs: Sequence[torch.Tensor],
-                labels: torch.Tensor):
+                labels: Optional[torch.Tensor]):
+        """Forward pass; ``labels=None`` is inference (logits only, no loss, no backward)."""
         assert feats.dtype == self.tdtype and feats.is_contiguous()
-        assert labels.dtype == torch.int32
+        assert labels is None or labels.dtype == torch.int32
         for W in Ws:
             assert W.dtype == self.tdtype and W.is_contiguous()
         for b in bs:
@@ -246,9 +247,9 @@ class SparseDeepCNet:
             self.logits = torch.empty(self.batch, self.n_classes, dtype=torch.float32, device=self.device)
         self._keep = [feats, list(Ws), list(bs), labels]
         sscn_forward(self.handle, feats.data_ptr() if feats.numel() else None, [W.data_ptr() for W in Ws],
-                     [b.data_ptr() for b in bs], labels.data_ptr(), self.logits.data_ptr(), self.loss.data_ptr(),
-                     _stream())
-        return self.logits, self.loss
+                     [b.data_ptr() for b in bs], labels.data_ptr() if labels is not None else None,
+                     self.logits.data_ptr(), self.loss.data_ptr() if labels is not None else None, _stream())
+        return self.logits, (self.loss if labels is not None else None)
 
     def backward(self, want_dfeats: bool = False):
         dfeats = None

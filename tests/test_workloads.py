@@ -45,3 +45,16 @@ def test_circle_fixture():
     assert c.batch == 1 and c.n > 80
     d = np.hypot(c.coords[:, 1] - 47.5, c.coords[:, 2] - 47.5)
     assert np.all(np.abs(d - 16) < 0.5)
+
+
+def test_digit_pictures_shape():
+    """Digit stand-ins (Section 2.5): about 150 grey-level pixels per sample, all inside the
+    centred 28 x 28 frame of the 96 x 96 grid, grey levels in (0, 1]."""
+    cfg = get_config("deepcnet5_10_digits_b1000")
+    assert cfg.mode == "infer" and cfg.grid == 96 and (cfg.ell, cfg.k, cfg.n_classes) == (5, 10, 10)
+    b = make_batch(cfg, 0)
+    per = np.bincount(b.coords[:, 0], minlength=cfg.batch)
+    assert 130 <= per.mean() <= 170 and per.min() > 0
+    lo = (96 - 28) // 2
+    assert b.coords[:, 1:].min() >= lo and b.coords[:, 1:].max() < lo + 28
+    assert b.feats.min() > 0.0 and b.feats.max() <= 1.0

@@ -8,7 +8,10 @@ with its parameters.  The generators stand in for the paper's datasets:
   Sections 2.4 and 3.1 (Pendigits, UJIpenchars, Assamese, CASIA; the 3755-class
   heads follow CASIA-OLHWDB1.1 in Section 3.1.3);
 * a dense RGB patch centred in a 96 x 96 grid stands in for CIFAR (Section 2.5,
-  Section 3.3).
+  Section 3.3);
+* grey-level digit strokes of about 150 pixels in the middle of a 96 x 96 grid
+  stand in for MNIST (Section 2.5), on the small network the paper times at test
+  time (DeepCNet(5,10), Section 3.2): a forward-only ("infer") workload.
 """
 
 from dataclasses import dataclass, field
@@ -24,9 +27,10 @@ class WorkloadConfig:
     batch: int
     n_classes: int
     dtypes: Tuple[str, ...]
-    generator: str  # "strokes" or "patch"
+    generator: str  # "strokes", "patch" or "digits"
     gen_args: Dict = field(default_factory=dict)
     seed: int = 0  # input seed; weights use 100 + seed, labels 200 + seed
+    mode: str = "train"  # "train": build + forward + backward; "infer": build + forward (logits)
 
     @property
     def grid(self) -> int:
@@ -84,6 +88,15 @@ CONFIGS = [
         generator="strokes",
         gen_args=dict(strokes=(1, 30), points=(10, 120), box=128, sigma=1.0, features="ones"),
         seed=4,
+    ),
+    # DeepCNet(5,10) classifying digit pictures: 28x28 frame (about 150 grey-level
+    # pixels) in the middle of the 96x96 grid, 10 classes, forward only.
+    WorkloadConfig(
+        name="deepcnet5_10_digits_b1000",
+        ell=5, k=10, c_in=1, batch=1000, n_classes=10, dtypes=("f32", "bf16"),
+        generator="digits",
+        gen_args=dict(strokes=(2, 4), points=(10, 18), box=20, sigma=2.5, brush=2),
+        seed=5, mode="infer",
     ),
 ]
 

@@ -1,4 +1,4 @@
-"""Seeded generators: pen strokes, RGB patch, circle fixture, weights, labels.
+"""Seeded generators: pen strokes, digit pictures, RGB patch, circle fixture, weights, labels.
 
 All randomness comes from numpy's PCG64 (``np.random.default_rng``).  Values are
 returned in float64; callers convert to the storage dtype they test.
@@ -101,6 +101,34 @@ def stroke_batch(rng: np.random.Generator, batch: int, grid: int, c_in: int, str
     return Batch(coords=coords.astype(np.int32), feats=feats, batch=batch, grid=grid)
 
 
+def digit_batch(rng: np.random.Generator, batch: int, grid: int, c_in: int = 1, strokes=(2, 4), points=(10, 18),
+                box=20, sigma=2.5, brush=2) -> Batch:
+    """Handwritten-digit stand-ins: grey-level strokes in the middle of the grid.
+
+    Section 2.5 places 28 x 28 digit pictures (on average about 150 non-zero
+    pixels on a zero background) in the middle of the 96 x 96 input layer.  Per
+    sample: random-walk strokes as in ``stroke_batch`` inside a centred
+    ``box x box`` square, each pixel widened to a ``brush x brush`` block (down
+    and right), so the digit stays inside the centred 28 x 28 frame; the
+    defaults give about 150 active pixels per sample.  Each active pixel gets
+    ``c_in`` grey levels uniform in (0, 1].
+    """
+    coords = []
+    for b in range(batch):
+        pix = _strokes_one(rng, grid, strokes, points, box, sigma)
+        seen = {}
+        for (y, x) in pix:
+            for dy in range(brush):
+                for dx in range(brush):
+                    seen.setdefault((y + dy, x + dx), None)
+        if seen:
+            arr = np.asarray(list(seen.keys()), dtype=np.int32)
+            coords.append(np.concatenate([np.full((len(arr), 1), b, np.int32), arr], axis=1))
+    coords = np.concatenate(coords, axis=0) if coords else np.zeros((0, 3), np.int32)
+    feats = 1.0 - rng.random(size=(coords.shape[0], c_in))
+    return Batch(coords=coords.astype(np.int32), feats=feats, batch=batch, grid=grid)
+
+
 def patch_batch(rng: np.random.Generator, batch: int, grid: int, c_in: int = 3, patch=32, region=40) -> Batch:
     """A dense ``patch x patch`` block of U[0,1) features at a random offset.
 
@@ -183,6 +211,8 @@ def make_batch(cfg: WorkloadConfig, index: int = 0) -> Batch:
         return stroke_batch(rng, cfg.batch, cfg.grid, cfg.c_in, **cfg.gen_args)
     if cfg.generator == "patch":
         return patch_batch(rng, cfg.batch, cfg.grid, cfg.c_in, **cfg.gen_args)
+    if cfg.generator == "digits":
+        return digit_batch(rng, cfg.batch, cfg.grid, cfg.c_in, **cfg.gen_args)
     raise ValueError(cfg.generator)
 
 
