@@ -9,6 +9,10 @@ What is computed (the paper's own description, restated):
   first layer and 2x2 afterwards; the input grid is N = 3 * 2**ell so that the
   last convolution leaves a 1x1 grid; ReLU on hidden layers and a softmax
   output layer (Section 2.1, activation paragraph).
+* DeepCNiN(ell, k) (Section 2.2): the same with a network-in-network layer --
+  a convolution with 1x1 filters, as many as the layer below has channels --
+  after every pooling layer and after the last convolution, and the leaky
+  rectifier f(x) = x for x >= 0, x/3 for x < 0 on every hidden layer.
 * Spatial sparsity (Section 2.3): every hidden variable has a ground state,
   the value it takes when its input region holds no meaningful input; only
   sites whose value can differ from it are computed.  Each layer keeps a
@@ -29,7 +33,8 @@ Readings where the paper is silent (each is also listed in the design notes):
 * feature-matrix rows are in ascending (b, y, x) order;
 * max-pool argmax is the first maximal window position in row-major order
   (dy, dx) = (0,0), (0,1), (1,0), (1,1);
-* ReLU'(0) = 0; the loss is softmax cross-entropy averaged over the batch;
+* ReLU'(0) = 0; for the leaky rectifier f'(x) = 1 for x >= 0 and 1/3 for x < 0;
+  the loss is softmax cross-entropy averaged over the batch;
 * the ground row takes part in backpropagation as one virtual site standing
   for all inactive sites together, so weight and bias gradients equal those
   of the dense network (derivation in ``backward``);
@@ -98,7 +103,7 @@ def round_store(x: np.ndarray, mode: str) -> np.ndarray:
 @dataclass(frozen=True)
 class Stage:
     kind: str  # "conv" or "pool"
-    F: int  # window side: 3 or 2 for convolutions, 2 for pooling
+    F: int  # window side: 3, 2 or 1 (network-in-network) for convolutions, 2 for pooling
     S_in: int  # spatial side of the layer below
     S: int  # spatial side of this layer
     c_in: int
@@ -109,21 +114,33 @@ class Stage:
         return self.F * self.F
 
 
-def stage_plan(ell: int, k: int, c_in: int) -> List[Stage]:
-    """The 2*ell + 1 stages of DeepCNet(ell, k) on an N = 3*2**ell input (Section 2.1).
+ARCHS = ("deepcnet", "deepcnin")
+
+
+def stage_plan(ell: int, k: int, c_in: int, arch: str = "deepcnet") -> List[Stage]:
+    """The stages of DeepCNet(ell, k) (2*ell + 1 of them, Section 2.1) or DeepCNiN(ell, k)
+    (Section 2.2: a 1x1 convolution added after every pooling layer and after the last
+    convolution, 3*ell + 2 stages) on an N = 3*2**ell input.
 
     A valid FxF convolution shrinks the side by F - 1; a 2x2 stride-2 pool halves it.
     """
     if ell < 1 or k < 1 or c_in < 1:
         raise ValueError("ell, k and c_in must be positive")
+    if arch not in ARCHS:
+        raise ValueError(arch)
+    nin = arch == "deepcnin"
     N = 3 * 2 ** ell
     stages = [Stage("conv", 3, N, N - 2, c_in, k)]
     S, C = N - 2, k
     for n in range(2, ell + 2):
         stages.append(Stage("pool", 2, S, S // 2, C, C))
         S //= 2
+        if nin:
+            stages.append(Stage("conv", 1, S, S, C, C))
         stages.append(Stage("conv", 2, S, S - 1, C, n * k))
         S, C = S - 1, n * k
+    if nin:
+        stages.append(Stage("conv", 1, S, S, C, C))
     assert S == 1
     return stages
 
@@ -148,7 +165,7 @@ class Layer:
     R: Optional[np.ndarray] = None
     X: Optional[np.ndarray] = None
     argmax: Optional[np.ndarray] = None  # pooling layers: [n + 1, C] window position of the max
-    relu_on: Optional[np.ndarray] = None  # convolution layers: [n + 1, C] ReLU derivative, 1 where X > 0
+    relu_on: Optional[np.ndarray] = None  # convolution layers: [n + 1, C] rectifier on its x >= 0 branch (ReLU: X > 0)
     grad: Optional[np.ndarray] = None  # conv: dL/dZ (pre-activation); pool and input: dL/dX
     extra: dict = field(default_factory=dict)
 
@@ -166,19 +183,23 @@ def _pointer_from_active(active: np.ndarray):
 
 
 class SparseDeepCNet:
-    """Sparse DeepCNet(ell, k) with a softmax head; calls mirror the C interface.
+    """Sparse DeepCNet(ell, k) or DeepCNiN(ell, k) with a softmax head; calls mirror the C interface.
 
     ``build`` makes every layer's pointer matrix and window lists, ``forward``
     fills the feature matrices and the loss, ``backward`` returns parameter
     gradients and, per layer, the gradient matrices.
     """
 
-    def __init__(self, ell: int, k: int, c_in: int, n_classes: int, mode: str = "f64"):
+    def __init__(self, ell: int, k: int, c_in: int, n_classes: int, mode: str = "f64", arch: str = "deepcnet"):
         if mode not in ("f64", "f32", "bf16"):
             raise ValueError(mode)
         self.ell, self.k, self.c_in, self.n_classes, self.mode = ell, k, c_in, n_classes, mode
+        self.arch = arch
         self.N = 3 * 2 ** ell
-        self.stages = stage_plan(ell, k, c_in)
+        self.stages = stage_plan(ell, k, c_in, arch)
+        # negative-side slope of the hidden layers' rectifier: ReLU (Section 2.1) or
+        # the leaky x/3 of DeepCNiN (Section 2.2)
+        self.slope = 1.0 / 3.0 if arch == "deepcnin" else 0.0
         self.layers: List[Layer] = []
 
     # -- parameters ---------------------------------------------------------
@@ -269,8 +290,12 @@ class SparseDeepCNet:
             V = below.X[L.R]  # [n + 1, A, C_in]: the gathered windows
             if st.kind == "conv":
                 Z = V.reshape(V.shape[0], -1) @ self.Ws[ci] + self.bs[ci]
-                L.X = round_store(np.maximum(Z, 0.0), m)
-                L.relu_on = L.X > 0  # ReLU'(Z): 1 where the stored output is positive, 0 at Z <= 0
+                if self.slope == 0.0:
+                    L.X = round_store(np.maximum(Z, 0.0), m)
+                    L.relu_on = L.X > 0  # ReLU'(Z): 1 where the stored output is positive, 0 at Z <= 0
+                else:
+                    L.relu_on = Z >= 0.0  # f'(Z) = 1 on the x >= 0 branch, 1/3 below
+                    L.X = round_store(np.where(L.relu_on, Z, Z / 3.0), m)
                 ci += 1
             else:
                 L.argmax = np.argmax(V, axis=1)  # first maximal window position
@@ -314,7 +339,7 @@ class SparseDeepCNet:
         top = self.layers[-1]
         dY = np.zeros_like(top.X)
         np.add.at(dY, self.head_rows(), dh)
-        top.grad = round_store(dY * top.relu_on, m)  # dL/dZ of the last convolution
+        top.grad = round_store(dY * self.act_grad(top), m)  # dL/dZ of the last convolution
 
         ci = len(self.Ws) - 2
         for si in range(len(self.stages) - 1, -1, -1):
@@ -327,19 +352,26 @@ class SparseDeepCNet:
                 dV = (delta @ self.Ws[ci].T).reshape(L.R.shape[0], st.A, st.c_in)
                 dX = np.zeros((below.n + 1, st.c_in))
                 np.add.at(dX, L.R.ravel(), dV.reshape(-1, st.c_in))
-                below.grad = round_store(dX, m)  # pooling layer (or input): dL/dX
+                if si > 0 and self.stages[si - 1].kind == "conv":
+                    below.grad = round_store(dX * self.act_grad(below), m)  # a convolution below: dL/dZ
+                else:
+                    below.grad = round_store(dX, m)  # pooling layer (or input): dL/dX
                 ci -= 1
             else:
                 dYp = L.grad  # dL/dY of the pooling layer
                 rows = L.R[np.arange(L.R.shape[0])[:, None], L.argmax]  # [n + 1, C] row of each max
                 dX = np.zeros((below.n + 1, st.c_in))
                 np.add.at(dX, (rows, np.broadcast_to(np.arange(st.c_in), rows.shape)), dYp)
-                below.grad = round_store(dX * below.relu_on, m)  # the convolution below: dL/dZ
+                below.grad = round_store(dX * self.act_grad(below), m)  # the convolution below: dL/dZ
         self.dW, self.db = dW, db
         dfeats = np.zeros((self.layers[0].n, self.c_in))
         dfeats[self.input_order] = self.layers[0].grad[1:]
         self.dfeats = dfeats
         return dW, db, dfeats
+
+    def act_grad(self, L: Layer) -> np.ndarray:
+        """Derivative of the hidden layers' rectifier at each of L's pre-activations."""
+        return np.where(L.relu_on, 1.0, self.slope)
 
     # -- inspection ---------------------------------------------------------
     def layer_view(self, i: int) -> Layer:

@@ -29,10 +29,16 @@ def dense_grid(coords, feats, batch, N, c_in):
 
 
 class DenseDeepCNet:
-    """Dense DeepCNet(ell, k): 3x3 conv, then (2x2/2 max-pool, 2x2 conv) x ell, ReLU, softmax head."""
+    """Dense DeepCNet(ell, k): 3x3 conv, then (2x2/2 max-pool, 2x2 conv) x ell, ReLU, softmax head.
 
-    def __init__(self, ell, k, c_in, n_classes):
+    arch="deepcnin": DeepCNiN(ell, k) (Section 2.2), a 1x1 convolution after every
+    pool and after the last convolution, and the leaky rectifier x/3 for x < 0
+    (torch's leaky_relu with negative slope 1/3) on every hidden layer.
+    """
+
+    def __init__(self, ell, k, c_in, n_classes, arch="deepcnet"):
         self.ell, self.k, self.c_in, self.n_classes = ell, k, c_in, n_classes
+        self.arch = arch
         self.N = 3 * 2 ** ell
 
     def run(self, coords, feats, batch, Ws, bs, labels):
@@ -41,24 +47,36 @@ class DenseDeepCNet:
         for W, b in zip(Ws, bs):
             params.append(torch.tensor(np.asarray(W), dtype=torch.float64, requires_grad=True))
             params.append(torch.tensor(np.asarray(b), dtype=torch.float64, requires_grad=True))
+        nin = self.arch == "deepcnin"
+        act = (lambda z: Fn.leaky_relu(z, 1.0 / 3.0)) if nin else torch.relu
         Zs, Ys = [], []  # per stage: pre-activation (conv) and output
         h = x
         c = self.c_in
+        pi = 0
+
+        def conv(h, F, c):
+            nonlocal pi
+            W, b = params[2 * pi], params[2 * pi + 1]
+            pi += 1
+            wt = W.reshape(F, F, c, W.shape[1]).permute(3, 2, 0, 1)
+            z = Fn.conv2d(h, wt) + b.view(1, -1, 1, 1)
+            z.retain_grad()
+            y = act(z)
+            Zs.append(z)
+            Ys.append(y)
+            return y, W.shape[1]
+
         for li in range(self.ell + 1):
             if li > 0:
                 h = Fn.max_pool2d(h, 2)
                 h.retain_grad()
                 Zs.append(None)
                 Ys.append(h)
-            F = 3 if li == 0 else 2
-            W, b = params[2 * li], params[2 * li + 1]
-            wt = W.reshape(F, F, c, W.shape[1]).permute(3, 2, 0, 1)
-            z = Fn.conv2d(h, wt) + b.view(1, -1, 1, 1)
-            z.retain_grad()
-            h = torch.relu(z)
-            Zs.append(z)
-            Ys.append(h)
-            c = W.shape[1]
+                if nin:
+                    h, c = conv(h, 1, c)
+            h, c = conv(h, 3 if li == 0 else 2, c)
+        if nin:
+            h, c = conv(h, 1, c)
         assert h.shape[-1] == 1 and h.shape[-2] == 1
         feat = h[:, :, 0, 0]
         logits = feat @ params[-2] + params[-1]

@@ -39,14 +39,14 @@ def _random_sites(rng, batch, N, p, c_in, empty_samples=(), full_samples=()):
     return coords.astype(np.int64), feats
 
 
-def _run_pair(ell, k, c_in, n_classes, batch, coords, feats, seed):
-    Ws, bs = he_params(ell, k, c_in, n_classes, seed)
+def _run_pair(ell, k, c_in, n_classes, batch, coords, feats, seed, arch="deepcnet"):
+    Ws, bs = he_params(ell, k, c_in, n_classes, seed, arch)
     labels = random_labels(batch, n_classes, seed + 1)
-    o = SparseDeepCNet(ell, k, c_in, n_classes, "f64")
+    o = SparseDeepCNet(ell, k, c_in, n_classes, "f64", arch)
     o.build(coords, batch)
     o.forward(feats, Ws, bs, labels)
     o.backward()
-    d = DenseDeepCNet(ell, k, c_in, n_classes).run(coords, feats, batch, Ws, bs, labels)
+    d = DenseDeepCNet(ell, k, c_in, n_classes, arch).run(coords, feats, batch, Ws, bs, labels)
     return o, d
 
 
@@ -80,11 +80,20 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("ell,k,c_in,ncls,batch,p,empty,full,seed", CASES)
-def test_oracle_equals_dense_network(ell, k, c_in, ncls, batch, p, empty, full, seed):
+ARCH_CASES = [("deepcnet",) + c for c in CASES] + [
+    # DeepCNiN (Section 2.2): 1x1 layers and the leaky rectifier
+    ("deepcnin", 1, 2, 1, 3, 2, 0.2, (), (), 21),
+    ("deepcnin", 2, 2, 2, 4, 3, 0.08, (1,), (), 22),
+    ("deepcnin", 2, 3, 1, 3, 2, 0.1, (), (0,), 23),
+    ("deepcnin", 3, 2, 1, 3, 1, 0.03, (), (), 24),
+]
+
+
+@pytest.mark.parametrize("arch,ell,k,c_in,ncls,batch,p,empty,full,seed", ARCH_CASES)
+def test_oracle_equals_dense_network(arch, ell, k, c_in, ncls, batch, p, empty, full, seed):
     rng = np.random.default_rng(seed)
     coords, feats = _random_sites(rng, batch, 3 * 2 ** ell, p, c_in, empty, full)
-    o, d = _run_pair(ell, k, c_in, ncls, batch, coords, feats, seed)
+    o, d = _run_pair(ell, k, c_in, ncls, batch, coords, feats, seed, arch)
     # forward: every layer, active and inactive sites
     for s in range(1, len(o.layers)):
         _check_layer_against_dense(o.layers[s], d.Ys[s - 1].detach().numpy())
@@ -166,18 +175,21 @@ def test_stage_sizes_closed_form():
         assert [s.kind for s in st] == ["conv"] + ["pool", "conv"] * ell
 
 
-def test_layer_list_golden():
-    with open(os.path.join(GOLDEN, "deepcnet_4_100_layer_list.txt")) as f:
+@pytest.mark.parametrize("arch,fname", [("deepcnet", "deepcnet_4_100_layer_list.txt"),
+                                        ("deepcnin", "deepcnin_4_100_layer_list.txt")])
+def test_layer_list_golden(arch, fname):
+    # Section 2.1 gives DeepCNet(4,100)'s layer list, Section 2.2 DeepCNiN(4,100)'s
+    with open(os.path.join(GOLDEN, fname)) as f:
         lines = [l.strip() for l in f if l.strip() and not l.startswith("#")]
     hdr = dict(kv.split("=") for kv in lines[0].split())
     ell, k = int(hdr["ell"]), int(hdr["k"])
     tokens = lines[1].split("-")
     assert tokens[0] == "input" and tokens[-1] == "output"
     expected = []
-    for s in stage_plan(ell, k, 1):
+    for s in stage_plan(ell, k, 1, arch):
         expected.append(f"{s.c_out}C{s.F}" if s.kind == "conv" else "MP2")
     assert tokens[1:-1] == expected
-    assert stage_plan(ell, k, 1)[0].S_in == int(hdr["N"])
+    assert stage_plan(ell, k, 1, arch)[0].S_in == int(hdr["N"])
 
 
 @pytest.mark.parametrize("ell,k,M", [(1, 3, 1), (4, 20, 1), (5, 50, 9), (6, 100, 1)])
@@ -305,19 +317,20 @@ def test_window_lists_point_at_the_right_sites():
                     assert L.R[row, dy * st.F + dx] == want
 
 
-def test_finite_differences():
+@pytest.mark.parametrize("arch", ["deepcnet", "deepcnin"])
+def test_finite_differences(arch):
     ell, k, c_in, ncls, batch = 1, 2, 2, 3, 2
     rng = np.random.default_rng(40)
     coords, feats = _random_sites(rng, batch, 6, 0.3, c_in)
-    Ws, bs = he_params(ell, k, c_in, ncls, 41)
+    Ws, bs = he_params(ell, k, c_in, ncls, 41, arch)
     labels = [1, 2]
-    o = SparseDeepCNet(ell, k, c_in, ncls)
+    o = SparseDeepCNet(ell, k, c_in, ncls, "f64", arch)
     o.build(coords, batch)
     o.forward(feats, Ws, bs, labels)
     dW, db, dfeats = o.backward()
 
     def loss_at(Ws_, bs_, feats_):
-        q = SparseDeepCNet(ell, k, c_in, ncls)
+        q = SparseDeepCNet(ell, k, c_in, ncls, "f64", arch)
         q.build(coords, batch)
         return q.forward(feats_, Ws_, bs_, labels)[1]
 
@@ -407,3 +420,27 @@ def test_round_bf16_matches_torch_cast():
     for arr in (x, ties, ties_odd):
         ref = torch.tensor(arr.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
         np.testing.assert_array_equal(round_bf16(arr), ref)
+
+
+def test_deepcnin_rectifier_is_leaky_x_over_3():
+    # Section 2.2: f(x) = x for x >= 0 and x/3 for x < 0 on every hidden layer; the
+    # 1x1 layers keep their input's active set (identity window lists)
+    rng = np.random.default_rng(60)
+    coords, feats = _random_sites(rng, 2, 12, 0.2, 1)
+    Ws, bs = he_params(2, 3, 1, 4, 61, "deepcnin")
+    o = SparseDeepCNet(2, 3, 1, 4, "f64", "deepcnin")
+    o.build(coords, 2)
+    o.forward(feats, Ws, bs, [0, 1])
+    ci = 0
+    neg = 0
+    for si, st in enumerate(o.stages):
+        L, below = o.layers[si + 1], o.layers[si]
+        if st.kind != "conv":
+            continue
+        Z = below.X[L.R].reshape(L.R.shape[0], -1) @ Ws[ci] + bs[ci]
+        np.testing.assert_allclose(L.X, np.where(Z >= 0, Z, Z / 3.0), rtol=0, atol=1e-12)
+        neg += int((Z < 0).sum())
+        if st.F == 1:
+            assert L.n == below.n and np.array_equal(L.R[:, 0], np.arange(L.n + 1))
+        ci += 1
+    assert neg > 0  # the negative branch is exercised

@@ -169,28 +169,35 @@ def circle_sites(grid: int = 96, diameter: int = 32) -> Batch:
     return Batch(coords=coords, feats=feats, batch=1, grid=grid)
 
 
-def _layer_shapes(ell: int, k: int, c_in: int):
-    """(fan_in_rows, c_out) of each convolution weight: 3x3 first, then 2x2; conv n has n*k filters."""
+def _layer_shapes(ell: int, k: int, c_in: int, arch: str = "deepcnet"):
+    """(fan_in_rows, c_out) of each convolution weight in stage order: 3x3 first, then
+    2x2; conv n has n*k filters.  DeepCNiN adds a 1x1 layer of the same width after
+    every pooling layer and after the last convolution."""
     shapes = [(9 * c_in, k)]
     for n in range(2, ell + 2):
+        if arch == "deepcnin":
+            shapes.append(((n - 1) * k, (n - 1) * k))
         shapes.append((4 * (n - 1) * k, n * k))
+    if arch == "deepcnin":
+        shapes.append(((ell + 1) * k, (ell + 1) * k))
     return shapes
 
 
-def he_params(ell: int, k: int, c_in: int, n_classes: int, seed: int):
+def he_params(ell: int, k: int, c_in: int, n_classes: int, seed: int, arch: str = "deepcnet"):
     """Random parameters for DeepCNet(ell, k): U[-0.1, 0.1] biases; He-normal
     convolution weights (N(0, 2/fan_in), the usual choice before a ReLU) and a
     Glorot-normal softmax layer (N(0, 2/(fan_in + fan_out)), the usual choice for
     a linear output layer; it keeps fresh logits O(1) instead of saturating the
     softmax).
 
-    Returns ``(Ws, bs)``: ``ell + 2`` matrices, the convolutions' ``[F*F*C_in, C_out]``
+    Returns ``(Ws, bs)``: one matrix per convolution in stage order (``ell + 1`` for
+    DeepCNet, ``2 ell + 2`` for DeepCNiN), each ``[F*F*C_in, C_out]``
     (rows ordered ``(dy*F + dx)*C_in + c``) followed by the softmax layer's
     ``[C_last, n_classes]``, and the matching bias vectors.  Biases are non-zero
     on purpose: with zero biases every ground state would be zero.
     """
     rng = np.random.default_rng(seed)
-    shapes = _layer_shapes(ell, k, c_in) + [((ell + 1) * k, n_classes)]
+    shapes = _layer_shapes(ell, k, c_in, arch) + [((ell + 1) * k, n_classes)]
     Ws, bs = [], []
     for i, (rows, cols) in enumerate(shapes):
         var = 2.0 / rows if i < len(shapes) - 1 else 2.0 / (rows + cols)
