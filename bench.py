@@ -45,13 +45,19 @@ def log(msg):
 
 
 def layer_shapes(cfg):
-    """(kind, A, C_in, C_out) per stage of DeepCNet(ell, k) (Section 2.1)."""
+    """(kind, A, C_in, C_out) per stage of DeepCNet(ell, k) (Section 2.1) or DeepCNiN(ell, k)
+    (Section 2.2: a 1x1 convolution after every pool and after the last convolution)."""
+    nin = cfg.arch == "deepcnin"
     st = [("conv", 9, cfg.c_in, cfg.k)]
     c = cfg.k
     for n in range(2, cfg.ell + 2):
         st.append(("pool", 4, c, c))
+        if nin:
+            st.append(("conv", 1, c, c))
         st.append(("conv", 4, c, n * cfg.k))
         c = n * cfg.k
+    if nin:
+        st.append(("conv", 1, c, c))
     return st
 
 
@@ -119,7 +125,7 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False):
     Wn = [w.double().numpy() for w in Wt]
     reps, t0 = 0, time.perf_counter()
     while True:
-        o = Oracle(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, dtype)
+        o = Oracle(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, dtype, cfg.arch)
         o.build(batch.coords, batch.batch)
         o.forward(feats, Wn, bs, labels)
         if not infer:
@@ -183,7 +189,7 @@ def main():
     tdt = torch.bfloat16 if args.dtype == "bf16" else torch.float32
     log(f"[bench] generating {args.batches} batches of {cfg.name}")
     batches = make_batches(cfg, args.batches)
-    Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed)
+    Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed, cfg.arch)
     labels = random_labels(cfg.batch, cfg.n_classes, cfg.label_seed)
     Ws_d = [torch.tensor(W, dtype=torch.float32).to(tdt).to(dev).contiguous() for W in Ws]
     bs_d = [torch.tensor(b, dtype=torch.float32).to(dev).contiguous() for b in bs]
@@ -194,7 +200,7 @@ def main():
                        torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous()))
     max_active = max(b.n for b in batches)
     net = SparseDeepCNet(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, batch_max=cfg.batch, max_active=max_active,
-                         dtype=args.dtype)
+                         dtype=args.dtype, arch=cfg.arch)
     sizes = []
     for c, _ in inputs:
         net.rulebook_build(c, cfg.batch)
@@ -274,6 +280,9 @@ def main():
         unit = "characters/s"
     else:
         metric = "DeepCNet(5,50) sparse-conv fwd+bwd samples/sec; GEMM % MFMA peak"
+        if cfg.arch != "deepcnet" or (cfg.ell, cfg.k) != (5, 50):
+            metric = (f"{'DeepCNiN' if cfg.arch == 'deepcnin' else 'DeepCNet'}({cfg.ell},{cfg.k}) "
+                      "sparse-conv fwd+bwd samples/sec; GEMM % MFMA peak")
         unit = "samples/s"
     out = {
         "metric": metric,
@@ -288,7 +297,9 @@ def main():
         "vs_baseline": None,
         "dtype": args.dtype,
         "data": "synthetic",
-        "config": {"workload": cfg.name, "net": f"DeepCNet({cfg.ell},{cfg.k})", "grid": cfg.grid,
+        "config": {"workload": cfg.name,
+                   "net": f"{'DeepCNiN' if cfg.arch == 'deepcnin' else 'DeepCNet'}({cfg.ell},{cfg.k})",
+                   "grid": cfg.grid,
                    "c_in": cfg.c_in, "classes": cfg.n_classes, "batch": cfg.batch,
                    "input_active_fraction": round(float(mean_sizes[0]) / (cfg.batch * cfg.grid ** 2), 4),
                    "step": "rulebook build + forward (logits)" if infer else "rulebook build + forward + backward"},

@@ -10,9 +10,18 @@
  *     input - kC3 - MP2 - 2kC2 - MP2 - ... - (ell+1)kC2 - softmax output
  *
  * with N = 3 * 2^ell, valid stride-1 convolutions, 2x2 stride-2 max-pooling,
- * ReLU on hidden layers.  Only active sites are computed; every inactive site
- * of a layer shares that layer's ground state (Section 2.3), kept as row 0 of
+ * ReLU on hidden layers, or of a DeepCNiN(ell, k) (Section 2.2): the same with
+ * a 1x1 convolution (kC1, 2kC1, ...) after every pooling layer and after the
+ * last convolution, and the leaky rectifier f(x) = x (x >= 0), x/3 (x < 0) on
+ * every hidden layer.  Only active sites are computed; every inactive site of
+ * a layer shares that layer's ground state (Section 2.3), kept as row 0 of
  * the layer's feature matrix.
+ *
+ * Stages, layers and parameters.  DeepCNet has L = 2*ell + 1 stages, DeepCNiN
+ * L = 3*ell + 2; layer 0 is the input and layer s = 1 .. L the output of stage s.
+ * The convolutions, counted in stage order, own weight matrices
+ * n = 0 .. n_conv - 1 (n_conv = ell + 1, or 2*ell + 2 for DeepCNiN); the
+ * softmax layer's matrix is n_conv, so there are n_conv + 1 of them.
  *
  * Memory ownership.  The caller owns every device buffer: inputs, parameters,
  * gradients, logits, loss and one workspace.  The library never allocates or
@@ -20,10 +29,10 @@
  * All work is enqueued on the stream passed in (a hipStream_t, NULL for the
  * null stream).  A net is used from one host thread and one stream at a time.
  *
- * Layouts.  Row-major throughout.  Convolution weight n (n = 0 .. ell) is a
- * [F*F*C_in, C_out] matrix whose row index is (dy*F + dx)*C_in + c
- * (cross-correlation: output (y, x) reads input (y+dy, x+dx)); F = 3 for
- * n = 0, else 2.  The softmax layer (index ell+1) is [C_last, n_classes].
+ * Layouts.  Row-major throughout.  Convolution weight n is a [F*F*C_in, C_out]
+ * matrix whose row index is (dy*F + dx)*C_in + c (cross-correlation: output
+ * (y, x) reads input (y+dy, x+dx)); F = 3 for n = 0, 1 for the 1x1 layers, else
+ * 2.  The softmax layer's matrix is [C_last, n_classes].
  * Weights and input features are in the net's storage dtype; biases, weight
  * and bias gradients, logits and the loss are float32.
  *
@@ -63,11 +72,18 @@ typedef enum {
 
 typedef enum { SSCN_F32 = 0, SSCN_BF16 = 1 } sscn_dtype;
 
-/* DeepCNet(ell, k) with c_in input features per site and an n_classes softmax
- * output (Section 2.1).  batch_max and max_active bound the batches that
- * sscn_rulebook_build accepts and size the workspace.  dtype is the storage
- * type of features, weights and stored activations/gradients; products and
- * sums accumulate in float32. */
+/* Network family (Sections 2.1, 2.2). */
+typedef enum {
+  SSCN_DEEPCNET = 0, /* DeepCNet(ell, k): conv3, then (2x2 max-pool, conv2) x ell; ReLU          */
+  SSCN_DEEPCNIN = 1  /* DeepCNiN(ell, k): DeepCNet plus a 1x1 convolution (same width) after every
+                        pooling layer and after the last convolution; leaky rectifier x/3 below 0 */
+} sscn_arch;
+
+/* A DeepCNet(ell, k) or DeepCNiN(ell, k) (arch) with c_in input features per
+ * site and an n_classes softmax output (Sections 2.1, 2.2).  batch_max and
+ * max_active bound the batches that sscn_rulebook_build accepts and size the
+ * workspace.  dtype is the storage type of features, weights and stored
+ * activations/gradients; products and sums accumulate in float32. */
 typedef struct {
   int32_t ell;
   int32_t k;
@@ -76,13 +92,14 @@ typedef struct {
   int32_t batch_max;
   int32_t max_active;
   int32_t dtype; /* sscn_dtype */
+  int32_t arch;  /* sscn_arch */
 } sscn_net_desc;
 
 typedef struct sscn_net sscn_net; /* opaque host-side plan */
 
 /* One layer of the network as stored in the workspace (for tests and
- * inspection).  Layer 0 is the input; layer s = 1 .. 2*ell+1 is the output of
- * stage s (odd s: convolution, even s: pooling).  All pointers are device
+ * inspection).  Layer 0 is the input; layer s = 1 .. L is the output of
+ * stage s (a convolution or a pooling layer, see kind).  All pointers are device
  * pointers into the workspace bound by the last sscn_rulebook_build. */
 typedef struct {
   int32_t kind;       /* 0 input, 1 convolution, 2 max-pooling                  */
@@ -108,12 +125,12 @@ typedef struct {
 } sscn_layer_view;
 
 /* Host only.  Validates desc (ell in 1..8, k, c_in, n_classes, batch_max,
- * max_active >= 1, dtype known) and builds the plan. */
+ * max_active >= 1, dtype and arch known) and builds the plan. */
 SSCN_API sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out);
 SSCN_API void sscn_net_destroy(sscn_net* net);
 SSCN_API const char* sscn_status_string(int32_t status);
 
-/* Number of parameter matrices (ell + 2) and the shape of matrix `layer`
+/* Number of parameter matrices (n_conv + 1) and the shape of matrix `layer`
  * (0 .. ell convolutions, ell+1 softmax layer); the bias has `cols` entries.
  * Section 2.1 gives the weight count 3^2*M*k + sum_n 2^2*(n k)*((n+1) k). */
 SSCN_API int32_t sscn_net_num_params(const sscn_net* net);
@@ -132,13 +149,13 @@ SSCN_API sscn_status sscn_net_workspace_bytes(const sscn_net* net, size_t* bytes
 SSCN_API sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t n, int32_t batch,
                                 void* d_workspace, size_t workspace_bytes, void* stream);
 
-/* Synchronises `stream`, copies the 2*ell+2 active-site counts (layer 0 =
+/* Synchronises `stream`, copies the L + 1 active-site counts (layer 0 =
  * input, then each stage) to h_counts, and returns any latched input error
  * (SSCN_ERR_OUT_OF_RANGE / SSCN_ERR_DUPLICATE_SITE). */
 SSCN_API sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream);
 
 /* Forward pass (Sections 2.1, 2.3): d_feats[n][c_in] (storage dtype, in the
- * order given to sscn_rulebook_build); h_W / h_b host arrays of ell+2 device
+ * order given to sscn_rulebook_build); h_W / h_b host arrays of n_conv + 1 device
  * pointers (weights in storage dtype, biases float32); d_labels[batch] int32
  * in [0, n_classes).  Writes d_logits[batch][n_classes] and *d_loss (mean
  * softmax cross-entropy), both float32.  With d_labels and d_loss both null
@@ -149,13 +166,13 @@ SSCN_API sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void
                          const int32_t* d_labels, float* d_logits, float* d_loss, void* stream);
 
 /* Backward pass of the last sscn_forward (Section 2.3: the same structures in
- * reverse).  h_dW / h_db: host arrays of ell+2 device float32 pointers shaped
+ * reverse).  h_dW / h_db: host arrays of n_conv + 1 device float32 pointers shaped
  * like the parameters; they are overwritten (not accumulated).  d_dfeats
  * (nullable): [n][c_in] storage dtype, gradient of the loss with respect to
  * the input features, in the caller's site order. */
 SSCN_API sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db, void* d_dfeats, void* stream);
 
-/* Runs only stage s (1 .. 2*ell+1) of the forward or backward pass on the
+/* Runs only stage s (1 .. L) of the forward or backward pass on the
  * current workspace contents, with the parameters of the last sscn_forward /
  * sscn_backward.  For checking one kernel group against known inputs.  A
  * backward convolution stage takes its output gradient (all rows) as it
@@ -195,7 +212,7 @@ SSCN_API sscn_status sscn_timing_enable(sscn_net* net, uint32_t class_mask);
 SSCN_API sscn_status sscn_timing_collect(sscn_net* net, int32_t kernel_class, int32_t* launches, float* total_ms,
                                          void* stream);
 
-/* Describes layer `layer` (0 .. 2*ell+1) of the bound workspace. */
+/* Describes layer `layer` (0 .. L) of the bound workspace. */
 SSCN_API sscn_status sscn_layer_view_get(const sscn_net* net, int32_t layer, sscn_layer_view* out);
 
 #ifdef __cplusplus

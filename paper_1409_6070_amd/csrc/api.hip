@@ -64,6 +64,9 @@ struct sscn_net {
   int esz, VE;
   int nlayers;
   int nparams;
+  int nconv;    // convolutional layers (weights 0 .. nconv-1; the softmax layer's is nconv)
+  bool nin;     // DeepCNiN (1x1 layers, leaky rectifier)
+  float slope;  // negative-side slope of the hidden layers' rectifier
   LayerPlan L[MAX_LAYERS];
   ParamPlan P[MAX_LAYERS];
   int dl_stride;  // dlogits row stride (elements)
@@ -247,6 +250,7 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   if (d.ell < 1 || d.ell > 8 || d.k < 1 || d.c_in < 1 || d.n_classes < 1 || d.batch_max < 1 || d.max_active < 1)
     return SSCN_ERR_INVALID_ARGUMENT;
   if (d.dtype != SSCN_F32 && d.dtype != SSCN_BF16) return SSCN_ERR_INVALID_ARGUMENT;
+  if (d.arch != SSCN_DEEPCNET && d.arch != SSCN_DEEPCNIN) return SSCN_ERR_INVALID_ARGUMENT;
   const int64_t N = 3ll << d.ell;
   if ((int64_t)d.batch_max * N * N >= (1ll << 31)) return SSCN_ERR_INVALID_ARGUMENT;
   if ((int64_t)(d.ell + 1) * d.k > (1 << 20) || d.n_classes > (1 << 24) || d.c_in > (1 << 16))
@@ -257,14 +261,35 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   net->bf16 = d.dtype == SSCN_BF16;
   net->esz = net->bf16 ? 2 : 4;
   net->VE = 16 / net->esz;
-  net->nlayers = 2 * d.ell + 2;
-  net->nparams = d.ell + 2;
+  const bool nin = d.arch == SSCN_DEEPCNIN;
+  net->nin = nin;
+  net->slope = nin ? 1.f / 3.f : 0.f;  // leaky rectifier x/3 (Section 2.2), else ReLU
+  net->nlayers = nin ? 3 * d.ell + 3 : 2 * d.ell + 2;
+  net->nconv = nin ? 2 * d.ell + 2 : d.ell + 1;
+  net->nparams = net->nconv + 1;
   net->pool_parts = 1024;  // most row blocks per slot of a bias / ground-row reduction
   net->wgrad_slabs = 8;    // slabs of sites per weight-gradient workgroup
   const int BK = net->bf16 ? 64 : 32;
   const int VE = net->VE;
   auto cp = [VE](int c) { return (int)round_up(c, VE); };
-  // layers (Section 2.1): input N; conv3 N-2; then (pool S/2, conv2 S-1) x ell
+  // layers: input N; conv3 N-2; then (pool S/2, conv2 S-1) x ell (Section 2.1);
+  // DeepCNiN adds a 1x1 convolution of the same width after every pool and after
+  // the last convolution (Section 2.2)
+  int kinds[MAX_LAYERS], Fs[MAX_LAYERS], widths[MAX_LAYERS];
+  {
+    int n = 0;
+    kinds[n] = 1, Fs[n] = 3, widths[n] = d.k, ++n;
+    for (int lv = 2; lv <= d.ell + 1; ++lv) {
+      kinds[n] = 2, Fs[n] = 2, widths[n] = (lv - 1) * d.k, ++n;
+      if (nin) kinds[n] = 1, Fs[n] = 1, widths[n] = (lv - 1) * d.k, ++n;
+      kinds[n] = 1, Fs[n] = 2, widths[n] = lv * d.k, ++n;
+    }
+    if (nin) kinds[n] = 1, Fs[n] = 1, widths[n] = (d.ell + 1) * d.k, ++n;
+    if (n + 1 != net->nlayers) {
+      delete net;
+      return SSCN_ERR_INVALID_ARGUMENT;
+    }
+  }
   LayerPlan* L = net->L;
   L[0] = LayerPlan{};
   L[0].kind = 0;
@@ -276,11 +301,11 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     LayerPlan& l = L[s];
     l = LayerPlan{};
     const int64_t below = L[s - 1].cap;
-    if (s % 2 == 1) {
+    if (kinds[s - 1] == 1) {
       l.kind = 1;
-      l.F = (s == 1) ? 3 : 2;
+      l.F = Fs[s - 1];
       l.S = S - (l.F - 1);
-      l.C = ((s + 1) / 2) * d.k;
+      l.C = widths[s - 1];
       l.conv_index = ci++;
     } else {
       // with N = 3 * 2^ell every pooling input side is even, so each site below
@@ -344,7 +369,7 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     }
   }
   {
-    ParamPlan& P = net->P[d.ell + 1];
+    ParamPlan& P = net->P[net->nconv];
     const LayerPlan& Lt = L[net->nlayers - 1];
     P.A = 1;
     P.c_in = Lt.C;
@@ -483,7 +508,8 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
     g.out_cols = L.Cp;
     g.out = L.X;
     g.out_stride = L.Cp;
-    g.epi = EPI_BIAS_RELU;
+    g.epi = net->slope == 0.f ? EPI_BIAS_RELU : EPI_BIAS_LRELU;
+    if (L.A == 1) g.rmap = nullptr;  // a 1x1 layer reads its own row of the layer below
     g.rows_dev = net->counts + s;
     g.rows_add = 1;
     g.row_begin = 0;
@@ -541,6 +567,7 @@ static GroundArgs ground_args(const sscn_net* net, int s, bool pool_above) {
   g.c_out = L.C;
   g.part = net->ppart;
   g.PM = net->pool_parts;
+  g.slope = net->slope;
   g.db = net->db[ci];
   g.D0 = net->D0;
   return g;
@@ -554,7 +581,8 @@ static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_
   const LayerPlan& Lb = net->L[s - 1];
   const int ci = L.conv_index;
   const ParamPlan& P = net->P[ci];
-  const bool row0 = needs_row0(net, s);
+  // a 1x1 layer's input-gradient GEMM covers row 0 itself (its window is the row)
+  const bool row0 = needs_row0(net, s) && L.A > 1;
   const GroundArgs g = ground_args(net, s, pool_above);
   hipError_t e;
   if ((e = timed(net, SSCN_KC_GROUND, st, [&] {
@@ -562,8 +590,11 @@ static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_
        })) != hipSuccess)
     return e;
   if (!row0) return hipSuccess;
+  // below a convolution the stored gradient is dL/dZ: times its rectifier derivative
+  const void* mask = Lb.kind == 1 ? Lb.X : nullptr;
   return timed(net, SSCN_KC_GROUND, st, [&] {
-    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, st);
+    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, mask, net->slope,
+                          st);
   });
 }
 
@@ -625,7 +656,7 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
     // rows >= 1 below with the partial sums of the convolution below
     if (Lb.kind != 1) return hipErrorInvalidValue;  // a pooling layer sits on a convolution
     const GroundArgs g = ground_args(net, s - 1, true);
-    const int Ac = needs_row0(net, s - 1) ? Lb.A : 0;
+    const int Ac = (needs_row0(net, s - 1) && Lb.A > 1) ? Lb.A : 0;
     return timed(net, SSCN_KC_POOL_BWD, st, [&] { return launch_ground(net->bf16, g, Ac, 1, st); });
   }
   if (!(s > 1 || net->want_dfeats)) return hipSuccess;
@@ -646,9 +677,19 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
   g.out = Lb.grad;
   g.out_stride = Lb.Cp;
   g.epi = EPI_STORE;
+  if (Lb.kind == 1) {  // a convolution below: store dL/dZ, the rectifier derivative applied
+    g.epi = EPI_STORE_MASK;
+    g.mask = Lb.X;
+    g.mask_stride = Lb.Cp;
+    g.slope = net->slope;
+  }
   g.rows_dev = net->counts + s - 1;
   g.rows_add = 1;
   g.row_begin = 1;
+  if (L.A == 1) {  // 1x1 layer: row i below takes row i's gradient, ground row included
+    g.rmap = nullptr;
+    g.row_begin = 0;
+  }
   set_plan(g, P.pd, P.rows_d, net->gpart);
   return timed_gemm(net, g, Lb.cap + 1, st);
 }
@@ -688,7 +729,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
     if (forward_stage(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
   // softmax layer on each sample's top-layer row
   const LayerPlan& Lt = net->L[net->nlayers - 1];
-  const ParamPlan& P = net->P[net->d.ell + 1];
+  const ParamPlan& P = net->P[net->nconv];
   GemmArgs g{};
   g.src = Lt.X;
   g.src_stride = Lt.Cp;
@@ -699,7 +740,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   g.Kpad = P.KpadF;
   g.Bt = P.WpF;
   g.Npad = P.NpadF;
-  g.bias = h_b[net->d.ell + 1];
+  g.bias = h_b[net->nconv];
   g.N = net->d.n_classes;
   g.out_cols = net->d.n_classes;
   g.out = d_logits;
@@ -733,7 +774,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   net->want_dfeats = d_dfeats != nullptr;
   const int top = net->nlayers - 1;
   const LayerPlan& Lt = net->L[top];
-  const int fc = net->d.ell + 1;
+  const int fc = net->nconv;
   const ParamPlan& P = net->P[fc];
   // softmax layer: dh = dlogits W^T, scattered to the top layer's rows
   GemmArgs g{};
@@ -758,7 +799,8 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   if (timed_gemm(net, g, net->batch, st) != hipSuccess)
     return SSCN_ERR_HIP;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
-        return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp, st);
+        return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp,
+                                   net->slope, st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
   // Stages from the top down, all on the caller's stream: each convolution's

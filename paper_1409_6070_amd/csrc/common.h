@@ -41,7 +41,15 @@ enum : int32_t { ERRBIT_RANGE = 1, ERRBIT_DUP = 2 };
 // ---------------------------------------------------------------------------
 // per-layer geometry of the occupancy bitmaps
 
-constexpr int MAX_LAYERS = 18;  // 2*ell + 2 for ell <= 8
+constexpr int MAX_LAYERS = 27;  // DeepCNet 2*ell + 2, DeepCNiN 3*ell + 3 layers, ell <= 8
+
+// Derivative of a hidden layer's rectifier, decided from its stored output y:
+// ReLU (slope 0): 1 for y > 0, else 0 (so ReLU'(0) = 0); leaky rectifier
+// (slope 1/3): 1 on the x >= 0 branch (sign bit of y clear), else the slope.
+__device__ inline float act_factor(float y, float slope) {
+  const bool pos = slope == 0.f ? (y > 0.f) : !__builtin_signbit(y);
+  return pos ? 1.f : slope;
+}
 
 struct LayerBits {
   uint64_t* bits;    // [batch * S * Wd] row-aligned occupancy words
@@ -54,10 +62,10 @@ struct LayerBits {
 };
 
 struct RulebookArgs {
-  int32_t nlayers;  // 2*ell + 2
+  int32_t nlayers;
   int32_t batch;
   LayerBits L[MAX_LAYERS];
-  int32_t kind[MAX_LAYERS];  // per layer s >= 1: 1 conv, 2 pool
+  int32_t kind[MAX_LAYERS];  // per layer s >= 1: 1 conv (F = 3, 2 or 1), 2 pool
   int32_t F[MAX_LAYERS];
   int32_t* rules[MAX_LAYERS];    // layer s >= 1: [(cap_s+1) * A]
   int32_t* rules_t[MAX_LAYERS];  // layer s >= 1: conv [(cap_{s-1}+1) * A], pool [cap_{s-1}+1]

@@ -105,7 +105,13 @@ template <typename T>
 __device__ inline float epi_value(const GemmArgs& a, float v, float bias) {
   v += bias;
   if (a.epi == EPI_BIAS_RELU) v = fmaxf(v, 0.f);
+  if (a.epi == EPI_BIAS_LRELU) v = v >= 0.f ? v : v / 3.f;
   return v;
+}
+
+// Epilogues that store in the storage dtype (the others store float32).
+__device__ inline bool epi_stores_T(int epi) {
+  return epi == EPI_BIAS_RELU || epi == EPI_STORE || epi == EPI_BIAS_LRELU || epi == EPI_STORE_MASK;
 }
 
 // q = k / d for 0 <= k < 2^20, 1 <= d < 2^16: float estimate, then exact correction.
@@ -119,7 +125,9 @@ __device__ inline int div_small(int k, int d, float rcp) {
 template <typename T>
 __device__ inline void store_out(const GemmArgs& a, int64_t m, int n, float v) {
   const int64_t o = m * a.out_stride + n;
-  if (a.epi == EPI_BIAS_RELU || a.epi == EPI_STORE)
+  if (a.epi == EPI_STORE_MASK)
+    v *= act_factor(Elem<T>::to_f32(((const T*)a.mask)[m * a.mask_stride + n]), a.slope);
+  if (epi_stores_T(a.epi))
     ((T*)a.out)[o] = Elem<T>::from_f32(v);
   else
     ((float*)a.out)[o] = v;
@@ -251,7 +259,7 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
             if (m < rows) part[(int64_t)m * a.Npad + n] = acc[i][j][r];
           }
         }
-    } else if (STAGE && (a.epi == EPI_BIAS_RELU || a.epi == EPI_STORE)) {
+    } else if (STAGE && epi_stores_T(a.epi)) {
       T* Cs = smem;
 #pragma unroll
       for (int i = 0; i < C::TM; ++i)
@@ -268,8 +276,17 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
       for (int v = tid; v < BM * (BN / VE); v += NT) {
         const int r = v / (BN / VE), nv = v - r * (BN / VE);
         const int m = m0 + r, n = n0 + nv * VE;
-        if (m < rows && n < a.out_cols)
-          *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = *(const u32x4*)(Cs + r * CS + nv * VE);
+        if (m < rows && n < a.out_cols) {
+          u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
+          if (a.epi == EPI_STORE_MASK) {  // the rectifier derivative of the layer below, 16 bytes at a time
+            const u32x4 y = *(const u32x4*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
+#pragma unroll
+            for (int e = 0; e < VE; ++e)
+              ((T*)&o)[e] = Elem<T>::from_f32(Elem<T>::to_f32(((const T*)&o)[e]) *
+                                              act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope));
+          }
+          *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
+        }
       }
     } else {
 #pragma unroll
@@ -521,7 +538,8 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
 
 template <typename T>
 __global__ void __launch_bounds__(256) k_row0_dx(const T* __restrict__ W, const float* __restrict__ D0, int32_t A,
-                                                 int32_t c_in, int32_t c_out, int32_t cp_in, T* grad_in) {
+                                                 int32_t c_in, int32_t c_out, int32_t cp_in, T* grad_in,
+                                                 const T* __restrict__ Y_below, float slope) {
   __shared__ float red[256];
   const int c = blockIdx.x;
   float s = 0.f;
@@ -538,7 +556,11 @@ __global__ void __launch_bounds__(256) k_row0_dx(const T* __restrict__ W, const 
     if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
     __syncthreads();
   }
-  if (threadIdx.x == 0 && c < cp_in) grad_in[c] = Elem<T>::from_f32(red[0]);
+  if (threadIdx.x == 0 && c < cp_in) {
+    float v = red[0];
+    if (Y_below) v *= act_factor(Elem<T>::to_f32(Y_below[c]), slope);
+    grad_in[c] = Elem<T>::from_f32(v);
+  }
 }
 
 static int device_grid_limit() { return 256 * 8; }
@@ -658,13 +680,13 @@ hipError_t launch_wgrad_reduce(bool bf16, const WGradArgs* layers, int n, hipStr
 }
 
 hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, int32_t c_in, int32_t c_out,
-                          int32_t cp_in, void* grad_in, hipStream_t st) {
+                          int32_t cp_in, void* grad_in, const void* Y_below, float slope, hipStream_t st) {
   if (bf16)
     hipLaunchKernelGGL(k_row0_dx<__bf16>, dim3(cp_in), dim3(256), 0, st, (const __bf16*)W, D0, A, c_in, c_out, cp_in,
-                       (__bf16*)grad_in);
+                       (__bf16*)grad_in, (const __bf16*)Y_below, slope);
   else
     hipLaunchKernelGGL(k_row0_dx<float>, dim3(cp_in), dim3(256), 0, st, (const float*)W, D0, A, c_in, c_out, cp_in,
-                       (float*)grad_in);
+                       (float*)grad_in, (const float*)Y_below, slope);
   return hipGetLastError();
 }
 

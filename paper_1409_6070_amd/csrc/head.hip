@@ -156,21 +156,22 @@ __global__ void k_loss_final(const float* __restrict__ loss_part, int32_t batch,
 template <typename T>
 __global__ void __launch_bounds__(256) k_head_scatter(const float* __restrict__ dh, int32_t dh_stride,
                                                       const int32_t* __restrict__ head_rows, int32_t batch,
-                                                      const T* __restrict__ Y_top, T* grad_top, int32_t cp) {
+                                                      const T* __restrict__ Y_top, T* grad_top, int32_t cp,
+                                                      float slope) {
   const int c = blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= cp) return;
   const int b = blockIdx.y;
   if (b < batch) {
     const int r = head_rows[b];
     if (r == 0) return;
-    const bool on = Elem<T>::to_f32(Y_top[(int64_t)r * cp + c]) > 0.f;
-    grad_top[(int64_t)r * cp + c] = on ? Elem<T>::from_f32(dh[(int64_t)b * dh_stride + c]) : Elem<T>::from_f32(0.f);
+    const float f = act_factor(Elem<T>::to_f32(Y_top[(int64_t)r * cp + c]), slope);
+    grad_top[(int64_t)r * cp + c] = Elem<T>::from_f32(dh[(int64_t)b * dh_stride + c] * f);
     return;
   }
   float g0 = 0.f;
   for (int bb = 0; bb < batch; ++bb)
     if (head_rows[bb] == 0) g0 += dh[(int64_t)bb * dh_stride + c];
-  grad_top[c] = (Elem<T>::to_f32(Y_top[c]) > 0.f) ? Elem<T>::from_f32(g0) : Elem<T>::from_f32(0.f);
+  grad_top[c] = Elem<T>::from_f32(g0 * act_factor(Elem<T>::to_f32(Y_top[c]), slope));
 }
 
 __global__ void __launch_bounds__(256) k_fill_zero(uint32_t* p, int64_t words) {
@@ -245,14 +246,15 @@ hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* la
 }
 
 hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
-                               int32_t batch, const void* Y_top, void* grad_top, int32_t cp, hipStream_t st) {
+                               int32_t batch, const void* Y_top, void* grad_top, int32_t cp, float slope,
+                               hipStream_t st) {
   dim3 grid((cp + 255) / 256, batch + 1);
   if (bf16)
     hipLaunchKernelGGL(k_head_scatter<__bf16>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
-                       (const __bf16*)Y_top, (__bf16*)grad_top, cp);
+                       (const __bf16*)Y_top, (__bf16*)grad_top, cp, slope);
   else
     hipLaunchKernelGGL(k_head_scatter<float>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
-                       (const float*)Y_top, (float*)grad_top, cp);
+                       (const float*)Y_top, (float*)grad_top, cp, slope);
   return hipGetLastError();
 }
 

@@ -31,10 +31,12 @@ hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const Rul
 //   rmap null: source row m, A must be 1)
 
 enum Epilogue : int32_t {
-  EPI_BIAS_RELU = 0,  // + bias, ReLU, store in storage dtype
-  EPI_BIAS_F32 = 1,   // + bias, store float32
-  EPI_F32 = 2,        // store float32
-  EPI_STORE = 3,      // store in storage dtype
+  EPI_BIAS_RELU = 0,   // + bias, ReLU, store in storage dtype
+  EPI_BIAS_F32 = 1,    // + bias, store float32
+  EPI_F32 = 2,         // store float32
+  EPI_STORE = 3,       // store in storage dtype
+  EPI_BIAS_LRELU = 4,  // + bias, leaky rectifier (x/3 below zero), store in storage dtype
+  EPI_STORE_MASK = 5,  // times act_factor(mask[m][n], slope), store in storage dtype
 };
 
 struct GemmArgs {
@@ -61,6 +63,11 @@ struct GemmArgs {
   int32_t ksplit;     // > 1: K split over workgroups, fp32 partials in part
   float* part;        // [ksplit][part_rows][Npad]
   int32_t part_rows;  // row capacity of part
+  // EPI_STORE_MASK: the rectifier derivative of the layer below, from its
+  // stored output [rows][mask_stride] (same rows and columns as out)
+  const void* mask;
+  int32_t mask_stride;
+  float slope;
   // optional timing events (timing-enabled events, or null): t_start is recorded
   // when the GEMM kernel starts, t_stop when the last kernel of the launch
   // (the GEMM, or its split-K reduce) ends
@@ -106,7 +113,7 @@ struct WGradArgs {
 };
 
 // Weight gradients of several layers in one launch (all with the same tile).
-constexpr int MAX_WG_LAYERS = MAX_LAYERS / 2 + 2;  // convolutions + softmax layer
+constexpr int MAX_WG_LAYERS = 20;  // convolutions (<= 2*ell + 2) + softmax layer
 struct WGradGroup {
   int32_t n;
   int32_t tile_beg[MAX_WG_LAYERS + 1];  // workgroup tiles of layer l: [tile_beg[l], tile_beg[l+1])
@@ -133,9 +140,11 @@ hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipS
 // part -> dW [A*c_in x c_out] (and db [c_out] when m_ones >= 0) for every layer
 // of the list with nchunks > 1, in one launch.
 hipError_t launch_wgrad_reduce(bool bf16, const WGradArgs* layers, int n, hipStream_t st);
-// grad_in[0][c] = sum_f sum_n W[(f*c_in + c)*c_out + n] * D0[f][n]
+// grad_in[0][c] = sum_f sum_n W[(f*c_in + c)*c_out + n] * D0[f][n], times
+// act_factor(Y_below[0][c], slope) when Y_below (the layer below's stored
+// output, a convolution) is given
 hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, int32_t c_in, int32_t c_out,
-                          int32_t cp_in, void* grad_in, hipStream_t st);
+                          int32_t cp_in, void* grad_in, const void* Y_below, float slope, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // max-pooling
@@ -161,6 +170,7 @@ struct GroundArgs {
   const int32_t* n_rows;
   int32_t B2;
   int32_t stride, cp, c_out;
+  float slope;  // rectifier of the convolution (0: ReLU, 1/3: leaky)
   float* part;  // [(2 + AC) * cp * PM]
   int32_t PM;   // partial stride, >= B1, B2
   float* db;
@@ -196,7 +206,8 @@ hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st);
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
                                void* dlogits, int32_t dl_stride, float* loss_part, float* loss, hipStream_t st);
 hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
-                               int32_t batch, const void* Y_top, void* grad_top, int32_t cp, hipStream_t st);
+                               int32_t batch, const void* Y_top, void* grad_top, int32_t cp, float slope,
+                               hipStream_t st);
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t st);
 
 }  // namespace sscn

@@ -113,7 +113,7 @@ __device__ inline void ground_flags(const int32_t* __restrict__ R, int64_t i, in
 // the pooling layer's rows o >= 1 (thread (lane l, channel vector v) of block b
 // takes rows 1 + b*lanes + l, then every gridDim*lanes-th).  For each window
 // position f of row o, with child row i = Rp[o][f]:
-//   i >= 1:  delta[i] = dY[o] where argmax[o] == f and Y_below[i] > 0, else 0
+//   i >= 1:  delta[i] = dY[o] * f'(Y_below[i]) where argmax[o] == f, else 0
 //            (each row >= 1 below lies in exactly one window: written once),
 //            summed into slot 1 and, where the convolution's window position f'
 //            of row i reads the ground row, into slot 2 + f';
@@ -160,8 +160,10 @@ __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g) {
           u32x4 out;
 #pragma unroll
           for (int j = 0; j < VE; ++j) {
-            const bool take = ((int)((am >> (8 * j)) & 0xff) == f) && (Elem<T>::to_f32(((const T*)&y)[j]) > 0.f);
-            ((T*)&out)[j] = take ? ((const T*)&gv)[j] : Elem<T>::from_f32(0.f);
+            const float fac = act_factor(Elem<T>::to_f32(((const T*)&y)[j]), g.slope);
+            ((T*)&out)[j] = ((int)((am >> (8 * j)) & 0xff) == f)
+                                ? Elem<T>::from_f32(Elem<T>::to_f32(((const T*)&gv)[j]) * fac)
+                                : Elem<T>::from_f32(0.f);
           }
           *(u32x4*)(dZ + (int64_t)i * g.stride + c) = out;
 #pragma unroll
@@ -260,7 +262,7 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
 // wave reduces with a butterfly over its 64 lanes and the 4 wave sums are added
 // in a fixed order (the same every run); thread 0 finishes:
 //   with a pooling layer above, row 0 of delta is
-//     z0 = mask(Y_below[0][c]) * (dY[0][c] + slot 0), written to delta[0][c];
+//     z0 = f'(Y_below[0][c]) * (dY[0][c] + slot 0), written to delta[0][c];
 //   without one, z0 = delta[0][c] as stored;
 //   db[c] = slot 1 + z0,  D0[f][c] = slot 2+f + z0  (row 0 reads the ground row
 //   at every window position), for c < c_out.
@@ -297,9 +299,8 @@ __global__ void __launch_bounds__(256) k_ground_final(GroundArgs g) {
   T* dZ = (T*)g.dZ;
   float z0;
   if (pool) {
-    const T g0 = (Elem<T>::to_f32(((const T*)g.Y_below)[c]) > 0.f)
-                     ? Elem<T>::from_f32(tot[0] + Elem<T>::to_f32(((const T*)g.dY)[c]))
-                     : Elem<T>::from_f32(0.f);
+    const T g0 = Elem<T>::from_f32((tot[0] + Elem<T>::to_f32(((const T*)g.dY)[c])) *
+                                   act_factor(Elem<T>::to_f32(((const T*)g.Y_below)[c]), g.slope));
     dZ[c] = g0;
     z0 = Elem<T>::to_f32(g0);
   } else {

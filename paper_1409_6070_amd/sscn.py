@@ -18,6 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsscn.so")
 
 SSCN_F32, SSCN_BF16 = 0, 1
+ARCHS = ("deepcnet", "deepcnin")  # sscn_arch values 0, 1
 STATUS = {
     0: "SSCN_OK",
     1: "SSCN_ERR_INVALID_ARGUMENT",
@@ -44,7 +45,8 @@ class SSCNError(RuntimeError):
 
 
 class NetDesc(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("ell", "k", "c_in", "n_classes", "batch_max", "max_active", "dtype")]
+    _fields_ = [(n, ctypes.c_int32)
+                for n in ("ell", "k", "c_in", "n_classes", "batch_max", "max_active", "dtype", "arch")]
 
 
 class LayerView(ctypes.Structure):
@@ -191,18 +193,22 @@ def sscn_timing_collect(net, kernel_class: int, stream):
 
 
 class SparseDeepCNet:
-    """DeepCNet(ell, k) on the GPU through libsscn; torch supplies memory and the stream."""
+    """DeepCNet(ell, k) or DeepCNiN(ell, k) on the GPU through libsscn; torch supplies memory and the stream."""
 
     def __init__(self, ell: int, k: int, c_in: int, n_classes: int, batch_max: int, max_active: int,
-                 dtype: str = "bf16", device: str = "cuda"):
+                 dtype: str = "bf16", device: str = "cuda", arch: str = "deepcnet"):
         if dtype not in ("f32", "bf16"):
             raise ValueError(dtype)
+        if arch not in ARCHS:
+            raise ValueError(arch)
         self.ell, self.k, self.c_in, self.n_classes = ell, k, c_in, n_classes
         self.dtype = dtype
+        self.arch = arch
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.device = torch.device(device)
-        self.nlayers = 2 * ell + 2
-        desc = NetDesc(ell, k, c_in, n_classes, batch_max, max_active, SSCN_BF16 if dtype == "bf16" else SSCN_F32)
+        self.nlayers = (3 * ell + 3) if arch == "deepcnin" else (2 * ell + 2)
+        desc = NetDesc(ell, k, c_in, n_classes, batch_max, max_active, SSCN_BF16 if dtype == "bf16" else SSCN_F32,
+                       ARCHS.index(arch))
         self.handle = sscn_net_create(desc)
         self.ws_bytes = sscn_net_workspace_bytes(self.handle)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)

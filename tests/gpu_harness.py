@@ -55,7 +55,7 @@ class Pair:
     """One problem run through both paths."""
 
     def __init__(self, ell, k, c_in, n_classes, batch, coords, feats, Ws, bs, labels, dtype,
-                 max_active=None, want_dfeats=True, run_oracle=True):
+                 max_active=None, want_dfeats=True, run_oracle=True, arch="deepcnet"):
         self.dtype = dtype
         self.batch = batch
         dev = torch.device("cuda")
@@ -63,8 +63,9 @@ class Pair:
         Ws_t = [to_dtype(W, dtype) for W in Ws]
         bs_t = [torch.tensor(np.asarray(b, dtype=np.float32)) for b in bs]
         n = int(np.asarray(coords).shape[0])
+        self.arch = arch
         self.net = GpuNet(ell, k, c_in, n_classes, batch_max=max(batch, 1), max_active=max_active or max(n, 1),
-                          dtype=dtype)
+                          dtype=dtype, arch=arch)
         self.coords_d = torch.tensor(np.asarray(coords, dtype=np.int32).reshape(-1, 3)).to(dev).contiguous()
         self.feats_d = feats_t.to(dev).contiguous()
         self.Ws_d = [w.to(dev).contiguous() for w in Ws_t]
@@ -74,7 +75,7 @@ class Pair:
         # the oracle receives exactly the values the GPU receives
         self.o = None
         if run_oracle:
-            self.o = Oracle(ell, k, c_in, n_classes, dtype)
+            self.o = Oracle(ell, k, c_in, n_classes, dtype, arch)
             self.o.build(np.asarray(coords), batch)
             self.o.forward(feats_t.double().numpy(), [w.double().numpy() for w in Ws_t],
                            [b.double().numpy() for b in bs_t], labels)
@@ -182,12 +183,13 @@ def _check_values(p: Pair, tol=None, check_grads=True):
             if bad[0].size:
                 flipped.append((s, bad, v["argmax"][bad].astype(np.int64)))
         if L.relu_on is not None:
-            gpu_on = v["X"] > 0
+            # the GPU's rectifier branch from its stored output: ReLU y > 0; leaky x/3: sign bit clear
+            gpu_on = v["X"] > 0 if o.slope == 0.0 else ~np.signbit(v["X"])
             bad = np.nonzero(gpu_on != L.relu_on)
             if bad[0].size:
                 scale = max(np.abs(L.X).max(), 1e-30)
                 near = np.maximum(np.abs(L.X[bad]), np.abs(v["X"][bad]))
-                assert np.all(near <= tol * scale), f"ReLU decision layer {s}: {bad[0].size} flips, max |Z| {near.max()}"
+                assert np.all(near <= tol * scale), f"rectifier decision layer {s}: {bad[0].size} flips, max |Z| {near.max()}"
                 relu_flips.append((s, gpu_on))
             report[f"relu{s}_mismatch"] = int(bad[0].size)
     e = rel_err(p.logits, o.logits)

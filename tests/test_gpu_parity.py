@@ -65,7 +65,7 @@ def test_small_networks(case, dtype):
 
 def _config_case(cfg, dtype, index=0):
     b = make_batch(cfg, index)
-    Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed)
+    Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed, cfg.arch)
     labels = random_labels(cfg.batch, cfg.n_classes, cfg.label_seed)
     return b, Ws, bs, labels
 
@@ -80,7 +80,7 @@ def test_workload_parity_full_size(name, dtype):
     b, Ws, bs, labels = _config_case(cfg, dtype)
     log(f"[workload] {name} {dtype} n={b.n} batch={cfg.batch}")
     pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, dtype,
-                max_active=int(b.n * 1.25)).run_gpu()
+                max_active=int(b.n * 1.25), arch=cfg.arch).run_gpu()
     check_structure(pair)
     rep = check_values(pair)
     worst = {k_: v for k_, v in rep.items() if not k_.startswith(("argmax", "relu"))}
@@ -248,3 +248,27 @@ def test_inference_digits_full_size(dtype):
     with pytest.raises(sscn.SSCNError) as err:
         net.backward()
     assert err.value.name == "SSCN_ERR_BAD_STATE"
+
+
+SMALL_NIN = [
+    # name, ell, k, c_in, classes, batch, p, empty, full, seed
+    ("nin_l1k3_m1_b2", 1, 3, 1, 4, 2, 0.3, (), (), 31),
+    ("nin_l2k5_m3_b3_empty", 2, 5, 3, 7, 3, 0.08, (1,), (), 32),
+    ("nin_l2k12_m1_b2_full", 2, 12, 1, 5, 2, 0.1, (), (0,), 33),
+    ("nin_l3k20_m2_b4", 3, 20, 2, 33, 4, 0.05, (), (), 34),
+    ("nin_l4k24_m1_b5", 4, 24, 1, 129, 5, 0.02, (), (), 36),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", SMALL_NIN, ids=[c[0] for c in SMALL_NIN])
+def test_small_deepcnin(case, dtype):
+    """DeepCNiN (Section 2.2): 1x1 layers after every pool and the last convolution, leaky rectifier x/3."""
+    name, ell, k, c_in, ncls, batch, p, empty, full, seed = case
+    coords, feats = _sparse_case(seed, ell, batch, p, c_in, empty, full)
+    log(f"[small-nin] {name} {dtype} n={len(coords)} seed={seed}")
+    Ws, bs = he_params(ell, k, c_in, ncls, 100 + seed, "deepcnin")
+    labels = random_labels(batch, ncls, 200 + seed)
+    pair = Pair(ell, k, c_in, ncls, batch, coords, feats, Ws, bs, labels, dtype, arch="deepcnin").run_gpu()
+    check_structure(pair)
+    check_values(pair)

@@ -36,13 +36,15 @@ def test_status_strings():
     assert "twice" in sscn.sscn_status_string(3)
 
 
-@pytest.mark.parametrize("ell,k,c_in,ncls", [(4, 20, 1, 10), (5, 50, 1, 3755), (5, 50, 8, 3755), (5, 100, 3, 10),
-                                             (6, 100, 1, 3755)])
-def test_param_shapes_match_oracle(ell, k, c_in, ncls):
-    h = sscn.sscn_net_create(sscn.NetDesc(ell, k, c_in, ncls, 8, 1000, sscn.SSCN_BF16))
+@pytest.mark.parametrize("arch,ell,k,c_in,ncls", [
+    ("deepcnet", 4, 20, 1, 10), ("deepcnet", 5, 50, 1, 3755), ("deepcnet", 5, 50, 8, 3755),
+    ("deepcnet", 5, 100, 3, 10), ("deepcnet", 6, 100, 1, 3755), ("deepcnet", 8, 10, 1, 10),
+    ("deepcnin", 4, 100, 1, 10), ("deepcnin", 5, 50, 1, 3755), ("deepcnin", 2, 3, 2, 4), ("deepcnin", 8, 10, 1, 10)])
+def test_param_shapes_match_oracle(arch, ell, k, c_in, ncls):
+    h = sscn.sscn_net_create(sscn.NetDesc(ell, k, c_in, ncls, 8, 1000, sscn.SSCN_BF16, sscn.ARCHS.index(arch)))
     try:
         got = [sscn.sscn_net_param_shape(h, i) for i in range(sscn.sscn_net_num_params(h))]
-        assert got == Oracle(ell, k, c_in, ncls).param_shapes()
+        assert got == Oracle(ell, k, c_in, ncls, arch=arch).param_shapes()
         assert sscn.sscn_net_workspace_bytes(h) > 0
     finally:
         sscn.sscn_net_destroy(h)
@@ -57,6 +59,7 @@ def test_param_shapes_match_oracle(ell, k, c_in, ncls):
     (4, 10, 1, 10, 0, 100, 0),       # batch_max
     (4, 10, 1, 10, 8, 0, 0),         # max_active
     (4, 10, 1, 10, 8, 100, 7),       # dtype
+    (4, 10, 1, 10, 8, 100, 0, 2),    # arch
     (7, 10, 1, 10, 100000, 100, 0),  # batch_max * N^2 beyond int32 keys
 ])
 def test_create_rejects_bad_descriptions(desc):

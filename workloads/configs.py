@@ -9,6 +9,7 @@ with its parameters.  The generators stand in for the paper's datasets:
   heads follow CASIA-OLHWDB1.1 in Section 3.1.3);
 * a dense RGB patch centred in a 96 x 96 grid stands in for CIFAR (Section 2.5,
   Section 3.3);
+* the DeepCNet(5,50) pen strokes also feed a DeepCNiN(5,50) (Section 2.2);
 * grey-level digit strokes of about 150 pixels in the middle of a 96 x 96 grid
   stand in for MNIST (Section 2.5), on the small network the paper times at test
   time (DeepCNet(5,10), Section 3.2): a forward-only ("infer") workload.
@@ -31,6 +32,7 @@ class WorkloadConfig:
     gen_args: Dict = field(default_factory=dict)
     seed: int = 0  # input seed; weights use 100 + seed, labels 200 + seed
     mode: str = "train"  # "train": build + forward + backward; "infer": build + forward (logits)
+    arch: str = "deepcnet"  # or "deepcnin" (Section 2.2)
 
     @property
     def grid(self) -> int:
@@ -97,6 +99,15 @@ CONFIGS = [
         generator="digits",
         gen_args=dict(strokes=(2, 4), points=(10, 18), box=20, sigma=2.5, brush=2),
         seed=5, mode="infer",
+    ),
+    # DeepCNiN(5,50) (1x1 layers after every pool and the last convolution, leaky
+    # rectifier) on the DeepCNet(5,50) pen-stroke inputs.
+    WorkloadConfig(
+        name="deepcnin5_50_strokes_b100",
+        ell=5, k=50, c_in=1, batch=100, n_classes=3755, dtypes=("bf16",),
+        generator="strokes",
+        gen_args=dict(strokes=(1, 20), points=(10, 60), box=64, sigma=2.0, features="ones"),
+        seed=6, arch="deepcnin",
     ),
 ]
 
