@@ -20,6 +20,9 @@ What is computed (the paper's own description, restated):
   pointer matrix (one entry per spatial location of the layer, naming that
   location's feature-matrix row).  Backpropagation runs over the same
   structures in reverse (Section 2.3, last paragraph).
+* Dropout (Section 2.1; Section 2.2 for DeepCNiN): one rate for the input of each
+  convolution that is not 1x1 and one for the softmax layer's input; masks from
+  the counter-based generator in ``philox``.
 
 Readings where the paper is silent (each is also listed in the design notes):
 
@@ -35,6 +38,9 @@ Readings where the paper is silent (each is also listed in the design notes):
   (dy, dx) = (0,0), (0,1), (1,0), (1,1);
 * ReLU'(0) = 0; for the leaky rectifier f'(x) = 1 for x >= 0 and 1/3 for x < 0;
   the loss is softmax cross-entropy averaged over the batch;
+* dropout is inverted (kept values times 1/(1 - p)) and touches only rows >= 1 of
+  a layer: the ground row is never dropped, so inactive sites keep one shared
+  ground state (``set_dropout``);
 * the ground row takes part in backpropagation as one virtual site standing
   for all inactive sites together, so weight and bias gradients equal those
   of the dense network (derivation in ``backward``);
@@ -50,6 +56,8 @@ from dataclasses import dataclass, field
 from typing import List, Optional
 
 import numpy as np
+
+from .philox import drop_scale, dropout_keep
 
 
 class OracleInputError(ValueError):
@@ -201,6 +209,48 @@ class SparseDeepCNet:
         # the leaky x/3 of DeepCNiN (Section 2.2)
         self.slope = 1.0 / 3.0 if arch == "deepcnin" else 0.0
         self.layers: List[Layer] = []
+        self.rates = None
+        self.seed = 0
+
+    # -- dropout ------------------------------------------------------------
+    def dropout_stages(self) -> List[int]:
+        """Stage index of each convolution whose input takes dropout: every convolution
+        except the 1x1 network-in-network layers (Section 2.2), in order; the softmax
+        layer's input follows as dropout site ``len(...)`` (Section 2.1: ell + 2 rates)."""
+        return [si for si, st in enumerate(self.stages) if st.kind == "conv" and st.F > 1]
+
+    def set_dropout(self, rates, seed: int):
+        """Dropout rates per level (ell + 1 convolution inputs, then the softmax layer's
+        input) and the 64-bit seed of the masks; ``None`` switches dropout off.
+
+        Reading: inverted dropout on the active rows of the layer feeding each of those
+        convolutions; the ground row (row 0) is never dropped, so every inactive site
+        keeps the shared ground state and the sparse structure of Section 2.3 is
+        unchanged.  Masks come from ``philox.dropout_keep``; dropout only applies in a
+        training pass (``forward`` with labels).
+        """
+        if rates is None:
+            self.rates = None
+            return
+        rates = [float(r) for r in rates]
+        if len(rates) != self.ell + 2:
+            raise ValueError(f"need {self.ell + 2} dropout rates, got {len(rates)}")
+        for r in rates:
+            if not 0.0 <= r < 1.0:
+                raise ValueError("dropout rates must be in [0, 1)")
+        self.rates, self.seed = rates, int(seed) & 0xFFFFFFFFFFFFFFFF
+
+    def _drop_factor(self, keys, channels: int, j: int):
+        """[n, C] multiplier of dropout site j for rows with the given keys (None: rate 0)."""
+        p = self.rates[j]
+        if p == 0.0:
+            return None
+        return np.where(dropout_keep(keys, channels, j, p, self.seed), drop_scale(p), 0.0)
+
+    def _apply_drop(self, X: np.ndarray, factor) -> np.ndarray:
+        """X * factor, rounded first to float32 and then to the storage type (modes f32, bf16)."""
+        Y = X * factor
+        return Y if self.mode == "f64" else round_store(round_f32(Y), self.mode)
 
     # -- parameters ---------------------------------------------------------
     def param_shapes(self):
@@ -270,6 +320,11 @@ class SparseDeepCNet:
     def forward(self, feats, Ws, bs, labels):
         """Feature matrices of every layer, logits and mean softmax cross-entropy.
 
+        ``labels=None`` is an inference pass: logits only (loss None), no dropout.
+        With dropout set (``set_dropout``) a training pass multiplies rows >= 1 of
+        each dropout site's input by its mask factor before use; the convolution
+        (and its weight gradient) reads the dropped matrix.
+
         Convolution: row o of the output is ReLU(b + sum_f W_f^T x_{R[o][f]}),
         row 0 included -- its window is all ground rows, which makes it the
         layer's ground state.  Pooling: channel-wise max over the window's rows
@@ -284,10 +339,23 @@ class SparseDeepCNet:
         L0.X = round_store(X, m)
         self.Ws = [round_store(np.asarray(W, dtype=np.float64), m) for W in Ws]
         self.bs = [np.asarray(b, dtype=np.float64) for b in bs]
+        train = labels is not None
+        drop = train and self.rates is not None
+        dsite = {si: j for j, si in enumerate(self.dropout_stages())}
         ci = 0
         for si, st in enumerate(self.stages):
             L, below = self.layers[si + 1], self.layers[si]
-            V = below.X[L.R]  # [n + 1, A, C_in]: the gathered windows
+            Xin = below.X
+            L.extra.pop("drop", None)
+            if drop and si in dsite:
+                keys = (below.sites[:, 0] * below.S + below.sites[:, 1]) * below.S + below.sites[:, 2]
+                fac = self._drop_factor(keys, st.c_in, dsite[si])
+                if fac is not None:
+                    Xin = below.X.copy()
+                    Xin[1:] = self._apply_drop(below.X[1:], fac)
+                    L.extra["drop"] = fac  # [n_below, C_in] factor on rows 1.. of the layer below
+            L.extra["Xin"] = Xin
+            V = Xin[L.R]  # [n + 1, A, C_in]: the gathered windows
             if st.kind == "conv":
                 Z = V.reshape(V.shape[0], -1) @ self.Ws[ci] + self.bs[ci]
                 if self.slope == 0.0:
@@ -302,8 +370,17 @@ class SparseDeepCNet:
                 L.X = V.max(axis=1)
         rows = self.head_rows()
         self.h = self.layers[-1].X[rows]
+        self.h_drop = None
+        if drop:
+            self.h_drop = self._drop_factor(np.arange(self.batch), self.h.shape[1], len(dsite))
+            if self.h_drop is not None:
+                self.h = self._apply_drop(self.h, self.h_drop)
         logits = self.h @ self.Ws[-1] + self.bs[-1]
         self.logits = logits if m == "f64" else round_f32(logits)
+        self.trained = train
+        if not train:
+            self.labels, self.loss = None, None
+            return self.logits, None
         labels = np.asarray(labels, dtype=np.int64)
         self.labels = labels
         z = self.logits - self.logits.max(axis=1, keepdims=True)
@@ -323,6 +400,8 @@ class SparseDeepCNet:
         treating row 0 as one more site gives the dense weight and bias
         gradients exactly; the same argument gives row 0 of the layer below.
         """
+        if not getattr(self, "trained", False):
+            raise RuntimeError("backward needs a training forward pass (with labels)")
         m = self.mode
         B = self.batch
         p = np.exp(self.logits - self.logits.max(axis=1, keepdims=True))
@@ -336,6 +415,8 @@ class SparseDeepCNet:
         dW[-1] = self.h.T @ dlogits
         db[-1] = dlogits.sum(axis=0)
         dh = dlogits @ self.Ws[-1].T
+        if self.h_drop is not None:
+            dh = dh * self.h_drop  # through the softmax layer's dropout
         top = self.layers[-1]
         dY = np.zeros_like(top.X)
         np.add.at(dY, self.head_rows(), dh)
@@ -346,12 +427,14 @@ class SparseDeepCNet:
             st, L, below = self.stages[si], self.layers[si + 1], self.layers[si]
             if st.kind == "conv":
                 delta = L.grad  # [n + 1, C_out]
-                V = below.X[L.R].reshape(L.R.shape[0], -1)
+                V = L.extra["Xin"][L.R].reshape(L.R.shape[0], -1)
                 dW[ci] = V.T @ delta
                 db[ci] = delta.sum(axis=0)
                 dV = (delta @ self.Ws[ci].T).reshape(L.R.shape[0], st.A, st.c_in)
                 dX = np.zeros((below.n + 1, st.c_in))
                 np.add.at(dX, L.R.ravel(), dV.reshape(-1, st.c_in))
+                if "drop" in L.extra:
+                    dX[1:] *= L.extra["drop"]  # through this convolution's input dropout
                 if si > 0 and self.stages[si - 1].kind == "conv":
                     below.grad = round_store(dX * self.act_grad(below), m)  # a convolution below: dL/dZ
                 else:

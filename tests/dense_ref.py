@@ -41,7 +41,11 @@ class DenseDeepCNet:
         self.arch = arch
         self.N = 3 * 2 ** ell
 
-    def run(self, coords, feats, batch, Ws, bs, labels):
+    def run(self, coords, feats, batch, Ws, bs, labels, masks=None):
+        """Forward and autograd backward.  ``masks``: optional per-level dropout multipliers,
+        one per convolution that is not 1x1 ([B, C_in, S, S], multiplying that convolution's
+        input) and one for the softmax layer's input ([B, C]); None entries mean no dropout."""
+        masks = masks or [None] * (self.ell + 2)
         x = dense_grid(coords, feats, batch, self.N, self.c_in).requires_grad_(True)
         params = []
         for W, b in zip(Ws, bs):
@@ -53,11 +57,16 @@ class DenseDeepCNet:
         h = x
         c = self.c_in
         pi = 0
+        di = 0
 
         def conv(h, F, c):
-            nonlocal pi
+            nonlocal pi, di
             W, b = params[2 * pi], params[2 * pi + 1]
             pi += 1
+            if F > 1:
+                if masks[di] is not None:
+                    h = h * torch.as_tensor(masks[di], dtype=torch.float64)
+                di += 1
             wt = W.reshape(F, F, c, W.shape[1]).permute(3, 2, 0, 1)
             z = Fn.conv2d(h, wt) + b.view(1, -1, 1, 1)
             z.retain_grad()
@@ -79,6 +88,8 @@ class DenseDeepCNet:
             h, c = conv(h, 1, c)
         assert h.shape[-1] == 1 and h.shape[-2] == 1
         feat = h[:, :, 0, 0]
+        if masks[-1] is not None:
+            feat = feat * torch.as_tensor(masks[-1], dtype=torch.float64)
         logits = feat @ params[-2] + params[-1]
         loss = Fn.cross_entropy(logits, torch.tensor(np.asarray(labels), dtype=torch.int64))
         loss.backward()
