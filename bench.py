@@ -127,6 +127,8 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False):
     while True:
         o = Oracle(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, dtype, cfg.arch)
         o.build(batch.coords, batch.batch)
+        if cfg.dropout and not infer:
+            o.set_dropout(cfg.dropout, cfg.dropout_seed + reps)
         o.forward(feats, Wn, bs, labels)
         if not infer:
             o.backward()
@@ -200,7 +202,7 @@ def main():
                        torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous()))
     max_active = max(b.n for b in batches)
     net = SparseDeepCNet(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, batch_max=cfg.batch, max_active=max_active,
-                         dtype=args.dtype, arch=cfg.arch)
+                         dtype=args.dtype, arch=cfg.arch, dropout=bool(cfg.dropout))
     sizes = []
     for c, _ in inputs:
         net.rulebook_build(c, cfg.batch)
@@ -215,6 +217,8 @@ def main():
         if infer:
             net.forward(f, Ws_d, bs_d, None)
         else:
+            if cfg.dropout:  # fresh masks every step (a host-side call)
+                net.set_dropout(cfg.dropout, cfg.dropout_seed + i)
             net.forward(f, Ws_d, bs_d, lab_d)
             net.backward()
 
@@ -283,6 +287,8 @@ def main():
         if cfg.arch != "deepcnet" or (cfg.ell, cfg.k) != (5, 50):
             metric = (f"{'DeepCNiN' if cfg.arch == 'deepcnin' else 'DeepCNet'}({cfg.ell},{cfg.k}) "
                       "sparse-conv fwd+bwd samples/sec; GEMM % MFMA peak")
+        if cfg.dropout:
+            metric = metric.replace("fwd+bwd", "fwd+bwd with dropout per level")
         unit = "samples/s"
     out = {
         "metric": metric,
@@ -302,7 +308,8 @@ def main():
                    "grid": cfg.grid,
                    "c_in": cfg.c_in, "classes": cfg.n_classes, "batch": cfg.batch,
                    "input_active_fraction": round(float(mean_sizes[0]) / (cfg.batch * cfg.grid ** 2), 4),
-                   "step": "rulebook build + forward (logits)" if infer else "rulebook build + forward + backward"},
+                   "step": "rulebook build + forward (logits)" if infer else "rulebook build + forward + backward",
+                   **({"dropout": list(cfg.dropout)} if cfg.dropout else {})},
         "conv_gemm_gflop_per_step": round(conv_flops / 1e9, 3),
         "roofline": roofline,
         "kernel_breakdown": breakdown,

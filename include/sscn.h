@@ -91,8 +91,10 @@ typedef struct {
   int32_t n_classes;
   int32_t batch_max;
   int32_t max_active;
-  int32_t dtype; /* sscn_dtype */
-  int32_t arch;  /* sscn_arch */
+  int32_t dtype;   /* sscn_dtype */
+  int32_t arch;    /* sscn_arch */
+  int32_t dropout; /* nonzero: the workspace also holds the dropped copies of every
+                      dropout level's input, so sscn_set_dropout may set rates > 0 */
 } sscn_net_desc;
 
 typedef struct sscn_net sscn_net; /* opaque host-side plan */
@@ -172,6 +174,33 @@ SSCN_API sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void
  * the input features, in the caller's site order. */
 SSCN_API sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db, void* d_dfeats, void* stream);
 
+/* Dropout per level (Section 2.1), applied by every following training pass
+ * (sscn_forward with labels, and its sscn_backward); inference passes ignore it.
+ * h_rates[n_rates] (host, n_rates = ell + 2): the rate for the input of each
+ * convolution that is not 1x1, in stage order (ell + 1 of them; Section 2.2
+ * applies no dropout to the 1x1 network-in-network layers), then the rate for
+ * the softmax layer's input; each in [0, 1).  n_rates = 0 (h_rates may be null)
+ * switches dropout off.  seed: the 64-bit key of the masks.
+ *
+ * Inverted dropout: a kept value is multiplied by 1/(1 - p) (a float32 value),
+ * a dropped one becomes 0; the backward pass applies the same factors.  Only
+ * rows 1.. (active sites) of a level's input are dropped: the ground row, the
+ * state shared by all inactive sites, passes unchanged.  Element (channel c)
+ * of the row with key q of level j is kept when word c % 4 of
+ * sscn_philox4x32_10(counter = {q, c / 4, j, 0}, key = {seed mod 2^32,
+ * seed / 2^32}) is >= floor(p * 2^32); q is the site key (b*S + y)*S + x of
+ * the level's input layer, or the sample index b for the softmax input.
+ * Rates > 0 need a net created with desc.dropout != 0, else
+ * SSCN_ERR_INVALID_ARGUMENT; so does a wrong n_rates or a rate outside [0, 1).
+ * A successful call also ends the current pass: sscn_backward then returns
+ * SSCN_ERR_BAD_STATE until the next training sscn_forward. */
+SSCN_API sscn_status sscn_set_dropout(sscn_net* net, const double* h_rates, int32_t n_rates, uint64_t seed);
+
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011), the generator of the
+ * dropout masks, evaluated on the host: out = the four output words for the
+ * four-word counter and two-word key (host arrays).  For reproducing masks. */
+SSCN_API void sscn_philox4x32_10(const uint32_t counter[4], const uint32_t key[2], uint32_t out[4]);
+
 /* Runs only stage s (1 .. L) of the forward or backward pass on the
  * current workspace contents, with the parameters of the last sscn_forward /
  * sscn_backward.  For checking one kernel group against known inputs.  A
@@ -196,7 +225,8 @@ typedef enum {
   SSCN_KC_HEAD = 6,       /* input scatter, weight packing, softmax, loss, scatter of dh */
   SSCN_KC_GROUND = 7,     /* bias and ground-window sums of a conv not under a
                              pooling layer; ground-row input gradient        */
-  SSCN_KC_COUNT = 8
+  SSCN_KC_DROPOUT = 8,    /* dropped copies of the dropout levels' inputs      */
+  SSCN_KC_COUNT = 9
 } sscn_kernel_class;
 
 /* While enabled, every launch of a kernel whose class bit (1 << class) is set

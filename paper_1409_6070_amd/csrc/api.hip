@@ -3,6 +3,7 @@
 // Sections 2.1 and 2.3).  Host code only; every kernel is enqueued on the
 // caller's stream and no call synchronises except sscn_layer_sizes().
 
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -20,6 +21,7 @@ struct LayerPlan {
   int S, C, Cp, F, A, Wd;
   int64_t cap;
   int conv_index;  // convolution layers: parameter index
+  int drop_level;  // convolutions that are not 1x1: dropout level of their input, else -1
   // workspace pointers
   uint64_t* bits;
   int32_t* wpre;
@@ -31,6 +33,7 @@ struct LayerPlan {
   int32_t* rules;
   int32_t* rules_t;
   uint8_t* argmax;
+  void* Xd;  // dropped copy of X when this layer feeds a dropout level (dropout workspace only)
 };
 
 struct ParamPlan {
@@ -84,6 +87,7 @@ struct sscn_net {
   float* gpart;  // split-K partials of the gather GEMMs
   float* D0;
   float* ppart;
+  void* hdrop;  // the softmax layer's dropped input [batch_max][Cp_top] (dropout workspace only)
   size_t ws_bytes;
   int32_t max_words;
   // bound state
@@ -98,6 +102,11 @@ struct sscn_net {
   bool want_dfeats;
   float* logits;
   const int32_t* labels;
+  // dropout (Section 2.1): rates per level, set by sscn_set_dropout
+  int n_rates = 0;
+  double rates[MAX_LAYERS] = {};
+  uint64_t seed = 0;
+  bool drop_on = false;  // the current pass applies dropout (a training pass with rates set)
   // kernel timing (HIP events around launcher calls of the selected classes)
   uint32_t tmask = 0;
   std::vector<hipEvent_t> ev_pool;
@@ -187,7 +196,14 @@ static void carve(sscn_net* net, void* base) {
       L.rules = L.rules_t = nullptr;
       L.argmax = nullptr;
     }
+    L.Xd = nullptr;
   }
+  if (net->d.dropout)
+    for (int s = 1; s < net->nlayers; ++s)
+      if (net->L[s].drop_level >= 0) {
+        LayerPlan& Lb = net->L[s - 1];
+        Lb.Xd = cv.take((size_t)(Lb.cap + 1) * Lb.Cp * net->esz);
+      }
   for (int p = 0; p < net->nparams; ++p) {
     ParamPlan& P = net->P[p];
     P.WpF = cv.take((size_t)P.NpadF * P.KpadF * net->esz);
@@ -207,6 +223,7 @@ static void carve(sscn_net* net, void* base) {
   net->gpart = (float*)cv.take(std::max<size_t>(max_gpart, 1) * 4);
   net->D0 = (float*)cv.take(max_d0 * 4);
   net->ppart = (float*)cv.take((size_t)net->pool_parts * (2 + 9) * max_cp * 4);
+  net->hdrop = net->d.dropout ? cv.take((size_t)B * Lt.Cp * net->esz) : nullptr;
   net->ws_bytes = cv.off + 256;
 }
 
@@ -296,10 +313,12 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   L[0].S = (int)N;
   L[0].C = d.c_in;
   L[0].cap = d.max_active;
-  int S = (int)N, C = d.c_in, ci = 0;
+  int S = (int)N, C = d.c_in, ci = 0, dl = 0;
+  L[0].drop_level = -1;
   for (int s = 1; s < net->nlayers; ++s) {
     LayerPlan& l = L[s];
     l = LayerPlan{};
+    l.drop_level = (kinds[s - 1] == 1 && Fs[s - 1] > 1) ? dl++ : -1;
     const int64_t below = L[s - 1].cap;
     if (kinds[s - 1] == 1) {
       l.kind = 1;
@@ -389,6 +408,10 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.bn_w = wgrad_bn(P.c_out);
     P.Npad_w = (int)round_up(P.c_out, P.bn_w);
     P.nchunks = 1;
+  }
+  if (dl != d.ell + 1) {
+    delete net;
+    return SSCN_ERR_INVALID_ARGUMENT;
   }
   carve(net, nullptr);
   *out = net;
@@ -488,13 +511,43 @@ sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream) {
   return SSCN_OK;
 }
 
+// Dropout of level j in the current pass (off unless a training pass with rate > 0).
+static DropArgs drop_args(const sscn_net* net, int j, const int32_t* keys) {
+  DropArgs d{};
+  if (!net->drop_on || j < 0 || j >= net->n_rates || !(net->rates[j] > 0.0)) return d;
+  const double p = net->rates[j];
+  d.keys = keys;
+  d.thr = (uint32_t)std::floor(p * 4294967296.0);
+  d.level = (uint32_t)j;
+  d.seed_lo = (uint32_t)net->seed;
+  d.seed_hi = (uint32_t)(net->seed >> 32);
+  d.scale = (float)(1.0 / (1.0 - p));
+  d.on = 1;
+  return d;
+}
+
+// Dropout on the input of convolution s (rows of layer s - 1, keyed by its sites).
+static DropArgs conv_drop(const sscn_net* net, int s) {
+  return drop_args(net, net->L[s].drop_level, net->L[s - 1].sites);
+}
+
+// Dropout on the softmax layer's input (the last level, keyed by sample).
+static DropArgs head_drop(const sscn_net* net) { return drop_args(net, net->d.ell + 1, nullptr); }
+
 static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
   if (L.kind == 1) {
     const ParamPlan& P = net->P[L.conv_index];
+    const DropArgs dr = conv_drop(net, s);
+    if (dr.on) {
+      const hipError_t e = timed(net, SSCN_KC_DROPOUT, st, [&] {
+        return launch_dropout_rows(net->bf16, Lb.X, Lb.Xd, Lb.Cp, net->counts + s - 1, Lb.cap + 1, dr, st);
+      });
+      if (e != hipSuccess) return e;
+    }
     GemmArgs g{};
-    g.src = Lb.X;
+    g.src = dr.on ? Lb.Xd : Lb.X;
     g.src_stride = Lb.Cp;
     g.rmap = L.rules;
     g.A = L.A;
@@ -605,7 +658,7 @@ static WGradArgs conv_wgrad_args(const sscn_net* net, int s) {
   const int ci = L.conv_index;
   const ParamPlan& P = net->P[ci];
   WGradArgs w{};
-  w.src = Lb.X;
+  w.src = conv_drop(net, s).on ? Lb.Xd : Lb.X;  // the input the forward pass used
   w.src_stride = Lb.Cp;
   w.rmap = L.rules;
   w.A = L.A;
@@ -691,7 +744,13 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
     g.row_begin = 0;
   }
   set_plan(g, P.pd, P.rows_d, net->gpart);
-  return timed_gemm(net, g, Lb.cap + 1, st);
+  hipError_t e = timed_gemm(net, g, Lb.cap + 1, st);
+  const DropArgs dr = conv_drop(net, s);
+  if (e == hipSuccess && dr.on)  // through the dropout of this convolution's input: rows >= 1, in place
+    e = timed(net, SSCN_KC_DROPOUT, st, [&] {
+      return launch_dropout_rows(net->bf16, Lb.grad, Lb.grad, Lb.Cp, net->counts + s - 1, Lb.cap + 1, dr, st);
+    });
+  return e;
 }
 
 sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* h_W, const float* const* h_b,
@@ -710,6 +769,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   }
   net->logits = d_logits;
   net->labels = d_labels;
+  net->drop_on = train && net->n_rates > 0;
   const LayerPlan& L0 = net->L[0];
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_scatter_input(net->bf16, d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, st);
@@ -730,10 +790,15 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   // softmax layer on each sample's top-layer row
   const LayerPlan& Lt = net->L[net->nlayers - 1];
   const ParamPlan& P = net->P[net->nconv];
+  const DropArgs hdr = head_drop(net);
+  if (hdr.on && timed(net, SSCN_KC_DROPOUT, st, [&] {
+        return launch_head_drop(net->bf16, Lt.X, net->head_rows, net->batch, Lt.Cp, net->hdrop, hdr, st);
+      }) != hipSuccess)
+    return SSCN_ERR_HIP;
   GemmArgs g{};
-  g.src = Lt.X;
+  g.src = hdr.on ? net->hdrop : Lt.X;
   g.src_stride = Lt.Cp;
-  g.rmap = net->head_rows;
+  g.rmap = hdr.on ? nullptr : net->head_rows;
   g.A = 1;
   g.cseg = Lt.Cp;
   g.K = Lt.Cp;
@@ -800,7 +865,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
     return SSCN_ERR_HIP;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp,
-                                   net->slope, st);
+                                   net->slope, head_drop(net), st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
   // Stages from the top down, all on the caller's stream: each convolution's
@@ -826,9 +891,10 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   {
     WGradArgs& f = w[nw++];
     f = WGradArgs{};
-    f.src = Lt.X;
+    const bool hd = head_drop(net).on;  // the softmax layer read its dropped input
+    f.src = hd ? net->hdrop : Lt.X;
     f.src_stride = Lt.Cp;
-    f.rmap = net->head_rows;
+    f.rmap = hd ? nullptr : net->head_rows;
     f.A = 1;
     f.cseg = Lt.Cp;
     f.m_ones = P.m_ones;
@@ -849,6 +915,33 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   }
   if (run_wgrads(net, w, nw, st) != hipSuccess) return SSCN_ERR_HIP;
   return SSCN_OK;
+}
+
+sscn_status sscn_set_dropout(sscn_net* net, const double* h_rates, int32_t n_rates, uint64_t seed) {
+  if (!net) return SSCN_ERR_INVALID_ARGUMENT;
+  if (n_rates == 0) {
+    net->n_rates = 0;
+    net->forwarded = false;
+    return SSCN_OK;
+  }
+  if (!h_rates || n_rates != net->d.ell + 2) return SSCN_ERR_INVALID_ARGUMENT;
+  bool any = false;
+  for (int j = 0; j < n_rates; ++j) {
+    if (!(h_rates[j] >= 0.0 && h_rates[j] < 1.0)) return SSCN_ERR_INVALID_ARGUMENT;
+    any = any || h_rates[j] > 0.0;
+  }
+  if (any && !net->d.dropout) return SSCN_ERR_INVALID_ARGUMENT;
+  for (int j = 0; j < n_rates; ++j) net->rates[j] = h_rates[j];
+  net->n_rates = n_rates;
+  net->seed = seed;
+  net->forwarded = false;  // a backward pass must follow a forward pass with the same masks
+  return SSCN_OK;
+}
+
+void sscn_philox4x32_10(const uint32_t counter[4], const uint32_t key[2], uint32_t out[4]) {
+  if (!counter || !key || !out) return;
+  const Philox4 r = philox4x32_10(counter[0], counter[1], counter[2], counter[3], key[0], key[1]);
+  for (int e = 0; e < 4; ++e) out[e] = r.w[e];
 }
 
 sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream) {

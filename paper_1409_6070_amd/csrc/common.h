@@ -51,6 +51,66 @@ __device__ inline float act_factor(float y, float slope) {
   return pos ? 1.f : slope;
 }
 
+// ---------------------------------------------------------------------------
+// dropout masks (Section 2.1)
+//
+// Philox4x32-10, the counter-based generator of Salmon, Moraes, Dror and Shaw
+// (SC 2011), from its definition: ten rounds over a four-word counter under a
+// two-word key; a round takes the 64-bit products M0*c0 and M1*c2 and maps
+// (c0, c1, c2, c3) to (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1,
+// lo(M0 c0)); the key advances by two Weyl constants between rounds.
+
+struct Philox4 {
+  uint32_t w[4];
+};
+
+__host__ __device__ inline Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                                 uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return Philox4{{c0, c1, c2, c3}};
+}
+
+// Inverted dropout of one level: element (row key q, channel c) is kept, and
+// multiplied by scale = 1/(1 - p), when word c % 4 of
+// philox4x32_10(q, c / 4, level, 0; seed_lo, seed_hi) is >= thr = floor(p 2^32);
+// otherwise it becomes 0.  Row keys: the packed site keys (b*S + y)*S + x of
+// rows 1.. of a layer (keys[r - 1] for row r; row 0, the ground state, is never
+// dropped), or the sample index for the softmax layer's input (keys null).
+struct DropArgs {
+  const int32_t* keys;
+  uint32_t thr;
+  uint32_t level;
+  uint32_t seed_lo, seed_hi;
+  float scale;
+  int32_t on;  // 0: no dropout
+};
+
+// Factors of the four channels 4*c4 .. 4*c4 + 3 of row key q.
+__device__ inline void drop_factors4(const DropArgs& d, uint32_t q, uint32_t c4, float f[4]) {
+  const Philox4 r = philox4x32_10(q, c4, d.level, 0u, d.seed_lo, d.seed_hi);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) f[e] = r.w[e] >= d.thr ? d.scale : 0.f;
+}
+
+__device__ inline float drop_factor(const DropArgs& d, uint32_t q, int c) {
+  const Philox4 r = philox4x32_10(q, (uint32_t)c >> 2, d.level, 0u, d.seed_lo, d.seed_hi);
+  const int e = c & 3;  // selects, not a dynamically indexed array
+  const uint32_t w = e == 0 ? r.w[0] : e == 1 ? r.w[1] : e == 2 ? r.w[2] : r.w[3];
+  return w >= d.thr ? d.scale : 0.f;
+}
+
 struct LayerBits {
   uint64_t* bits;    // [batch * S * Wd] row-aligned occupancy words
   int32_t* wpre;     // [batch * S * Wd] exclusive popcount prefix within the sample

@@ -157,20 +157,22 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_head_scatter(const float* __restrict__ dh, int32_t dh_stride,
                                                       const int32_t* __restrict__ head_rows, int32_t batch,
                                                       const T* __restrict__ Y_top, T* grad_top, int32_t cp,
-                                                      float slope) {
+                                                      float slope, DropArgs drop) {
   const int c = blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= cp) return;
   const int b = blockIdx.y;
   if (b < batch) {
     const int r = head_rows[b];
     if (r == 0) return;
-    const float f = act_factor(Elem<T>::to_f32(Y_top[(int64_t)r * cp + c]), slope);
+    float f = act_factor(Elem<T>::to_f32(Y_top[(int64_t)r * cp + c]), slope);
+    if (drop.on) f *= drop_factor(drop, (uint32_t)b, c);
     grad_top[(int64_t)r * cp + c] = Elem<T>::from_f32(dh[(int64_t)b * dh_stride + c] * f);
     return;
   }
   float g0 = 0.f;
   for (int bb = 0; bb < batch; ++bb)
-    if (head_rows[bb] == 0) g0 += dh[(int64_t)bb * dh_stride + c];
+    if (head_rows[bb] == 0)
+      g0 += dh[(int64_t)bb * dh_stride + c] * (drop.on ? drop_factor(drop, (uint32_t)bb, c) : 1.f);
   grad_top[c] = Elem<T>::from_f32(g0 * act_factor(Elem<T>::to_f32(Y_top[c]), slope));
 }
 
@@ -247,14 +249,14 @@ hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* la
 
 hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
                                int32_t batch, const void* Y_top, void* grad_top, int32_t cp, float slope,
-                               hipStream_t st) {
+                               const DropArgs& drop, hipStream_t st) {
   dim3 grid((cp + 255) / 256, batch + 1);
   if (bf16)
     hipLaunchKernelGGL(k_head_scatter<__bf16>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
-                       (const __bf16*)Y_top, (__bf16*)grad_top, cp, slope);
+                       (const __bf16*)Y_top, (__bf16*)grad_top, cp, slope, drop);
   else
     hipLaunchKernelGGL(k_head_scatter<float>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
-                       (const float*)Y_top, (float*)grad_top, cp, slope);
+                       (const float*)Y_top, (float*)grad_top, cp, slope, drop);
   return hipGetLastError();
 }
 

@@ -205,9 +205,18 @@ struct PackArgs {
 hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st);
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
                                void* dlogits, int32_t dl_stride, float* loss_part, float* loss, hipStream_t st);
+// drop: the softmax layer input's dropout (row key = sample), or off
 hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
                                int32_t batch, const void* Y_top, void* grad_top, int32_t cp, float slope,
-                               hipStream_t st);
+                               const DropArgs& drop, hipStream_t st);
+
+// dropout.hip: Xd = X with rows 1 .. *n_rows dropped (row 0 copied; X == Xd:
+// in place, row 0 untouched); the softmax layer's input hd[b] =
+// X_top[head_rows[b]] dropped with row key b
+hipError_t launch_dropout_rows(bool bf16, const void* X, void* Xd, int32_t cp, const int32_t* n_rows, int64_t max_rows,
+                               const DropArgs& d, hipStream_t st);
+hipError_t launch_head_drop(bool bf16, const void* X_top, const int32_t* head_rows, int32_t batch, int32_t cp,
+                            void* hd, const DropArgs& d, hipStream_t st);
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t st);
 
 }  // namespace sscn

@@ -33,8 +33,10 @@ EXPORTED = [
     "sscn_net_create", "sscn_net_destroy", "sscn_status_string", "sscn_net_num_params", "sscn_net_param_shape",
     "sscn_net_workspace_bytes", "sscn_rulebook_build", "sscn_layer_sizes", "sscn_forward", "sscn_backward",
     "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get", "sscn_timing_enable", "sscn_timing_collect",
+    "sscn_set_dropout", "sscn_philox4x32_10",
 ]
-KERNEL_CLASSES = ["rulebook", "gather_gemm", "wgrad", "wgrad_reduce", "pool_fwd", "pool_bwd", "head", "ground"]
+KERNEL_CLASSES = ["rulebook", "gather_gemm", "wgrad", "wgrad_reduce", "pool_fwd", "pool_bwd", "head", "ground",
+                  "dropout"]
 
 
 class SSCNError(RuntimeError):
@@ -46,7 +48,7 @@ class SSCNError(RuntimeError):
 
 class NetDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32)
-                for n in ("ell", "k", "c_in", "n_classes", "batch_max", "max_active", "dtype", "arch")]
+                for n in ("ell", "k", "c_in", "n_classes", "batch_max", "max_active", "dtype", "arch", "dropout")]
 
 
 class LayerView(ctypes.Structure):
@@ -87,6 +89,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sscn_layer_view_get": (I32, [VP, I32, P(LayerView)]),
         "sscn_timing_enable": (I32, [VP, ctypes.c_uint32]),
         "sscn_timing_collect": (I32, [VP, I32, P(I32), P(ctypes.c_float), VP]),
+        "sscn_set_dropout": (I32, [VP, P(ctypes.c_double), I32, ctypes.c_uint64]),
+        "sscn_philox4x32_10": (None, [P(ctypes.c_uint32), P(ctypes.c_uint32), P(ctypes.c_uint32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -177,6 +181,21 @@ def sscn_layer_view_get(net, layer) -> LayerView:
     return v
 
 
+def sscn_set_dropout(net, rates: Optional[Sequence[float]], seed: int) -> None:
+    rates = list(rates or [])
+    arr = (ctypes.c_double * max(len(rates), 1))(*rates)
+    _check(load_library().sscn_set_dropout(net, arr if rates else None, len(rates), seed & (2 ** 64 - 1)),
+           "sscn_set_dropout")
+
+
+def sscn_philox4x32_10(counter: Sequence[int], key: Sequence[int]) -> List[int]:
+    c = (ctypes.c_uint32 * 4)(*counter)
+    k = (ctypes.c_uint32 * 2)(*key)
+    out = (ctypes.c_uint32 * 4)()
+    load_library().sscn_philox4x32_10(c, k, out)
+    return list(out)
+
+
 def sscn_timing_enable(net, class_mask: int) -> None:
     _check(load_library().sscn_timing_enable(net, class_mask), "sscn_timing_enable")
 
@@ -196,7 +215,7 @@ class SparseDeepCNet:
     """DeepCNet(ell, k) or DeepCNiN(ell, k) on the GPU through libsscn; torch supplies memory and the stream."""
 
     def __init__(self, ell: int, k: int, c_in: int, n_classes: int, batch_max: int, max_active: int,
-                 dtype: str = "bf16", device: str = "cuda", arch: str = "deepcnet"):
+                 dtype: str = "bf16", device: str = "cuda", arch: str = "deepcnet", dropout: bool = False):
         if dtype not in ("f32", "bf16"):
             raise ValueError(dtype)
         if arch not in ARCHS:
@@ -208,7 +227,7 @@ class SparseDeepCNet:
         self.device = torch.device(device)
         self.nlayers = (3 * ell + 3) if arch == "deepcnin" else (2 * ell + 2)
         desc = NetDesc(ell, k, c_in, n_classes, batch_max, max_active, SSCN_BF16 if dtype == "bf16" else SSCN_F32,
-                       ARCHS.index(arch))
+                       ARCHS.index(arch), int(bool(dropout)))
         self.handle = sscn_net_create(desc)
         self.ws_bytes = sscn_net_workspace_bytes(self.handle)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
@@ -236,6 +255,11 @@ class SparseDeepCNet:
         self._coords = coords
         sscn_rulebook_build(self.handle, coords.data_ptr() if self.n else None, self.n, batch, self.ws.data_ptr(),
                             self.ws_bytes, _stream())
+
+    def set_dropout(self, rates: Optional[Sequence[float]], seed: int = 0) -> None:
+        """Dropout rates per level (ell + 2: each convolution that is not 1x1, then the softmax
+        input) for the following training passes; None switches it off."""
+        sscn_set_dropout(self.handle, rates, seed)
 
     def layer_sizes(self) -> List[int]:
         return sscn_layer_sizes(self.handle, self.nlayers, _stream())

@@ -55,7 +55,7 @@ class Pair:
     """One problem run through both paths."""
 
     def __init__(self, ell, k, c_in, n_classes, batch, coords, feats, Ws, bs, labels, dtype,
-                 max_active=None, want_dfeats=True, run_oracle=True, arch="deepcnet"):
+                 max_active=None, want_dfeats=True, run_oracle=True, arch="deepcnet", rates=None, dseed=0):
         self.dtype = dtype
         self.batch = batch
         dev = torch.device("cuda")
@@ -65,7 +65,9 @@ class Pair:
         n = int(np.asarray(coords).shape[0])
         self.arch = arch
         self.net = GpuNet(ell, k, c_in, n_classes, batch_max=max(batch, 1), max_active=max_active or max(n, 1),
-                          dtype=dtype, arch=arch)
+                          dtype=dtype, arch=arch, dropout=rates is not None)
+        if rates is not None:
+            self.net.set_dropout(rates, dseed)
         self.coords_d = torch.tensor(np.asarray(coords, dtype=np.int32).reshape(-1, 3)).to(dev).contiguous()
         self.feats_d = feats_t.to(dev).contiguous()
         self.Ws_d = [w.to(dev).contiguous() for w in Ws_t]
@@ -77,6 +79,7 @@ class Pair:
         if run_oracle:
             self.o = Oracle(ell, k, c_in, n_classes, dtype, arch)
             self.o.build(np.asarray(coords), batch)
+            self.o.set_dropout(rates, dseed)
             self.o.forward(feats_t.double().numpy(), [w.double().numpy() for w in Ws_t],
                            [b.double().numpy() for b in bs_t], labels)
             self.o.backward()

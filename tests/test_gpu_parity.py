@@ -80,7 +80,8 @@ def test_workload_parity_full_size(name, dtype):
     b, Ws, bs, labels = _config_case(cfg, dtype)
     log(f"[workload] {name} {dtype} n={b.n} batch={cfg.batch}")
     pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, dtype,
-                max_active=int(b.n * 1.25), arch=cfg.arch).run_gpu()
+                max_active=int(b.n * 1.25), arch=cfg.arch, rates=list(cfg.dropout) or None,
+                dseed=cfg.dropout_seed).run_gpu()
     check_structure(pair)
     rep = check_values(pair)
     worst = {k_: v for k_, v in rep.items() if not k_.startswith(("argmax", "relu"))}

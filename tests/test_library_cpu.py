@@ -24,7 +24,7 @@ def _declared():
 def test_library_exports_every_declared_symbol():
     lib = sscn.load_library()
     names = _declared()
-    assert len(names) >= 13
+    assert len(names) >= 15
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(sscn.EXPORTED) == names
@@ -92,3 +92,49 @@ def test_host_checked_errors_need_no_gpu():
         assert lib.sscn_layer_view_get(h, 0, ctypes.byref(v)) == 5  # no workspace bound yet
     finally:
         sscn.sscn_net_destroy(h)
+
+
+def _kat_rows():
+    rows = []
+    with open(os.path.join(ROOT, "tests", "golden", "philox4x32_10_kat.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                rows.append([int(t, 16) for t in line.split()])
+    return rows
+
+
+def test_library_generator_matches_published_vectors_and_oracle():
+    """The library's Philox4x32-10 (host build of the device code) against the generator's
+    published known-answer vectors, and against the oracle's separate implementation."""
+    from oracle.philox import philox4x32_10 as oracle_philox
+    import numpy as np
+
+    for row in _kat_rows():
+        assert sscn.sscn_philox4x32_10(row[:4], row[4:6]) == row[6:]
+    rng = np.random.default_rng(1)
+    for _ in range(200):
+        c = [int(x) for x in rng.integers(0, 2 ** 32, 4, dtype=np.uint64)]
+        k = [int(x) for x in rng.integers(0, 2 ** 32, 2, dtype=np.uint64)]
+        assert sscn.sscn_philox4x32_10(c, k) == [int(w) for w in oracle_philox(*c, *k)]
+
+
+def test_set_dropout_host_checks():
+    plain = sscn.sscn_net_create(sscn.NetDesc(3, 4, 1, 5, 4, 100, sscn.SSCN_BF16, 0, 0))
+    drop = sscn.sscn_net_create(sscn.NetDesc(3, 4, 1, 5, 4, 100, sscn.SSCN_BF16, 0, 1))
+    nin = sscn.sscn_net_create(sscn.NetDesc(3, 4, 1, 5, 4, 100, sscn.SSCN_BF16, 1, 1))
+    try:
+        # dropped copies of every level's input make the workspace larger
+        assert sscn.sscn_net_workspace_bytes(drop) > sscn.sscn_net_workspace_bytes(plain)
+        sscn.sscn_set_dropout(plain, [0.0] * 5, 1)  # rate 0 needs no workspace
+        sscn.sscn_set_dropout(plain, None, 1)
+        for bad_net, rates in ((plain, [0.5] * 5), (drop, [0.5] * 4), (drop, [0.5] * 6), (drop, [0.1, 0.2, 1.0, 0, 0]),
+                               (drop, [0.1, -0.1, 0, 0, 0]), (drop, [float("nan")] + [0.0] * 4)):
+            with pytest.raises(sscn.SSCNError) as e:
+                sscn.sscn_set_dropout(bad_net, rates, 1)
+            assert e.value.name == "SSCN_ERR_INVALID_ARGUMENT"
+        sscn.sscn_set_dropout(drop, [0.0, 0.0, 0.5, 0.5, 0.5], 2 ** 64 - 1)
+        sscn.sscn_set_dropout(nin, [0.1, 0.2, 0.3, 0.4, 0.5], 7)  # ell + 2 rates for DeepCNiN too
+        sscn.sscn_set_dropout(drop, None, 0)
+    finally:
+        for h in (plain, drop, nin):
+            sscn.sscn_net_destroy(h)

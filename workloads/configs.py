@@ -1,4 +1,4 @@
-"""The five synthetic workloads the hot path is tested and measured on.
+"""The synthetic workloads the hot path is tested and measured on.
 
 Each names a DeepCNet(ell, k) (Section 2.1), an input feature count M, a batch,
 a class count for the softmax head, a storage dtype, and an input generator
@@ -12,7 +12,8 @@ with its parameters.  The generators stand in for the paper's datasets:
 * the DeepCNet(5,50) pen strokes also feed a DeepCNiN(5,50) (Section 2.2);
 * grey-level digit strokes of about 150 pixels in the middle of a 96 x 96 grid
   stand in for MNIST (Section 2.5), on the small network the paper times at test
-  time (DeepCNet(5,10), Section 3.2): a forward-only ("infer") workload.
+  time (DeepCNet(5,10), Section 3.2): a forward-only ("infer") workload;
+* the DeepCNet(5,50) pen strokes once more with dropout per level (Section 2.1).
 """
 
 from dataclasses import dataclass, field
@@ -33,6 +34,11 @@ class WorkloadConfig:
     seed: int = 0  # input seed; weights use 100 + seed, labels 200 + seed
     mode: str = "train"  # "train": build + forward + backward; "infer": build + forward (logits)
     arch: str = "deepcnet"  # or "deepcnin" (Section 2.2)
+    dropout: Tuple[float, ...] = ()  # rates per level (ell + 2, Section 2.1); () for none
+
+    @property
+    def dropout_seed(self) -> int:
+        return 300 + self.seed
 
     @property
     def grid(self) -> int:
@@ -108,6 +114,17 @@ CONFIGS = [
         generator="strokes",
         gen_args=dict(strokes=(1, 20), points=(10, 60), box=64, sigma=2.0, features="ones"),
         seed=6, arch="deepcnin",
+    ),
+    # DeepCNet(5,50) pen strokes trained with dropout per level (Section 2.1): none
+    # on the three lowest convolutions, one half on the three above them and on the
+    # softmax layer's input -- the profile of the paper's dropout DeepCNet(5,60)
+    # (Section 3.2).
+    WorkloadConfig(
+        name="deepcnet5_50_strokes_dropout_b100",
+        ell=5, k=50, c_in=1, batch=100, n_classes=3755, dtypes=("bf16",),
+        generator="strokes",
+        gen_args=dict(strokes=(1, 20), points=(10, 60), box=64, sigma=2.0, features="ones"),
+        seed=7, dropout=(0.0, 0.0, 0.0, 0.5, 0.5, 0.5, 0.5),
     ),
 ]
 
