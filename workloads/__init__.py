@@ -1,8 +1,10 @@
 """Seeded synthetic inputs for the sparse DeepCNet hot path.
 
-This module only draws random numbers and rasterises pen strokes: it holds none
-of the network's arithmetic, so the CPU oracle and the HIP path can both take
-their inputs from it without sharing any of the method.
+This module only draws random numbers and rasterises pen strokes for the picture
+inputs (the histogram encoding of raw pen paths is a method step and lives on
+both sides, not here): it holds none of the network's arithmetic, so the CPU
+oracle and the HIP path can both take their inputs from it without sharing any
+of the method.
 
 The paper's workloads (online handwriting, MNIST, CIFAR; Sections 2.4, 2.5 and
 3) are datasets that are not available here.  The generators below stand in for
@@ -18,9 +20,12 @@ from .synth import (
     he_params,
     make_batch,
     make_batches,
+    make_paths,
     patch_batch,
+    Paths,
     random_labels,
     stroke_batch,
+    stroke_paths,
 )
 
 __all__ = [
@@ -32,7 +37,10 @@ __all__ = [
     "he_params",
     "make_batch",
     "make_batches",
+    "make_paths",
     "patch_batch",
+    "Paths",
+    "stroke_paths",
     "random_labels",
     "stroke_batch",
 ]

@@ -74,6 +74,57 @@ def _strokes_one(rng: np.random.Generator, grid: int, strokes, points, box, sigm
     return list(seen.keys())
 
 
+@dataclass
+class Paths:
+    """A batch of raw pen paths: stroke s is ``points[stroke_begin[s]:stroke_begin[s + 1]]``
+    ((y, x) integer grid points, in drawing order) of sample ``stroke_sample[s]``."""
+
+    points: np.ndarray  # int32 [P, 2]
+    stroke_begin: np.ndarray  # int32 [S + 1]
+    stroke_sample: np.ndarray  # int32 [S]
+    batch: int
+    grid: int
+
+    @property
+    def n_points(self) -> int:
+        return int(self.points.shape[0])
+
+    @property
+    def n_strokes(self) -> int:
+        return int(self.stroke_sample.shape[0])
+
+
+def _walk(rng: np.random.Generator, n_pts: int, lo: int, hi: int, sigma: float) -> np.ndarray:
+    """One random-walk stroke: a uniform start in [lo, hi]^2, then round(N(0, sigma^2)) steps, clamped."""
+    y = int(rng.integers(lo, hi + 1))
+    x = int(rng.integers(lo, hi + 1))
+    steps = np.rint(rng.normal(0.0, sigma, size=(n_pts - 1, 2))).astype(np.int64)
+    pts = [(y, x)]
+    for sy, sx in steps:
+        y = min(max(y + int(sy), lo), hi)
+        x = min(max(x + int(sx), lo), hi)
+        pts.append((y, x))
+    return np.asarray(pts, dtype=np.int32)
+
+
+def stroke_paths(rng: np.random.Generator, batch: int, grid: int, strokes=(1, 20), points=(10, 60), box=64,
+                 sigma=2.0) -> Paths:
+    """Random-walk pen paths as in ``stroke_batch``, left as point sequences (not rasterised):
+    the input of the 8-direction histogram encoding of Section 2.4."""
+    lo = (grid - box) // 2
+    hi = lo + box - 1
+    pts, begin, sample = [], [0], []
+    for b in range(batch):
+        for _ in range(int(rng.integers(strokes[0], strokes[1] + 1))):
+            w = _walk(rng, int(rng.integers(points[0], points[1] + 1)), lo, hi, sigma)
+            pts.append(w)
+            begin.append(begin[-1] + w.shape[0])
+            sample.append(b)
+    points_arr = np.concatenate(pts, axis=0) if pts else np.zeros((0, 2), np.int32)
+    return Paths(points=points_arr.astype(np.int32), stroke_begin=np.asarray(begin, np.int32),
+                 stroke_sample=np.asarray(sample, np.int32), batch=batch, grid=grid)
+
+
 def stroke_batch(rng: np.random.Generator, batch: int, grid: int, c_in: int, strokes=(1, 20),
                  points=(10, 60), box=64, sigma=2.0, features="ones") -> Batch:
     """Random-walk pen strokes rasterised 1 px wide inside a centred box.
@@ -211,8 +262,18 @@ def random_labels(batch: int, n_classes: int, seed: int) -> np.ndarray:
     return rng.integers(0, n_classes, size=batch).astype(np.int32)
 
 
+def make_paths(cfg: WorkloadConfig, index: int = 0) -> Paths:
+    """Pen-path batch number ``index`` of a workload whose input is encoded from paths."""
+    if cfg.generator != "paths":
+        raise ValueError(f"{cfg.name} does not draw pen paths")
+    rng = np.random.default_rng([cfg.seed, index])
+    return stroke_paths(rng, cfg.batch, cfg.grid, **cfg.gen_args)
+
+
 def make_batch(cfg: WorkloadConfig, index: int = 0) -> Batch:
     """Batch number ``index`` of a workload (seeded by the workload seed and ``index``)."""
+    if cfg.generator == "paths":
+        raise ValueError(f"{cfg.name} draws pen paths: use make_paths and encode them")
     rng = np.random.default_rng([cfg.seed, index])
     if cfg.generator == "strokes":
         return stroke_batch(rng, cfg.batch, cfg.grid, cfg.c_in, **cfg.gen_args)
