@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 import numpy as np  # noqa: E402
 import torch  # noqa: E402
 
-from workloads import get_config, he_params, make_batches, random_labels  # noqa: E402
+from workloads import get_config, he_params, make_batches, make_paths, random_labels  # noqa: E402
 
 DEFAULT_WORKLOAD = "deepcnet5_50_strokes_b100"
 MFMA_PEAK = {"bf16": 2.5e15, "f32": 157.3e12}  # dense MFMA FLOP/s, MI355X
@@ -106,9 +106,14 @@ def read_traffic(kernel, dtype, workload):
         return None
 
 
-def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False):
-    """The oracle, as it stands, on batch 0: build + forward (+ backward unless infer), repeated for ~budget_s."""
+def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False, paths=None):
+    """The oracle, as it stands, on batch 0: build + forward (+ backward unless infer), repeated for ~budget_s.
+
+    With pen paths (``paths``) each repetition is a whole training step: the oracle's encoding,
+    build, forward, backward and SGD update."""
     from oracle import SparseDeepCNet as Oracle
+    from oracle.sgd import sgd_step
+    from oracle.strokes import encode_strokes
 
     try:
         from threadpoolctl import threadpool_info
@@ -116,22 +121,31 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         threads = 1
-    feats = torch.tensor(batch.feats, dtype=torch.float32)
-    Wt = [torch.tensor(W, dtype=torch.float32) for W in Ws]
-    if dtype == "bf16":
-        feats = feats.to(torch.bfloat16)
-        Wt = [w.to(torch.bfloat16) for w in Wt]
-    feats = feats.double().numpy()
-    Wn = [w.double().numpy() for w in Wt]
+    def storage(x):
+        t = torch.tensor(np.asarray(x, np.float64), dtype=torch.float32)
+        return (t.to(torch.bfloat16) if dtype == "bf16" else t).double().numpy()
+
+    feats = storage(batch.feats) if batch is not None else None
+    Wn = [storage(W) for W in Ws]
+    if paths is not None:
+        vW = [np.zeros_like(w) for w in Wn]
+        vb = [np.zeros_like(np.asarray(x, np.float64)) for x in bs]
     reps, t0 = 0, time.perf_counter()
     while True:
         o = Oracle(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, dtype, cfg.arch)
-        o.build(batch.coords, batch.batch)
+        if paths is not None:
+            coords, f = encode_strokes(paths.points, paths.stroke_begin, paths.stroke_sample, paths.batch, paths.grid)
+            feats = storage(f)
+            o.build(coords, paths.batch)
+        else:
+            o.build(batch.coords, batch.batch)
         if cfg.dropout and not infer:
             o.set_dropout(cfg.dropout, cfg.dropout_seed + reps)
         o.forward(feats, Wn, bs, labels)
         if not infer:
-            o.backward()
+            dW, db, _ = o.backward()
+            if cfg.sgd:
+                Wn, _, bs, vW, vb = sgd_step(Wn, bs, dW, db, vW, vb, *cfg.sgd, mode=dtype)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 50:
@@ -145,6 +159,10 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False):
     except OSError:
         pass
     what = "build + forward" if infer else "build + forward + backward"
+    if paths is not None:
+        what = "encode + " + what
+    if cfg.sgd:
+        what += " + SGD update"
     return {"value": round(reps * cfg.batch / el, 3), "unit": "characters/s" if infer else "samples/s",
             "cores": threads, "kind": "oracle",
             "sample": f"batch 0 of {cfg.name} ({cfg.batch} samples), {reps} x ({what}), "
@@ -190,21 +208,46 @@ def main():
     dev = torch.device("cuda:0")
     tdt = torch.bfloat16 if args.dtype == "bf16" else torch.float32
     log(f"[bench] generating {args.batches} batches of {cfg.name}")
-    batches = make_batches(cfg, args.batches)
+    paths = cfg.generator == "paths"
     Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed, cfg.arch)
     labels = random_labels(cfg.batch, cfg.n_classes, cfg.label_seed)
-    Ws_d = [torch.tensor(W, dtype=torch.float32).to(tdt).to(dev).contiguous() for W in Ws]
+    W32_d = [torch.tensor(W, dtype=torch.float32).to(dev).contiguous() for W in Ws]
+    Ws_d = [w.to(tdt).contiguous() for w in W32_d] if args.dtype == "bf16" else W32_d
     bs_d = [torch.tensor(b, dtype=torch.float32).to(dev).contiguous() for b in bs]
+    vW_d = [torch.zeros_like(w) for w in W32_d]
+    vb_d = [torch.zeros_like(b) for b in bs_d]
     lab_d = torch.tensor(labels, dtype=torch.int32, device=dev)
-    inputs = []
-    for b in batches:
-        inputs.append((torch.tensor(b.coords, dtype=torch.int32, device=dev).contiguous(),
-                       torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous()))
-    max_active = max(b.n for b in batches)
+    inputs, raw, path_batches, enc = [], [], [], None
+    if paths:
+        # raw pen paths: every step encodes them on the device (Section 2.4); one
+        # untimed pass learns the site counts that size the encoder and the net
+        from paper_1409_6070_amd.sscn import StrokeEncoder
+        path_batches = [make_paths(cfg, i) for i in range(args.batches)]
+        raw = [tuple(torch.tensor(a, dtype=torch.int32, device=dev).contiguous()
+                     for a in (p.points, p.stroke_begin, p.stroke_sample)) for p in path_batches]
+        probe = StrokeEncoder(cfg.grid, cfg.batch, cfg.batch * cfg.grid * cfg.grid, args.dtype)
+        counts = [int(probe.encode(*r, cfg.batch)[0].shape[0]) for r in raw]
+        del probe
+        max_active = max(counts)
+        enc = StrokeEncoder(cfg.grid, cfg.batch, max_active, args.dtype)
+        batches = []
+    else:
+        batches = make_batches(cfg, args.batches)
+        for b in batches:
+            inputs.append((torch.tensor(b.coords, dtype=torch.int32, device=dev).contiguous(),
+                           torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous()))
+        max_active = max(b.n for b in batches)
     net = SparseDeepCNet(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, batch_max=cfg.batch, max_active=max_active,
                          dtype=args.dtype, arch=cfg.arch, dropout=bool(cfg.dropout))
+
+    def inputs_of(i):
+        if paths:
+            return enc.encode(*raw[i % len(raw)], cfg.batch)  # synchronises: the site count goes to the host
+        return inputs[i % len(inputs)]
+
     sizes = []
-    for c, _ in inputs:
+    for i in range(len(raw) if paths else len(inputs)):
+        c, _ = inputs_of(i)
         net.rulebook_build(c, cfg.batch)
         sizes.append(net.layer_sizes())
     torch.cuda.synchronize()
@@ -212,7 +255,7 @@ def main():
     infer = cfg.mode == "infer"
 
     def step(i):
-        c, f = inputs[i % len(inputs)]
+        c, f = inputs_of(i)
         net.rulebook_build(c, cfg.batch)
         if infer:
             net.forward(f, Ws_d, bs_d, None)
@@ -221,6 +264,8 @@ def main():
                 net.set_dropout(cfg.dropout, cfg.dropout_seed + i)
             net.forward(f, Ws_d, bs_d, lab_d)
             net.backward()
+            if cfg.sgd:
+                net.sgd_step(W32_d, Ws_d if args.dtype == "bf16" else None, bs_d, vW_d, vb_d, *cfg.sgd)
 
     log(f"[bench] warmup {args.warmup} steps")
     for i in range(args.warmup):
@@ -289,6 +334,9 @@ def main():
                       "sparse-conv fwd+bwd samples/sec; GEMM % MFMA peak")
         if cfg.dropout:
             metric = metric.replace("fwd+bwd", "fwd+bwd with dropout per level")
+        if paths:
+            metric = (f"DeepCNet({cfg.ell},{cfg.k}) M=9 training step (8-direction histogram encoding + "
+                      "fwd + bwd + SGD) samples/sec; GEMM % MFMA peak")
         unit = "samples/s"
     out = {
         "metric": metric,
@@ -308,7 +356,9 @@ def main():
                    "grid": cfg.grid,
                    "c_in": cfg.c_in, "classes": cfg.n_classes, "batch": cfg.batch,
                    "input_active_fraction": round(float(mean_sizes[0]) / (cfg.batch * cfg.grid ** 2), 4),
-                   "step": "rulebook build + forward (logits)" if infer else "rulebook build + forward + backward",
+                   "step": ("rulebook build + forward (logits)" if infer else
+                            ("pen-path encoding + " if paths else "") + "rulebook build + forward + backward" +
+                            (" + SGD update" if cfg.sgd else "")),
                    **({"dropout": list(cfg.dropout)} if cfg.dropout else {})},
         "conv_gemm_gflop_per_step": round(conv_flops / 1e9, 3),
         "roofline": roofline,
@@ -322,7 +372,8 @@ def main():
         out["baseline_context"] = "paper: 3000 characters/s, DeepCNet(5,10) forward on digit pictures, GTX 680 (Section 3.2)"
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(cfg, batches[0], Ws, bs, labels, args.dtype, infer=infer)
+        out["cpu_baseline"] = cpu_baseline(cfg, batches[0] if batches else None, Ws, bs, labels, args.dtype,
+                                           infer=infer, paths=path_batches[0] if paths else None)
     print(json.dumps(out), flush=True)
 
 

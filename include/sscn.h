@@ -201,6 +201,56 @@ SSCN_API sscn_status sscn_set_dropout(sscn_net* net, const double* h_rates, int3
  * four-word counter and two-word key (host arrays).  For reproducing masks. */
 SSCN_API void sscn_philox4x32_10(const uint32_t counter[4], const uint32_t key[2], uint32_t out[4]);
 
+/* One stochastic-gradient-descent update of every parameter from the gradients
+ * of the last sscn_backward (the dW / db arrays passed to it, which must still
+ * hold them).  Host arrays of n_conv + 1 device pointers:
+ *   h_W32  float32 master weights [rows][cols] (updated in place)
+ *   h_W    the storage-dtype weights the next sscn_forward reads, rewritten from
+ *          the updated masters (required for bf16 nets; for float32 nets it may
+ *          be null or equal to h_W32, and the masters are then those weights)
+ *   h_b    float32 biases (updated in place)
+ *   h_vW, h_vb  float32 velocities shaped like the weights and biases (zero
+ *          them before the first step)
+ * Classical momentum with L2 weight decay on the weights only (the optimiser is
+ * not stated in the paper; this is the usual library convention):
+ *   g = dW + weight_decay * W (biases: g = db);  v = momentum * v + g;
+ *   W = W - lr * v.
+ * lr, momentum and weight_decay must be finite and >= 0.  Returns
+ * SSCN_ERR_BAD_STATE unless sscn_backward has run since the last forward or
+ * build.  One launch; asynchronous. */
+SSCN_API sscn_status sscn_sgd_step(sscn_net* net, float* const* h_W32, void* const* h_W, float* const* h_b,
+                                   float* const* h_vW, float* const* h_vb, float lr, float momentum,
+                                   float weight_decay, void* stream);
+
+/* Online pen strokes -> sparse input with M = 9 features (Section 2.4): per
+ * grid square the picture of the pen's path (feature 0, 1 where the pen went)
+ * and an 8-bin histogram of its movement in the compass directions E, NE, N,
+ * NW, W, SW, S, SE (features 1..8; counter-clockwise, north = -y).
+ *
+ * d_points[n_points][2]: (y, x) int32 grid points, 0 <= y, x < N, all strokes
+ * concatenated; stroke s is points d_stroke_begin[s] .. d_stroke_begin[s+1]-1
+ * (d_stroke_begin has n_strokes + 1 entries, from 0 to n_points,
+ * non-decreasing) and belongs to sample d_stroke_sample[s] in [0, batch).
+ * Consecutive points p0, p1 of a stroke are joined by the pixels
+ * p0 + round_half_up(i * (p1 - p0) / L), i = 0 .. L, L = max(|dy|, |dx|)
+ * (an 8-connected line).  Each unit move between consecutive pixels gives half
+ * its length (1, or sqrt 2 for a diagonal) to its direction's feature at both
+ * squares it joins.  Sites: every touched square, ascending (b, y, x).
+ *
+ * Writes d_coords[n][3] (b, y, x) and d_feats[n][9] (dtype: sscn_dtype) for
+ * the n distinct sites, *h_count = n, and synchronises `stream`.  Returns
+ * SSCN_ERR_CAPACITY when n > max_sites (*h_count still set; the first
+ * max_sites sites written), SSCN_ERR_OUT_OF_RANGE for a point outside the grid
+ * or a sample outside the batch, SSCN_ERR_INVALID_ARGUMENT for bad offsets.
+ * d_ws: device scratch of sscn_encode_workspace_bytes(N, batch, max_sites)
+ * bytes, 256-byte aligned, free for other use between calls. */
+SSCN_API sscn_status sscn_encode_workspace_bytes(int32_t N, int32_t batch_max, int32_t max_sites, size_t* bytes);
+SSCN_API sscn_status sscn_encode_strokes(int32_t N, int32_t dtype, const int32_t* d_points, int32_t n_points,
+                                         const int32_t* d_stroke_begin, const int32_t* d_stroke_sample,
+                                         int32_t n_strokes, int32_t batch, int32_t* d_coords, void* d_feats,
+                                         int32_t max_sites, int32_t* h_count, void* d_ws, size_t ws_bytes,
+                                         void* stream);
+
 /* Runs only stage s (1 .. L) of the forward or backward pass on the
  * current workspace contents, with the parameters of the last sscn_forward /
  * sscn_backward.  For checking one kernel group against known inputs.  A
@@ -226,7 +276,8 @@ typedef enum {
   SSCN_KC_GROUND = 7,     /* bias and ground-window sums of a conv not under a
                              pooling layer; ground-row input gradient        */
   SSCN_KC_DROPOUT = 8,    /* dropped copies of the dropout levels' inputs      */
-  SSCN_KC_COUNT = 9
+  SSCN_KC_SGD = 9,        /* the parameter update of sscn_sgd_step             */
+  SSCN_KC_COUNT = 10
 } sscn_kernel_class;
 
 /* While enabled, every launch of a kernel whose class bit (1 << class) is set

@@ -94,7 +94,7 @@ struct sscn_net {
   void* ws;
   int batch;
   int n;
-  bool built, forwarded;
+  bool built, forwarded, backwarded;
   const void* W[MAX_LAYERS];
   const float* b[MAX_LAYERS];
   float* dW[MAX_LAYERS];
@@ -442,7 +442,7 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   if (n > 0 && !d_coords) return SSCN_ERR_INVALID_ARGUMENT;
   if (n > net->d.max_active || batch > net->d.batch_max) return SSCN_ERR_CAPACITY;
   if (!d_ws || ws_bytes < net->ws_bytes || ((uintptr_t)d_ws & 255u)) return SSCN_ERR_WORKSPACE;
-  net->built = net->forwarded = false;
+  net->built = net->forwarded = net->backwarded = false;
   if (net->ws != d_ws) {
     carve(net, d_ws);
     net->ws = d_ws;
@@ -770,6 +770,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   net->logits = d_logits;
   net->labels = d_labels;
   net->drop_on = train && net->n_rates > 0;
+  net->backwarded = false;
   const LayerPlan& L0 = net->L[0];
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_scatter_input(net->bf16, d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, st);
@@ -914,6 +915,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
     f.c_out = P.c_out;
   }
   if (run_wgrads(net, w, nw, st) != hipSuccess) return SSCN_ERR_HIP;
+  net->backwarded = true;
   return SSCN_OK;
 }
 
@@ -942,6 +944,123 @@ void sscn_philox4x32_10(const uint32_t counter[4], const uint32_t key[2], uint32
   if (!counter || !key || !out) return;
   const Philox4 r = philox4x32_10(counter[0], counter[1], counter[2], counter[3], key[0], key[1]);
   for (int e = 0; e < 4; ++e) out[e] = r.w[e];
+}
+
+sscn_status sscn_sgd_step(sscn_net* net, float* const* h_W32, void* const* h_W, float* const* h_b,
+                          float* const* h_vW, float* const* h_vb, float lr, float momentum, float weight_decay,
+                          void* stream) {
+  if (!net || !h_W32 || !h_b || !h_vW || !h_vb) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!(lr >= 0.f) || !(momentum >= 0.f) || !(weight_decay >= 0.f) || !std::isfinite(lr) ||
+      !std::isfinite(momentum) || !std::isfinite(weight_decay))
+    return SSCN_ERR_INVALID_ARGUMENT;
+  if (!net->backwarded) return SSCN_ERR_BAD_STATE;
+  SgdArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.store_bf16 = net->bf16 ? 1 : 0;
+  a.lr = lr;
+  a.momentum = momentum;
+  int blocks = 0;
+  auto add = [&](float* w, void* ws, const float* g, float* v, int64_t n, float wd) {
+    SgdJob& J = a.job[a.njobs];
+    J.w = w;
+    J.w_store = (ws == (void*)w) ? nullptr : ws;
+    J.g = g;
+    J.v = v;
+    J.n = n;
+    J.wd = wd;
+    a.blk_beg[a.njobs] = blocks;
+    blocks += (int)std::max<int64_t>(1, std::min<int64_t>(2048, (n + 255) / 256));
+    ++a.njobs;
+  };
+  for (int p = 0; p < net->nparams; ++p) {
+    const ParamPlan& P = net->P[p];
+    if (!h_W32[p] || !h_b[p] || !h_vW[p] || !h_vb[p]) return SSCN_ERR_INVALID_ARGUMENT;
+    void* store = h_W ? h_W[p] : nullptr;
+    if (net->bf16 && !store) return SSCN_ERR_INVALID_ARGUMENT;  // the forward reads the bf16 copy
+    add(h_W32[p], store, net->dW[p], h_vW[p], (int64_t)P.A * P.c_in * P.c_out, weight_decay);
+    add(h_b[p], nullptr, net->db[p], h_vb[p], P.c_out, 0.f);
+  }
+  a.blk_beg[a.njobs] = blocks;
+  return timed(net, SSCN_KC_SGD, (hipStream_t)stream, [&] { return launch_sgd(a, (hipStream_t)stream); }) ==
+                 hipSuccess
+             ? SSCN_OK
+             : SSCN_ERR_HIP;
+}
+
+static size_t encode_bytes(int64_t N, int64_t batch, int64_t max_sites, size_t* offs) {
+  const int64_t Wd = (N + 63) / 64;
+  const int64_t words = batch * N * Wd;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = (off + 255) / 256 * 256;
+    off = o + bytes;
+    return o;
+  };
+  offs[0] = take(words * 8);            // bits
+  offs[1] = take(words * 4);            // wpre
+  offs[2] = take(batch * 4);            // scount
+  offs[3] = take(batch * 4);            // soff
+  offs[4] = take(4);                    // total
+  offs[5] = take(4);                    // err
+  offs[6] = take(max_sites * 8 * 4);    // counts
+  return off + 256;
+}
+
+static bool encode_dims_ok(int32_t N, int32_t batch, int32_t max_sites) {
+  return N >= 1 && N <= (3 << 8) && batch >= 0 && max_sites >= 0 && (int64_t)batch * N * N < (1ll << 31);
+}
+
+sscn_status sscn_encode_workspace_bytes(int32_t N, int32_t batch_max, int32_t max_sites, size_t* bytes) {
+  if (!bytes || !encode_dims_ok(N, batch_max, max_sites)) return SSCN_ERR_INVALID_ARGUMENT;
+  size_t offs[7];
+  *bytes = encode_bytes(N, batch_max, max_sites, offs);
+  return SSCN_OK;
+}
+
+sscn_status sscn_encode_strokes(int32_t N, int32_t dtype, const int32_t* d_points, int32_t n_points,
+                                const int32_t* d_stroke_begin, const int32_t* d_stroke_sample, int32_t n_strokes,
+                                int32_t batch, int32_t* d_coords, void* d_feats, int32_t max_sites, int32_t* h_count,
+                                void* d_ws, size_t ws_bytes, void* stream) {
+  if (!h_count || !encode_dims_ok(N, batch, max_sites) || n_points < 0 || n_strokes < 0) return SSCN_ERR_INVALID_ARGUMENT;
+  if (dtype != SSCN_F32 && dtype != SSCN_BF16) return SSCN_ERR_INVALID_ARGUMENT;
+  if (!d_stroke_begin || (n_points > 0 && !d_points) || (n_strokes > 0 && !d_stroke_sample) ||
+      (max_sites > 0 && (!d_coords || !d_feats)))
+    return SSCN_ERR_INVALID_ARGUMENT;
+  size_t offs[7];
+  if (!d_ws || ((uintptr_t)d_ws & 255u) || ws_bytes < encode_bytes(N, batch, max_sites, offs))
+    return SSCN_ERR_WORKSPACE;
+  char* base = (char*)d_ws;
+  EncodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.points = d_points;
+  a.begin = d_stroke_begin;
+  a.sample = d_stroke_sample;
+  a.n_points = n_points;
+  a.n_strokes = n_strokes;
+  a.batch = batch;
+  a.N = N;
+  a.Wd = (N + 63) / 64;
+  a.max_sites = max_sites;
+  a.bits = (uint64_t*)(base + offs[0]);
+  a.wpre = (int32_t*)(base + offs[1]);
+  a.scount = (int32_t*)(base + offs[2]);
+  a.soff = (int32_t*)(base + offs[3]);
+  a.total = (int32_t*)(base + offs[4]);
+  a.err = (int32_t*)(base + offs[5]);
+  a.counts = (int32_t*)(base + offs[6]);
+  a.coords = d_coords;
+  hipStream_t st = (hipStream_t)stream;
+  if (launch_encode(dtype == SSCN_BF16, a, d_feats, st) != hipSuccess) return SSCN_ERR_HIP;
+  int32_t res[2] = {0, 0};
+  if (hipMemcpyAsync(&res[0], a.total, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(&res[1], a.err, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return SSCN_ERR_HIP;
+  *h_count = res[0];
+  if (res[1] & ERRBIT_ORDER) return SSCN_ERR_INVALID_ARGUMENT;
+  if (res[1] & ERRBIT_RANGE) return SSCN_ERR_OUT_OF_RANGE;
+  if (res[0] > max_sites) return SSCN_ERR_CAPACITY;
+  return SSCN_OK;
 }
 
 sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream) {

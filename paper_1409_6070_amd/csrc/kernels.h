@@ -219,4 +219,40 @@ hipError_t launch_head_drop(bool bf16, const void* X_top, const int32_t* head_ro
                             void* hd, const DropArgs& d, hipStream_t st);
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t st);
 
+// encode.hip: pen paths -> sites and 9 features (Section 2.4)
+struct EncodeArgs {
+  const int32_t* points;  // [n_points][2] (y, x)
+  const int32_t* begin;   // [n_strokes + 1]
+  const int32_t* sample;  // [n_strokes]
+  int32_t n_points, n_strokes, batch, N, Wd, max_sites;
+  uint64_t* bits;    // [batch][N][Wd] occupancy
+  int32_t* wpre;     // [batch][N][Wd] exclusive popcount prefix within the sample
+  int32_t* scount;   // [batch]
+  int32_t* soff;     // [batch]
+  int32_t* total;    // [1] distinct sites
+  int32_t* err;      // [1] ERRBIT_*
+  int32_t* counts;   // [max_sites][8] move counts
+  int32_t* coords;   // [max_sites][3] output
+};
+hipError_t launch_encode(bool bf16, const EncodeArgs& a, void* feats, hipStream_t st);
+
+// sgd.hip: one momentum-SGD update of many parameter arrays in one launch
+constexpr int MAX_SGD_JOBS = 2 * MAX_LAYERS;
+struct SgdJob {
+  float* w;          // fp32 master
+  void* w_store;     // storage-dtype copy to refresh, or null
+  const float* g;    // gradient
+  float* v;          // velocity
+  int64_t n;
+  float wd;          // weight decay
+};
+struct SgdArgs {
+  int32_t njobs;
+  int32_t store_bf16;
+  float lr, momentum;
+  int32_t blk_beg[MAX_SGD_JOBS + 1];
+  SgdJob job[MAX_SGD_JOBS];
+};
+hipError_t launch_sgd(const SgdArgs& a, hipStream_t st);
+
 }  // namespace sscn

@@ -33,10 +33,10 @@ EXPORTED = [
     "sscn_net_create", "sscn_net_destroy", "sscn_status_string", "sscn_net_num_params", "sscn_net_param_shape",
     "sscn_net_workspace_bytes", "sscn_rulebook_build", "sscn_layer_sizes", "sscn_forward", "sscn_backward",
     "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get", "sscn_timing_enable", "sscn_timing_collect",
-    "sscn_set_dropout", "sscn_philox4x32_10",
+    "sscn_set_dropout", "sscn_philox4x32_10", "sscn_sgd_step", "sscn_encode_workspace_bytes", "sscn_encode_strokes",
 ]
 KERNEL_CLASSES = ["rulebook", "gather_gemm", "wgrad", "wgrad_reduce", "pool_fwd", "pool_bwd", "head", "ground",
-                  "dropout"]
+                  "dropout", "sgd"]
 
 
 class SSCNError(RuntimeError):
@@ -91,6 +91,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sscn_timing_collect": (I32, [VP, I32, P(I32), P(ctypes.c_float), VP]),
         "sscn_set_dropout": (I32, [VP, P(ctypes.c_double), I32, ctypes.c_uint64]),
         "sscn_philox4x32_10": (None, [P(ctypes.c_uint32), P(ctypes.c_uint32), P(ctypes.c_uint32)]),
+        "sscn_sgd_step": (I32, [VP, P(VP), P(VP), P(VP), P(VP), P(VP), ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                VP]),
+        "sscn_encode_workspace_bytes": (I32, [I32, I32, I32, P(SZ)]),
+        "sscn_encode_strokes": (I32, [I32, I32, VP, I32, VP, VP, I32, I32, VP, VP, I32, P(I32), VP, SZ, VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -196,6 +200,32 @@ def sscn_philox4x32_10(counter: Sequence[int], key: Sequence[int]) -> List[int]:
     return list(out)
 
 
+def sscn_sgd_step(net, W32_ptrs, W_ptrs, b_ptrs, vW_ptrs, vb_ptrs, lr, momentum, weight_decay, stream) -> None:
+    _check(load_library().sscn_sgd_step(net, _ptr_array(W32_ptrs), _ptr_array(W_ptrs) if W_ptrs is not None else None,
+                                        _ptr_array(b_ptrs), _ptr_array(vW_ptrs), _ptr_array(vb_ptrs), lr, momentum,
+                                        weight_decay, stream), "sscn_sgd_step")
+
+
+def sscn_encode_workspace_bytes(N: int, batch_max: int, max_sites: int) -> int:
+    out = ctypes.c_size_t()
+    _check(load_library().sscn_encode_workspace_bytes(N, batch_max, max_sites, ctypes.byref(out)),
+           "sscn_encode_workspace_bytes")
+    return out.value
+
+
+def sscn_encode_strokes(N, dtype, d_points, n_points, d_begin, d_sample, n_strokes, batch, d_coords, d_feats,
+                        max_sites, d_ws, ws_bytes, stream) -> int:
+    """Returns the site count; raises SSCNError (the count is in .count) on failure."""
+    cnt = ctypes.c_int32(0)
+    st = load_library().sscn_encode_strokes(N, dtype, d_points, n_points, d_begin, d_sample, n_strokes, batch,
+                                            d_coords, d_feats, max_sites, ctypes.byref(cnt), d_ws, ws_bytes, stream)
+    if st != 0:
+        err = SSCNError(st, "sscn_encode_strokes")
+        err.count = cnt.value
+        raise err
+    return cnt.value
+
+
 def sscn_timing_enable(net, class_mask: int) -> None:
     _check(load_library().sscn_timing_enable(net, class_mask), "sscn_timing_enable")
 
@@ -289,6 +319,20 @@ class SparseDeepCNet:
                       dfeats.data_ptr() if (dfeats is not None and self.n) else None, _stream())
         return self.dW, self.db, dfeats
 
+    def sgd_step(self, W32: Sequence[torch.Tensor], W: Optional[Sequence[torch.Tensor]], bs: Sequence[torch.Tensor],
+                 vW: Sequence[torch.Tensor], vb: Sequence[torch.Tensor], lr: float, momentum: float = 0.0,
+                 weight_decay: float = 0.0) -> None:
+        """SGD update from the last backward's gradients: fp32 masters W32 (and biases, velocities)
+        in place, then the storage copies W the next forward reads."""
+        for t in list(W32) + list(bs) + list(vW) + list(vb):
+            assert t.dtype == torch.float32 and t.is_contiguous()
+        if W is not None:
+            for t in W:
+                assert t.dtype == self.tdtype and t.is_contiguous()
+        sscn_sgd_step(self.handle, [t.data_ptr() for t in W32], [t.data_ptr() for t in W] if W is not None else None,
+                      [t.data_ptr() for t in bs], [t.data_ptr() for t in vW], [t.data_ptr() for t in vb], lr,
+                      momentum, weight_decay, _stream())
+
     def timing(self, classes: Sequence[str]) -> None:
         """Bracket launches of the named kernel classes with HIP events (empty: off)."""
         mask = 0
@@ -336,3 +380,33 @@ class SparseDeepCNet:
         if v.kind == 1:
             return self._slice(v.rules_t, (n_below + 1) * v.window * 4, torch.int32).view(n_below + 1, v.window)
         return self._slice(v.rules_t, (n_below + 1) * 4, torch.int32)
+
+
+class StrokeEncoder:
+    """Pen paths -> sparse input with 9 features per site (Section 2.4) on the GPU, through
+    sscn_encode_strokes; holds the scratch and output buffers for batches within its limits."""
+
+    def __init__(self, N: int, batch_max: int, max_sites: int, dtype: str = "bf16", device: str = "cuda"):
+        if dtype not in ("f32", "bf16"):
+            raise ValueError(dtype)
+        self.N, self.batch_max, self.max_sites, self.dtype = N, batch_max, max_sites, dtype
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.device = torch.device(device)
+        self.ws_bytes = sscn_encode_workspace_bytes(N, batch_max, max_sites)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        self.coords = torch.empty(max(max_sites, 1), 3, dtype=torch.int32, device=self.device)
+        self.feats = torch.empty(max(max_sites, 1), 9, dtype=self.tdtype, device=self.device)
+
+    def encode(self, points: torch.Tensor, stroke_begin: torch.Tensor, stroke_sample: torch.Tensor, batch: int):
+        """(coords [n, 3], feats [n, 9]) views of the encoder's buffers (valid until the next call)."""
+        for t in (points, stroke_begin, stroke_sample):
+            assert t.dtype == torch.int32 and t.is_contiguous() and t.device.type == "cuda"
+        if batch > self.batch_max:
+            raise SSCNError(4, "StrokeEncoder.encode")
+        n_strokes = int(stroke_sample.shape[0])
+        n = sscn_encode_strokes(self.N, SSCN_BF16 if self.dtype == "bf16" else SSCN_F32,
+                                points.data_ptr() if points.numel() else None, int(points.shape[0]),
+                                stroke_begin.data_ptr(), stroke_sample.data_ptr() if n_strokes else None, n_strokes,
+                                batch, self.coords.data_ptr(), self.feats.data_ptr(), self.max_sites,
+                                self.ws.data_ptr(), self.ws_bytes, _stream())
+        return self.coords[:n], self.feats[:n]

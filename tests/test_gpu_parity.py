@@ -64,7 +64,14 @@ def test_small_networks(case, dtype):
 
 
 def _config_case(cfg, dtype, index=0):
-    b = make_batch(cfg, index)
+    if cfg.generator == "paths":  # the parity of the net itself: inputs from the oracle's encoding
+        from oracle.strokes import encode_strokes
+        from workloads import Batch, make_paths
+        p = make_paths(cfg, index)
+        coords, feats = encode_strokes(p.points, p.stroke_begin, p.stroke_sample, p.batch, p.grid)
+        b = Batch(coords=coords.astype(np.int32), feats=feats, batch=cfg.batch, grid=cfg.grid)
+    else:
+        b = make_batch(cfg, index)
     Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed, cfg.arch)
     labels = random_labels(cfg.batch, cfg.n_classes, cfg.label_seed)
     return b, Ws, bs, labels

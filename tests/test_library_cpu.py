@@ -138,3 +138,32 @@ def test_set_dropout_host_checks():
     finally:
         for h in (plain, drop, nin):
             sscn.sscn_net_destroy(h)
+
+
+def test_encode_and_sgd_host_checks():
+    lib = sscn.load_library()
+    assert sscn.sscn_encode_workspace_bytes(96, 100, 50000) > 50000 * 32
+    for bad in ((0, 4, 10), (769, 4, 10), (96, -1, 10), (96, 4, -1), (768, 4000, 10)):
+        with pytest.raises(sscn.SSCNError):
+            sscn.sscn_encode_workspace_bytes(*bad)
+    fake = 1 << 20  # never dereferenced: every call below fails its host checks first
+    cnt = ctypes.c_int32()
+    ws = sscn.sscn_encode_workspace_bytes(48, 4, 100)
+    assert lib.sscn_encode_strokes(48, 0, fake, 10, fake, fake, 2, 4, fake, fake, 100, None, fake, ws, None) == 1
+    assert lib.sscn_encode_strokes(48, 5, fake, 10, fake, fake, 2, 4, fake, fake, 100, ctypes.byref(cnt), fake, ws,
+                                   None) == 1  # dtype
+    assert lib.sscn_encode_strokes(48, 0, fake, 10, None, fake, 2, 4, fake, fake, 100, ctypes.byref(cnt), fake, ws,
+                                   None) == 1  # no offsets
+    assert lib.sscn_encode_strokes(48, 0, fake, 10, fake, fake, 2, 4, fake, fake, 100, ctypes.byref(cnt), fake,
+                                   ws - 1, None) == 7  # workspace too small
+    assert lib.sscn_encode_strokes(48, 0, fake, 10, fake, fake, 2, 4, fake, fake, 100, ctypes.byref(cnt), fake + 8,
+                                   ws, None) == 7  # misaligned
+    h = sscn.sscn_net_create(sscn.NetDesc(2, 3, 9, 4, 4, 100, sscn.SSCN_BF16))
+    try:
+        ptrs = (ctypes.c_void_p * 4)(*([fake] * 4))
+        assert lib.sscn_sgd_step(h, ptrs, ptrs, ptrs, ptrs, ptrs, 0.1, 0.9, 0.0, None) == 5  # no backward yet
+        assert lib.sscn_sgd_step(h, ptrs, ptrs, ptrs, ptrs, ptrs, -0.1, 0.9, 0.0, None) == 1
+        assert lib.sscn_sgd_step(h, ptrs, ptrs, ptrs, ptrs, ptrs, float("nan"), 0.9, 0.0, None) == 1
+        assert lib.sscn_sgd_step(h, None, ptrs, ptrs, ptrs, ptrs, 0.1, 0.9, 0.0, None) == 1
+    finally:
+        sscn.sscn_net_destroy(h)

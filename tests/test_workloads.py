@@ -3,10 +3,27 @@
 import numpy as np
 import pytest
 
-from workloads import CONFIGS, circle_sites, get_config, make_batch
+from workloads import CONFIGS, circle_sites, get_config, make_batch, make_paths
+
+SITE_CONFIGS = [c for c in CONFIGS if c.generator != "paths"]
+PATH_CONFIGS = [c for c in CONFIGS if c.generator == "paths"]
 
 
-@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", PATH_CONFIGS, ids=lambda c: c.name)
+def test_paths_are_valid_and_deterministic(cfg):
+    a, b = make_paths(cfg, 0), make_paths(cfg, 0)
+    np.testing.assert_array_equal(a.points, b.points)
+    np.testing.assert_array_equal(a.stroke_begin, b.stroke_begin)
+    assert a.stroke_begin[0] == 0 and a.stroke_begin[-1] == a.n_points and np.all(np.diff(a.stroke_begin) > 0)
+    assert a.stroke_sample.min() >= 0 and a.stroke_sample.max() < cfg.batch
+    lo = (cfg.grid - cfg.gen_args["box"]) // 2
+    assert a.points.min() >= lo and a.points.max() < lo + cfg.gen_args["box"]
+    assert not np.array_equal(make_paths(cfg, 1).points[:10], a.points[:10])
+    with pytest.raises(ValueError):
+        make_batch(cfg, 0)
+
+
+@pytest.mark.parametrize("cfg", SITE_CONFIGS, ids=lambda c: c.name)
 def test_batches_are_valid_and_deterministic(cfg):
     a = make_batch(cfg, 0)
     b = make_batch(cfg, 0)
@@ -23,7 +40,7 @@ def test_batches_are_valid_and_deterministic(cfg):
 
 def test_active_fractions():
     # stroke workloads: ~3-8% (96x96, 64x64 box), <3% (192x192); the RGB patch is 32*32/96^2 exactly
-    f = {c.name: make_batch(c, 0).active_fraction() for c in CONFIGS}
+    f = {c.name: make_batch(c, 0).active_fraction() for c in SITE_CONFIGS}
     assert 0.03 <= f["deepcnet5_50_strokes_b100"] <= 0.08
     assert 0.03 <= f["deepcnet5_50_strokes_m8_b100"] <= 0.08
     assert f["deepcnet6_100_strokes_b64"] < 0.03

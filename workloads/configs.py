@@ -13,7 +13,10 @@ with its parameters.  The generators stand in for the paper's datasets:
 * grey-level digit strokes of about 150 pixels in the middle of a 96 x 96 grid
   stand in for MNIST (Section 2.5), on the small network the paper times at test
   time (DeepCNet(5,10), Section 3.2): a forward-only ("infer") workload;
-* the DeepCNet(5,50) pen strokes once more with dropout per level (Section 2.1).
+* the DeepCNet(5,50) pen strokes once more with dropout per level (Section 2.1);
+* raw pen paths for DeepCNet(4,20), encoded by the method itself into 9 features
+  per site (picture plus 8-direction histograms, Section 2.4), for a whole
+  training step with the SGD update.
 """
 
 from dataclasses import dataclass, field
@@ -29,12 +32,13 @@ class WorkloadConfig:
     batch: int
     n_classes: int
     dtypes: Tuple[str, ...]
-    generator: str  # "strokes", "patch" or "digits"
+    generator: str  # "strokes", "patch", "digits" or "paths" (raw pen paths, encoded by the method)
     gen_args: Dict = field(default_factory=dict)
     seed: int = 0  # input seed; weights use 100 + seed, labels 200 + seed
     mode: str = "train"  # "train": build + forward + backward; "infer": build + forward (logits)
     arch: str = "deepcnet"  # or "deepcnin" (Section 2.2)
     dropout: Tuple[float, ...] = ()  # rates per level (ell + 2, Section 2.1); () for none
+    sgd: Tuple[float, ...] = ()  # (lr, momentum, weight decay): a training step ends with the update
 
     @property
     def dropout_seed(self) -> int:
@@ -125,6 +129,17 @@ CONFIGS = [
         generator="strokes",
         gen_args=dict(strokes=(1, 20), points=(10, 60), box=64, sigma=2.0, features="ones"),
         seed=7, dropout=(0.0, 0.0, 0.0, 0.5, 0.5, 0.5, 0.5),
+    ),
+    # A whole training step on DeepCNet(4,20) (the network of Section 3.1.2's M = 1 / M = 9
+    # comparison): raw pen paths (1-3 strokes of 10-30 points, step sd 2 px, 32x32 box in
+    # 48x48), encoded on the device into the picture plus 8-direction histograms (M = 9,
+    # Section 2.4), then build + forward + backward + SGD update.
+    WorkloadConfig(
+        name="deepcnet4_20_paths_m9_b100",
+        ell=4, k=20, c_in=9, batch=100, n_classes=10, dtypes=("f32", "bf16"),
+        generator="paths",
+        gen_args=dict(strokes=(1, 3), points=(10, 30), box=32, sigma=2.0),
+        seed=8, sgd=(0.01, 0.9, 1e-4),
     ),
 ]
 
