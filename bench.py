@@ -61,26 +61,47 @@ def layer_shapes(cfg):
     return st
 
 
-def gemm_work(cfg, sizes, infer=False):
-    """Algorithmic FLOPs of one step, per kernel class.
+def gemm_work(cfg, sizes, infer=False, e=2):
+    """Algorithmic FLOPs of one step, per kernel class, and the compulsory bytes of the
+    gather-GEMM launches (e bytes per stored element).
 
     gather_gemm: convolution forward 2(n_s+1)A C_in C_out per stage, convolution
     input gradient 2 n_{s-1} A C_out C_in per stage s > 1 (the first layer's
     input gradient is not part of a training step), softmax layer forward and
     dh, 2 B C_last classes each.
     wgrad: 2(n_s+1)A C_in C_out per stage plus 2 B C_last classes.
+
+    Compulsory bytes of a gather-GEMM launch (each operand moved once, channel
+    padding not counted): forward (n_{s-1}+1)C_in e + (n_s+1)A*4 (window list,
+    none for 1x1) + (n_s+1)C_out e + A C_in C_out e; input gradient
+    (n_s+1)C_out e + (n_{s-1}+1)A*4 + n_{s-1}C_in e (+ the same again for the
+    rectifier mask when a convolution lies below) + the weights; softmax layer
+    forward B C e + 4B + 4B classes + C classes e, dh B classes e + 4 B C + the
+    weights.
     """
     fwd = dgrad = 0.0
-    for s, (kind, A, ci, co) in enumerate(layer_shapes(cfg), start=1):
+    fbytes = dbytes = 0.0
+    shapes = layer_shapes(cfg)
+    for s, (kind, A, ci, co) in enumerate(shapes, start=1):
         if kind != "conv":
             continue
-        fwd += 2.0 * (sizes[s] + 1) * A * ci * co
+        n, nb = sizes[s], sizes[s - 1]
+        w = A * ci * co * e
+        fwd += 2.0 * (n + 1) * A * ci * co
+        fbytes += (nb + 1) * ci * e + (n + 1) * (A * 4 if A > 1 else 0) + (n + 1) * co * e + w
         if s > 1:
-            dgrad += 2.0 * sizes[s - 1] * A * co * ci
-    head = 2.0 * cfg.batch * (cfg.ell + 1) * cfg.k * cfg.n_classes
+            dgrad += 2.0 * nb * A * co * ci
+            mask = nb * ci * e if shapes[s - 2][0] == "conv" else 0
+            dbytes += (n + 1) * co * e + (nb + 1) * (A * 4 if A > 1 else 0) + nb * ci * e + mask + w
+    C = (cfg.ell + 1) * cfg.k
+    B, K = cfg.batch, cfg.n_classes
+    head = 2.0 * B * C * K
+    hf_bytes = B * C * e + 4 * B + 4 * B * K + C * K * e
+    hd_bytes = B * K * e + 4 * B * C + C * K * e
     if infer:  # forward only: conv forward and the logits
-        return {"gather_gemm": fwd + head, "wgrad": 0.0, "conv_total": fwd}
-    return {"gather_gemm": fwd + dgrad + 2 * head, "wgrad": fwd + head, "conv_total": 2 * fwd + dgrad}
+        return {"gather_gemm": fwd + head, "wgrad": 0.0, "conv_total": fwd, "gather_gemm_bytes": fbytes + hf_bytes}
+    return {"gather_gemm": fwd + dgrad + 2 * head, "wgrad": fwd + head, "conv_total": 2 * fwd + dgrad,
+            "gather_gemm_bytes": fbytes + dbytes + hf_bytes + hd_bytes}
 
 
 def read_traffic(kernel, dtype, workload):
@@ -294,8 +315,10 @@ def main():
 
     # algorithmic work of the timed steps (batches cycle in order)
     step_sizes = [sizes[i % len(sizes)] for i in range(args.steps)]
-    work = [gemm_work(cfg, s, infer) for s in step_sizes]
+    esz = 2 if args.dtype == "bf16" else 4
+    work = [gemm_work(cfg, s, infer, esz) for s in step_sizes]
     g_flops = sum(w["gather_gemm"] for w in work)
+    g_bytes = sum(w["gather_gemm_bytes"] for w in work)
     avg_launch_s = g_ms / 1e3 / max(g_launches, 1)
     achieved = g_flops / max(g_launches, 1) / avg_launch_s if g_launches else 0.0
     peak = MFMA_PEAK[args.dtype]
@@ -308,6 +331,17 @@ def main():
         "launches_per_step": g_launches / args.steps, "avg_launch_us": round(avg_launch_s * 1e6, 3),
         "algorithmic_gflop_per_launch": round(g_flops / max(g_launches, 1) / 1e9, 4),
     }
+    # the class's arithmetic intensity against the compulsory bytes; the attainable
+    # rate is min(MFMA peak, intensity x HBM bandwidth)
+    ai = g_flops / max(g_bytes, 1.0)
+    attainable = min(peak, ai * HBM_PEAK)
+    roofline.update({
+        "compulsory_mb_per_launch": round(g_bytes / max(g_launches, 1) / 1e6, 3),
+        "ai_flop_per_byte": round(ai, 1),
+        "attainable_tflops": round(attainable / 1e12, 1),
+        "frac_of_attainable": round(achieved / attainable, 4) if attainable else None,
+        "hbm_gbps_compulsory": round(g_bytes / max(g_launches, 1) / avg_launch_s / 1e9, 1) if g_launches else 0.0,
+    })
 
     # breakdown of one pass over a few steps with every class timed
     from paper_1409_6070_amd.sscn import KERNEL_CLASSES

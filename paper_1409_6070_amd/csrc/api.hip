@@ -77,7 +77,8 @@ struct sscn_net {
   int wgrad_slabs;
   // global workspace pointers
   int32_t* counts;
-  int32_t* err;
+  int32_t* err;   // [4]: the input-error word, then completion counters (zeroed by every rulebook build,
+                  // returned to zero by the kernel that uses them): [1] softmax loss
   int32_t* perm;
   int32_t* head_rows;
   void* dlogits;
@@ -229,6 +230,7 @@ static void carve(sscn_net* net, void* base) {
 
 static void set_plan(GemmArgs& g, const GemmPlan& p, int64_t rows_cap, float* gpart) {
   g.cfg = p.cfg;
+  g.sk = p.sk;
   g.ksplit = p.ksplit;
   g.part = gpart;
   g.part_rows = (int32_t)rows_cap;
@@ -821,7 +823,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   if (!train) return SSCN_OK;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_softmax_xent(net->bf16, d_logits, d_labels, net->batch, net->d.n_classes, net->dlogits,
-                                   net->dl_stride, net->loss_part, d_loss, st);
+                                   net->dl_stride, net->loss_part, d_loss, net->err + 1, st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
   net->forwarded = true;

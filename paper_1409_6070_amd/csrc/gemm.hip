@@ -17,6 +17,7 @@
 // always fp32.
 
 #include "common.h"
+#include "epilogue.h"
 #include "kernels.h"
 
 #include <hip/hip_ext.h>
@@ -101,36 +102,12 @@ __device__ inline void mma_slab(const T* As, const T* Bs, f32x4 (&acc)[C::TM][C:
   }
 }
 
-template <typename T>
-__device__ inline float epi_value(const GemmArgs& a, float v, float bias) {
-  v += bias;
-  if (a.epi == EPI_BIAS_RELU) v = fmaxf(v, 0.f);
-  if (a.epi == EPI_BIAS_LRELU) v = v >= 0.f ? v : v / 3.f;
-  return v;
-}
-
-// Epilogues that store in the storage dtype (the others store float32).
-__device__ inline bool epi_stores_T(int epi) {
-  return epi == EPI_BIAS_RELU || epi == EPI_STORE || epi == EPI_BIAS_LRELU || epi == EPI_STORE_MASK;
-}
-
 // q = k / d for 0 <= k < 2^20, 1 <= d < 2^16: float estimate, then exact correction.
 __device__ inline int div_small(int k, int d, float rcp) {
   int q = (int)((float)k * rcp);
   q += (q + 1) * d <= k ? 1 : 0;
   q -= q * d > k ? 1 : 0;
   return q;
-}
-
-template <typename T>
-__device__ inline void store_out(const GemmArgs& a, int64_t m, int n, float v) {
-  const int64_t o = m * a.out_stride + n;
-  if (a.epi == EPI_STORE_MASK)
-    v *= act_factor(Elem<T>::to_f32(((const T*)a.mask)[m * a.mask_stride + n]), a.slope);
-  if (epi_stores_T(a.epi))
-    ((T*)a.out)[o] = Elem<T>::from_f32(v);
-  else
-    ((float*)a.out)[o] = v;
 }
 
 // Implicit-gather GEMM.  Per tile: the tile's window rows go to LDS once; the
@@ -598,6 +575,7 @@ static void launch_gemm_t(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
 
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   if (max_rows - a.row_begin <= 0) return hipSuccess;
+  if (a.cfg == GEMM_DIRECT) return bf16 ? launch_gemm_direct(a, max_rows, st) : hipErrorInvalidValue;
   if (bf16)
     launch_gemm_t<__bf16>(a, max_rows, st);
   else
@@ -606,6 +584,30 @@ hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream
 }
 
 GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K) {
+  // bf16 launches with few output tiles (at the row bound) go to the
+  // direct-operand kernel, whose waves split K and so keep many loads in flight
+  // per tile; launches with many tiles keep the LDS-tiled kernel, whose 128-row
+  // tiles share each weight slab between four waves.  (Measured on the pen-stroke
+  // DeepCNet(5,50): the direct kernel wins at <= 3.3k tiles of 32 x 64 and loses
+  // from 4.5k up; very deep K keeps split-K.)
+  const int64_t direct_tiles = ((max_rows + DIRECT_BM - 1) / DIRECT_BM) * ((N + DIRECT_BN - 1) / DIRECT_BN);
+  if (bf16 && direct_tiles <= 4000 && K <= 2048) {
+    // waves per tile so that each sums at most about four 32-wide k blocks,
+    // and more while the grid stays small
+    GemmPlan p;
+    p.cfg = GEMM_DIRECT;
+    p.BN = DIRECT_BN;
+    p.Npad = (int)round_up(N, DIRECT_BN);
+    p.Kpad = (int)round_up(K, 64);
+    p.ksplit = 1;
+    const int ksteps = (K + 31) / 32;
+    const int64_t tiles = ((max_rows + DIRECT_BM - 1) / DIRECT_BM) * (p.Npad / DIRECT_BN);
+    int sk = 1;
+    while (sk < 4 && sk * 4 < ksteps) sk *= 2;
+    while (sk < 4 && sk * 2 <= ksteps && tiles * sk < 4096) sk *= 2;
+    p.sk = sk;
+    return p;
+  }
   // Tile width: 128 when that pads N no more than 64 does and still gives >= 256
   // tiles; otherwise 64-wide tiles with the tallest of 128/64/32 rows that gives
   // >= 256 tiles.  K is split when even 32-row tiles leave the GPU mostly idle.

@@ -1,0 +1,192 @@
+// Gather GEMM with MFMA operands loaded straight from memory (bf16).
+//
+// The operand layout of v_mfma_f32_16x16x32_bf16 is 8 consecutive k of one row
+// per lane (lane l: row l % 16, k 8 * (l / 16) .. + 7) for both A and B.  With
+// channels padded to multiples of 8 those 16 bytes are contiguous in the
+// gathered input row (A = the window's rows, Section 2.3) and in the packed
+// weights Bt[n][k], so each lane issues one 16-byte load per operand and k
+// block -- no LDS staging and no barrier in the K loop.  A workgroup of SK
+// waves computes one 32 x 64 output tile; wave w sums its own contiguous K
+// range, four k blocks of loads in flight at a time, and the partial sums meet
+// in LDS (in wave order, so the result is deterministic) for the epilogue,
+// which writes 16-byte vectors.
+
+#include "common.h"
+#include "epilogue.h"
+#include "kernels.h"
+
+#include <hip/hip_ext.h>
+
+namespace sscn {
+
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+constexpr int DIR_AMAX = 9;  // largest window (3x3)
+
+// k / d for 0 <= k < 2^20, 1 <= d < 2^16: float estimate, then exact correction
+__device__ inline int dir_div(int k, int d, float rcp) {
+  int q = (int)((float)k * rcp);
+  q += (q + 1) * d <= k ? 1 : 0;
+  q -= q * d > k ? 1 : 0;
+  return q;
+}
+
+template <int SK>
+__global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
+  typedef __bf16 T;
+  constexpr int TM = DIRECT_BM / 16, TN = DIRECT_BN / 16;
+  constexpr int BM = DIRECT_BM, BN = DIRECT_BN, NT = 64 * SK;
+  constexpr int CH = 4;        // k blocks (32 k each) of loads in flight per wave
+  constexpr int RP = BN + 4;   // LDS pitch of the partial sums (floats)
+  __shared__ int32_t Rs[BM * DIR_AMAX];
+  __shared__ __attribute__((aligned(16))) float red[SK][BM][RP];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
+  const int span = rows - a.row_begin;
+  if (span <= 0) return;
+  const int tiles_m = (span + BM - 1) / BM;
+  const int tiles_n = a.Npad / BN;
+  const int ntiles = tiles_m * tiles_n;
+  const int A = a.A;
+  const int ksteps = (a.K + 31) / 32;
+  const int per = (ksteps + SK - 1) / SK;
+  const int kb = min(ksteps, w * per), ke = min(ksteps, kb + per);
+  const float rcp = 1.f / (float)a.cseg;
+  const T* src = (const T*)a.src;
+  const T* Bt = (const T*)a.Bt;
+
+  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int tn = tile % tiles_n, tm = tile / tiles_n;
+    const int m0 = a.row_begin + tm * BM, n0 = tn * BN;
+    for (int e = tid; e < BM * A; e += NT) {  // the tile's window rows (-1: none)
+      const int r = e / A, f = e - r * A;
+      const int m = m0 + r;
+      int v = -1;
+      if (m < rows) v = a.rmap ? a.rmap[(int64_t)m * A + f] : (f == 0 ? m : -1);
+      Rs[e] = v;
+    }
+    __syncthreads();
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = kb; k0 < ke; k0 += CH) {
+      v4u ra[CH][TM], rb[CH][TN];
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const int ks = k0 + c;
+        if (ks < ke) {  // uniform over the wave
+          const int k = ks * 32 + g * 8;
+          const bool in_k = k < a.K;
+          const int f = in_k ? dir_div(k, a.cseg, rcp) : 0;
+          const int col = in_k ? k - f * a.cseg : 0;
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const int srow = in_k ? Rs[(i * 16 + r16) * A + f] : -1;
+            const v4u val = *(const v4u*)(src + (int64_t)max(srow, 0) * a.src_stride + col);
+            ra[c][i] = srow >= 0 ? val : v4u{0u, 0u, 0u, 0u};
+          }
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            rb[c][j] = *(const v4u*)(Bt + (int64_t)(n0 + j * 16 + r16) * a.Kpad + ks * 32 + g * 8);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        if (k0 + c < ke) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ra[c][i]),
+                                                                  __builtin_bit_cast(bf16x8, rb[c][j]), acc[i][j], 0,
+                                                                  0, 0);
+        }
+      }
+    }
+
+    // partial sums of every wave to LDS (MFMA output: lane holds rows 4g..4g+3 of column r16)
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[w][i * 16 + g * 4 + r][j * 16 + r16] = acc[i][j][r];
+    __syncthreads();
+
+    if (epi_stores_T(a.epi)) {
+      // 16-byte vectors: 8 columns of one row, summed over the waves in order
+      for (int v = tid; v < BM * (BN / 8); v += NT) {
+        const int r = v / (BN / 8), c8 = (v - r * (BN / 8)) * 8;
+        const int m = m0 + r, n = n0 + c8;
+        if (m >= rows || n >= a.out_cols) continue;
+        float s[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] = 0.f;
+#pragma unroll
+        for (int q = 0; q < SK; ++q) {
+          const f32x4 lo = *(const f32x4*)&red[q][r][c8], hi = *(const f32x4*)&red[q][r][c8 + 4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s[e] += lo[e];
+            s[4 + e] += hi[e];
+          }
+        }
+        v4u o;
+        v4u y{0u, 0u, 0u, 0u};
+        if (a.epi == EPI_STORE_MASK) y = *(const v4u*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float b = (a.bias && n + e < a.N) ? a.bias[n + e] : 0.f;
+          float v8 = epi_value<T>(a, s[e], b);
+          if (a.epi == EPI_STORE_MASK) v8 *= act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope);
+          ((T*)&o)[e] = Elem<T>::from_f32(v8);
+        }
+        *(v4u*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
+      }
+    } else {
+      for (int e = tid; e < BM * BN; e += NT) {
+        const int r = e / BN, c = e - r * BN;
+        const int m = m0 + r, n = n0 + c;
+        if (m >= rows || n >= a.out_cols) continue;
+        float s = 0.f;
+#pragma unroll
+        for (int q = 0; q < SK; ++q) s += red[q][r][c];
+        store_out<T>(a, m, n, epi_value<T>(a, s, (a.bias && n < a.N) ? a.bias[n] : 0.f));
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <int SK>
+static void launch_direct_sk(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
+  const int64_t span = max_rows - a.row_begin;
+  const int64_t tiles = ((span + DIRECT_BM - 1) / DIRECT_BM) * (a.Npad / DIRECT_BN);
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), 2048);
+  if (a.t_start || a.t_stop)
+    hipExtLaunchKernelGGL(k_gemm_direct<SK>, dim3(grid), dim3(64 * SK), 0, st, a.t_start, a.t_stop, 0, a);
+  else
+    hipLaunchKernelGGL(k_gemm_direct<SK>, dim3(grid), dim3(64 * SK), 0, st, a);
+}
+
+hipError_t launch_gemm_direct(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
+  if (max_rows - a.row_begin <= 0) return hipSuccess;
+  if (a.A < 1 || a.A > DIR_AMAX || a.cseg % 8 || a.src_stride % 8 || a.Npad % DIRECT_BN || a.Kpad % 32 ||
+      a.Kpad < (a.K + 31) / 32 * 32 || a.ksplit != 1)
+    return hipErrorInvalidValue;
+  switch (a.sk) {
+    case 1: launch_direct_sk<1>(a, max_rows, st); break;
+    case 2: launch_direct_sk<2>(a, max_rows, st); break;
+    case 4: launch_direct_sk<4>(a, max_rows, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sscn

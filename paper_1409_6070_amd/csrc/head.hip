@@ -37,8 +37,8 @@ __global__ void __launch_bounds__(256) k_gather_dfeats(const T* __restrict__ gra
   }
 }
 
-// All weight packings of a step in one launch: blockIdx.y selects the job,
-// blockIdx.x a tile of 64 n x 32 k of its output.
+// All weight packings of a step in one launch: one workgroup per tile of 64 n
+// x 32 k of some job's output (tile_beg maps the flat block index to the job).
 //   mode 0 (forward):   Bt[n][f*cp_in + c]  = W[(f*c_in + c)*c_out + n]
 //     a transpose: the tile's 32 source rows are read along n (coalesced) into
 //     LDS and written out along k;
@@ -49,13 +49,15 @@ constexpr int PACK_N = 64, PACK_K = 32;
 template <typename T>
 __global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
   __shared__ T tile[PACK_K][PACK_N + 2];
-  const PackJob& j = pa.job[blockIdx.y];
-  const T* W = (const T*)j.W;
-  T* Bt = (T*)j.Bt;
-  const int tiles_k = j.Kpad / PACK_K;
-  const int ntiles = (j.Npad / PACK_N) * tiles_k;
   const T zero = Elem<T>::from_f32(0.f);
-  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  for (int g = blockIdx.x; g < pa.tile_beg[pa.njobs]; g += gridDim.x) {
+    int ji = 0;
+    while (ji + 1 < pa.njobs && g >= pa.tile_beg[ji + 1]) ++ji;
+    const PackJob& j = pa.job[ji];
+    const T* W = (const T*)j.W;
+    T* Bt = (T*)j.Bt;
+    const int tiles_k = j.Kpad / PACK_K;
+    const int t = g - pa.tile_beg[ji];
     const int n0 = (t / tiles_k) * PACK_N, k0 = (t % tiles_k) * PACK_K;
     if (j.mode == 0) {
       for (int i = threadIdx.x; i < PACK_K * PACK_N; i += 256) {
@@ -97,9 +99,10 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_softmax_xent(const float* __restrict__ logits,
                                                       const int32_t* __restrict__ labels, int32_t batch,
                                                       int32_t classes, T* dlogits, int32_t dl_stride,
-                                                      float* loss_part) {
+                                                      float* loss_part, float* loss, int32_t* counter) {
   constexpr int CACHE = 16;
   __shared__ float red[4];
+  __shared__ int last;
   const int b = blockIdx.x, t = threadIdx.x, w = t >> 6;
   const float* z = logits + (int64_t)b * classes;
   float v[CACHE];
@@ -137,19 +140,27 @@ __global__ void __launch_bounds__(256) k_softmax_xent(const float* __restrict__ 
   }
   for (int c = t + CACHE * 256; c < dl_stride; c += 256)
     dl[c] = Elem<T>::from_f32(c < classes ? (expf(z[c] - mx) * inv_s - (c == label ? 1.f : 0.f)) * inv_b : 0.f);
+  // this sample's loss term; the last workgroup to finish sums all of them in
+  // sample order (lane-strided, then a fixed butterfly) and resets the counter
   if (t == 0) {
     const bool ok = label >= 0 && label < classes;
     loss_part[b] = ok ? (logf(sum) + mx - z[label]) : 0.f;
+    __threadfence();
+    last = atomicAdd(counter, 1) == batch - 1;
+  }
+  __syncthreads();
+  if (!last || w != 0) return;
+  __threadfence();
+  float acc = 0.f;
+  for (int i = t; i < batch; i += 64) acc += __hip_atomic_load(&loss_part[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  acc = wave_sum(acc);
+  if (t == 0) {
+    *loss = acc / (float)batch;
+    __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
-__global__ void k_loss_final(const float* __restrict__ loss_part, int32_t batch, float* loss) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    float s = 0.f;
-    for (int b = 0; b < batch; ++b) s += loss_part[b];
-    *loss = batch > 0 ? s / (float)batch : 0.f;
-  }
-}
+__global__ void k_loss_zero(float* loss) { *loss = 0.f; }
 
 // grad_top[row(b)] = mask * dh[b] for non-empty samples (blockIdx.y = b < batch);
 // grad_top[0] = mask0 * sum of dh over empty samples (blockIdx.y = batch).
@@ -216,34 +227,40 @@ hipError_t launch_gather_dfeats(bool bf16, const void* grad0, int32_t cp0, const
   return hipGetLastError();
 }
 
-hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st) {
-  int64_t most = 0;
+hipError_t launch_pack_all(bool bf16, const PackArgs& in, hipStream_t st) {
+  PackArgs pa = in;
+  int64_t total = 0;
   for (int i = 0; i < pa.njobs; ++i) {
     const PackJob& j = pa.job[i];
     // GEMM padding: N to a multiple of 64, K to a multiple of 32
     if (j.Npad % PACK_N || j.Kpad % PACK_K) return hipErrorInvalidValue;
-    most = std::max<int64_t>(most, (int64_t)(j.Npad / PACK_N) * (j.Kpad / PACK_K));
+    pa.tile_beg[i] = (int32_t)total;
+    total += (int64_t)(j.Npad / PACK_N) * (j.Kpad / PACK_K);
   }
-  if (pa.njobs <= 0 || most <= 0) return hipSuccess;
-  const int gx = (int)std::max<int64_t>(1, std::min<int64_t>(most, 256));
+  if (pa.njobs <= 0 || total <= 0) return hipSuccess;
+  if (total >= (1ll << 31)) return hipErrorInvalidValue;
+  pa.tile_beg[pa.njobs] = (int32_t)total;
+  const int grid = (int)std::min<int64_t>(total, 16384);  // one tile per workgroup up to this many
   if (bf16)
-    hipLaunchKernelGGL(k_pack_all<__bf16>, dim3(gx, pa.njobs), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(k_pack_all<__bf16>, dim3(grid), dim3(256), 0, st, pa);
   else
-    hipLaunchKernelGGL(k_pack_all<float>, dim3(gx, pa.njobs), dim3(256), 0, st, pa);
+    hipLaunchKernelGGL(k_pack_all<float>, dim3(grid), dim3(256), 0, st, pa);
   return hipGetLastError();
 }
 
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
-                               void* dlogits, int32_t dl_stride, float* loss_part, float* loss, hipStream_t st) {
+                               void* dlogits, int32_t dl_stride, float* loss_part, float* loss, int32_t* counter,
+                               hipStream_t st) {
   if (batch > 0) {
     if (bf16)
       hipLaunchKernelGGL(k_softmax_xent<__bf16>, dim3(batch), dim3(256), 0, st, logits, labels, batch, classes,
-                         (__bf16*)dlogits, dl_stride, loss_part);
+                         (__bf16*)dlogits, dl_stride, loss_part, loss, counter);
     else
       hipLaunchKernelGGL(k_softmax_xent<float>, dim3(batch), dim3(256), 0, st, logits, labels, batch, classes,
-                         (float*)dlogits, dl_stride, loss_part);
+                         (float*)dlogits, dl_stride, loss_part, loss, counter);
+  } else {
+    hipLaunchKernelGGL(k_loss_zero, dim3(1), dim3(1), 0, st, loss);
   }
-  hipLaunchKernelGGL(k_loss_final, dim3(1), dim3(64), 0, st, loss_part, batch, loss);
   return hipGetLastError();
 }
 

@@ -60,6 +60,7 @@ struct GemmArgs {
   int32_t rows_host;
   int32_t row_begin;
   int32_t cfg;        // tile shape (see plan_gemm)
+  int32_t sk;         // GEMM_DIRECT: waves per workgroup, each summing one K range
   int32_t ksplit;     // > 1: K split over workgroups, fp32 partials in part
   float* part;        // [ksplit][part_rows][Npad]
   int32_t part_rows;  // row capacity of part
@@ -81,7 +82,13 @@ struct GemmPlan {
   int Npad = 0;
   int Kpad = 0;
   int ksplit = 1;
+  int sk = 1;  // direct kernel (cfg = GEMM_DIRECT): waves per workgroup splitting K
 };
+
+// cfg value of the bf16 direct-operand kernel (gemm_direct.hip): 32 x 64 output
+// tiles, each wave loading its MFMA operands straight from memory
+constexpr int GEMM_DIRECT = 4;
+constexpr int DIRECT_BM = 32, DIRECT_BN = 64;
 
 // weight-gradient GEMM, split over sites:
 //   part[chunk][m][n] = sum_{o in chunk} A(o, m) * dsrc[o][n]
@@ -133,6 +140,7 @@ constexpr int WG_BM = 128;
 inline int wgrad_bn(int c_out) { return (c_out + 127) / 128 * 128 <= (c_out + 63) / 64 * 64 ? 128 : 64; }
 
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st);
+hipError_t launch_gemm_direct(const GemmArgs& a, int64_t max_rows, hipStream_t st);
 // Weight gradients of n layers that all use tile shape cfg (0: 128 x 128,
 // 1: 128 x 64) in one launch.
 hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st);
@@ -200,11 +208,15 @@ struct PackJob {
 };
 struct PackArgs {
   int32_t njobs;
+  int32_t tile_beg[2 * MAX_LAYERS + 1];  // first tile of each job in the flat tile range (set by the launcher)
   PackJob job[2 * MAX_LAYERS];
 };
 hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st);
+// counter: a zero int32 in device memory; the last workgroup sums the loss terms
+// and sets it back to zero
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
-                               void* dlogits, int32_t dl_stride, float* loss_part, float* loss, hipStream_t st);
+                               void* dlogits, int32_t dl_stride, float* loss_part, float* loss, int32_t* counter,
+                               hipStream_t st);
 // drop: the softmax layer input's dropout (row key = sample), or off
 hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
                                int32_t batch, const void* Y_top, void* grad_top, int32_t cp, float slope,

@@ -25,7 +25,7 @@ __global__ void __launch_bounds__(256) k_rb_clear(uint64_t* bits0, int64_t nword
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (; i < nwords; i += stride) bits0[i] = 0ull;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *err = 0;
+  if (blockIdx.x == 0 && threadIdx.x < 4) err[threadIdx.x] = 0;  // error word and the completion counters
 }
 
 __global__ void __launch_bounds__(256) k_rb_insert(const int32_t* __restrict__ coords, int32_t n, int32_t batch,
@@ -62,6 +62,27 @@ __device__ inline uint64_t row_mask_word(int w, int S) {
   return (1ull << nb) - 1ull;
 }
 
+// Exclusive prefix of one value per thread over the block (RB_THREADS = 4
+// waves): an inclusive scan inside each wave with lane shuffles, then the wave
+// totals through LDS -- two barriers.  Returns the prefix; *total gets the sum.
+__device__ inline int block_exclusive_scan(int local, int* scratch, int* total) {
+  static_assert(RB_THREADS == 256, "four waves");
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  int v = local;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int u = __shfl_up(v, off, 64);
+    if (lane >= off) v += u;
+  }
+  if (lane == 63) scratch[wv] = v;
+  __syncthreads();
+  int base = 0;
+  for (int i = 0; i < wv; ++i) base += scratch[i];
+  *total = (scratch[0] + scratch[1]) + (scratch[2] + scratch[3]);
+  __syncthreads();
+  return base + v - local;
+}
+
 // Block-wide exclusive prefix of popcounts over nw words held in LDS.
 // Writes wpre[0..nw) (global) and returns the total.
 __device__ int block_popcount_scan(const uint64_t* words, int nw, int32_t* wpre, int* scratch) {
@@ -73,16 +94,8 @@ __device__ int block_popcount_scan(const uint64_t* words, int nw, int32_t* wpre,
     int w = beg + j;
     if (w < nw) local += __popcll(words[w]);
   }
-  scratch[t] = local;
-  __syncthreads();
-  // Hillis-Steele inclusive scan over RB_THREADS values
-  for (int off = 1; off < RB_THREADS; off <<= 1) {
-    int v = (t >= off) ? scratch[t - off] : 0;
-    __syncthreads();
-    scratch[t] += v;
-    __syncthreads();
-  }
-  int run = scratch[t] - local;
+  int total;
+  int run = block_exclusive_scan(local, scratch, &total);
   for (int j = 0; j < per; ++j) {
     int w = beg + j;
     if (w < nw) {
@@ -90,8 +103,6 @@ __device__ int block_popcount_scan(const uint64_t* words, int nw, int32_t* wpre,
       run += __popcll(words[w]);
     }
   }
-  int total = scratch[RB_THREADS - 1];
-  __syncthreads();
   return total;
 }
 
@@ -163,7 +174,7 @@ __global__ void __launch_bounds__(RB_THREADS) k_rb_bitmaps(RulebookArgs a, int32
 // Sample offsets and layer totals: one workgroup per layer, a block-wide
 // exclusive scan of the per-sample counts.
 __global__ void __launch_bounds__(RB_THREADS) k_rb_offsets(RulebookArgs a) {
-  __shared__ int scratch[RB_THREADS];
+  __shared__ int scratch[RB_THREADS / 64];
   const int s = blockIdx.x;
   const int t = threadIdx.x;
   const LayerBits& L = a.L[s];
@@ -172,21 +183,14 @@ __global__ void __launch_bounds__(RB_THREADS) k_rb_offsets(RulebookArgs a) {
   int local = 0;
   for (int j = 0; j < per; ++j)
     if (beg + j < a.batch) local += L.scount[beg + j];
-  scratch[t] = local;
-  __syncthreads();
-  for (int off = 1; off < RB_THREADS; off <<= 1) {
-    const int v = (t >= off) ? scratch[t - off] : 0;
-    __syncthreads();
-    scratch[t] += v;
-    __syncthreads();
-  }
-  int run = scratch[t] - local;
+  int total;
+  int run = block_exclusive_scan(local, scratch, &total);
   for (int j = 0; j < per; ++j)
     if (beg + j < a.batch) {
       L.soff[beg + j] = run;
       run += L.scount[beg + j];
     }
-  if (t == RB_THREADS - 1) a.counts[s] = scratch[RB_THREADS - 1];
+  if (t == 0) a.counts[s] = total;
 }
 
 // Site keys of every layer, in row order: one thread per bitmap word.
