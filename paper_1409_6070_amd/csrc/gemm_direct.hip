@@ -36,7 +36,7 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   typedef __bf16 T;
   constexpr int TM = DIRECT_BM / 16, TN = DIRECT_BN / 16;
   constexpr int BM = DIRECT_BM, BN = DIRECT_BN, NT = 64 * SK;
-  constexpr int CH = 4;        // k blocks (32 k each) of loads in flight per wave
+  constexpr int CH = 3;        // k blocks (32 k each) of loads in flight per wave
   constexpr int RP = BN + 4;   // LDS pitch of the partial sums (floats)
   __shared__ int32_t Rs[BM * DIR_AMAX];
   __shared__ __attribute__((aligned(16))) float red[SK][BM][RP];
@@ -60,6 +60,12 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int tn = tile % tiles_n, tm = tile / tiles_n;
     const int m0 = a.row_begin + tm * BM, n0 = tn * BN;
+    // bias of the 8 columns this thread writes in the epilogue (its vectors all
+    // share one column group), fetched now so that it arrives during the K loop
+    const int c8e = (tid % (BN / 8)) * 8;
+    float bias8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bias8[e] = (a.bias && n0 + c8e + e < a.N) ? a.bias[n0 + c8e + e] : 0.f;
     for (int e = tid; e < BM * A; e += NT) {  // the tile's window rows (-1: none)
       const int r = e / A, f = e - r * A;
       const int m = m0 + r;
@@ -121,8 +127,9 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
 
     if (epi_stores_T(a.epi)) {
       // 16-byte vectors: 8 columns of one row, summed over the waves in order
+      static_assert(NT % (BN / 8) == 0, "each thread keeps one column group");
       for (int v = tid; v < BM * (BN / 8); v += NT) {
-        const int r = v / (BN / 8), c8 = (v - r * (BN / 8)) * 8;
+        const int r = v / (BN / 8), c8 = c8e;
         const int m = m0 + r, n = n0 + c8;
         if (m >= rows || n >= a.out_cols) continue;
         float s[8];
@@ -142,8 +149,7 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
         if (a.epi == EPI_STORE_MASK) y = *(const v4u*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float b = (a.bias && n + e < a.N) ? a.bias[n + e] : 0.f;
-          float v8 = epi_value<T>(a, s[e], b);
+          float v8 = epi_value<T>(a, s[e], bias8[e]);
           if (a.epi == EPI_STORE_MASK) v8 *= act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope);
           ((T*)&o)[e] = Elem<T>::from_f32(v8);
         }
