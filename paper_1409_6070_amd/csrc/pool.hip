@@ -75,23 +75,37 @@ __global__ void __launch_bounds__(256) k_pool_fwd(const T* __restrict__ X_in, in
   }
 }
 
-// Sum over one block's rows, per channel: thread t holds VE channels of vector
-// t % nv; the 256/nv row lanes are combined in LDS in a fixed order; the sum of
-// channel e goes to out[e * PM].
-template <int VE>
-__device__ inline void block_channel_sums(const float (&acc)[VE], float* red, int nv, int cp, float* out, int PM) {
+// Sums over one block's rows for K slots at once: thread t holds acc[k][0..VE)
+// for channel vector t % nv (the 256/nv row lanes of a vector are combined in
+// a fixed order); the sum of slot k, channel e goes to out[k * slot_stride +
+// e * PM].  Up to SB slots share one pass through LDS (red holds SB * 256 * VE
+// floats): one barrier pair per pass, every (slot, channel) summed by one thread
+// with independent LDS reads.
+constexpr int SUM_SB = 6;
+template <int VE, int K>
+__device__ inline void block_channel_sums(const float (&acc)[K][VE], float* red, int nv, int cp, float* out,
+                                          int64_t slot_stride, int PM) {
   const int t = threadIdx.x;
   const int lanes = 256 / nv;
 #pragma unroll
-  for (int j = 0; j < VE; ++j) red[t * VE + j] = acc[j];
-  __syncthreads();
-  for (int e = t; e < cp; e += 256) {  // channel e = vector e / VE, element e % VE
-    const int vv = e / VE, jj = e - vv * VE;
-    float s = 0.f;
-    for (int l = 0; l < lanes; ++l) s += red[(l * nv + vv) * VE + jj];
-    out[(int64_t)e * PM] = s;
+  for (int k0 = 0; k0 < K; k0 += SUM_SB) {
+#pragma unroll
+    for (int kk = 0; kk < SUM_SB; ++kk)
+      if (k0 + kk < K)
+#pragma unroll
+        for (int j = 0; j < VE; ++j) red[(kk * 256 + t) * VE + j] = acc[k0 + kk < K ? k0 + kk : 0][j];
+    __syncthreads();
+    const int kn = K - k0 < SUM_SB ? K - k0 : SUM_SB;
+    for (int item = t; item < kn * cp; item += 256) {
+      const int kk = item / cp, e = item - kk * cp;
+      const int vv = e / VE, jj = e - vv * VE;
+      const float* base = red + kk * 256 * VE + vv * VE + jj;
+      float s = 0.f;
+      for (int l = 0; l < lanes; ++l) s += base[l * nv * VE];
+      out[(int64_t)(k0 + kk) * slot_stride + (int64_t)e * PM] = s;
+    }
+    __syncthreads();
   }
-  __syncthreads();
 }
 
 // gnd[k] = (R[i][k] == 0): window position k of row i reads the ground row.
@@ -125,7 +139,7 @@ __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g) {
   constexpr int VE = Elem<T>::VE;
   constexpr int J = 2 + AC;
   typedef typename ArgPack<VE>::W AW;
-  __shared__ float red[256 * VE];
+  __shared__ float red[SUM_SB * 256 * VE];
   const int nv = g.cp / VE;
   const int lanes = 256 / nv;
   const int t = threadIdx.x;
@@ -177,9 +191,7 @@ __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g) {
       }
     }
   }
-#pragma unroll
-  for (int k = 0; k < J; ++k)
-    block_channel_sums<VE>(acc[k], red, nv, g.cp, g.part + (int64_t)k * g.cp * g.PM + blockIdx.x, g.PM);
+  block_channel_sums<VE, J>(acc, red, nv, g.cp, g.part + blockIdx.x, (int64_t)g.cp * g.PM, g.PM);
 }
 
 // Partial sums behind a convolution's bias gradient and ground-row sums, and
@@ -195,7 +207,7 @@ template <typename T, int AC>
 __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
   constexpr int VE = Elem<T>::VE;
   typedef typename ArgPack<VE>::W AW;
-  __shared__ float red[256 * VE];
+  __shared__ float red[SUM_SB * 256 * VE];
   const int nv = g.cp / VE;
   const int lanes = 256 / nv;
   const int t = threadIdx.x;
@@ -224,7 +236,10 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
         }
       }
     }
-    block_channel_sums<VE>(acc, red, nv, g.cp, g.part + blockIdx.x, g.PM);
+    float acc1[1][VE];
+#pragma unroll
+    for (int j = 0; j < VE; ++j) acc1[0][j] = acc[j];
+    block_channel_sums<VE, 1>(acc1, red, nv, g.cp, g.part + blockIdx.x, (int64_t)g.cp * g.PM, g.PM);
     return;
   }
   const int b = blockIdx.x - g.B1;
@@ -252,9 +267,7 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
       }
     }
   }
-#pragma unroll
-  for (int k = 0; k <= AC; ++k)
-    block_channel_sums<VE>(acc[k], red, nv, g.cp, g.part + (int64_t)(1 + k) * g.cp * g.PM + b, g.PM);
+  block_channel_sums<VE, 1 + AC>(acc, red, nv, g.cp, g.part + (int64_t)g.cp * g.PM + b, (int64_t)g.cp * g.PM, g.PM);
 }
 
 // Final pass: one block per channel c; its 4 wavefronts sum each slot's
