@@ -115,10 +115,13 @@ def read_traffic(kernel, dtype, workload):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    src = os.path.join(ROOT, "paper_1409_6070_amd", "csrc", kv.get("source", "gemm.hip"))
-    if not os.path.exists(src):
-        return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in kv.get("source", "gemm.hip").split():
+        src = os.path.join(ROOT, "paper_1409_6070_amd", "csrc", name)
+        if not os.path.exists(src):
+            return None
+        h.update(open(src, "rb").read())
+    sha = h.hexdigest()[:16]
     if kv.get("source_sha256_16") != sha or kv.get("dtype") != dtype or kv.get("workload") != workload:
         return None
     try:
@@ -324,8 +327,9 @@ def main():
     peak = MFMA_PEAK[args.dtype]
     traffic = read_traffic("gather_gemm", args.dtype, cfg.name)
     roofline = {
-        "kernel": ("k_gemm_gather (implicit-gather MFMA GEMM: conv forward, softmax layer logits)" if infer else
-                   "k_gemm_gather (implicit-gather MFMA GEMM: conv forward, conv input gradient, softmax layer)"),
+        "kernel": ("gather-GEMM class: k_gemm_gather (LDS-tiled) and k_gemm_direct (direct-operand) implicit-gather "
+                   "MFMA GEMMs; " + ("conv forward, softmax layer logits" if infer else
+                                     "conv forward, conv input gradient, softmax layer")),
         "bound": "mfma", "achieved": round(achieved / 1e12, 3), "peak": peak / 1e12, "unit": "TFLOP/s",
         "frac": round(achieved / peak, 5), "traffic": traffic,
         "launches_per_step": g_launches / args.steps, "avg_launch_us": round(avg_launch_s * 1e6, 3),
