@@ -476,40 +476,47 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp) {
 // dW (and db) from the split-K partials, for a group of layers (block b
 // belongs to layer l with blk_beg[l] <= b < blk_beg[l + 1]).  A block has G
 // thread groups (G = 16, or fewer when there are fewer chunks) of 256/G
-// threads, one output per thread of a group; group g sums chunks g, g+G, ...;
-// the G group sums are added in a fixed order.
+// threads, four consecutive outputs (one 16-byte partial load per chunk) per
+// thread of a group; group g sums chunks g, g+G, ...; the G group sums are
+// added in a fixed order.
 __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
-  __shared__ float red[256];
+  __shared__ f32x4 red[256];
   int l = 0;
   while (l + 1 < grp.n && (int)blockIdx.x >= grp.blk_beg[l + 1]) ++l;
   const WGradArgs& a = grp.L[l];
   const int nch = wgrad_chunks_dev(a, a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host, grp.BK);
   if (nch <= 1) return;  // the weight-gradient kernel wrote the results
   const int G = grp.G[l];
-  const int E = 256 / G;  // outputs per block
+  const int E = 256 / G;  // output quads per block
   const int m_gather = a.A * a.cseg;
   const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;
-  const int64_t total = (int64_t)m_rows * a.c_out;
+  const int q_per_row = (a.c_out + 3) / 4;  // quads of 4 consecutive columns (the partials are Npad wide)
+  const int64_t total = (int64_t)m_rows * q_per_row;
   const int el = threadIdx.x % E, grpi = threadIdx.x / E;
   const int64_t t = (int64_t)((int)blockIdx.x - grp.blk_beg[l]) * E + el;
   int m = 0, n = 0;
-  float s = 0.f;
+  f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
   if (t < total) {
-    m = (int)(t / a.c_out);
-    n = (int)(t - (int64_t)m * a.c_out);
-    const float* part = a.part;
-    for (int ch = grpi; ch < nch; ch += G) s += part[((int64_t)ch * a.Mpad + m) * a.Npad + n];
+    m = (int)(t / q_per_row);
+    n = (int)(t - (int64_t)m * q_per_row) * 4;
+    const float* part = a.part + (int64_t)m * a.Npad + n;
+    const int64_t cstride = (int64_t)a.Mpad * a.Npad;
+    for (int ch = grpi; ch < nch; ch += G) s += *(const f32x4*)(part + ch * cstride);
   }
   red[threadIdx.x] = s;
   __syncthreads();
   if (grpi != 0 || t >= total) return;
-  s = 0.f;
+  s = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int g = 0; g < G; ++g) s += red[g * E + el];
-  if (m < m_gather) {
-    const int f = m / a.cseg, c = m - f * a.cseg;
-    if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + n] = s;
-  } else if (m == a.m_ones) {
-    if (a.db) a.db[n] = s;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (n + e >= a.c_out) break;
+    if (m < m_gather) {
+      const int f = m / a.cseg, c = m - f * a.cseg;
+      if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + n + e] = s[e];
+    } else if (m == a.m_ones) {
+      if (a.db) a.db[n + e] = s[e];
+    }
   }
 }
 
@@ -668,7 +675,8 @@ hipError_t launch_wgrad_reduce(bool bf16, const WGradArgs* layers, int n, hipStr
     const WGradArgs& a = layers[l];
     if (a.nchunks <= 1) continue;  // the weight-gradient kernel wrote the results
     const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : a.A * a.cseg;
-    const int64_t total = (int64_t)m_rows * a.c_out;
+    const int64_t total = (int64_t)m_rows * ((a.c_out + 3) / 4);  // output quads
+    if (a.Npad % 4) return hipErrorInvalidValue;
     const int G = a.nchunks >= 16 ? 16 : (a.nchunks >= 8 ? 8 : (a.nchunks >= 4 ? 4 : 2));
     const int E = 256 / G;
     g.L[g.n] = a;
