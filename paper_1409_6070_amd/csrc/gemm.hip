@@ -283,19 +283,23 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   }
 }
 
-// Sum of the split-K partials plus the epilogue.
+// Sum of the split-K partials plus the epilogue: four consecutive columns per
+// thread, one 16-byte partial load per split (the partials are Npad wide).
 template <typename T>
 __global__ void __launch_bounds__(256) k_gemm_splitk_reduce(GemmArgs a) {
   const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
   const int64_t span = rows - a.row_begin;
   if (span <= 0) return;
-  const int64_t total = span * a.out_cols;
+  const int quads = (a.out_cols + 3) / 4;
+  const int64_t total = span * quads;
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t m = a.row_begin + t / a.out_cols;
-    const int n = (int)(t % a.out_cols);
-    float s = 0.f;
-    for (int ks = 0; ks < a.ksplit; ++ks) s += a.part[((int64_t)ks * a.part_rows + m) * a.Npad + n];
-    store_out<T>(a, m, n, epi_value<T>(a, s, (a.bias && n < a.N) ? a.bias[n] : 0.f));
+    const int64_t m = a.row_begin + t / quads;
+    const int n = (int)(t % quads) * 4;
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < a.ksplit; ++ks) s += *(const f32x4*)(a.part + ((int64_t)ks * a.part_rows + m) * a.Npad + n);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n + e < a.out_cols) store_out<T>(a, m, n + e, epi_value<T>(a, s[e], (a.bias && n + e < a.N) ? a.bias[n + e] : 0.f));
   }
 }
 
@@ -561,7 +565,7 @@ static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   else
     hipLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a);
   if (a.ksplit > 1) {
-    const int64_t total = span * a.out_cols;
+    const int64_t total = span * ((a.out_cols + 3) / 4);
     const int g2 = (int)std::min<int64_t>(std::max<int64_t>((total + 255) / 256, 1), 4096);
     if (timed)
       hipExtLaunchKernelGGL(k_gemm_splitk_reduce<T>, dim3(g2), dim3(256), 0, st, nullptr, a.t_stop, 0, a);
