@@ -653,6 +653,31 @@ static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_
   });
 }
 
+// The final ground pass of convolution s as an extra task.
+static ExtraTask final_task(const sscn_net* net, int s, bool pool_above) {
+  const LayerPlan& L = net->L[s];
+  ExtraTask x{};
+  x.kind = 1;
+  x.blocks = L.Cp;
+  x.AC = (needs_row0(net, s) && L.A > 1) ? L.A : 0;
+  x.g = ground_args(net, s, pool_above);
+  return x;
+}
+
+// Row 0 of the gradient below convolution s as an extra task (reads D0 from
+// its final pass, which must have run in an earlier launch).
+static ExtraTask row0_task(const sscn_net* net, int s) {
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lb = net->L[s - 1];
+  const ParamPlan& P = net->P[L.conv_index];
+  ExtraTask x{};
+  x.kind = 2;
+  x.blocks = Lb.Cp;
+  x.r = Row0Args{net->W[L.conv_index], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad,
+                 Lb.kind == 1 ? Lb.X : nullptr, net->slope};
+  return x;
+}
+
 // Weight-gradient arguments of convolution s (run once its delta is complete).
 static WGradArgs conv_wgrad_args(const sscn_net* net, int s) {
   const LayerPlan& L = net->L[s];
@@ -704,7 +729,7 @@ static hipError_t run_wgrads(sscn_net* net, const WGradArgs* w, int n, hipStream
 // partial sums of the convolution below), or the input-gradient GEMM of a
 // convolution.  (The GEMM reads delta rows >= 1 only: a window list entry of -1
 // selects zero, whatever its load of row 0 returned.)
-static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
+static hipError_t rows_below(sscn_net* net, int s, hipStream_t st, const ExtraTask* extra = nullptr) {
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
   if (L.kind == 2) {
@@ -712,7 +737,7 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
     if (Lb.kind != 1) return hipErrorInvalidValue;  // a pooling layer sits on a convolution
     const GroundArgs g = ground_args(net, s - 1, true);
     const int Ac = (needs_row0(net, s - 1) && Lb.A > 1) ? Lb.A : 0;
-    return timed(net, SSCN_KC_POOL_BWD, st, [&] { return launch_ground(net->bf16, g, Ac, 1, st); });
+    return timed(net, SSCN_KC_POOL_BWD, st, [&] { return launch_ground(net->bf16, g, Ac, 1, st, extra); });
   }
   if (!(s > 1 || net->want_dfeats)) return hipSuccess;
   const ParamPlan& P = net->P[L.conv_index];
@@ -738,6 +763,7 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st) {
     g.mask_stride = Lb.Cp;
     g.slope = net->slope;
   }
+  if (extra) g.x = *extra;
   g.rows_dev = net->counts + s - 1;
   g.rows_add = 1;
   g.row_begin = 1;
@@ -871,14 +897,50 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
                                    net->slope, head_drop(net), st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
-  // Stages from the top down, all on the caller's stream: each convolution's
-  // delta is completed (row 0, bias and ground-row sums, row 0 of the
-  // gradient below), then rows >= 1 of the gradient below it.
+  // Stages from the top down, all on the caller's stream.  Per convolution:
+  // its bias and ground-row sums (with a pooling layer above they come out of
+  // that layer's backward), rows >= 1 of the gradient below, the final ground
+  // pass (row 0 of delta, db, D0) and row 0 of the gradient below.  The final
+  // pass needs only the sums and rides as extra workgroups on the input-gradient
+  // GEMM, which reads delta rows >= 1 only (a 1x1 layer's GEMM reads row 0 too:
+  // it rides there only when row 0 is not rewritten, i.e. without a pooling
+  // layer above); row 0 below needs D0 and rides on the next launch.
+  ExtraTask pending{};  // row 0 of a gradient below, waiting for the next launch
   for (int s = top; s >= 1; --s) {
-    if (net->L[s].kind == 1 && ground_level(net, s, s < top && net->L[s + 1].kind == 2, st) != hipSuccess)
-      return SSCN_ERR_HIP;
-    if (rows_below(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
+    const LayerPlan& L = net->L[s];
+    hipError_t e = hipSuccess;
+    if (L.kind == 2) {
+      e = rows_below(net, s, st, pending.kind ? &pending : nullptr);
+      pending = ExtraTask{};
+    } else {
+      const bool pool_above = s < top && net->L[s + 1].kind == 2;
+      const bool row0 = needs_row0(net, s) && L.A > 1;
+      const ExtraTask fin = final_task(net, s, pool_above);
+      if (!pool_above) {  // the sums over delta rows, as their own launch
+        const GroundArgs g = ground_args(net, s, false);
+        e = timed(net, SSCN_KC_GROUND, st, [&] {
+          return launch_ground(net->bf16, g, fin.AC, 3, st, pending.kind ? &pending : nullptr);
+        });
+        pending = ExtraTask{};
+      }
+      const bool gemm_below = s > 1 || net->want_dfeats;
+      if (e == hipSuccess && gemm_below && (!pool_above || L.A > 1)) {
+        e = rows_below(net, s, st, &fin);
+      } else if (e == hipSuccess) {
+        const GroundArgs g = ground_args(net, s, pool_above);
+        e = timed(net, SSCN_KC_GROUND, st, [&] {
+          return launch_ground(net->bf16, g, fin.AC, 2, st, pending.kind ? &pending : nullptr);
+        });
+        pending = ExtraTask{};
+        if (e == hipSuccess && gemm_below) e = rows_below(net, s, st);
+      }
+      if (row0) pending = row0_task(net, s);
+    }
+    if (e != hipSuccess) return SSCN_ERR_HIP;
   }
+  if (pending.kind &&
+      timed(net, SSCN_KC_GROUND, st, [&] { return launch_extra(net->bf16, pending, st); }) != hipSuccess)
+    return SSCN_ERR_HIP;
   if (d_dfeats) {
     const LayerPlan& L0 = net->L[0];
     if (timed(net, SSCN_KC_HEAD, st, [&] {

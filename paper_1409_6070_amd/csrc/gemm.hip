@@ -18,6 +18,7 @@
 
 #include "common.h"
 #include "epilogue.h"
+#include "ground_tasks.h"
 #include "kernels.h"
 
 #include <hip/hip_ext.h>
@@ -129,6 +130,7 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave / C::WN, wn = wave % C::WN;
+  if (run_extra<T>(a.x)) return;
   const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
   const int span = rows - a.row_begin;
   if (span <= 0) return;
@@ -141,7 +143,8 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   const T* Bt = (const T*)a.Bt;
   const int A = a.A;
 
-  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+  const int grid = own_grid(a.x);
+  for (int tile = blockIdx.x; tile < ntiles; tile += grid) {
     const int tn = tile % tiles_n;
     const int t2 = tile / tiles_n;
     const int tm = t2 % tiles_m;
@@ -525,30 +528,8 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
 }
 
 template <typename T>
-__global__ void __launch_bounds__(256) k_row0_dx(const T* __restrict__ W, const float* __restrict__ D0, int32_t A,
-                                                 int32_t c_in, int32_t c_out, int32_t cp_in, T* grad_in,
-                                                 const T* __restrict__ Y_below, float slope) {
-  __shared__ float red[256];
-  const int c = blockIdx.x;
-  float s = 0.f;
-  if (c < c_in) {
-    const int len = A * c_out;
-    for (int t = threadIdx.x; t < len; t += blockDim.x) {
-      const int f = t / c_out, n = t - f * c_out;
-      s += Elem<T>::to_f32(W[((int64_t)f * c_in + c) * c_out + n]) * D0[t];
-    }
-  }
-  red[threadIdx.x] = s;
-  __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
-    if (threadIdx.x < off) red[threadIdx.x] += red[threadIdx.x + off];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0 && c < cp_in) {
-    float v = red[0];
-    if (Y_below) v *= act_factor(Elem<T>::to_f32(Y_below[c]), slope);
-    grad_in[c] = Elem<T>::from_f32(v);
-  }
+__global__ void __launch_bounds__(256) k_row0_dx(Row0Args r) {
+  row0_dx_block<T>(r, blockIdx.x);
 }
 
 static int device_grid_limit() { return 256 * 8; }
@@ -557,7 +538,8 @@ template <typename T, class C>
 static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   const int64_t span = max_rows - a.row_begin;
   const int64_t tiles = ((span + C::BM - 1) / C::BM) * (a.Npad / C::BN) * a.ksplit;
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit());
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit()) +
+                   (a.x.kind ? a.x.blocks : 0);
   const bool timed = a.t_start || a.t_stop;
   if (timed)
     hipExtLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a.t_start,
@@ -695,12 +677,11 @@ hipError_t launch_wgrad_reduce(bool bf16, const WGradArgs* layers, int n, hipStr
 
 hipError_t launch_row0_dx(bool bf16, const void* W, const float* D0, int32_t A, int32_t c_in, int32_t c_out,
                           int32_t cp_in, void* grad_in, const void* Y_below, float slope, hipStream_t st) {
+  const Row0Args r{W, D0, A, c_in, c_out, cp_in, grad_in, Y_below, slope};
   if (bf16)
-    hipLaunchKernelGGL(k_row0_dx<__bf16>, dim3(cp_in), dim3(256), 0, st, (const __bf16*)W, D0, A, c_in, c_out, cp_in,
-                       (__bf16*)grad_in, (const __bf16*)Y_below, slope);
+    hipLaunchKernelGGL(k_row0_dx<__bf16>, dim3(cp_in), dim3(256), 0, st, r);
   else
-    hipLaunchKernelGGL(k_row0_dx<float>, dim3(cp_in), dim3(256), 0, st, (const float*)W, D0, A, c_in, c_out, cp_in,
-                       (float*)grad_in, (const float*)Y_below, slope);
+    hipLaunchKernelGGL(k_row0_dx<float>, dim3(cp_in), dim3(256), 0, st, r);
   return hipGetLastError();
 }
 

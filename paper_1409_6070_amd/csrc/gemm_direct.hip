@@ -13,6 +13,7 @@
 
 #include "common.h"
 #include "epilogue.h"
+#include "ground_tasks.h"
 #include "kernels.h"
 
 #include <hip/hip_ext.h>
@@ -41,6 +42,7 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   __shared__ int32_t Rs[BM * DIR_AMAX];
   __shared__ __attribute__((aligned(16))) float red[SK][BM][RP];
 
+  if (run_extra<T>(a.x)) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
@@ -57,7 +59,8 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   const T* src = (const T*)a.src;
   const T* Bt = (const T*)a.Bt;
 
-  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+  const int grid = own_grid(a.x);
+  for (int tile = blockIdx.x; tile < ntiles; tile += grid) {
     const int tn = tile % tiles_n, tm = tile / tiles_n;
     const int m0 = a.row_begin + tm * BM, n0 = tn * BN;
     // bias of the 8 columns this thread writes in the epilogue (its vectors all
@@ -174,7 +177,7 @@ template <int SK>
 static void launch_direct_sk(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   const int64_t span = max_rows - a.row_begin;
   const int64_t tiles = ((span + DIRECT_BM - 1) / DIRECT_BM) * (a.Npad / DIRECT_BN);
-  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), 2048);
+  const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), 2048) + (a.x.kind ? a.x.blocks : 0);
   if (a.t_start || a.t_stop)
     hipExtLaunchKernelGGL(k_gemm_direct<SK>, dim3(grid), dim3(64 * SK), 0, st, a.t_start, a.t_stop, 0, a);
   else

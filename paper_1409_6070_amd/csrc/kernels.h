@@ -39,6 +39,53 @@ enum Epilogue : int32_t {
   EPI_STORE_MASK = 5,  // times act_factor(mask[m][n], slope), store in storage dtype
 };
 
+// Arguments of the bias and ground-row sums of one convolution (launch_ground).
+struct GroundArgs {
+  // pooling layer above (B1 = 0: none)
+  const void* dY;
+  const uint8_t* argmax;
+  const int32_t* Rp;
+  const int32_t* n_pool;
+  int32_t B1;
+  const void* Y_below;  // the convolution's output (ReLU mask of row 0)
+  // the convolution
+  void* dZ;            // delta, rows 0..n; row 0 written when B1 > 0
+  const int32_t* R;    // its window list [rows][AC]
+  const int32_t* n_rows;
+  int32_t B2;
+  int32_t stride, cp, c_out;
+  float slope;  // rectifier of the convolution (0: ReLU, 1/3: leaky)
+  float* part;  // [(2 + AC) * cp * PM]
+  int32_t PM;   // partial stride, >= B1, B2
+  float* db;
+  float* D0;
+};
+
+// Row 0 of the gradient below a convolution (its ground row): for input channel
+// c, sum over window positions f and outputs n of W[f][c][n] * D0[f][n], times
+// the rectifier derivative of the layer below when that layer is a convolution
+// (Y_below non-null).
+struct Row0Args {
+  const void* W;
+  const float* D0;
+  int32_t A, c_in, c_out, cp_in;
+  void* grad_in;
+  const void* Y_below;
+  float slope;
+};
+
+// Work that rides along as extra workgroups at the end of another launch (the
+// last `blocks` workgroups of the grid), independent of that launch's own work:
+//   kind 1: the ground final pass of a convolution (one workgroup per channel, cp);
+//   kind 2: row 0 of the gradient below a convolution (one per channel, cp_in).
+struct ExtraTask {
+  int32_t kind;    // 0: none
+  int32_t blocks;
+  int32_t AC;      // kind 1: window positions whose ground sums are finished (0..9)
+  GroundArgs g;
+  Row0Args r;
+};
+
 struct GemmArgs {
   const void* src;
   int32_t src_stride;
@@ -73,6 +120,7 @@ struct GemmArgs {
   // when the GEMM kernel starts, t_stop when the last kernel of the launch
   // (the GEMM, or its split-K reduce) ends
   hipEvent_t t_start, t_stop;
+  ExtraTask x;  // extra workgroups appended to the launch (kind 0: none)
 };
 
 // Tile shape and padding of one GEMM, chosen on the host from its row bound.
@@ -164,32 +212,17 @@ hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const
 // 9}) of a convolution with output gradient delta = dZ, and, with a pooling
 // layer above (B1 > 0), row 0 of delta itself.  Needs delta rows >= 1 and, with
 // a pooling layer, that layer's dY (rows 0..n_pool), argmax and windows Rp.
-struct GroundArgs {
-  // pooling layer above (B1 = 0: none)
-  const void* dY;
-  const uint8_t* argmax;
-  const int32_t* Rp;
-  const int32_t* n_pool;
-  int32_t B1;
-  const void* Y_below;  // the convolution's output (ReLU mask of row 0)
-  // the convolution
-  void* dZ;            // delta, rows 0..n; row 0 written when B1 > 0
-  const int32_t* R;    // its window list [rows][AC]
-  const int32_t* n_rows;
-  int32_t B2;
-  int32_t stride, cp, c_out;
-  float slope;  // rectifier of the convolution (0: ReLU, 1/3: leaky)
-  float* part;  // [(2 + AC) * cp * PM]
-  int32_t PM;   // partial stride, >= B1, B2
-  float* db;
-  float* D0;
-};
 // kind 0: partial sums over delta rows >= 1 (and, with B1 > 0, over the pooling
 //         rows), then the final pass;
 // kind 1: pooling backward fused with those partial sums (writes delta rows >= 1;
 //         needs B1 == B2);
-// kind 2: the final pass alone, over partials written by kind 1.
-hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, hipStream_t st);
+// kind 2: the final pass alone, over partials written by kind 1 or 3;
+// kind 3: the partial sums of kind 0 alone.
+// extra: work appended as extra workgroups of the first kernel launched.
+hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, hipStream_t st,
+                         const ExtraTask* extra = nullptr);
+// the extra task alone, as its own launch
+hipError_t launch_extra(bool bf16, const ExtraTask& x, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // input, parameters, head

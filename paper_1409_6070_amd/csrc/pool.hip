@@ -15,6 +15,7 @@
 // a fixed-order final pass: deterministic).
 
 #include "common.h"
+#include "ground_tasks.h"
 #include "kernels.h"
 
 namespace sscn {
@@ -135,7 +136,8 @@ __device__ inline void ground_flags(const int32_t* __restrict__ R, int64_t i, in
 //            the ground state).
 // Partial p = block b of slot k, channel c: part[(k * cp + c) * PM + b].
 template <typename T, int AC>
-__global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g) {
+__global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g, ExtraTask x) {
+  if (run_extra<T>(x)) return;
   constexpr int VE = Elem<T>::VE;
   constexpr int J = 2 + AC;
   typedef typename ArgPack<VE>::W AW;
@@ -156,7 +158,7 @@ __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g) {
     for (int j = 0; j < VE; ++j) acc[k][j] = 0.f;
   if (rl < lanes) {
 #pragma unroll 2
-    for (int o = 1 + blockIdx.x * lanes + rl; o <= n; o += gridDim.x * lanes) {
+    for (int o = 1 + blockIdx.x * lanes + rl; o <= n; o += own_grid(x) * lanes) {
       const i32x4 r = *(const i32x4*)(g.Rp + (int64_t)o * 4);
       const AW am = *(const AW*)(g.argmax + (int64_t)o * g.stride + c);
       const u32x4 gv = *(const u32x4*)(dY + (int64_t)o * g.stride + c);
@@ -204,7 +206,8 @@ __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g) {
 // Row 0 of delta enters in the final pass.  A block takes a contiguous range of
 // rows; partial p of slot k, channel c is part[(k * cp + c) * PM + p].
 template <typename T, int AC>
-__global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
+__global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g, ExtraTask x) {
+  if (run_extra<T>(x)) return;
   constexpr int VE = Elem<T>::VE;
   typedef typename ArgPack<VE>::W AW;
   __shared__ float red[SUM_SB * 256 * VE];
@@ -270,60 +273,16 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g) {
   block_channel_sums<VE, 1 + AC>(acc, red, nv, g.cp, g.part + (int64_t)g.cp * g.PM + b, (int64_t)g.cp * g.PM, g.PM);
 }
 
-// Final pass: one block per channel c; its 4 wavefronts sum each slot's
-// partials (lane l of wave w takes partials 64w + l, then every 256th), each
-// wave reduces with a butterfly over its 64 lanes and the 4 wave sums are added
-// in a fixed order (the same every run); thread 0 finishes:
-//   with a pooling layer above, row 0 of delta is
-//     z0 = f'(Y_below[0][c]) * (dY[0][c] + slot 0), written to delta[0][c];
-//   without one, z0 = delta[0][c] as stored;
-//   db[c] = slot 1 + z0,  D0[f][c] = slot 2+f + z0  (row 0 reads the ground row
-//   at every window position), for c < c_out.
+// Final pass: one workgroup per channel (ground_final_block).
 template <typename T, int AC>
-__global__ void __launch_bounds__(256) k_ground_final(GroundArgs g) {
-  __shared__ float wsum[4][2 + AC];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int c = blockIdx.x;
-  const bool pool = g.B1 > 0;
-  float tot[2 + AC];
-#pragma unroll
-  for (int k = 0; k < 2 + AC; ++k) tot[k] = 0.f;
-  const float* pc = g.part + (int64_t)c * g.PM;
-  const int64_t slot = (int64_t)g.cp * g.PM;
-  const int npm = max(g.B1, g.B2);
-#pragma unroll 2
-  for (int p = threadIdx.x; p < npm; p += 256) {
-    if (p < g.B1) tot[0] += pc[p];
-    if (p < g.B2) {
-#pragma unroll
-      for (int k = 1; k < 2 + AC; ++k) tot[k] += pc[k * slot + p];
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < 2 + AC; ++k) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) tot[k] += __shfl_xor(tot[k], off);
-    if (lane == 0) wsum[w][k] = tot[k];
-  }
-  __syncthreads();
-  if (threadIdx.x != 0) return;
-#pragma unroll
-  for (int k = 0; k < 2 + AC; ++k) tot[k] = ((wsum[0][k] + wsum[1][k]) + wsum[2][k]) + wsum[3][k];
-  T* dZ = (T*)g.dZ;
-  float z0;
-  if (pool) {
-    const T g0 = Elem<T>::from_f32((tot[0] + Elem<T>::to_f32(((const T*)g.dY)[c])) *
-                                   act_factor(Elem<T>::to_f32(((const T*)g.Y_below)[c]), g.slope));
-    dZ[c] = g0;
-    z0 = Elem<T>::to_f32(g0);
-  } else {
-    z0 = Elem<T>::to_f32(dZ[c]);
-  }
-  if (c >= g.c_out) return;
-  g.db[c] = tot[1] + z0;
-#pragma unroll
-  for (int k = 0; k < AC; ++k) g.D0[(int64_t)k * g.c_out + c] = tot[2 + k] + z0;
+__global__ void __launch_bounds__(256) k_ground_final(GroundArgs g, ExtraTask x) {
+  if (run_extra<T>(x)) return;
+  ground_final_block<T, AC>(g, blockIdx.x);
 }
+
+// An extra task as its own launch.
+template <typename T>
+__global__ void __launch_bounds__(256) k_extra(ExtraTask x) { run_extra<T>(x); }
 
 static int grid_for(int64_t items) { return (int)std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 4096)); }
 
@@ -342,19 +301,34 @@ hipError_t launch_pool_fwd(bool bf16, const void* X_in, int32_t stride_in, const
 }
 
 // kind 0: sums over delta rows (and pooling rows), then the final pass;
-// kind 1: the fused pooling backward (B1 == B2 blocks), then the final pass;
-// kind 2: the final pass alone (partials already written).
+// kind 1: the fused pooling backward (B1 == B2 blocks);
+// kind 2: the final pass alone (partials already written);
+// kind 3: the sums alone.  The extra task rides on the first kernel of the call.
 template <typename T, int AC>
-static void launch_ground_t(const GroundArgs& g, int kind, hipStream_t st) {
-  if (kind == 0) hipLaunchKernelGGL((k_ground_sums<T, AC>), dim3(g.B1 + g.B2), dim3(256), 0, st, g);
-  if (kind == 1) hipLaunchKernelGGL((k_pool_bwd<T, AC>), dim3(g.B2), dim3(256), 0, st, g);
-  if (kind != 1) hipLaunchKernelGGL((k_ground_final<T, AC>), dim3(g.cp), dim3(256), 0, st, g);
+static void launch_ground_t(const GroundArgs& g, int kind, hipStream_t st, const ExtraTask& x) {
+  const ExtraTask none{};
+  const int xb = x.kind ? x.blocks : 0;
+  if (kind == 0 || kind == 3)
+    hipLaunchKernelGGL((k_ground_sums<T, AC>), dim3(g.B1 + g.B2 + xb), dim3(256), 0, st, g, x);
+  if (kind == 1) hipLaunchKernelGGL((k_pool_bwd<T, AC>), dim3(g.B2 + xb), dim3(256), 0, st, g, x);
+  if (kind == 0 || kind == 2)
+    hipLaunchKernelGGL((k_ground_final<T, AC>), dim3(g.cp + (kind == 2 ? xb : 0)), dim3(256), 0, st, g,
+                       kind == 2 ? x : none);
 }
 
-hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, hipStream_t st) {
+static bool extra_ok(const ExtraTask& x) {
+  if (x.kind == 0) return true;
+  if (x.blocks < 1 || (x.kind != 1 && x.kind != 2)) return false;
+  return x.kind == 2 || x.AC == 0 || x.AC == 1 || x.AC == 4 || x.AC == 9;
+}
+
+hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, hipStream_t st,
+                         const ExtraTask* extra) {
   if (g.B2 < 1 || g.B1 < 0 || g.B1 > g.PM || g.B2 > g.PM) return hipErrorInvalidValue;
   if (kind == 1 && g.B1 != g.B2) return hipErrorInvalidValue;
-#define SSCN_GROUND(T, A) launch_ground_t<T, A>(g, kind, st)
+  const ExtraTask x = extra ? *extra : ExtraTask{};
+  if (!extra_ok(x)) return hipErrorInvalidValue;
+#define SSCN_GROUND(T, A) launch_ground_t<T, A>(g, kind, st, x)
   if (bf16) {
     switch (AC) {
       case 0: SSCN_GROUND(__bf16, 0); break;
@@ -373,6 +347,16 @@ hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, h
     }
   }
 #undef SSCN_GROUND
+  return hipGetLastError();
+}
+
+hipError_t launch_extra(bool bf16, const ExtraTask& x, hipStream_t st) {
+  if (x.kind == 0) return hipSuccess;
+  if (!extra_ok(x)) return hipErrorInvalidValue;
+  if (bf16)
+    hipLaunchKernelGGL(k_extra<__bf16>, dim3(x.blocks), dim3(256), 0, st, x);
+  else
+    hipLaunchKernelGGL(k_extra<float>, dim3(x.blocks), dim3(256), 0, st, x);
   return hipGetLastError();
 }
 
