@@ -800,12 +800,10 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   net->drop_on = train && net->n_rates > 0;
   net->backwarded = false;
   const LayerPlan& L0 = net->L[0];
-  if (timed(net, SSCN_KC_HEAD, st, [&] {
-        return launch_scatter_input(net->bf16, d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, st);
-      }) != hipSuccess)
-    return SSCN_ERR_HIP;
+  // the weight packings, with the input scatter as extra workgroups of the launch
   PackArgs pa;
   std::memset(&pa, 0, sizeof(pa));
+  pa.sc = ScatterArgs{d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, 0};
   for (int p = 0; p < net->nparams; ++p) {
     const ParamPlan& P = net->P[p];
     pa.job[pa.njobs++] = PackJob{h_W[p], P.WpF, 0, P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.NpadF, P.KpadF};

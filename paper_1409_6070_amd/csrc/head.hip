@@ -6,12 +6,13 @@
 
 namespace sscn {
 
-// X0[perm[i]][c] = feats[i][c] (zero padding columns); row 0 = 0, the input ground state.
+// X0[perm[i]][c] = feats[i][c] (zero padding columns); row 0 = 0, the input
+// ground state.  Workgroup b of nb.
 template <typename T>
-__global__ void __launch_bounds__(256) k_scatter_input(const T* __restrict__ feats, int32_t n, int32_t c_in,
-                                                       const int32_t* __restrict__ perm, T* X0, int32_t cp0) {
+__device__ inline void scatter_input_part(const T* __restrict__ feats, int32_t n, int32_t c_in,
+                                          const int32_t* __restrict__ perm, T* X0, int32_t cp0, int b, int nb) {
   const int64_t total = (int64_t)(n + 1) * cp0;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (int64_t)gridDim.x * blockDim.x) {
+  for (int64_t t = (int64_t)b * blockDim.x + threadIdx.x; t < total; t += (int64_t)nb * blockDim.x) {
     const int64_t i = t / cp0;
     const int c = (int)(t - i * cp0);
     if (i == n) {  // the ground row
@@ -22,6 +23,12 @@ __global__ void __launch_bounds__(256) k_scatter_input(const T* __restrict__ fea
     if (r < 1) continue;  // rejected site
     X0[(int64_t)r * cp0 + c] = (c < c_in) ? feats[i * c_in + c] : Elem<T>::from_f32(0.f);
   }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) k_scatter_input(const T* __restrict__ feats, int32_t n, int32_t c_in,
+                                                       const int32_t* __restrict__ perm, T* X0, int32_t cp0) {
+  scatter_input_part<T>(feats, n, c_in, perm, X0, cp0, blockIdx.x, gridDim.x);
 }
 
 template <typename T>
@@ -50,7 +57,13 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
   __shared__ T tile[PACK_K][PACK_N + 2];
   const T zero = Elem<T>::from_f32(0.f);
-  for (int g = blockIdx.x; g < pa.tile_beg[pa.njobs]; g += gridDim.x) {
+  const int own = (int)gridDim.x - pa.sc.blocks;
+  if ((int)blockIdx.x >= own) {  // the input scatter's workgroups
+    scatter_input_part<T>((const T*)pa.sc.feats, pa.sc.n, pa.sc.c_in, pa.sc.perm, (T*)pa.sc.X0, pa.sc.cp0,
+                          (int)blockIdx.x - own, pa.sc.blocks);
+    return;
+  }
+  for (int g = blockIdx.x; g < pa.tile_beg[pa.njobs]; g += own) {
     int ji = 0;
     while (ji + 1 < pa.njobs && g >= pa.tile_beg[ji + 1]) ++ji;
     const PackJob& j = pa.job[ji];
@@ -240,7 +253,9 @@ hipError_t launch_pack_all(bool bf16, const PackArgs& in, hipStream_t st) {
   if (pa.njobs <= 0 || total <= 0) return hipSuccess;
   if (total >= (1ll << 31)) return hipErrorInvalidValue;
   pa.tile_beg[pa.njobs] = (int32_t)total;
-  const int grid = (int)std::min<int64_t>(total, 16384);  // one tile per workgroup up to this many
+  if (pa.sc.X0) pa.sc.blocks = grid_for((int64_t)(pa.sc.n + 1) * pa.sc.cp0);
+  else pa.sc.blocks = 0;
+  const int grid = (int)std::min<int64_t>(total, 16384) + pa.sc.blocks;  // one tile per workgroup up to 16384
   if (bf16)
     hipLaunchKernelGGL(k_pack_all<__bf16>, dim3(grid), dim3(256), 0, st, pa);
   else

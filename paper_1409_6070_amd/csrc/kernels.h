@@ -239,11 +239,24 @@ struct PackJob {
   void* Bt;
   int32_t mode, A, c_in, c_out, cp_in, cp_out, Npad, Kpad;
 };
+// The input scatter (rows of X0 from the caller's feature rows), run as extra
+// workgroups of the packing launch: X0[perm[i]] = feats[i], row 0 = 0.
+struct ScatterArgs {
+  const void* feats;
+  int32_t n, c_in;
+  const int32_t* perm;
+  void* X0;
+  int32_t cp0;
+  int32_t blocks;  // workgroups given to it (0: no scatter)
+};
 struct PackArgs {
   int32_t njobs;
   int32_t tile_beg[2 * MAX_LAYERS + 1];  // first tile of each job in the flat tile range (set by the launcher)
   PackJob job[2 * MAX_LAYERS];
+  ScatterArgs sc;
 };
+// All packings of a step (and, with sc.feats or sc.n == 0 and sc.X0 set, the
+// input scatter) in one launch.
 hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st);
 // counter: a zero int32 in device memory; the last workgroup sums the loss terms
 // and sets it back to zero
