@@ -888,21 +888,34 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   g.rows_host = net->batch;
   g.row_begin = 0;
   set_plan(g, P.pd, P.rows_d, net->gpart);
+  g.partials_only = g.ksplit > 1;  // the head backward sums the split-K partials itself
   if (timed_gemm(net, g, net->batch, st) != hipSuccess)
     return SSCN_ERR_HIP;
-  if (timed(net, SSCN_KC_HEAD, st, [&] {
-        return launch_head_scatter(net->bf16, net->dh, Lt.Cp, net->head_rows, net->batch, Lt.X, Lt.grad, Lt.Cp,
-                                   net->slope, head_drop(net), st);
-      }) != hipSuccess)
-    return SSCN_ERR_HIP;
+  // the head backward (scatter of dh into the top layer, with its ground sums)
+  // runs in the stage loop below as the top convolution's sums launch
+  HeadBwdArgs hb{};
+  hb.dh_part = g.ksplit > 1 ? net->gpart : net->dh;
+  hb.ksplit = g.ksplit;
+  hb.ks_stride = (int64_t)g.part_rows * g.Npad;
+  hb.dh_stride = g.ksplit > 1 ? g.Npad : Lt.Cp;
+  hb.head_rows = net->head_rows;
+  hb.batch = net->batch;
+  hb.Y_top = Lt.X;
+  hb.grad_top = Lt.grad;
+  hb.cp = Lt.Cp;
+  hb.slope = net->slope;
+  hb.drop = head_drop(net);
+  hb.R = Lt.rules;
+  hb.part = net->ppart;
+  hb.PM = net->pool_parts;
   // Stages from the top down, all on the caller's stream.  Per convolution:
   // its bias and ground-row sums (with a pooling layer above they come out of
   // that layer's backward), rows >= 1 of the gradient below, the final ground
   // pass (row 0 of delta, db, D0) and row 0 of the gradient below.  The final
   // pass needs only the sums and rides as extra workgroups on the input-gradient
   // GEMM, which reads delta rows >= 1 only (a 1x1 layer's GEMM reads row 0 too:
-  // it rides there only when row 0 is not rewritten, i.e. without a pooling
-  // layer above); row 0 below needs D0 and rides on the next launch.
+  // it rides there only when the pass does not rewrite row 0); row 0 below needs
+  // D0 and rides on the next launch.
   ExtraTask pending{};  // row 0 of a gradient below, waiting for the next launch
   for (int s = top; s >= 1; --s) {
     const LayerPlan& L = net->L[s];
@@ -913,8 +926,14 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
     } else {
       const bool pool_above = s < top && net->L[s + 1].kind == 2;
       const bool row0 = needs_row0(net, s) && L.A > 1;
-      const ExtraTask fin = final_task(net, s, pool_above);
-      if (!pool_above) {  // the sums over delta rows, as their own launch
+      ExtraTask fin = final_task(net, s, pool_above);
+      if (s == top) {  // the head backward writes delta and its sums
+        fin.g.B1 = fin.g.B2 = head_backward_parts(net->batch);
+        fin.g.dY = L.grad;  // row 0 zeroed by the head backward
+        fin.g.Y_below = L.X;
+        if (pending.kind) return SSCN_ERR_HIP;  // nothing precedes the top layer
+        e = timed(net, SSCN_KC_HEAD, st, [&] { return launch_head_backward(net->bf16, hb, fin.AC, st); });
+      } else if (!pool_above) {  // the sums over delta rows, as their own launch
         const GroundArgs g = ground_args(net, s, false);
         e = timed(net, SSCN_KC_GROUND, st, [&] {
           return launch_ground(net->bf16, g, fin.AC, 3, st, pending.kind ? &pending : nullptr);
@@ -922,10 +941,13 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
         pending = ExtraTask{};
       }
       const bool gemm_below = s > 1 || net->want_dfeats;
-      if (e == hipSuccess && gemm_below && (!pool_above || L.A > 1)) {
+      // the final pass writes row 0 of delta when it finishes a pooling layer's (or
+      // the head's) sums: then only a GEMM that does not read row 0 may carry it
+      const bool writes_row0 = pool_above || s == top;
+      if (e == hipSuccess && gemm_below && (L.A > 1 || !writes_row0)) {
         e = rows_below(net, s, st, &fin);
       } else if (e == hipSuccess) {
-        const GroundArgs g = ground_args(net, s, pool_above);
+        const GroundArgs g = fin.g;
         e = timed(net, SSCN_KC_GROUND, st, [&] {
           return launch_ground(net->bf16, g, fin.AC, 2, st, pending.kind ? &pending : nullptr);
         });

@@ -543,10 +543,10 @@ static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   const bool timed = a.t_start || a.t_stop;
   if (timed)
     hipExtLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a.t_start,
-                          a.ksplit > 1 ? nullptr : a.t_stop, 0, a);
+                          a.ksplit > 1 && !a.partials_only ? nullptr : a.t_stop, 0, a);
   else
     hipLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a);
-  if (a.ksplit > 1) {
+  if (a.ksplit > 1 && !a.partials_only) {
     const int64_t total = span * ((a.out_cols + 3) / 4);
     const int g2 = (int)std::min<int64_t>(std::max<int64_t>((total + 255) / 256, 1), 4096);
     if (timed)

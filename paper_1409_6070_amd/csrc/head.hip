@@ -2,6 +2,7 @@
 // softmax on the output layer) with its cross-entropy loss.
 
 #include "common.h"
+#include "ground_tasks.h"
 #include "kernels.h"
 
 namespace sscn {
@@ -175,30 +176,61 @@ __global__ void __launch_bounds__(256) k_softmax_xent(const float* __restrict__ 
 
 __global__ void k_loss_zero(float* loss) { *loss = 0.f; }
 
-// grad_top[row(b)] = mask * dh[b] for non-empty samples (blockIdx.y = b < batch);
-// grad_top[0] = mask0 * sum of dh over empty samples (blockIdx.y = batch).
-template <typename T>
-__global__ void __launch_bounds__(256) k_head_scatter(const float* __restrict__ dh, int32_t dh_stride,
-                                                      const int32_t* __restrict__ head_rows, int32_t batch,
-                                                      const T* __restrict__ Y_top, T* grad_top, int32_t cp,
-                                                      float slope, DropArgs drop) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= cp) return;
-  const int b = blockIdx.y;
-  if (b < batch) {
-    const int r = head_rows[b];
-    if (r == 0) return;
-    float f = act_factor(Elem<T>::to_f32(Y_top[(int64_t)r * cp + c]), slope);
-    if (drop.on) f *= drop_factor(drop, (uint32_t)b, c);
-    grad_top[(int64_t)r * cp + c] = Elem<T>::from_f32(dh[(int64_t)b * dh_stride + c] * f);
-    return;
+// Workgroup (x, p): 64 channels, samples 8p .. 8p+7; thread (channel c,
+// sample lane l) takes samples 8p + l and 8p + l + 4; the four lanes are
+// combined in LDS in a fixed order into partial p of each slot:
+//   slot 0: sum of dh over empty samples (their top feature is the ground row),
+//   slot 1: sum of the written delta rows (bias), slot 2+f: those whose window
+//   position f reads the ground row.
+// Row 0 of grad_top is set to zero (workgroups with p = 0): the final ground
+// pass then finishes it as f'(Y_top[0]) * (0 + slot 0), the form it uses below
+// a pooling layer.
+template <typename T, int AC>
+__global__ void __launch_bounds__(256) k_head_backward(HeadBwdArgs h, ExtraTask x) {
+  if (run_extra<T>(x)) return;
+  constexpr int J = 2 + AC;
+  __shared__ float red[4][J][64];
+  const int cl = threadIdx.x & 63, sl = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + cl;
+  const int p = blockIdx.y;
+  const T* Y = (const T*)h.Y_top;
+  T* G = (T*)h.grad_top;
+  float acc[J];
+#pragma unroll
+  for (int k = 0; k < J; ++k) acc[k] = 0.f;
+  if (c < h.cp) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int b = p * 8 + sl + 4 * q;
+      if (b >= h.batch) break;
+      float g = 0.f;
+      for (int ks = 0; ks < h.ksplit; ++ks) g += h.dh_part[ks * h.ks_stride + (int64_t)b * h.dh_stride + c];
+      if (h.drop.on) g *= drop_factor(h.drop, (uint32_t)b, c);
+      const int r = h.head_rows[b];
+      if (r == 0) {
+        acc[0] += g;
+        continue;
+      }
+      const T v = Elem<T>::from_f32(g * act_factor(Elem<T>::to_f32(Y[(int64_t)r * h.cp + c]), h.slope));
+      G[(int64_t)r * h.cp + c] = v;
+      const float d = Elem<T>::to_f32(v);
+      acc[1] += d;
+#pragma unroll
+      for (int f = 0; f < AC; ++f) acc[2 + f] += h.R[(int64_t)r * AC + f] == 0 ? d : 0.f;
+    }
   }
-  float g0 = 0.f;
-  for (int bb = 0; bb < batch; ++bb)
-    if (head_rows[bb] == 0)
-      g0 += dh[(int64_t)bb * dh_stride + c] * (drop.on ? drop_factor(drop, (uint32_t)bb, c) : 1.f);
-  grad_top[c] = Elem<T>::from_f32(g0 * act_factor(Elem<T>::to_f32(Y_top[c]), slope));
+#pragma unroll
+  for (int k = 0; k < J; ++k) red[sl][k][cl] = acc[k];
+  __syncthreads();
+  if (sl != 0 || c >= h.cp) return;
+  if (p == 0) G[c] = Elem<T>::from_f32(0.f);
+#pragma unroll
+  for (int k = 0; k < J; ++k)
+    h.part[((int64_t)k * h.cp + c) * h.PM + p] = ((red[0][k][cl] + red[1][k][cl]) + red[2][k][cl]) + red[3][k][cl];
 }
+
+// Partials (sample chunks of 8) of the head backward.
+int head_backward_parts(int32_t batch) { return std::max(1, (batch + 7) / 8); }
 
 __global__ void __launch_bounds__(256) k_fill_zero(uint32_t* p, int64_t words) {
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < words; t += (int64_t)gridDim.x * blockDim.x)
@@ -279,16 +311,31 @@ hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* la
   return hipGetLastError();
 }
 
-hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
-                               int32_t batch, const void* Y_top, void* grad_top, int32_t cp, float slope,
-                               const DropArgs& drop, hipStream_t st) {
-  dim3 grid((cp + 255) / 256, batch + 1);
-  if (bf16)
-    hipLaunchKernelGGL(k_head_scatter<__bf16>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
-                       (const __bf16*)Y_top, (__bf16*)grad_top, cp, slope, drop);
-  else
-    hipLaunchKernelGGL(k_head_scatter<float>, grid, dim3(256), 0, st, dh, dh_stride, head_rows, batch,
-                       (const float*)Y_top, (float*)grad_top, cp, slope, drop);
+hipError_t launch_head_backward(bool bf16, const HeadBwdArgs& h, int32_t AC, hipStream_t st, const ExtraTask* extra) {
+  const ExtraTask x = extra ? *extra : ExtraTask{};
+  if (x.kind) return hipErrorInvalidValue;  // a 2-D grid: no extra workgroups
+  const int P = head_backward_parts(h.batch);
+  if (P > h.PM) return hipErrorInvalidValue;
+  const dim3 grid((h.cp + 63) / 64, P);
+#define SSCN_HEAD(T, A) hipLaunchKernelGGL((k_head_backward<T, A>), grid, dim3(256), 0, st, h, x)
+  if (bf16) {
+    switch (AC) {
+      case 0: SSCN_HEAD(__bf16, 0); break;
+      case 1: SSCN_HEAD(__bf16, 1); break;
+      case 4: SSCN_HEAD(__bf16, 4); break;
+      case 9: SSCN_HEAD(__bf16, 9); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (AC) {
+      case 0: SSCN_HEAD(float, 0); break;
+      case 1: SSCN_HEAD(float, 1); break;
+      case 4: SSCN_HEAD(float, 4); break;
+      case 9: SSCN_HEAD(float, 9); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
+#undef SSCN_HEAD
   return hipGetLastError();
 }
 

@@ -121,6 +121,7 @@ struct GemmArgs {
   // (the GEMM, or its split-K reduce) ends
   hipEvent_t t_start, t_stop;
   ExtraTask x;  // extra workgroups appended to the launch (kind 0: none)
+  int32_t partials_only;  // ksplit > 1: leave the fp32 partials, no reduce launch
 };
 
 // Tile shape and padding of one GEMM, chosen on the host from its row bound.
@@ -263,10 +264,7 @@ hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st);
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
                                void* dlogits, int32_t dl_stride, float* loss_part, float* loss, int32_t* counter,
                                hipStream_t st);
-// drop: the softmax layer input's dropout (row key = sample), or off
-hipError_t launch_head_scatter(bool bf16, const float* dh, int32_t dh_stride, const int32_t* head_rows,
-                               int32_t batch, const void* Y_top, void* grad_top, int32_t cp, float slope,
-                               const DropArgs& drop, hipStream_t st);
+
 
 // dropout.hip: Xd = X with rows 1 .. *n_rows dropped (row 0 copied; X == Xd:
 // in place, row 0 untouched); the softmax layer's input hd[b] =
@@ -276,6 +274,34 @@ hipError_t launch_dropout_rows(bool bf16, const void* X, void* Xd, int32_t cp, c
 hipError_t launch_head_drop(bool bf16, const void* X_top, const int32_t* head_rows, int32_t batch, int32_t cp,
                             void* hd, const DropArgs& d, hipStream_t st);
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t st);
+
+// Backward of the softmax layer's input, fused with the top convolution's
+// bias / ground-row sums: dh[b] = sum over splits of dh_part (the softmax-layer
+// input-gradient GEMM's split-K partials, or dh itself with ksplit 1), times the
+// dropout factor; the top layer's row of sample b gets dh[b] * f'(Y_top); the
+// partial sums (head_backward_parts(batch) partials per slot) hold slot 0, the
+// sum over empty samples, and slots 1, 2+f as in launch_ground; row 0 of
+// grad_top is zeroed so that the final ground pass, run with B1 = B2 = parts,
+// dY = Y_below = the top layer, finishes row 0 as below a pooling layer.
+struct HeadBwdArgs {
+  const float* dh_part;
+  int32_t ksplit;
+  int64_t ks_stride;  // floats between splits
+  int32_t dh_stride;  // floats between samples
+  const int32_t* head_rows;
+  int32_t batch;
+  const void* Y_top;
+  void* grad_top;
+  int32_t cp;
+  float slope;
+  DropArgs drop;
+  const int32_t* R;  // the top convolution's window list [rows][AC]
+  float* part;       // [(2 + AC) * cp * PM]
+  int32_t PM;
+};
+int head_backward_parts(int32_t batch);
+hipError_t launch_head_backward(bool bf16, const HeadBwdArgs& h, int32_t AC, hipStream_t st,
+                                const ExtraTask* extra = nullptr);
 
 // encode.hip: pen paths -> sites and 9 features (Section 2.4)
 struct EncodeArgs {
