@@ -88,6 +88,8 @@ struct sscn_net {
   float* gpart;  // split-K partials of the gather GEMMs
   float* D0;
   float* ppart;
+  size_t ppart_half;  // floats per convolution-parity half of ppart
+  size_t d0_half;     // and of D0
   void* hdrop;  // the softmax layer's dropped input [batch_max][Cp_top] (dropout workspace only)
   size_t ws_bytes;
   int32_t max_words;
@@ -165,6 +167,21 @@ static hipError_t timed(sscn_net* net, int cls, hipStream_t st, F&& launch) {
   return e;
 }
 
+// Row tiles at capacity (and their height) of the input-gradient GEMM of
+// convolution s when it computes the gradient of a pooling layer s-1 on a
+// convolution, with a tile shape that can run that layer's backward in its
+// epilogue; 0 otherwise.
+static int64_t route_tiles(const sscn_net* net, int s, int* bm) {
+  if (s < 3) return 0;
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lp = net->L[s - 1];
+  if (L.kind != 1 || Lp.kind != 2 || net->L[s - 2].kind != 1 || L.A < 2) return 0;
+  const ParamPlan& P = net->P[L.conv_index];
+  if (P.pd.ksplit != 1 || !gemm_routes(net->bf16, P.pd.cfg)) return 0;
+  *bm = gemm_bm(net->bf16, P.pd.cfg);
+  return (Lp.cap + *bm - 1) / *bm;  // rows 1 .. cap
+}
+
 static void carve(sscn_net* net, void* base) {
   Carver cv(base);
   const int B = net->d.batch_max;
@@ -222,8 +239,20 @@ static void carve(sscn_net* net, void* base) {
   net->loss_part = (float*)cv.take((size_t)B * 4);
   net->wpart = (float*)cv.take(std::max<size_t>(max_part, 1) * 4);
   net->gpart = (float*)cv.take(std::max<size_t>(max_gpart, 1) * 4);
-  net->D0 = (float*)cv.take(max_d0 * 4);
-  net->ppart = (float*)cv.take((size_t)net->pool_parts * (2 + 9) * max_cp * 4);
+  // two of each, by convolution parity: a launch may finish one convolution's
+  // sums while it writes the next one's partials, or read the D0 of the
+  // convolution above a pooling layer while it writes the one below
+  net->d0_half = (max_d0 + 63) / 64 * 64;
+  net->D0 = (float*)cv.take(2 * net->d0_half * 4);
+  // (a pooling backward run in a GEMM epilogue keeps one partial per row tile:
+  // up to 2 + 4 slots, cp channels, its row tiles at capacity)
+  net->ppart_half = (size_t)net->pool_parts * (2 + 9) * max_cp;
+  for (int s = 3; s < net->nlayers; ++s) {
+    int bm = 0;
+    const int64_t t = route_tiles(net, s, &bm);
+    if (t > 0) net->ppart_half = std::max(net->ppart_half, (size_t)(2 + 4) * net->L[s - 2].Cp * (size_t)t);
+  }
+  net->ppart = (float*)cv.take(2 * net->ppart_half * 4);
   net->hdrop = net->d.dropout ? cv.take((size_t)B * Lt.Cp * net->esz) : nullptr;
   net->ws_bytes = cv.off + 256;
 }
@@ -590,6 +619,14 @@ static int pool_bwd_blocks(const sscn_net* net, int64_t rows, int cp) {
   return (int)std::min<int64_t>(std::min(512, net->pool_parts), std::max<int64_t>(1, (rows + lanes - 1) / lanes));
 }
 
+// Slot partials and ground sums D0 of convolution s (alternating halves).
+static float* part_of(const sscn_net* net, int s) {
+  return net->ppart + (size_t)(net->L[s].conv_index & 1) * net->ppart_half;
+}
+static float* d0_of(const sscn_net* net, int s) {
+  return net->D0 + (size_t)(net->L[s].conv_index & 1) * net->d0_half;
+}
+
 // Whether the backward pass needs row 0 of the gradient below convolution s
 // (the ground row of its input): always above the first layer; for the first,
 // only when the caller asks for the input-feature gradient, which its
@@ -620,11 +657,11 @@ static GroundArgs ground_args(const sscn_net* net, int s, bool pool_above) {
   g.stride = L.Cp;
   g.cp = L.Cp;
   g.c_out = L.C;
-  g.part = net->ppart;
+  g.part = part_of(net, s);
   g.PM = net->pool_parts;
   g.slope = net->slope;
   g.db = net->db[ci];
-  g.D0 = net->D0;
+  g.D0 = d0_of(net, s);
   return g;
 }
 
@@ -648,7 +685,7 @@ static hipError_t ground_level(sscn_net* net, int s, bool pool_above, hipStream_
   // below a convolution the stored gradient is dL/dZ: times its rectifier derivative
   const void* mask = Lb.kind == 1 ? Lb.X : nullptr;
   return timed(net, SSCN_KC_GROUND, st, [&] {
-    return launch_row0_dx(net->bf16, net->W[ci], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, mask, net->slope,
+    return launch_row0_dx(net->bf16, net->W[ci], d0_of(net, s), P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad, mask, net->slope,
                           st);
   });
 }
@@ -673,7 +710,7 @@ static ExtraTask row0_task(const sscn_net* net, int s) {
   ExtraTask x{};
   x.kind = 2;
   x.blocks = Lb.Cp;
-  x.r = Row0Args{net->W[L.conv_index], net->D0, P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad,
+  x.r = Row0Args{net->W[L.conv_index], d0_of(net, s), P.A, P.c_in, P.c_out, Lb.Cp, Lb.grad,
                  Lb.kind == 1 ? Lb.X : nullptr, net->slope};
   return x;
 }
@@ -725,11 +762,35 @@ static hipError_t run_wgrads(sscn_net* net, const WGradArgs* w, int n, hipStream
   return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] { return launch_wgrad_reduce(net->bf16, w, n, st); });
 }
 
+// Whether the input-gradient GEMM of convolution s, when it computes the
+// gradient of a pooling layer s-1 on convolution s-2, runs that pooling
+// layer's backward in its epilogue (GemmArgs::route): not through a dropout of
+// the pooling output, not for a 3x3 convolution below that must finish its
+// nine ground sums, and only for a tile shape that stages its output with one
+// partial per row tile (*bm rows, *tiles at capacity).
+static bool route_into(const sscn_net* net, int s, int* ac, int* bm, int* tiles) {
+  int b = 0;
+  const int64_t t = route_tiles(net, s, &b);
+  if (t < 1 || !needs_row0(net, s) || conv_drop(net, s).on) return false;
+  const LayerPlan& Lc = net->L[s - 2];
+  const int a = (needs_row0(net, s - 2) && Lc.A > 1) ? Lc.A : 0;
+  if (a != 0 && a != 4) return false;
+  if ((size_t)(2 + a) * Lc.Cp * (size_t)t > net->ppart_half || t > (1 << 30)) return false;
+  *ac = a;
+  *bm = b;
+  *tiles = (int)t;
+  return true;
+}
+
 // Rows >= 1 of the gradient below stage s: the pooling backward (with the
 // partial sums of the convolution below), or the input-gradient GEMM of a
 // convolution.  (The GEMM reads delta rows >= 1 only: a window list entry of -1
-// selects zero, whatever its load of row 0 returned.)
-static hipError_t rows_below(sscn_net* net, int s, hipStream_t st, const ExtraTask* extra = nullptr) {
+// selects zero, whatever its load of row 0 returned.)  With allow_route the
+// GEMM also runs the pooling backward below it where route_into allows, and
+// *routed says whether it did.
+static hipError_t rows_below(sscn_net* net, int s, hipStream_t st, const ExtraTask* extra = nullptr,
+                             bool allow_route = false, bool* routed = nullptr) {
+  if (routed) *routed = false;
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
   if (L.kind == 2) {
@@ -772,6 +833,14 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st, const ExtraTa
     g.row_begin = 0;
   }
   set_plan(g, P.pd, P.rows_d, net->gpart);
+  int rac = 0, rbm = 0, rtiles = 0;
+  if (allow_route && route_into(net, s, &rac, &rbm, &rtiles)) {
+    g.route = 1;
+    g.route_ac = rac;
+    g.pr = ground_args(net, s - 2, true);
+    g.pr.PM = rtiles;  // one partial per row tile
+    if (routed) *routed = true;
+  }
   hipError_t e = timed_gemm(net, g, Lb.cap + 1, st);
   const DropArgs dr = conv_drop(net, s);
   if (e == hipSuccess && dr.on)  // through the dropout of this convolution's input: rows >= 1, in place
@@ -906,7 +975,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   hb.slope = net->slope;
   hb.drop = head_drop(net);
   hb.R = Lt.rules;
-  hb.part = net->ppart;
+  hb.part = part_of(net, top);
   hb.PM = net->pool_parts;
   // Stages from the top down, all on the caller's stream.  Per convolution:
   // its bias and ground-row sums (with a pooling layer above they come out of
@@ -916,17 +985,39 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   // GEMM, which reads delta rows >= 1 only (a 1x1 layer's GEMM reads row 0 too:
   // it rides there only when the pass does not rewrite row 0); row 0 below needs
   // D0 and rides on the next launch.
+  //
+  // A pooling layer's backward runs in the epilogue of the GEMM that computes
+  // its gradient where route_into allows: its row 0 (row 0 below the
+  // convolution above) then cannot ride on the next launch, whose final pass
+  // reads it, and is computed by that final pass itself (extra task kind 3).
   ExtraTask pending{};  // row 0 of a gradient below, waiting for the next launch
+  ExtraTask pool_row0{};  // row 0 of a routed pooling layer's gradient, for the final pass below it
+  bool routed[MAX_LAYERS] = {};
   for (int s = top; s >= 1; --s) {
     const LayerPlan& L = net->L[s];
     hipError_t e = hipSuccess;
     if (L.kind == 2) {
+      if (routed[s]) {
+        pool_row0 = pending;
+        pending = ExtraTask{};
+        if (pool_row0.kind != 2) return SSCN_ERR_HIP;
+        continue;
+      }
       e = rows_below(net, s, st, pending.kind ? &pending : nullptr);
       pending = ExtraTask{};
     } else {
       const bool pool_above = s < top && net->L[s + 1].kind == 2;
       const bool row0 = needs_row0(net, s) && L.A > 1;
       ExtraTask fin = final_task(net, s, pool_above);
+      if (pool_above && routed[s + 1]) {  // partials from the routed GEMM above, its row 0 computed here
+        int rac = 0, rbm = 0, rtiles = 0;
+        if (!route_into(net, s + 2, &rac, &rbm, &rtiles) || pool_row0.kind != 2) return SSCN_ERR_HIP;
+        fin.g.B1 = fin.g.B2 = fin.g.PM = rtiles;
+        fin.g.route_bm = rbm;
+        fin.kind = 3;
+        fin.r = pool_row0.r;
+        pool_row0 = ExtraTask{};
+      }
       if (s == top) {  // the head backward writes delta and its sums
         fin.g.B1 = fin.g.B2 = head_backward_parts(net->batch);
         fin.g.dY = L.grad;  // row 0 zeroed by the head backward
@@ -945,14 +1036,20 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
       // the head's) sums: then only a GEMM that does not read row 0 may carry it
       const bool writes_row0 = pool_above || s == top;
       if (e == hipSuccess && gemm_below && (L.A > 1 || !writes_row0)) {
-        e = rows_below(net, s, st, &fin);
+        e = rows_below(net, s, st, &fin, true, s >= 2 ? &routed[s - 1] : nullptr);
       } else if (e == hipSuccess) {
-        const GroundArgs g = fin.g;
-        e = timed(net, SSCN_KC_GROUND, st, [&] {
-          return launch_ground(net->bf16, g, fin.AC, 2, st, pending.kind ? &pending : nullptr);
-        });
+        if (fin.kind == 3) {  // the final pass with its row 0 above, as a launch of its own
+          if (pending.kind)
+            e = timed(net, SSCN_KC_GROUND, st, [&] { return launch_extra(net->bf16, pending, st); });
+          if (e == hipSuccess) e = timed(net, SSCN_KC_GROUND, st, [&] { return launch_extra(net->bf16, fin, st); });
+        } else {
+          const GroundArgs g = fin.g;
+          e = timed(net, SSCN_KC_GROUND, st, [&] {
+            return launch_ground(net->bf16, g, fin.AC, 2, st, pending.kind ? &pending : nullptr);
+          });
+        }
         pending = ExtraTask{};
-        if (e == hipSuccess && gemm_below) e = rows_below(net, s, st);
+        if (e == hipSuccess && gemm_below) e = rows_below(net, s, st, nullptr, true, s >= 2 ? &routed[s - 1] : nullptr);
       }
       if (row0) pending = row0_task(net, s);
     }

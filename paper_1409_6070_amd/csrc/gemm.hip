@@ -18,6 +18,7 @@
 
 #include "common.h"
 #include "epilogue.h"
+#include "pool_route.h"
 #include "ground_tasks.h"
 #include "kernels.h"
 
@@ -78,6 +79,23 @@ template <typename T> using C128x64 = GCfg<T, 4, 1, 2, 4>;
 template <typename T> using C64x64 = GCfg<T, 2, 2, 2, 2>;
 template <typename T> using C32x64 = GCfg<T, 2, 2, 1, 2>;
 
+template <class C>
+constexpr bool stages_tile() {
+  return C::BM * (C::BN + C::VE) <= (C::BM + C::BN) * C::LDK;
+}
+
+bool gemm_routes(bool bf16, int cfg) {
+  if (cfg == GEMM_DIRECT) return bf16;
+  switch (cfg) {
+    case 0: return bf16 ? stages_tile<C128x128<__bf16>>() : stages_tile<C128x128<float>>();
+    case 1: return bf16 ? stages_tile<C128x64<__bf16>>() : stages_tile<C128x64<float>>();
+    case 2: return bf16 ? stages_tile<C64x64<__bf16>>() : stages_tile<C64x64<float>>();
+    default: return bf16 ? stages_tile<C32x64<__bf16>>() : stages_tile<C32x64<float>>();
+  }
+}
+
+int gemm_bm(bool bf16, int cfg) { return cfg == GEMM_DIRECT ? DIRECT_BM : gemm_tile(bf16, cfg).BM; }
+
 GemmTile gemm_tile(bool bf16, int cfg) {
   const int BK = bf16 ? 64 : 32;
   switch (cfg) {
@@ -111,17 +129,53 @@ __device__ inline int div_small(int k, int d, float rcp) {
   return q;
 }
 
+// Stores of an output tile staged in LDS (Cs, pitch CS), 16 bytes at a time.
+// AC >= 0: the pooling backward of every row m >= 1 as well, and the tile's
+// slot partial sums as partial tm (lds: the staging buffer, reused).
+template <typename T, class C, int CS, int AC>
+__device__ inline void store_staged(const GemmArgs& a, const T* Cs, int m0, int n0, int tm, int rows, float* lds) {
+  constexpr int VE = C::VE, BM = C::BM, BN = C::BN, NT = C::NT, NV = BN / VE;
+  constexpr int J = AC >= 0 ? 2 + AC : 1;
+  static_assert(NT % NV == 0, "each thread keeps one channel vector");
+  float acc[J][VE];
+  if constexpr (AC >= 0) {
+#pragma unroll
+    for (int k = 0; k < J; ++k)
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[k][e] = 0.f;
+  }
+  for (int v = threadIdx.x; v < BM * NV; v += NT) {
+    const int r = v / NV, nv = v - r * NV;
+    const int m = m0 + r, n = n0 + nv * VE;
+    if (m < rows && n < a.out_cols) {
+      u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
+      if (a.epi == EPI_STORE_MASK) {  // the rectifier derivative of the layer below, 16 bytes at a time
+        const u32x4 y = *(const u32x4*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
+#pragma unroll
+        for (int e = 0; e < VE; ++e)
+          ((T*)&o)[e] = Elem<T>::from_f32(Elem<T>::to_f32(((const T*)&o)[e]) *
+                                          act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope));
+      }
+      *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
+      if constexpr (AC >= 0)
+        if (m >= 1) pool_route_item<T, AC>(a.pr, m, n, (const T*)&o, acc);
+    }
+  }
+  if constexpr (AC >= 0) tile_slot_sums<VE, J, NT, NV, (BM + BN) * C::LDK * (int)sizeof(T) / 4>(acc, lds, a.pr, n0, tm);
+}
+
 // Implicit-gather GEMM.  Per tile: the tile's window rows go to LDS once; the
 // next K slab's global loads are issued before the current slab's MFMAs
 // (register prefetch); the output tile is staged in LDS for 16-byte stores.
 // With ksplit > 1 each workgroup covers one K range and writes fp32 partial
 // sums, reduced (with the epilogue) by k_gemm_splitk_reduce.
-template <typename T, class C>
+template <typename T, class C, int RAC>
 __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   constexpr int VE = C::VE, BK = C::BK, KV = C::KV, LDK = C::LDK, BM = C::BM, BN = C::BN, NT = C::NT;
   constexpr int SMEM = (BM + BN) * LDK;
   constexpr int CS = BN + VE;  // staging pitch
-  constexpr bool STAGE = BM * CS <= SMEM;
+  constexpr bool STAGE = stages_tile<C>();
+  static_assert(STAGE == (BM * CS <= SMEM), "staging fits");
   __shared__ __attribute__((aligned(16))) T smem[SMEM];
   __shared__ int32_t Rs[BM * AMAX];
   T* As = smem;
@@ -253,21 +307,7 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
           }
         }
       __syncthreads();
-      for (int v = tid; v < BM * (BN / VE); v += NT) {
-        const int r = v / (BN / VE), nv = v - r * (BN / VE);
-        const int m = m0 + r, n = n0 + nv * VE;
-        if (m < rows && n < a.out_cols) {
-          u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
-          if (a.epi == EPI_STORE_MASK) {  // the rectifier derivative of the layer below, 16 bytes at a time
-            const u32x4 y = *(const u32x4*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
-#pragma unroll
-            for (int e = 0; e < VE; ++e)
-              ((T*)&o)[e] = Elem<T>::from_f32(Elem<T>::to_f32(((const T*)&o)[e]) *
-                                              act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope));
-          }
-          *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
-        }
-      }
+      store_staged<T, C, CS, RAC>(a, Cs, m0, n0, tm, rows, (float*)smem);
     } else {
 #pragma unroll
       for (int i = 0; i < C::TM; ++i)
@@ -541,11 +581,16 @@ static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit()) +
                    (a.x.kind ? a.x.blocks : 0);
   const bool timed = a.t_start || a.t_stop;
+  // the pooling-backward epilogue has instantiations of its own (its slot sums
+  // would otherwise cost every launch registers)
+  void (*kern)(GemmArgs) = !a.route ? k_gemm_gather<T, C, -1>
+                           : a.route_ac == 4 ? k_gemm_gather<T, C, 4>
+                                             : k_gemm_gather<T, C, 0>;
   if (timed)
-    hipExtLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a.t_start,
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), 0, st, a.t_start,
                           a.ksplit > 1 && !a.partials_only ? nullptr : a.t_stop, 0, a);
   else
-    hipLaunchKernelGGL((k_gemm_gather<T, C>), dim3(grid), dim3(C::NT), 0, st, a);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), 0, st, a);
   if (a.ksplit > 1 && !a.partials_only) {
     const int64_t total = span * ((a.out_cols + 3) / 4);
     const int g2 = (int)std::min<int64_t>(std::max<int64_t>((total + 255) / 256, 1), 4096);
@@ -568,6 +613,13 @@ static void launch_gemm_t(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
 
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   if (max_rows - a.row_begin <= 0) return hipSuccess;
+  if (a.route) {  // pooling backward in the epilogue: one partial per row tile
+    const int bm = gemm_bm(bf16, a.cfg);
+    if (a.epi != EPI_STORE || a.ksplit != 1 || !gemm_routes(bf16, a.cfg) || (a.route_ac != 0 && a.route_ac != 4) ||
+        !a.pr.part || !a.pr.Rp || !a.pr.argmax || !a.pr.dZ || !a.pr.Y_below || (a.route_ac > 0 && !a.pr.R) ||
+        a.pr.cp != a.out_cols || a.pr.stride != a.pr.cp || (max_rows - a.row_begin + bm - 1) / bm > a.pr.PM)
+      return hipErrorInvalidValue;
+  }
   if (a.cfg == GEMM_DIRECT) return bf16 ? launch_gemm_direct(a, max_rows, st) : hipErrorInvalidValue;
   if (bf16)
     launch_gemm_t<__bf16>(a, max_rows, st);

@@ -14,9 +14,12 @@
 #include "common.h"
 #include "epilogue.h"
 #include "ground_tasks.h"
+#include "pool_route.h"
 #include "kernels.h"
 
 #include <hip/hip_ext.h>
+
+#include <type_traits>
 
 namespace sscn {
 
@@ -32,7 +35,67 @@ __device__ inline int dir_div(int k, int d, float rcp) {
   return q;
 }
 
-template <int SK>
+// Epilogue in 16-byte vectors (8 columns of one row, the waves' partial sums
+// added in wave order), thread t keeping column group c8e.  AC >= 0: the
+// pooling backward of every row m >= 1 as well, and the tile's slot partial
+// sums as partial tm (through red, reused).
+struct NoPrefetch {};
+template <int AC, bool PRE>
+using PrefetchT = typename std::conditional<PRE, RouteIn<__bf16, AC < 0 ? 0 : AC>, NoPrefetch>::type;
+
+template <int SK, int RP, int AC, bool PRE>
+__device__ inline void store_vectors(const GemmArgs& a, float (*red)[DIRECT_BM][RP], const float (&bias8)[8], int c8e,
+                                     int m0, int n0, int tm, int rows, const PrefetchT<AC, PRE>& pre) {
+  typedef __bf16 T;
+  constexpr int BM = DIRECT_BM, BN = DIRECT_BN, NT = 64 * SK, NV = BN / 8;
+  constexpr int J = AC >= 0 ? 2 + AC : 1;
+  static_assert(NT % NV == 0, "each thread keeps one column group");
+  float acc[J][8];
+  if constexpr (AC >= 0) {
+#pragma unroll
+    for (int k = 0; k < J; ++k)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[k][e] = 0.f;
+  }
+  for (int v = threadIdx.x; v < BM * NV; v += NT) {
+    const int r = v / NV, c8 = c8e;
+    const int m = m0 + r, n = n0 + c8;
+    if (m >= rows || n >= a.out_cols) continue;
+    float s[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = 0.f;
+#pragma unroll
+    for (int q = 0; q < SK; ++q) {
+      const f32x4 lo = *(const f32x4*)&red[q][r][c8], hi = *(const f32x4*)&red[q][r][c8 + 4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[e] += lo[e];
+        s[4 + e] += hi[e];
+      }
+    }
+    v4u o;
+    v4u y{0u, 0u, 0u, 0u};
+    if (a.epi == EPI_STORE_MASK) y = *(const v4u*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float v8 = epi_value<T>(a, s[e], bias8[e]);
+      if (a.epi == EPI_STORE_MASK) v8 *= act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope);
+      ((T*)&o)[e] = Elem<T>::from_f32(v8);
+    }
+    *(v4u*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
+    if constexpr (AC >= 0) {
+      if (m >= 1) {
+        if constexpr (PRE)  // this thread's only row, its loads issued earlier
+          route_apply<T, AC>(a.pr, n, pre, (const T*)&o, acc);
+        else
+          pool_route_item<T, AC>(a.pr, m, n, (const T*)&o, acc);
+      }
+    }
+  }
+  if constexpr (AC >= 0) tile_slot_sums<8, J, NT, NV, SK * BM * RP>(acc, &red[0][0][0], a.pr, n0, tm);
+}
+
+template <int SK, int RAC>
 __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   typedef __bf16 T;
   constexpr int TM = DIRECT_BM / 16, TN = DIRECT_BN / 16;
@@ -69,6 +132,15 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
     float bias8[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) bias8[e] = (a.bias && n0 + c8e + e < a.N) ? a.bias[n0 + c8e + e] : 0.f;
+    // pooling backward in the epilogue with one row per thread (four waves):
+    // that row's window and argmax now, its children's rows after the K loop
+    constexpr int RA = RAC < 0 ? 0 : RAC;
+    constexpr bool PRE = RAC >= 0 && NT == BM * (BN / 8);
+    PrefetchT<RAC, PRE> pre;
+    const int pre_m = m0 + tid / (BN / 8);
+    const bool pre_on = PRE && pre_m >= 1 && pre_m < rows && n0 + c8e < a.out_cols;
+    if constexpr (PRE)
+      if (pre_on) route_load_window<T, RA>(a.pr, pre_m, n0 + c8e, pre);
     for (int e = tid; e < BM * A; e += NT) {  // the tile's window rows (-1: none)
       const int r = e / A, f = e - r * A;
       const int m = m0 + r;
@@ -119,6 +191,8 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
       }
     }
 
+    if constexpr (PRE)
+      if (pre_on) route_load_children<T, RA>(a.pr, n0 + c8e, pre);
     // partial sums of every wave to LDS (MFMA output: lane holds rows 4g..4g+3 of column r16)
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -129,35 +203,7 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
     __syncthreads();
 
     if (epi_stores_T(a.epi)) {
-      // 16-byte vectors: 8 columns of one row, summed over the waves in order
-      static_assert(NT % (BN / 8) == 0, "each thread keeps one column group");
-      for (int v = tid; v < BM * (BN / 8); v += NT) {
-        const int r = v / (BN / 8), c8 = c8e;
-        const int m = m0 + r, n = n0 + c8;
-        if (m >= rows || n >= a.out_cols) continue;
-        float s[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s[e] = 0.f;
-#pragma unroll
-        for (int q = 0; q < SK; ++q) {
-          const f32x4 lo = *(const f32x4*)&red[q][r][c8], hi = *(const f32x4*)&red[q][r][c8 + 4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            s[e] += lo[e];
-            s[4 + e] += hi[e];
-          }
-        }
-        v4u o;
-        v4u y{0u, 0u, 0u, 0u};
-        if (a.epi == EPI_STORE_MASK) y = *(const v4u*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          float v8 = epi_value<T>(a, s[e], bias8[e]);
-          if (a.epi == EPI_STORE_MASK) v8 *= act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope);
-          ((T*)&o)[e] = Elem<T>::from_f32(v8);
-        }
-        *(v4u*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
-      }
+      store_vectors<SK, RP, RAC, PRE>(a, red, bias8, c8e, m0, n0, tm, rows, pre);
     } else {
       for (int e = tid; e < BM * BN; e += NT) {
         const int r = e / BN, c = e - r * BN;
@@ -178,10 +224,11 @@ static void launch_direct_sk(const GemmArgs& a, int64_t max_rows, hipStream_t st
   const int64_t span = max_rows - a.row_begin;
   const int64_t tiles = ((span + DIRECT_BM - 1) / DIRECT_BM) * (a.Npad / DIRECT_BN);
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), 2048) + (a.x.kind ? a.x.blocks : 0);
+  void (*kern)(GemmArgs) = !a.route ? k_gemm_direct<SK, -1> : a.route_ac == 4 ? k_gemm_direct<SK, 4> : k_gemm_direct<SK, 0>;
   if (a.t_start || a.t_stop)
-    hipExtLaunchKernelGGL(k_gemm_direct<SK>, dim3(grid), dim3(64 * SK), 0, st, a.t_start, a.t_stop, 0, a);
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(64 * SK), 0, st, a.t_start, a.t_stop, 0, a);
   else
-    hipLaunchKernelGGL(k_gemm_direct<SK>, dim3(grid), dim3(64 * SK), 0, st, a);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * SK), 0, st, a);
 }
 
 hipError_t launch_gemm_direct(const GemmArgs& a, int64_t max_rows, hipStream_t st) {

@@ -59,6 +59,10 @@ struct GroundArgs {
   int32_t PM;   // partial stride, >= B1, B2
   float* db;
   float* D0;
+  // > 0: the partials come from the epilogue of the GEMM that wrote dY, one per
+  // tile of route_bm pooling rows (rows 1..n_pool): only the first
+  // ceil(n_pool / route_bm) of the B1 = B2 are read
+  int32_t route_bm;
 };
 
 // Row 0 of the gradient below a convolution (its ground row): for input channel
@@ -77,7 +81,9 @@ struct Row0Args {
 // Work that rides along as extra workgroups at the end of another launch (the
 // last `blocks` workgroups of the grid), independent of that launch's own work:
 //   kind 1: the ground final pass of a convolution (one workgroup per channel, cp);
-//   kind 2: row 0 of the gradient below a convolution (one per channel, cp_in).
+//   kind 2: row 0 of the gradient below a convolution (one per channel, cp_in);
+//   kind 3: kind 1 below a pooling layer whose row 0 gradient (kind 2 of the
+//           convolution above it, r) is computed first, in the same workgroup.
 struct ExtraTask {
   int32_t kind;    // 0: none
   int32_t blocks;
@@ -122,7 +128,23 @@ struct GemmArgs {
   hipEvent_t t_start, t_stop;
   ExtraTask x;  // extra workgroups appended to the launch (kind 0: none)
   int32_t partials_only;  // ksplit > 1: leave the fp32 partials, no reduce launch
+  // Pooling backward in the epilogue (route = 1; EPI_STORE, ksplit == 1, a
+  // tile shape that stages its output): the output rows m >= 1 are the gradient
+  // of a pooling layer, routed through its windows to the convolution below
+  // (delta rows >= 1, rectifier derivative applied) with that convolution's slot
+  // partial sums, one partial per row tile; pr describes both layers (its dY
+  // field is unused) and route_ac is the convolution's finished window count
+  // (0 or 4).
+  int32_t route;
+  int32_t route_ac;
+  GroundArgs pr;
 };
+
+// Whether a tile shape stages its output tile through LDS (16-byte stores), as
+// the pooling backward in the epilogue needs.
+bool gemm_routes(bool bf16, int cfg);
+// Row tile height of a tile shape.
+int gemm_bm(bool bf16, int cfg);
 
 // Tile shape and padding of one GEMM, chosen on the host from its row bound.
 struct GemmPlan {

@@ -17,23 +17,12 @@
 #include "common.h"
 #include "ground_tasks.h"
 #include "kernels.h"
+#include "pool_route.h"
 
 namespace sscn {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-
-// Packs VE argmax bytes (VE = 8 or 4) into one integer store/load.
-template <int VE>
-struct ArgPack;
-template <>
-struct ArgPack<8> {
-  typedef uint64_t W;
-};
-template <>
-struct ArgPack<4> {
-  typedef uint32_t W;
-};
 
 template <typename T>
 __global__ void __launch_bounds__(256) k_pool_fwd(const T* __restrict__ X_in, int32_t stride_in,
@@ -109,38 +98,16 @@ __device__ inline void block_channel_sums(const float (&acc)[K][VE], float* red,
   }
 }
 
-// gnd[k] = (R[i][k] == 0): window position k of row i reads the ground row.
-template <int AC>
-__device__ inline void ground_flags(const int32_t* __restrict__ R, int64_t i, int (&gnd)[AC > 0 ? AC : 1]) {
-  if constexpr (AC == 4) {
-    const i32x4 r = *(const i32x4*)(R + i * 4);
-    gnd[0] = r.x == 0;
-    gnd[1] = r.y == 0;
-    gnd[2] = r.z == 0;
-    gnd[3] = r.w == 0;
-  } else {
-#pragma unroll
-    for (int k = 0; k < AC; ++k) gnd[k] = R[i * AC + k] == 0;
-  }
-}
-
-// Pooling backward fused with the sums of the convolution below, one pass over
-// the pooling layer's rows o >= 1 (thread (lane l, channel vector v) of block b
-// takes rows 1 + b*lanes + l, then every gridDim*lanes-th).  For each window
-// position f of row o, with child row i = Rp[o][f]:
-//   i >= 1:  delta[i] = dY[o] * f'(Y_below[i]) where argmax[o] == f, else 0
-//            (each row >= 1 below lies in exactly one window: written once),
-//            summed into slot 1 and, where the convolution's window position f'
-//            of row i reads the ground row, into slot 2 + f';
-//   i == 0:  dY[o] where argmax[o] == f is summed into slot 0 (maxima taken from
-//            the ground state).
-// Partial p = block b of slot k, channel c: part[(k * cp + c) * PM + b].
+// Pooling backward fused with the sums of the convolution below (each row as
+// in pool_route_item), one pass over the pooling layer's rows o >= 1: thread
+// (lane l, channel vector v) of block b takes rows 1 + b*lanes + l, then every
+// gridDim*lanes-th.  Partial p = block b of slot k, channel c:
+// part[(k * cp + c) * PM + b].
 template <typename T, int AC>
 __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g, ExtraTask x) {
   if (run_extra<T>(x)) return;
   constexpr int VE = Elem<T>::VE;
   constexpr int J = 2 + AC;
-  typedef typename ArgPack<VE>::W AW;
   __shared__ float red[SUM_SB * 256 * VE];
   const int nv = g.cp / VE;
   const int lanes = 256 / nv;
@@ -148,8 +115,6 @@ __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g, ExtraTask x) {
   const int v = t % nv, rl = t / nv;
   const int c = v * VE;
   const T* dY = (const T*)g.dY;
-  const T* Yb = (const T*)g.Y_below;
-  T* dZ = (T*)g.dZ;
   const int n = *g.n_pool;
   float acc[J][VE];
 #pragma unroll
@@ -157,40 +122,10 @@ __global__ void __launch_bounds__(256) k_pool_bwd(GroundArgs g, ExtraTask x) {
 #pragma unroll
     for (int j = 0; j < VE; ++j) acc[k][j] = 0.f;
   if (rl < lanes) {
-#pragma unroll 2
+#pragma unroll 1
     for (int o = 1 + blockIdx.x * lanes + rl; o <= n; o += own_grid(x) * lanes) {
-      const i32x4 r = *(const i32x4*)(g.Rp + (int64_t)o * 4);
-      const AW am = *(const AW*)(g.argmax + (int64_t)o * g.stride + c);
       const u32x4 gv = *(const u32x4*)(dY + (int64_t)o * g.stride + c);
-#pragma unroll
-      for (int f = 0; f < 4; ++f) {
-        const int i = r[f];
-        if (i == 0) {
-#pragma unroll
-          for (int j = 0; j < VE; ++j)
-            acc[0][j] += ((int)((am >> (8 * j)) & 0xff) == f) ? Elem<T>::to_f32(((const T*)&gv)[j]) : 0.f;
-        } else {
-          const u32x4 y = *(const u32x4*)(Yb + (int64_t)i * g.stride + c);
-          int gnd[AC > 0 ? AC : 1];
-          ground_flags<AC>(g.R, i, gnd);
-          u32x4 out;
-#pragma unroll
-          for (int j = 0; j < VE; ++j) {
-            const float fac = act_factor(Elem<T>::to_f32(((const T*)&y)[j]), g.slope);
-            ((T*)&out)[j] = ((int)((am >> (8 * j)) & 0xff) == f)
-                                ? Elem<T>::from_f32(Elem<T>::to_f32(((const T*)&gv)[j]) * fac)
-                                : Elem<T>::from_f32(0.f);
-          }
-          *(u32x4*)(dZ + (int64_t)i * g.stride + c) = out;
-#pragma unroll
-          for (int j = 0; j < VE; ++j) {
-            const float d = Elem<T>::to_f32(((const T*)&out)[j]);
-            acc[1][j] += d;
-#pragma unroll
-            for (int k = 0; k < AC; ++k) acc[2 + k][j] += gnd[k] ? d : 0.f;
-          }
-        }
-      }
+      pool_route_item<T, AC>(g, o, c, (const T*)&gv, acc);
     }
   }
   block_channel_sums<VE, J>(acc, red, nv, g.cp, g.part + blockIdx.x, (int64_t)g.cp * g.PM, g.PM);
@@ -259,14 +194,13 @@ __global__ void __launch_bounds__(256) k_ground_sums(GroundArgs g, ExtraTask x) 
 #pragma unroll 4
     for (int i = i_beg + rl; i < i_end; i += lanes) {
       const u32x4 gv = *(const u32x4*)(dZ + (int64_t)i * g.stride + c);
-      int gnd[AC > 0 ? AC : 1];
-      ground_flags<AC>(g.R, i, gnd);
+      const WinRow<AC> wr = load_win_row<AC>(g.R, i);
 #pragma unroll
       for (int j = 0; j < VE; ++j) {
         const float d = Elem<T>::to_f32(((const T*)&gv)[j]);
         acc[0][j] += d;
 #pragma unroll
-        for (int k = 0; k < AC; ++k) acc[1 + k][j] += gnd[k] ? d : 0.f;
+        for (int k = 0; k < AC; ++k) acc[1 + k][j] += wr.v[k] == 0 ? d : 0.f;
       }
     }
   }
@@ -318,7 +252,7 @@ static void launch_ground_t(const GroundArgs& g, int kind, hipStream_t st, const
 
 static bool extra_ok(const ExtraTask& x) {
   if (x.kind == 0) return true;
-  if (x.blocks < 1 || (x.kind != 1 && x.kind != 2)) return false;
+  if (x.blocks < 1 || x.kind < 1 || x.kind > 3) return false;
   return x.kind == 2 || x.AC == 0 || x.AC == 1 || x.AC == 4 || x.AC == 9;
 }
 

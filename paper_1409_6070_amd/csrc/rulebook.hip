@@ -226,6 +226,89 @@ __device__ inline int32_t rank_row(const LayerBits& L, int b, int y, int x) {
   return 1 + L.soff[b] + L.wpre[idx] + __popcll(w & ((1ull << bit) - 1ull));
 }
 
+// Rows of the F x F locations (y0 + SIGN*dy, x0 + SIGN*dx), dy, dx < F, of
+// layer L in sample b: 0 where a location is inactive, `outside` where it lies
+// off the grid.  Every word and prefix load is issued before any is used.
+template <int F, int SIGN>
+__device__ inline void rank_window(const LayerBits& L, int b, int y0, int x0, int32_t outside,
+                                   int32_t (&r)[F * F]) {
+  constexpr int A = F * F;
+  int64_t idx[A];
+  int bit[A];
+  bool in[A];
+#pragma unroll
+  for (int dy = 0; dy < F; ++dy)
+#pragma unroll
+    for (int dx = 0; dx < F; ++dx) {
+      const int f = dy * F + dx, y = y0 + SIGN * dy, x = x0 + SIGN * dx;
+      in[f] = y >= 0 && x >= 0 && y < L.S && x < L.S;
+      idx[f] = in[f] ? ((int64_t)b * L.S + y) * L.Wd + (x >> 6) : 0;
+      bit[f] = x & 63;
+    }
+  uint64_t w[A];
+  int32_t pre[A];
+#pragma unroll
+  for (int f = 0; f < A; ++f) {
+    w[f] = L.bits[idx[f]];
+    pre[f] = L.wpre[idx[f]];
+  }
+  const int32_t off = L.soff[b];
+#pragma unroll
+  for (int f = 0; f < A; ++f) {
+    const bool on = (w[f] >> bit[f]) & 1ull;
+    r[f] = !in[f] ? outside : on ? 1 + off + pre[f] + __popcll(w[f] & ((1ull << bit[f]) - 1ull)) : 0;
+  }
+}
+
+// (b, y, x) of a site key of a layer with side S
+struct SiteKey {
+  int b, y, x;
+};
+__device__ inline SiteKey decode_key(int key, int S) {
+  const int x = key % S, t = key / S;
+  return SiteKey{t / S, t % S, x};
+}
+
+// R_s for rows [tid, n_out] step `stride` of a layer whose windows are F x F
+// locations below, `step` apart (1: convolution, 2: pooling).
+template <int F>
+__device__ inline void window_rows(const LayerBits& Lo, const LayerBits& Li, int step, int n_out, int32_t* R,
+                                   int64_t tid, int64_t stride) {
+  constexpr int A = F * F;
+  for (int64_t o = tid; o <= n_out; o += stride) {
+    int32_t r[A];
+    if (o == 0) {
+#pragma unroll
+      for (int f = 0; f < A; ++f) r[f] = 0;
+    } else {
+      const SiteKey k = decode_key(Lo.sites[o - 1], Lo.S);
+      rank_window<F, 1>(Li, k.b, step * k.y, step * k.x, 0, r);
+    }
+#pragma unroll
+    for (int f = 0; f < A; ++f) R[o * A + f] = r[f];
+  }
+}
+
+// Transposed convolution windows: for rows [tid, n_in] of layer s-1, the rows of
+// layer s whose window holds it at each position (-1: none).
+template <int F>
+__device__ inline void window_rows_t(const LayerBits& Lo, const LayerBits& Li, int n_in, int32_t* Rt, int64_t tid,
+                                     int64_t stride) {
+  constexpr int A = F * F;
+  for (int64_t i = tid; i <= n_in; i += stride) {
+    int32_t r[A];
+    if (i == 0) {
+#pragma unroll
+      for (int f = 0; f < A; ++f) r[f] = -1;
+    } else {
+      const SiteKey k = decode_key(Li.sites[i - 1], Li.S);
+      rank_window<F, -1>(Lo, k.b, k.y, k.x, -1, r);
+    }
+#pragma unroll
+    for (int f = 0; f < A; ++f) Rt[i * A + f] = r[f];
+  }
+}
+
 // Window lists (rules), their transposes, the caller-site -> row map and the
 // head rows.  Each list is a segment with its own range of workgroups
 // (RulesWork), grid-strided over its device-side count.
@@ -240,58 +323,36 @@ __global__ void __launch_bounds__(256) k_rb_rules(RulebookArgs a, RulesWork rw) 
     const LayerBits& Lo = a.L[s];
     const LayerBits& Li = a.L[s - 1];
     const int F = a.F[s];
-    const int A = F * F;
     if (kind == 0) {  // R_s: the window of every row of layer s
       const int step = (a.kind[s] == 1) ? 1 : 2;
       const int n_out = a.counts[s];
       int32_t* R = a.rules[s];
-      for (int64_t o = tid; o <= n_out; o += stride) {
-        if (o == 0) {
-          for (int f = 0; f < A; ++f) R[f] = 0;
-          continue;
-        }
-        const int key = Lo.sites[o - 1];
-        const int X = key % Lo.S;
-        const int tq = key / Lo.S;
-        const int Y = tq % Lo.S;
-        const int b = tq / Lo.S;
-        for (int dy = 0; dy < F; ++dy)
-          for (int dx = 0; dx < F; ++dx) R[o * A + dy * F + dx] = rank_row(Li, b, step * Y + dy, step * X + dx);
-      }
+      if (F == 3)
+        window_rows<3>(Lo, Li, step, n_out, R, tid, stride);
+      else if (F == 2)
+        window_rows<2>(Lo, Li, step, n_out, R, tid, stride);
+      else
+        window_rows<1>(Lo, Li, step, n_out, R, tid, stride);
     } else {  // transposes: for every row of layer s-1, the rows of layer s whose window holds it
       const int n_in = a.counts[s - 1];
       int32_t* Rt = a.rules_t[s];
-      for (int64_t i = tid; i <= n_in; i += stride) {
-        if (a.kind[s] == 1) {
-          if (i == 0) {
-            for (int f = 0; f < A; ++f) Rt[f] = -1;
-            continue;
-          }
-          const int key = Li.sites[i - 1];
-          const int x = key % Li.S;
-          const int tq = key / Li.S;
-          const int y = tq % Li.S;
-          const int b = tq / Li.S;
-          for (int dy = 0; dy < F; ++dy)
-            for (int dx = 0; dx < F; ++dx) {
-              const int Y = y - dy, X = x - dx;
-              int r = -1;
-              if (Y >= 0 && X >= 0 && Y < Lo.S && X < Lo.S) r = rank_row(Lo, b, Y, X);
-              Rt[i * A + dy * F + dx] = r;
-            }
-        } else {
+      if (a.kind[s] == 1) {
+        if (F == 3)
+          window_rows_t<3>(Lo, Li, n_in, Rt, tid, stride);
+        else if (F == 2)
+          window_rows_t<2>(Lo, Li, n_in, Rt, tid, stride);
+        else
+          window_rows_t<1>(Lo, Li, n_in, Rt, tid, stride);
+      } else {
+        for (int64_t i = tid; i <= n_in; i += stride) {
           if (i == 0) {
             Rt[0] = -1;
             continue;
           }
-          const int key = Li.sites[i - 1];
-          const int x = key % Li.S;
-          const int tq = key / Li.S;
-          const int y = tq % Li.S;
-          const int b = tq / Li.S;
-          const int Y = y >> 1, X = x >> 1;
+          const SiteKey k = decode_key(Li.sites[i - 1], Li.S);
+          const int Y = k.y >> 1, X = k.x >> 1;
           int r = -1;
-          if (Y < Lo.S && X < Lo.S) r = rank_row(Lo, b, Y, X) * 4 + (y & 1) * 2 + (x & 1);
+          if (Y < Lo.S && X < Lo.S) r = rank_row(Lo, k.b, Y, X) * 4 + (k.y & 1) * 2 + (k.x & 1);
           Rt[i] = r;
         }
       }
