@@ -89,6 +89,9 @@ struct sscn_net {
   float* D0;
   float* ppart;
   size_t ppart_half;  // floats per convolution-parity half of ppart
+  uint64_t* bits0_alt;  // the second input bitmap (builds alternate with L[0].bits)
+  int32_t rb_parity;    // which input bitmap and error word the next build uses
+  int32_t* err_cur;     // the last build's error word
   size_t d0_half;     // and of D0
   void* hdrop;  // the softmax layer's dropped input [batch_max][Cp_top] (dropout workspace only)
   size_t ws_bytes;
@@ -195,6 +198,7 @@ static void carve(sscn_net* net, void* base) {
     LayerPlan& L = net->L[s];
     const size_t words = (size_t)B * L.S * L.Wd;
     L.bits = (uint64_t*)cv.take(words * 8);
+    if (s == 0) net->bits0_alt = (uint64_t*)cv.take(words * 8);  // builds alternate input bitmaps
     L.wpre = (int32_t*)cv.take(words * 4);
     L.scount = (int32_t*)cv.take((size_t)B * 4);
     L.soff = (int32_t*)cv.take((size_t)B * 4);
@@ -474,13 +478,18 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   if (n > net->d.max_active || batch > net->d.batch_max) return SSCN_ERR_CAPACITY;
   if (!d_ws || ws_bytes < net->ws_bytes || ((uintptr_t)d_ws & 255u)) return SSCN_ERR_WORKSPACE;
   net->built = net->forwarded = net->backwarded = false;
+  hipStream_t st = (hipStream_t)stream;
   if (net->ws != d_ws) {
     carve(net, d_ws);
     net->ws = d_ws;
+    net->rb_parity = 0;
+    const LayerPlan& L0 = net->L[0];
+    if (launch_rulebook_reset(L0.bits, net->bits0_alt, (int64_t)net->d.batch_max * L0.S * L0.Wd, net->err, st) !=
+        hipSuccess)
+      return SSCN_ERR_HIP;
   }
   net->batch = batch;
   net->n = n;
-  hipStream_t st = (hipStream_t)stream;
   RulebookArgs a;
   std::memset(&a, 0, sizeof(a));
   a.nlayers = net->nlayers;
@@ -501,7 +510,16 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   wk.base[net->nlayers] = acc;
   wk.total = acc;
   a.counts = net->counts;
-  a.err = net->err;
+  // this build's input bitmap and error word, and the next build's (cleared
+  // here); err[1] is the loss counter, err[0] spare
+  const int par = net->rb_parity;
+  uint64_t* bits0[2] = {net->L[0].bits, net->bits0_alt};
+  a.L[0].bits = bits0[par];
+  a.bits0_next = bits0[1 - par];
+  a.err = net->err + 2 + par;
+  a.err_next = net->err + 2 + (1 - par);
+  a.batch_max = net->d.batch_max;
+  net->err_cur = a.err;
   a.perm = net->perm;
   a.head_rows = net->head_rows;
   a.coords = d_coords;
@@ -524,6 +542,7 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   add_seg(3, 0, batch);
   if (timed(net, SSCN_KC_RULEBOOK, st, [&] { return launch_rulebook(a, wk, rw, net->max_words, st); }) != hipSuccess)
     return SSCN_ERR_HIP;
+  net->rb_parity = 1 - par;
   net->built = true;
   return SSCN_OK;
 }
@@ -535,7 +554,7 @@ sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream) {
   int32_t err = 0;
   if (hipMemcpyAsync(h_counts, net->counts, sizeof(int32_t) * net->nlayers, hipMemcpyDeviceToHost, st) != hipSuccess)
     return SSCN_ERR_HIP;
-  if (hipMemcpyAsync(&err, net->err, sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (hipMemcpyAsync(&err, net->err_cur, sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess) return SSCN_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return SSCN_ERR_HIP;
   if (err & ERRBIT_RANGE) return SSCN_ERR_OUT_OF_RANGE;
   if (err & ERRBIT_DUP) return SSCN_ERR_DUPLICATE_SITE;

@@ -130,7 +130,10 @@ struct RulebookArgs {
   int32_t* rules[MAX_LAYERS];    // layer s >= 1: [(cap_s+1) * A]
   int32_t* rules_t[MAX_LAYERS];  // layer s >= 1: conv [(cap_{s-1}+1) * A], pool [cap_{s-1}+1]
   int32_t* counts;               // [nlayers]
-  int32_t* err;
+  int32_t* err;                  // this build's error word (zero on entry)
+  int32_t* err_next;             // the next build's error word, cleared here
+  uint64_t* bits0_next;          // the next build's input bitmap [batch_max * S0 * Wd0], cleared here
+  int32_t batch_max;
   int32_t* perm;                 // [n] row of each caller site (or -1)
   int32_t* head_rows;            // [batch]
   const int32_t* coords;         // [n][3]

@@ -24,6 +24,9 @@ struct RulesWork {
 
 hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const RulesWork& rw, int32_t max_words,
                            hipStream_t st);
+// Clears both alternating input bitmaps (nwords each) and the four error /
+// counter words: once per bound workspace, before its first build.
+hipError_t launch_rulebook_reset(uint64_t* bits_a, uint64_t* bits_b, int64_t nwords, int32_t* err, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // gather GEMM: out[m][n] = epi( sum_k A(m,k) * Bt[n][k] ),

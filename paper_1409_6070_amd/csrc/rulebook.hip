@@ -12,20 +12,30 @@
 // Active sets follow Section 2.3 and Figure 2: a convolution output is active
 // when any location of its FxF window below is active, a pooling output when
 // any of its 2x2 stride-2 window is.  Both are computed bit-parallel on whole
-// 64-bit words, one workgroup per sample with the sample's bitmaps in LDS.
+// 64-bit words, one wave per sample with the sample's bitmaps in LDS; a second
+// launch turns the per-sample counts into sample offsets (a last-workgroup
+// pattern would need a device-scope release fence, which costs more here than
+// the launch).
+//
+// Builds alternate between two input bitmaps (and error words): each build
+// inserts into one that is all zero and clears the other for the next build,
+// so no clearing launch precedes the insertion.
 
 #include "common.h"
 #include "kernels.h"
 
 namespace sscn {
 
-static constexpr int RB_THREADS = 256;
-
-__global__ void __launch_bounds__(256) k_rb_clear(uint64_t* bits0, int64_t nwords, int32_t* err) {
+// Clears both input bitmaps and the error and counter words (when a workspace
+// is bound; afterwards each build clears what the next one needs).
+__global__ void __launch_bounds__(256) k_rb_clear(uint64_t* bits_a, uint64_t* bits_b, int64_t nwords, int32_t* err) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (; i < nwords; i += stride) bits0[i] = 0ull;
-  if (blockIdx.x == 0 && threadIdx.x < 4) err[threadIdx.x] = 0;  // error word and the completion counters
+  for (; i < nwords; i += stride) {
+    bits_a[i] = 0ull;
+    bits_b[i] = 0ull;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < 4) err[threadIdx.x] = 0;
 }
 
 __global__ void __launch_bounds__(256) k_rb_insert(const int32_t* __restrict__ coords, int32_t n, int32_t batch,
@@ -62,134 +72,136 @@ __device__ inline uint64_t row_mask_word(int w, int S) {
   return (1ull << nb) - 1ull;
 }
 
-// Exclusive prefix of one value per thread over the block (RB_THREADS = 4
-// waves): an inclusive scan inside each wave with lane shuffles, then the wave
-// totals through LDS -- two barriers.  Returns the prefix; *total gets the sum.
-__device__ inline int block_exclusive_scan(int local, int* scratch, int* total) {
-  static_assert(RB_THREADS == 256, "four waves");
-  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-  int v = local;
+// Exclusive prefix of one value per lane over a wave; *total gets the sum.
+__device__ inline int wave_exclusive_scan(int v, int* total) {
+  const int lane = threadIdx.x & 63;
+  int x = v;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
-    const int u = __shfl_up(v, off, 64);
-    if (lane >= off) v += u;
+    const int u = __shfl_up(x, off, 64);
+    if (lane >= off) x += u;
   }
-  if (lane == 63) scratch[wv] = v;
-  __syncthreads();
-  int base = 0;
-  for (int i = 0; i < wv; ++i) base += scratch[i];
-  *total = (scratch[0] + scratch[1]) + (scratch[2] + scratch[3]);
-  __syncthreads();
-  return base + v - local;
+  *total = __shfl(x, 63, 64);
+  return x - v;
 }
 
-// Block-wide exclusive prefix of popcounts over nw words held in LDS.
-// Writes wpre[0..nw) (global) and returns the total.
-__device__ int block_popcount_scan(const uint64_t* words, int nw, int32_t* wpre, int* scratch) {
+// Popcount prefix of nw words held in LDS by one wave (lane t takes the
+// contiguous words [t * per, (t + 1) * per)): writes wpre[0..nw) and returns
+// the total.
+__device__ inline int wave_popcount_scan(const uint64_t* words, int nw, int32_t* wpre) {
   const int t = threadIdx.x;
-  const int per = (nw + RB_THREADS - 1) / RB_THREADS;
-  const int beg = t * per;
+  const int per = (nw + 63) / 64;
+  const int beg = min(nw, t * per), end = min(nw, beg + per);
   int local = 0;
-  for (int j = 0; j < per; ++j) {
-    int w = beg + j;
-    if (w < nw) local += __popcll(words[w]);
-  }
+  for (int w = beg; w < end; ++w) local += __popcll(words[w]);
   int total;
-  int run = block_exclusive_scan(local, scratch, &total);
-  for (int j = 0; j < per; ++j) {
-    int w = beg + j;
-    if (w < nw) {
-      wpre[w] = run;
-      run += __popcll(words[w]);
-    }
+  int run = wave_exclusive_scan(local, &total);
+  for (int w = beg; w < end; ++w) {
+    wpre[w] = run;
+    run += __popcll(words[w]);
   }
   return total;
 }
 
-// One workgroup per sample: every layer's bitmap from the input bitmap.
-__global__ void __launch_bounds__(RB_THREADS) k_rb_bitmaps(RulebookArgs a, int32_t max_words) {
+// Output word idx of an F x F valid convolution's active set, from the bitmap
+// below in LDS.
+template <int F>
+__device__ inline uint64_t conv_word(const uint64_t* cur, int idx, int Wo, int Wi, int So) {
+  const int Y = idx / Wo, w = idx - Y * Wo;
+  uint64_t acc = 0;
+#pragma unroll
+  for (int dy = 0; dy < F; ++dy) {
+    const uint64_t* row = cur + (Y + dy) * Wi;
+    const uint64_t lo = row[w];
+    const uint64_t hi = (w + 1 < Wi) ? row[w + 1] : 0ull;
+    acc |= lo;
+#pragma unroll
+    for (int dx = 1; dx < F; ++dx) acc |= (lo >> dx) | (hi << (64 - dx));
+  }
+  return acc & row_mask_word(w, So);
+}
+
+// Every layer's bitmap from the input bitmap, one wave (workgroup) per sample;
+// workgroups b >= batch only clear.  Each workgroup also clears its share of
+// the next build's input bitmap.
+__global__ void __launch_bounds__(64) k_rb_bitmaps(RulebookArgs a, int32_t max_words) {
   extern __shared__ uint64_t lds[];
   uint64_t* cur = lds;
   uint64_t* nxt = lds + max_words;
-  int* scratch = (int*)(lds + 2 * max_words);
   const int b = blockIdx.x;
   const int t = threadIdx.x;
-
-  {  // layer 0
-    const LayerBits& L = a.L[0];
-    const int nw = L.S * L.Wd;
-    const uint64_t* src = L.bits + (int64_t)b * nw;
-    for (int w = t; w < nw; w += RB_THREADS) cur[w] = src[w];
-    __syncthreads();
-    int tot = block_popcount_scan(cur, nw, L.wpre + (int64_t)b * nw, scratch);
-    if (t == 0) L.scount[b] = tot;
+  {
+    const int64_t nw0 = (int64_t)a.L[0].S * a.L[0].Wd;
+    for (int64_t smp = b; smp < a.batch_max; smp += gridDim.x)
+      for (int64_t w = t; w < nw0; w += 64) a.bits0_next[smp * nw0 + w] = 0ull;
+    if (b == 0 && t == 0) *a.err_next = 0;
   }
-  for (int s = 1; s < a.nlayers; ++s) {
-    const LayerBits& Li = a.L[s - 1];
-    const LayerBits& Lo = a.L[s];
-    const int nwo = Lo.S * Lo.Wd;
-    if (a.kind[s] == 1) {  // convolution, F x F valid window
-      const int F = a.F[s];
-      for (int idx = t; idx < nwo; idx += RB_THREADS) {
-        const int Y = idx / Lo.Wd, w = idx - Y * Lo.Wd;
-        uint64_t acc = 0;
-        for (int dy = 0; dy < F; ++dy) {
-          const uint64_t* row = cur + (Y + dy) * Li.Wd;
-          const uint64_t lo = row[w];
-          const uint64_t hi = (w + 1 < Li.Wd) ? row[w + 1] : 0ull;
-          acc |= lo;
-          for (int dx = 1; dx < F; ++dx) acc |= (lo >> dx) | (hi << (64 - dx));
-        }
-        nxt[idx] = acc & row_mask_word(w, Lo.S);
-      }
-    } else {  // 2x2 stride-2 pooling
-      for (int idx = t; idx < nwo; idx += RB_THREADS) {
-        const int Y = idx / Lo.Wd, w = idx - Y * Lo.Wd;
-        const uint64_t* r0 = cur + (2 * Y) * Li.Wd;
-        const uint64_t* r1 = r0 + Li.Wd;
-        uint64_t p0 = 0, p1 = 0;
-        if (2 * w < Li.Wd) {
-          uint64_t r = r0[2 * w] | r1[2 * w];
-          p0 = compress_even_bits(r | (r >> 1));
-        }
-        if (2 * w + 1 < Li.Wd) {
-          uint64_t r = r0[2 * w + 1] | r1[2 * w + 1];
-          p1 = compress_even_bits(r | (r >> 1));
-        }
-        nxt[idx] = (p0 | (p1 << 32)) & row_mask_word(w, Lo.S);
-      }
+  if (b < a.batch) {
+    {  // layer 0
+      const LayerBits& L = a.L[0];
+      const int nw = L.S * L.Wd;
+      const uint64_t* src = L.bits + (int64_t)b * nw;
+      for (int w = t; w < nw; w += 64) cur[w] = src[w];
+      __syncthreads();
+      const int tot = wave_popcount_scan(cur, nw, L.wpre + (int64_t)b * nw);
+      if (t == 0) L.scount[b] = tot;
     }
-    __syncthreads();
-    uint64_t* dst = Lo.bits + (int64_t)b * nwo;
-    for (int w = t; w < nwo; w += RB_THREADS) dst[w] = nxt[w];
-    int tot = block_popcount_scan(nxt, nwo, Lo.wpre + (int64_t)b * nwo, scratch);
-    if (t == 0) Lo.scount[b] = tot;
-    uint64_t* tmp = cur;
-    cur = nxt;
-    nxt = tmp;
-    __syncthreads();
+    for (int s = 1; s < a.nlayers; ++s) {
+      const LayerBits& Li = a.L[s - 1];
+      const LayerBits& Lo = a.L[s];
+      const int nwo = Lo.S * Lo.Wd;
+      if (a.kind[s] == 1) {  // convolution, F x F valid window
+        const int F = a.F[s];
+        for (int idx = t; idx < nwo; idx += 64)
+          nxt[idx] = F == 3   ? conv_word<3>(cur, idx, Lo.Wd, Li.Wd, Lo.S)
+                     : F == 2 ? conv_word<2>(cur, idx, Lo.Wd, Li.Wd, Lo.S)
+                              : conv_word<1>(cur, idx, Lo.Wd, Li.Wd, Lo.S);
+      } else {  // 2x2 stride-2 pooling
+        for (int idx = t; idx < nwo; idx += 64) {
+          const int Y = idx / Lo.Wd, w = idx - Y * Lo.Wd;
+          const uint64_t* r0 = cur + (2 * Y) * Li.Wd;
+          const uint64_t* r1 = r0 + Li.Wd;
+          uint64_t p0 = 0, p1 = 0;
+          if (2 * w < Li.Wd) {
+            const uint64_t r = r0[2 * w] | r1[2 * w];
+            p0 = compress_even_bits(r | (r >> 1));
+          }
+          if (2 * w + 1 < Li.Wd) {
+            const uint64_t r = r0[2 * w + 1] | r1[2 * w + 1];
+            p1 = compress_even_bits(r | (r >> 1));
+          }
+          nxt[idx] = (p0 | (p1 << 32)) & row_mask_word(w, Lo.S);
+        }
+      }
+      __syncthreads();
+      uint64_t* dst = Lo.bits + (int64_t)b * nwo;
+      for (int w = t; w < nwo; w += 64) dst[w] = nxt[w];
+      const int tot = wave_popcount_scan(nxt, nwo, Lo.wpre + (int64_t)b * nwo);
+      if (t == 0) Lo.scount[b] = tot;
+      uint64_t* tmp = cur;
+      cur = nxt;
+      nxt = tmp;
+      __syncthreads();
+    }
   }
 }
 
-// Sample offsets and layer totals: one workgroup per layer, a block-wide
-// exclusive scan of the per-sample counts.
-__global__ void __launch_bounds__(RB_THREADS) k_rb_offsets(RulebookArgs a) {
-  __shared__ int scratch[RB_THREADS / 64];
-  const int s = blockIdx.x;
-  const int t = threadIdx.x;
+
+// Sample offsets and layer totals: one wave per layer, an exclusive scan of the
+// per-sample counts.
+__global__ void __launch_bounds__(64) k_rb_offsets(RulebookArgs a) {
+  const int s = blockIdx.x, t = threadIdx.x;
   const LayerBits& L = a.L[s];
-  const int per = (a.batch + RB_THREADS - 1) / RB_THREADS;
-  const int beg = t * per;
+  const int per = (a.batch + 63) / 64;
+  const int beg = min(a.batch, t * per), end = min(a.batch, beg + per);
   int local = 0;
-  for (int j = 0; j < per; ++j)
-    if (beg + j < a.batch) local += L.scount[beg + j];
+  for (int i = beg; i < end; ++i) local += L.scount[i];
   int total;
-  int run = block_exclusive_scan(local, scratch, &total);
-  for (int j = 0; j < per; ++j)
-    if (beg + j < a.batch) {
-      L.soff[beg + j] = run;
-      run += L.scount[beg + j];
-    }
+  int run = wave_exclusive_scan(local, &total);
+  for (int i = beg; i < end; ++i) {
+    L.soff[i] = run;
+    run += L.scount[i];
+  }
   if (t == 0) a.counts[s] = total;
 }
 
@@ -374,22 +386,22 @@ __global__ void __launch_bounds__(256) k_rb_rules(RulebookArgs a, RulesWork rw) 
 hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const RulesWork& rw, int32_t max_words,
                            hipStream_t st) {
   const LayerBits& L0 = a.L[0];
-  int64_t nw0 = (int64_t)a.batch * L0.S * L0.Wd;
-  int g = (int)std::min<int64_t>((nw0 + 255) / 256, 1024);
-  if (g < 1) g = 1;
-  hipLaunchKernelGGL(k_rb_clear, dim3(g), dim3(256), 0, st, L0.bits, nw0, a.err);
   if (a.n > 0)
     hipLaunchKernelGGL(k_rb_insert, dim3((a.n + 255) / 256), dim3(256), 0, st, a.coords, a.n, a.batch, L0.S, L0.Wd,
                        L0.bits, a.err);
-  if (a.batch > 0) {
-    size_t lds = (size_t)2 * max_words * sizeof(uint64_t) + RB_THREADS * sizeof(int);
-    hipLaunchKernelGGL(k_rb_bitmaps, dim3(a.batch), dim3(RB_THREADS), lds, st, a, max_words);
-  }
-  hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(RB_THREADS), 0, st, a);
+  const size_t lds = (size_t)2 * max_words * sizeof(uint64_t);
+  hipLaunchKernelGGL(k_rb_bitmaps, dim3(std::max(a.batch, 1)), dim3(64), lds, st, a, max_words);
+  hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
   int gs = (int)std::min<int64_t>((wk.total + 255) / 256, 2048);
   if (gs < 1) gs = 1;
   hipLaunchKernelGGL(k_rb_sites, dim3(gs), dim3(256), 0, st, a, wk);
   hipLaunchKernelGGL(k_rb_rules, dim3(rw.blk[rw.nseg]), dim3(256), 0, st, a, rw);
+  return hipGetLastError();
+}
+
+hipError_t launch_rulebook_reset(uint64_t* bits_a, uint64_t* bits_b, int64_t nwords, int32_t* err, hipStream_t st) {
+  const int g = (int)std::max<int64_t>(1, std::min<int64_t>((nwords + 255) / 256, 1024));
+  hipLaunchKernelGGL(k_rb_clear, dim3(g), dim3(256), 0, st, bits_a, bits_b, nwords, err);
   return hipGetLastError();
 }
 

@@ -228,6 +228,41 @@ def test_invalid_sites_are_reported(bad, status):
     assert net.layer_sizes()[0] == 2
 
 
+def test_rebuilds_alternate_input_bitmaps():
+    """Consecutive builds on one net.  Each build inserts into one of two input bitmaps (and error
+    words) and clears the other for the next build, so every build must be bit-exact whatever the
+    builds before it held: a larger batch after a smaller one, an empty batch, and a clean build
+    right after one that reported a duplicate site."""
+    from paper_1409_6070_amd import sscn
+    from tests.gpu_harness import decode_sites
+    ell, k, c_in, ncls, bmax = 3, 4, 1, 5, 5
+    net = sscn.SparseDeepCNet(ell, k, c_in, ncls, batch_max=bmax, max_active=24 * 24 * bmax, dtype="f32")
+    seq = [(5, 0.3, 11), (2, 0.05, 12), (0, 0.0, 13), (5, 0.15, 14), (4, 0.1, 15, "dup"), (3, 0.2, 16),
+           (5, 0.02, 17), (1, 0.5, 18)]
+    for step in seq:
+        batch, p, seed = step[:3]
+        coords, _ = _sparse_case(seed, ell, batch, p, c_in) if batch else (np.zeros((0, 3), np.int64), None)
+        log(f"[rebuild] batch={batch} n={len(coords)} seed={seed} {'dup' if len(step) > 3 else ''}")
+        if len(step) > 3:
+            coords = np.concatenate([coords, coords[:1]])
+            net.rulebook_build(torch.tensor(coords, dtype=torch.int32).cuda(), batch)
+            with pytest.raises(sscn.SSCNError) as e:
+                net.layer_sizes()
+            assert e.value.name == "SSCN_ERR_DUPLICATE_SITE"
+            continue
+        net.rulebook_build(torch.tensor(coords, dtype=torch.int32).cuda().reshape(-1, 3), batch)
+        counts = net.layer_sizes()
+        o = Oracle(ell, k, c_in, ncls, "f32")
+        o.build(np.asarray(coords).reshape(-1, 3), batch)
+        assert counts == o.layer_sizes(), (counts, o.layer_sizes())
+        for s_, L in enumerate(o.layers):
+            v = net.layer_view(s_, counts[s_])
+            np.testing.assert_array_equal(decode_sites(v["sites"].cpu().numpy(), L.S), L.sites,
+                                          err_msg=f"sites layer {s_} batch {batch}")
+            if s_:
+                np.testing.assert_array_equal(v["rules"].cpu().numpy(), L.R, err_msg=f"rules layer {s_}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_inference_digits_full_size(dtype):
     """Forward-only classification (Section 3.2's timed workload, DeepCNet(5,10) on digit pictures
