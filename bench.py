@@ -61,7 +61,7 @@ def layer_shapes(cfg):
     return st
 
 
-def gemm_work(cfg, sizes, infer=False, e=2):
+def gemm_work(cfg, sizes, infer=False, e=2, routed=True):
     """Algorithmic FLOPs of one step, per kernel class, and the compulsory bytes of the
     gather-GEMM launches (e bytes per stored element).
 
@@ -77,7 +77,11 @@ def gemm_work(cfg, sizes, infer=False, e=2):
     (n_s+1)C_out e + (n_{s-1}+1)A*4 + n_{s-1}C_in e (+ the same again for the
     rectifier mask when a convolution lies below) + the weights; softmax layer
     forward B C e + 4B + 4B classes + C classes e, dh B classes e + 4 B C + the
-    weights.
+    weights.  With ``routed`` an input-gradient GEMM whose output is a pooling
+    layer also runs that layer's backward in its epilogue: + the convolution
+    below's output read and delta written (n_c C e each), the argmax bytes
+    (n_{s-1} C), the pooling windows (16 n_{s-1}) and, above the first layer,
+    the convolution's window lists (n_c A_c 4).
     """
     fwd = dgrad = 0.0
     fbytes = dbytes = 0.0
@@ -93,6 +97,9 @@ def gemm_work(cfg, sizes, infer=False, e=2):
             dgrad += 2.0 * nb * A * co * ci
             mask = nb * ci * e if shapes[s - 2][0] == "conv" else 0
             dbytes += (n + 1) * co * e + (nb + 1) * (A * 4 if A > 1 else 0) + nb * ci * e + mask + w
+            if routed and shapes[s - 2][0] == "pool" and A > 1:
+                nc, Ac = sizes[s - 2], shapes[s - 3][1]
+                dbytes += 2 * nc * ci * e + nb * ci + 16 * nb + (nc * Ac * 4 if s - 2 > 1 else 0)
     C = (cfg.ell + 1) * cfg.k
     B, K = cfg.batch, cfg.n_classes
     head = 2.0 * B * C * K
@@ -319,7 +326,8 @@ def main():
     # algorithmic work of the timed steps (batches cycle in order)
     step_sizes = [sizes[i % len(sizes)] for i in range(args.steps)]
     esz = 2 if args.dtype == "bf16" else 4
-    work = [gemm_work(cfg, s, infer, esz) for s in step_sizes]
+    # (the pooling backward runs in the GEMM epilogues except through dropout)
+    work = [gemm_work(cfg, s, infer, esz, routed=not cfg.dropout) for s in step_sizes]
     g_flops = sum(w["gather_gemm"] for w in work)
     g_bytes = sum(w["gather_gemm_bytes"] for w in work)
     avg_launch_s = g_ms / 1e3 / max(g_launches, 1)
@@ -329,7 +337,8 @@ def main():
     roofline = {
         "kernel": ("gather-GEMM class: k_gemm_gather (LDS-tiled) and k_gemm_direct (direct-operand) implicit-gather "
                    "MFMA GEMMs; " + ("conv forward, softmax layer logits" if infer else
-                                     "conv forward, conv input gradient, softmax layer")),
+                                     "conv forward, conv input gradient (with the pooling backward in its "
+                                     "epilogue), softmax layer")),
         "bound": "mfma", "achieved": round(achieved / 1e12, 3), "peak": peak / 1e12, "unit": "TFLOP/s",
         "frac": round(achieved / peak, 5), "traffic": traffic,
         "launches_per_step": g_launches / args.steps, "avg_launch_us": round(avg_launch_s * 1e6, 3),
