@@ -103,11 +103,30 @@ __device__ inline int wave_popcount_scan(const uint64_t* words, int nw, int32_t*
   return total;
 }
 
+// q = k / d for 0 <= k < 2^20, 1 <= d < 2^16 (rcp = 1/d): float estimate,
+// then exact correction (an integer division by a runtime value costs tens of
+// instructions).
+__device__ inline int div_rcp(int k, int d, float rcp) {
+  int q = (int)((float)k * rcp);
+  q += (q + 1) * d <= k ? 1 : 0;
+  q -= q * d > k ? 1 : 0;
+  return q;
+}
+
+// q = k / d for 0 <= k < 2^40, 1 <= d < 2^20: double estimate, then exact
+// correction.
+__device__ inline int div_rcp_d(int64_t k, int d) {
+  int64_t q = (int64_t)((double)k * (1.0 / (double)d));
+  q += (q + 1) * d <= k ? 1 : 0;
+  q -= q * d > k ? 1 : 0;
+  return (int)q;
+}
+
 // Output word idx of an F x F valid convolution's active set, from the bitmap
 // below in LDS.
 template <int F>
-__device__ inline uint64_t conv_word(const uint64_t* cur, int idx, int Wo, int Wi, int So) {
-  const int Y = idx / Wo, w = idx - Y * Wo;
+__device__ inline uint64_t conv_word(const uint64_t* cur, int idx, int Wo, float rcp_wo, int Wi, int So) {
+  const int Y = div_rcp(idx, Wo, rcp_wo), w = idx - Y * Wo;
   uint64_t acc = 0;
 #pragma unroll
   for (int dy = 0; dy < F; ++dy) {
@@ -150,15 +169,16 @@ __global__ void __launch_bounds__(64) k_rb_bitmaps(RulebookArgs a, int32_t max_w
       const LayerBits& Li = a.L[s - 1];
       const LayerBits& Lo = a.L[s];
       const int nwo = Lo.S * Lo.Wd;
+      const float rcp_wo = 1.f / (float)Lo.Wd;
       if (a.kind[s] == 1) {  // convolution, F x F valid window
         const int F = a.F[s];
         for (int idx = t; idx < nwo; idx += 64)
-          nxt[idx] = F == 3   ? conv_word<3>(cur, idx, Lo.Wd, Li.Wd, Lo.S)
-                     : F == 2 ? conv_word<2>(cur, idx, Lo.Wd, Li.Wd, Lo.S)
-                              : conv_word<1>(cur, idx, Lo.Wd, Li.Wd, Lo.S);
+          nxt[idx] = F == 3   ? conv_word<3>(cur, idx, Lo.Wd, rcp_wo, Li.Wd, Lo.S)
+                     : F == 2 ? conv_word<2>(cur, idx, Lo.Wd, rcp_wo, Li.Wd, Lo.S)
+                              : conv_word<1>(cur, idx, Lo.Wd, rcp_wo, Li.Wd, Lo.S);
       } else {  // 2x2 stride-2 pooling
         for (int idx = t; idx < nwo; idx += 64) {
-          const int Y = idx / Lo.Wd, w = idx - Y * Lo.Wd;
+          const int Y = div_rcp(idx, Lo.Wd, rcp_wo), w = idx - Y * Lo.Wd;
           const uint64_t* r0 = cur + (2 * Y) * Li.Wd;
           const uint64_t* r1 = r0 + Li.Wd;
           uint64_t p0 = 0, p1 = 0;
@@ -216,10 +236,10 @@ __global__ void __launch_bounds__(256) k_rb_sites(RulebookArgs a, SitesWork wk) 
     int64_t idx = g - wk.base[s];
     uint64_t word = L.bits[idx];
     if (!word) continue;
-    int64_t per_sample = (int64_t)L.S * L.Wd;
-    int b = (int)(idx / per_sample);
-    int rem = (int)(idx - (int64_t)b * per_sample);
-    int y = rem / L.Wd, w = rem - y * L.Wd;
+    const int per_sample = L.S * L.Wd;  // words per sample (< 2^20)
+    const int b = div_rcp_d(idx, per_sample);
+    const int rem = (int)(idx - (int64_t)b * per_sample);
+    const int y = div_rcp(rem, L.Wd, 1.f / (float)L.Wd), w = rem - y * L.Wd;
     int row = L.soff[b] + L.wpre[idx];
     while (word) {
       int bit = __ffsll((long long)word) - 1;
@@ -277,8 +297,9 @@ struct SiteKey {
   int b, y, x;
 };
 __device__ inline SiteKey decode_key(int key, int S) {
-  const int x = key % S, t = key / S;
-  return SiteKey{t / S, t % S, x};
+  const int t = div_rcp_d(key, S), x = key - t * S;
+  const int b = div_rcp_d(t, S), y = t - b * S;
+  return SiteKey{b, y, x};
 }
 
 // R_s for rows [tid, n_out] step `stride` of a layer whose windows are F x F
