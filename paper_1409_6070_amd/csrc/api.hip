@@ -766,18 +766,41 @@ static WGradArgs conv_wgrad_args(const sscn_net* net, int s) {
 }
 
 // Weight gradients of a list of layers: one launch per tile shape, then one
-// launch reducing every split-K layer.
-static hipError_t run_wgrads(sscn_net* net, const WGradArgs* w, int n, hipStream_t st) {
+// launch reducing every split-K layer.  A ground final pass that must precede
+// layer fin_layer's weight gradient (it writes that layer's delta row 0) rides
+// on the first launch when that launch does not hold fin_layer, else runs alone
+// first.
+static hipError_t run_wgrads(sscn_net* net, const WGradArgs* w, int n, hipStream_t st,
+                             const ExtraTask* fin = nullptr, int fin_layer = -1) {
   hipError_t e;
+  bool fin_done = !fin || !fin->kind;
   for (int cfg = 0; cfg < 2; ++cfg) {
     WGradArgs sel[MAX_WG_LAYERS];
     int k = 0;
+    bool holds = false;
     for (int i = 0; i < n; ++i)
-      if (w[i].cfg == cfg) sel[k++] = w[i];
-    if (k && (e = timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, cfg, sel, k, st); })) !=
-                 hipSuccess)
+      if (w[i].cfg == cfg) {
+        holds = holds || i == fin_layer;
+        sel[k++] = w[i];
+      }
+    if (!k) continue;
+    const ExtraTask* x = nullptr;
+    if (!fin_done) {
+      if (holds) {
+        if ((e = timed(net, SSCN_KC_GROUND, st, [&] { return launch_extra(net->bf16, *fin, st); })) != hipSuccess)
+          return e;
+      } else {
+        x = fin;
+      }
+      fin_done = true;
+    }
+    if ((e = timed(net, SSCN_KC_WGRAD, st, [&] { return launch_wgrad(net->bf16, cfg, sel, k, st, x); })) !=
+        hipSuccess)
       return e;
   }
+  if (!fin_done &&
+      (e = timed(net, SSCN_KC_GROUND, st, [&] { return launch_extra(net->bf16, *fin, st); })) != hipSuccess)
+    return e;
   return timed(net, SSCN_KC_WGRAD_REDUCE, st, [&] { return launch_wgrad_reduce(net->bf16, w, n, st); });
 }
 
@@ -1011,6 +1034,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   // reads it, and is computed by that final pass itself (extra task kind 3).
   ExtraTask pending{};  // row 0 of a gradient below, waiting for the next launch
   ExtraTask pool_row0{};  // row 0 of a routed pooling layer's gradient, for the final pass below it
+  ExtraTask deferred_fin{};  // the first layer's final pass, when no launch of the stage loop follows it
   bool routed[MAX_LAYERS] = {};
   for (int s = top; s >= 1; --s) {
     const LayerPlan& L = net->L[s];
@@ -1056,6 +1080,11 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
       const bool writes_row0 = pool_above || s == top;
       if (e == hipSuccess && gemm_below && (L.A > 1 || !writes_row0)) {
         e = rows_below(net, s, st, &fin, true, s >= 2 ? &routed[s - 1] : nullptr);
+      } else if (e == hipSuccess && !gemm_below && s == 1) {
+        // the first layer's final pass: on the weight-gradient launches at the end
+        if (pending.kind) e = timed(net, SSCN_KC_GROUND, st, [&] { return launch_extra(net->bf16, pending, st); });
+        pending = ExtraTask{};
+        deferred_fin = fin;
       } else if (e == hipSuccess) {
         if (fin.kind == 3) {  // the final pass with its row 0 above, as a launch of its own
           if (pending.kind)
@@ -1114,7 +1143,8 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
     f.c_in = P.c_in;
     f.c_out = P.c_out;
   }
-  if (run_wgrads(net, w, nw, st) != hipSuccess) return SSCN_ERR_HIP;
+  // (w[0] is the first convolution's, which the deferred final pass must precede)
+  if (run_wgrads(net, w, nw, st, &deferred_fin, 0) != hipSuccess) return SSCN_ERR_HIP;
   net->backwarded = true;
   return SSCN_OK;
 }

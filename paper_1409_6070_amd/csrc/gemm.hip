@@ -382,7 +382,7 @@ __device__ inline int wgrad_chunks_dev(const WGradArgs& a, int rows, int BK) {
 // One launch serves a group of layers: workgroup tile t belongs to the layer l
 // with tile_beg[l] <= t < tile_beg[l + 1].
 template <typename T, class C>
-__global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp) {
+__global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp, ExtraTask x) {
   constexpr int VE = C::VE, BK = C::BK, LDK = C::LDK, BM = C::BM, BN = C::BN, NT = C::NT;
   constexpr int MV = BM / VE, NV = BN / VE;  // vectors across a slab row
   static_assert(MV * (BK / 4) == NT && NV * (BK / 4) <= NT, "one quad of sites per thread");
@@ -401,8 +401,9 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp) {
   const int qa = tid % NQ, mv = tid / NQ;
   const int qb = tid % NQ, nvv = tid / NQ;
   const bool b_active = tid < NV * NQ;
+  if (run_extra<T>(x)) return;
 
-  for (int t = blockIdx.x; t < grp.tile_beg[grp.n]; t += gridDim.x) {
+  for (int t = blockIdx.x; t < grp.tile_beg[grp.n]; t += own_grid(x)) {
     int l = 0;
     while (l + 1 < grp.n && t >= grp.tile_beg[l + 1]) ++l;
     const WGradArgs& a = grp.L[l];
@@ -679,9 +680,11 @@ GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K) {
   return p;
 }
 
-hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st) {
+hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st, const ExtraTask* extra) {
   // cfg: 0 = 128 x 128 tiles, 1 = 128 x 64
   if (n < 1 || n > MAX_WG_LAYERS) return hipErrorInvalidValue;
+  const ExtraTask x = extra ? *extra : ExtraTask{};
+  if (x.kind && (x.blocks < 1 || (x.kind != 1 && x.kind != 3))) return hipErrorInvalidValue;
   const int BN = cfg == 0 ? 128 : 64;
   WGradGroup g{};
   g.n = n;
@@ -690,17 +693,17 @@ hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipS
     g.L[l] = layers[l];
     g.tile_beg[l + 1] = g.tile_beg[l] + (layers[l].Mpad / 128) * (layers[l].Npad / BN) * layers[l].nchunks;
   }
-  const int grid = std::min(std::max(g.tile_beg[n], 1), device_grid_limit());
+  const int grid = std::min(std::max(g.tile_beg[n], 1), device_grid_limit()) + (x.kind ? x.blocks : 0);
   if (bf16) {
     if (cfg == 0)
-      hipLaunchKernelGGL((k_wgrad<__bf16, C128x128<__bf16>>), dim3(grid), dim3(256), 0, st, g);
+      hipLaunchKernelGGL((k_wgrad<__bf16, C128x128<__bf16>>), dim3(grid), dim3(256), 0, st, g, x);
     else
-      hipLaunchKernelGGL((k_wgrad<__bf16, C128x64<__bf16>>), dim3(grid), dim3(256), 0, st, g);
+      hipLaunchKernelGGL((k_wgrad<__bf16, C128x64<__bf16>>), dim3(grid), dim3(256), 0, st, g, x);
   } else {
     if (cfg == 0)
-      hipLaunchKernelGGL((k_wgrad<float, C128x128<float>>), dim3(grid), dim3(256), 0, st, g);
+      hipLaunchKernelGGL((k_wgrad<float, C128x128<float>>), dim3(grid), dim3(256), 0, st, g, x);
     else
-      hipLaunchKernelGGL((k_wgrad<float, C128x64<float>>), dim3(grid), dim3(256), 0, st, g);
+      hipLaunchKernelGGL((k_wgrad<float, C128x64<float>>), dim3(grid), dim3(256), 0, st, g, x);
   }
   return hipGetLastError();
 }

@@ -217,7 +217,10 @@ hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream
 hipError_t launch_gemm_direct(const GemmArgs& a, int64_t max_rows, hipStream_t st);
 // Weight gradients of n layers that all use tile shape cfg (0: 128 x 128,
 // 1: 128 x 64) in one launch.
-hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st);
+// extra: a ground final pass (ExtraTask kind 1 or 3) riding on the launch; it
+// must not write what the launch's layers read.
+hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st,
+                        const ExtraTask* extra = nullptr);
 
 // part -> dW [A*c_in x c_out] (and db [c_out] when m_ones >= 0) for every layer
 // of the list with nchunks > 1, in one launch.
