@@ -584,7 +584,23 @@ static DropArgs conv_drop(const sscn_net* net, int s) {
 // Dropout on the softmax layer's input (the last level, keyed by sample).
 static DropArgs head_drop(const sscn_net* net) { return drop_args(net, net->d.ell + 1, nullptr); }
 
-static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
+// Whether convolution s runs the pooling layer above it in its GEMM epilogue
+// (GemmArgs::pool_fwd): every site of the convolution must lie in a pooling
+// window (an even grid side), and its plan must be a single-pass tile shape
+// that stages its output.
+static bool pool_fused(const sscn_net* net, int s) {
+  if (s + 1 >= net->nlayers) return false;
+  const LayerPlan& L = net->L[s];
+  const LayerPlan& Lp = net->L[s + 1];
+  if (L.kind != 1 || Lp.kind != 2 || L.S % 2 != 0 || Lp.Cp != L.Cp) return false;
+  const ParamPlan& P = net->P[L.conv_index];
+  return P.pf.ksplit == 1 && gemm_routes(net->bf16, P.pf.cfg);
+}
+
+// Stage s of the forward pass; with fuse_pool a convolution whose pooling
+// layer above pool_fused allows also computes that layer (whose own stage is
+// then skipped).
+static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st, bool fuse_pool = false) {
   const LayerPlan& L = net->L[s];
   const LayerPlan& Lb = net->L[s - 1];
   if (L.kind == 1) {
@@ -617,6 +633,16 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st) {
     g.rows_add = 1;
     g.row_begin = 0;
     set_plan(g, P.pf, P.rows_f, net->gpart);
+    if (fuse_pool && pool_fused(net, s)) {  // rows: the four slots of every pooling window
+      const LayerPlan& Lp = net->L[s + 1];
+      g.pool_fwd = 1;
+      g.pslot = Lp.rules;
+      g.pool_out = Lp.X;
+      g.pool_argmax = Lp.argmax;
+      g.pool_stride = Lp.Cp;
+      g.rows_dev = net->counts + s + 1;
+      return timed_gemm(net, g, 4 * (Lp.cap + 1), st);
+    }
     return timed_gemm(net, g, L.cap + 1, st);
   }
   return timed(net, SSCN_KC_POOL_FWD, st, [&] {
@@ -923,8 +949,10 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   }
   if (timed(net, SSCN_KC_HEAD, st, [&] { return launch_pack_all(net->bf16, pa, st); }) != hipSuccess)
     return SSCN_ERR_HIP;
-  for (int s = 1; s < net->nlayers; ++s)
-    if (forward_stage(net, s, st) != hipSuccess) return SSCN_ERR_HIP;
+  for (int s = 1; s < net->nlayers; ++s) {
+    if (net->L[s].kind == 2 && pool_fused(net, s - 1)) continue;  // computed by the convolution below
+    if (forward_stage(net, s, st, true) != hipSuccess) return SSCN_ERR_HIP;
+  }
   // softmax layer on each sample's top-layer row
   const LayerPlan& Lt = net->L[net->nlayers - 1];
   const ParamPlan& P = net->P[net->nconv];

@@ -164,6 +164,48 @@ __device__ inline void store_staged(const GemmArgs& a, const T* Cs, int m0, int 
   if constexpr (AC >= 0) tile_slot_sums<VE, J, NT, NV, (BM + BN) * C::LDK * (int)sizeof(T) / 4>(acc, lds, a.pr, n0, tm);
 }
 
+// Pooling forward in the epilogue (GemmArgs::pool_fwd): the staged tile's
+// rows are the slots 4 p + f of pooling windows p (m0 is a multiple of 4).
+// Every slot's convolution row Cr is stored (row 0 from slot 0 only: the
+// ground value), then each window's first maximum over its four slots, per
+// channel, goes to the pooling layer with its position.
+template <typename T, class C, int CS>
+__device__ inline void store_pooled(const GemmArgs& a, const T* Cs, const int32_t* Cr, int m0, int n0, int rows) {
+  constexpr int VE = C::VE, BM = C::BM, BN = C::BN, NT = C::NT, NV = BN / VE;
+  typedef typename ArgPack<VE>::W AW;
+  static_assert(BM % 4 == 0, "whole windows per tile");
+  for (int v = threadIdx.x; v < BM * NV; v += NT) {
+    const int r = v / NV, nv = v - r * NV;
+    const int m = m0 + r, n = n0 + nv * VE;
+    const int row = Cr[r];
+    if (m < rows && n < a.out_cols && (row > 0 || m == 0))
+      *(u32x4*)((T*)a.out + (int64_t)row * a.out_stride + n) = *(const u32x4*)(Cs + r * CS + nv * VE);
+  }
+  for (int v = threadIdx.x; v < (BM / 4) * NV; v += NT) {
+    const int pr = v / NV, nv = v - pr * NV;
+    const int m = m0 + 4 * pr, n = n0 + nv * VE;
+    if (m >= rows || n >= a.out_cols) continue;
+    // running first maximum over the four slots (one staged vector at a time)
+    u32x4 out = *(const u32x4*)(Cs + (4 * pr) * CS + nv * VE);
+    AW am = 0;
+#pragma unroll
+    for (int f = 1; f < 4; ++f) {
+      const u32x4 in = *(const u32x4*)(Cs + (4 * pr + f) * CS + nv * VE);
+#pragma unroll
+      for (int j = 0; j < VE; ++j) {
+        const bool gt = Elem<T>::to_f32(((const T*)&in)[j]) > Elem<T>::to_f32(((const T*)&out)[j]);
+        if (gt) {
+          ((T*)&out)[j] = ((const T*)&in)[j];
+          am = (am & ~((AW)0xff << (8 * j))) | ((AW)f << (8 * j));
+        }
+      }
+    }
+    const int64_t p = m / 4;
+    *(u32x4*)((T*)a.pool_out + p * a.pool_stride + n) = out;
+    *(AW*)(a.pool_argmax + p * a.pool_stride + n) = am;
+  }
+}
+
 // Implicit-gather GEMM.  Per tile: the tile's window rows go to LDS once; the
 // next K slab's global loads are issued before the current slab's MFMAs
 // (register prefetch); the output tile is staged in LDS for 16-byte stores.
@@ -176,8 +218,10 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   constexpr int CS = BN + VE;  // staging pitch
   constexpr bool STAGE = stages_tile<C>();
   static_assert(STAGE == (BM * CS <= SMEM), "staging fits");
+  constexpr bool POOL = RAC == POOL_FWD_MODE;
   __shared__ __attribute__((aligned(16))) T smem[SMEM];
   __shared__ int32_t Rs[BM * AMAX];
+  __shared__ int32_t Cr[POOL ? BM : 1];  // pooling forward: the convolution row of each slot
   T* As = smem;
   T* Bs = smem + BM * LDK;
 
@@ -185,7 +229,7 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave / C::WN, wn = wave % C::WN;
   if (run_extra<T>(a.x)) return;
-  const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
+  const int rows = (a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host) * (POOL ? 4 : 1);
   const int span = rows - a.row_begin;
   if (span <= 0) return;
   const int tiles_m = (span + BM - 1) / BM;
@@ -209,12 +253,17 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
 
     if (tid < BM) {  // the tile's window rows: one row per thread, independent loads
       const int m = m0 + tid;
-      const int32_t* rp = a.rmap ? a.rmap + (int64_t)m * A : nullptr;
+      int row = m;  // the output row (pooling forward: the slot's convolution row)
+      if constexpr (POOL) {
+        row = m < rows ? a.pslot[m] : 0;
+        Cr[tid] = row;
+      }
+      const int32_t* rp = a.rmap ? a.rmap + (int64_t)row * A : nullptr;
 #pragma unroll
       for (int f = 0; f < AMAX; ++f) {
         if (f < A) {
           int v = -1;
-          if (m < rows) v = rp ? rp[f] : (f == 0 ? m : -1);
+          if (m < rows) v = rp ? rp[f] : (f == 0 ? row : -1);
           Rs[tid * A + f] = v;
         }
       }
@@ -307,7 +356,10 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
           }
         }
       __syncthreads();
-      store_staged<T, C, CS, RAC>(a, Cs, m0, n0, tm, rows, (float*)smem);
+      if constexpr (POOL)
+        store_pooled<T, C, CS>(a, Cs, Cr, m0, n0, rows);
+      else
+        store_staged<T, C, CS, RAC>(a, Cs, m0, n0, tm, rows, (float*)smem);
     } else {
 #pragma unroll
       for (int i = 0; i < C::TM; ++i)
@@ -584,7 +636,8 @@ static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   const bool timed = a.t_start || a.t_stop;
   // the pooling-backward epilogue has instantiations of its own (its slot sums
   // would otherwise cost every launch registers)
-  void (*kern)(GemmArgs) = !a.route ? k_gemm_gather<T, C, -1>
+  void (*kern)(GemmArgs) = a.pool_fwd ? k_gemm_gather<T, C, POOL_FWD_MODE>
+                           : !a.route ? k_gemm_gather<T, C, -1>
                            : a.route_ac == 4 ? k_gemm_gather<T, C, 4>
                                              : k_gemm_gather<T, C, 0>;
   if (timed)
@@ -614,6 +667,10 @@ static void launch_gemm_t(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
 
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   if (max_rows - a.row_begin <= 0) return hipSuccess;
+  if (a.pool_fwd && (a.route || a.ksplit != 1 || !gemm_routes(bf16, a.cfg) || a.row_begin != 0 || !a.pslot ||
+                     !a.pool_out || !a.pool_argmax || !a.rows_dev ||
+                     (a.epi != EPI_BIAS_RELU && a.epi != EPI_BIAS_LRELU)))
+    return hipErrorInvalidValue;
   if (a.route) {  // pooling backward in the epilogue: one partial per row tile
     const int bm = gemm_bm(bf16, a.cfg);
     if (a.epi != EPI_STORE || a.ksplit != 1 || !gemm_routes(bf16, a.cfg) || (a.route_ac != 0 && a.route_ac != 4) ||

@@ -95,6 +95,68 @@ __device__ inline void store_vectors(const GemmArgs& a, float (*red)[DIRECT_BM][
   if constexpr (AC >= 0) tile_slot_sums<8, J, NT, NV, SK * BM * RP>(acc, &red[0][0][0], a.pr, n0, tm);
 }
 
+// Pooling forward in the epilogue (GemmArgs::pool_fwd): the tile's rows are
+// the slots 4 p + f of pooling windows p.  Each thread forms its 16-byte
+// vectors as the plain epilogue does, stores the slot's convolution row (row 0
+// from slot 0 only) and stages the vector in LDS; then the first maximum over
+// each window's four slots, per channel, goes to the pooling layer with its
+// position.
+template <int SK, int RP>
+__device__ inline void store_pooled_direct(const GemmArgs& a, float (*red)[DIRECT_BM][RP], const float (&bias8)[8],
+                                           int c8e, int m0, int n0, int rows, const int32_t* Cr) {
+  typedef __bf16 T;
+  constexpr int BM = DIRECT_BM, BN = DIRECT_BN, NT = 64 * SK, NV = BN / 8, SP = BN + 8;
+  typedef typename ArgPack<8>::W AW;
+  __shared__ __attribute__((aligned(16))) T Ps[BM * SP];  // the tile's stored values
+  for (int v = threadIdx.x; v < BM * NV; v += NT) {
+    const int r = v / NV, c8 = c8e;
+    const int m = m0 + r, n = n0 + c8;
+    if (m >= rows || n >= a.out_cols) continue;
+    float s[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = 0.f;
+#pragma unroll
+    for (int q = 0; q < SK; ++q) {
+      const f32x4 lo = *(const f32x4*)&red[q][r][c8], hi = *(const f32x4*)&red[q][r][c8 + 4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[e] += lo[e];
+        s[4 + e] += hi[e];
+      }
+    }
+    v4u o;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ((T*)&o)[e] = Elem<T>::from_f32(epi_value<T>(a, s[e], bias8[e]));
+    const int row = Cr[r];
+    if (row > 0 || m == 0) *(v4u*)((T*)a.out + (int64_t)row * a.out_stride + n) = o;
+    *(v4u*)(Ps + r * SP + c8) = o;
+  }
+  __syncthreads();
+  for (int v = threadIdx.x; v < (BM / 4) * NV; v += NT) {
+    const int pr = v / NV, c8 = (v - pr * NV) * 8;
+    const int m = m0 + 4 * pr, n = n0 + c8;
+    if (m >= rows || n >= a.out_cols) continue;
+    // running first maximum over the four slots (one staged vector at a time)
+    v4u out = *(const v4u*)(Ps + (4 * pr) * SP + c8);
+    AW am = 0;
+#pragma unroll
+    for (int f = 1; f < 4; ++f) {
+      const v4u in = *(const v4u*)(Ps + (4 * pr + f) * SP + c8);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const bool gt = Elem<T>::to_f32(((const T*)&in)[j]) > Elem<T>::to_f32(((const T*)&out)[j]);
+        if (gt) {
+          ((T*)&out)[j] = ((const T*)&in)[j];
+          am = (am & ~((AW)0xff << (8 * j))) | ((AW)f << (8 * j));
+        }
+      }
+    }
+    const int64_t p = m / 4;
+    *(v4u*)((T*)a.pool_out + p * a.pool_stride + n) = out;
+    *(AW*)(a.pool_argmax + p * a.pool_stride + n) = am;
+  }
+}
+
 template <int SK, int RAC>
 __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   typedef __bf16 T;
@@ -102,13 +164,15 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   constexpr int BM = DIRECT_BM, BN = DIRECT_BN, NT = 64 * SK;
   constexpr int CH = 3;        // k blocks (32 k each) of loads in flight per wave
   constexpr int RP = BN + 4;   // LDS pitch of the partial sums (floats)
+  constexpr bool POOL = RAC == POOL_FWD_MODE;
   __shared__ int32_t Rs[BM * DIR_AMAX];
   __shared__ __attribute__((aligned(16))) float red[SK][BM][RP];
+  __shared__ int32_t Cr[POOL ? BM : 1];  // pooling forward: the convolution row of each slot
 
   if (run_extra<T>(a.x)) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
+  const int rows = (a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host) * (POOL ? 4 : 1);
   const int span = rows - a.row_begin;
   if (span <= 0) return;
   const int tiles_m = (span + BM - 1) / BM;
@@ -145,7 +209,14 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
       const int r = e / A, f = e - r * A;
       const int m = m0 + r;
       int v = -1;
-      if (m < rows) v = a.rmap ? a.rmap[(int64_t)m * A + f] : (f == 0 ? m : -1);
+      if (m < rows) {
+        int row = m;  // the output row (pooling forward: the slot's convolution row)
+        if constexpr (POOL) {
+          row = a.pslot[m];
+          if (f == 0) Cr[r] = row;
+        }
+        v = a.rmap ? a.rmap[(int64_t)row * A + f] : (f == 0 ? row : -1);
+      }
       Rs[e] = v;
     }
     __syncthreads();
@@ -202,7 +273,9 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
         for (int r = 0; r < 4; ++r) red[w][i * 16 + g * 4 + r][j * 16 + r16] = acc[i][j][r];
     __syncthreads();
 
-    if (epi_stores_T(a.epi)) {
+    if constexpr (POOL) {
+      store_pooled_direct<SK, RP>(a, red, bias8, c8e, m0, n0, rows, Cr);
+    } else if (epi_stores_T(a.epi)) {
       store_vectors<SK, RP, RAC, PRE>(a, red, bias8, c8e, m0, n0, tm, rows, pre);
     } else {
       for (int e = tid; e < BM * BN; e += NT) {
@@ -224,7 +297,10 @@ static void launch_direct_sk(const GemmArgs& a, int64_t max_rows, hipStream_t st
   const int64_t span = max_rows - a.row_begin;
   const int64_t tiles = ((span + DIRECT_BM - 1) / DIRECT_BM) * (a.Npad / DIRECT_BN);
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), 2048) + (a.x.kind ? a.x.blocks : 0);
-  void (*kern)(GemmArgs) = !a.route ? k_gemm_direct<SK, -1> : a.route_ac == 4 ? k_gemm_direct<SK, 4> : k_gemm_direct<SK, 0>;
+  void (*kern)(GemmArgs) = a.pool_fwd ? k_gemm_direct<SK, POOL_FWD_MODE>
+                           : !a.route ? k_gemm_direct<SK, -1>
+                           : a.route_ac == 4 ? k_gemm_direct<SK, 4>
+                                             : k_gemm_direct<SK, 0>;
   if (a.t_start || a.t_stop)
     hipExtLaunchKernelGGL(kern, dim3(grid), dim3(64 * SK), 0, st, a.t_start, a.t_stop, 0, a);
   else

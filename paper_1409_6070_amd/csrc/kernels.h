@@ -141,7 +141,24 @@ struct GemmArgs {
   int32_t route;
   int32_t route_ac;
   GroundArgs pr;
+  // Pooling forward in the epilogue (pool_fwd = 1; a convolution with the
+  // bias-rectifier epilogue, ksplit == 1, a tile shape that stages its output):
+  // the GEMM rows are the slots 4 p + f of the pooling windows, rows = 4 (n_pool
+  // + 1) from rows_dev / rows_add (the pooling layer's count); slot q computes
+  // the convolution row pslot[q] (the pooling layer's window list; row 0 for an
+  // inactive location, which then gives the ground value) and stores it (row 0
+  // from slot 0 only), and each window's first maximum goes to pool_out /
+  // pool_argmax (row stride pool_stride).
+  int32_t pool_fwd;
+  const int32_t* pslot;
+  void* pool_out;
+  uint8_t* pool_argmax;
+  int32_t pool_stride;
 };
+
+// Template value of the gather GEMMs for the pooling-forward epilogue (the
+// others: -1 plain, 0 or 4 the pooling backward with that window count).
+constexpr int POOL_FWD_MODE = -2;
 
 // Whether a tile shape stages its output tile through LDS (16-byte stores), as
 // the pooling backward in the epilogue needs.
