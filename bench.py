@@ -81,7 +81,10 @@ def gemm_work(cfg, sizes, infer=False, e=2, routed=True):
     layer also runs that layer's backward in its epilogue: + the convolution
     below's output read and delta written (n_c C e each), the argmax bytes
     (n_{s-1} C), the pooling windows (16 n_{s-1}) and, above the first layer,
-    the convolution's window lists (n_c A_c 4).
+    the convolution's window lists (n_c A_c 4).  A convolution with a pooling
+    layer above computes that layer in its epilogue (even grid sides): + the
+    pooling windows read (16 (n_p + 1)), the pooled rows and argmax written
+    (n_p C_out (e + 1)).
     """
     fwd = dgrad = 0.0
     fbytes = dbytes = 0.0
@@ -93,6 +96,9 @@ def gemm_work(cfg, sizes, infer=False, e=2, routed=True):
         w = A * ci * co * e
         fwd += 2.0 * (n + 1) * A * ci * co
         fbytes += (nb + 1) * ci * e + (n + 1) * (A * 4 if A > 1 else 0) + (n + 1) * co * e + w
+        if s < len(shapes) and shapes[s][0] == "pool":  # the pooling layer above, in the epilogue
+            npool = sizes[s + 1]
+            fbytes += 16 * (npool + 1) + npool * co * (e + 1)
         if s > 1:
             dgrad += 2.0 * nb * A * co * ci
             mask = nb * ci * e if shapes[s - 2][0] == "conv" else 0
@@ -337,8 +343,8 @@ def main():
     roofline = {
         "kernel": ("gather-GEMM class: k_gemm_gather (LDS-tiled) and k_gemm_direct (direct-operand) implicit-gather "
                    "MFMA GEMMs; " + ("conv forward, softmax layer logits" if infer else
-                                     "conv forward, conv input gradient (with the pooling backward in its "
-                                     "epilogue), softmax layer")),
+                                     "conv forward (with the pooling forward in its epilogue), conv input "
+                                     "gradient (with the pooling backward in its epilogue), softmax layer")),
         "bound": "mfma", "achieved": round(achieved / 1e12, 3), "peak": peak / 1e12, "unit": "TFLOP/s",
         "frac": round(achieved / peak, 5), "traffic": traffic,
         "launches_per_step": g_launches / args.steps, "avg_launch_us": round(avg_launch_s * 1e6, 3),
