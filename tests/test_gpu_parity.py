@@ -147,6 +147,31 @@ def test_stage_kernels_on_oracle_inputs(dtype):
         assert e <= TOL[dtype], f"backward stage {s}: {e}"
 
 
+@pytest.mark.parametrize("name,dtype", [("deepcnet4_20_strokes_b8", "f32"), ("deepcnet4_20_strokes_b8", "bf16"),
+                                        ("deepcnet5_50_strokes_b100", "bf16"), ("deepcnin5_50_strokes_b100", "bf16")])
+def test_fused_pool_forward_matches_stage_kernels(name, dtype):
+    """The full forward pass runs each pooling layer in the epilogue of the convolution below it
+    (GEMM rows in pooling-window order); the per-stage entry point runs the separate kernels.
+    Both compute every row's dot products in the same order, so every layer's features and every
+    argmax must agree bit for bit."""
+    cfg = get_config(name)
+    b, Ws, bs, labels = _config_case(cfg, dtype)
+    log(f"[fused-pool] {name} {dtype}")
+    pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, dtype,
+                run_oracle=False, arch=cfg.arch).run_gpu()
+    n = len(pair.counts)
+    fused = [pair.view(s) for s in range(n)]
+    fused = [(v["X"].copy(), None if "argmax" not in v else v["argmax"].copy()) for v in fused]
+    for s in range(1, n):
+        pair.net.forward_stage(s)
+    torch.cuda.synchronize()
+    for s in range(1, n):
+        v = pair.view(s)
+        np.testing.assert_array_equal(v["X"], fused[s][0], err_msg=f"features layer {s}")
+        if fused[s][1] is not None:
+            np.testing.assert_array_equal(v["argmax"], fused[s][1], err_msg=f"argmax layer {s}")
+
+
 def test_rulebook_path_counts_full_grid():
     """Fully active 96x96 input of DeepCNet(5,.): routes through the GPU window lists (Section 2.6)."""
     ell, N = 5, 96
