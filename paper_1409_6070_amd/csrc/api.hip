@@ -509,6 +509,15 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   }
   wk.base[net->nlayers] = acc;
   wk.total = acc;
+  // composite windows: a valid F x F convolution widens the square by F - 1
+  // steps of the layer below, a 2 x 2 stride-2 pooling by one step and doubles
+  // the step
+  a.rf_a[0] = 1, a.rf_r[0] = 1;
+  for (int s = 1; s < net->nlayers; ++s) {
+    const LayerPlan& L = net->L[s];
+    a.rf_a[s] = L.kind == 2 ? 2 * a.rf_a[s - 1] : a.rf_a[s - 1];
+    a.rf_r[s] = a.rf_r[s - 1] + a.rf_a[s - 1] * (L.F - 1);
+  }
   a.counts = net->counts;
   // this build's input bitmap and error word, and the next build's (cleared
   // here); err[1] is the loss counter, err[0] spare

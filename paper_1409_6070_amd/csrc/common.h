@@ -127,6 +127,10 @@ struct RulebookArgs {
   LayerBits L[MAX_LAYERS];
   int32_t kind[MAX_LAYERS];  // per layer s >= 1: 1 conv (F = 3, 2 or 1), 2 pool
   int32_t F[MAX_LAYERS];
+  // composite window of layer s on the input grid: output (Y, X) is active iff
+  // an input site lies in [rf_a Y, rf_a Y + rf_r - 1] x [rf_a X, rf_a X + rf_r - 1]
+  int32_t rf_a[MAX_LAYERS];
+  int32_t rf_r[MAX_LAYERS];
   int32_t* rules[MAX_LAYERS];    // layer s >= 1: [(cap_s+1) * A]
   int32_t* rules_t[MAX_LAYERS];  // layer s >= 1: conv [(cap_{s-1}+1) * A], pool [cap_{s-1}+1]
   int32_t* counts;               // [nlayers]

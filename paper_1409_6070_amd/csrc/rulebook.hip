@@ -11,11 +11,16 @@
 //
 // Active sets follow Section 2.3 and Figure 2: a convolution output is active
 // when any location of its FxF window below is active, a pooling output when
-// any of its 2x2 stride-2 window is.  Both are computed bit-parallel on whole
-// 64-bit words, one wave per sample with the sample's bitmaps in LDS; a second
-// launch turns the per-sample counts into sample offsets (a last-workgroup
-// pattern would need a device-scope release fence, which costs more here than
-// the launch).
+// any of its 2x2 stride-2 window is.  Composed down to the input, the windows
+// of layer s cover one contiguous square: output (Y, X) is active iff an input
+// site lies in [a Y, a Y + r - 1]^2, where a convolution adds a (F - 1) to r and
+// a pooling layer adds a to r and doubles a (r >= a throughout, so the union of
+// the windows below is contiguous).  Every layer's bitmap therefore comes
+// straight from the input bitmap, one wave per (sample, layer), with no chain
+// through the layers: the rows of each square are ORed word-parallel, then
+// each output bit tests its column range.  A second launch turns the
+// per-sample counts into sample offsets (a last-workgroup pattern would need a
+// device-scope release fence, which costs more here than the launch).
 //
 // Builds alternate between two input bitmaps (and error words): each build
 // inserts into one that is all zero and clears the other for the next build,
@@ -51,17 +56,6 @@ __global__ void __launch_bounds__(256) k_rb_insert(const int32_t* __restrict__ c
   unsigned long long* w = (unsigned long long*)&bits0[((int64_t)b * N + y) * Wd + (x >> 6)];
   unsigned long long old = atomicOr(w, bit);
   if (old & bit) atomicOr(err, ERRBIT_DUP);
-}
-
-// Keep the even-numbered bits of a 64-bit word, packed into the low 32 bits.
-__device__ inline uint64_t compress_even_bits(uint64_t v) {
-  v &= 0x5555555555555555ull;
-  v = (v | (v >> 1)) & 0x3333333333333333ull;
-  v = (v | (v >> 2)) & 0x0F0F0F0F0F0F0F0Full;
-  v = (v | (v >> 4)) & 0x00FF00FF00FF00FFull;
-  v = (v | (v >> 8)) & 0x0000FFFF0000FFFFull;
-  v = (v | (v >> 16)) & 0x00000000FFFFFFFFull;
-  return v;
 }
 
 __device__ inline uint64_t row_mask_word(int w, int S) {
@@ -122,90 +116,83 @@ __device__ inline int div_rcp_d(int64_t k, int d) {
   return (int)q;
 }
 
-// Output word idx of an F x F valid convolution's active set, from the bitmap
-// below in LDS.
-template <int F>
-__device__ inline uint64_t conv_word(const uint64_t* cur, int idx, int Wo, float rcp_wo, int Wi, int So) {
-  const int Y = div_rcp(idx, Wo, rcp_wo), w = idx - Y * Wo;
-  uint64_t acc = 0;
-#pragma unroll
-  for (int dy = 0; dy < F; ++dy) {
-    const uint64_t* row = cur + (Y + dy) * Wi;
-    const uint64_t lo = row[w];
-    const uint64_t hi = (w + 1 < Wi) ? row[w + 1] : 0ull;
-    acc |= lo;
-#pragma unroll
-    for (int dx = 1; dx < F; ++dx) acc |= (lo >> dx) | (hi << (64 - dx));
-  }
-  return acc & row_mask_word(w, So);
-}
-
-// Every layer's bitmap from the input bitmap, one wave (workgroup) per sample;
-// workgroups b >= batch only clear.  Each workgroup also clears its share of
-// the next build's input bitmap.
+// Layer s of sample b, b = blockIdx / nlayers, s = blockIdx % nlayers (one
+// wave): the sample's input bitmap goes to LDS; each lane takes whole output
+// rows, ORs the input rows of their squares into its own row buffer, and sets
+// each output bit whose column range of that row holds a set bit (a word-
+// parallel dilation when a = 1).  Then the layer's word prefix and count, as
+// the layer-by-layer definition gives them.  Every workgroup also clears its
+// share of the next build's input bitmap; workgroups of samples b >= batch only
+// clear.
 __global__ void __launch_bounds__(64) k_rb_bitmaps(RulebookArgs a, int32_t max_words) {
   extern __shared__ uint64_t lds[];
-  uint64_t* cur = lds;
-  uint64_t* nxt = lds + max_words;
-  const int b = blockIdx.x;
+  const LayerBits& L0 = a.L[0];
+  const int S0 = L0.S, W0 = L0.Wd, nw0 = S0 * W0;
+  uint64_t* in = lds;                      // [S0][W0]
+  uint64_t* out = lds + max_words;         // [So][Wo]
+  uint64_t* rowbuf = lds + 2 * max_words;  // [64][W0]
+  const int s = (int)blockIdx.x % a.nlayers, b = (int)blockIdx.x / a.nlayers;
   const int t = threadIdx.x;
   {
-    const int64_t nw0 = (int64_t)a.L[0].S * a.L[0].Wd;
-    for (int64_t smp = b; smp < a.batch_max; smp += gridDim.x)
-      for (int64_t w = t; w < nw0; w += 64) a.bits0_next[smp * nw0 + w] = 0ull;
-    if (b == 0 && t == 0) *a.err_next = 0;
+    const int64_t total = (int64_t)a.batch_max * nw0;
+    for (int64_t i = (int64_t)blockIdx.x * 64 + t; i < total; i += (int64_t)gridDim.x * 64) a.bits0_next[i] = 0ull;
+    if (blockIdx.x == 0 && t == 0) *a.err_next = 0;
   }
-  if (b < a.batch) {
-    {  // layer 0
-      const LayerBits& L = a.L[0];
-      const int nw = L.S * L.Wd;
-      const uint64_t* src = L.bits + (int64_t)b * nw;
-      for (int w = t; w < nw; w += 64) cur[w] = src[w];
-      __syncthreads();
-      const int tot = wave_popcount_scan(cur, nw, L.wpre + (int64_t)b * nw);
-      if (t == 0) L.scount[b] = tot;
+  if (b >= a.batch) return;
+  const uint64_t* src = L0.bits + (int64_t)b * nw0;
+  for (int w = t; w < nw0; w += 64) in[w] = src[w];
+  __syncthreads();
+  if (s == 0) {  // the input layer: its prefix and count only
+    const int tot = wave_popcount_scan(in, nw0, L0.wpre + (int64_t)b * nw0);
+    if (t == 0) L0.scount[b] = tot;
+    return;
+  }
+  const LayerBits& Lo = a.L[s];
+  const int Wo = Lo.Wd, So = Lo.S, nwo = So * Wo;
+  const int ra = a.rf_a[s], rr = a.rf_r[s];
+  uint64_t* row = rowbuf + t * W0;
+  for (int Y = t; Y < So; Y += 64) {
+    const int y_end = min(ra * Y + rr, S0);
+    for (int w = 0; w < W0; ++w) {  // OR of the square's input rows
+      uint64_t v = 0;
+#pragma unroll 4
+      for (int y = ra * Y; y < y_end; ++y) v |= in[y * W0 + w];
+      row[w] = v;
     }
-    for (int s = 1; s < a.nlayers; ++s) {
-      const LayerBits& Li = a.L[s - 1];
-      const LayerBits& Lo = a.L[s];
-      const int nwo = Lo.S * Lo.Wd;
-      const float rcp_wo = 1.f / (float)Lo.Wd;
-      if (a.kind[s] == 1) {  // convolution, F x F valid window
-        const int F = a.F[s];
-        for (int idx = t; idx < nwo; idx += 64)
-          nxt[idx] = F == 3   ? conv_word<3>(cur, idx, Lo.Wd, rcp_wo, Li.Wd, Lo.S)
-                     : F == 2 ? conv_word<2>(cur, idx, Lo.Wd, rcp_wo, Li.Wd, Lo.S)
-                              : conv_word<1>(cur, idx, Lo.Wd, rcp_wo, Li.Wd, Lo.S);
-      } else {  // 2x2 stride-2 pooling
-        for (int idx = t; idx < nwo; idx += 64) {
-          const int Y = div_rcp(idx, Lo.Wd, rcp_wo), w = idx - Y * Lo.Wd;
-          const uint64_t* r0 = cur + (2 * Y) * Li.Wd;
-          const uint64_t* r1 = r0 + Li.Wd;
-          uint64_t p0 = 0, p1 = 0;
-          if (2 * w < Li.Wd) {
-            const uint64_t r = r0[2 * w] | r1[2 * w];
-            p0 = compress_even_bits(r | (r >> 1));
-          }
-          if (2 * w + 1 < Li.Wd) {
-            const uint64_t r = r0[2 * w + 1] | r1[2 * w + 1];
-            p1 = compress_even_bits(r | (r >> 1));
-          }
-          nxt[idx] = (p0 | (p1 << 32)) & row_mask_word(w, Lo.S);
-        }
+    if (ra == 1) {  // output bit X covers input bits X .. X + rr - 1
+      for (int w = 0; w < Wo; ++w) {
+        const uint64_t lo = row[w], hi = w + 1 < W0 ? row[w + 1] : 0ull;
+        uint64_t acc = lo;
+        for (int d = 1; d < rr; ++d) acc |= (lo >> d) | (hi << (64 - d));
+        out[Y * Wo + w] = acc & row_mask_word(w, So);
       }
-      __syncthreads();
-      uint64_t* dst = Lo.bits + (int64_t)b * nwo;
-      for (int w = t; w < nwo; w += 64) dst[w] = nxt[w];
-      const int tot = wave_popcount_scan(nxt, nwo, Lo.wpre + (int64_t)b * nwo);
-      if (t == 0) Lo.scount[b] = tot;
-      uint64_t* tmp = cur;
-      cur = nxt;
-      nxt = tmp;
-      __syncthreads();
+    } else {  // output bit X covers input bits [a X, a X + rr)
+      for (int w = 0; w < Wo; ++w) {
+        uint64_t acc = 0;
+        const int x_end = min(So, (w + 1) * 64);
+#pragma unroll 4
+        for (int x = w * 64; x < x_end; ++x) {
+          const int lo = ra * x, hi = min(lo + rr, S0);
+          const int wl = lo >> 6, wh = (hi - 1) >> 6;
+          uint64_t any = 0;
+          for (int q = wl; q <= wh; ++q) {
+            uint64_t v = row[q];
+            if (q == wl) v &= ~0ull << (lo & 63);
+            if (q == wh && (hi & 63)) v &= (1ull << (hi & 63)) - 1ull;
+            any |= v;
+          }
+          acc |= (any ? 1ull : 0ull) << (x - w * 64);
+        }
+        out[Y * Wo + w] = acc;
+      }
     }
   }
+  __syncthreads();
+  uint64_t* dst = Lo.bits + (int64_t)b * nwo;
+  for (int w = t; w < nwo; w += 64) dst[w] = out[w];
+  const int tot = wave_popcount_scan(out, nwo, Lo.wpre + (int64_t)b * nwo);
+  if (t == 0) Lo.scount[b] = tot;
 }
-
 
 // Sample offsets and layer totals: one wave per layer, an exclusive scan of the
 // per-sample counts.
@@ -410,8 +397,8 @@ hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const Rul
   if (a.n > 0)
     hipLaunchKernelGGL(k_rb_insert, dim3((a.n + 255) / 256), dim3(256), 0, st, a.coords, a.n, a.batch, L0.S, L0.Wd,
                        L0.bits, a.err);
-  const size_t lds = (size_t)2 * max_words * sizeof(uint64_t);
-  hipLaunchKernelGGL(k_rb_bitmaps, dim3(std::max(a.batch, 1)), dim3(64), lds, st, a, max_words);
+  const size_t lds = (size_t)(2 * max_words + 64 * L0.Wd) * sizeof(uint64_t);
+  hipLaunchKernelGGL(k_rb_bitmaps, dim3(std::max(a.batch, 1) * a.nlayers), dim3(64), lds, st, a, max_words);
   hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
   int gs = (int)std::min<int64_t>((wk.total + 255) / 256, 2048);
   if (gs < 1) gs = 1;
