@@ -65,7 +65,10 @@ def gemm_work(cfg, sizes, infer=False, e=2, routed=True):
     """Algorithmic FLOPs of one step, per kernel class, and the compulsory bytes of the
     gather-GEMM launches (e bytes per stored element).
 
-    gather_gemm: convolution forward 2(n_s+1)A C_in C_out per stage, convolution
+    gather_gemm: convolution forward 2(n_s+1)A C_in C_out per stage (except a
+    layer with at most 32 products per output and one 16-byte vector of input
+    channels, the first layer of a one- or three-channel input: conv_narrow,
+    the vector-ALU kernel), convolution
     input gradient 2 n_{s-1} A C_out C_in per stage s > 1 (the first layer's
     input gradient is not part of a training step), softmax layer forward and
     dh, 2 B C_last classes each.
@@ -86,19 +89,23 @@ def gemm_work(cfg, sizes, infer=False, e=2, routed=True):
     pooling windows read (16 (n_p + 1)), the pooled rows and argmax written
     (n_p C_out (e + 1)).
     """
-    fwd = dgrad = 0.0
+    fwd = dgrad = narrow = 0.0
     fbytes = dbytes = 0.0
     shapes = layer_shapes(cfg)
+    ve = 16 // e
     for s, (kind, A, ci, co) in enumerate(shapes, start=1):
         if kind != "conv":
             continue
         n, nb = sizes[s], sizes[s - 1]
         w = A * ci * co * e
-        fwd += 2.0 * (n + 1) * A * ci * co
-        fbytes += (nb + 1) * ci * e + (n + 1) * (A * 4 if A > 1 else 0) + (n + 1) * co * e + w
-        if s < len(shapes) and shapes[s][0] == "pool":  # the pooling layer above, in the epilogue
-            npool = sizes[s + 1]
-            fbytes += 16 * (npool + 1) + npool * co * (e + 1)
+        if A > 1 and ci <= ve and A * ci <= 32:  # few input channels: the vector-ALU kernel, not a GEMM
+            narrow += 2.0 * (n + 1) * A * ci * co
+        else:
+            fwd += 2.0 * (n + 1) * A * ci * co
+            fbytes += (nb + 1) * ci * e + (n + 1) * (A * 4 if A > 1 else 0) + (n + 1) * co * e + w
+            if s < len(shapes) and shapes[s][0] == "pool":  # the pooling layer above, in the epilogue
+                npool = sizes[s + 1]
+                fbytes += 16 * (npool + 1) + npool * co * (e + 1)
         if s > 1:
             dgrad += 2.0 * nb * A * co * ci
             mask = nb * ci * e if shapes[s - 2][0] == "conv" else 0
@@ -112,9 +119,10 @@ def gemm_work(cfg, sizes, infer=False, e=2, routed=True):
     hf_bytes = B * C * e + 4 * B + 4 * B * K + C * K * e
     hd_bytes = B * K * e + 4 * B * C + C * K * e
     if infer:  # forward only: conv forward and the logits
-        return {"gather_gemm": fwd + head, "wgrad": 0.0, "conv_total": fwd, "gather_gemm_bytes": fbytes + hf_bytes}
-    return {"gather_gemm": fwd + dgrad + 2 * head, "wgrad": fwd + head, "conv_total": 2 * fwd + dgrad,
-            "gather_gemm_bytes": fbytes + dbytes + hf_bytes + hd_bytes}
+        return {"gather_gemm": fwd + head, "wgrad": 0.0, "conv_narrow": narrow, "conv_total": fwd + narrow,
+                "gather_gemm_bytes": fbytes + hf_bytes}
+    return {"gather_gemm": fwd + dgrad + 2 * head, "wgrad": fwd + narrow + head, "conv_narrow": narrow,
+            "conv_total": 2 * (fwd + narrow) + dgrad, "gather_gemm_bytes": fbytes + dbytes + hf_bytes + hd_bytes}
 
 
 def read_traffic(kernel, dtype, workload):

@@ -277,7 +277,11 @@ typedef enum {
                              pooling layer; ground-row input gradient        */
   SSCN_KC_DROPOUT = 8,    /* dropped copies of the dropout levels' inputs      */
   SSCN_KC_SGD = 9,        /* the parameter update of sscn_sgd_step             */
-  SSCN_KC_COUNT = 10
+  SSCN_KC_CONV_NARROW = 10,/* convolution forward with few input channels (at most
+                             32 products per output, e.g. the first layer of a
+                             one-channel input) on the vector ALUs, with the
+                             pooling forward above it                        */
+  SSCN_KC_COUNT = 11
 } sscn_kernel_class;
 
 /* While enabled, every launch of a kernel whose class bit (1 << class) is set

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsscn.so")
-SOURCES = ["rulebook.hip", "gemm.hip", "gemm_direct.hip", "pool.hip", "head.hip", "dropout.hip", "encode.hip", "sgd.hip", "api.hip"]
+SOURCES = ["rulebook.hip", "gemm.hip", "gemm_direct.hip", "conv_narrow.hip", "pool.hip", "head.hip", "dropout.hip", "encode.hip", "sgd.hip", "api.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

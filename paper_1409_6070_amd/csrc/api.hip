@@ -642,6 +642,7 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st, bool fuse_
     g.rows_add = 1;
     g.row_begin = 0;
     set_plan(g, P.pf, P.rows_f, net->gpart);
+    int64_t max_rows = L.cap + 1;
     if (fuse_pool && pool_fused(net, s)) {  // rows: the four slots of every pooling window
       const LayerPlan& Lp = net->L[s + 1];
       g.pool_fwd = 1;
@@ -650,9 +651,12 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st, bool fuse_
       g.pool_argmax = Lp.argmax;
       g.pool_stride = Lp.Cp;
       g.rows_dev = net->counts + s + 1;
-      return timed_gemm(net, g, 4 * (Lp.cap + 1), st);
+      max_rows = 4 * (Lp.cap + 1);
     }
-    return timed_gemm(net, g, L.cap + 1, st);
+    if (conv_narrow_ok(net->bf16, g, Lb.C))  // few input channels: no GEMM
+      return timed(net, SSCN_KC_CONV_NARROW, st,
+                   [&] { return launch_conv_narrow(net->bf16, g, Lb.C, max_rows, st); });
+    return timed_gemm(net, g, max_rows, st);
   }
   return timed(net, SSCN_KC_POOL_FWD, st, [&] {
     return launch_pool_fwd(net->bf16, Lb.X, Lb.Cp, L.rules, L.X, L.Cp, L.argmax, L.Cp, net->counts + s, L.cap, st);

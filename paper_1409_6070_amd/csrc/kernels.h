@@ -232,6 +232,14 @@ inline int wgrad_bn(int c_out) { return (c_out + 127) / 128 * 128 <= (c_out + 63
 
 hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st);
 hipError_t launch_gemm_direct(const GemmArgs& a, int64_t max_rows, hipStream_t st);
+// Convolution forward on the vector ALUs for layers with few input channels:
+// at most NARROW_KMAX products per output (A * cin, 1 <= cin <= 4, within one
+// 16-byte vector of input channels), a window list, the bias-rectifier epilogue,
+// optionally the pooling forward above (GemmArgs::pool_fwd, max_rows then counting the
+// slots).  conv_narrow_ok tells whether a launch qualifies.
+constexpr int NARROW_KMAX = 32;
+bool conv_narrow_ok(bool bf16, const GemmArgs& a, int cin);
+hipError_t launch_conv_narrow(bool bf16, const GemmArgs& a, int cin, int64_t max_rows, hipStream_t st);
 // Weight gradients of n layers that all use tile shape cfg (0: 128 x 128,
 // 1: 128 x 64) in one launch.
 // extra: a ground final pass (ExtraTask kind 1 or 3) riding on the launch; it

@@ -36,7 +36,7 @@ EXPORTED = [
     "sscn_set_dropout", "sscn_philox4x32_10", "sscn_sgd_step", "sscn_encode_workspace_bytes", "sscn_encode_strokes",
 ]
 KERNEL_CLASSES = ["rulebook", "gather_gemm", "wgrad", "wgrad_reduce", "pool_fwd", "pool_bwd", "head", "ground",
-                  "dropout", "sgd"]
+                  "dropout", "sgd", "conv_narrow"]
 
 
 class SSCNError(RuntimeError):

@@ -172,6 +172,29 @@ def test_fused_pool_forward_matches_stage_kernels(name, dtype):
             np.testing.assert_array_equal(v["argmax"], fused[s][1], err_msg=f"argmax layer {s}")
 
 
+@pytest.mark.parametrize("c_in,narrow", [(1, True), (2, True), (3, True), (9, False)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_first_layer_kernel_choice(c_in, narrow, dtype):
+    """A first layer with at most 32 products per output (3 x 3 window, c_in <= 3) runs on the
+    vector-ALU kernel, a wider one as a gather GEMM; either way its output equals the oracle's
+    (the per-stage entry point recomputes the layer in place, so it must reproduce the pass's bits)."""
+    coords, feats = _sparse_case(40 + c_in, 2, 3, 0.15, c_in)
+    Ws, bs = he_params(2, 6, c_in, 5, 140 + c_in)
+    labels = random_labels(3, 5, 240 + c_in)
+    log(f"[first-layer] c_in={c_in} {dtype} n={len(coords)}")
+    pair = Pair(2, 6, c_in, 5, 3, coords, feats, Ws, bs, labels, dtype).run_gpu()
+    before = pair.view(1)["X"].copy()
+    pair.net.timing(["conv_narrow", "gather_gemm"])
+    pair.net.forward_stage(1)
+    torch.cuda.synchronize()
+    n_narrow, _ = pair.net.timing_collect("conv_narrow")
+    n_gemm, _ = pair.net.timing_collect("gather_gemm")
+    pair.net.timing([])
+    assert (n_narrow, n_gemm) == ((1, 0) if narrow else (0, 1))
+    np.testing.assert_array_equal(pair.view(1)["X"], before)
+    check_values(pair)
+
+
 def test_rulebook_path_counts_full_grid():
     """Fully active 96x96 input of DeepCNet(5,.): routes through the GPU window lists (Section 2.6)."""
     ell, N = 5, 96
