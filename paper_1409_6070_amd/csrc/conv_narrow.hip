@@ -196,7 +196,7 @@ void* narrow_kernel(bool pool) {
 
 bool conv_narrow_ok(bool bf16, const GemmArgs& a, int cin) {
   const int VE = bf16 ? 8 : 4;
-  return a.rmap && a.A >= 1 && a.A <= NARROW_AMAX && cin >= 1 && cin <= 4 && cin <= VE &&
+  return a.rmap && a.src && a.Bt && a.out && a.A >= 1 && a.A <= NARROW_AMAX && cin >= 1 && cin <= 4 && cin <= VE &&
          a.A * cin <= NARROW_KMAX && a.cseg >= VE && a.cseg % VE == 0 && a.src_stride % VE == 0 &&
          a.out_cols % VE == 0 && a.out_stride % VE == 0 && a.ksplit == 1 && !a.route && a.row_begin == 0 &&
          !a.x.kind && (a.epi == EPI_BIAS_RELU || a.epi == EPI_BIAS_LRELU) &&

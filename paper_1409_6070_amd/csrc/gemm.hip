@@ -391,6 +391,7 @@ __global__ void __launch_bounds__(256) k_gemm_splitk_reduce(GemmArgs a) {
     const int64_t m = a.row_begin + t / quads;
     const int n = (int)(t % quads) * 4;
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
     for (int ks = 0; ks < a.ksplit; ++ks) s += *(const f32x4*)(a.part + ((int64_t)ks * a.part_rows + m) * a.Npad + n);
 #pragma unroll
     for (int e = 0; e < 4; ++e)

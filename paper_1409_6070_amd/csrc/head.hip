@@ -204,6 +204,8 @@ __global__ void __launch_bounds__(256) k_head_backward(HeadBwdArgs h, ExtraTask 
       const int b = p * 8 + sl + 4 * q;
       if (b >= h.batch) break;
       float g = 0.f;
+      // unrolled so that several partials' loads are in flight; the sum keeps split order
+#pragma unroll 4
       for (int ks = 0; ks < h.ksplit; ++ks) g += h.dh_part[ks * h.ks_stride + (int64_t)b * h.dh_stride + c];
       if (h.drop.on) g *= drop_factor(h.drop, (uint32_t)b, c);
       const int r = h.head_rows[b];
