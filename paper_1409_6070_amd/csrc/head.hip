@@ -8,21 +8,25 @@
 namespace sscn {
 
 // X0[perm[i]][c] = feats[i][c] (zero padding columns); row 0 = 0, the input
-// ground state.  Workgroup b of nb.
+// ground state.  One 16-byte vector of a row per item (cp0 is a multiple of
+// the vector width); workgroup b of nb.
 template <typename T>
 __device__ inline void scatter_input_part(const T* __restrict__ feats, int32_t n, int32_t c_in,
                                           const int32_t* __restrict__ perm, T* X0, int32_t cp0, int b, int nb) {
-  const int64_t total = (int64_t)(n + 1) * cp0;
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  constexpr int VE = Elem<T>::VE;
+  const int nv = cp0 / VE;
+  const int64_t total = (int64_t)(n + 1) * nv;
   for (int64_t t = (int64_t)b * blockDim.x + threadIdx.x; t < total; t += (int64_t)nb * blockDim.x) {
-    const int64_t i = t / cp0;
-    const int c = (int)(t - i * cp0);
-    if (i == n) {  // the ground row
-      X0[c] = Elem<T>::from_f32(0.f);
-      continue;
-    }
-    const int r = perm[i];
-    if (r < 1) continue;  // rejected site
-    X0[(int64_t)r * cp0 + c] = (c < c_in) ? feats[i * c_in + c] : Elem<T>::from_f32(0.f);
+    const int64_t i = t / nv;
+    const int c0 = (int)(t - i * nv) * VE;
+    const int r = i == n ? 0 : perm[i];  // item n: the ground row
+    if (i < n && r < 1) continue;        // rejected site
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < VE; ++e)
+      ((T*)&o)[e] = (i < n && c0 + e < c_in) ? feats[i * c_in + c0 + e] : Elem<T>::from_f32(0.f);
+    *(u32x4*)(X0 + (int64_t)r * cp0 + c0) = o;
   }
 }
 
@@ -73,26 +77,49 @@ __global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
     const int tiles_k = j.Kpad / PACK_K;
     const int t = g - pa.tile_beg[ji];
     const int n0 = (t / tiles_k) * PACK_N, k0 = (t % tiles_k) * PACK_K;
+    // every thread moves PACK_K * PACK_N / 256 elements; their loads are issued
+    // together (clamped index, selected value), then stored
+    constexpr int PER = PACK_K * PACK_N / 256;
+    T v[PER];
     if (j.mode == 0) {
-      for (int i = threadIdx.x; i < PACK_K * PACK_N; i += 256) {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int i = (int)threadIdx.x + u * 256;
         const int kk = i / PACK_N, nn = i % PACK_N;
         const int k = k0 + kk, n = n0 + nn;
         const int f = k / j.cp_in, c = k - f * j.cp_in;
-        tile[kk][nn] = (f < j.A && c < j.c_in && n < j.c_out) ? W[((int64_t)f * j.c_in + c) * j.c_out + n] : zero;
+        const bool ok = f < j.A && c < j.c_in && n < j.c_out;
+        const T w = W[ok ? ((int64_t)f * j.c_in + c) * j.c_out + n : 0];
+        v[u] = ok ? w : zero;
+      }
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int i = (int)threadIdx.x + u * 256;
+        tile[i / PACK_N][i % PACK_N] = v[u];
       }
       __syncthreads();
-      for (int i = threadIdx.x; i < PACK_N * PACK_K; i += 256) {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int i = (int)threadIdx.x + u * 256;
         const int nn = i / PACK_K, kk = i % PACK_K;
         Bt[(int64_t)(n0 + nn) * j.Kpad + k0 + kk] = tile[kk][nn];
       }
       __syncthreads();
     } else {
-      for (int i = threadIdx.x; i < PACK_N * PACK_K; i += 256) {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int i = (int)threadIdx.x + u * 256;
         const int nn = i / PACK_K, kk = i % PACK_K;
         const int c = n0 + nn, k = k0 + kk;
         const int f = k / j.cp_out, o = k - f * j.cp_out;
-        Bt[(int64_t)c * j.Kpad + k] =
-            (f < j.A && o < j.c_out && c < j.c_in) ? W[((int64_t)f * j.c_in + c) * j.c_out + o] : zero;
+        const bool ok = f < j.A && o < j.c_out && c < j.c_in;
+        const T w = W[ok ? ((int64_t)f * j.c_in + c) * j.c_out + o : 0];
+        v[u] = ok ? w : zero;
+      }
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int i = (int)threadIdx.x + u * 256;
+        Bt[(int64_t)(n0 + i / PACK_K) * j.Kpad + k0 + i % PACK_K] = v[u];
       }
     }
   }
@@ -251,7 +278,7 @@ static int grid_for(int64_t items) { return (int)std::max<int64_t>(1, std::min<i
 
 hipError_t launch_scatter_input(bool bf16, const void* feats, int32_t n, int32_t c_in, const int32_t* perm, void* X0,
                                 int32_t cp0, hipStream_t st) {
-  int grid = grid_for((int64_t)(n + 1) * cp0);
+  int grid = grid_for((int64_t)(n + 1) * (cp0 / (bf16 ? 8 : 4)));
   if (bf16)
     hipLaunchKernelGGL(k_scatter_input<__bf16>, dim3(grid), dim3(256), 0, st, (const __bf16*)feats, n, c_in, perm,
                        (__bf16*)X0, cp0);
@@ -287,7 +314,7 @@ hipError_t launch_pack_all(bool bf16, const PackArgs& in, hipStream_t st) {
   if (pa.njobs <= 0 || total <= 0) return hipSuccess;
   if (total >= (1ll << 31)) return hipErrorInvalidValue;
   pa.tile_beg[pa.njobs] = (int32_t)total;
-  if (pa.sc.X0) pa.sc.blocks = grid_for((int64_t)(pa.sc.n + 1) * pa.sc.cp0);
+  if (pa.sc.X0) pa.sc.blocks = grid_for((int64_t)(pa.sc.n + 1) * (pa.sc.cp0 / (bf16 ? 8 : 4)));
   else pa.sc.blocks = 0;
   const int grid = (int)std::min<int64_t>(total, 16384) + pa.sc.blocks;  // one tile per workgroup up to 16384
   if (bf16)
