@@ -251,22 +251,27 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
     const int kbeg = ks * kper;
     const int kend = min(a.Kpad, kbeg + kper);
 
-    if (tid < BM) {  // the tile's window rows: one row per thread, independent loads
+    if (tid < BM) {  // the tile's window rows: one row per thread, all loads issued before any store
       const int m = m0 + tid;
+      const bool live = m < rows;
       int row = m;  // the output row (pooling forward: the slot's convolution row)
       if constexpr (POOL) {
-        row = m < rows ? a.pslot[m] : 0;
+        const int pr = a.pslot[live ? m : 0];
+        row = live ? pr : 0;
         Cr[tid] = row;
       }
-      const int32_t* rp = a.rmap ? a.rmap + (int64_t)row * A : nullptr;
+      int v[AMAX];
+      if (a.rmap) {  // rows past the count read row 0's window and discard it
+        const int32_t* rp = a.rmap + (int64_t)(live ? row : 0) * A;
 #pragma unroll
-      for (int f = 0; f < AMAX; ++f) {
-        if (f < A) {
-          int v = -1;
-          if (m < rows) v = rp ? rp[f] : (f == 0 ? row : -1);
-          Rs[tid * A + f] = v;
-        }
+        for (int f = 0; f < AMAX; ++f) v[f] = rp[f < A ? f : 0];
+      } else {
+#pragma unroll
+        for (int f = 0; f < AMAX; ++f) v[f] = f == 0 ? row : -1;
       }
+#pragma unroll
+      for (int f = 0; f < AMAX; ++f)
+        if (f < A) Rs[tid * A + f] = live ? v[f] : -1;
     }
     __syncthreads();
 
