@@ -140,7 +140,14 @@ __global__ void __launch_bounds__(64) k_rb_bitmaps(RulebookArgs a, int32_t max_w
   }
   if (b >= a.batch) return;
   const uint64_t* src = L0.bits + (int64_t)b * nw0;
-  for (int w = t; w < nw0; w += 64) in[w] = src[w];
+  for (int w0 = t; w0 < nw0; w0 += 4 * 64) {  // four words per lane in flight
+    uint64_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = src[min(w0 + u * 64, nw0 - 1)];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (w0 + u * 64 < nw0) in[w0 + u * 64] = v[u];
+  }
   __syncthreads();
   if (s == 0) {  // the input layer: its prefix and count only
     const int tot = wave_popcount_scan(in, nw0, L0.wpre + (int64_t)b * nw0);
@@ -202,6 +209,7 @@ __global__ void __launch_bounds__(64) k_rb_offsets(RulebookArgs a) {
   const int per = (a.batch + 63) / 64;
   const int beg = min(a.batch, t * per), end = min(a.batch, beg + per);
   int local = 0;
+#pragma unroll 4
   for (int i = beg; i < end; ++i) local += L.scount[i];
   int total;
   int run = wave_exclusive_scan(local, &total);
