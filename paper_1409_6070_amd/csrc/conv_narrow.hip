@@ -86,6 +86,36 @@ __device__ inline nv4u narrow_vector(const GemmArgs& a, const float (&xs)[NARROW
   return o;
 }
 
+// One step of the first maximum over a window's slots: `late` (the later
+// slots) replaces `early` element by element only where it is strictly greater,
+// compared as fp32 exactly as the stored values convert; the argmax bytes follow
+// the same choice.  Works on whole 32-bit words: a per-word select mask and one
+// bit-select per word instead of per-element inserts.
+template <typename T>
+__device__ inline void first_max_step(const nv4u& early, const nv4u& late, typename NarrowArg<Elem<T>::VE>::W eam,
+                                      typename NarrowArg<Elem<T>::VE>::W lam, nv4u& r,
+                                      typename NarrowArg<Elem<T>::VE>::W& am) {
+  typedef typename NarrowArg<Elem<T>::VE>::W AW;
+  AW amask = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t E = early[w], L = late[w];
+    uint32_t m;
+    if constexpr (Elem<T>::VE == 8) {  // two bf16 per word: element 2w low, 2w + 1 high
+      const bool g0 = __uint_as_float(L << 16) > __uint_as_float(E << 16);
+      const bool g1 = __uint_as_float(L & 0xffff0000u) > __uint_as_float(E & 0xffff0000u);
+      m = (g0 ? 0x0000ffffu : 0u) | (g1 ? 0xffff0000u : 0u);
+      amask |= (AW)((g0 ? 0x00ffu : 0u) | (g1 ? 0xff00u : 0u)) << (16 * w);
+    } else {  // one fp32 per word
+      const bool g = __uint_as_float(L) > __uint_as_float(E);
+      m = g ? 0xffffffffu : 0u;
+      amask |= (AW)(g ? 0xffu : 0u) << (8 * w);
+    }
+    r[w] = (L & m) | (E & ~m);
+  }
+  am = (lam & amask) | (eam & ~amask);
+}
+
 template <typename T, int CIN, bool POOL>
 __global__ void __launch_bounds__(256) k_conv_narrow(GemmArgs a) {
   constexpr int VE = Elem<T>::VE;
@@ -168,13 +198,8 @@ __global__ void __launch_bounds__(256) k_conv_narrow(GemmArgs a) {
           const nv4u early = upper ? po : o, late = upper ? o : po;
           const AW eam = upper ? pam : am, lam = upper ? am : pam;
           nv4u r;
-          AW ram = 0;
-#pragma unroll
-          for (int e = 0; e < VE; ++e) {
-            const bool gt = Elem<T>::to_f32(((const T*)&late)[e]) > Elem<T>::to_f32(((const T*)&early)[e]);
-            ((T*)&r)[e] = gt ? ((const T*)&late)[e] : ((const T*)&early)[e];
-            ram |= ((gt ? lam : eam) >> (8 * e) & (AW)0xff) << (8 * e);
-          }
+          AW ram;
+          first_max_step<T>(early, late, eam, lam, r, ram);
           o = r;
           am = ram;
         }
