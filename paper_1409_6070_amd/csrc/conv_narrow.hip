@@ -5,16 +5,19 @@
 // As a gather GEMM such a layer has K = A * Cp_in with Cp_in the channel count
 // padded to a 16-byte vector, so a 3 x 3 window over one channel is 9 products
 // per output in a K of 72 (128 after tile padding): the matrix cores would
-// mostly multiply padding.  Here each thread computes one 16-byte vector of one
-// output row from the A input vectors of its window, with the weights staged
-// in LDS as fp32, and applies the same bias-rectifier epilogue as the GEMM.
+// mostly multiply padding.  Here NARROW_SPLIT threads share an output row: each
+// loads the row's window and its A input rows once, then computes every
+// NARROW_SPLIT-th 16-byte output vector of the row with the weights staged in
+// LDS as fp32 (read by broadcast), with the same bias-rectifier epilogue as the
+// GEMM.
 //
 // With the pooling forward of the layer above (GemmArgs::pool_fwd) the rows
-// are the pooling windows' slots 4 p + f, as in the GEMM's fused epilogue: the
-// four lanes 4 j .. 4 j + 3 of a wave take the four slots of one window and one
-// output vector, each stores its convolution row (row 0 from window 0's slot 0
-// only), and the window's first maximum and its position are combined across
-// the four lanes (earlier slots win ties) and stored by the slot-0 lane.
+// are the pooling windows' slots 4 p + f, as in the GEMM's fused epilogue: four
+// adjacent lanes take the four slots of one window (and the same share of its
+// output vectors), each stores its convolution row (row 0 from window 0's slot
+// 0 only), and per output vector the window's first maximum and its position
+// are combined across the four lanes (earlier slots win ties) and stored by the
+// slot-0 lane.
 
 #include "common.h"
 #include "epilogue.h"
@@ -212,9 +215,10 @@ __global__ void __launch_bounds__(256) k_conv_narrow(GemmArgs a) {
   }
 }
 
+typedef void (*NarrowKernel)(GemmArgs);
 template <typename T, int CIN>
-void* narrow_kernel(bool pool) {
-  return pool ? (void*)k_conv_narrow<T, CIN, true> : (void*)k_conv_narrow<T, CIN, false>;
+NarrowKernel narrow_kernel(bool pool) {
+  return pool ? k_conv_narrow<T, CIN, true> : k_conv_narrow<T, CIN, false>;
 }
 
 }  // namespace
@@ -240,14 +244,13 @@ hipError_t launch_conv_narrow(bool bf16, const GemmArgs& in, int cin, int64_t ma
   const int grid = (int)std::min<int64_t>(std::max<int64_t>((items + 255) / 256, 1), 2048);
   const size_t lds = (size_t)(NARROW_AMAX * cin + 1) * a.out_cols * sizeof(float);
   const bool pool = a.pool_fwd != 0;
-  void* k = nullptr;
+  NarrowKernel kern = nullptr;
   switch (cin) {
-    case 1: k = bf16 ? narrow_kernel<__bf16, 1>(pool) : narrow_kernel<float, 1>(pool); break;
-    case 2: k = bf16 ? narrow_kernel<__bf16, 2>(pool) : narrow_kernel<float, 2>(pool); break;
-    case 3: k = bf16 ? narrow_kernel<__bf16, 3>(pool) : narrow_kernel<float, 3>(pool); break;
-    default: k = bf16 ? narrow_kernel<__bf16, 4>(pool) : narrow_kernel<float, 4>(pool); break;
+    case 1: kern = bf16 ? narrow_kernel<__bf16, 1>(pool) : narrow_kernel<float, 1>(pool); break;
+    case 2: kern = bf16 ? narrow_kernel<__bf16, 2>(pool) : narrow_kernel<float, 2>(pool); break;
+    case 3: kern = bf16 ? narrow_kernel<__bf16, 3>(pool) : narrow_kernel<float, 3>(pool); break;
+    default: kern = bf16 ? narrow_kernel<__bf16, 4>(pool) : narrow_kernel<float, 4>(pool); break;
   }
-  void (*kern)(GemmArgs) = (void (*)(GemmArgs))k;
   if (a.t_start || a.t_stop)
     hipExtLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, a.t_start, a.t_stop, 0, a);
   else
