@@ -220,27 +220,95 @@ __global__ void __launch_bounds__(64) k_rb_offsets(RulebookArgs a) {
   if (t == 0) a.counts[s] = total;
 }
 
-// Site keys of every layer, in row order: one thread per bitmap word.
+// Batches up to this size have their sample offsets scanned inside the sites
+// kernel (no separate offsets launch).
+constexpr int SITES_SCAN_MAX = 1024;
+
+// Exclusive prefix of scount[0, batch) into the LDS array off, by one
+// workgroup of 256 threads (batch <= SITES_SCAN_MAX); returns the total.  All
+// threads call it; it synchronises before returning.
+__device__ inline int block_count_scan(const int32_t* scount, int batch, int* off, int* wsum) {
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int per = (batch + 255) / 256;  // <= 4
+  const int beg = min(batch, t * per), end = min(batch, beg + per);
+  int c[4];
+  int local = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    c[u] = beg + u < end ? scount[beg + u] : 0;
+    local += c[u];
+  }
+  int wt;
+  int run = wave_exclusive_scan(local, &wt);
+  if (lane == 0) wsum[wv] = wt;
+  __syncthreads();
+  for (int q = 0; q < wv; ++q) run += wsum[q];
+  const int total = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    if (beg + u < end) {
+      off[beg + u] = run;
+      run += c[u];
+    }
+  __syncthreads();
+  return total;
+}
+
+// The keys of the sites in bitmap word `word` (word rem of sample b in layer
+// L), from row soff_b + wp on (wp: the word's popcount prefix).
+__device__ inline void word_sites(const LayerBits& L, uint64_t word, int wp, int b, int rem, int soff_b) {
+  if (!word) return;
+  const int y = div_rcp(rem, L.Wd, 1.f / (float)L.Wd), w = rem - y * L.Wd;
+  int row = soff_b + wp;
+  while (word) {
+    int bit = __ffsll((long long)word) - 1;
+    word &= word - 1;
+    int x = w * 64 + bit;
+    L.sites[row++] = (b * L.S + y) * L.S + x;
+  }
+}
+
+// Site keys of every layer, in row order: one thread per bitmap word.  SCAN
+// (1 <= batch <= SITES_SCAN_MAX): each workgroup takes 256 consecutive words
+// at a time and scans the per-sample counts of the layers they belong to
+// itself; the thread holding a sample's first word of a layer stores its offset
+// and the thread holding a layer's last word the layer's total.  Otherwise the
+// offsets kernel has stored both.
+template <bool SCAN>
 __global__ void __launch_bounds__(256) k_rb_sites(RulebookArgs a, SitesWork wk) {
-  int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (; g < wk.total; g += stride) {
+  __shared__ int off[SCAN ? SITES_SCAN_MAX : 1];
+  __shared__ int wsum[4];
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t g0 = (int64_t)blockIdx.x * blockDim.x; g0 < wk.total; g0 += stride) {  // uniform per workgroup
+    const int64_t g = g0 + threadIdx.x;
+    const bool live = g < wk.total;
     int s = 0;
-    while (s + 1 < a.nlayers && g >= wk.base[s + 1]) ++s;
+    while (s + 1 < a.nlayers && (live ? g : wk.total - 1) >= wk.base[s + 1]) ++s;
     const LayerBits& L = a.L[s];
-    int64_t idx = g - wk.base[s];
-    uint64_t word = L.bits[idx];
-    if (!word) continue;
+    const int64_t idx = (live ? g : wk.total - 1) - wk.base[s];
     const int per_sample = L.S * L.Wd;  // words per sample (< 2^20)
     const int b = div_rcp_d(idx, per_sample);
     const int rem = (int)(idx - (int64_t)b * per_sample);
-    const int y = div_rcp(rem, L.Wd, 1.f / (float)L.Wd), w = rem - y * L.Wd;
-    int row = L.soff[b] + L.wpre[idx];
-    while (word) {
-      int bit = __ffsll((long long)word) - 1;
-      word &= word - 1;
-      int x = w * 64 + bit;
-      L.sites[row++] = (b * L.S + y) * L.S + x;
+    // the word and its prefix do not depend on the offsets: loaded first
+    const uint64_t word = live ? L.bits[idx] : 0ull;
+    const int wp = live ? L.wpre[idx] : 0;
+    if constexpr (SCAN) {
+      int s_lo = 0;
+      while (s_lo + 1 < a.nlayers && g0 >= wk.base[s_lo + 1]) ++s_lo;
+      const int64_t g_last = min(g0 + (int64_t)blockDim.x, wk.total) - 1;
+      int s_hi = s_lo;
+      while (s_hi + 1 < a.nlayers && g_last >= wk.base[s_hi + 1]) ++s_hi;
+      for (int sl = s_lo; sl <= s_hi; ++sl) {
+        const int total = block_count_scan(a.L[sl].scount, a.batch, off, wsum);
+        if (live && s == sl) {
+          if (rem == 0) L.soff[b] = off[b];
+          if (g == wk.base[s + 1] - 1) a.counts[s] = total;
+          word_sites(L, word, wp, b, rem, off[b]);
+        }
+        __syncthreads();  // off is rewritten by the next layer's scan
+      }
+    } else if (live) {
+      word_sites(L, word, wp, b, rem, L.soff[b]);
     }
   }
 }
@@ -407,10 +475,14 @@ hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const Rul
                        L0.bits, a.err);
   const size_t lds = (size_t)(2 * max_words + 64 * L0.Wd) * sizeof(uint64_t);
   hipLaunchKernelGGL(k_rb_bitmaps, dim3(std::max(a.batch, 1) * a.nlayers), dim3(64), lds, st, a, max_words);
-  hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
+  const bool scan = a.batch >= 1 && a.batch <= SITES_SCAN_MAX;
+  if (!scan) hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
   int gs = (int)std::min<int64_t>((wk.total + 255) / 256, 2048);
   if (gs < 1) gs = 1;
-  hipLaunchKernelGGL(k_rb_sites, dim3(gs), dim3(256), 0, st, a, wk);
+  if (scan)
+    hipLaunchKernelGGL(k_rb_sites<true>, dim3(gs), dim3(256), 0, st, a, wk);
+  else
+    hipLaunchKernelGGL(k_rb_sites<false>, dim3(gs), dim3(256), 0, st, a, wk);
   hipLaunchKernelGGL(k_rb_rules, dim3(rw.blk[rw.nseg]), dim3(256), 0, st, a, rw);
   return hipGetLastError();
 }

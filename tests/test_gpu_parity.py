@@ -195,6 +195,19 @@ def test_first_layer_kernel_choice(c_in, narrow, dtype):
     check_values(pair)
 
 
+@pytest.mark.parametrize("batch", [1, 1024, 1100])
+def test_rulebook_batch_sizes_around_offset_scan(batch):
+    """Up to 1024 samples the sites kernel scans the per-sample counts itself; above, a separate
+    offsets launch does. Both must give the oracle's rows, windows and values."""
+    coords, feats = _sparse_case(60 + batch % 7, 1, batch, 0.3, 1)
+    log(f"[batch-scan] batch={batch} n={len(coords)}")
+    Ws, bs = he_params(1, 3, 1, 4, 160)
+    labels = random_labels(batch, 4, 260)
+    pair = Pair(1, 3, 1, 4, batch, coords, feats, Ws, bs, labels, "f32").run_gpu()
+    check_structure(pair)
+    check_values(pair)
+
+
 def test_rulebook_path_counts_full_grid():
     """Fully active 96x96 input of DeepCNet(5,.): routes through the GPU window lists (Section 2.6)."""
     ell, N = 5, 96
