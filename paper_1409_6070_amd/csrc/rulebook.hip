@@ -220,8 +220,9 @@ __global__ void __launch_bounds__(64) k_rb_offsets(RulebookArgs a) {
   if (t == 0) a.counts[s] = total;
 }
 
-// Batches up to this size have their sample offsets scanned inside the sites
-// kernel (no separate offsets launch).
+// Batches up to this size (and builds of at most two 256-word chunks per
+// workgroup) have their sample offsets scanned inside the sites kernel (no
+// separate offsets launch).
 constexpr int SITES_SCAN_MAX = 1024;
 
 // Exclusive prefix of scount[0, batch) into the LDS array off, by one
@@ -475,10 +476,12 @@ hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const Rul
                        L0.bits, a.err);
   const size_t lds = (size_t)(2 * max_words + 64 * L0.Wd) * sizeof(uint64_t);
   hipLaunchKernelGGL(k_rb_bitmaps, dim3(std::max(a.batch, 1) * a.nlayers), dim3(64), lds, st, a, max_words);
-  const bool scan = a.batch >= 1 && a.batch <= SITES_SCAN_MAX;
-  if (!scan) hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
   int gs = (int)std::min<int64_t>((wk.total + 255) / 256, 2048);
   if (gs < 1) gs = 1;
+  // the in-kernel scan repeats per chunk of 256 words: only while each
+  // workgroup has at most two chunks
+  const bool scan = a.batch >= 1 && a.batch <= SITES_SCAN_MAX && wk.total <= (int64_t)gs * 256 * 2;
+  if (!scan) hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
   if (scan)
     hipLaunchKernelGGL(k_rb_sites<true>, dim3(gs), dim3(256), 0, st, a, wk);
   else
