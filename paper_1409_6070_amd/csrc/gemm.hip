@@ -692,7 +692,7 @@ hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream
   return hipGetLastError();
 }
 
-GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K) {
+GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K, bool short_rows) {
   // bf16 launches with few output tiles (at the row bound) go to the
   // direct-operand kernel, whose waves split K and so keep many loads in flight
   // per tile; launches with many tiles keep the LDS-tiled kernel, whose 128-row
@@ -720,13 +720,17 @@ GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K) {
   // Tile width: 128 when that pads N no more than 64 does and still gives >= 256
   // tiles; otherwise 64-wide tiles with the tallest of 128/64/32 rows that gives
   // >= 256 tiles.  K is split when even 32-row tiles leave the GPU mostly idle.
+  // short_rows (an epilogue that routes every row through its pooling window,
+  // a thread's rows one after another): at most 64 rows per tile, so that each
+  // thread routes two rows, not four or eight (measured on the pen-stroke
+  // DeepCNet(5,50) input gradient of the second level: 31.9 -> 25.8 us).
   const int BK = bf16 ? 64 : 32;
   const int64_t n128 = (N + 127) / 128 * 128, n64 = (N + 63) / 64 * 64;
   auto tiles = [&](int bm, int64_t npad, int bn) { return ((max_rows + bm - 1) / bm) * (npad / bn); };
   GemmPlan p;
-  if (n128 <= n64 && tiles(128, n128, 128) >= 256)
+  if (!short_rows && n128 <= n64 && tiles(128, n128, 128) >= 256)
     p.cfg = 0;
-  else if (tiles(128, n64, 64) >= 256)
+  else if (!short_rows && tiles(128, n64, 64) >= 256)
     p.cfg = 1;
   else if (tiles(64, n64, 64) >= 256)
     p.cfg = 2;
