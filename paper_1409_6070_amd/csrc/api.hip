@@ -405,7 +405,9 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.cp_out = L[s].Cp;
     P.rows_f = L[s].cap + 1;
     P.rows_d = L[s - 1].cap + 1;
-    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.A * P.cp_in);
+    // a convolution under a pooling layer computes that layer in its epilogue
+    const bool pooled = s + 1 < net->nlayers && L[s + 1].kind == 2;
+    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.A * P.cp_in, false, pooled ? 1000 : 4000);
     // an input gradient that is a pooling layer's may route its rows through the
     // pooling windows in its epilogue
     P.pd = plan_gemm(net->bf16, P.rows_d, P.c_in, P.A * P.cp_out, L[s - 1].kind == 2);

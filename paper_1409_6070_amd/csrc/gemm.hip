@@ -692,15 +692,17 @@ hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream
   return hipGetLastError();
 }
 
-GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K, bool short_rows) {
+GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K, bool short_rows, int direct_max) {
   // bf16 launches with few output tiles (at the row bound) go to the
   // direct-operand kernel, whose waves split K and so keep many loads in flight
   // per tile; launches with many tiles keep the LDS-tiled kernel, whose 128-row
   // tiles share each weight slab between four waves.  (Measured on the pen-stroke
   // DeepCNet(5,50): the direct kernel wins at <= 3.3k tiles of 32 x 64 and loses
-  // from 4.5k up; very deep K keeps split-K.)
+  // from 4.5k up; very deep K keeps split-K.  A convolution with the pooling
+  // forward in its epilogue passes a lower bound, 1,000 tiles: its 1.25k-tile
+  // launch there takes 21.1 us LDS-tiled against 22.7 us direct.)
   const int64_t direct_tiles = ((max_rows + DIRECT_BM - 1) / DIRECT_BM) * ((N + DIRECT_BN - 1) / DIRECT_BN);
-  if (bf16 && direct_tiles <= 4000 && K <= 2048) {
+  if (bf16 && direct_tiles <= direct_max && K <= 2048) {
     // waves per tile so that each sums at most about four 32-wide k blocks,
     // and more while the grid stays small
     GemmPlan p;
