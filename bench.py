@@ -125,6 +125,55 @@ def gemm_work(cfg, sizes, infer=False, e=2, routed=True):
             "conv_total": 2 * (fwd + narrow) + dgrad, "gather_gemm_bytes": fbytes + dbytes + hf_bytes + hd_bytes}
 
 
+def flops_8d(cfg, sizes):
+    """Per convolution stage s: 2 (n_s + 1) A C_in C_out, the unit of algorithmic work that each of the
+    forward, the input gradient and the weight gradient of that stage does (the per-stage figure of the
+    measurement plan; the input gradient is counted over the stage's output rows like the others)."""
+    out = {}
+    for s, (kind, A, ci, co) in enumerate(layer_shapes(cfg), start=1):
+        if kind == "conv":
+            out[s] = 2.0 * (sizes[s] + 1) * A * ci * co
+    return out
+
+
+def rulebook_bytes(cfg, sizes):
+    """Algorithmic bytes of the rulebook per step: n_in (8 + 8A) + n_out (8 + 4A) per stage."""
+    tot = 0.0
+    for s, (kind, A, ci, co) in enumerate(layer_shapes(cfg), start=1):
+        tot += sizes[s - 1] * (8 + 8 * A) + sizes[s] * (8 + 4 * A)
+    return tot
+
+
+def narrow_bytes(cfg, sizes, e):
+    """Algorithmic bytes of the first-layer vector-ALU kernel (with the pooling layer above it fused):
+    per convolution row (ground row included) its window list 4A, its inputs A C_in e and its output C_out e;
+    per pooling row its window 16 and its pooled value and argmax C_out (e + 1)."""
+    kind, A, ci, co = layer_shapes(cfg)[0]
+    n1, n2 = sizes[1], sizes[2]
+    return (n1 + 1) * (4 * A + A * ci * e + co * e) + (n2 + 1) * 16 + n2 * co * (e + 1)
+
+
+ROLE_NAMES = {0: "forward", 1: "input gradient", 2: "softmax logits", 3: "softmax dh", 4: "other"}
+PLAN_NAMES = {0: "k_gemm_gather 128x128", 1: "k_gemm_gather 128x64", 2: "k_gemm_gather 64x64",
+              3: "k_gemm_gather 32x64", 4: "k_gemm_direct 32x64", 15: ""}
+
+
+def decode_tag(tag):
+    return {"stage": tag & 0xFF, "role": (tag >> 8) & 0xF, "plan": (tag >> 12) & 0xF,
+            "routed": bool((tag >> 16) & 1), "pooled": bool((tag >> 17) & 1)}
+
+
+def group_key(kc, t):
+    """A kernel instantiation: class, role, tile plan and fused epilogue."""
+    if kc == "conv_narrow":
+        return "k_conv_narrow (first layer, vector ALUs, pooling forward fused)"
+    if kc == "wgrad":
+        return "k_wgrad (all weight gradients, grouped)"
+    name = PLAN_NAMES.get(t["plan"], f"plan {t['plan']}")
+    extra = " + pooling backward" if t["routed"] else (" + pooling forward" if t["pooled"] else "")
+    return f"{name}: {ROLE_NAMES[t['role']]}{extra}"
+
+
 def read_traffic(kernel, dtype, workload):
     """HBM bytes per launch from the committed counter summary, if it matches the current kernel source,
     the dtype and the workload."""
@@ -151,21 +200,12 @@ def read_traffic(kernel, dtype, workload):
         return None
 
 
-def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False, paths=None):
-    """The oracle, as it stands, on batch 0: build + forward (+ backward unless infer), repeated for ~budget_s.
-
-    With pen paths (``paths``) each repetition is a whole training step: the oracle's encoding,
-    build, forward, backward and SGD update."""
+def _oracle_reps(cfg, batch, Ws, bs, labels, dtype, budget_s, infer, paths):
+    """Repeats the oracle's step on batch 0 for about budget_s seconds; returns (reps, seconds)."""
     from oracle import SparseDeepCNet as Oracle
     from oracle.sgd import sgd_step
     from oracle.strokes import encode_strokes
 
-    try:
-        from threadpoolctl import threadpool_info
-
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        threads = 1
     def storage(x):
         t = torch.tensor(np.asarray(x, np.float64), dtype=torch.float32)
         return (t.to(torch.bfloat16) if dtype == "bf16" else t).double().numpy()
@@ -194,7 +234,27 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False, 
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 50:
-            break
+            return reps, el
+
+
+def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False, paths=None):
+    """The oracle, as it stands, on batch 0: build + forward (+ backward unless infer), repeated for
+    ~budget_s with the host's BLAS threads, then for ~budget_s / 2 on one thread.
+
+    With pen paths (``paths``) each repetition is a whole training step: the oracle's encoding,
+    build, forward, backward and SGD update."""
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threadpool_limits, threads = None, 1
+    reps, el = _oracle_reps(cfg, batch, Ws, bs, labels, dtype, budget_s, infer, paths)
+    single = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            r1, e1 = _oracle_reps(cfg, batch, Ws, bs, labels, dtype, budget_s / 2, infer, paths)
+        single = round(r1 * cfg.batch / e1, 3)
     cpu = ""
     try:
         for line in open("/proc/cpuinfo"):
@@ -209,9 +269,10 @@ def cpu_baseline(cfg, batch, Ws, bs, labels, dtype, budget_s=12.0, infer=False, 
     if cfg.sgd:
         what += " + SGD update"
     return {"value": round(reps * cfg.batch / el, 3), "unit": "characters/s" if infer else "samples/s",
-            "cores": threads, "kind": "oracle",
+            "cores": threads, "kind": "oracle", "value_1_thread": single,
             "sample": f"batch 0 of {cfg.name} ({cfg.batch} samples), {reps} x ({what}), "
-                      f"mode {dtype}, {el:.1f} s; NumPy float64, BLAS threads {threads}; host CPU: {cpu}"}
+                      f"mode {dtype}, {el:.1f} s; NumPy float64, BLAS threads {threads} "
+                      f"(value_1_thread: the same on one thread); host CPU: {cpu}"}
 
 
 def calibrate_copy():
@@ -225,39 +286,21 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}))
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
-    ap.add_argument("--batches", type=int, default=8)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--calibrate-copy", action="store_true")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported here "
-              "(the path would shard over samples with one all-reduce of dW/db per step)", file=sys.stderr)
-        sys.exit(2)
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(2)
-    if args.calibrate_copy:
-        calibrate_copy()
-        return
+TIMED = ["gather_gemm", "conv_narrow", "wgrad", "wgrad_reduce", "rulebook"]
 
-    from paper_1409_6070_amd.sscn import SparseDeepCNet
 
-    cfg = get_config(args.workload)
+def measure(cfg, dtype, steps, warmup, nbatches, cpu=True):
+    """Times one workload; returns the JSON record (see the module docstring)."""
+    from paper_1409_6070_amd.sscn import KERNEL_CLASSES, SparseDeepCNet, StrokeEncoder
+
     dev = torch.device("cuda:0")
-    tdt = torch.bfloat16 if args.dtype == "bf16" else torch.float32
-    log(f"[bench] generating {args.batches} batches of {cfg.name}")
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    log(f"[bench] {cfg.name} {dtype}: generating {nbatches} batches")
     paths = cfg.generator == "paths"
     Ws, bs = he_params(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.weight_seed, cfg.arch)
     labels = random_labels(cfg.batch, cfg.n_classes, cfg.label_seed)
     W32_d = [torch.tensor(W, dtype=torch.float32).to(dev).contiguous() for W in Ws]
-    Ws_d = [w.to(tdt).contiguous() for w in W32_d] if args.dtype == "bf16" else W32_d
+    Ws_d = [w.to(tdt).contiguous() for w in W32_d] if dtype == "bf16" else W32_d
     bs_d = [torch.tensor(b, dtype=torch.float32).to(dev).contiguous() for b in bs]
     vW_d = [torch.zeros_like(w) for w in W32_d]
     vb_d = [torch.zeros_like(b) for b in bs_d]
@@ -266,24 +309,23 @@ def main():
     if paths:
         # raw pen paths: every step encodes them on the device (Section 2.4); one
         # untimed pass learns the site counts that size the encoder and the net
-        from paper_1409_6070_amd.sscn import StrokeEncoder
-        path_batches = [make_paths(cfg, i) for i in range(args.batches)]
+        path_batches = [make_paths(cfg, i) for i in range(nbatches)]
         raw = [tuple(torch.tensor(a, dtype=torch.int32, device=dev).contiguous()
                      for a in (p.points, p.stroke_begin, p.stroke_sample)) for p in path_batches]
-        probe = StrokeEncoder(cfg.grid, cfg.batch, cfg.batch * cfg.grid * cfg.grid, args.dtype)
+        probe = StrokeEncoder(cfg.grid, cfg.batch, cfg.batch * cfg.grid * cfg.grid, dtype)
         counts = [int(probe.encode(*r, cfg.batch)[0].shape[0]) for r in raw]
         del probe
         max_active = max(counts)
-        enc = StrokeEncoder(cfg.grid, cfg.batch, max_active, args.dtype)
+        enc = StrokeEncoder(cfg.grid, cfg.batch, max_active, dtype)
         batches = []
     else:
-        batches = make_batches(cfg, args.batches)
+        batches = make_batches(cfg, nbatches)
         for b in batches:
             inputs.append((torch.tensor(b.coords, dtype=torch.int32, device=dev).contiguous(),
                            torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous()))
         max_active = max(b.n for b in batches)
     net = SparseDeepCNet(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, batch_max=cfg.batch, max_active=max_active,
-                         dtype=args.dtype, arch=cfg.arch, dropout=bool(cfg.dropout))
+                         dtype=dtype, arch=cfg.arch, dropout=bool(cfg.dropout))
 
     def inputs_of(i):
         if paths:
@@ -310,71 +352,121 @@ def main():
             net.forward(f, Ws_d, bs_d, lab_d)
             net.backward()
             if cfg.sgd:
-                net.sgd_step(W32_d, Ws_d if args.dtype == "bf16" else None, bs_d, vW_d, vb_d, *cfg.sgd)
+                net.sgd_step(W32_d, Ws_d if dtype == "bf16" else None, bs_d, vW_d, vb_d, *cfg.sgd)
 
-    log(f"[bench] warmup {args.warmup} steps")
-    for i in range(args.warmup):
+    log(f"[bench] warmup {warmup} steps")
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    log(f"[bench] timing {args.steps} steps")
+    log(f"[bench] timing {steps} steps")
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         step(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    sec = (t1 - t0) / args.steps
+    sec = (t1 - t0) / steps
     value = cfg.batch / sec
     log(f"[bench] {sec * 1e3:.3f} ms/step, {value:.1f} samples/s")
 
-    # the same K steps again, now with every gather-GEMM launch bracketed by HIP
-    # events on its own stream (the brackets slow the step, so `value` above
-    # comes from the unbracketed pass)
-    net.timing_collect("gather_gemm")  # drop anything recorded so far
-    net.timing(["gather_gemm"])
-    for i in range(args.steps):
+    # The same K steps again with the launches of the convolution kernels and the
+    # rulebook bracketed by HIP events on the stream they run on (the GEMM kernels
+    # record their own start and end); the brackets slow the step, so `value`
+    # above comes from the unbracketed pass.
+    for kc in KERNEL_CLASSES:
+        net.timing_launches(kc)  # drop anything recorded so far
+    net.timing(TIMED)
+    for i in range(steps):
         step(i)
     torch.cuda.synchronize()
-    g_launches, g_ms = net.timing_collect("gather_gemm")
+    recs = {kc: net.timing_launches(kc) for kc in TIMED}
     net.timing([])
 
     # algorithmic work of the timed steps (batches cycle in order)
-    step_sizes = [sizes[i % len(sizes)] for i in range(args.steps)]
-    esz = 2 if args.dtype == "bf16" else 4
-    # (the pooling backward runs in the GEMM epilogues except through dropout)
-    work = [gemm_work(cfg, s, infer, esz, routed=not cfg.dropout) for s in step_sizes]
-    g_flops = sum(w["gather_gemm"] for w in work)
-    g_bytes = sum(w["gather_gemm_bytes"] for w in work)
-    avg_launch_s = g_ms / 1e3 / max(g_launches, 1)
-    achieved = g_flops / max(g_launches, 1) / avg_launch_s if g_launches else 0.0
-    peak = MFMA_PEAK[args.dtype]
-    traffic = read_traffic("gather_gemm", args.dtype, cfg.name)
+    step_sizes = [sizes[i % len(sizes)] for i in range(steps)]
+    esz = 2 if dtype == "bf16" else 4
+    peak = MFMA_PEAK[dtype]
+    conv_fl = [flops_8d(cfg, sz) for sz in step_sizes]
+    head_fl = 2.0 * cfg.batch * layer_shapes(cfg)[-1][3] * cfg.n_classes
+    # each launch's algorithmic FLOPs from the sizes of its own step: in launch order a
+    # step's forward launches precede its softmax logits, its input gradients follow them
+    groups = {}  # key -> [launches, ms, flops]
+
+    def add(key, ms, fl):
+        g = groups.setdefault(key, [0, 0.0, 0.0])
+        g[0] += 1
+        g[1] += ms
+        g[2] += fl
+
+    conv_ms = conv_flops = 0.0
+    for kc in ("gather_gemm", "conv_narrow"):
+        nlog = 0
+        for j, (tag, ms) in enumerate(recs[kc]):
+            t = decode_tag(tag)
+            if kc == "conv_narrow":
+                si = j  # one launch per step
+            elif t["role"] == 2:
+                si, nlog = nlog, nlog + 1
+            else:
+                si = nlog if t["role"] == 0 else nlog - 1
+            fl_step = conv_fl[min(max(si, 0), len(conv_fl) - 1)]
+            if t["role"] in (0, 1):
+                fl = fl_step.get(t["stage"], 0.0)
+                conv_ms += ms
+                conv_flops += fl
+            else:
+                fl = head_fl
+            add(group_key(kc, t), ms, fl)
+    wg_ms = sum(ms for _, ms in recs["wgrad"])
+    wr_ms = sum(ms for _, ms in recs["wgrad_reduce"])
+    if recs["wgrad"]:
+        wg_fl = sum(sum(f.values()) for f in conv_fl)  # the softmax layer's weight gradient not counted
+        g = groups.setdefault(group_key("wgrad", None), [0, 0.0, 0.0])
+        g[0] += len(recs["wgrad"])
+        g[1] += wg_ms
+        g[2] += wg_fl
+        conv_ms += wg_ms + wr_ms
+        conv_flops += wg_fl
+    table = []
+    for key, (n, ms, fl) in groups.items():
+        if "softmax" in key:
+            continue
+        table.append({"kernel": key, "launches_per_step": n / steps, "us_per_step": round(ms * 1e3 / steps, 2),
+                      "avg_launch_us": round(ms * 1e3 / n, 3), "gflop_per_launch": round(fl / n / 1e9, 4),
+                      "tflops": round(fl / (ms / 1e3) / 1e12, 3) if ms else 0.0,
+                      "frac": round(fl / (ms / 1e3) / peak, 5) if ms else 0.0})
+    table.sort(key=lambda r: -r["us_per_step"])
+    dom = table[0]
     roofline = {
-        "kernel": ("gather-GEMM class: k_gemm_gather (LDS-tiled) and k_gemm_direct (direct-operand) implicit-gather "
-                   "MFMA GEMMs; " + ("conv forward, softmax layer logits" if infer else
-                                     "conv forward (with the pooling forward in its epilogue), conv input "
-                                     "gradient (with the pooling backward in its epilogue), softmax layer")),
-        "bound": "mfma", "achieved": round(achieved / 1e12, 3), "peak": peak / 1e12, "unit": "TFLOP/s",
-        "frac": round(achieved / peak, 5), "traffic": traffic,
-        "launches_per_step": g_launches / args.steps, "avg_launch_us": round(avg_launch_s * 1e6, 3),
-        "algorithmic_gflop_per_launch": round(g_flops / max(g_launches, 1) / 1e9, 4),
+        "kernel": dom["kernel"], "bound": "mfma", "achieved": dom["tflops"], "peak": peak / 1e12,
+        "unit": "TFLOP/s", "frac": dom["frac"],
+        "traffic": read_traffic(traffic_key(dom["kernel"]), dtype, cfg.name),
+        "launches_per_step": dom["launches_per_step"], "avg_launch_us": dom["avg_launch_us"],
+        "algorithmic_gflop_per_launch": dom["gflop_per_launch"],
+        "flop_convention": "2 (n_s + 1) A C_in C_out per convolution stage, for each of forward, input gradient "
+                           "and weight gradient",
     }
-    # the class's arithmetic intensity against the compulsory bytes; the attainable
-    # rate is min(MFMA peak, intensity x HBM bandwidth)
-    ai = g_flops / max(g_bytes, 1.0)
-    attainable = min(peak, ai * HBM_PEAK)
-    roofline.update({
-        "compulsory_mb_per_launch": round(g_bytes / max(g_launches, 1) / 1e6, 3),
-        "ai_flop_per_byte": round(ai, 1),
-        "attainable_tflops": round(attainable / 1e12, 1),
-        "frac_of_attainable": round(achieved / attainable, 4) if attainable else None,
-        "hbm_gbps_compulsory": round(g_bytes / max(g_launches, 1) / avg_launch_s / 1e9, 1) if g_launches else 0.0,
-    })
+    conv_frac = conv_flops / (conv_ms / 1e3) / peak if conv_ms else 0.0
+
+    # memory-bound kernels against HBM bandwidth
+    def hbm(kc, bytes_per_step):
+        n = len(recs[kc])
+        if not n:
+            return None
+        ms = sum(m for _, m in recs[kc])
+        gbps = bytes_per_step * steps / (ms / 1e3) / 1e9
+        return {"kernel_class": kc, "launches_per_step": n / steps, "us_per_step": round(ms * 1e3 / steps, 2),
+                "algorithmic_mb_per_step": round(bytes_per_step / 1e6, 3), "achieved": round(gbps, 1),
+                "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": round(gbps * 1e9 / HBM_PEAK, 4)}
+
+    mean_sizes = np.mean(np.array(step_sizes, dtype=np.float64), axis=0)
+    hbm_objs = {"rulebook": hbm("rulebook", float(np.mean([rulebook_bytes(cfg, sz) for sz in step_sizes])))}
+    if recs["conv_narrow"]:
+        hbm_objs["conv_narrow"] = hbm("conv_narrow", float(np.mean([narrow_bytes(cfg, sz, esz)
+                                                                    for sz in step_sizes])))
 
     # breakdown of one pass over a few steps with every class timed
-    from paper_1409_6070_amd.sscn import KERNEL_CLASSES
-
     net.timing(KERNEL_CLASSES)
-    nb = min(5, args.steps)
+    nb = min(5, steps)
     for i in range(nb):
         step(i)
     breakdown = {}
@@ -383,8 +475,6 @@ def main():
         breakdown[kc] = {"launches_per_step": n / nb, "us_per_step": round(ms * 1e3 / nb, 2)}
     net.timing([])
 
-    mean_sizes = np.mean(np.array(sizes, dtype=np.float64), axis=0)
-    conv_flops = float(np.mean([w["conv_total"] for w in work]))
     if infer:
         metric = f"DeepCNet({cfg.ell},{cfg.k}) forward-only characters/sec (digit pictures in a {cfg.grid}x{cfg.grid} grid)"
         unit = "characters/s"
@@ -404,13 +494,13 @@ def main():
         "value": round(value, 2),
         "unit": unit,
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(sec * 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": args.dtype,
+        "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": cfg.name,
                    "net": f"{'DeepCNiN' if cfg.arch == 'deepcnin' else 'DeepCNet'}({cfg.ell},{cfg.k})",
@@ -421,8 +511,16 @@ def main():
                             ("pen-path encoding + " if paths else "") + "rulebook build + forward + backward" +
                             (" + SGD update" if cfg.sgd else "")),
                    **({"dropout": list(cfg.dropout)} if cfg.dropout else {})},
-        "conv_gemm_gflop_per_step": round(conv_flops / 1e9, 3),
+        "conv_gemm_gflop_per_step": round(float(np.mean([sum(f.values()) for f in conv_fl])) *
+                                          (1 if infer else 3) / 1e9, 3),
         "roofline": roofline,
+        "conv_gemm": {"frac": round(conv_frac, 5), "achieved": round(conv_flops / (conv_ms / 1e3) / 1e12, 3)
+                      if conv_ms else 0.0, "peak": peak / 1e12, "unit": "TFLOP/s",
+                      "us_per_step": round(conv_ms * 1e3 / steps, 2),
+                      "kernels": "every convolution launch: forward (GEMM and vector-ALU), input gradient, "
+                                 "weight gradient and its reduce; the softmax layer excluded"},
+        "kernels": table,
+        "hbm": hbm_objs,
         "kernel_breakdown": breakdown,
         "cpu_baseline": None,
     }
@@ -431,10 +529,91 @@ def main():
         # by DeepCNet(5,10) on a GTX 680 (Section 3.2) -- another machine, context only
         out["vs_baseline"] = round(value / PAPER_DIGITS_PER_S, 2)
         out["baseline_context"] = "paper: 3000 characters/s, DeepCNet(5,10) forward on digit pictures, GTX 680 (Section 3.2)"
-    if not args.no_cpu_baseline:
+    if cpu:
         log("[bench] cpu baseline (oracle)")
-        out["cpu_baseline"] = cpu_baseline(cfg, batches[0] if batches else None, Ws, bs, labels, args.dtype,
+        out["cpu_baseline"] = cpu_baseline(cfg, batches[0] if batches else None, Ws, bs, labels, dtype,
                                            infer=infer, paths=path_batches[0] if paths else None)
+    del net
+    torch.cuda.synchronize()
+    return out
+
+
+def traffic_key(kernel_name):
+    """File-name key of a kernel group's counter summary in profiles/."""
+    k = kernel_name.lower()
+    for a, b in ((":", ""), ("+", ""), ("(", ""), (")", ""), (",", ""), (" ", "_")):
+        k = k.replace(a, b)
+    while "__" in k:
+        k = k.replace("__", "_")
+    return k
+
+
+TABLE_ORDER = ["deepcnet4_20_strokes_b8", "deepcnet5_50_strokes_b100", "deepcnet5_50_strokes_m8_b100",
+               "deepcnet5_100_rgbpatch_b128", "deepcnet6_100_strokes_b64"]
+
+
+def write_table(path, rows, steps, warmup):
+    lines = ["# Throughput and roofline of every workload (one MI355X)", "",
+             f"Command: `python bench.py --table {os.path.relpath(path, ROOT)} --steps {steps} --warmup {warmup}`",
+             "", "samples/s from an unbracketed loop of the timed steps; the fractions from a second loop of the "
+             "same steps with every convolution launch, the weight gradients and the rulebook bracketed by HIP "
+             "events. Convolution GEMM fraction: 2 (n_s + 1) A C_in C_out per stage for each of forward, input "
+             "gradient and weight gradient, over the time of every convolution launch (softmax layer excluded), "
+             "against the dense MFMA peak of the dtype (bf16 2.5 PFLOP/s, f32 157.3 TFLOP/s). HBM fractions: "
+             "algorithmic bytes over event time, against 8 TB/s.", "",
+             "| workload | dtype | samples/s | ms/step | conv GEMM frac | dominant kernel | its frac | "
+             "rulebook µs, HBM frac | first layer µs, HBM frac |",
+             "|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        rb = r["hbm"].get("rulebook") or {}
+        cn = r["hbm"].get("conv_narrow") or {}
+        lines.append(
+            f"| {r['config']['workload']} | {r['dtype']} | {r['value']:,.0f} | {r['ms_per_step']:.3f} | "
+            f"{r['conv_gemm']['frac']:.4f} | {r['roofline']['kernel']} ({r['roofline']['avg_launch_us']:.1f} µs × "
+            f"{r['roofline']['launches_per_step']:g}) | {r['roofline']['frac']:.4f} | "
+            f"{rb.get('us_per_step', '–')}, {rb.get('frac', '–')} | {cn.get('us_per_step', '–')}, "
+            f"{cn.get('frac', '–')} |")
+    lines += ["", "Per kernel (µs per step, achieved fraction of the MFMA peak):", ""]
+    for r in rows:
+        lines.append(f"* {r['config']['workload']} {r['dtype']}: " + "; ".join(
+            f"{k['kernel']} {k['us_per_step']} µs, {k['frac']:.4f}" for k in r["kernels"]))
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--batches", type=int, default=8)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true")
+    ap.add_argument("--table", default=None, help="time every workload of the measurement plan, write a table")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported here "
+              "(the path would shard over samples with one all-reduce of dW/db per step)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+    if args.table:
+        rows = []
+        for name in TABLE_ORDER:
+            cfg = get_config(name)
+            for dt in cfg.dtypes:
+                rows.append(measure(cfg, dt, args.steps, args.warmup, args.batches, cpu=False))
+                print(json.dumps(rows[-1]), flush=True)
+        write_table(args.table, rows, args.steps, args.warmup)
+        return
+    out = measure(get_config(args.workload), args.dtype, args.steps, args.warmup, args.batches,
+                  cpu=not args.no_cpu_baseline)
     print(json.dumps(out), flush=True)
 
 

@@ -153,14 +153,18 @@ SSCN_API sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords,
 
 /* Synchronises `stream`, copies the L + 1 active-site counts (layer 0 =
  * input, then each stage) to h_counts, and returns any latched input error
- * (SSCN_ERR_OUT_OF_RANGE / SSCN_ERR_DUPLICATE_SITE). */
+ * (SSCN_ERR_OUT_OF_RANGE / SSCN_ERR_DUPLICATE_SITE).  It also returns
+ * SSCN_ERR_OUT_OF_RANGE, once, when a training sscn_forward since the last such
+ * report met a label outside [0, n_classes) (counts are still written). */
 SSCN_API sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream);
 
 /* Forward pass (Sections 2.1, 2.3): d_feats[n][c_in] (storage dtype, in the
  * order given to sscn_rulebook_build); h_W / h_b host arrays of n_conv + 1 device
  * pointers (weights in storage dtype, biases float32); d_labels[batch] int32
  * in [0, n_classes).  Writes d_logits[batch][n_classes] and *d_loss (mean
- * softmax cross-entropy), both float32.  With d_labels and d_loss both null
+ * softmax cross-entropy), both float32.  A label outside [0, n_classes) is
+ * latched on the device (the next sscn_layer_sizes returns
+ * SSCN_ERR_OUT_OF_RANGE); that sample's loss term and one-hot term are 0.  With d_labels and d_loss both null
  * the pass is inference only: it writes the logits, skips the loss and the
  * backward-only work, and a following sscn_backward returns
  * SSCN_ERR_BAD_STATE.  Exactly one of them null: SSCN_ERR_INVALID_ARGUMENT. */
@@ -296,6 +300,32 @@ SSCN_API sscn_status sscn_timing_enable(sscn_net* net, uint32_t class_mask);
  * (milliseconds) since the previous collect, and forgets those records. */
 SSCN_API sscn_status sscn_timing_collect(sscn_net* net, int32_t kernel_class, int32_t* launches, float* total_ms,
                                          void* stream);
+
+/* Launch roles and plans in the tags of sscn_timing_launches. */
+typedef enum {
+  SSCN_ROLE_FORWARD = 0,     /* a convolution's forward (with a fused pooling forward: pooled bit) */
+  SSCN_ROLE_INPUT_GRAD = 1,  /* a convolution's input gradient (with a fused pooling backward: routed bit) */
+  SSCN_ROLE_SOFTMAX_FWD = 2, /* the softmax layer's logits GEMM                                    */
+  SSCN_ROLE_SOFTMAX_DH = 3,  /* the softmax layer's input-gradient GEMM                            */
+  SSCN_ROLE_OTHER = 4        /* any other launch                                                  */
+} sscn_launch_role;
+enum { SSCN_PLAN_NONE = 15 }; /* plan field of a launch that is not a gather GEMM */
+
+/* Like sscn_timing_collect, but per launch: synchronises `stream`, writes the
+ * first min(capacity, count) timed launches of `kernel_class` since the
+ * previous collect, in launch order, as h_tags[i] and h_ms[i] (event-measured
+ * duration, milliseconds), sets *count to the number recorded, and forgets
+ * them.  tag = stage | role << 8 | plan << 12 | routed << 16 | pooled << 17:
+ * stage (bits 0-7) the stage the launch serves (1 .. L; 0 for the softmax
+ * layer and other launches), role (bits 8-11) an sscn_launch_role, plan
+ * (bits 12-15) the gather-GEMM tile plan (0: 128 x 128, 1: 128 x 64, 2: 64 x 64,
+ * 3: 32 x 64 LDS-tiled tiles, 4: the direct-operand 32 x 64 kernel) or
+ * SSCN_PLAN_NONE, routed (bit 16) an input gradient that runs the pooling
+ * backward below it in its epilogue, pooled (bit 17) a forward that runs the
+ * pooling layer above it in its epilogue.  Host arrays; capacity 0 (null
+ * arrays) just counts and forgets. */
+SSCN_API sscn_status sscn_timing_launches(sscn_net* net, int32_t kernel_class, int32_t* h_tags, float* h_ms,
+                                          int32_t capacity, int32_t* count, void* stream);
 
 /* Describes layer `layer` (0 .. L) of the bound workspace. */
 SSCN_API sscn_status sscn_layer_view_get(const sscn_net* net, int32_t layer, sscn_layer_view* out);

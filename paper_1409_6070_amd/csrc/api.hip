@@ -119,6 +119,7 @@ struct sscn_net {
   size_t ev_next = 0;
   struct Rec {
     int cls;
+    int32_t tag;  // launch tag (sscn_timing_launches)
     hipEvent_t a, b;
   };
   std::vector<Rec> recs;
@@ -142,7 +143,13 @@ static hipEvent_t next_event(sscn_net* net) {
 // A gather-GEMM launch; while its class is timed, the kernels themselves record
 // the start and end events (the span of the GEMM kernel and its split-K reduce,
 // without the dispatch latency that events recorded around the launch include).
-static hipError_t timed_gemm(sscn_net* net, GemmArgs g, int64_t max_rows, hipStream_t st) {
+// Launch tag of a timed record: stage | role << 8 | plan << 12 | routed << 16 | pooled << 17.
+static int32_t launch_tag(int stage, int role, int plan, bool routed = false, bool pooled = false) {
+  return (int32_t)(stage & 0xFF) | (role << 8) | (plan << 12) | ((int)routed << 16) | ((int)pooled << 17);
+}
+static const int32_t TAG_OTHER = launch_tag(0, SSCN_ROLE_OTHER, SSCN_PLAN_NONE);
+
+static hipError_t timed_gemm(sscn_net* net, GemmArgs g, int64_t max_rows, hipStream_t st, int stage, int role) {
   g.t_start = g.t_stop = nullptr;
   hipEvent_t a = nullptr, b = nullptr;
   if ((net->tmask & (1u << SSCN_KC_GATHER_GEMM)) && net->recs.size() < MAX_TIMED && max_rows - g.row_begin > 0) {
@@ -154,19 +161,20 @@ static hipError_t timed_gemm(sscn_net* net, GemmArgs g, int64_t max_rows, hipStr
     }
   }
   const hipError_t e = launch_gemm(net->bf16, g, max_rows, st);
-  if (g.t_start && e == hipSuccess) net->recs.push_back({SSCN_KC_GATHER_GEMM, a, b});
+  if (g.t_start && e == hipSuccess)
+    net->recs.push_back({SSCN_KC_GATHER_GEMM, launch_tag(stage, role, g.cfg, g.route != 0, g.pool_fwd != 0), a, b});
   return e;
 }
 
 template <class F>
-static hipError_t timed(sscn_net* net, int cls, hipStream_t st, F&& launch) {
+static hipError_t timed(sscn_net* net, int cls, hipStream_t st, F&& launch, int32_t tag = TAG_OTHER) {
   if (!(net->tmask & (1u << cls)) || net->recs.size() >= MAX_TIMED) return launch();
   hipEvent_t a = next_event(net), b = next_event(net);
   if (!a || !b) return launch();
   if (hipEventRecord(a, st) != hipSuccess) return hipErrorUnknown;
   hipError_t e = launch();
   if (hipEventRecord(b, st) != hipSuccess) return hipErrorUnknown;
-  net->recs.push_back({cls, a, b});
+  net->recs.push_back({cls, tag, a, b});
   return e;
 }
 
@@ -524,7 +532,8 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   }
   a.counts = net->counts;
   // this build's input bitmap and error word, and the next build's (cleared
-  // here); err[1] is the loss counter, err[0] spare
+  // here); err[1] is the loss counter, err[0] the label-error word of the
+  // training forward passes (cleared by the sscn_layer_sizes that reports it)
   const int par = net->rb_parity;
   uint64_t* bits0[2] = {net->L[0].bits, net->bits0_alt};
   a.L[0].bits = bits0[par];
@@ -564,11 +573,20 @@ sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream) {
   if (!net || !h_counts) return SSCN_ERR_INVALID_ARGUMENT;
   if (!net->built) return SSCN_ERR_BAD_STATE;
   hipStream_t st = (hipStream_t)stream;
-  int32_t err = 0;
+  int32_t err = 0, label_err = 0;
   if (hipMemcpyAsync(h_counts, net->counts, sizeof(int32_t) * net->nlayers, hipMemcpyDeviceToHost, st) != hipSuccess)
     return SSCN_ERR_HIP;
   if (hipMemcpyAsync(&err, net->err_cur, sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess) return SSCN_ERR_HIP;
+  if (hipMemcpyAsync(&label_err, net->err, sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return SSCN_ERR_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return SSCN_ERR_HIP;
+  if (label_err) {  // an earlier training forward saw a label outside [0, n_classes): report it once
+    static const int32_t zero = 0;
+    if (hipMemcpyAsync(net->err, &zero, sizeof(int32_t), hipMemcpyHostToDevice, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+      return SSCN_ERR_HIP;
+    return SSCN_ERR_OUT_OF_RANGE;
+  }
   if (err & ERRBIT_RANGE) return SSCN_ERR_OUT_OF_RANGE;
   if (err & ERRBIT_DUP) return SSCN_ERR_DUPLICATE_SITE;
   return SSCN_OK;
@@ -658,9 +676,10 @@ static hipError_t forward_stage(sscn_net* net, int s, hipStream_t st, bool fuse_
       max_rows = 4 * (Lp.cap + 1);
     }
     if (conv_narrow_ok(net->bf16, g, Lb.C))  // few input channels: no GEMM
-      return timed(net, SSCN_KC_CONV_NARROW, st,
-                   [&] { return launch_conv_narrow(net->bf16, g, Lb.C, max_rows, st); });
-    return timed_gemm(net, g, max_rows, st);
+      return timed(
+          net, SSCN_KC_CONV_NARROW, st, [&] { return launch_conv_narrow(net->bf16, g, Lb.C, max_rows, st); },
+          launch_tag(s, SSCN_ROLE_FORWARD, SSCN_PLAN_NONE, false, g.pool_fwd != 0));
+    return timed_gemm(net, g, max_rows, st, s, SSCN_ROLE_FORWARD);
   }
   return timed(net, SSCN_KC_POOL_FWD, st, [&] {
     return launch_pool_fwd(net->bf16, Lb.X, Lb.Cp, L.rules, L.X, L.Cp, L.argmax, L.Cp, net->counts + s, L.cap, st);
@@ -926,7 +945,7 @@ static hipError_t rows_below(sscn_net* net, int s, hipStream_t st, const ExtraTa
     g.pr.PM = rtiles;  // one partial per row tile
     if (routed) *routed = true;
   }
-  hipError_t e = timed_gemm(net, g, Lb.cap + 1, st);
+  hipError_t e = timed_gemm(net, g, Lb.cap + 1, st, s, SSCN_ROLE_INPUT_GRAD);
   const DropArgs dr = conv_drop(net, s);
   if (e == hipSuccess && dr.on)  // through the dropout of this convolution's input: rows >= 1, in place
     e = timed(net, SSCN_KC_DROPOUT, st, [&] {
@@ -998,12 +1017,12 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   g.row_begin = 0;
   set_plan(g, P.pf, P.rows_f, net->gpart);
   net->forwarded = false;
-  if (timed_gemm(net, g, net->batch, st) != hipSuccess)
+  if (timed_gemm(net, g, net->batch, st, 0, SSCN_ROLE_SOFTMAX_FWD) != hipSuccess)
     return SSCN_ERR_HIP;
   if (!train) return SSCN_OK;
   if (timed(net, SSCN_KC_HEAD, st, [&] {
         return launch_softmax_xent(net->bf16, d_logits, d_labels, net->batch, net->d.n_classes, net->dlogits,
-                                   net->dl_stride, net->loss_part, d_loss, net->err + 1, st);
+                                   net->dl_stride, net->loss_part, d_loss, net->err + 1, net->err, st);
       }) != hipSuccess)
     return SSCN_ERR_HIP;
   net->forwarded = true;
@@ -1045,7 +1064,7 @@ sscn_status sscn_backward(sscn_net* net, float* const* h_dW, float* const* h_db,
   g.row_begin = 0;
   set_plan(g, P.pd, P.rows_d, net->gpart);
   g.partials_only = g.ksplit > 1;  // the head backward sums the split-K partials itself
-  if (timed_gemm(net, g, net->batch, st) != hipSuccess)
+  if (timed_gemm(net, g, net->batch, st, 0, SSCN_ROLE_SOFTMAX_DH) != hipSuccess)
     return SSCN_ERR_HIP;
   // the head backward (scatter of dh into the top layer, with its ground sums)
   // runs in the stage loop below as the top convolution's sums launch
@@ -1389,6 +1408,33 @@ sscn_status sscn_timing_collect(sscn_net* net, int32_t kernel_class, int32_t* la
   if (net->recs.empty()) net->ev_next = 0;
   *launches = n;
   *total_ms = tot;
+  return SSCN_OK;
+}
+
+sscn_status sscn_timing_launches(sscn_net* net, int32_t kernel_class, int32_t* h_tags, float* h_ms,
+                                 int32_t capacity, int32_t* count, void* stream) {
+  if (!net || !count || kernel_class < 0 || kernel_class >= SSCN_KC_COUNT || capacity < 0 ||
+      (capacity > 0 && (!h_tags || !h_ms)))
+    return SSCN_ERR_INVALID_ARGUMENT;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return SSCN_ERR_HIP;
+  int32_t n = 0;
+  std::vector<sscn_net::Rec> keep;
+  for (const auto& r : net->recs) {
+    if (r.cls != kernel_class) {
+      keep.push_back(r);
+      continue;
+    }
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return SSCN_ERR_HIP;
+    if (n < capacity) {
+      h_tags[n] = r.tag;
+      h_ms[n] = ms;
+    }
+    ++n;
+  }
+  net->recs.swap(keep);
+  if (net->recs.empty()) net->ev_next = 0;
+  *count = n;
   return SSCN_OK;
 }
 

@@ -36,7 +36,7 @@ struct Elem<__bf16> {
 // ---------------------------------------------------------------------------
 // device error latch bits
 
-enum : int32_t { ERRBIT_RANGE = 1, ERRBIT_DUP = 2, ERRBIT_ORDER = 4 };
+enum : int32_t { ERRBIT_RANGE = 1, ERRBIT_DUP = 2, ERRBIT_ORDER = 4, ERRBIT_LABEL = 8 };
 
 // ---------------------------------------------------------------------------
 // per-layer geometry of the occupancy bitmaps

@@ -148,14 +148,7 @@ __device__ inline void store_staged(const GemmArgs& a, const T* Cs, int m0, int 
     const int r = v / NV, nv = v - r * NV;
     const int m = m0 + r, n = n0 + nv * VE;
     if (m < rows && n < a.out_cols) {
-      u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
-      if (a.epi == EPI_STORE_MASK) {  // the rectifier derivative of the layer below, 16 bytes at a time
-        const u32x4 y = *(const u32x4*)((const T*)a.mask + (int64_t)m * a.mask_stride + n);
-#pragma unroll
-        for (int e = 0; e < VE; ++e)
-          ((T*)&o)[e] = Elem<T>::from_f32(Elem<T>::to_f32(((const T*)&o)[e]) *
-                                          act_factor(Elem<T>::to_f32(((const T*)&y)[e]), a.slope));
-      }
+      const u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
       *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
       if constexpr (AC >= 0)
         if (m >= 1) pool_route_item<T, AC>(a.pr, m, n, (const T*)&o, acc);
@@ -357,7 +350,11 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int ml = wm * C::TM * 16 + i * 16 + g * 4 + r;
-            Cs[ml * CS + nl] = Elem<T>::from_f32(epi_value<T>(a, acc[i][j][r], bias[j]));
+            float v = epi_value<T>(a, acc[i][j][r], bias[j]);
+            if (a.epi == EPI_STORE_MASK && m0 + ml < rows && n0 + nl < a.out_cols)  // the rectifier
+              v *= act_factor(  // derivative of the layer below, before the one rounding to storage
+                  Elem<T>::to_f32(((const T*)a.mask)[(int64_t)(m0 + ml) * a.mask_stride + n0 + nl]), a.slope);
+            Cs[ml * CS + nl] = Elem<T>::from_f32(v);
           }
         }
       __syncthreads();

@@ -140,7 +140,8 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_softmax_xent(const float* __restrict__ logits,
                                                       const int32_t* __restrict__ labels, int32_t batch,
                                                       int32_t classes, T* dlogits, int32_t dl_stride,
-                                                      float* loss_part, float* loss, int32_t* counter) {
+                                                      float* loss_part, float* loss, int32_t* counter,
+                                                      int32_t* err) {
   constexpr int CACHE = 16;
   __shared__ float red[4];
   __shared__ int last;
@@ -186,6 +187,7 @@ __global__ void __launch_bounds__(256) k_softmax_xent(const float* __restrict__ 
   if (t == 0) {
     const bool ok = label >= 0 && label < classes;
     loss_part[b] = ok ? (logf(sum) + mx - z[label]) : 0.f;
+    if (!ok) atomicOr(err, ERRBIT_LABEL);  // reported by the next sscn_layer_sizes
     __threadfence();
     last = atomicAdd(counter, 1) == batch - 1;
   }
@@ -326,14 +328,14 @@ hipError_t launch_pack_all(bool bf16, const PackArgs& in, hipStream_t st) {
 
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
                                void* dlogits, int32_t dl_stride, float* loss_part, float* loss, int32_t* counter,
-                               hipStream_t st) {
+                               int32_t* err, hipStream_t st) {
   if (batch > 0) {
     if (bf16)
       hipLaunchKernelGGL(k_softmax_xent<__bf16>, dim3(batch), dim3(256), 0, st, logits, labels, batch, classes,
-                         (__bf16*)dlogits, dl_stride, loss_part, loss, counter);
+                         (__bf16*)dlogits, dl_stride, loss_part, loss, counter, err);
     else
       hipLaunchKernelGGL(k_softmax_xent<float>, dim3(batch), dim3(256), 0, st, logits, labels, batch, classes,
-                         (float*)dlogits, dl_stride, loss_part, loss, counter);
+                         (float*)dlogits, dl_stride, loss_part, loss, counter, err);
   } else {
     hipLaunchKernelGGL(k_loss_zero, dim3(1), dim3(1), 0, st, loss);
   }

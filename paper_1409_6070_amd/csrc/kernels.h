@@ -316,7 +316,7 @@ hipError_t launch_pack_all(bool bf16, const PackArgs& pa, hipStream_t st);
 // and sets it back to zero
 hipError_t launch_softmax_xent(bool bf16, const float* logits, const int32_t* labels, int32_t batch, int32_t classes,
                                void* dlogits, int32_t dl_stride, float* loss_part, float* loss, int32_t* counter,
-                               hipStream_t st);
+                               int32_t* err, hipStream_t st);
 
 
 // dropout.hip: Xd = X with rows 1 .. *n_rows dropped (row 0 copied; X == Xd:

@@ -33,6 +33,7 @@ EXPORTED = [
     "sscn_net_create", "sscn_net_destroy", "sscn_status_string", "sscn_net_num_params", "sscn_net_param_shape",
     "sscn_net_workspace_bytes", "sscn_rulebook_build", "sscn_layer_sizes", "sscn_forward", "sscn_backward",
     "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get", "sscn_timing_enable", "sscn_timing_collect",
+    "sscn_timing_launches",
     "sscn_set_dropout", "sscn_philox4x32_10", "sscn_sgd_step", "sscn_encode_workspace_bytes", "sscn_encode_strokes",
 ]
 KERNEL_CLASSES = ["rulebook", "gather_gemm", "wgrad", "wgrad_reduce", "pool_fwd", "pool_bwd", "head", "ground",
@@ -89,6 +90,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sscn_layer_view_get": (I32, [VP, I32, P(LayerView)]),
         "sscn_timing_enable": (I32, [VP, ctypes.c_uint32]),
         "sscn_timing_collect": (I32, [VP, I32, P(I32), P(ctypes.c_float), VP]),
+        "sscn_timing_launches": (I32, [VP, I32, P(I32), P(ctypes.c_float), I32, P(I32), VP]),
         "sscn_set_dropout": (I32, [VP, P(ctypes.c_double), I32, ctypes.c_uint64]),
         "sscn_philox4x32_10": (None, [P(ctypes.c_uint32), P(ctypes.c_uint32), P(ctypes.c_uint32)]),
         "sscn_sgd_step": (I32, [VP, P(VP), P(VP), P(VP), P(VP), P(VP), ctypes.c_float, ctypes.c_float, ctypes.c_float,
@@ -237,6 +239,16 @@ def sscn_timing_collect(net, kernel_class: int, stream):
     return n.value, ms.value
 
 
+def sscn_timing_launches(net, kernel_class: int, capacity: int, stream):
+    tags = (ctypes.c_int32 * max(capacity, 1))()
+    ms = (ctypes.c_float * max(capacity, 1))()
+    n = ctypes.c_int32()
+    _check(load_library().sscn_timing_launches(net, kernel_class, tags, ms, capacity, ctypes.byref(n), stream),
+           "sscn_timing_launches")
+    k = min(n.value, capacity)
+    return list(tags[:k]), list(ms[:k]), n.value
+
+
 # ---------------------------------------------------------------------------
 # convenience wrapper
 
@@ -343,6 +355,11 @@ class SparseDeepCNet:
     def timing_collect(self, kernel_class: str):
         """(launches, total milliseconds) of a class since the last collect."""
         return sscn_timing_collect(self.handle, KERNEL_CLASSES.index(kernel_class), _stream())
+
+    def timing_launches(self, kernel_class: str, capacity: int = 65536):
+        """Per-launch records of a class since the last collect: [(tag, milliseconds)], launch order."""
+        tags, ms, _ = sscn_timing_launches(self.handle, KERNEL_CLASSES.index(kernel_class), capacity, _stream())
+        return list(zip(tags, ms))
 
     def forward_stage(self, stage: int) -> None:
         sscn_forward_stage(self.handle, stage, _stream())

@@ -20,6 +20,40 @@ def conv_weight(W: np.ndarray, F: int, c_in: int) -> torch.Tensor:
     return w.permute(3, 2, 0, 1).contiguous()
 
 
+def cast_storage(t: torch.Tensor, mode: str) -> torch.Tensor:
+    """Value of a float64 tensor after storing it in the mode's type: float32, or bfloat16 through
+    float32 (the device accumulates in float32 and rounds that to bfloat16), by torch's casts."""
+    if mode == "f64":
+        return t
+    t32 = t.to(torch.float32)
+    return (t32 if mode == "f32" else t32.to(torch.bfloat16)).to(torch.float64)
+
+
+class StoreValue(torch.autograd.Function):
+    """Rounds a value to the storage type; the gradient passes unchanged."""
+
+    @staticmethod
+    def forward(ctx, x, mode):
+        return cast_storage(x, mode)
+
+    @staticmethod
+    def backward(ctx, g):
+        return g, None
+
+
+class StoreGrad(torch.autograd.Function):
+    """Leaves a value unchanged; rounds the gradient flowing back through it to the storage type."""
+
+    @staticmethod
+    def forward(ctx, x, mode):
+        ctx.mode = mode
+        return x.view_as(x)
+
+    @staticmethod
+    def backward(ctx, g):
+        return cast_storage(g, ctx.mode), None
+
+
 def dense_grid(coords, feats, batch, N, c_in):
     x = torch.zeros(batch, c_in, N, N, dtype=torch.float64)
     coords = np.asarray(coords).reshape(-1, 3)
@@ -36,25 +70,34 @@ class DenseDeepCNet:
     (torch's leaky_relu with negative slope 1/3) on every hidden layer.
     """
 
-    def __init__(self, ell, k, c_in, n_classes, arch="deepcnet"):
+    def __init__(self, ell, k, c_in, n_classes, arch="deepcnet", mode="f64"):
         self.ell, self.k, self.c_in, self.n_classes = ell, k, c_in, n_classes
         self.arch = arch
         self.N = 3 * 2 ** ell
+        # "f64": no rounding.  "f32" / "bf16": every stored quantity of the device path rounded to
+        # that type where it is stored -- the input, the weights, every layer's output, the
+        # logits (float32), the loss gradient at the logits, every convolution's dL/dZ and every
+        # pooling layer's and the input's dL/dX -- with all products and sums in float64.
+        self.mode = mode
 
     def run(self, coords, feats, batch, Ws, bs, labels, masks=None):
         """Forward and autograd backward.  ``masks``: optional per-level dropout multipliers,
         one per convolution that is not 1x1 ([B, C_in, S, S], multiplying that convolution's
         input) and one for the softmax layer's input ([B, C]); None entries mean no dropout."""
         masks = masks or [None] * (self.ell + 2)
-        x = dense_grid(coords, feats, batch, self.N, self.c_in).requires_grad_(True)
+        m = self.mode
+        sv = (lambda t: t) if m == "f64" else (lambda t: StoreValue.apply(t, m))
+        sg = (lambda t: t) if m == "f64" else (lambda t: StoreGrad.apply(t, m))
+        x = cast_storage(dense_grid(coords, feats, batch, self.N, self.c_in), m).requires_grad_(True)
         params = []
         for W, b in zip(Ws, bs):
-            params.append(torch.tensor(np.asarray(W), dtype=torch.float64, requires_grad=True))
+            w = cast_storage(torch.tensor(np.asarray(W), dtype=torch.float64), m)
+            params.append(w.requires_grad_(True))
             params.append(torch.tensor(np.asarray(b), dtype=torch.float64, requires_grad=True))
         nin = self.arch == "deepcnin"
         act = (lambda z: Fn.leaky_relu(z, 1.0 / 3.0)) if nin else torch.relu
         Zs, Ys = [], []  # per stage: pre-activation (conv) and output
-        h = x
+        h = sg(x)  # the input's gradient is stored
         c = self.c_in
         pi = 0
         di = 0
@@ -65,22 +108,26 @@ class DenseDeepCNet:
             pi += 1
             if F > 1:
                 if masks[di] is not None:
+                    # the dropped copy is stored: rounded to float32, then to the storage type
                     h = h * torch.as_tensor(masks[di], dtype=torch.float64)
+                    if m != "f64":
+                        h = sv(StoreValue.apply(h, "f32"))
                 di += 1
             wt = W.reshape(F, F, c, W.shape[1]).permute(3, 2, 0, 1)
             z = Fn.conv2d(h, wt) + b.view(1, -1, 1, 1)
             z.retain_grad()
-            y = act(z)
+            y = sv(act(sg(z)))  # dL/dZ and the output are stored
             Zs.append(z)
             Ys.append(y)
             return y, W.shape[1]
 
         for li in range(self.ell + 1):
             if li > 0:
-                h = Fn.max_pool2d(h, 2)
-                h.retain_grad()
+                pooled = Fn.max_pool2d(h, 2)
+                pooled.retain_grad()
                 Zs.append(None)
-                Ys.append(h)
+                Ys.append(pooled)
+                h = sg(pooled)  # the pooling layer's dL/dX is stored
                 if nin:
                     h, c = conv(h, 1, c)
             h, c = conv(h, 3 if li == 0 else 2, c)
@@ -90,7 +137,11 @@ class DenseDeepCNet:
         feat = h[:, :, 0, 0]
         if masks[-1] is not None:
             feat = feat * torch.as_tensor(masks[-1], dtype=torch.float64)
+            if m != "f64":
+                feat = sv(StoreValue.apply(feat, "f32"))
         logits = feat @ params[-2] + params[-1]
+        if m != "f64":  # logits are float32; the loss gradient at them is stored
+            logits = sg(StoreValue.apply(logits, "f32"))
         loss = Fn.cross_entropy(logits, torch.tensor(np.asarray(labels), dtype=torch.int64))
         loss.backward()
         self.x, self.params, self.Zs, self.Ys = x, params, Zs, Ys

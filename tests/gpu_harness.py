@@ -1,22 +1,37 @@
 """Runs the HIP path and the CPU oracle on the same seeded inputs and compares them.
 
-Tolerances: float32 storage 1e-4, bfloat16 storage 2e-2, as the normwise
-relative error max|gpu - ref| / max|ref| of each tensor.  Integer structures
-(active counts, site lists, window lists and their transposes) must match
-exactly.
+Integer structures (active counts, site lists, window lists and their
+transposes) must match exactly.
 
-Two discrete decisions are taken from floating-point values: the pool argmax
-and the ReLU derivative [Z > 0].  Each must match the oracle's exactly except
-at a near tie -- two window values within the tolerance of each other, or a
-pre-activation within the tolerance of zero -- which a different (equally
-valid) summation order can decide the other way.  Both decisions are then
-correct, but they route a gradient differently, so gradients are compared with
-the oracle's backward evaluated under the GPU's decision at those validated
-near ties (and under its own decision everywhere else, which is everywhere
-the two agree).  The oracle's arithmetic is unchanged; only which of two valid
-answers it follows is aligned.
+Floating point.  Every feature and gradient matrix is compared in two parts,
+each at its own scale: row 0 (the ground state of Section 2.3; for a gradient,
+the sum over every inactive site) and rows >= 1 (the active sites).  For each
+part the normwise relative error max|gpu - ref| / max|ref| must stay within the
+tolerance (float32 storage 1e-4, bfloat16 storage 2e-2).  The elementwise
+relative error |gpu - ref| / max(|ref|, 1e-3 max|ref|) of rows >= 1 is reported
+beside it and, for float32 storage, bounded by 1e-2 (for bfloat16 a small
+element's error is set by the rounding of the large terms of its sum, so the
+elementwise figure only reports).  Logits, loss and the parameter gradients
+are single tensors.
+
+Discrete decisions.  The pool argmax and the rectifier branch are taken from
+floating-point values.  The pooling kernel's own decision is checked exactly
+on every pooling layer: each stored maximum and argmax must be the first
+maximum of the GPU's own stored window values.  Against the oracle a decision
+may differ only within the rounding band of the sums that decide it: a
+rectifier branch where |Z| <= eps * (sum_k |w_k x_k| + |b|), an argmax where the
+oracle's gap between the two window values is within eps times the sum of
+both values' magnitude sums (eps the storage type's unit roundoff, the
+magnitudes over the oracle's inputs of the deciding convolution rows), and
+the gap must be covered by the two values' own differences between GPU and
+oracle.  At most 0.1% of a layer's decisions (and at least 2) may differ; the
+counts are printed.  Gradients are then compared with the oracle's backward
+evaluated under the GPU's decision at those validated near ties (and under its
+own everywhere else): the oracle's arithmetic is unchanged, only which of two
+valid answers it follows is aligned.
 """
 
+import math
 import sys
 
 import numpy as np
@@ -25,7 +40,31 @@ import torch
 from oracle import SparseDeepCNet as Oracle
 from paper_1409_6070_amd.sscn import SparseDeepCNet as GpuNet
 
+
+def conv_magnitude(o, s, rows, cols):
+    """sum_k |w_kc x_k| + |b_c| of convolution layer s (1 ..) at the given rows and channels, from the
+    oracle's own inputs of that convolution (its dropped copy where dropout applies)."""
+    L = o.layers[s]
+    ci = sum(1 for t in o.stages[:s - 1] if t.kind == "conv")
+    V = np.abs(L.extra["Xin"][L.R[rows]].reshape(rows.size, -1))
+    return (V * np.abs(o.Ws[ci][:, cols]).T).sum(axis=1) + np.abs(o.bs[ci][cols])
+
 TOL = {"f32": 1e-4, "bf16": 2e-2}
+# unit roundoff of the storage types (half an ulp at 1.0)
+EPS = {"f32": 2.0 ** -24, "bf16": 2.0 ** -8}
+# relative error floor of the elementwise check: a fraction of the part's largest value
+ELEM_FLOOR = 1e-3
+# bound on the elementwise error of rows >= 1 (None: reported only)
+ELEM_TOL = {"f32": 1e-2, "bf16": None}
+# A decision may differ only within the rounding band of the sums that decide it: a
+# differing rectifier branch only where |Z| <= TIE x eps x (sum_k |w_k x_k| + |b|), a
+# differing argmax only where the oracle's gap between the two window values is within
+# TIE x eps x (the same magnitude sums of both values), eps the storage type's unit
+# roundoff and the magnitudes over the oracle's inputs of the convolution row.
+TIE = 1.0
+# at most this fraction of a layer's decisions may differ (and at least FLIP_MIN)
+FLIP_FRAC = 1e-3
+FLIP_MIN = 2
 
 
 def log(msg):
@@ -39,6 +78,7 @@ def to_dtype(x: np.ndarray, dtype: str) -> torch.Tensor:
 
 
 def rel_err(got, ref) -> float:
+    """Normwise relative error max|got - ref| / max|ref| (absolute when ref is all zero)."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert got.shape == ref.shape, (got.shape, ref.shape)
@@ -49,6 +89,33 @@ def rel_err(got, ref) -> float:
     if scale == 0:
         return float(diff)
     return float(diff / scale)
+
+
+def elem_err(got, ref, floor=ELEM_FLOOR) -> float:
+    """Elementwise relative error max |got - ref| / max(|ref|, floor * max|ref|)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    scale = np.abs(ref).max()
+    if scale == 0:
+        return float(np.abs(got - ref).max())
+    return float((np.abs(got - ref) / np.maximum(np.abs(ref), floor * scale)).max())
+
+
+def split_err(got, ref):
+    """(row 0 normwise, rows >= 1 normwise, rows >= 1 elementwise) of a row matrix."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    return rel_err(got[:1], ref[:1]), rel_err(got[1:], ref[1:]), elem_err(got[1:], ref[1:])
+
+
+def storage_ulp(x, dtype: str) -> np.ndarray:
+    """Spacing of the storage type's numbers at |x| (at the smallest normal for 0)."""
+    a = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), np.finfo(np.float32).tiny)
+    e = np.floor(np.log2(a))
+    return np.exp2(e - (23 if dtype == "f32" else 7))
 
 
 class Pair:
@@ -122,7 +189,6 @@ def decode_sites(keys, S):
 def expected_rules_t(R: np.ndarray, n_below: int, kind: str):
     """Transposed window lists from the oracle's window lists."""
     A = R.shape[1]
-    n = R.shape[0] - 1
     if kind == "conv":
         Rt = -np.ones((n_below + 1, A), np.int64)
         o, f = np.nonzero(R[1:] > 0)
@@ -150,59 +216,126 @@ def check_structure(p: Pair):
                                       err_msg=f"transposed rules layer {s}")
 
 
+def flip_cap(n_decisions: int) -> int:
+    return max(FLIP_MIN, int(math.floor(FLIP_FRAC * n_decisions)))
+
+
+def check_pool_self(v_pool, X_below_gpu, R):
+    """The pooling kernel's own decision, exactly: max and first-max argmax of the GPU's stored window values."""
+    V = X_below_gpu[R]  # [n + 1, 4, C]
+    want_arg = np.argmax(V, axis=1)
+    np.testing.assert_array_equal(v_pool["argmax"], want_arg, err_msg="argmax is not the first maximum of the "
+                                  "GPU's own window values")
+    np.testing.assert_array_equal(v_pool["X"], V.max(axis=1), err_msg="pooled value is not the maximum of the "
+                                  "GPU's own window values")
+
+
 def check_values(p: Pair, tol=None, check_grads=True):
-    """Features, argmax, logits, loss, gradients: normwise within the dtype's tolerance.
+    """Features, argmax, logits, loss, gradients (see the module docstring).
 
     Every error is measured and printed before the first failing one is asserted."""
+    p.report, p.stats, p.failures = {}, {}, []
     try:
-        return _check_values(p, tol, check_grads)
+        _check_values(p, tol, check_grads)
     finally:
-        rep = getattr(p, "report", {})
+        rep = p.report
         if rep:
             log("  " + " ".join(f"{k}={v:.2g}" if isinstance(v, float) else f"{k}={v}" for k, v in rep.items()))
+    if p.failures:
+        raise AssertionError("; ".join(p.failures))
+    return p.report
+
+
+def _expect(p, ok, msg):
+    if not ok:
+        p.failures.append(msg)
+
+
+def _check_matrix(p, name, got, ref, tol):
+    e0, e1, ee = split_err(got, ref)
+    p.report[f"{name}r0"] = e0
+    p.report[f"{name}"] = e1
+    p.stats[name] = {"row0": e0, "rows": e1, "elem": ee}
+    _expect(p, e0 <= tol, f"{name} row 0: rel err {e0:.3g} > {tol}")
+    _expect(p, e1 <= tol, f"{name} rows >= 1: rel err {e1:.3g} > {tol}")
+    et = ELEM_TOL[p.dtype]
+    _expect(p, et is None or ee <= et, f"{name} rows >= 1: elementwise rel err {ee:.3g} > {et}")
+
+
+def _check_tensor(p, name, got, ref, tol):
+    e = rel_err(got, ref)
+    ee = elem_err(got, ref)
+    p.report[name] = e
+    p.stats[name] = {"rows": e, "elem": ee}
+    _expect(p, e <= tol, f"{name}: rel err {e:.3g} > {tol}")
 
 
 def _check_values(p: Pair, tol=None, check_grads=True):
     o = p.o
-    tol = tol if tol is not None else TOL[p.dtype]
-    report = p.report = {}
+    dt = p.dtype
+    tol = tol if tol is not None else TOL[dt]
     flipped = []
     relu_flips = []
+    X_gpu = []
     for s, L in enumerate(o.layers):
         v = p.view(s)
-        e = rel_err(v["X"], L.X)
-        report[f"X{s}"] = e
-        assert e <= tol, f"features layer {s}: rel err {e:.3g} > {tol}"
+        X_gpu.append(v["X"])
+        _check_matrix(p, f"X{s}", v["X"], L.X, tol)
         if "argmax" in v:
             below = o.layers[s - 1]
-            V = below.X[L.R]  # [n+1, 4, C]
+            check_pool_self(v, X_gpu[s - 1], L.R)
+            Vo = below.X[L.R]  # [n + 1, 4, C] the oracle's window values
+            Vg = X_gpu[s - 1][L.R]
             bad = np.nonzero(v["argmax"] != L.argmax)
-            if bad[0].size:
+            nb = int(bad[0].size)
+            st = {"decisions": int(L.argmax.size), "flips": nb, "cap": flip_cap(L.argmax.size)}
+            if nb:
                 rows, cols = bad
-                gap = np.abs(V[rows, L.argmax[rows, cols], cols] - V[rows, v["argmax"][rows, cols].astype(np.int64), cols])
-                scale = max(np.abs(below.X).max(), 1e-30)
-                assert np.all(gap <= tol * scale), f"argmax layer {s}: {rows.size} mismatches, max gap {gap.max()}"
-            report[f"argmax{s}_mismatch"] = int(bad[0].size)
-            if bad[0].size:
-                flipped.append((s, bad, v["argmax"][bad].astype(np.int64)))
+                ao, ag = L.argmax[rows, cols], v["argmax"][rows, cols].astype(np.int64)
+                vo_o, vo_g = Vo[rows, ao, cols], Vo[rows, ag, cols]
+                gap = vo_o - vo_g  # >= 0: the oracle's choice is its first maximum
+                cover = np.abs(Vg[rows, ao, cols] - vo_o) + np.abs(Vg[rows, ag, cols] - vo_g)
+                mag = conv_magnitude(o, s - 1, L.R[rows, ao], cols) + conv_magnitude(o, s - 1, L.R[rows, ag], cols)
+                band = gap / (EPS[dt] * np.maximum(mag, np.finfo(np.float32).tiny))
+                st.update(max_band=float(band.max()), uncovered=int((gap > cover).sum()),
+                          max_gap_ulps=float((gap / storage_ulp(np.maximum(np.abs(vo_o), np.abs(vo_g)), dt)).max()))
+                _expect(p, nb <= st["cap"], f"argmax layer {s}: {nb} decisions differ (cap {st['cap']})")
+                _expect(p, st["uncovered"] == 0, f"argmax layer {s}: {st['uncovered']} differing decisions not "
+                        "explained by the inputs' differences")
+                _expect(p, band.max() <= TIE, f"argmax layer {s}: oracle gap {band.max():.2f} x eps x magnitude "
+                        f"at a differing decision (band {TIE})")
+                flipped.append((s, bad, ag))
+            p.stats[f"argmax{s}"] = st
+            p.report[f"argmax{s}_flips"] = nb
         if L.relu_on is not None:
             # the GPU's rectifier branch from its stored output: ReLU y > 0; leaky x/3: sign bit clear
             gpu_on = v["X"] > 0 if o.slope == 0.0 else ~np.signbit(v["X"])
             bad = np.nonzero(gpu_on != L.relu_on)
-            if bad[0].size:
-                scale = max(np.abs(L.X).max(), 1e-30)
-                near = np.maximum(np.abs(L.X[bad]), np.abs(v["X"][bad]))
-                assert np.all(near <= tol * scale), f"rectifier decision layer {s}: {bad[0].size} flips, max |Z| {near.max()}"
+            nb = int(bad[0].size)
+            st = {"decisions": int(L.relu_on.size), "flips": nb, "cap": flip_cap(L.relu_on.size)}
+            if nb:
+                # |Z| at a differing branch against the rounding scale of its own sum
+                rows, cols = bad
+                cond = conv_magnitude(o, s, rows, cols)
+                # |Z| from each side's stored output (x/3 below zero for the leaky rectifier)
+                xo, xg = L.X[bad], v["X"][bad].astype(np.float64)
+                un = 1.0 / o.slope if o.slope else 1.0
+                z = np.maximum(np.abs(xo) * np.where(xo < 0, un, 1.0), np.abs(xg) * np.where(np.signbit(xg), un, 1.0))
+                band = z / (EPS[dt] * np.maximum(cond, np.finfo(np.float32).tiny))
+                st["max_band"] = float(band.max())
+                _expect(p, nb <= st["cap"], f"rectifier layer {s}: {nb} decisions differ (cap {st['cap']})")
+                _expect(p, band.max() <= TIE, f"rectifier layer {s}: |Z| {band.max():.2f} x eps x magnitude at a "
+                        f"differing decision (band {TIE})")
                 relu_flips.append((s, gpu_on))
-            report[f"relu{s}_mismatch"] = int(bad[0].size)
-    e = rel_err(p.logits, o.logits)
-    report["logits"] = e
-    assert e <= tol, f"logits rel err {e}"
+            p.stats[f"relu{s}"] = st
+            p.report[f"relu{s}_flips"] = nb
+    _check_tensor(p, "logits", p.logits, o.logits, tol)
     e = abs(p.loss - o.loss) / max(abs(o.loss), 1e-30)
-    report["loss"] = e
-    assert e <= tol, f"loss {p.loss} vs {o.loss}"
+    p.report["loss"] = e
+    p.stats["loss"] = {"rows": e}
+    _expect(p, e <= tol, f"loss {p.loss} vs {o.loss}")
     if not check_grads:
-        return report
+        return
     if flipped or relu_flips:
         # every differing decision was validated above as a near tie
         for s, idx, gpu_choice in flipped:
@@ -211,22 +344,12 @@ def _check_values(p: Pair, tol=None, check_grads=True):
             o.layers[s].relu_on = gpu_on
         o.backward()
     for i, (a, b) in enumerate(zip(p.dW, o.dW)):
-        e = rel_err(a, b)
-        report[f"dW{i}"] = e
-        assert e <= tol, f"dW[{i}] rel err {e:.3g}"
+        _check_tensor(p, f"dW{i}", a, b, tol)
     for i, (a, b) in enumerate(zip(p.db, o.db)):
-        e = rel_err(a, b)
-        report[f"db{i}"] = e
-        assert e <= tol, f"db[{i}] rel err {e:.3g}"
+        _check_tensor(p, f"db{i}", a, b, tol)
     for s, L in enumerate(o.layers):
         if s == 0 and not p.want_dfeats:
             continue
-        v = p.view(s)
-        e = rel_err(v["G"], L.grad)
-        report[f"G{s}"] = e
-        assert e <= tol, f"gradient layer {s}: rel err {e:.3g}"
+        _check_matrix(p, f"G{s}", p.view(s)["G"], L.grad, tol)
     if p.want_dfeats:
-        e = rel_err(p.dfeats, o.dfeats)
-        report["dfeats"] = e
-        assert e <= tol, f"dfeats rel err {e}"
-    return report
+        _check_tensor(p, "dfeats", p.dfeats, o.dfeats, tol)

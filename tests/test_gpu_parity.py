@@ -147,8 +147,14 @@ def test_stage_kernels_on_oracle_inputs(dtype):
         assert e <= TOL[dtype], f"backward stage {s}: {e}"
 
 
-@pytest.mark.parametrize("name,dtype", [("deepcnet4_20_strokes_b8", "f32"), ("deepcnet4_20_strokes_b8", "bf16"),
-                                        ("deepcnet5_50_strokes_b100", "bf16"), ("deepcnin5_50_strokes_b100", "bf16")])
+# every training workload's tile plans, both dtypes of the first two
+PLAN_CASES = [("deepcnet4_20_strokes_b8", "f32"), ("deepcnet4_20_strokes_b8", "bf16"),
+              ("deepcnet5_50_strokes_b100", "f32"), ("deepcnet5_50_strokes_b100", "bf16"),
+              ("deepcnet5_50_strokes_m8_b100", "bf16"), ("deepcnet5_100_rgbpatch_b128", "bf16"),
+              ("deepcnet6_100_strokes_b64", "bf16"), ("deepcnin5_50_strokes_b100", "bf16")]
+
+
+@pytest.mark.parametrize("name,dtype", PLAN_CASES, ids=[f"{n}-{d}" for n, d in PLAN_CASES])
 def test_fused_pool_forward_matches_stage_kernels(name, dtype):
     """The full forward pass runs each pooling layer in the epilogue of the convolution below it
     (GEMM rows in pooling-window order); the per-stage entry point runs the separate kernels.
@@ -251,19 +257,24 @@ def test_empty_inputs(dtype):
     check_values(pair)
 
 
-def test_repeat_runs_are_bitwise_identical():
-    cfg = get_config("deepcnet5_50_strokes_b100")
-    b, Ws, bs, labels = _config_case(cfg, "bf16", index=1)
-    log("[determinism] deepcnet5_50 bf16 batch 1")
-    pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, "bf16",
-                run_oracle=False)
+@pytest.mark.parametrize("name,dtype", PLAN_CASES, ids=[f"{n}-{d}" for n, d in PLAN_CASES])
+def test_repeat_runs_are_bitwise_identical(name, dtype):
+    """No float atomics and fixed reduction orders: two runs of a step give the same bits in every
+    layer's features and gradients, the logits, the loss and every parameter gradient."""
+    cfg = get_config(name)
+    b, Ws, bs, labels = _config_case(cfg, dtype, index=1)
+    log(f"[determinism] {name} {dtype} batch 1")
+    pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, dtype,
+                run_oracle=False, arch=cfg.arch)
     outs = []
     for _ in range(2):
         pair.run_gpu()
-        outs.append([pair.logits.copy(), *[w.copy() for w in pair.dW], *[x.copy() for x in pair.db],
-                     pair.dfeats.copy(), pair.view(3)["X"].copy(), pair.view(4)["G"].copy()])
-    for a, c in zip(*outs):
-        np.testing.assert_array_equal(a, c)
+        layers = [pair.view(s) for s in range(len(pair.counts))]
+        outs.append([pair.logits.copy(), np.float64(pair.loss), *[w.copy() for w in pair.dW],
+                     *[x.copy() for x in pair.db], pair.dfeats.copy(), *[v["X"].copy() for v in layers],
+                     *[v["G"].copy() for v in layers]])
+    for i, (a, c) in enumerate(zip(*outs)):
+        np.testing.assert_array_equal(a, c, err_msg=f"output {i}")
 
 
 @pytest.mark.parametrize("bad,status", [("dup", "SSCN_ERR_DUPLICATE_SITE"), ("range", "SSCN_ERR_OUT_OF_RANGE"),
@@ -376,3 +387,31 @@ def test_small_deepcnin(case, dtype):
     pair = Pair(ell, k, c_in, ncls, batch, coords, feats, Ws, bs, labels, dtype, arch="deepcnin").run_gpu()
     check_structure(pair)
     check_values(pair)
+
+
+def test_out_of_range_label_is_reported():
+    """A training forward with a label outside [0, n_classes) latches an error that the next
+    sscn_layer_sizes reports once; the bad sample contributes nothing to the loss."""
+    from paper_1409_6070_amd import sscn
+    log("[errors] label out of range")
+    coords, feats = _sparse_case(70, 2, 3, 0.2, 1)
+    Ws, bs = he_params(2, 4, 1, 5, 170)
+    good = random_labels(3, 5, 270)
+    for bad_label in (5, -1):
+        labels = good.copy()
+        labels[1] = bad_label
+        pair = Pair(2, 4, 1, 5, 3, coords, feats, Ws, bs, good, "f32")
+        pair.labels_d = torch.tensor(labels, dtype=torch.int32).cuda()
+        pair.run_gpu()
+        # samples 0 and 2 as the oracle has them; sample 1 adds nothing to the mean
+        o = pair.o
+        z = o.logits - o.logits.max(axis=1, keepdims=True)
+        terms = np.log(np.exp(z).sum(axis=1)) - z[np.arange(3), good]
+        want = (terms[0] + terms[2]) / 3
+        assert abs(pair.loss - want) <= 1e-5 * abs(want)
+        net = pair.net
+        net.rulebook_build(pair.coords_d, 3)
+        with pytest.raises(sscn.SSCNError) as e:
+            net.layer_sizes()
+        assert e.value.name == "SSCN_ERR_OUT_OF_RANGE"
+        assert net.layer_sizes() == o.layer_sizes()  # reported once
