@@ -255,6 +255,22 @@ SSCN_API sscn_status sscn_encode_strokes(int32_t N, int32_t dtype, const int32_t
                                          int32_t max_sites, int32_t* h_count, void* d_ws, size_t ws_bytes,
                                          void* stream);
 
+/* sscn_encode_strokes for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments and results without d_ws / ws_bytes.  Its
+ * scratch is a fixed array of SSCN_ENCODE_STATIC_SCRATCH_BYTES in device memory
+ * that every GPU the library runs on holds until the process ends; the call
+ * itself allocates and frees nothing.  It returns SSCN_ERR_WORKSPACE when
+ * sscn_encode_workspace_bytes(N, batch, max_sites) exceeds that size, and
+ * SSCN_ERR_HIP if the scratch's device address cannot be obtained.  All calls on
+ * one GPU share its scratch: calls that overlap on one GPU (concurrent streams
+ * or host threads) race and must be serialised by the caller. */
+#define SSCN_ENCODE_STATIC_SCRATCH_BYTES ((size_t)16 << 20)
+SSCN_API sscn_status sscn_encode_strokes_static(int32_t N, int32_t dtype, const int32_t* d_points, int32_t n_points,
+                                                const int32_t* d_stroke_begin, const int32_t* d_stroke_sample,
+                                                int32_t n_strokes, int32_t batch, int32_t* d_coords, void* d_feats,
+                                                int32_t max_sites, int32_t* h_count, void* stream);
+
 /* Runs only stage s (1 .. L) of the forward or backward pass on the
  * current workspace contents, with the parameters of the last sscn_forward /
  * sscn_backward.  For checking one kernel group against known inputs.  A

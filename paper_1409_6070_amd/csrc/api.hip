@@ -5,6 +5,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -1311,10 +1312,33 @@ sscn_status sscn_encode_workspace_bytes(int32_t N, int32_t batch_max, int32_t ma
   return SSCN_OK;
 }
 
-sscn_status sscn_encode_strokes(int32_t N, int32_t dtype, const int32_t* d_points, int32_t n_points,
-                                const int32_t* d_stroke_begin, const int32_t* d_stroke_sample, int32_t n_strokes,
-                                int32_t batch, int32_t* d_coords, void* d_feats, int32_t max_sites, int32_t* h_count,
-                                void* d_ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+// The scratch of sscn_encode_strokes_static: one copy per GPU (a device
+// variable of this code object), held until the process ends.  Host code never
+// uses its name as an address: static_scratch() returns the device address
+// taken with hipGetSymbolAddress on each device once.
+static __device__ __align__(256) unsigned char scratch[SSCN_ENCODE_STATIC_SCRATCH_BYTES];
+
+static void* static_scratch() {
+  constexpr int MAX_DEVICES = 64;
+  static std::mutex mu;
+  static void* ptr[MAX_DEVICES] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    ptr[dev] = p;
+  }
+  return ptr[dev];
+}
+
+static sscn_status encode_strokes(int32_t N, int32_t dtype, const int32_t* d_points, int32_t n_points,
+                                  const int32_t* d_stroke_begin, const int32_t* d_stroke_sample, int32_t n_strokes,
+                                  int32_t batch, int32_t* d_coords, void* d_feats, int32_t max_sites,
+                                  int32_t* h_count, void* d_ws, size_t ws_bytes, void* stream) {
   if (!h_count || !encode_dims_ok(N, batch, max_sites) || n_points < 0 || n_strokes < 0) return SSCN_ERR_INVALID_ARGUMENT;
   if (dtype != SSCN_F32 && dtype != SSCN_BF16) return SSCN_ERR_INVALID_ARGUMENT;
   if (!d_stroke_begin || (n_points > 0 && !d_points) || (n_strokes > 0 && !d_stroke_sample) ||
@@ -1355,6 +1379,29 @@ sscn_status sscn_encode_strokes(int32_t N, int32_t dtype, const int32_t* d_point
   if (res[1] & ERRBIT_RANGE) return SSCN_ERR_OUT_OF_RANGE;
   if (res[0] > max_sites) return SSCN_ERR_CAPACITY;
   return SSCN_OK;
+}
+
+extern "C" {
+
+sscn_status sscn_encode_strokes(int32_t N, int32_t dtype, const int32_t* d_points, int32_t n_points,
+                                const int32_t* d_stroke_begin, const int32_t* d_stroke_sample, int32_t n_strokes,
+                                int32_t batch, int32_t* d_coords, void* d_feats, int32_t max_sites, int32_t* h_count,
+                                void* d_ws, size_t ws_bytes, void* stream) {
+  return encode_strokes(N, dtype, d_points, n_points, d_stroke_begin, d_stroke_sample, n_strokes, batch, d_coords,
+                        d_feats, max_sites, h_count, d_ws, ws_bytes, stream);
+}
+
+sscn_status sscn_encode_strokes_static(int32_t N, int32_t dtype, const int32_t* d_points, int32_t n_points,
+                                       const int32_t* d_stroke_begin, const int32_t* d_stroke_sample,
+                                       int32_t n_strokes, int32_t batch, int32_t* d_coords, void* d_feats,
+                                       int32_t max_sites, int32_t* h_count, void* stream) {
+  if (!h_count || !encode_dims_ok(N, batch, max_sites)) return SSCN_ERR_INVALID_ARGUMENT;
+  size_t offs[7];
+  if (encode_bytes(N, batch, max_sites, offs) > SSCN_ENCODE_STATIC_SCRATCH_BYTES) return SSCN_ERR_WORKSPACE;
+  void* ws = static_scratch();
+  if (!ws) return SSCN_ERR_HIP;
+  return encode_strokes(N, dtype, d_points, n_points, d_stroke_begin, d_stroke_sample, n_strokes, batch, d_coords,
+                        d_feats, max_sites, h_count, ws, SSCN_ENCODE_STATIC_SCRATCH_BYTES, stream);
 }
 
 sscn_status sscn_forward_stage(sscn_net* net, int32_t stage, void* stream) {

@@ -35,6 +35,7 @@ EXPORTED = [
     "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get", "sscn_timing_enable", "sscn_timing_collect",
     "sscn_timing_launches",
     "sscn_set_dropout", "sscn_philox4x32_10", "sscn_sgd_step", "sscn_encode_workspace_bytes", "sscn_encode_strokes",
+    "sscn_encode_strokes_static",
 ]
 KERNEL_CLASSES = ["rulebook", "gather_gemm", "wgrad", "wgrad_reduce", "pool_fwd", "pool_bwd", "head", "ground",
                   "dropout", "sgd", "conv_narrow"]
@@ -97,6 +98,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                 VP]),
         "sscn_encode_workspace_bytes": (I32, [I32, I32, I32, P(SZ)]),
         "sscn_encode_strokes": (I32, [I32, I32, VP, I32, VP, VP, I32, I32, VP, VP, I32, P(I32), VP, SZ, VP]),
+        "sscn_encode_strokes_static": (I32, [I32, I32, VP, I32, VP, VP, I32, I32, VP, VP, I32, P(I32), VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -223,6 +225,22 @@ def sscn_encode_strokes(N, dtype, d_points, n_points, d_begin, d_sample, n_strok
                                             d_coords, d_feats, max_sites, ctypes.byref(cnt), d_ws, ws_bytes, stream)
     if st != 0:
         err = SSCNError(st, "sscn_encode_strokes")
+        err.count = cnt.value
+        raise err
+    return cnt.value
+
+
+ENCODE_STATIC_SCRATCH_BYTES = 16 << 20  # SSCN_ENCODE_STATIC_SCRATCH_BYTES
+
+
+def sscn_encode_strokes_static(N, dtype, d_points, n_points, d_begin, d_sample, n_strokes, batch, d_coords,
+                               d_feats, max_sites, stream) -> int:
+    """sscn_encode_strokes without a workspace (the library's fixed per-GPU scratch); returns the site count."""
+    cnt = ctypes.c_int32(0)
+    st = load_library().sscn_encode_strokes_static(N, dtype, d_points, n_points, d_begin, d_sample, n_strokes,
+                                                   batch, d_coords, d_feats, max_sites, ctypes.byref(cnt), stream)
+    if st != 0:
+        err = SSCNError(st, "sscn_encode_strokes_static")
         err.count = cnt.value
         raise err
     return cnt.value
