@@ -18,9 +18,12 @@
 // the windows below is contiguous).  Every layer's bitmap therefore comes
 // straight from the input bitmap, one wave per (sample, layer), with no chain
 // through the layers: the rows of each square are ORed word-parallel, then
-// each output bit tests its column range.  A second launch turns the
-// per-sample counts into sample offsets (a last-workgroup pattern would need a
-// device-scope release fence, which costs more here than the launch).
+// each output bit tests its column range.  The sample offsets (exclusive scan
+// of the per-sample counts) come from the sites kernel itself for batches of
+// up to 1024 samples: each of its workgroups scans the counts of the layers its
+// words belong to; above that a separate offsets launch computes them (a
+// last-workgroup pattern in the bitmap kernel would need a device-scope release
+// fence, which costs more here than the launch).
 //
 // Builds alternate between two input bitmaps (and error words): each build
 // inserts into one that is all zero and clears the other for the next build,
