@@ -351,9 +351,10 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
           for (int r = 0; r < 4; ++r) {
             const int ml = wm * C::TM * 16 + i * 16 + g * 4 + r;
             float v = epi_value<T>(a, acc[i][j][r], bias[j]);
-            if (a.epi == EPI_STORE_MASK && m0 + ml < rows && n0 + nl < a.out_cols)  // the rectifier
-              v *= act_factor(  // derivative of the layer below, before the one rounding to storage
-                  Elem<T>::to_f32(((const T*)a.mask)[(int64_t)(m0 + ml) * a.mask_stride + n0 + nl]), a.slope);
+            if constexpr (RAC == MASK_MODE)  // the rectifier derivative of the layer below,
+              if (m0 + ml < rows && n0 + nl < a.out_cols)  // before the one rounding to storage
+                v *= act_factor(
+                    Elem<T>::to_f32(((const T*)a.mask)[(int64_t)(m0 + ml) * a.mask_stride + n0 + nl]), a.slope);
             Cs[ml * CS + nl] = Elem<T>::from_f32(v);
           }
         }
@@ -637,9 +638,11 @@ static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   const int grid = (int)std::min<int64_t>(std::max<int64_t>(tiles, 1), device_grid_limit()) +
                    (a.x.kind ? a.x.blocks : 0);
   const bool timed = a.t_start || a.t_stop;
-  // the pooling-backward epilogue has instantiations of its own (its slot sums
-  // would otherwise cost every launch registers)
+  // the pooling-backward epilogue and the masked store have instantiations of
+  // their own (their extra loads and sums would otherwise cost every launch
+  // registers)
   void (*kern)(GemmArgs) = a.pool_fwd ? k_gemm_gather<T, C, POOL_FWD_MODE>
+                           : a.epi == EPI_STORE_MASK ? k_gemm_gather<T, C, MASK_MODE>
                            : !a.route ? k_gemm_gather<T, C, -1>
                            : a.route_ac == 4 ? k_gemm_gather<T, C, 4>
                                              : k_gemm_gather<T, C, 0>;

@@ -157,8 +157,10 @@ struct GemmArgs {
 };
 
 // Template value of the gather GEMMs for the pooling-forward epilogue (the
-// others: -1 plain, 0 or 4 the pooling backward with that window count).
+// others: -1 plain, -3 the masked store EPI_STORE_MASK, 0 or 4 the pooling
+// backward with that window count).
 constexpr int POOL_FWD_MODE = -2;
+constexpr int MASK_MODE = -3;
 
 // Whether a tile shape stages its output tile through LDS (16-byte stores), as
 // the pooling backward in the epilogue needs.
