@@ -124,6 +124,12 @@ typedef struct {
                             pooling and input dL/dX; row 0 = sum over inactive sites */
   uint8_t* argmax;       /* pooling: [(capacity+1) * row_stride] window position
                             (0..3, first maximum in (dy, dx) order) of each max  */
+  const uint16_t* gmask; /* pooling layer on a 2x2 convolution (else NULL):
+                            [capacity+1] per row, bit 4 f + k set when window
+                            position k of the convolution row at pooling position
+                            f reads an inactive location (the ground row) of the
+                            layer below that convolution; row 0 all set.  Used by
+                            the pooling backward for the ground-row sums.       */
 } sscn_layer_view;
 
 /* Host only.  Validates desc (ell in 1..8, k, c_in, n_classes, batch_max,

@@ -34,6 +34,7 @@ struct LayerPlan {
   int32_t* rules;
   int32_t* rules_t;
   uint8_t* argmax;
+  uint16_t* gmask;  // pooling layer on a 2x2 convolution: child ground masks (RulebookArgs::gmask)
   void* Xd;  // dropped copy of X when this layer feeds a dropout level (dropout workspace only)
 };
 
@@ -223,9 +224,12 @@ static void carve(sscn_net* net, void* base) {
       else
         L.rules_t = (int32_t*)cv.take((size_t)(Lb.cap + 1) * 4);
       L.argmax = (L.kind == 2) ? (uint8_t*)cv.take((size_t)(L.cap + 1) * L.Cp) : nullptr;
+      L.gmask = (L.kind == 2 && s >= 2 && Lb.kind == 1 && Lb.F == 2) ? (uint16_t*)cv.take((size_t)(L.cap + 1) * 2)
+                                                                     : nullptr;
     } else {
       L.rules = L.rules_t = nullptr;
       L.argmax = nullptr;
+      L.gmask = nullptr;
     }
     L.Xd = nullptr;
   }
@@ -517,6 +521,7 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
     a.F[s] = L.F;
     a.rules[s] = L.rules;
     a.rules_t[s] = L.rules_t;
+    a.gmask[s] = L.gmask;
     wk.base[s] = acc;
     acc += (int64_t)batch * L.S * L.Wd;
   }
@@ -730,6 +735,8 @@ static GroundArgs ground_args(const sscn_net* net, int s, bool pool_above) {
     g.B1 = pool_bwd_blocks(net, Lp.cap, Lp.Cp);
     g.B2 = g.B1;  // one pass: the fused pooling backward
     g.Y_below = L.X;
+    g.X_pool = Lp.X;
+    g.gmask = Lp.gmask;
   } else {
     g.B2 = ground_parts(net, L.cap, L.Cp);
   }
@@ -1502,6 +1509,7 @@ sscn_status sscn_layer_view_get(const sscn_net* net, int32_t layer, sscn_layer_v
   out->features = L.X;
   out->grad = L.grad;
   out->argmax = L.argmax;
+  out->gmask = L.gmask;
   return SSCN_OK;
 }
 

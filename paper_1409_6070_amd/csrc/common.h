@@ -133,6 +133,10 @@ struct RulebookArgs {
   int32_t rf_r[MAX_LAYERS];
   int32_t* rules[MAX_LAYERS];    // layer s >= 1: [(cap_s+1) * A]
   int32_t* rules_t[MAX_LAYERS];  // layer s >= 1: conv [(cap_{s-1}+1) * A], pool [cap_{s-1}+1]
+  // pooling layer s on a 2x2 convolution (null otherwise): [cap_s + 1] child
+  // ground masks, bit 4 f + k set when window position k of the convolution
+  // row at pooling position f reads an inactive location of layer s - 2
+  uint16_t* gmask[MAX_LAYERS];
   int32_t* counts;               // [nlayers]
   int32_t* err;                  // this build's error word (zero on entry)
   int32_t* err_next;             // the next build's error word, cleared here

@@ -680,7 +680,7 @@ hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream
   if (a.route) {  // pooling backward in the epilogue: one partial per row tile
     const int bm = gemm_bm(bf16, a.cfg);
     if (a.epi != EPI_STORE || a.ksplit != 1 || !gemm_routes(bf16, a.cfg) || (a.route_ac != 0 && a.route_ac != 4) ||
-        !a.pr.part || !a.pr.Rp || !a.pr.argmax || !a.pr.dZ || !a.pr.Y_below || (a.route_ac > 0 && !a.pr.R) ||
+        !a.pr.part || !a.pr.Rp || !a.pr.argmax || !a.pr.dZ || !a.pr.X_pool || (a.route_ac == 4 && !a.pr.gmask) ||
         a.pr.cp != a.out_cols || a.pr.stride != a.pr.cp || (max_rows - a.row_begin + bm - 1) / bm > a.pr.PM)
       return hipErrorInvalidValue;
   }

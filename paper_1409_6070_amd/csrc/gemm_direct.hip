@@ -192,10 +192,12 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
     const int m0 = a.row_begin + tm * BM, n0 = tn * BN;
     // bias of the 8 columns this thread writes in the epilogue (its vectors all
     // share one column group), fetched now so that it arrives during the K loop
+    // (the pooling backward's launches are input gradients: no bias)
     const int c8e = (tid % (BN / 8)) * 8;
     float bias8[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) bias8[e] = (a.bias && n0 + c8e + e < a.N) ? a.bias[n0 + c8e + e] : 0.f;
+    for (int e = 0; e < 8; ++e)
+      bias8[e] = (RAC < 0 && a.bias && n0 + c8e + e < a.N) ? a.bias[n0 + c8e + e] : 0.f;
     // pooling backward in the epilogue with one row per thread (four waves):
     // that row's window and argmax now, its children's rows after the K loop
     constexpr int RA = RAC < 0 ? 0 : RAC;

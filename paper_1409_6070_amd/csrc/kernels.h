@@ -51,6 +51,11 @@ struct GroundArgs {
   const int32_t* n_pool;
   int32_t B1;
   const void* Y_below;  // the convolution's output (ReLU mask of row 0)
+  // the pooling layer's output: the routed child's value, so its rectifier
+  // derivative (a window's maximum is a copy of the child it came from)
+  const void* X_pool;
+  // AC == 4: the pooling layer's child ground masks (RulebookArgs::gmask)
+  const uint16_t* gmask;
   // the convolution
   void* dZ;            // delta, rows 0..n; row 0 written when B1 > 0
   const int32_t* R;    // its window list [rows][AC]

@@ -259,7 +259,8 @@ static bool extra_ok(const ExtraTask& x) {
 hipError_t launch_ground(bool bf16, const GroundArgs& g, int32_t AC, int kind, hipStream_t st,
                          const ExtraTask* extra) {
   if (g.B2 < 1 || g.B1 < 0 || g.B1 > g.PM || g.B2 > g.PM) return hipErrorInvalidValue;
-  if (kind == 1 && g.B1 != g.B2) return hipErrorInvalidValue;
+  if (kind == 1 && (g.B1 != g.B2 || !g.X_pool || (AC == 4 && !g.gmask) || (AC != 0 && AC != 4 && !g.R)))
+    return hipErrorInvalidValue;
   const ExtraTask x = extra ? *extra : ExtraTask{};
   if (!extra_ok(x)) return hipErrorInvalidValue;
 #define SSCN_GROUND(T, A) launch_ground_t<T, A>(g, kind, st, x)

@@ -55,22 +55,37 @@ __device__ inline WinRow<AC> load_win_row(const int32_t* __restrict__ R, int64_t
   return w;
 }
 
-// Pooling row o >= 1, channels c .. c+VE-1, with its stored gradient gv: for
-// each window position f, child row i = Rp[o][f]:
-//   i >= 1:  delta[i] = gv * f'(Y_below[i]) where argmax[o] == f, else 0
+// Pooling row o >= 1, channels c .. c+VE-1, with its stored gradient gv: the
+// window's first maximum came from child row i = Rp[o][a] (a = argmax[o]),
+// whose stored value it copies, so the rectifier derivative of the convolution
+// below is read off the pooling output X_pool[o]:
+//   i >= 1:  delta[i] = gv * f'(X_pool[o]), delta of the other children 0
 //            (written: each child row lies in exactly one window), added to
 //            slot 1 and, where the convolution's window position k of row i
 //            reads the ground row (R[i][k] == 0), to slot 2 + k;
-//   i == 0:  gv where argmax[o] == f is added to slot 0.
-// The loads come in two steps that a caller may issue early: the row's window
-// and argmax, then every child's rows at once (a ground child loads row 0,
-// which exists, and ignores it).
+//   i == 0:  gv is added to slot 0.
+// The ground pattern of the children's windows comes from the rulebook's
+// child ground mask for AC == 4 and from the children's window rows for other
+// AC.  The loads come in two steps that a caller may issue early: the row's
+// window, argmax, pooled values (and mask), then (AC not 0 or 4 only) every
+// child's window row.
+template <int AC>
+struct ChildWins {
+  WinRow<AC> wr[4];
+};
+template <>
+struct ChildWins<0> {};
+template <>
+struct ChildWins<4> {
+  uint32_t gm;
+};
+
 template <typename T, int AC>
 struct RouteIn {
   ri32x4 r;
   typename ArgPack<Elem<T>::VE>::W am;
-  ru32x4 y[4];
-  WinRow<AC> wr[4];
+  ru32x4 xp;
+  ChildWins<AC> cw;
 };
 
 template <typename T, int AC>
@@ -78,15 +93,15 @@ __device__ inline void route_load_window(const GroundArgs& g, int64_t o, int c, 
   typedef typename ArgPack<Elem<T>::VE>::W AW;
   q.r = *(const ri32x4*)(g.Rp + o * 4);
   q.am = *(const AW*)(g.argmax + o * g.stride + c);
+  q.xp = *(const ru32x4*)((const T*)g.X_pool + o * g.stride + c);
+  if constexpr (AC == 4) q.cw.gm = g.gmask[o];
 }
 
 template <typename T, int AC>
 __device__ inline void route_load_children(const GroundArgs& g, int c, RouteIn<T, AC>& q) {
-  const T* Yb = (const T*)g.Y_below;
+  if constexpr (AC != 0 && AC != 4) {
 #pragma unroll
-  for (int f = 0; f < 4; ++f) {
-    q.y[f] = *(const ru32x4*)(Yb + (int64_t)q.r[f] * g.stride + c);
-    if constexpr (AC > 0) q.wr[f] = load_win_row<AC>(g.R, q.r[f]);
+    for (int f = 0; f < 4; ++f) q.cw.wr[f] = load_win_row<AC>(g.R, q.r[f]);
   }
 }
 
@@ -95,27 +110,41 @@ __device__ inline void route_apply(const GroundArgs& g, int c, const RouteIn<T, 
                                    float (&acc)[2 + AC][Elem<T>::VE]) {
   constexpr int VE = Elem<T>::VE;
   T* dZ = (T*)g.dZ;
+  // bit f: child f is the ground row; bit AC f + k: child f's window position k reads it
+  const uint32_t gch = (q.r[0] == 0 ? 1u : 0u) | (q.r[1] == 0 ? 2u : 0u) | (q.r[2] == 0 ? 4u : 0u) |
+                       (q.r[3] == 0 ? 8u : 0u);
+  uint64_t gw = 0;
+  if constexpr (AC == 4) {
+    gw = q.cw.gm;
+  } else if constexpr (AC > 0) {
+#pragma unroll
+    for (int f = 0; f < 4; ++f)
+#pragma unroll
+      for (int k = 0; k < AC; ++k) gw |= (uint64_t)(q.cw.wr[f].v[k] == 0 ? 1u : 0u) << (AC * f + k);
+  }
+  ru32x4 out[4];
   // every sum is updated on both branches (a select, not a branch), so that
   // the accumulators stay in registers
 #pragma unroll
-  for (int f = 0; f < 4; ++f) {
-    const bool ground = q.r[f] == 0;
-    ru32x4 out;
+  for (int j = 0; j < VE; ++j) {
+    const int a = (int)((q.am >> (8 * j)) & 3);
+    const float gj = Elem<T>::to_f32(gv[j]);
+    const T o = Elem<T>::from_f32(gj * act_factor(Elem<T>::to_f32(((const T*)&q.xp)[j]), g.slope));
+    const bool ground = (gch >> a) & 1u;
+    const float d = ground ? 0.f : Elem<T>::to_f32(o);
+    acc[0][j] += ground ? gj : 0.f;
+    acc[1][j] += d;
+    if constexpr (AC > 0) {
+      const uint64_t ga = gw >> (AC * a);
 #pragma unroll
-    for (int j = 0; j < VE; ++j) {
-      const bool pick = (int)((q.am >> (8 * j)) & 0xff) == f;
-      const float gj = Elem<T>::to_f32(gv[j]);
-      const float fac = act_factor(Elem<T>::to_f32(((const T*)&q.y[f])[j]), g.slope);
-      const T o = pick ? Elem<T>::from_f32(gj * fac) : Elem<T>::from_f32(0.f);
-      ((T*)&out)[j] = o;
-      const float d = ground ? 0.f : Elem<T>::to_f32(o);
-      acc[0][j] += (ground && pick) ? gj : 0.f;
-      acc[1][j] += d;
-#pragma unroll
-      for (int k = 0; k < AC; ++k) acc[2 + k][j] += q.wr[f].v[k] == 0 ? d : 0.f;
+      for (int k = 0; k < AC; ++k) acc[2 + k][j] += ((ga >> k) & 1u) ? d : 0.f;
     }
-    if (!ground) *(ru32x4*)(dZ + (int64_t)q.r[f] * g.stride + c) = out;
+#pragma unroll
+    for (int f = 0; f < 4; ++f) ((T*)&out[f])[j] = a == f ? o : Elem<T>::from_f32(0.f);
   }
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+    if (q.r[f] != 0) *(ru32x4*)(dZ + (int64_t)q.r[f] * g.stride + c) = out[f];
 }
 
 template <typename T, int AC>

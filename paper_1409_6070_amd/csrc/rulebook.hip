@@ -369,23 +369,69 @@ __device__ inline SiteKey decode_key(int key, int S) {
   return SiteKey{b, y, x};
 }
 
+// Child ground mask of pooling location (Y, X) of sample b over a 2x2
+// convolution whose input is layer L: bit 4 f + k, for pooling position
+// f = 2 dy + dx and convolution window position k = 2 ky + kx, is set when
+// location (2Y + dy + ky, 2X + dx + kx) of L is inactive or off its grid, i.e.
+// when that child's window reads the ground row there.  The nine locations
+// are one 3x3 square: three rows of at most two words each.
+__device__ inline uint16_t child_ground_mask(const LayerBits& L, int b, int Y, int X) {
+  const int y0 = 2 * Y, x0 = 2 * X;
+  const int wi = x0 >> 6, bi = x0 & 63;
+  const bool two = bi > 61 && wi + 1 < L.Wd;
+  uint64_t w0[3], w1[3];
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    const bool in = y0 + i < L.S && wi < L.Wd;
+    const int64_t idx = ((int64_t)b * L.S + (in ? y0 + i : 0)) * L.Wd + (in ? wi : 0);
+    w0[i] = in ? L.bits[idx] : 0ull;
+    w1[i] = in && two ? L.bits[idx + 1] : 0ull;
+  }
+  uint32_t cols = 0;  // columns x0 .. x0 + 2 on the grid
+#pragma unroll
+  for (int j = 0; j < 3; ++j) cols |= (x0 + j < L.S ? 1u : 0u) << j;
+  uint32_t act = 0;  // bit 3 i + j: location (y0 + i, x0 + j) active
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    const uint64_t v = (w0[i] >> bi) | (bi > 61 ? w1[i] << (64 - bi) : 0ull);
+    act |= ((uint32_t)v & cols) << (3 * i);
+  }
+  uint32_t m = 0;
+#pragma unroll
+  for (int dy = 0; dy < 2; ++dy)
+#pragma unroll
+    for (int dx = 0; dx < 2; ++dx)
+#pragma unroll
+      for (int ky = 0; ky < 2; ++ky)
+#pragma unroll
+        for (int kx = 0; kx < 2; ++kx)
+          m |= (((act >> (3 * (dy + ky) + dx + kx)) & 1u) ^ 1u) << (4 * (2 * dy + dx) + 2 * ky + kx);
+  return (uint16_t)m;
+}
+
 // R_s for rows [tid, n_out] step `stride` of a layer whose windows are F x F
-// locations below, `step` apart (1: convolution, 2: pooling).
+// locations below, `step` apart (1: convolution, 2: pooling).  With gm (a
+// pooling layer on a 2x2 convolution over layer Lg) also each row's child
+// ground mask (row 0: all set).  (Lg is a reference into the kernel
+// arguments: taking its address would copy them to scratch memory.)
 template <int F>
 __device__ inline void window_rows(const LayerBits& Lo, const LayerBits& Li, int step, int n_out, int32_t* R,
-                                   int64_t tid, int64_t stride) {
+                                   int64_t tid, int64_t stride, const LayerBits& Lg, uint16_t* gm) {
   constexpr int A = F * F;
   for (int64_t o = tid; o <= n_out; o += stride) {
     int32_t r[A];
+    uint16_t m = 0xFFFF;
     if (o == 0) {
 #pragma unroll
       for (int f = 0; f < A; ++f) r[f] = 0;
     } else {
       const SiteKey k = decode_key(Lo.sites[o - 1], Lo.S);
       rank_window<F, 1>(Li, k.b, step * k.y, step * k.x, 0, r);
+      if (gm) m = child_ground_mask(Lg, k.b, k.y, k.x);
     }
 #pragma unroll
     for (int f = 0; f < A; ++f) R[o * A + f] = r[f];
+    if (gm) gm[o] = m;
   }
 }
 
@@ -427,12 +473,14 @@ __global__ void __launch_bounds__(256) k_rb_rules(RulebookArgs a, RulesWork rw) 
       const int step = (a.kind[s] == 1) ? 1 : 2;
       const int n_out = a.counts[s];
       int32_t* R = a.rules[s];
+      const LayerBits& Lg = a.L[s >= 2 ? s - 2 : 0];
+      uint16_t* gm = s >= 2 ? a.gmask[s] : nullptr;
       if (F == 3)
-        window_rows<3>(Lo, Li, step, n_out, R, tid, stride);
+        window_rows<3>(Lo, Li, step, n_out, R, tid, stride, Lg, nullptr);
       else if (F == 2)
-        window_rows<2>(Lo, Li, step, n_out, R, tid, stride);
+        window_rows<2>(Lo, Li, step, n_out, R, tid, stride, Lg, gm);
       else
-        window_rows<1>(Lo, Li, step, n_out, R, tid, stride);
+        window_rows<1>(Lo, Li, step, n_out, R, tid, stride, Lg, nullptr);
     } else {  // transposes: for every row of layer s-1, the rows of layer s whose window holds it
       const int n_in = a.counts[s - 1];
       int32_t* Rt = a.rules_t[s];

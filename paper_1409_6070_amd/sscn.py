@@ -59,7 +59,7 @@ class LayerView(ctypes.Structure):
         ("row_stride", ctypes.c_int32), ("window", ctypes.c_int32), ("capacity", ctypes.c_int32),
         ("count", ctypes.c_void_p), ("sites", ctypes.c_void_p), ("rules", ctypes.c_void_p),
         ("rules_t", ctypes.c_void_p), ("features", ctypes.c_void_p), ("grad", ctypes.c_void_p),
-        ("argmax", ctypes.c_void_p),
+        ("argmax", ctypes.c_void_p), ("gmask", ctypes.c_void_p),
     ]
 
 
@@ -408,6 +408,8 @@ class SparseDeepCNet:
             out["rules"] = self._slice(v.rules, (n + 1) * A * 4, torch.int32).view(n + 1, A)
             if v.argmax:
                 out["argmax"] = self._slice(v.argmax, (n + 1) * rs, torch.uint8).view(n + 1, rs)
+            if v.gmask:
+                out["gmask"] = self._slice(v.gmask, (n + 1) * 2, torch.int16)
         return out
 
     def rules_t(self, layer: int, n_below: int) -> torch.Tensor:

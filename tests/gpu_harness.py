@@ -214,6 +214,31 @@ def check_structure(p: Pair):
         Rt = p.net.rules_t(s, o.layers[s - 1].n).cpu().numpy()
         np.testing.assert_array_equal(Rt, expected_rules_t(L.R, o.layers[s - 1].n, st.kind),
                                       err_msg=f"transposed rules layer {s}")
+        if "gmask" in v:
+            got = v["gmask"].cpu().numpy().astype(np.int64) & 0xFFFF
+            np.testing.assert_array_equal(got, expected_gmask(L, o.layers[s - 2]),
+                                          err_msg=f"child ground masks layer {s}")
+
+
+def expected_gmask(Lp, L2):
+    """Child ground masks of a pooling layer on a 2x2 convolution over layer L2, from L2's pointer
+    matrix: bit 4 (2 dy + dx) + 2 ky + kx of row o set when location (2Y + dy + ky, 2X + dx + kx) of
+    L2 is inactive or off its grid, (b, Y, X) the site of row o; row 0 all set."""
+    n = len(Lp.sites)
+    out = np.full(n + 1, 0xFFFF, dtype=np.int64)
+    if n == 0:
+        return out
+    P = np.pad(L2.P, ((0, 0), (0, 3), (0, 3)))  # off-grid locations read as inactive
+    b, Y, X = (Lp.sites[:, i].astype(np.int64) for i in range(3))
+    m = np.zeros(n, dtype=np.int64)
+    for dy in range(2):
+        for dx in range(2):
+            for ky in range(2):
+                for kx in range(2):
+                    ground = P[b, 2 * Y + dy + ky, 2 * X + dx + kx] == 0
+                    m |= ground.astype(np.int64) << (4 * (2 * dy + dx) + 2 * ky + kx)
+    out[1:] = m
+    return out
 
 
 def flip_cap(n_decisions: int) -> int:
