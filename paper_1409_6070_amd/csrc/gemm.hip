@@ -671,8 +671,11 @@ static void launch_gemm_t(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   }
 }
 
-hipError_t launch_gemm(bool bf16, const GemmArgs& a, int64_t max_rows, hipStream_t st) {
-  if (max_rows - a.row_begin <= 0) return hipSuccess;
+hipError_t launch_gemm(bool bf16, const GemmArgs& args, int64_t max_rows, hipStream_t st) {
+  if (max_rows - args.row_begin <= 0) return hipSuccess;
+  if (max_rows > INT32_MAX) return hipErrorInvalidValue;
+  GemmArgs a = args;
+  a.rows_cap = (int32_t)max_rows;
   if (a.pool_fwd && (a.route || a.ksplit != 1 || !gemm_routes(bf16, a.cfg) || a.row_begin != 0 || !a.pslot ||
                      !a.pool_out || !a.pool_argmax || !a.rows_dev ||
                      (a.epi != EPI_BIAS_RELU && a.epi != EPI_BIAS_LRELU)))

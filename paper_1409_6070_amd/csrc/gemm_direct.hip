@@ -172,13 +172,47 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   if (run_extra<T>(a.x)) return;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int rows = (a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host) * (POOL ? 4 : 1);
+  const int rows_in = a.rows_dev ? *a.rows_dev : a.rows_host;
+  const int tiles_n = a.Npad / BN;
+  const int A = a.A;
+  const int c8e = (tid % (BN / 8)) * 8;  // the column group this thread stores in the epilogue
+  constexpr int RA = RAC < 0 ? 0 : RAC;
+  // pooling backward in the epilogue with one row per thread (four waves):
+  // that row's window, argmax, pooled values and ground mask before the K loop
+  constexpr bool PRE = RAC >= 0 && NT == BM * (BN / 8);
+  constexpr int EPT = (BM * DIR_AMAX + NT - 1) / NT;  // window entries per thread
+  // A tile's window entries (the pooling forward: its slots' convolution rows)
+  // for output rows m < bound.
+  auto first_level = [&](int e, int m0, int bound) -> int {
+    const int r = e / A, f = e - r * A, m = m0 + r;
+    if (e >= BM * A || m >= bound) return -1;
+    if constexpr (POOL) return a.pslot[m];
+    return a.rmap ? a.rmap[(int64_t)m * A + f] : (f == 0 ? m : -1);
+  };
+  // The first tile's loads that do not need the row count are issued before it
+  // arrives, bounded by the rows the grid was sized for (which every list and
+  // row buffer holds): its window entries, its bias and its routing inputs.
+  int first[EPT];
+  float bias8[8];
+  PrefetchT<RAC, PRE> pre;
+  {
+    const int m0 = a.row_begin + ((int)blockIdx.x / tiles_n) * BM, n0 = ((int)blockIdx.x % tiles_n) * BN;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) first[i] = first_level(tid + i * NT, m0, a.rows_cap);
+    // (the pooling backward's launches are input gradients: no bias)
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      bias8[e] = (RAC < 0 && a.bias && n0 + c8e + e < a.N) ? a.bias[n0 + c8e + e] : 0.f;
+    const int pre_m = m0 + tid / (BN / 8);
+    if constexpr (PRE)
+      if (pre_m >= 1 && pre_m < a.rows_cap && n0 + c8e < a.out_cols)
+        route_load_window<T, RA>(a.pr, pre_m, n0 + c8e, pre);
+  }
+  const int rows = (rows_in + (a.rows_dev ? a.rows_add : 0)) * (POOL ? 4 : 1);
   const int span = rows - a.row_begin;
   if (span <= 0) return;
   const int tiles_m = (span + BM - 1) / BM;
-  const int tiles_n = a.Npad / BN;
   const int ntiles = tiles_m * tiles_n;
-  const int A = a.A;
   const int ksteps = (a.K + 31) / 32;
   const int per = (ksteps + SK - 1) / SK;
   const int kb = min(ksteps, w * per), ke = min(ksteps, kb + per);
@@ -190,36 +224,33 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   for (int tile = blockIdx.x; tile < ntiles; tile += grid) {
     const int tn = tile % tiles_n, tm = tile / tiles_n;
     const int m0 = a.row_begin + tm * BM, n0 = tn * BN;
-    // bias of the 8 columns this thread writes in the epilogue (its vectors all
-    // share one column group), fetched now so that it arrives during the K loop
-    // (the pooling backward's launches are input gradients: no bias)
-    const int c8e = (tid % (BN / 8)) * 8;
-    float bias8[8];
+    const bool later = tile != (int)blockIdx.x;  // the first tile's loads were issued above
+    if (later) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      bias8[e] = (RAC < 0 && a.bias && n0 + c8e + e < a.N) ? a.bias[n0 + c8e + e] : 0.f;
-    // pooling backward in the epilogue with one row per thread (four waves):
-    // that row's window and argmax now, its children's rows after the K loop
-    constexpr int RA = RAC < 0 ? 0 : RAC;
-    constexpr bool PRE = RAC >= 0 && NT == BM * (BN / 8);
-    PrefetchT<RAC, PRE> pre;
+      for (int e = 0; e < 8; ++e)
+        bias8[e] = (RAC < 0 && a.bias && n0 + c8e + e < a.N) ? a.bias[n0 + c8e + e] : 0.f;
+    }
     const int pre_m = m0 + tid / (BN / 8);
     const bool pre_on = PRE && pre_m >= 1 && pre_m < rows && n0 + c8e < a.out_cols;
     if constexpr (PRE)
-      if (pre_on) route_load_window<T, RA>(a.pr, pre_m, n0 + c8e, pre);
-    for (int e = tid; e < BM * A; e += NT) {  // the tile's window rows (-1: none)
-      const int r = e / A, f = e - r * A;
-      const int m = m0 + r;
-      int v = -1;
-      if (m < rows) {
-        int row = m;  // the output row (pooling forward: the slot's convolution row)
-        if constexpr (POOL) {
-          row = a.pslot[m];
-          if (f == 0) Cr[r] = row;
+      if (later && pre_on) route_load_window<T, RA>(a.pr, pre_m, n0 + c8e, pre);
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {  // the tile's window rows (-1: none)
+      const int e = tid + i * NT;
+      if (e < BM * A) {
+        const int r = e / A, f = e - r * A;
+        int v = -1;
+        if (m0 + r < rows) {
+          const int l1 = later ? first_level(e, m0, rows) : first[i];
+          if constexpr (POOL) {  // l1 is the slot's convolution row
+            if (f == 0) Cr[r] = l1;
+            v = a.rmap ? a.rmap[(int64_t)l1 * A + f] : (f == 0 ? l1 : -1);
+          } else {
+            v = l1;
+          }
         }
-        v = a.rmap ? a.rmap[(int64_t)row * A + f] : (f == 0 ? row : -1);
+        Rs[e] = v;
       }
-      Rs[e] = v;
     }
     __syncthreads();
 
@@ -311,6 +342,7 @@ static void launch_direct_sk(const GemmArgs& a, int64_t max_rows, hipStream_t st
 
 hipError_t launch_gemm_direct(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
   if (max_rows - a.row_begin <= 0) return hipSuccess;
+  if (a.rows_cap != max_rows) return hipErrorInvalidValue;
   if (a.A < 1 || a.A > DIR_AMAX || a.cseg % 8 || a.src_stride % 8 || a.Npad % DIRECT_BN || a.Kpad % 32 ||
       a.Kpad < (a.K + 31) / 32 * 32 || a.ksplit != 1)
     return hipErrorInvalidValue;

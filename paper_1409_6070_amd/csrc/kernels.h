@@ -159,6 +159,10 @@ struct GemmArgs {
   void* pool_out;
   uint8_t* pool_argmax;
   int32_t pool_stride;
+  // set by launch_gemm: the row bound the grid is sized for (rows, or slots with
+  // pool_fwd); every window list and row buffer a launch reads holds that many
+  // rows, so loads below it may be issued before the device-side count arrives
+  int32_t rows_cap;
 };
 
 // Template value of the gather GEMMs for the pooling-forward epilogue (the
