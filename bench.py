@@ -548,6 +548,94 @@ def traffic_key(kernel_name):
     return k
 
 
+# rocprofv3 kernel names of each kernel group of the bench line (template arguments
+# of the direct kernel: <waves per tile, epilogue>, 0 and 4 the pooling backward),
+# and the sources whose hash a counter summary records
+COUNTER_GROUPS = {
+    "k_gemm_direct 32x64: input gradient + pooling backward": (
+        r"k_gemm_direct<\d+, [04]>", "gemm_direct.hip epilogue.h pool_route.h ground_tasks.h kernels.h common.h"),
+    "k_wgrad (all weight gradients, grouped)": (
+        r"k_wgradI|k_wgrad<", "gemm.hip kernels.h common.h ground_tasks.h"),
+}
+
+
+def _counter_rows(d):
+    """(kernel name, counter, value) of every dispatch in a rocprofv3 --pmc csv directory."""
+    import csv
+    import glob
+    rows = []
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                rows.append((r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"]), r.get("Dispatch_Id")))
+    return rows
+
+
+def counter_summary(group, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, workload, dtype, commands):
+    """Writes profiles/<group>_traffic.txt: HBM bytes per launch of a kernel group from FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch), scaled by what the same counters read for a 256 MiB device copy."""
+    import re
+    pat, sources = COUNTER_GROUPS[group]
+    n_copy = 256 << 20
+
+    def per_dispatch(d, counter, name_re):
+        vals = {}
+        for name, c, v, disp in _counter_rows(d):
+            if c.startswith(counter) and re.search(name_re, name):
+                vals[disp] = vals.get(disp, 0.0) + v  # summed over the counter's instances
+        return list(vals.values())
+
+    cf = max(per_dispatch(copy_fetch_dir, "FETCH_SIZE", r"copy|Copy"))
+    cw = max(per_dispatch(copy_write_dir, "WRITE_SIZE", r"copy|Copy"))
+    fs, ws = n_copy / (cf * 1024.0), n_copy / (cw * 1024.0)
+    f = per_dispatch(fetch_dir, "FETCH_SIZE", pat)
+    w = per_dispatch(write_dir, "WRITE_SIZE", pat)
+    rd, wr = float(np.mean(f)) * 1024 * fs, float(np.mean(w)) * 1024 * ws
+    h = hashlib.sha256()
+    for name in sources.split():
+        h.update(open(os.path.join(ROOT, "paper_1409_6070_amd", "csrc", name), "rb").read())
+    path = os.path.join(PROFILES, f"{traffic_key(group)}_traffic.txt")
+    lines = [f"# HBM traffic per launch of {group}, {workload} {dtype} (one MI355X)",
+             "# Commands (repository root):"] + [f"#   {c}" for c in commands] + [
+             f"# Calibration: a 256 MiB device copy reads {fs:.4f} x FETCH_SIZE KiB x 1024 bytes and writes "
+             f"{ws:.4f} x WRITE_SIZE KiB x 1024 bytes.",
+             f"# {len(f)} FETCH_SIZE and {len(w)} WRITE_SIZE dispatches of the group (rocprofv3 names matching "
+             f"{pat}), averaged per launch.",
+             f"kernel: {group}", f"source: {sources}", f"workload: {workload}",
+             f"source_sha256_16: {h.hexdigest()[:16]}", f"dtype: {dtype}",
+             f"fetch_scale: {fs:.4f}", f"write_scale: {ws:.4f}",
+             f"read_bytes_per_launch: {rd:.0f}", f"write_bytes_per_launch: {wr:.0f}",
+             f"hbm_bytes_per_launch: {rd + wr:.0f}"]
+    with open(path, "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def trace_summary(trace_dir, out, title, command, top=30):
+    """A markdown table of a rocprofv3 --kernel-trace --stats run's per-kernel statistics."""
+    import csv
+    import glob
+    paths = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    rows = []
+    for path in paths:
+        with open(path) as f:
+            rows += list(csv.DictReader(f))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = [f"# {title}", "", "Command (repository root):", "```", command, "```", "",
+             "| kernel | calls | avg us | min us | max us | % of kernel time |", "|---|---:|---:|---:|---:|---:|"]
+    for r in rows[:top]:
+        name = r["Name"].replace("|", "/")
+        if len(name) > 90:
+            name = name[:87] + "..."
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{100 * float(r['TotalDurationNs']) / tot:.1f} |")
+    with open(out, "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 TABLE_ORDER = ["deepcnet4_20_strokes_b8", "deepcnet5_50_strokes_b100", "deepcnet5_50_strokes_m8_b100",
                "deepcnet5_100_rgbpatch_b128", "deepcnet6_100_strokes_b64"]
 
@@ -592,7 +680,22 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true")
     ap.add_argument("--table", default=None, help="time every workload of the measurement plan, write a table")
+    ap.add_argument("--counter-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="write profiles/<group>_traffic.txt from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of "
+                         "this benchmark and of --calibrate-copy (no GPU needed)")
+    ap.add_argument("--group", default="k_gemm_direct 32x64: input gradient + pooling backward")
+    ap.add_argument("--commands", nargs="*", default=[], help="the commands that made the counter runs")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "OUT_MD"),
+                    help="a markdown table of a rocprofv3 --kernel-trace --stats run (no GPU needed)")
+    ap.add_argument("--title", default="Kernel trace")
     args = ap.parse_args()
+    if args.counter_summary:
+        counter_summary(args.group, *args.counter_summary, args.workload, args.dtype, args.commands)
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary[0], args.trace_summary[1], args.title,
+                      " ".join(args.commands) if args.commands else "")
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported here "
               "(the path would shard over samples with one all-reduce of dW/db per step)", file=sys.stderr)
