@@ -43,7 +43,7 @@ struct NoPrefetch {};
 template <int AC, bool PRE>
 using PrefetchT = typename std::conditional<PRE, RouteIn<__bf16, AC < 0 ? 0 : AC>, NoPrefetch>::type;
 
-template <int SK, int RP, int AC, bool PRE>
+template <int SK, int RP, int AC, bool PRE, int LDSF>
 __device__ inline void store_vectors(const GemmArgs& a, float (*red)[DIRECT_BM][RP], const float (&bias8)[8], int c8e,
                                      int m0, int n0, int tm, int rows, const PrefetchT<AC, PRE>& pre) {
   typedef __bf16 T;
@@ -92,7 +92,7 @@ __device__ inline void store_vectors(const GemmArgs& a, float (*red)[DIRECT_BM][
       }
     }
   }
-  if constexpr (AC >= 0) tile_slot_sums<8, J, NT, NV, SK * BM * RP>(acc, &red[0][0][0], a.pr, n0, tm);
+  if constexpr (AC >= 0) tile_slot_sums<8, J, NT, NV, LDSF>(acc, &red[0][0][0], a.pr, n0, tm);
 }
 
 // Pooling forward in the epilogue (GemmArgs::pool_fwd): the tile's rows are
@@ -166,7 +166,12 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
   constexpr int RP = BN + 4;   // LDS pitch of the partial sums (floats)
   constexpr bool POOL = RAC == POOL_FWD_MODE;
   __shared__ int32_t Rs[BM * DIR_AMAX];
-  __shared__ __attribute__((aligned(16))) float red[SK][BM][RP];
+  // the waves' partial sums; with the pooling backward also every slot sum of
+  // the tile at once (one pass through LDS)
+  constexpr int REDF = SK * BM * RP, SLOTF = RAC >= 0 ? (2 + RAC) * NT * 8 : 0;
+  constexpr int LDSF = REDF > SLOTF ? REDF : SLOTF;
+  __shared__ __attribute__((aligned(16))) float red_lds[LDSF];
+  float(*red)[BM][RP] = (float(*)[BM][RP])red_lds;
   __shared__ int32_t Cr[POOL ? BM : 1];  // pooling forward: the convolution row of each slot
 
   if (run_extra<T>(a.x)) return;
@@ -309,7 +314,7 @@ __global__ void __launch_bounds__(64 * SK) k_gemm_direct(GemmArgs a) {
     if constexpr (POOL) {
       store_pooled_direct<SK, RP>(a, red, bias8, c8e, m0, n0, rows, Cr);
     } else if (epi_stores_T(a.epi)) {
-      store_vectors<SK, RP, RAC, PRE>(a, red, bias8, c8e, m0, n0, tm, rows, pre);
+      store_vectors<SK, RP, RAC, PRE, LDSF>(a, red, bias8, c8e, m0, n0, tm, rows, pre);
     } else {
       for (int e = tid; e < BM * BN; e += NT) {
         const int r = e / BN, c = e - r * BN;
