@@ -636,6 +636,61 @@ def trace_summary(trace_dir, out, title, command, top=30):
     print("\n".join(lines))
 
 
+def wave_summary(dirs, out, title, commands, top=20):
+    """Per-kernel wave counters from several rocprofv3 --pmc runs (one counter set each): the mean per
+    dispatch of every counter, and the derived columns of the table."""
+    per = {}  # kernel -> counter -> [values per dispatch]
+    for d in dirs:
+        acc = {}
+        for name, c, v, disp in _counter_rows(d):
+            acc.setdefault((name, c), {}).setdefault(disp, 0.0)
+            acc[(name, c)][disp] += v
+        for (name, c), dd in acc.items():
+            per.setdefault(name, {})[c] = float(np.mean(list(dd.values())))
+    rows = []
+    for name, c in per.items():
+        w = c.get("SQ_WAVES", 0.0)
+        if w <= 0:
+            continue
+        cyc = c.get("SQ_WAVE_CYCLES", 0.0)
+        hits, miss = c.get("TCC_HIT_sum", 0.0), c.get("TCC_MISS_sum", 0.0)
+
+        def f(key, scale=1.0):
+            return c[key] * scale if key in c else None
+
+        rows.append((cyc * 4 / w * w, name, {
+            "VMEM lat": f("VmemLatency"), "waves/SIMD": f("MeanOccupancyPerActiveCU"),
+            "L2 hit": hits / (hits + miss) if hits + miss else None,
+            "wait": c["SQ_WAIT_ANY"] / cyc if cyc and "SQ_WAIT_ANY" in c else None,
+            "issue": c["SQ_ACTIVE_INST_ANY"] / cyc if cyc and "SQ_ACTIVE_INST_ANY" in c else None,
+            "VALU/wave": f("SQ_INSTS_VALU", 1 / w), "SALU": f("SQ_INSTS_SALU", 1 / w),
+            "MFMA": f("SQ_INSTS_MFMA", 1 / w), "VMEM": f("SQ_INSTS_VMEM", 1 / w), "LDS": f("SQ_INSTS_LDS", 1 / w),
+            "wave life (cycles)": cyc * 4 / w if cyc else None}))
+    rows.sort(key=lambda r: -r[0])
+    cols = ["VMEM lat", "waves/SIMD", "L2 hit", "wait", "issue", "VALU/wave", "SALU", "MFMA", "VMEM", "LDS",
+            "wave life (cycles)"]
+    lines = [f"# {title}", "", "Commands (repository root), one rocprofv3 pass per counter set:", "```"] + \
+        list(commands) + ["```", "",
+                          "Columns: VMEM latency (cycles, derived `VmemLatency`); mean waves per SIMD "
+                          "(`MeanOccupancyPerActiveCU`); L2 hit rate; fractions of wave time waiting on anything "
+                          "(`SQ_WAIT_ANY`) and issuing (`SQ_ACTIVE_INST_ANY`) out of `SQ_WAVE_CYCLES`; instructions "
+                          "per wave; wave lifetime in cycles (4 x `SQ_WAVE_CYCLES` / `SQ_WAVES`). Means per "
+                          "dispatch; kernels ordered by total wave time.", "",
+                          "| kernel | " + " | ".join(cols) + " |", "|---|" + "---:|" * len(cols)]
+    for _, name, v in rows[:top]:
+        nm = name.replace("|", "/")
+        nm = nm[:70] + "..." if len(nm) > 73 else nm
+
+        def fmt(x, k):
+            if x is None:
+                return "–"
+            return f"{x:.2f}" if k in ("L2 hit", "wait", "issue", "waves/SIMD") else f"{x:.0f}"
+        lines.append(f"| `{nm}` | " + " | ".join(fmt(v[k], k) for k in cols) + " |")
+    with open(out, "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 TABLE_ORDER = ["deepcnet4_20_strokes_b8", "deepcnet5_50_strokes_b100", "deepcnet5_50_strokes_m8_b100",
                "deepcnet5_100_rgbpatch_b128", "deepcnet6_100_strokes_b64"]
 
@@ -688,7 +743,12 @@ def main():
     ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "OUT_MD"),
                     help="a markdown table of a rocprofv3 --kernel-trace --stats run (no GPU needed)")
     ap.add_argument("--title", default="Kernel trace")
+    ap.add_argument("--wave-summary", nargs="+", metavar="DIR",
+                    help="per-kernel wave counters from rocprofv3 --pmc runs; the last argument is the output .md")
     args = ap.parse_args()
+    if args.wave_summary:
+        wave_summary(args.wave_summary[:-1], args.wave_summary[-1], args.title, args.commands)
+        return
     if args.counter_summary:
         counter_summary(args.group, *args.counter_summary, args.workload, args.dtype, args.commands)
         return
