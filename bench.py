@@ -724,6 +724,27 @@ def write_table(path, rows, steps, warmup):
         f.write("\n".join(lines) + "\n")
 
 
+def write_batch_sweep(path, rows, steps, warmup, base):
+    """Throughput and roofline fractions of one workload at several batch sizes (context for the
+    fixed-batch headline: how far the same kernels go when each launch has more work)."""
+    lines = [f"# Batch sweep: {base} (one MI355X)", "",
+             f"Command: `python bench.py --workload {base} --batch-sweep {' '.join(str(r['config']['batch']) for r in rows)} "
+             f"--sweep-out {os.path.relpath(path, ROOT)} --steps {steps} --warmup {warmup}`", "",
+             "The same workload generator and network at other batch sizes (the headline is the batch of the "
+             "measurement plan). Fractions as in the bench line: the dominant kernel group's algorithmic FLOPs over "
+             "its event time, every convolution launch likewise (softmax layer excluded), against the dense MFMA "
+             "peak of the dtype; the rulebook's algorithmic bytes over its event time against 8 TB/s.", "",
+             "| batch | samples/s | ms/step | conv GEMM frac | dominant kernel | its frac | its µs per launch | "
+             "rulebook µs, HBM frac |", "|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        rb = r["hbm"].get("rulebook") or {}
+        lines.append(f"| {r['config']['batch']} | {r['value']:,.0f} | {r['ms_per_step']:.3f} | "
+                     f"{r['conv_gemm']['frac']:.4f} | {r['roofline']['kernel']} | {r['roofline']['frac']:.4f} | "
+                     f"{r['roofline']['avg_launch_us']:.1f} | {rb.get('us_per_step', '–')}, {rb.get('frac', '–')} |")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -743,6 +764,9 @@ def main():
     ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "OUT_MD"),
                     help="a markdown table of a rocprofv3 --kernel-trace --stats run (no GPU needed)")
     ap.add_argument("--title", default="Kernel trace")
+    ap.add_argument("--batch-sweep", nargs="+", type=int, default=None,
+                    help="time the workload at these batch sizes (context only), write --sweep-out")
+    ap.add_argument("--sweep-out", default=None)
     ap.add_argument("--wave-summary", nargs="+", metavar="DIR",
                     help="per-kernel wave counters from rocprofv3 --pmc runs; the last argument is the output .md")
     args = ap.parse_args()
@@ -765,6 +789,18 @@ def main():
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.batch_sweep:
+        import dataclasses
+        base = get_config(args.workload)
+        rows = []
+        for b in args.batch_sweep:
+            cfg = dataclasses.replace(base, batch=b, name=f"{base.name}@{b}")
+            rows.append(measure(cfg, args.dtype, args.steps, args.warmup, args.batches, cpu=False))
+            rows[-1]["config"]["batch"] = b
+            print(json.dumps(rows[-1]), flush=True)
+        if args.sweep_out:
+            write_batch_sweep(args.sweep_out, rows, args.steps, args.warmup, base.name)
         return
     if args.table:
         rows = []
