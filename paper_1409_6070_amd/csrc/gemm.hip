@@ -121,6 +121,62 @@ __device__ inline void mma_slab(const T* As, const T* Bs, f32x4 (&acc)[C::TM][C:
   }
 }
 
+// acc += A_tile * B_tile over one slab held in LDS unpadded and swizzled (the
+// bf16 pipeline below): row r's 16-byte chunk c sits in slot c ^ ((r / 2) % 8)
+// of its 128-byte row, so the sixteen rows an MFMA operand read touches cover
+// all 64 banks once.
+template <class C>
+__device__ inline void mma_slab_sw(const __bf16* As, const __bf16* Bs, f32x4 (&acc)[C::TM][C::TN], int wm, int wn,
+                                   int lane) {
+  const int r16 = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int kb = 0; kb < C::BK; kb += C::KB) {
+    const int chunk = kb / 8 + g;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) {
+        const int ra = wm * C::TM * 16 + i * 16 + r16, rb = wn * C::TN * 16 + j * 16 + r16;
+        MfmaCore<__bf16>::step(As + ra * C::BK + ((chunk ^ ((ra >> 1) & 7)) * 8),
+                               Bs + rb * C::BK + ((chunk ^ ((rb >> 1) & 7)) * 8), acc[i][j]);
+      }
+  }
+}
+
+// s_waitcnt vmcnt(n) lgkmcnt(0), n a compile-time constant: the LDS reads of
+// the previous slab are done before its stage is refilled
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));  // lgkmcnt(0) too
+}
+
+// One 16-byte load per lane from a buffer straight into LDS: lane l's bytes
+// land at LDS byte address lds + 16 l (lds uniform over the wave). An offset
+// at or past the buffer's size reads zero. The compiler does not see this
+// load, so the caller waits for it with wait_vmcnt; its own waits only grow
+// stricter with loads it does not know of. No memory clobber: the caller
+// orders the load against the LDS reads of the same stage with compiler
+// fences around its barriers.
+__device__ inline void dma16(u32x4 rsrc, uint32_t lds, uint32_t off) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds),
+      "v"(off), "s"(rsrc)
+      : "m0");
+}
+
+// raw buffer descriptor: base, no stride, size in bytes
+__device__ inline u32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  return u32x4{(uint32_t)b, (uint32_t)(b >> 32) & 0xffffu, bytes, 0x00020000u};
+}
+
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
 // q = k / d for 0 <= k < 2^20, 1 <= d < 2^16: float estimate, then exact correction.
 __device__ inline int div_small(int k, int d, float rcp) {
   int q = (int)((float)k * rcp);
@@ -200,8 +256,9 @@ __device__ inline void store_pooled(const GemmArgs& a, const T* Cs, const int32_
 }
 
 // Implicit-gather GEMM.  Per tile: the tile's window rows go to LDS once; the
-// next K slab's global loads are issued before the current slab's MFMAs
-// (register prefetch); the output tile is staged in LDS for 16-byte stores.
+// K slabs stream through a ring of LDS stages filled by buffer loads with an
+// LDS destination (bf16; float32 prefetches the next slab into registers);
+// the output tile is staged in LDS for 16-byte stores.
 // With ksplit > 1 each workgroup covers one K range and writes fp32 partial
 // sums, reduced (with the epilogue) by k_gemm_splitk_reduce.
 template <typename T, class C, int RAC>
@@ -212,7 +269,17 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   constexpr bool STAGE = stages_tile<C>();
   static_assert(STAGE == (BM * CS <= SMEM), "staging fits");
   constexpr bool POOL = RAC == POOL_FWD_MODE;
-  __shared__ __attribute__((aligned(16))) T smem[SMEM];
+  // bf16: the operands go from memory straight into LDS (buffer loads with an
+  // LDS destination; an offset past the buffer reads zero), NST slabs in LDS,
+  // NST - 1 of them in flight while one is multiplied, one barrier per slab.
+  // Two stages where three would cost occupancy (the 128x128 tile) or measured
+  // slower (the routed tiles, whose epilogue holds more registers).
+  constexpr bool DMA = sizeof(T) == 2;
+  constexpr int NST = (BM + BN >= 256 || RAC >= 0) ? 2 : 3;
+  constexpr int STG = (BM + BN) * BK;          // elements per stage
+  constexpr int LPS = C::AV + C::BV;           // loads per thread and slab
+  constexpr int SMEM_ALL = DMA ? (NST * STG > SMEM ? NST * STG : SMEM) : SMEM;
+  __shared__ __attribute__((aligned(16))) T smem[SMEM_ALL];
   __shared__ int32_t Rs[BM * AMAX];
   __shared__ int32_t Cr[POOL ? BM : 1];  // pooling forward: the convolution row of each slot
   T* As = smem;
@@ -274,50 +341,101 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    u32x4 ra[C::AV], rb[C::BV];
     const float rcp_cseg = 1.f / (float)a.cseg;
-    auto load = [&](int k0) {
-      int srow[C::AV], col[C::AV];
+    if constexpr (DMA) {
+      // A: one 16-byte slot per load (row v / 8, slot v % 8 holding chunk
+      // (v % 8) ^ ((row / 2) % 8)); rows without a window entry and k past K read zero
+      const u32x4 rsA = buffer_rsrc(src, GATHER_SRC_BYTES);
+      const u32x4 rsB = buffer_rsrc(Bt, (uint32_t)a.Npad * (uint32_t)a.Kpad * 2u);
+      const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // in a scalar register
+      const uint32_t lds0 = lds_addr(smem);
+      auto issue = [&](int k0, int st) {
+        const uint32_t la = lds0 + (uint32_t)(st * STG) * 2u, lb = la + BM * BK * 2;
+        uint32_t off[C::AV];
 #pragma unroll
-      for (int j = 0; j < C::AV; ++j) {  // window row and channel of each vector, then all loads at once
-        const int v = tid + j * NT;
-        const int r = v / KV, kv = v - r * KV;
-        const int k = k0 + kv * VE;
-        const bool in_k = k < a.K;
-        const int f = in_k ? div_small(k, a.cseg, rcp_cseg) : 0;
-        srow[j] = in_k ? Rs[r * A + f] : -1;
-        col[j] = in_k ? k - f * a.cseg : 0;
-      }
+        for (int j = 0; j < C::AV; ++j) {  // every window row read before the first load goes out
+          const int v = tid + j * NT;
+          const int r = v >> 3, c = (v & 7) ^ ((r >> 1) & 7);
+          const int k = k0 + c * 8;
+          const bool in_k = k < a.K;
+          const int f = div_small(k, a.cseg, rcp_cseg);
+          const int srow = Rs[r * A + (in_k ? f : 0)];
+          off[j] = in_k && srow >= 0 ? (uint32_t)(srow * a.src_stride + (k - f * a.cseg)) * 2u : GATHER_SRC_BYTES;
+        }
 #pragma unroll
-      for (int j = 0; j < C::AV; ++j) {
-        const u32x4 val = *(const u32x4*)(src + (int64_t)max(srow[j], 0) * a.src_stride + col[j]);
-        ra[j] = srow[j] >= 0 ? val : u32x4{0u, 0u, 0u, 0u};
-      }
+        for (int j = 0; j < C::AV; ++j) dma16(rsA, la + (uint32_t)(wave_u * 64 + j * NT) * 16u, off[j]);
 #pragma unroll
-      for (int j = 0; j < C::BV; ++j) {
-        const int v = tid + j * NT;
-        const int r = v / KV, kv = v - r * KV;
-        rb[j] = *(const u32x4*)(Bt + (int64_t)(n0 + r) * a.Kpad + k0 + kv * VE);
-      }
-    };
-    if (kbeg < kend) load(kbeg);
-    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+        for (int j = 0; j < C::BV; ++j) {
+          const int v = tid + j * NT;
+          const int r = v >> 3, c = (v & 7) ^ ((r >> 1) & 7);
+          dma16(rsB, lb + (uint32_t)(wave_u * 64 + j * NT) * 16u, (uint32_t)((n0 + r) * a.Kpad + k0 + c * 8) * 2u);
+        }
+      };
+      const int nsl = (kend - kbeg) / BK;
 #pragma unroll
-      for (int j = 0; j < C::AV; ++j) {
-        const int v = tid + j * NT;
-        const int r = v / KV, kv = v - r * KV;
-        *(u32x4*)(As + r * LDK + kv * VE) = ra[j];
+      for (int p = 0; p < NST - 1; ++p)
+        if (p < nsl) issue(kbeg + p * BK, p);
+      for (int s = 0; s < nsl; ++s) {
+        // this wave's loads of slab s have landed once at most those of the
+        // slabs after it are outstanding; the barrier makes it every wave's
+        asm volatile("" ::: "memory");
+        if constexpr (NST == 3) {
+          if (s + 1 < nsl) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
+        } else {
+          wait_vmcnt<0>();
+        }
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (s + NST - 1 < nsl) issue(kbeg + (s + NST - 1) * BK, (s + NST - 1) % NST);
+        mma_slab_sw<C>(smem + (s % NST) * STG, smem + (s % NST) * STG + BM * BK, acc, wm, wn, lane);
       }
+      asm volatile("" ::: "memory");
+      __syncthreads();  // every wave done with the slabs before the epilogue reuses the memory
+    } else {
+      u32x4 ra[C::AV], rb[C::BV];
+      auto load = [&](int k0) {
+        int srow[C::AV], col[C::AV];
 #pragma unroll
-      for (int j = 0; j < C::BV; ++j) {
-        const int v = tid + j * NT;
-        const int r = v / KV, kv = v - r * KV;
-        *(u32x4*)(Bs + r * LDK + kv * VE) = rb[j];
+        for (int j = 0; j < C::AV; ++j) {  // window row and channel of each vector, then all loads at once
+          const int v = tid + j * NT;
+          const int r = v / KV, kv = v - r * KV;
+          const int k = k0 + kv * VE;
+          const bool in_k = k < a.K;
+          const int f = in_k ? div_small(k, a.cseg, rcp_cseg) : 0;
+          srow[j] = in_k ? Rs[r * A + f] : -1;
+          col[j] = in_k ? k - f * a.cseg : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < C::AV; ++j) {
+          const u32x4 val = *(const u32x4*)(src + (int64_t)max(srow[j], 0) * a.src_stride + col[j]);
+          ra[j] = srow[j] >= 0 ? val : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int j = 0; j < C::BV; ++j) {
+          const int v = tid + j * NT;
+          const int r = v / KV, kv = v - r * KV;
+          rb[j] = *(const u32x4*)(Bt + (int64_t)(n0 + r) * a.Kpad + k0 + kv * VE);
+        }
+      };
+      if (kbeg < kend) load(kbeg);
+      for (int k0 = kbeg; k0 < kend; k0 += BK) {
+#pragma unroll
+        for (int j = 0; j < C::AV; ++j) {
+          const int v = tid + j * NT;
+          const int r = v / KV, kv = v - r * KV;
+          *(u32x4*)(As + r * LDK + kv * VE) = ra[j];
+        }
+#pragma unroll
+        for (int j = 0; j < C::BV; ++j) {
+          const int v = tid + j * NT;
+          const int r = v / KV, kv = v - r * KV;
+          *(u32x4*)(Bs + r * LDK + kv * VE) = rb[j];
+        }
+        __syncthreads();
+        if (k0 + BK < kend) load(k0 + BK);
+        mma_slab<T, C>(As, Bs, acc, wm, wn, lane);
+        __syncthreads();
       }
-      __syncthreads();
-      if (k0 + BK < kend) load(k0 + BK);
-      mma_slab<T, C>(As, Bs, acc, wm, wn, lane);
-      __syncthreads();
     }
 
     const int g = lane >> 4, c16 = lane & 15;

@@ -171,6 +171,11 @@ struct GemmArgs {
 constexpr int POOL_FWD_MODE = -2;
 constexpr int MASK_MODE = -3;
 
+// Byte range of the buffer descriptor through which the bf16 gather GEMM reads
+// its source rows; offsets at or past it read zero (rows without a window
+// entry use that), so every source row must end below it.
+constexpr uint32_t GATHER_SRC_BYTES = 0x7ffffff0u;
+
 // Whether a tile shape stages its output tile through LDS (16-byte stores), as
 // the pooling backward in the epilogue needs.
 bool gemm_routes(bool bf16, int cfg);
