@@ -423,10 +423,10 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.rows_d = L[s - 1].cap + 1;
     // a convolution under a pooling layer computes that layer in its epilogue
     const bool pooled = s + 1 < net->nlayers && L[s + 1].kind == 2;
-    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.A * P.cp_in, false, pooled ? 1000 : 4000);
+    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.A * P.cp_in, false, pooled ? 256 : 128);
     // an input gradient that is a pooling layer's may route its rows through the
     // pooling windows in its epilogue
-    P.pd = plan_gemm(net->bf16, P.rows_d, P.c_in, P.A * P.cp_out, L[s - 1].kind == 2);
+    P.pd = plan_gemm(net->bf16, P.rows_d, P.c_in, P.A * P.cp_out, L[s - 1].kind == 2, 600);
     P.NpadF = P.pf.Npad;
     P.KpadF = P.pf.Kpad;
     P.NpadD = P.pd.Npad;
@@ -452,8 +452,8 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
     P.cp_out = net->dl_stride;
     P.rows_f = d.batch_max;
     P.rows_d = d.batch_max;
-    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.cp_in);
-    P.pd = plan_gemm(net->bf16, P.rows_d, P.c_in, P.cp_out);
+    P.pf = plan_gemm(net->bf16, P.rows_f, P.c_out, P.cp_in, false, 128);
+    P.pd = plan_gemm(net->bf16, P.rows_d, P.c_in, P.cp_out, false, 128);
     P.NpadF = P.pf.Npad;
     P.KpadF = P.pf.Kpad;
     P.NpadD = P.pd.Npad;

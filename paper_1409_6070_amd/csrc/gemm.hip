@@ -816,12 +816,14 @@ hipError_t launch_gemm(bool bf16, const GemmArgs& args, int64_t max_rows, hipStr
 GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K, bool short_rows, int direct_max) {
   // bf16 launches with few output tiles (at the row bound) go to the
   // direct-operand kernel, whose waves split K and so keep many loads in flight
-  // per tile; launches with many tiles keep the LDS-tiled kernel, whose 128-row
-  // tiles share each weight slab between four waves.  (Measured on the pen-stroke
-  // DeepCNet(5,50): the direct kernel wins at <= 3.3k tiles of 32 x 64 and loses
-  // from 4.5k up; very deep K keeps split-K.  A convolution with the pooling
-  // forward in its epilogue passes a lower bound, 1,000 tiles: its 1.25k-tile
-  // launch there takes 21.1 us LDS-tiled against 22.7 us direct.)
+  // per tile; launches with more tiles keep the LDS-tiled kernel, whose slabs
+  // stream through LDS stages shared by the tile's waves.  (Measured on the
+  // pen-stroke DeepCNet(5,50), bf16, batch 100, tiles counted as 32 x 64 at the
+  // row bound: input gradients with the pooling backward, direct 18.7 us against
+  // 19.6 us at 316 tiles, but 24.1 against 20.4 at 1.1k and 31.1 against 20.9
+  // at 3.3k; forward with the pooling forward even at 204 tiles; the softmax
+  // layer's forward, 236 tiles, 7.2 us direct against 6.6 LDS-tiled.  The
+  // callers pass 600, 256 and 128.)
   const int64_t direct_tiles = ((max_rows + DIRECT_BM - 1) / DIRECT_BM) * ((N + DIRECT_BN - 1) / DIRECT_BN);
   if (bf16 && direct_tiles <= direct_max && K <= 2048) {
     // waves per tile so that each sums at most about four 32-wide k blocks,

@@ -241,7 +241,7 @@ struct GemmTile {
   int BM, BN, BK;
 };
 GemmTile gemm_tile(bool bf16, int cfg);
-GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K, bool short_rows = false, int direct_max = 4000);
+GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K, bool short_rows, int direct_max);
 // weight-gradient tiles: 128 rows of dW, 128 or 64 columns
 constexpr int WG_BM = 128;
 inline int wgrad_bn(int c_out) { return (c_out + 127) / 128 * 128 <= (c_out + 63) / 64 * 64 ? 128 : 64; }
