@@ -400,10 +400,11 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
       return SSCN_ERR_INVALID_ARGUMENT;
     }
     L[s].Wd = (L[s].S + 63) / 64;
-    // 32-bit element offsets everywhere; bf16 feature rows are also read
-    // through buffer descriptors whose byte range stops below 2^31
+    // 32-bit element offsets everywhere; bf16 feature rows and window lists
+    // are also read through buffer descriptors whose byte range stops below 2^31
     const int64_t elems = (L[s].cap + 1) * (int64_t)std::max(L[s].Cp, std::max(L[s].A, 1));
-    if (elems >= (1ll << 31) || (net->bf16 && elems * 2 > GATHER_SRC_BYTES)) {
+    const int64_t rule_bytes = (L[s].cap + 1) * (int64_t)std::max(L[s].A, 1) * 4;  // window lists, read the same way
+    if (elems >= (1ll << 31) || (net->bf16 && (elems * 2 > GATHER_SRC_BYTES || rule_bytes > GATHER_SRC_BYTES))) {
       delete net;
       return SSCN_ERR_INVALID_ARGUMENT;
     }

@@ -167,6 +167,16 @@ __device__ inline void dma16(u32x4 rsrc, uint32_t lds, uint32_t off) {
       : "m0");
 }
 
+// The same for 4 bytes per lane: lane l's dword lands at lds + 4 l.
+__device__ inline void dma4(u32x4 rsrc, uint32_t lds, uint32_t off) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dword %1, %2, 0 offen lds" ::"s"(lds),
+      "v"(off), "s"(rsrc)
+      : "m0");
+}
+
 // raw buffer descriptor: base, no stride, size in bytes
 __device__ inline u32x4 buffer_rsrc(const void* base, uint32_t bytes) {
   const uint64_t b = (uint64_t)base;
@@ -695,6 +705,273 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp, ExtraTask x) {
   }
 }
 
+// Pair swizzle of an LDS row of sites for the transpose reads below: the
+// 32-byte pair p of row r sits at pair slot p ^ swz(r).  A wavefront's read
+// touches rows {0..3, 8..11} (+ 16, + 4, + 32) in each half, so the swizzle
+// spreads each such set of eight rows over all 64 banks: 256-byte rows by
+// (r % 4, r / 8 % 2), 128-byte rows (two per bank sweep) by (r / 2 % 2, r / 8 % 2).
+template <int ROW_BYTES>
+__device__ inline int site_row_swz(int r) {
+  static_assert(ROW_BYTES == 256 || ROW_BYTES == 128, "row width");
+  if constexpr (ROW_BYTES == 256)
+    return (r & 3) | (((r >> 3) & 1) << 2);
+  else
+    return ((r >> 1) & 1) | (((r >> 3) & 1) << 1);
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+// 8 consecutive sites of one column as an MFMA operand (k = sites): two LDS
+// transpose reads of 4 sites each.  Within each 16-lane group, lane q reads
+// 4 columns (4 (q % 4) .. + 3) of site row q / 4 and receives column q of the
+// group's 4 rows; `p` points at lane q's 4 columns of the group's first row.
+template <int ROW>
+__device__ inline bf16x8 tr_operand(const __bf16* p) {
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)lds_addr(p));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)lds_addr(p + 4 * ROW));
+  const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// acc += G_slab^T * delta_slab for one slab of BKS sites held as [site][column]
+// (A: BM columns, B: BN columns, pair-swizzled rows).  ONES: this wave's rows
+// hold the bias row m_loc, whose operand is 1 for each of the slab's first
+// `valid` sites and 0 after.
+template <class C, int BKS, bool ONES>
+__device__ inline void mma_slab_tr(const __bf16* As, const __bf16* Bs, f32x4 (&acc)[C::TM][C::TN], int wm, int wn,
+                                   int lane, int m_loc, int valid) {
+  constexpr int BM = C::BM, BN = C::BN;
+  const int g = lane >> 4, q = lane & 15;
+  const int e4 = 4 * (q & 3);
+#pragma unroll
+  for (int kb = 0; kb < BKS; kb += C::KB) {
+    const int row = kb + 8 * g + (q >> 2);
+    const int ha = site_row_swz<BM * 2>(row), hb = site_row_swz<BN * 2>(row);
+    bf16x8 bv[C::TN];
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) bv[j] = tr_operand<BN>(Bs + row * BN + (((wn * C::TN + j) ^ hb) << 4) + e4);
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) {
+      bf16x8 av = tr_operand<BM>(As + row * BM + (((wm * C::TM + i) ^ ha) << 4) + e4);
+      if constexpr (ONES) {
+        if (wm * C::TM * 16 + i * 16 + q == m_loc) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) av[e] = (__bf16)(kb + 8 * g + e < valid ? 1.f : 0.f);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv[j], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+// s_waitcnt vmcnt(BASE + STEP x steps) lgkmcnt(0), steps a run-time value in 0 .. 3
+template <int BASE, int STEP>
+__device__ inline void wait_vmcnt_steps(int steps) {
+  switch (steps) {
+    case 0: wait_vmcnt<BASE>(); break;
+    case 1: wait_vmcnt<BASE + STEP>(); break;
+    case 2: wait_vmcnt<BASE + 2 * STEP>(); break;
+    default: wait_vmcnt<BASE + 3 * STEP>(); break;
+  }
+}
+
+// Weight gradients, bf16: the tiles and site chunks of k_wgrad, but the operand
+// slabs (BKS sites) go from memory straight into LDS as stored, one site per
+// LDS row (buffer loads with an LDS destination; an offset past the buffer
+// reads zero), and the MFMA operands are read across sites with the LDS
+// transpose read.  NST stages: the loads of NST - 1 slabs fly while one is
+// multiplied, one barrier per slab.  The window rows of a slab reach LDS the
+// same way, into a ring of NST slots, issued with the operand loads NST - 1
+// slabs before the ones that read them (so that waiting for a slab's operands
+// also covers the window rows of the slab NST - 1 after it).  Every wave issues
+// the same number of window-row loads per slab (unused ones read zero into a
+// spare row), which keeps the wait counts compile-time constants.
+template <class C, int BKS, int NST>
+__global__ void __launch_bounds__(C::NT) k_wgrad_tr(WGradGroup grp, ExtraTask x) {
+  using T = __bf16;
+  constexpr int BM = C::BM, BN = C::BN, NT = C::NT, BK = C::BK;
+  static_assert(NT == 256 && BM == 128 && BK % BKS == 0 && BKS % C::KB == 0 && NST >= 2 && NST <= 4,
+                "slab and thread layout below");
+  constexpr int ACH = BM / 8, BCH = BN / 8;  // 16-byte chunks per LDS row
+  constexpr int AV = BKS * ACH / NT, BV = BKS * BCH / NT;
+  static_assert(AV * NT == BKS * ACH && BV * NT == BKS * BCH, "slab splits evenly over the threads");
+  constexpr int LPS = AV + BV;                       // operand loads per thread and slab
+  constexpr int STG = BKS * (BM + BN);               // elements per stage
+  // window-row entries per slab, rounded up to whole 64-dword loads: a load's
+  // lanes past the slab's entries still write (zeros) to LDS
+  constexpr int RSLOT = (BKS * AMAX + 63) / 64 * 64;
+  constexpr int NRW = (RSLOT / 64 + 3) / 4;          // window-row loads per wave and slab
+  __shared__ __attribute__((aligned(16))) T smem[NST * STG];
+  __shared__ __attribute__((aligned(16))) int32_t Rr[NST * RSLOT + 64];  // + a spare row for unused loads
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  if (run_extra<T>(x)) return;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lds_s = lds_addr(smem), lds_r = lds_addr(Rr), lds_spare = lds_r + NST * RSLOT * 4;
+  // this thread's 16-byte LDS slots, the same in every slab: A rows tid / ACH +
+  // j NT / ACH at slot tid % ACH, B rows tid / BCH + j NT / BCH at slot tid % BCH
+  // (the row bits the swizzle reads do not change with j), and the logical
+  // column chunk each slot holds
+  const int ra0 = tid / ACH, ta = tid % ACH, rb0 = tid / BCH, tb = tid % BCH;
+  const int ca = 2 * ((ta >> 1) ^ site_row_swz<BM * 2>(ra0)) + (ta & 1);
+  const int cb = 2 * ((tb >> 1) ^ site_row_swz<BN * 2>(rb0)) + (tb & 1);
+
+  for (int t = blockIdx.x; t < grp.tile_beg[grp.n]; t += own_grid(x)) {
+    int l = 0;
+    while (l + 1 < grp.n && t >= grp.tile_beg[l + 1]) ++l;
+    const WGradArgs& a = grp.L[l];
+    const int tile = t - grp.tile_beg[l];
+    const int rows = a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host;
+    const int tiles_m = a.Mpad / BM, tiles_n = a.Npad / BN;
+    const int nch = wgrad_chunks_dev(a, rows, BK);
+    const int per = ((rows + nch - 1) / nch + BK - 1) / BK * BK;
+    const int m_gather = a.A * a.cseg;
+    const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;  // rows of dW / db that are read back
+    const int tn = tile % tiles_n;
+    const int tq = tile / tiles_n;
+    const int tm = tq % tiles_m;
+    const int chunk = tq / tiles_m;
+    if (chunk >= nch) continue;  // fewer rows than the plan allowed for
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int o_beg = chunk * per;
+    const int o_end = min(rows, o_beg + per);
+    const int nsl = o_end > o_beg ? (o_end - o_beg + BKS - 1) / BKS : 0;
+    f32x4 acc[C::TM][C::TN];
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int A = a.A;
+    const int ma = m0 + 8 * ca;  // first column of this thread's A chunk: window position fa, channel cola
+    const bool a_col = ma < m_gather;
+    const int fa = a_col ? ma / a.cseg : 0;
+    const int cola = ma - fa * a.cseg;
+    const int nb = n0 + 8 * cb;
+    const bool b_col = nb < a.dsrc_cols;
+    const bool has_r = a.rmap != nullptr;
+    const int r_loads = has_r ? (BKS * A + 63) / 64 : 0;  // 64-dword loads that carry window rows
+    const u32x4 rsA = buffer_rsrc(a.src, GATHER_SRC_BYTES);
+    const u32x4 rsB = buffer_rsrc(a.dsrc, GATHER_SRC_BYTES);
+    const u32x4 rsR = buffer_rsrc(a.rmap, GATHER_SRC_BYTES);
+    const float rcpA = 1.f / (float)A;
+    // window rows of slab s (sites ob .. ob + BKS - 1, A entries each,
+    // contiguous) into ring slot s % NST: wave w's i-th load takes dwords
+    // 64 k .. 64 k + 63, k = w + 4 i; NRW loads per wave whatever A and s
+    auto issue_rows = [&](int s) {
+      const int ob = o_beg + s * BKS;
+      const uint32_t dst = lds_r + (uint32_t)((s % NST) * RSLOT) * 4u;
+#pragma unroll
+      for (int i = 0; i < NRW; ++i) {
+        const int k = wave_u + 4 * i;
+        const bool used = s < nsl && k < r_loads;
+        const int d = 64 * k + lane;
+        const bool live = used && d < BKS * A && ob + div_small(d, A, rcpA) < o_end;
+        dma4(rsR, used ? dst + (uint32_t)k * 256u : lds_spare, live ? (uint32_t)(ob * A + d) * 4u : GATHER_SRC_BYTES);
+      }
+    };
+    // operand slab s into stage s % NST, reading its window rows from ring slot s % NST
+    auto issue_slab = [&](int s) {
+      const int ob = o_beg + s * BKS;
+      const uint32_t sa = lds_s + (uint32_t)((s % NST) * STG) * 2u, sb = sa + BM * BKS * 2;
+      const int32_t* R = Rr + (s % NST) * RSLOT;
+      uint32_t offa[AV];
+#pragma unroll
+      for (int j = 0; j < AV; ++j) {  // every window row read before the first load goes out
+        const int r = ra0 + j * (NT / ACH);
+        const int o = ob + r;
+        const int srow = has_r ? R[r * A + fa] : o;
+        offa[j] = a_col && o < o_end ? (uint32_t)(srow * a.src_stride + cola) * 2u : GATHER_SRC_BYTES;
+      }
+#pragma unroll
+      for (int j = 0; j < AV; ++j) dma16(rsA, sa + (uint32_t)(wave_u * 64 + j * NT) * 16u, offa[j]);
+#pragma unroll
+      for (int j = 0; j < BV; ++j) {
+        const int o = ob + rb0 + j * (NT / BCH);
+        dma16(rsB, sb + (uint32_t)(wave_u * 64 + j * NT) * 16u,
+              b_col && o < o_end ? (uint32_t)(o * a.dsrc_stride + nb) * 2u : GATHER_SRC_BYTES);
+      }
+    };
+    // the bias row (softmax layer): the wave whose rows hold it patches its operand
+    const int m_loc = a.m_ones - m0;
+    const bool ones = a.m_ones >= 0 && m_loc >= wm * C::TM * 16 && m_loc < (wm + 1) * C::TM * 16;
+
+    if (nsl > 0) {
+      // window rows of the first NST - 1 slabs, their operands, then (once
+      // every wave has read those ring slots) the window rows of the next NST - 1
+      for (int p = 0; p < NST - 1; ++p) issue_rows(p);
+      asm volatile("" ::: "memory");
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      for (int p = 0; p < NST - 1; ++p)
+        if (p < nsl) issue_slab(p);
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0) only: the operand loads stay in flight
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      for (int p = NST - 1; p < 2 * NST - 2; ++p) issue_rows(p);
+    }
+    for (int s = 0; s < nsl; ++s) {
+      // slab s and the window rows of slab s + NST - 1 have landed (this
+      // wave's, and after the barrier every wave's); every wave is done with
+      // slab s - 1 and with the ring slot refilled below.  Loads issued after
+      // those may stay in flight: the window rows issued since (NRW per slab)
+      // and the operand slabs after s that exist.
+      asm volatile("" ::: "memory");
+      if constexpr (NST == 2) {
+        wait_vmcnt<0>();
+      } else {
+        // issued after the last load slab s needs (its operands, or at s <=
+        // NST - 2 the prologue's window rows of slab s + NST - 1): NST - 2
+        // batches of window rows, and the operand slabs i + NST - 1 < nsl
+        // issued by iterations i = max(0, s - NST + 2) .. s - 1
+        const int lo = max(0, s - NST + 2), hi = min(s - 1, nsl - NST);
+        wait_vmcnt_steps<(NST - 2) * NRW, LPS>(hi >= lo ? hi - lo + 1 : 0);
+      }
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      issue_rows(s + 2 * NST - 2);
+      if (s + NST - 1 < nsl) issue_slab(s + NST - 1);
+      const T* As = smem + (s % NST) * STG;
+      const int valid = o_end - (o_beg + s * BKS);
+      if (ones)
+        mma_slab_tr<C, BKS, true>(As, As + BM * BKS, acc, wm, wn, lane, m_loc, valid);
+      else
+        mma_slab_tr<C, BKS, false>(As, As + BM * BKS, acc, wm, wn, lane, m_loc, valid);
+    }
+
+    float* part = a.part + (int64_t)chunk * a.Mpad * a.Npad;
+    const int g = lane >> 4, c16 = lane & 15;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) {
+        const int nn = n0 + wn * C::TN * 16 + j * 16 + c16;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int mm = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
+          if (mm >= m_rows) continue;
+          if (nch > 1) {
+            part[(int64_t)mm * a.Npad + nn] = acc[i][j][r];
+          } else if (nn < a.c_out) {  // single chunk: the sum is final
+            if (mm < m_gather) {
+              const int f = mm / a.cseg, c = mm - f * a.cseg;
+              if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + nn] = acc[i][j][r];
+            } else if (mm == a.m_ones) {
+              a.db[nn] = acc[i][j][r];
+            }
+          }
+        }
+      }
+  }
+}
+
 // dW (and db) from the split-K partials, for a group of layers (block b
 // belongs to layer l with blk_beg[l] <= b < blk_beg[l + 1]).  A block has G
 // thread groups (G = 16, or fewer when there are fewer chunks) of 256/G
@@ -872,6 +1149,14 @@ GemmPlan plan_gemm(bool bf16, int64_t max_rows, int N, int K, bool short_rows, i
   return p;
 }
 
+// sites per slab and LDS stages of the bf16 weight-gradient tiles
+#ifndef WG_SLAB_128
+#define WG_SLAB_128 32
+#define WG_STAGES_128 4
+#define WG_SLAB_64 32
+#define WG_STAGES_64 3
+#endif
+
 hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipStream_t st, const ExtraTask* extra) {
   // cfg: 0 = 128 x 128 tiles, 1 = 128 x 64
   if (n < 1 || n > MAX_WG_LAYERS) return hipErrorInvalidValue;
@@ -882,15 +1167,16 @@ hipError_t launch_wgrad(bool bf16, int cfg, const WGradArgs* layers, int n, hipS
   g.n = n;
   g.tile_beg[0] = 0;
   for (int l = 0; l < n; ++l) {
+    if (layers[l].A < 1 || layers[l].A > AMAX) return hipErrorInvalidValue;
     g.L[l] = layers[l];
     g.tile_beg[l + 1] = g.tile_beg[l] + (layers[l].Mpad / 128) * (layers[l].Npad / BN) * layers[l].nchunks;
   }
   const int grid = std::min(std::max(g.tile_beg[n], 1), device_grid_limit()) + (x.kind ? x.blocks : 0);
   if (bf16) {
     if (cfg == 0)
-      hipLaunchKernelGGL((k_wgrad<__bf16, C128x128<__bf16>>), dim3(grid), dim3(256), 0, st, g, x);
+      hipLaunchKernelGGL((k_wgrad_tr<C128x128<__bf16>, WG_SLAB_128, WG_STAGES_128>), dim3(grid), dim3(256), 0, st, g, x);
     else
-      hipLaunchKernelGGL((k_wgrad<__bf16, C128x64<__bf16>>), dim3(grid), dim3(256), 0, st, g, x);
+      hipLaunchKernelGGL((k_wgrad_tr<C128x64<__bf16>, WG_SLAB_64, WG_STAGES_64>), dim3(grid), dim3(256), 0, st, g, x);
   } else {
     if (cfg == 0)
       hipLaunchKernelGGL((k_wgrad<float, C128x128<float>>), dim3(grid), dim3(256), 0, st, g, x);
