@@ -195,6 +195,28 @@ __device__ inline int div_small(int k, int d, float rcp) {
   return q;
 }
 
+// Routing inputs of the items a thread takes in store_staged (AC >= 0 and at
+// most two items per thread), all loaded before the first item is routed: one
+// memory round trip for the thread's items, not one each.
+template <typename T, class C, int AC>
+struct StagedRoute {
+  static constexpr int NV = C::BN / C::VE;
+  static constexpr int IPT = (C::BM * NV + C::NT - 1) / C::NT;  // items per thread
+  static constexpr bool ON = AC >= 0 && IPT <= 2;
+  RouteIn<T, AC < 0 ? 0 : AC> q[ON ? IPT : 1];
+  __device__ inline void load(const GemmArgs& a, int m0, int n0, int rows) {
+    if constexpr (ON) {
+#pragma unroll
+      for (int i = 0; i < IPT; ++i) {
+        const int v = threadIdx.x + i * C::NT;
+        const int r = v / NV, m = m0 + r, n = n0 + (v - r * NV) * C::VE;
+        if (v < C::BM * NV && m >= 1 && m < rows && n < a.out_cols)
+          route_load_window<T, AC < 0 ? 0 : AC>(a.pr, m, n, q[i]);
+      }
+    }
+  }
+};
+
 // Stores of an output tile staged in LDS (Cs, pitch CS), 16 bytes at a time.
 // AC >= 0: the pooling backward of every row m >= 1 as well, and the tile's
 // slot partial sums as partial tm (lds: the staging buffer, reused).
@@ -210,14 +232,33 @@ __device__ inline void store_staged(const GemmArgs& a, const T* Cs, int m0, int 
 #pragma unroll
       for (int e = 0; e < VE; ++e) acc[k][e] = 0.f;
   }
-  for (int v = threadIdx.x; v < BM * NV; v += NT) {
-    const int r = v / NV, nv = v - r * NV;
-    const int m = m0 + r, n = n0 + nv * VE;
-    if (m < rows && n < a.out_cols) {
-      const u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
-      *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
-      if constexpr (AC >= 0)
-        if (m >= 1) pool_route_item<T, AC>(a.pr, m, n, (const T*)&o, acc);
+  if constexpr (StagedRoute<T, C, AC>::ON) {
+    StagedRoute<T, C, AC> pre;
+    pre.load(a, m0, n0, rows);
+#pragma unroll
+    for (int i = 0; i < StagedRoute<T, C, AC>::IPT; ++i) {
+      const int v = threadIdx.x + i * NT;
+      const int r = v / NV, nv = v - r * NV;
+      const int m = m0 + r, n = n0 + nv * VE;
+      if (v < BM * NV && m < rows && n < a.out_cols) {
+        const u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
+        *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
+        if (m >= 1) {
+          route_load_children<T, AC>(a.pr, n, pre.q[i]);
+          route_apply<T, AC>(a.pr, n, pre.q[i], (const T*)&o, acc);
+        }
+      }
+    }
+  } else {
+    for (int v = threadIdx.x; v < BM * NV; v += NT) {
+      const int r = v / NV, nv = v - r * NV;
+      const int m = m0 + r, n = n0 + nv * VE;
+      if (m < rows && n < a.out_cols) {
+        const u32x4 o = *(const u32x4*)(Cs + r * CS + nv * VE);
+        *(u32x4*)((T*)a.out + (int64_t)m * a.out_stride + n) = o;
+        if constexpr (AC >= 0)
+          if (m >= 1) pool_route_item<T, AC>(a.pr, m, n, (const T*)&o, acc);
+      }
     }
   }
   if constexpr (AC >= 0) tile_slot_sums<VE, J, NT, NV, (BM + BN) * C::LDK * (int)sizeof(T) / 4>(acc, lds, a.pr, n0, tm);
