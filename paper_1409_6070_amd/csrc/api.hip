@@ -13,6 +13,12 @@
 #include "common.h"
 #include "kernels.h"
 
+// site slabs (64 sites) per weight-gradient chunk, 128- and 64-wide tiles
+#ifndef WG_SLABS_128
+#define WG_SLABS_128 8
+#define WG_SLABS_64 12
+#endif
+
 using namespace sscn;
 
 namespace {
@@ -76,7 +82,7 @@ struct sscn_net {
   ParamPlan P[MAX_LAYERS];
   int dl_stride;  // dlogits row stride (elements)
   int pool_parts;
-  int wgrad_slabs;
+  int wgrad_slabs[2];  // slabs of sites per weight-gradient chunk, 128- and 64-wide tiles
   // global workspace pointers
   int32_t* counts;
   int32_t* err;   // [4]: the input-error word, then completion counters (zeroed by every rulebook build,
@@ -333,7 +339,8 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
   net->nconv = nin ? 2 * d.ell + 2 : d.ell + 1;
   net->nparams = net->nconv + 1;
   net->pool_parts = 1024;  // most row blocks per slot of a bias / ground-row reduction
-  net->wgrad_slabs = 8;    // slabs of sites per weight-gradient workgroup
+  net->wgrad_slabs[0] = WG_SLABS_128;
+  net->wgrad_slabs[1] = WG_SLABS_64;
   const int BK = net->bf16 ? 64 : 32;
   const int VE = net->VE;
   auto cp = [VE](int c) { return (int)round_up(c, VE); };
@@ -440,7 +447,7 @@ sscn_status sscn_net_create(const sscn_net_desc* desc, sscn_net** out) {
       const int m_rows = P.A * P.cp_in;
       const int64_t row_bytes = (int64_t)(P.A * P.cp_in + P.cp_out) * net->esz;
       const int64_t part_bytes = (int64_t)m_rows * P.Npad_w * 4;
-      P.nchunks = wgrad_chunks(L[s].cap + 1, net->wgrad_slabs, BK, row_bytes, part_bytes);
+      P.nchunks = wgrad_chunks(L[s].cap + 1, net->wgrad_slabs[P.bn_w == 128 ? 0 : 1], BK, row_bytes, part_bytes);
     }
   }
   {
@@ -829,7 +836,7 @@ static WGradArgs conv_wgrad_args(const sscn_net* net, int s) {
   w.rows_dev = net->counts + s;
   w.rows_add = 1;
   w.nchunks = P.nchunks;
-  w.slabs = net->wgrad_slabs;
+  w.slabs = net->wgrad_slabs[P.bn_w == 128 ? 0 : 1];
   w.part = net->wpart + P.part_off;
   w.cfg = P.bn_w == 128 ? 0 : 1;
   w.dW = net->dW[ci];
