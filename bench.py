@@ -555,7 +555,10 @@ COUNTER_GROUPS = {
     "k_gemm_direct 32x64: input gradient + pooling backward": (
         r"k_gemm_direct<\d+, [04]>", "gemm_direct.hip epilogue.h pool_route.h ground_tasks.h kernels.h common.h"),
     "k_wgrad (all weight gradients, grouped)": (
-        r"k_wgradI|k_wgrad<", "gemm.hip kernels.h common.h ground_tasks.h"),
+        r"k_wgrad_trI|k_wgradI|k_wgrad<", "gemm.hip kernels.h common.h ground_tasks.h"),
+    "k_gemm_gather 64x64: input gradient + pooling backward": (
+        r"k_gemm_gatherIDF16bNS_4GCfgIDF16bLi2ELi2ELi2ELi2EEELi[04]EEE|k_gemm_gather<.*, [04]>\(sscn::GemmArgs\)",
+        "gemm.hip epilogue.h pool_route.h ground_tasks.h kernels.h common.h"),
 }
 
 
