@@ -323,15 +323,17 @@ __global__ void __launch_bounds__(C::NT) k_gemm_gather(GemmArgs a) {
   // bf16: the operands go from memory straight into LDS (buffer loads with an
   // LDS destination; an offset past the buffer reads zero), NST slabs in LDS,
   // NST - 1 of them in flight while one is multiplied, one barrier per slab.
-  // Two stages where three would cost occupancy (the 128x128 tile) or measured
-  // slower (the routed tiles, whose epilogue holds more registers).
+  // Two stages where three would cost occupancy (the 128x128 tile; the pooled
+  // forward, which then fits three workgroups per compute unit and its
+  // launches one round of workgroups) or measured slower (the routed tiles,
+  // whose epilogue holds more registers).
   constexpr bool DMA = sizeof(T) == 2;
-  constexpr int NST = (BM + BN >= 256 || RAC >= 0) ? 2 : 3;
+  constexpr int NST = (BM + BN >= 256 || RAC >= 0 || POOL) ? 2 : 3;
   constexpr int STG = (BM + BN) * BK;          // elements per stage
   constexpr int LPS = C::AV + C::BV;           // loads per thread and slab
   constexpr int SMEM_ALL = DMA ? (NST * STG > SMEM ? NST * STG : SMEM) : SMEM;
   __shared__ __attribute__((aligned(16))) T smem[SMEM_ALL];
-  __shared__ int32_t Rs[BM * AMAX];
+  extern __shared__ int32_t Rs[];  // [BM * A] window entries, sized at launch
   __shared__ int32_t Cr[POOL ? BM : 1];  // pooling forward: the convolution row of each slot
   T* As = smem;
   T* Bs = smem + BM * LDK;
@@ -1082,11 +1084,12 @@ static void launch_cfg(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
                            : !a.route ? k_gemm_gather<T, C, -1>
                            : a.route_ac == 4 ? k_gemm_gather<T, C, 4>
                                              : k_gemm_gather<T, C, 0>;
+  const size_t lds = (size_t)C::BM * a.A * sizeof(int32_t);  // the window table: a workgroup's LDS follows A
   if (timed)
-    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), 0, st, a.t_start,
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), lds, st, a.t_start,
                           a.ksplit > 1 && !a.partials_only ? nullptr : a.t_stop, 0, a);
   else
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), 0, st, a);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(C::NT), lds, st, a);
   if (a.ksplit > 1 && !a.partials_only) {
     const int64_t total = span * ((a.out_cols + 3) / 4);
     const int g2 = (int)std::min<int64_t>(std::max<int64_t>((total + 255) / 256, 1), 4096);
@@ -1110,6 +1113,7 @@ static void launch_gemm_t(const GemmArgs& a, int64_t max_rows, hipStream_t st) {
 hipError_t launch_gemm(bool bf16, const GemmArgs& args, int64_t max_rows, hipStream_t st) {
   if (max_rows - args.row_begin <= 0) return hipSuccess;
   if (max_rows > INT32_MAX) return hipErrorInvalidValue;
+  if (args.A < 1 || args.A > AMAX) return hipErrorInvalidValue;  // window tables hold at most AMAX entries a row
   GemmArgs a = args;
   a.rows_cap = (int32_t)max_rows;
   if (a.pool_fwd && (a.route || a.ksplit != 1 || !gemm_routes(bf16, a.cfg) || a.row_begin != 0 || !a.pslot ||
