@@ -215,6 +215,116 @@ __global__ void __launch_bounds__(256) k_conv_narrow(GemmArgs a) {
   }
 }
 
+// bf16: the same layer on the matrix cores.  A wave takes 16 GEMM rows at a
+// time (pooling forward: four windows' slots, window-major) and every output
+// channel in 16-wide blocks.  Its A operand is the rows' gathered inputs with
+// k = f * CIN + c (A * CIN <= 32: one v_mfma_f32_16x16x32_bf16 step, zero
+// past it), its B operand the weights of that k for each block's channels,
+// loaded once per wave.  In the result lane (g, n) holds rows 4 g .. 4 g + 3 of
+// channel n: with pooling, exactly one window's four slots, so the window's
+// first maximum and its position are taken within the lane.  Non-pooled and
+// pooled launches compute every row with the same operation, so their stored
+// rows agree bit for bit.
+constexpr int NARROW_NB = 8;  // at most 8 blocks of 16 output channels
+#ifndef NARROW_MFMA_GRID
+#define NARROW_MFMA_GRID 1280  // workgroups: about one round at five waves per SIMD
+#endif
+
+template <int CIN, bool POOL, int NBM>
+__global__ void __launch_bounds__(256) k_conv_narrow_mfma(GemmArgs a) {
+  typedef __bf16 T;
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const int lane = (int)threadIdx.x & 63;
+  const int i = lane & 15, g = lane >> 4;
+  const int A = a.A;
+  const int nb = (a.out_cols + 15) / 16;
+  const T* Bt = (const T*)a.Bt;
+  const T* X = (const T*)a.src;
+  // (32-bit offsets: the planner keeps every feature, window-list and weight
+  // array of a layer below 2^31 elements)
+  // The weights at k = f * CIN + c (zero past A * CIN) and the bias, staged in
+  // LDS once per workgroup: rows of 32 k padded to 40 elements, so that the
+  // 16 lanes reading one k group (16 channels, 16 bytes each) hit distinct banks.
+  constexpr int LDW = 40;
+  __shared__ __attribute__((aligned(16))) T wl[16 * NBM * LDW];
+  __shared__ float bl[16 * NBM];
+  for (int t = (int)threadIdx.x; t < 16 * NBM * 32; t += (int)blockDim.x) {
+    const int n = t >> 5, k = t & 31, f = k / CIN, c = k - f * CIN;
+    const bool ok = f < A && n < a.N;
+    const T v = Bt[ok ? n * a.Kpad + f * a.cseg + c : 0];
+    wl[n * LDW + k] = ok ? v : Elem<T>::from_f32(0.f);
+  }
+  for (int t = (int)threadIdx.x; t < 16 * NBM; t += (int)blockDim.x) bl[t] = (a.bias && t < a.N) ? a.bias[t] : 0.f;
+  __syncthreads();
+  bf16x8 bw[NBM];
+  float bias[NBM];
+#pragma unroll
+  for (int j = 0; j < NBM; ++j) {  // lane: channel 16 j + i, k = 8 g .. 8 g + 7
+    bw[j] = *(const bf16x8*)(wl + (16 * j + i) * LDW + 8 * g);
+    bias[j] = bl[16 * j + (lane & 15)];
+  }
+  const int64_t rows = a.rows_dev ? (int64_t)(*a.rows_dev + a.rows_add) : (int64_t)a.rows_host;
+  const int64_t M = rows * (POOL ? 4 : 1);  // GEMM rows (pooling: the windows' slots)
+  const int64_t waves = (int64_t)gridDim.x * (blockDim.x / 64);
+  for (int64_t blk = (int64_t)blockIdx.x * (blockDim.x / 64) + ((int)threadIdx.x >> 6); blk * 16 < M; blk += waves) {
+    const int64_t m0 = blk * 16, m = m0 + i;
+    const bool live = m < M;
+    int crow = (int)m;  // this lane's A row: its convolution row
+    if constexpr (POOL) crow = live ? a.pslot[m] : 0;
+    if (!live) crow = 0;
+    // A operand: the row's inputs at k = 8 g .. 8 g + 7
+    int idx[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = 8 * g + e, f = k / CIN;
+      idx[e] = f < A ? a.rmap[crow * A + f] : 0;
+    }
+    s16x8 xa;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = 8 * g + e, f = k / CIN, c = k - f * CIN;
+      const T v = X[idx[e] * a.src_stride + c];
+      xa[e] = (f < A && live) ? __builtin_bit_cast(short, v) : (short)0;
+    }
+    const bf16x8 av = __builtin_bit_cast(bf16x8, xa);
+    // the convolution rows of this lane's result rows 4 g .. 4 g + 3
+    int orow[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) orow[r] = __shfl(crow, 4 * g + r, 64);
+#pragma unroll
+    for (int j = 0; j < NBM; ++j) {
+      if (j >= nb) break;
+      const f32x4 d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bw[j], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+      const int n = 16 * j + (lane & 15);
+      if (n >= a.out_cols) continue;
+      T o[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[r] = Elem<T>::from_f32(epi_value<T>(a, d[r], bias[j]));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t mr = m0 + 4 * g + r;
+        // pooling: every slot's convolution row, row 0 from window 0's slot 0 only
+        if (mr < M && (!POOL || orow[r] > 0 || mr == 0)) ((T*)a.out)[orow[r] * a.out_stride + n] = o[r];
+      }
+      if constexpr (POOL) {
+        const int64_t p = (m0 >> 2) + g;
+        if (4 * p < M) {  // first maximum over the window's slots (a later slot only when strictly greater)
+          T mx = o[0];
+          uint8_t am = 0;
+#pragma unroll
+          for (int r = 1; r < 4; ++r)
+            if (Elem<T>::to_f32(o[r]) > Elem<T>::to_f32(mx)) {
+              mx = o[r];
+              am = (uint8_t)r;
+            }
+          ((T*)a.pool_out)[(int)p * a.pool_stride + n] = mx;
+          a.pool_argmax[(int)p * a.pool_stride + n] = am;
+        }
+      }
+    }
+  }
+}
+
 typedef void (*NarrowKernel)(GemmArgs);
 template <typename T, int CIN>
 NarrowKernel narrow_kernel(bool pool) {
@@ -250,6 +360,28 @@ hipError_t launch_conv_narrow(bool bf16, const GemmArgs& in, int cin, int64_t ma
     case 2: kern = bf16 ? narrow_kernel<__bf16, 2>(pool) : narrow_kernel<float, 2>(pool); break;
     case 3: kern = bf16 ? narrow_kernel<__bf16, 3>(pool) : narrow_kernel<float, 3>(pool); break;
     default: kern = bf16 ? narrow_kernel<__bf16, 4>(pool) : narrow_kernel<float, 4>(pool); break;
+  }
+  if (bf16 && a.out_cols <= 16 * NARROW_NB && a.A * cin <= 32) {
+    // matrix cores: one wave per 16 GEMM rows, at most eight waves per SIMD resident
+    const int64_t rows16 = (max_rows * (pool ? 4 : 1) + 15) / 16;
+    const int mgrid = (int)std::min<int64_t>(std::max<int64_t>((rows16 + 3) / 4, 1), NARROW_MFMA_GRID);
+    NarrowKernel mk = nullptr;
+    const bool w4 = a.out_cols <= 64;  // at most four channel blocks: fewer registers
+#define SSCN_NARROW_PICK(C) \
+  mk = pool ? (w4 ? k_conv_narrow_mfma<C, true, 4> : k_conv_narrow_mfma<C, true, NARROW_NB>) \
+            : (w4 ? k_conv_narrow_mfma<C, false, 4> : k_conv_narrow_mfma<C, false, NARROW_NB>)
+    switch (cin) {
+      case 1: SSCN_NARROW_PICK(1); break;
+      case 2: SSCN_NARROW_PICK(2); break;
+      case 3: SSCN_NARROW_PICK(3); break;
+      default: SSCN_NARROW_PICK(4); break;
+    }
+#undef SSCN_NARROW_PICK
+    if (a.t_start || a.t_stop)
+      hipExtLaunchKernelGGL(mk, dim3(mgrid), dim3(256), 0, st, a.t_start, a.t_stop, 0, a);
+    else
+      hipLaunchKernelGGL(mk, dim3(mgrid), dim3(256), 0, st, a);
+    return hipGetLastError();
   }
   if (a.t_start || a.t_stop)
     hipExtLaunchKernelGGL(kern, dim3(grid), dim3(256), lds, st, a.t_start, a.t_stop, 0, a);
