@@ -248,6 +248,11 @@ __global__ void __launch_bounds__(256) k_conv_narrow_mfma(GemmArgs a) {
   constexpr int LDW = 40;
   __shared__ __attribute__((aligned(16))) T wl[16 * NBM * LDW];
   __shared__ float bl[16 * NBM];
+  // each wave's result rows, pooled rows and argmax bytes, staged for 16-byte stores
+  constexpr int CW = 16 * NBM + 8;
+  __shared__ __attribute__((aligned(16))) T cst[4][16 * CW];
+  __shared__ __attribute__((aligned(16))) T pst[4][POOL ? 4 * CW : 8];
+  __shared__ __attribute__((aligned(16))) uint8_t ast[4][POOL ? 4 * CW : 16];
   for (int t = (int)threadIdx.x; t < 16 * NBM * 32; t += (int)blockDim.x) {
     const int n = t >> 5, k = t & 31, f = k / CIN, c = k - f * CIN;
     const bool ok = f < A && n < a.N;
@@ -287,39 +292,49 @@ __global__ void __launch_bounds__(256) k_conv_narrow_mfma(GemmArgs a) {
       xa[e] = (f < A && live) ? __builtin_bit_cast(short, v) : (short)0;
     }
     const bf16x8 av = __builtin_bit_cast(bf16x8, xa);
-    // the convolution rows of this lane's result rows 4 g .. 4 g + 3
-    int orow[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) orow[r] = __shfl(crow, 4 * g + r, 64);
+    T* ct = cst[threadIdx.x >> 6];
 #pragma unroll
     for (int j = 0; j < NBM; ++j) {
       if (j >= nb) break;
       const f32x4 d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bw[j], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
       const int n = 16 * j + (lane & 15);
-      if (n >= a.out_cols) continue;
       T o[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) o[r] = Elem<T>::from_f32(epi_value<T>(a, d[r], bias[j]));
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t mr = m0 + 4 * g + r;
-        // pooling: every slot's convolution row, row 0 from window 0's slot 0 only
-        if (mr < M && (!POOL || orow[r] > 0 || mr == 0)) ((T*)a.out)[orow[r] * a.out_stride + n] = o[r];
-      }
-      if constexpr (POOL) {
-        const int64_t p = (m0 >> 2) + g;
-        if (4 * p < M) {  // first maximum over the window's slots (a later slot only when strictly greater)
-          T mx = o[0];
-          uint8_t am = 0;
+      for (int r = 0; r < 4; ++r) ct[(4 * g + r) * CW + n] = o[r];
+      if constexpr (POOL) {  // first maximum over the window's slots (a later slot only when strictly greater)
+        T mx = o[0];
+        uint8_t am = 0;
 #pragma unroll
-          for (int r = 1; r < 4; ++r)
-            if (Elem<T>::to_f32(o[r]) > Elem<T>::to_f32(mx)) {
-              mx = o[r];
-              am = (uint8_t)r;
-            }
-          ((T*)a.pool_out)[(int)p * a.pool_stride + n] = mx;
-          a.pool_argmax[(int)p * a.pool_stride + n] = am;
-        }
+        for (int r = 1; r < 4; ++r)
+          if (Elem<T>::to_f32(o[r]) > Elem<T>::to_f32(mx)) {
+            mx = o[r];
+            am = (uint8_t)r;
+          }
+        pst[threadIdx.x >> 6][g * CW + n] = mx;
+        ast[threadIdx.x >> 6][g * CW + n] = am;
+      }
+    }
+    // (a wave's LDS operations run in order: the reads below see the writes above)
+    const int nv = a.out_cols / 8;  // 16-byte vectors per row
+#pragma unroll
+    for (int it = 0; it < NBM / 2; ++it) {  // 16 rows x nv vectors, nv <= 2 NBM
+      const int v = lane + 64 * it, row = min(v / nv, 15), cv = v - (v / nv) * nv;
+      const int orr = __shfl(crow, row, 64);  // every lane takes part: the row's convolution row
+      const int64_t mr = m0 + row;
+      // pooling: every slot's convolution row, row 0 from window 0's slot 0 only
+      if (v < 16 * nv && mr < M && (!POOL || orr > 0 || mr == 0))
+        *(uint4*)((T*)a.out + orr * a.out_stride + 8 * cv) = *(const uint4*)(ct + row * CW + 8 * cv);
+    }
+    if constexpr (POOL) {
+      const int w = lane / nv, cv = lane - w * nv;
+      const int64_t p = (m0 >> 2) + w;
+      if (lane < 4 * nv && 4 * p < M) {
+        *(uint4*)((T*)a.pool_out + (int)p * a.pool_stride + 8 * cv) =
+            *(const uint4*)(pst[threadIdx.x >> 6] + w * CW + 8 * cv);
+        *(uint64_t*)(a.pool_argmax + (int)p * a.pool_stride + 8 * cv) =
+            *(const uint64_t*)(ast[threadIdx.x >> 6] + w * CW + 8 * cv);
       }
     }
   }
