@@ -253,31 +253,30 @@ __global__ void __launch_bounds__(256) k_conv_narrow_mfma(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) T cst[4][16 * CW];
   __shared__ __attribute__((aligned(16))) T pst[4][POOL ? 4 * CW : 8];
   __shared__ __attribute__((aligned(16))) uint8_t ast[4][POOL ? 4 * CW : 16];
-  for (int t = (int)threadIdx.x; t < 16 * NBM * 32; t += (int)blockDim.x) {
+  // weight and bias loads first; they reach LDS after the first rows' operand loads went out
+  constexpr int WPT = 16 * NBM * 32 / 256;
+  static_assert(WPT * 256 == 16 * NBM * 32, "whole weight tile per workgroup");
+  T wv[WPT];
+#pragma unroll
+  for (int u = 0; u < WPT; ++u) {
+    const int t = (int)threadIdx.x + 256 * u;
     const int n = t >> 5, k = t & 31, f = k / CIN, c = k - f * CIN;
     const bool ok = f < A && n < a.N;
     const T v = Bt[ok ? n * a.Kpad + f * a.cseg + c : 0];
-    wl[n * LDW + k] = ok ? v : Elem<T>::from_f32(0.f);
+    wv[u] = ok ? v : Elem<T>::from_f32(0.f);
   }
-  for (int t = (int)threadIdx.x; t < 16 * NBM; t += (int)blockDim.x) bl[t] = (a.bias && t < a.N) ? a.bias[t] : 0.f;
-  __syncthreads();
-  bf16x8 bw[NBM];
-  float bias[NBM];
-#pragma unroll
-  for (int j = 0; j < NBM; ++j) {  // lane: channel 16 j + i, k = 8 g .. 8 g + 7
-    bw[j] = *(const bf16x8*)(wl + (16 * j + i) * LDW + 8 * g);
-    bias[j] = bl[16 * j + (lane & 15)];
-  }
+  const float bv = ((int)threadIdx.x < 16 * NBM && a.bias && (int)threadIdx.x < a.N) ? a.bias[threadIdx.x] : 0.f;
   const int64_t rows = a.rows_dev ? (int64_t)(*a.rows_dev + a.rows_add) : (int64_t)a.rows_host;
   const int64_t M = rows * (POOL ? 4 : 1);  // GEMM rows (pooling: the windows' slots)
   const int64_t waves = (int64_t)gridDim.x * (blockDim.x / 64);
-  for (int64_t blk = (int64_t)blockIdx.x * (blockDim.x / 64) + ((int)threadIdx.x >> 6); blk * 16 < M; blk += waves) {
-    const int64_t m0 = blk * 16, m = m0 + i;
+  // this lane's A row of block blk (16 GEMM rows): its convolution row and its
+  // inputs at k = 8 g .. 8 g + 7
+  auto load_a = [&](int64_t blk, int& crow, bf16x8& av) {
+    const int64_t m = blk * 16 + i;
     const bool live = m < M;
-    int crow = (int)m;  // this lane's A row: its convolution row
+    crow = (int)m;
     if constexpr (POOL) crow = live ? a.pslot[m] : 0;
     if (!live) crow = 0;
-    // A operand: the row's inputs at k = 8 g .. 8 g + 7
     int idx[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -291,7 +290,31 @@ __global__ void __launch_bounds__(256) k_conv_narrow_mfma(GemmArgs a) {
       const T v = X[idx[e] * a.src_stride + c];
       xa[e] = (f < A && live) ? __builtin_bit_cast(short, v) : (short)0;
     }
-    const bf16x8 av = __builtin_bit_cast(bf16x8, xa);
+    av = __builtin_bit_cast(bf16x8, xa);
+  };
+  int64_t blk = (int64_t)blockIdx.x * (blockDim.x / 64) + ((int)threadIdx.x >> 6);
+  int crow_n = 0;
+  bf16x8 av_n{};
+  if (blk * 16 < M) load_a(blk, crow_n, av_n);
+#pragma unroll
+  for (int u = 0; u < WPT; ++u) {
+    const int t = (int)threadIdx.x + 256 * u;
+    wl[(t >> 5) * LDW + (t & 31)] = wv[u];
+  }
+  if ((int)threadIdx.x < 16 * NBM) bl[threadIdx.x] = bv;
+  __syncthreads();
+  bf16x8 bw[NBM];
+  float bias[NBM];
+#pragma unroll
+  for (int j = 0; j < NBM; ++j) {  // lane: channel 16 j + i, k = 8 g .. 8 g + 7
+    bw[j] = *(const bf16x8*)(wl + (16 * j + i) * LDW + 8 * g);
+    bias[j] = bl[16 * j + (lane & 15)];
+  }
+  for (; blk * 16 < M; blk += waves) {
+    const int64_t m0 = blk * 16;
+    const int crow = crow_n;
+    const bf16x8 av = av_n;
+    if ((blk + waves) * 16 < M) load_a(blk + waves, crow_n, av_n);  // the next block's loads during this one
     T* ct = cst[threadIdx.x >> 6];
 #pragma unroll
     for (int j = 0; j < NBM; ++j) {
