@@ -24,6 +24,8 @@
 
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 namespace sscn {
 
 template <typename T>
@@ -600,6 +602,48 @@ __device__ inline int wgrad_chunks_dev(const WGradArgs& a, int rows, int BK) {
   return max(1, min(a.nchunks, want));
 }
 
+// A tile's sums for one site chunk.  Several chunks: split-K partials stored
+// as the MFMA result fragments, the layout the reduce reads: per chunk,
+// 16 x 16 blocks (bm, bn) for bm < ceil(m_rows / 16), bn < ceil(c_out / 16)
+// (blocks past the rows and columns read back are not stored), block
+// bm * NB + bn holding 64 lanes x 4 floats, lane 16 g + c the rows 4 g .. 4 g + 3
+// of column c; one 16-byte store per lane and block.  A single chunk: the sums
+// are final and go to dW / db.
+template <class C>
+__device__ inline void store_wgrad_tile(const WGradArgs& a, const f32x4 (&acc)[C::TM][C::TN], int chunk, int nch,
+                                        int m0, int n0, int wm, int wn, int lane, int m_rows, int m_gather) {
+  const int g = lane >> 4, c16 = lane & 15;
+  if (nch > 1) {
+    const int MB = (m_rows + 15) / 16, NB = (a.c_out + 15) / 16;
+    float* part = a.part + (int64_t)chunk * MB * NB * 256;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) {
+        const int bm = m0 / 16 + wm * C::TM + i, bn = n0 / 16 + wn * C::TN + j;
+        if (bm < MB && bn < NB) *(f32x4*)(part + ((int64_t)(bm * NB + bn) * 64 + lane) * 4) = acc[i][j];
+      }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int nn = n0 + wn * C::TN * 16 + j * 16 + c16;
+      if (nn >= a.c_out) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int mm = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
+        if (mm < m_gather) {
+          const int f = mm / a.cseg, c = mm - f * a.cseg;
+          if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + nn] = acc[i][j][r];
+        } else if (mm == a.m_ones) {
+          a.db[nn] = acc[i][j][r];
+        }
+      }
+    }
+}
+
 // Weight-gradient GEMM, split over sites (the K dimension).  A^T and delta^T
 // slabs are staged in LDS as [row of dW / col of dW][site]: each thread loads
 // 16-byte vectors (VE consecutive channels) of 4 consecutive sites and stores
@@ -722,29 +766,7 @@ __global__ void __launch_bounds__(C::NT) k_wgrad(WGradGroup grp, ExtraTask x) {
       __syncthreads();
     }
 
-    float* part = a.part + (int64_t)chunk * a.Mpad * a.Npad;
-    const int g = lane >> 4, c16 = lane & 15;
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int nn = n0 + wn * C::TN * 16 + j * 16 + c16;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int mm = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
-          if (mm >= m_rows) continue;
-          if (nch > 1) {
-            part[(int64_t)mm * a.Npad + nn] = acc[i][j][r];
-          } else if (nn < a.c_out) {  // single chunk: the sum is final
-            if (mm < m_gather) {
-              const int f = mm / a.cseg, c = mm - f * a.cseg;
-              if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + nn] = acc[i][j][r];
-            } else if (mm == a.m_ones) {
-              a.db[nn] = acc[i][j][r];
-            }
-          }
-        }
-      }
+    store_wgrad_tile<C>(a, acc, chunk, nch, m0, n0, wm, wn, lane, m_rows, m_gather);
   }
 }
 
@@ -899,6 +921,9 @@ __global__ void __launch_bounds__(C::NT) k_wgrad_tr(WGradGroup grp, ExtraTask x)
     const bool b_col = nb < a.dsrc_cols;
     const bool has_r = a.rmap != nullptr;
     const int r_loads = has_r ? (BKS * A + 63) / 64 : 0;  // 64-dword loads that carry window rows
+    // (held in registers: the loop's compiler fences would otherwise reload
+    // them from the kernel arguments on every slab)
+    const int src_stride = a.src_stride, dsrc_stride = a.dsrc_stride;
     const u32x4 rsA = buffer_rsrc(a.src, GATHER_SRC_BYTES);
     const u32x4 rsB = buffer_rsrc(a.dsrc, GATHER_SRC_BYTES);
     const u32x4 rsR = buffer_rsrc(a.rmap, GATHER_SRC_BYTES);
@@ -929,7 +954,7 @@ __global__ void __launch_bounds__(C::NT) k_wgrad_tr(WGradGroup grp, ExtraTask x)
         const int r = ra0 + j * (NT / ACH);
         const int o = ob + r;
         const int srow = has_r ? R[r * A + fa] : o;
-        offa[j] = a_col && o < o_end ? (uint32_t)(srow * a.src_stride + cola) * 2u : GATHER_SRC_BYTES;
+        offa[j] = a_col && o < o_end ? (uint32_t)(srow * src_stride + cola) * 2u : GATHER_SRC_BYTES;
       }
 #pragma unroll
       for (int j = 0; j < AV; ++j) dma16(rsA, sa + (uint32_t)(wave_u * 64 + j * NT) * 16u, offa[j]);
@@ -937,7 +962,7 @@ __global__ void __launch_bounds__(C::NT) k_wgrad_tr(WGradGroup grp, ExtraTask x)
       for (int j = 0; j < BV; ++j) {
         const int o = ob + rb0 + j * (NT / BCH);
         dma16(rsB, sb + (uint32_t)(wave_u * 64 + j * NT) * 16u,
-              b_col && o < o_end ? (uint32_t)(o * a.dsrc_stride + nb) * 2u : GATHER_SRC_BYTES);
+              b_col && o < o_end ? (uint32_t)(o * dsrc_stride + nb) * 2u : GATHER_SRC_BYTES);
       }
     };
     // the bias row (softmax layer): the wave whose rows hold it patches its operand
@@ -960,67 +985,52 @@ __global__ void __launch_bounds__(C::NT) k_wgrad_tr(WGradGroup grp, ExtraTask x)
       asm volatile("" ::: "memory");
       for (int p = NST - 1; p < 2 * NST - 2; ++p) issue_rows(p);
     }
-    for (int s = 0; s < nsl; ++s) {
-      // slab s and the window rows of slab s + NST - 1 have landed (this
-      // wave's, and after the barrier every wave's); every wave is done with
-      // slab s - 1 and with the ring slot refilled below.  Loads issued after
-      // those may stay in flight: the window rows issued since (NRW per slab)
-      // and the operand slabs after s that exist.
-      asm volatile("" ::: "memory");
-      if constexpr (NST == 2) {
-        wait_vmcnt<0>();
-      } else {
-        // issued after the last load slab s needs (its operands, or at s <=
-        // NST - 2 the prologue's window rows of slab s + NST - 1): NST - 2
-        // batches of window rows, and the operand slabs i + NST - 1 < nsl
-        // issued by iterations i = max(0, s - NST + 2) .. s - 1
-        const int lo = max(0, s - NST + 2), hi = min(s - 1, nsl - NST);
-        wait_vmcnt_steps<(NST - 2) * NRW, LPS>(hi >= lo ? hi - lo + 1 : 0);
-      }
-      __builtin_amdgcn_s_barrier();
-      asm volatile("" ::: "memory");
-      issue_rows(s + 2 * NST - 2);
-      if (s + NST - 1 < nsl) issue_slab(s + NST - 1);
-      const T* As = smem + (s % NST) * STG;
-      const int valid = o_end - (o_beg + s * BKS);
-      if (ones)
-        mma_slab_tr<C, BKS, true>(As, As + BM * BKS, acc, wm, wn, lane, m_loc, valid);
-      else
-        mma_slab_tr<C, BKS, false>(As, As + BM * BKS, acc, wm, wn, lane, m_loc, valid);
-    }
-
-    float* part = a.part + (int64_t)chunk * a.Mpad * a.Npad;
-    const int g = lane >> 4, c16 = lane & 15;
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int nn = n0 + wn * C::TN * 16 + j * 16 + c16;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int mm = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
-          if (mm >= m_rows) continue;
-          if (nch > 1) {
-            part[(int64_t)mm * a.Npad + nn] = acc[i][j][r];
-          } else if (nn < a.c_out) {  // single chunk: the sum is final
-            if (mm < m_gather) {
-              const int f = mm / a.cseg, c = mm - f * a.cseg;
-              if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + nn] = acc[i][j][r];
-            } else if (mm == a.m_ones) {
-              a.db[nn] = acc[i][j][r];
-            }
-          }
+    // the slab loop, with the bias-row patch compiled into a copy of its own
+    // (a branch per slab made the compiler copy the accumulators between the
+    // two MFMA sequences on every slab)
+    auto slab_loop = [&](auto ones_c) {
+      constexpr bool ONES = decltype(ones_c)::value;
+      for (int s = 0; s < nsl; ++s) {
+        // slab s and the window rows of slab s + NST - 1 have landed (this
+        // wave's, and after the barrier every wave's); every wave is done with
+        // slab s - 1 and with the ring slot refilled below.  Loads issued after
+        // those may stay in flight: the window rows issued since (NRW per slab)
+        // and the operand slabs after s that exist.
+        asm volatile("" ::: "memory");
+        if constexpr (NST == 2) {
+          wait_vmcnt<0>();
+        } else {
+          // issued after the last load slab s needs (its operands, or at s <=
+          // NST - 2 the prologue's window rows of slab s + NST - 1): NST - 2
+          // batches of window rows, and the operand slabs i + NST - 1 < nsl
+          // issued by iterations i = max(0, s - NST + 2) .. s - 1
+          const int lo = max(0, s - NST + 2), hi = min(s - 1, nsl - NST);
+          wait_vmcnt_steps<(NST - 2) * NRW, LPS>(hi >= lo ? hi - lo + 1 : 0);
         }
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        issue_rows(s + 2 * NST - 2);
+        if (s + NST - 1 < nsl) issue_slab(s + NST - 1);
+        const T* As = smem + (s % NST) * STG;
+        const int valid = o_end - (o_beg + s * BKS);
+        mma_slab_tr<C, BKS, ONES>(As, As + BM * BKS, acc, wm, wn, lane, m_loc, valid);
       }
+    };
+    if (ones)
+      slab_loop(std::integral_constant<bool, true>{});
+    else
+      slab_loop(std::integral_constant<bool, false>{});
+
+    store_wgrad_tile<C>(a, acc, chunk, nch, m0, n0, wm, wn, lane, m_rows, m_gather);
   }
 }
 
 // dW (and db) from the split-K partials, for a group of layers (block b
 // belongs to layer l with blk_beg[l] <= b < blk_beg[l + 1]).  A block has G
 // thread groups (G = 16, or fewer when there are fewer chunks) of 256/G
-// threads, four consecutive outputs (one 16-byte partial load per chunk) per
-// thread of a group; group g sums chunks g, g+G, ...; the G group sums are
-// added in a fixed order.
+// threads, one 16-byte fragment quad of the partial layout (rows 4 g .. 4 g + 3
+// of one column) per thread of a group; group g sums chunks g, g+G, ...; the G
+// group sums are added in a fixed order.
 __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
   __shared__ f32x4 red[256];
   int l = 0;
@@ -1029,20 +1039,17 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
   const int nch = wgrad_chunks_dev(a, a.rows_dev ? (*a.rows_dev + a.rows_add) : a.rows_host, grp.BK);
   if (nch <= 1) return;  // the weight-gradient kernel wrote the results
   const int G = grp.G[l];
-  const int E = 256 / G;  // output quads per block
+  const int E = 256 / G;  // quads per block
   const int m_gather = a.A * a.cseg;
   const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : m_gather;
-  const int q_per_row = (a.c_out + 3) / 4;  // quads of 4 consecutive columns (the partials are Npad wide)
-  const int64_t total = (int64_t)m_rows * q_per_row;
+  const int MB = (m_rows + 15) / 16, NB = (a.c_out + 15) / 16;
+  const int64_t total = (int64_t)MB * NB * 64;
   const int el = threadIdx.x % E, grpi = threadIdx.x / E;
   const int64_t t = (int64_t)((int)blockIdx.x - grp.blk_beg[l]) * E + el;
-  int m = 0, n = 0;
   f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
   if (t < total) {
-    m = (int)(t / q_per_row);
-    n = (int)(t - (int64_t)m * q_per_row) * 4;
-    const float* part = a.part + (int64_t)m * a.Npad + n;
-    const int64_t cstride = (int64_t)a.Mpad * a.Npad;
+    const float* part = a.part + t * 4;
+    const int64_t cstride = total * 4;
     for (int ch = grpi; ch < nch; ch += G) s += *(const f32x4*)(part + ch * cstride);
   }
   red[threadIdx.x] = s;
@@ -1050,14 +1057,18 @@ __global__ void __launch_bounds__(256) k_wgrad_reduce(WGradGroup grp) {
   if (grpi != 0 || t >= total) return;
   s = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int g = 0; g < G; ++g) s += red[g * E + el];
+  const int blk = (int)(t >> 6), ln = (int)(t & 63);
+  const int bm = blk / NB, bn = blk - bm * NB;
+  const int n = 16 * bn + (ln & 15);
+  if (n >= a.c_out) return;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    if (n + e >= a.c_out) break;
+  for (int r = 0; r < 4; ++r) {
+    const int m = 16 * bm + 4 * (ln >> 4) + r;
     if (m < m_gather) {
       const int f = m / a.cseg, c = m - f * a.cseg;
-      if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + n + e] = s[e];
+      if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + n] = s[r];
     } else if (m == a.m_ones) {
-      if (a.db) a.db[n + e] = s[e];
+      if (a.db) a.db[n] = s[r];
     }
   }
 }
@@ -1239,8 +1250,9 @@ hipError_t launch_wgrad_reduce(bool bf16, const WGradArgs* layers, int n, hipStr
     const WGradArgs& a = layers[l];
     if (a.nchunks <= 1) continue;  // the weight-gradient kernel wrote the results
     const int m_rows = a.m_ones >= 0 ? a.m_ones + 1 : a.A * a.cseg;
-    const int64_t total = (int64_t)m_rows * ((a.c_out + 3) / 4);  // output quads
-    if (a.Npad % 4) return hipErrorInvalidValue;
+    // fragment quads of the partial layout: 16 x 16 blocks over the rows and
+    // columns read back, 64 per block
+    const int64_t total = (int64_t)((m_rows + 15) / 16) * ((a.c_out + 15) / 16) * 64;
     const int G = a.nchunks >= 16 ? 16 : (a.nchunks >= 8 ? 8 : (a.nchunks >= 4 ? 4 : 2));
     const int E = 256 / G;
     g.L[g.n] = a;
