@@ -625,23 +625,34 @@ __device__ inline void store_wgrad_tile(const WGradArgs& a, const f32x4 (&acc)[C
       }
     return;
   }
+  // a lane's 4 rows 4 g .. 4 g + 3 of block i share one window position f
+  // (cseg and the rows' first index are multiples of 4): one division per block
+  const float rcp_cseg = 1.f / (float)a.cseg;
 #pragma unroll
-  for (int i = 0; i < C::TM; ++i)
+  for (int i = 0; i < C::TM; ++i) {
+    const int mb = m0 + wm * C::TM * 16 + i * 16 + g * 4;
+    const int f = div_small(mb, a.cseg, rcp_cseg), c = mb - f * a.cseg;
+    int idx[4];
+    bool wr[4], br[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      wr[r] = mb + r < m_gather && c + r < a.c_in;
+      br[r] = mb + r == a.m_ones && a.db;
+      idx[r] = (f * a.c_in + c + r) * a.c_out;
+    }
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) {
       const int nn = n0 + wn * C::TN * 16 + j * 16 + c16;
       if (nn >= a.c_out) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int mm = m0 + wm * C::TM * 16 + i * 16 + g * 4 + r;
-        if (mm < m_gather) {
-          const int f = mm / a.cseg, c = mm - f * a.cseg;
-          if (c < a.c_in) a.dW[((int64_t)f * a.c_in + c) * a.c_out + nn] = acc[i][j][r];
-        } else if (mm == a.m_ones) {
+        if (wr[r])
+          a.dW[idx[r] + nn] = acc[i][j][r];
+        else if (br[r])
           a.db[nn] = acc[i][j][r];
-        }
       }
     }
+  }
 }
 
 // Weight-gradient GEMM, split over sites (the K dimension).  A^T and delta^T
