@@ -522,9 +522,6 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   std::memset(&a, 0, sizeof(a));
   a.nlayers = net->nlayers;
   a.batch = batch;
-  SitesWork wk;
-  std::memset(&wk, 0, sizeof(wk));
-  int64_t acc = 0;
   for (int s = 0; s < net->nlayers; ++s) {
     const LayerPlan& L = net->L[s];
     a.L[s] = LayerBits{L.bits, L.wpre, L.scount, L.soff, L.sites, L.S, L.Wd};
@@ -533,11 +530,7 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
     a.rules[s] = L.rules;
     a.rules_t[s] = L.rules_t;
     a.gmask[s] = L.gmask;
-    wk.base[s] = acc;
-    acc += (int64_t)batch * L.S * L.Wd;
   }
-  wk.base[net->nlayers] = acc;
-  wk.total = acc;
   // composite windows: a valid F x F convolution widens the square by F - 1
   // steps of the layer below, a 2 x 2 stride-2 pooling by one step and doubles
   // the step
@@ -563,23 +556,22 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   a.head_rows = net->head_rows;
   a.coords = d_coords;
   a.n = n;
-  // window-list segments, each with workgroups for about two rows per thread at capacity
-  RulesWork rw;
-  std::memset(&rw, 0, sizeof(rw));
-  auto add_seg = [&](int kind, int layer, int64_t rows) {
-    const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>(2048, (rows + 511) / 512));
-    rw.kind[rw.nseg] = kind;
-    rw.layer[rw.nseg] = layer;
-    rw.blk[rw.nseg + 1] = rw.blk[rw.nseg] + blocks;
-    ++rw.nseg;
+  // window-list segments: LISTS_WPB bitmap words of a layer per workgroup (one
+  // workgroup for an empty batch, which writes the ground rows), 256 caller
+  // sites or samples per workgroup
+  ListsWork lw;
+  std::memset(&lw, 0, sizeof(lw));
+  auto add_seg = [&](int kind, int layer, int64_t blocks) {
+    lw.kind[lw.nseg] = kind;
+    lw.layer[lw.nseg] = layer;
+    lw.blk[lw.nseg + 1] = lw.blk[lw.nseg] + (int)std::max<int64_t>(1, blocks);
+    ++lw.nseg;
   };
-  for (int s = 1; s < net->nlayers; ++s) {
-    add_seg(0, s, net->L[s].cap + 1);
-    add_seg(1, s, net->L[s - 1].cap + 1);
-  }
-  add_seg(2, 0, n);
-  add_seg(3, 0, batch);
-  if (timed(net, SSCN_KC_RULEBOOK, st, [&] { return launch_rulebook(a, wk, rw, net->max_words, st); }) != hipSuccess)
+  for (int s = 0; s < net->nlayers; ++s)
+    add_seg(0, s, ((int64_t)batch * net->L[s].S * net->L[s].Wd + LISTS_WPB - 1) / LISTS_WPB);
+  add_seg(2, 0, ((int64_t)n + 255) / 256);
+  add_seg(3, 0, ((int64_t)batch + 255) / 256);
+  if (timed(net, SSCN_KC_RULEBOOK, st, [&] { return launch_rulebook(a, lw, net->max_words, st); }) != hipSuccess)
     return SSCN_ERR_HIP;
   net->rb_parity = 1 - par;
   net->built = true;

@@ -7,23 +7,24 @@
 
 namespace sscn {
 
-struct SitesWork {
-  int64_t total;
-  int64_t base[MAX_LAYERS + 1];
-};
+// Bitmap words of a layer per workgroup of the window-list kernel.
+constexpr int LISTS_WPB = 32;
 
-// Segments of the window-list kernel: kind 0 = R of layer s, 1 = transposes of
-// layer s, 2 = caller-site rows, 3 = head rows; segment i owns workgroups
-// [blk[i], blk[i+1]).
-struct RulesWork {
+// Segments of the window-list kernel: kind 0 = the rows of layer `layer`
+// (their keys, R of that layer, the transposes of the layer above), with
+// ceil(batch * S * Wd / LISTS_WPB) workgroups; 2 = caller-site rows and 3 = head
+// rows, 256 per workgroup; segment i owns workgroups [blk[i], blk[i+1]).
+struct ListsWork {
   int32_t nseg;
-  int32_t kind[2 * MAX_LAYERS + 2];
-  int32_t layer[2 * MAX_LAYERS + 2];
-  int32_t blk[2 * MAX_LAYERS + 3];
+  int32_t kind[MAX_LAYERS + 2];
+  int32_t layer[MAX_LAYERS + 2];
+  int32_t blk[MAX_LAYERS + 3];
 };
 
-hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const RulesWork& rw, int32_t max_words,
-                           hipStream_t st);
+// Insertion, every layer's bitmap, then the window lists (with the sample
+// offsets scanned in each workgroup for 1 <= batch <= 1024, else an offsets
+// launch first).
+hipError_t launch_rulebook(const RulebookArgs& a, const ListsWork& lw, int32_t max_words, hipStream_t st);
 // Clears both alternating input bitmaps (nwords each) and the four error /
 // counter words: once per bound workspace, before its first build.
 hipError_t launch_rulebook_reset(uint64_t* bits_a, uint64_t* bits_b, int64_t nwords, int32_t* err, hipStream_t st);

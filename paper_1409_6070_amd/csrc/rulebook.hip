@@ -18,10 +18,12 @@
 // the windows below is contiguous).  Every layer's bitmap therefore comes
 // straight from the input bitmap, one wave per (sample, layer), with no chain
 // through the layers: the rows of each square are ORed word-parallel, then
-// each output bit tests its column range.  The sample offsets (exclusive scan
-// of the per-sample counts) come from the sites kernel itself for batches of
-// up to 1024 samples: each of its workgroups scans the counts of the layers its
-// words belong to; above that a separate offsets launch computes them (a
+// each output bit tests its column range.  The rows, window lists and
+// transposes of a layer then come from one pass over its bitmap words: a
+// workgroup lists its words' sites in row order in LDS and its threads take
+// them one after another.  The sample offsets (exclusive scan of the
+// per-sample counts) are scanned by every workgroup of that kernel for batches
+// of up to 1024 samples; above that a separate offsets launch computes them (a
 // last-workgroup pattern in the bitmap kernel would need a device-scope release
 // fence, which costs more here than the launch).
 //
@@ -223,13 +225,12 @@ __global__ void __launch_bounds__(64) k_rb_offsets(RulebookArgs a) {
   if (t == 0) a.counts[s] = total;
 }
 
-// Batches up to this size (and builds of at most two 256-word chunks per
-// workgroup) have their sample offsets scanned inside the sites kernel (no
-// separate offsets launch).
-constexpr int SITES_SCAN_MAX = 1024;
+// Batches up to this size have their sample offsets scanned inside the
+// window-list kernel (no separate offsets launch).
+constexpr int LISTS_SCAN_MAX = 1024;
 
 // Exclusive prefix of scount[0, batch) into the LDS array off, by one
-// workgroup of 256 threads (batch <= SITES_SCAN_MAX); returns the total.  All
+// workgroup of 256 threads (batch <= LISTS_SCAN_MAX); returns the total.  All
 // threads call it; it synchronises before returning.
 __device__ inline int block_count_scan(const int32_t* scount, int batch, int* off, int* wsum) {
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
@@ -258,78 +259,22 @@ __device__ inline int block_count_scan(const int32_t* scount, int batch, int* of
   return total;
 }
 
-// The keys of the sites in bitmap word `word` (word rem of sample b in layer
-// L), from row soff_b + wp on (wp: the word's popcount prefix).
-__device__ inline void word_sites(const LayerBits& L, uint64_t word, int wp, int b, int rem, int soff_b) {
-  if (!word) return;
-  const int y = div_rcp(rem, L.Wd, 1.f / (float)L.Wd), w = rem - y * L.Wd;
-  int row = soff_b + wp;
-  while (word) {
-    int bit = __ffsll((long long)word) - 1;
-    word &= word - 1;
-    int x = w * 64 + bit;
-    L.sites[row++] = (b * L.S + y) * L.S + x;
-  }
-}
-
-// Site keys of every layer, in row order: one thread per bitmap word.  SCAN
-// (1 <= batch <= SITES_SCAN_MAX): each workgroup takes 256 consecutive words
-// at a time and scans the per-sample counts of the layers they belong to
-// itself; the thread holding a sample's first word of a layer stores its offset
-// and the thread holding a layer's last word the layer's total.  Otherwise the
-// offsets kernel has stored both.
-template <bool SCAN>
-__global__ void __launch_bounds__(256) k_rb_sites(RulebookArgs a, SitesWork wk) {
-  __shared__ int off[SCAN ? SITES_SCAN_MAX : 1];
-  __shared__ int wsum[4];
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t g0 = (int64_t)blockIdx.x * blockDim.x; g0 < wk.total; g0 += stride) {  // uniform per workgroup
-    const int64_t g = g0 + threadIdx.x;
-    const bool live = g < wk.total;
-    int s = 0;
-    while (s + 1 < a.nlayers && (live ? g : wk.total - 1) >= wk.base[s + 1]) ++s;
-    const LayerBits& L = a.L[s];
-    const int64_t idx = (live ? g : wk.total - 1) - wk.base[s];
-    const int per_sample = L.S * L.Wd;  // words per sample (< 2^20)
-    const int b = div_rcp_d(idx, per_sample);
-    const int rem = (int)(idx - (int64_t)b * per_sample);
-    // the word and its prefix do not depend on the offsets: loaded first
-    const uint64_t word = live ? L.bits[idx] : 0ull;
-    const int wp = live ? L.wpre[idx] : 0;
-    if constexpr (SCAN) {
-      int s_lo = 0;
-      while (s_lo + 1 < a.nlayers && g0 >= wk.base[s_lo + 1]) ++s_lo;
-      const int64_t g_last = min(g0 + (int64_t)blockDim.x, wk.total) - 1;
-      int s_hi = s_lo;
-      while (s_hi + 1 < a.nlayers && g_last >= wk.base[s_hi + 1]) ++s_hi;
-      for (int sl = s_lo; sl <= s_hi; ++sl) {
-        const int total = block_count_scan(a.L[sl].scount, a.batch, off, wsum);
-        if (live && s == sl) {
-          if (rem == 0) L.soff[b] = off[b];
-          if (g == wk.base[s + 1] - 1) a.counts[s] = total;
-          word_sites(L, word, wp, b, rem, off[b]);
-        }
-        __syncthreads();  // off is rewritten by the next layer's scan
-      }
-    } else if (live) {
-      word_sites(L, word, wp, b, rem, L.soff[b]);
-    }
-  }
-}
-
-__device__ inline int32_t rank_row(const LayerBits& L, int b, int y, int x) {
+// Row of location (y, x) of sample b in layer L (0 when inactive); off: the
+// sample's offset (sites in earlier samples).
+__device__ inline int32_t rank_row(const LayerBits& L, int b, int y, int x, int32_t off) {
   int64_t idx = ((int64_t)b * L.S + y) * L.Wd + (x >> 6);
   uint64_t w = L.bits[idx];
   int bit = x & 63;
   if (!((w >> bit) & 1ull)) return 0;
-  return 1 + L.soff[b] + L.wpre[idx] + __popcll(w & ((1ull << bit) - 1ull));
+  return 1 + off + L.wpre[idx] + __popcll(w & ((1ull << bit) - 1ull));
 }
 
 // Rows of the F x F locations (y0 + SIGN*dy, x0 + SIGN*dx), dy, dx < F, of
-// layer L in sample b: 0 where a location is inactive, `outside` where it lies
-// off the grid.  Every word and prefix load is issued before any is used.
+// layer L in sample b (offset off): 0 where a location is inactive, `outside`
+// where it lies off the grid.  Every word and prefix load is issued before any
+// is used.
 template <int F, int SIGN>
-__device__ inline void rank_window(const LayerBits& L, int b, int y0, int x0, int32_t outside,
+__device__ inline void rank_window(const LayerBits& L, int b, int y0, int x0, int32_t outside, int32_t off,
                                    int32_t (&r)[F * F]) {
   constexpr int A = F * F;
   int64_t idx[A];
@@ -351,22 +296,11 @@ __device__ inline void rank_window(const LayerBits& L, int b, int y0, int x0, in
     w[f] = L.bits[idx[f]];
     pre[f] = L.wpre[idx[f]];
   }
-  const int32_t off = L.soff[b];
 #pragma unroll
   for (int f = 0; f < A; ++f) {
     const bool on = (w[f] >> bit[f]) & 1ull;
     r[f] = !in[f] ? outside : on ? 1 + off + pre[f] + __popcll(w[f] & ((1ull << bit[f]) - 1ull)) : 0;
   }
-}
-
-// (b, y, x) of a site key of a layer with side S
-struct SiteKey {
-  int b, y, x;
-};
-__device__ inline SiteKey decode_key(int key, int S) {
-  const int t = div_rcp_d(key, S), x = key - t * S;
-  const int b = div_rcp_d(t, S), y = t - b * S;
-  return SiteKey{b, y, x};
 }
 
 // Child ground mask of pooling location (Y, X) of sample b over a 2x2
@@ -409,135 +343,188 @@ __device__ inline uint16_t child_ground_mask(const LayerBits& L, int b, int Y, i
   return (uint16_t)m;
 }
 
-// R_s for rows [tid, n_out] step `stride` of a layer whose windows are F x F
-// locations below, `step` apart (1: convolution, 2: pooling).  With gm (a
-// pooling layer on a 2x2 convolution over layer Lg) also each row's child
-// ground mask (row 0: all set).  (Lg is a reference into the kernel
-// arguments: taking its address would copy them to scratch memory.)
+// R_s of one row: the rows of layer Li under the F x F window of location
+// (y, x) of sample b (locations step * (y, x) + (dy, dx)), 0 where inactive.
 template <int F>
-__device__ inline void window_rows(const LayerBits& Lo, const LayerBits& Li, int step, int n_out, int32_t* R,
-                                   int64_t tid, int64_t stride, const LayerBits& Lg, uint16_t* gm) {
-  constexpr int A = F * F;
-  for (int64_t o = tid; o <= n_out; o += stride) {
-    int32_t r[A];
-    uint16_t m = 0xFFFF;
-    if (o == 0) {
+__device__ inline void row_window(const LayerBits& Li, int b, int y, int x, int step, int32_t off, int32_t* R) {
+  int32_t r[F * F];
+  rank_window<F, 1>(Li, b, step * y, step * x, 0, off, r);
 #pragma unroll
-      for (int f = 0; f < A; ++f) r[f] = 0;
-    } else {
-      const SiteKey k = decode_key(Lo.sites[o - 1], Lo.S);
-      rank_window<F, 1>(Li, k.b, step * k.y, step * k.x, 0, r);
-      if (gm) m = child_ground_mask(Lg, k.b, k.y, k.x);
-    }
-#pragma unroll
-    for (int f = 0; f < A; ++f) R[o * A + f] = r[f];
-    if (gm) gm[o] = m;
-  }
+  for (int f = 0; f < F * F; ++f) R[f] = r[f];
 }
 
-// Transposed convolution windows: for rows [tid, n_in] of layer s-1, the rows of
-// layer s whose window holds it at each position (-1: none).
+// Rt_s of one row of layer s - 1 at (y, x): the rows of layer Lo (a
+// convolution) whose window holds it at each position, -1 where none.
 template <int F>
-__device__ inline void window_rows_t(const LayerBits& Lo, const LayerBits& Li, int n_in, int32_t* Rt, int64_t tid,
-                                     int64_t stride) {
-  constexpr int A = F * F;
-  for (int64_t i = tid; i <= n_in; i += stride) {
-    int32_t r[A];
-    if (i == 0) {
+__device__ inline void row_window_t(const LayerBits& Lo, int b, int y, int x, int32_t off, int32_t* Rt) {
+  int32_t r[F * F];
+  rank_window<F, -1>(Lo, b, y, x, -1, off, r);
 #pragma unroll
-      for (int f = 0; f < A; ++f) r[f] = -1;
-    } else {
-      const SiteKey k = decode_key(Li.sites[i - 1], Li.S);
-      rank_window<F, -1>(Lo, k.b, k.y, k.x, -1, r);
-    }
-#pragma unroll
-    for (int f = 0; f < A; ++f) Rt[i * A + f] = r[f];
-  }
+  for (int f = 0; f < F * F; ++f) Rt[f] = r[f];
 }
 
-// Window lists (rules), their transposes, the caller-site -> row map and the
-// head rows.  Each list is a segment with its own range of workgroups
-// (RulesWork), grid-strided over its device-side count.
-__global__ void __launch_bounds__(256) k_rb_rules(RulebookArgs a, RulesWork rw) {
+// Rows of every layer, their window lists and transposes, the caller-site ->
+// row map and the head rows, in one launch.  Segment kind 0 (one per layer
+// r): each workgroup takes LISTS_WPB consecutive bitmap words of layer r; the
+// words' sites are listed in LDS in row order (row = 1 + sample offset + word
+// prefix + rank in the word), then every thread takes listed sites one after
+// another and writes, for its site, the key (sites), R_r and the child ground
+// mask (r >= 1), and the row's entries of Rt_{r+1} (r + 1 < nlayers).  Kind 2:
+// caller site -> input row; kind 3: each sample's top-layer row.  SCAN: every
+// workgroup scans the per-sample counts of the layers it looks up (dynamic
+// LDS: three arrays of batch ints); otherwise the offsets kernel has stored
+// them (soff) and the layer totals.
+
+template <bool SCAN>
+__global__ void __launch_bounds__(256) k_rb_lists(RulebookArgs a, ListsWork lw) {
+  extern __shared__ int32_t offs[];  // SCAN: [3][batch], layers r - 1, r, r + 1
+  __shared__ int2 ent[LISTS_WPB * 64];
+  __shared__ int wloc[LISTS_WPB][3];
+  __shared__ int wsum[4];
+  __shared__ int ntot;
   int seg = 0;
-  while (seg + 1 < rw.nseg && (int)blockIdx.x >= rw.blk[seg + 1]) ++seg;
-  const int kind = rw.kind[seg], s = rw.layer[seg];
-  const int nblk = rw.blk[seg + 1] - rw.blk[seg];
-  const int64_t tid = (int64_t)((int)blockIdx.x - rw.blk[seg]) * blockDim.x + threadIdx.x;
-  const int64_t stride = (int64_t)nblk * blockDim.x;
-  if (kind == 0 || kind == 1) {
-    const LayerBits& Lo = a.L[s];
-    const LayerBits& Li = a.L[s - 1];
-    const int F = a.F[s];
-    if (kind == 0) {  // R_s: the window of every row of layer s
-      const int step = (a.kind[s] == 1) ? 1 : 2;
-      const int n_out = a.counts[s];
-      int32_t* R = a.rules[s];
-      const LayerBits& Lg = a.L[s >= 2 ? s - 2 : 0];
-      uint16_t* gm = s >= 2 ? a.gmask[s] : nullptr;
-      if (F == 3)
-        window_rows<3>(Lo, Li, step, n_out, R, tid, stride, Lg, nullptr);
-      else if (F == 2)
-        window_rows<2>(Lo, Li, step, n_out, R, tid, stride, Lg, gm);
+  while (seg + 1 < lw.nseg && (int)blockIdx.x >= lw.blk[seg + 1]) ++seg;
+  const int kind = lw.kind[seg], r = lw.layer[seg];
+  const int t = threadIdx.x;
+  const int bi = (int)blockIdx.x - lw.blk[seg];
+  const int B = a.batch;
+  if (kind == 0) {
+    const LayerBits& Lr = a.L[r];
+    const bool lo = r >= 1, hi = r + 1 < a.nlayers;
+    const int per_s = Lr.S * Lr.Wd;  // words per sample (< 2^20)
+    const int64_t nwords = (int64_t)B * per_s;
+    const int64_t w0 = (int64_t)bi * LISTS_WPB;
+    // the words and prefixes do not depend on the offsets: loaded first
+    uint64_t word = 0ull;
+    int wp = 0;
+    if (t < LISTS_WPB && w0 + t < nwords) {
+      word = Lr.bits[w0 + t];
+      wp = Lr.wpre[w0 + t];
+    }
+    int tot_r = 0;
+    if constexpr (SCAN) {
+      if (lo) block_count_scan(a.L[r - 1].scount, B, offs, wsum);
+      tot_r = block_count_scan(Lr.scount, B, offs + B, wsum);
+      if (hi) block_count_scan(a.L[r + 1].scount, B, offs + 2 * B, wsum);
+    }
+    auto off_of = [&](int which, int b) -> int32_t {  // which: 0 layer r - 1, 1 layer r, 2 layer r + 1
+      if constexpr (SCAN)
+        return offs[which * B + b];
       else
-        window_rows<1>(Lo, Li, step, n_out, R, tid, stride, Lg, nullptr);
-    } else {  // transposes: for every row of layer s-1, the rows of layer s whose window holds it
-      const int n_in = a.counts[s - 1];
-      int32_t* Rt = a.rules_t[s];
-      if (a.kind[s] == 1) {
+        return a.L[r - 1 + which].soff[b];
+    };
+    // list this workgroup's sites (wave 0 holds the words)
+    const int c = __popcll(word);
+    int tot;
+    const int pre = wave_exclusive_scan(c, &tot);
+    if (t == 0) ntot = tot;
+    if (word) {
+      const int64_t g = w0 + t;
+      const int b = div_rcp_d(g, per_s);
+      const int rem = (int)(g - (int64_t)b * per_s);
+      const int y = div_rcp(rem, Lr.Wd, 1.f / (float)Lr.Wd);
+      wloc[t][0] = b;
+      wloc[t][1] = y;
+      wloc[t][2] = (rem - y * Lr.Wd) * 64;
+      int row = 1 + off_of(1, b) + wp;
+      int k = pre;
+      while (word) {
+        const int bit = __ffsll((long long)word) - 1;
+        word &= word - 1;
+        ent[k++] = make_int2(row++, t * 64 + bit);
+      }
+    }
+    __syncthreads();
+    const int total = ntot;
+    for (int i = t; i < total; i += blockDim.x) {
+      const int2 e = ent[i];
+      const int row = e.x, wt = e.y >> 6;
+      const int b = wloc[wt][0], y = wloc[wt][1], x = wloc[wt][2] + (e.y & 63);
+      Lr.sites[row - 1] = (b * Lr.S + y) * Lr.S + x;
+      if (lo) {
+        const LayerBits& Li = a.L[r - 1];
+        const int F = a.F[r], step = a.kind[r] == 1 ? 1 : 2;
+        const int32_t off = off_of(0, b);
+        int32_t* R = a.rules[r] + (int64_t)row * F * F;
         if (F == 3)
-          window_rows_t<3>(Lo, Li, n_in, Rt, tid, stride);
+          row_window<3>(Li, b, y, x, step, off, R);
         else if (F == 2)
-          window_rows_t<2>(Lo, Li, n_in, Rt, tid, stride);
+          row_window<2>(Li, b, y, x, step, off, R);
         else
-          window_rows_t<1>(Lo, Li, n_in, Rt, tid, stride);
-      } else {
-        for (int64_t i = tid; i <= n_in; i += stride) {
-          if (i == 0) {
-            Rt[0] = -1;
-            continue;
-          }
-          const SiteKey k = decode_key(Li.sites[i - 1], Li.S);
-          const int Y = k.y >> 1, X = k.x >> 1;
-          int r = -1;
-          if (Y < Lo.S && X < Lo.S) r = rank_row(Lo, k.b, Y, X) * 4 + (k.y & 1) * 2 + (k.x & 1);
-          Rt[i] = r;
+          row_window<1>(Li, b, y, x, step, off, R);
+        if (r >= 2 && a.gmask[r]) a.gmask[r][row] = child_ground_mask(a.L[r - 2], b, y, x);
+      }
+      if (hi) {
+        const LayerBits& Lo = a.L[r + 1];
+        const int32_t off = off_of(2, b);
+        if (a.kind[r + 1] == 1) {
+          const int F = a.F[r + 1];
+          int32_t* Rt = a.rules_t[r + 1] + (int64_t)row * F * F;
+          if (F == 3)
+            row_window_t<3>(Lo, b, y, x, off, Rt);
+          else if (F == 2)
+            row_window_t<2>(Lo, b, y, x, off, Rt);
+          else
+            row_window_t<1>(Lo, b, y, x, off, Rt);
+        } else {  // pooling above: the parent's row times 4 plus the position in its window
+          const int Y = y >> 1, X = x >> 1;
+          int32_t p = -1;
+          if (Y < Lo.S && X < Lo.S) p = rank_row(Lo, b, Y, X, off) * 4 + (y & 1) * 2 + (x & 1);
+          a.rules_t[r + 1][row] = p;
         }
       }
     }
+    if (bi == 0) {  // row 0 (the ground row) of every list this segment writes, and the layer's total
+      if (lo) {
+        const int A = a.F[r] * a.F[r];
+        if (t < A) a.rules[r][t] = 0;
+        if (t == 0 && r >= 2 && a.gmask[r]) a.gmask[r][0] = 0xFFFF;
+      }
+      if (hi) {
+        const int At = a.kind[r + 1] == 1 ? a.F[r + 1] * a.F[r + 1] : 1;
+        if (t < At) a.rules_t[r + 1][t] = -1;
+      }
+      if (SCAN && t == 0) a.counts[r] = tot_r;
+    }
   } else if (kind == 2) {  // caller site -> input row
     const LayerBits& L0 = a.L[0];
-    for (int64_t i = tid; i < a.n; i += stride) {
-      const int b = a.coords[3 * i], y = a.coords[3 * i + 1], x = a.coords[3 * i + 2];
-      int r = -1;
-      if (b >= 0 && b < a.batch && y >= 0 && y < L0.S && x >= 0 && x < L0.S) r = rank_row(L0, b, y, x);
-      a.perm[i] = r;
+    const int64_t i = (int64_t)bi * blockDim.x + t;
+    int b = -1, y = 0, x = 0;
+    if (i < a.n) {
+      b = a.coords[3 * i];
+      y = a.coords[3 * i + 1];
+      x = a.coords[3 * i + 2];
+    }
+    if constexpr (SCAN) block_count_scan(L0.scount, B, offs, wsum);
+    if (i < a.n) {
+      int32_t p = -1;
+      if (b >= 0 && b < B && y >= 0 && y < L0.S && x >= 0 && x < L0.S)
+        p = rank_row(L0, b, y, x, SCAN ? offs[b] : L0.soff[b]);
+      a.perm[i] = p;
     }
   } else {  // each sample's single top-layer site (row 0 when the sample is empty)
     const LayerBits& Lt = a.L[a.nlayers - 1];
-    for (int64_t b = tid; b < a.batch; b += stride) a.head_rows[b] = rank_row(Lt, (int)b, 0, 0);
+    if constexpr (SCAN) block_count_scan(Lt.scount, B, offs, wsum);
+    const int64_t b = (int64_t)bi * blockDim.x + t;
+    if (b < B) a.head_rows[b] = rank_row(Lt, (int)b, 0, 0, SCAN ? offs[b] : Lt.soff[b]);
   }
 }
 
-hipError_t launch_rulebook(const RulebookArgs& a, const SitesWork& wk, const RulesWork& rw, int32_t max_words,
-                           hipStream_t st) {
+hipError_t launch_rulebook(const RulebookArgs& a, const ListsWork& lw, int32_t max_words, hipStream_t st) {
   const LayerBits& L0 = a.L[0];
   if (a.n > 0)
     hipLaunchKernelGGL(k_rb_insert, dim3((a.n + 255) / 256), dim3(256), 0, st, a.coords, a.n, a.batch, L0.S, L0.Wd,
                        L0.bits, a.err);
   const size_t lds = (size_t)(2 * max_words + 64 * L0.Wd) * sizeof(uint64_t);
   hipLaunchKernelGGL(k_rb_bitmaps, dim3(std::max(a.batch, 1) * a.nlayers), dim3(64), lds, st, a, max_words);
-  int gs = (int)std::min<int64_t>((wk.total + 255) / 256, 2048);
-  if (gs < 1) gs = 1;
-  // the in-kernel scan repeats per chunk of 256 words: only while each
-  // workgroup has at most two chunks
-  const bool scan = a.batch >= 1 && a.batch <= SITES_SCAN_MAX && wk.total <= (int64_t)gs * 256 * 2;
-  if (!scan) hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
-  if (scan)
-    hipLaunchKernelGGL(k_rb_sites<true>, dim3(gs), dim3(256), 0, st, a, wk);
-  else
-    hipLaunchKernelGGL(k_rb_sites<false>, dim3(gs), dim3(256), 0, st, a, wk);
-  hipLaunchKernelGGL(k_rb_rules, dim3(rw.blk[rw.nseg]), dim3(256), 0, st, a, rw);
+  const bool scan = a.batch >= 1 && a.batch <= LISTS_SCAN_MAX;
+  if (scan) {
+    hipLaunchKernelGGL(k_rb_lists<true>, dim3(lw.blk[lw.nseg]), dim3(256), (size_t)3 * a.batch * sizeof(int32_t), st, a,
+                       lw);
+  } else {
+    hipLaunchKernelGGL(k_rb_offsets, dim3(a.nlayers), dim3(64), 0, st, a);
+    hipLaunchKernelGGL(k_rb_lists<false>, dim3(lw.blk[lw.nseg]), dim3(256), 0, st, a, lw);
+  }
   return hipGetLastError();
 }
 
