@@ -163,20 +163,45 @@ __global__ void __launch_bounds__(64) k_rb_bitmaps(RulebookArgs a, int32_t max_w
   const int Wo = Lo.Wd, So = Lo.S, nwo = So * Wo;
   const int ra = a.rf_a[s], rr = a.rf_r[s];
   uint64_t* row = rowbuf + t * W0;
-  for (int Y = t; Y < So; Y += 64) {
-    const int y_end = min(ra * Y + rr, S0);
+  // P lanes per output row (a power of two, P * So <= 64 when So < 64): the
+  // deep layers have few rows, each the OR of many input rows, which the P
+  // lanes split and combine by shuffles
+  const int P = So >= 64 ? 1 : 1 << (31 - __clz(64 / So));
+  for (int Y0 = 0; Y0 < So; Y0 += 64 / P) {  // uniform over the wave
+    const int Y = Y0 + t / P, sub = t % P;
+    const bool live = Y < So;
+    const int y_end = live ? min(ra * Y + rr, S0) : 0;
     for (int w = 0; w < W0; ++w) {  // OR of the square's input rows
       uint64_t v = 0;
 #pragma unroll 4
-      for (int y = ra * Y; y < y_end; ++y) v |= in[y * W0 + w];
+      for (int y = ra * Y + sub; y < y_end; y += P) v |= in[y * W0 + w];
+      for (int m = 1; m < P; m <<= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)v, m, 64), hi = __shfl_xor((uint32_t)(v >> 32), m, 64);
+        v |= ((uint64_t)hi << 32) | lo;
+      }
       row[w] = v;
     }
+    if (!live || sub) continue;
     if (ra == 1) {  // output bit X covers input bits X .. X + rr - 1
       for (int w = 0; w < Wo; ++w) {
         const uint64_t lo = row[w], hi = w + 1 < W0 ? row[w + 1] : 0ull;
         uint64_t acc = lo;
         for (int d = 1; d < rr; ++d) acc |= (lo >> d) | (hi << (64 - d));
         out[Y * Wo + w] = acc & row_mask_word(w, So);
+      }
+    } else if (W0 <= 2 && rr <= 64) {  // the input row in registers: bit X = any of bits [a X, a X + rr)
+      const uint64_t r0 = row[0], r1 = W0 > 1 ? row[1] : 0ull;
+      const uint64_t lmask = rr == 64 ? ~0ull : (1ull << rr) - 1ull;
+      for (int w = 0; w < Wo; ++w) {
+        uint64_t acc = 0;
+        const int x_end = min(So, (w + 1) * 64);
+#pragma unroll 4
+        for (int x = w * 64; x < x_end; ++x) {
+          const int lo = ra * x;  // < S0 <= 128; bits past S0 are zero
+          const uint64_t v = lo < 64 ? (r0 >> lo) | (lo ? r1 << (64 - lo) : 0ull) : r1 >> (lo - 64);
+          acc |= ((v & lmask) ? 1ull : 0ull) << (x - w * 64);
+        }
+        out[Y * Wo + w] = acc;
       }
     } else {  // output bit X covers input bits [a X, a X + rr)
       for (int w = 0; w < Wo; ++w) {
@@ -229,32 +254,42 @@ __global__ void __launch_bounds__(64) k_rb_offsets(RulebookArgs a) {
 // window-list kernel (no separate offsets launch).
 constexpr int LISTS_SCAN_MAX = 1024;
 
-// Exclusive prefix of scount[0, batch) into the LDS array off, by one
-// workgroup of 256 threads (batch <= LISTS_SCAN_MAX); returns the total.  All
-// threads call it; it synchronises before returning.
-__device__ inline int block_count_scan(const int32_t* scount, int batch, int* off, int* wsum) {
+// Exclusive prefixes of up to three count arrays sc[k][0, batch) (null: not
+// scanned) into the LDS arrays off + k * batch, by one workgroup of 256
+// threads (batch <= LISTS_SCAN_MAX): every count is loaded before the first
+// is used.  Returns the total of sc[1] (or of sc[0] when nk == 1).  All threads
+// call it; it synchronises before returning.
+__device__ inline int block_count_scan(const int32_t* const (&sc)[3], int nk, int batch, int* off, int (*wsum)[4]) {
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int per = (batch + 255) / 256;  // <= 4
   const int beg = min(batch, t * per), end = min(batch, beg + per);
-  int c[4];
-  int local = 0;
+  int c[3][4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    c[u] = beg + u < end ? scount[beg + u] : 0;
-    local += c[u];
+  for (int k = 0; k < 3; ++k)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) c[k][u] = k < nk && sc[k] && beg + u < end ? sc[k][beg + u] : 0;
+  int run[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const int local = (c[k][0] + c[k][1]) + (c[k][2] + c[k][3]);
+    int wt;
+    run[k] = wave_exclusive_scan(local, &wt);
+    if (lane == 0) wsum[k][wv] = wt;
   }
-  int wt;
-  int run = wave_exclusive_scan(local, &wt);
-  if (lane == 0) wsum[wv] = wt;
   __syncthreads();
-  for (int q = 0; q < wv; ++q) run += wsum[q];
-  const int total = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
-    if (beg + u < end) {
-      off[beg + u] = run;
-      run += c[u];
-    }
+  for (int k = 0; k < 3; ++k) {
+    if (k >= nk || !sc[k]) continue;
+    for (int q = 0; q < wv; ++q) run[k] += wsum[k][q];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (beg + u < end) {
+        off[k * batch + beg + u] = run[k];
+        run[k] += c[k][u];
+      }
+  }
+  const int kt = nk == 1 ? 0 : 1;
+  const int total = (wsum[kt][0] + wsum[kt][1]) + (wsum[kt][2] + wsum[kt][3]);
   __syncthreads();
   return total;
 }
@@ -365,9 +400,10 @@ __device__ inline void row_window_t(const LayerBits& Lo, int b, int y, int x, in
 
 // Rows of every layer, their window lists and transposes, the caller-site ->
 // row map and the head rows, in one launch.  Segment kind 0 (one per layer
-// r): each workgroup takes LISTS_WPB consecutive bitmap words of layer r; the
-// words' sites are listed in LDS in row order (row = 1 + sample offset + word
-// prefix + rank in the word), then every thread takes listed sites one after
+// r): each workgroup takes LISTS_WPB consecutive bitmap words of layer r,
+// eight threads per word, one byte each; the words' sites are listed in LDS
+// in row order (row = 1 + sample offset + word prefix + rank in the word, a
+// block scan over the threads' bytes), then every thread takes listed sites one after
 // another and writes, for its site, the key (sites), R_r and the child ground
 // mask (r >= 1), and the row's entries of Rt_{r+1} (r + 1 < nlayers).  Kind 2:
 // caller site -> input row; kind 3: each sample's top-layer row.  SCAN: every
@@ -377,10 +413,11 @@ __device__ inline void row_window_t(const LayerBits& Lo, int b, int y, int x, in
 
 template <bool SCAN>
 __global__ void __launch_bounds__(256) k_rb_lists(RulebookArgs a, ListsWork lw) {
+  static_assert(LISTS_WPB * 8 == 256, "eight threads per bitmap word");
   extern __shared__ int32_t offs[];  // SCAN: [3][batch], layers r - 1, r, r + 1
   __shared__ int2 ent[LISTS_WPB * 64];
   __shared__ int wloc[LISTS_WPB][3];
-  __shared__ int wsum[4];
+  __shared__ int wsum[3][4];
   __shared__ int ntot;
   int seg = 0;
   while (seg + 1 < lw.nseg && (int)blockIdx.x >= lw.blk[seg + 1]) ++seg;
@@ -394,18 +431,19 @@ __global__ void __launch_bounds__(256) k_rb_lists(RulebookArgs a, ListsWork lw) 
     const int per_s = Lr.S * Lr.Wd;  // words per sample (< 2^20)
     const int64_t nwords = (int64_t)B * per_s;
     const int64_t w0 = (int64_t)bi * LISTS_WPB;
-    // the words and prefixes do not depend on the offsets: loaded first
+    // the words and prefixes do not depend on the offsets: loaded first.
+    // Thread t takes bits 8 (t % 8) .. + 7 of word t / 8.
+    const int wi = t >> 3, part = t & 7;
     uint64_t word = 0ull;
     int wp = 0;
-    if (t < LISTS_WPB && w0 + t < nwords) {
-      word = Lr.bits[w0 + t];
-      wp = Lr.wpre[w0 + t];
+    if (w0 + wi < nwords) {
+      word = Lr.bits[w0 + wi];
+      wp = Lr.wpre[w0 + wi];
     }
     int tot_r = 0;
     if constexpr (SCAN) {
-      if (lo) block_count_scan(a.L[r - 1].scount, B, offs, wsum);
-      tot_r = block_count_scan(Lr.scount, B, offs + B, wsum);
-      if (hi) block_count_scan(a.L[r + 1].scount, B, offs + 2 * B, wsum);
+      const int32_t* const sc[3] = {lo ? a.L[r - 1].scount : nullptr, Lr.scount, hi ? a.L[r + 1].scount : nullptr};
+      tot_r = block_count_scan(sc, 3, B, offs, wsum);
     }
     auto off_of = [&](int which, int b) -> int32_t {  // which: 0 layer r - 1, 1 layer r, 2 layer r + 1
       if constexpr (SCAN)
@@ -413,25 +451,32 @@ __global__ void __launch_bounds__(256) k_rb_lists(RulebookArgs a, ListsWork lw) 
       else
         return a.L[r - 1 + which].soff[b];
     };
-    // list this workgroup's sites (wave 0 holds the words)
-    const int c = __popcll(word);
-    int tot;
-    const int pre = wave_exclusive_scan(c, &tot);
-    if (t == 0) ntot = tot;
+    // list this workgroup's sites in row order: thread t's bits follow those
+    // of threads < t (a block scan of the per-thread counts)
+    const uint32_t mine = (uint32_t)(word >> (8 * part)) & 0xffu;
+    int tw;
+    int pre = wave_exclusive_scan(__popc(mine), &tw);
+    if ((t & 63) == 0) wsum[0][t >> 6] = tw;
+    __syncthreads();
+    for (int q = 0; q < (t >> 6); ++q) pre += wsum[0][q];
+    if (t == 0) ntot = (wsum[0][0] + wsum[0][1]) + (wsum[0][2] + wsum[0][3]);
     if (word) {
-      const int64_t g = w0 + t;
+      const int64_t g = w0 + wi;
       const int b = div_rcp_d(g, per_s);
-      const int rem = (int)(g - (int64_t)b * per_s);
-      const int y = div_rcp(rem, Lr.Wd, 1.f / (float)Lr.Wd);
-      wloc[t][0] = b;
-      wloc[t][1] = y;
-      wloc[t][2] = (rem - y * Lr.Wd) * 64;
-      int row = 1 + off_of(1, b) + wp;
+      if (part == 0) {
+        const int rem = (int)(g - (int64_t)b * per_s);
+        const int y = div_rcp(rem, Lr.Wd, 1.f / (float)Lr.Wd);
+        wloc[wi][0] = b;
+        wloc[wi][1] = y;
+        wloc[wi][2] = (rem - y * Lr.Wd) * 64;
+      }
+      int row = 1 + off_of(1, b) + wp + __popcll(word & ((1ull << (8 * part)) - 1ull));
       int k = pre;
-      while (word) {
-        const int bit = __ffsll((long long)word) - 1;
-        word &= word - 1;
-        ent[k++] = make_int2(row++, t * 64 + bit);
+      uint32_t m = mine;
+      while (m) {
+        const int bit = __ffs(m) - 1;
+        m &= m - 1;
+        ent[k++] = make_int2(row++, wi * 64 + 8 * part + bit);
       }
     }
     __syncthreads();
@@ -495,7 +540,10 @@ __global__ void __launch_bounds__(256) k_rb_lists(RulebookArgs a, ListsWork lw) 
       y = a.coords[3 * i + 1];
       x = a.coords[3 * i + 2];
     }
-    if constexpr (SCAN) block_count_scan(L0.scount, B, offs, wsum);
+    if constexpr (SCAN) {
+      const int32_t* const sc[3] = {L0.scount, nullptr, nullptr};
+      block_count_scan(sc, 1, B, offs, wsum);
+    }
     if (i < a.n) {
       int32_t p = -1;
       if (b >= 0 && b < B && y >= 0 && y < L0.S && x >= 0 && x < L0.S)
@@ -504,7 +552,10 @@ __global__ void __launch_bounds__(256) k_rb_lists(RulebookArgs a, ListsWork lw) 
     }
   } else {  // each sample's single top-layer site (row 0 when the sample is empty)
     const LayerBits& Lt = a.L[a.nlayers - 1];
-    if constexpr (SCAN) block_count_scan(Lt.scount, B, offs, wsum);
+    if constexpr (SCAN) {
+      const int32_t* const sc[3] = {Lt.scount, nullptr, nullptr};
+      block_count_scan(sc, 1, B, offs, wsum);
+    }
     const int64_t b = (int64_t)bi * blockDim.x + t;
     if (b < B) a.head_rows[b] = rank_row(Lt, (int)b, 0, 0, SCAN ? offs[b] : Lt.soff[b]);
   }
