@@ -166,7 +166,7 @@ def decode_tag(tag):
 def group_key(kc, t):
     """A kernel instantiation: class, role, tile plan and fused epilogue."""
     if kc == "conv_narrow":
-        return "k_conv_narrow (first layer, vector ALUs, pooling forward fused)"
+        return "k_conv_narrow (first layer, pooling forward fused; bf16 on the matrix cores, f32 on the vector ALUs)"
     if kc == "wgrad":
         return "k_wgrad (all weight gradients, grouped)"
     name = PLAN_NAMES.get(t["plan"], f"plan {t['plan']}")
