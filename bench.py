@@ -321,29 +321,34 @@ def measure(cfg, dtype, steps, warmup, nbatches, cpu=True):
     else:
         batches = make_batches(cfg, nbatches)
         for b in batches:
+            # sites listed sample by sample (as the stroke and picture generators emit them): the
+            # grouped rulebook build, given the per-sample offsets
+            grouped = len(b.coords) == 0 or bool(np.all(np.diff(b.coords[:, 0]) >= 0))
+            sb = (torch.tensor(np.searchsorted(b.coords[:, 0], np.arange(cfg.batch + 1)), dtype=torch.int32,
+                               device=dev).contiguous() if grouped else None)
             inputs.append((torch.tensor(b.coords, dtype=torch.int32, device=dev).contiguous(),
-                           torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous()))
+                           torch.tensor(b.feats, dtype=torch.float32).to(tdt).to(dev).contiguous(), sb))
         max_active = max(b.n for b in batches)
     net = SparseDeepCNet(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, batch_max=cfg.batch, max_active=max_active,
                          dtype=dtype, arch=cfg.arch, dropout=bool(cfg.dropout))
 
     def inputs_of(i):
-        if paths:
-            return enc.encode(*raw[i % len(raw)], cfg.batch)  # synchronises: the site count goes to the host
+        if paths:  # synchronises: the site count goes to the host
+            return (*enc.encode(*raw[i % len(raw)], cfg.batch), None)
         return inputs[i % len(inputs)]
 
     sizes = []
     for i in range(len(raw) if paths else len(inputs)):
-        c, _ = inputs_of(i)
-        net.rulebook_build(c, cfg.batch)
+        c, _, sb = inputs_of(i)
+        net.rulebook_build(c, cfg.batch, sample_begin=sb)
         sizes.append(net.layer_sizes())
     torch.cuda.synchronize()
 
     infer = cfg.mode == "infer"
 
     def step(i):
-        c, f = inputs_of(i)
-        net.rulebook_build(c, cfg.batch)
+        c, f, sb = inputs_of(i)
+        net.rulebook_build(c, cfg.batch, sample_begin=sb)
         if infer:
             net.forward(f, Ws_d, bs_d, None)
         else:

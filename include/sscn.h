@@ -157,6 +157,22 @@ SSCN_API sscn_status sscn_net_workspace_bytes(const sscn_net* net, size_t* bytes
 SSCN_API sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t n, int32_t batch,
                                 void* d_workspace, size_t workspace_bytes, void* stream);
 
+/* sscn_rulebook_build for sites grouped by sample (Section 2.3 builds each
+ * sample's pointer matrices from that sample's input alone): d_sample_begin
+ * is a device array of batch + 1 int32, non-decreasing, d_sample_begin[0] = 0,
+ * d_sample_begin[batch] = n, and sample b's sites are rows
+ * d_sample_begin[b] .. d_sample_begin[b + 1] - 1 of d_coords, each with b in
+ * its first column (any order within the sample).  The result is the same as
+ * sscn_rulebook_build's on the same sites; the bitmap pass inserts each
+ * sample's sites itself, so no insertion launch precedes it.  A site outside
+ * its sample's range or the grid, inconsistent offsets (read with every
+ * index clamped to 0 .. n) and duplicate sites are device-side input errors
+ * (SSCN_ERR_OUT_OF_RANGE, SSCN_ERR_DUPLICATE_SITE from sscn_layer_sizes);
+ * argument errors as for sscn_rulebook_build, and d_sample_begin null. */
+SSCN_API sscn_status sscn_rulebook_build_grouped(sscn_net* net, const int32_t* d_coords, const int32_t* d_sample_begin,
+                                                 int32_t n, int32_t batch, void* d_workspace, size_t workspace_bytes,
+                                                 void* stream);
+
 /* Synchronises `stream`, copies the L + 1 active-site counts (layer 0 =
  * input, then each stage) to h_counts, and returns any latched input error
  * (SSCN_ERR_OUT_OF_RANGE / SSCN_ERR_DUPLICATE_SITE).  It also returns

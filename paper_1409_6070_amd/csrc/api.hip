@@ -499,8 +499,8 @@ sscn_status sscn_net_workspace_bytes(const sscn_net* net, size_t* bytes) {
   return SSCN_OK;
 }
 
-sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t n, int32_t batch, void* d_ws,
-                                size_t ws_bytes, void* stream) {
+static sscn_status rulebook_build(sscn_net* net, const int32_t* d_coords, const int32_t* d_sample_begin, int32_t n,
+                                  int32_t batch, void* d_ws, size_t ws_bytes, void* stream) {
   if (!net || n < 0 || batch < 0) return SSCN_ERR_INVALID_ARGUMENT;
   if (n > 0 && !d_coords) return SSCN_ERR_INVALID_ARGUMENT;
   if (n > net->d.max_active || batch > net->d.batch_max) return SSCN_ERR_CAPACITY;
@@ -556,6 +556,7 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   a.head_rows = net->head_rows;
   a.coords = d_coords;
   a.n = n;
+  a.sample_begin = batch > 0 ? d_sample_begin : nullptr;
   // window-list segments: LISTS_WPB bitmap words of a layer per workgroup (one
   // workgroup for an empty batch, which writes the ground rows), 256 caller
   // sites or samples per workgroup
@@ -576,6 +577,17 @@ sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t 
   net->rb_parity = 1 - par;
   net->built = true;
   return SSCN_OK;
+}
+
+sscn_status sscn_rulebook_build(sscn_net* net, const int32_t* d_coords, int32_t n, int32_t batch, void* d_ws,
+                                size_t ws_bytes, void* stream) {
+  return rulebook_build(net, d_coords, nullptr, n, batch, d_ws, ws_bytes, stream);
+}
+
+sscn_status sscn_rulebook_build_grouped(sscn_net* net, const int32_t* d_coords, const int32_t* d_sample_begin, int32_t n,
+                                        int32_t batch, void* d_ws, size_t ws_bytes, void* stream) {
+  if (!d_sample_begin) return SSCN_ERR_INVALID_ARGUMENT;
+  return rulebook_build(net, d_coords, d_sample_begin, n, batch, d_ws, ws_bytes, stream);
 }
 
 sscn_status sscn_layer_sizes(sscn_net* net, int32_t* h_counts, void* stream) {

@@ -146,6 +146,7 @@ struct RulebookArgs {
   int32_t* head_rows;            // [batch]
   const int32_t* coords;         // [n][3]
   int32_t n;
+  const int32_t* sample_begin;   // [batch + 1] when the sites are grouped by sample (no insertion launch), else null
 };
 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }

@@ -121,8 +121,45 @@ __device__ inline int div_rcp_d(int64_t k, int d) {
   return (int)q;
 }
 
+// Sites beg .. end - 1 of sample b into the sample's LDS bitmap `in` ([S0][W0]
+// words) by atomic ORs, sixteen sites per lane in flight; returns the error
+// bits (a site of another sample or off the grid; with DUP a site set twice).
+template <bool DUP>
+__device__ inline int insert_sample(const int32_t* coords, int beg, int end, int b, int S0, int W0, uint64_t* in) {
+  constexpr int SPL = 16;
+  int err = 0;
+  for (int i0 = beg + (int)threadIdx.x; i0 < end; i0 += SPL * 64) {
+    int cb[SPL], cy[SPL], cx[SPL];
+#pragma unroll
+    for (int u = 0; u < SPL; ++u) {
+      const int64_t i = i0 + 64 * u < end ? i0 + 64 * u : beg;
+      cb[u] = coords[3 * i];
+      cy[u] = coords[3 * i + 1];
+      cx[u] = coords[3 * i + 2];
+    }
+#pragma unroll
+    for (int u = 0; u < SPL; ++u) {
+      if (i0 + 64 * u >= end) break;
+      if (cb[u] != b || cy[u] < 0 || cy[u] >= S0 || cx[u] < 0 || cx[u] >= S0) {
+        err |= ERRBIT_RANGE;
+        continue;
+      }
+      const unsigned long long bit = 1ull << (cx[u] & 63);
+      unsigned long long* w = (unsigned long long*)&in[cy[u] * W0 + (cx[u] >> 6)];
+      if constexpr (DUP) {
+        if (atomicOr(w, bit) & bit) err |= ERRBIT_DUP;
+      } else {
+        __hip_atomic_fetch_or(w, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
+  }
+  return err;
+}
+
 // Layer s of sample b, b = blockIdx / nlayers, s = blockIdx % nlayers (one
-// wave): the sample's input bitmap goes to LDS; each lane takes whole output
+// wave): the sample's input bitmap goes to LDS (read from the inserted bitmap,
+// or, with the sites grouped by sample, built here from the sample's own
+// sites by LDS atomic ORs, the input layer's wave storing it); each lane takes whole output
 // rows, ORs the input rows of their squares into its own row buffer, and sets
 // each output bit whose column range of that row holds a set bit (a word-
 // parallel dilation when a = 1).  Then the layer's word prefix and count, as
@@ -144,16 +181,42 @@ __global__ void __launch_bounds__(64) k_rb_bitmaps(RulebookArgs a, int32_t max_w
     if (blockIdx.x == 0 && t == 0) *a.err_next = 0;
   }
   if (b >= a.batch) return;
-  const uint64_t* src = L0.bits + (int64_t)b * nw0;
-  for (int w0 = t; w0 < nw0; w0 += 4 * 64) {  // four words per lane in flight
-    uint64_t v[4];
+  if (a.sample_begin) {
+    // sites grouped by sample: this wave inserts sample b's sites into its own
+    // LDS bitmap (every wave of the sample does; the input layer's reports
+    // the errors and stores the bitmap for the window lists)
+    for (int w = t; w < nw0; w += 64) in[w] = 0ull;
+    __syncthreads();
+    const int n = a.n;
+    int beg = a.sample_begin[b], end = a.sample_begin[b + 1];
+    const bool bad = beg < 0 || end < beg || end > n || (b == 0 && beg != 0) || (b == a.batch - 1 && end != n);
+    beg = min(max(beg, 0), n);
+    end = min(max(end, beg), n);
+    int err;
+    // the input layer's wave looks for duplicates in the values its ORs return;
+    // the others need no returned value
+    if (s == 0)
+      err = insert_sample<true>(a.coords, beg, end, b, S0, W0, in);
+    else
+      err = insert_sample<false>(a.coords, beg, end, b, S0, W0, in);
+    if (s == 0 && (err || (bad && t == 0))) atomicOr(a.err, err | (bad ? ERRBIT_RANGE : 0));
+    __syncthreads();
+    if (s == 0) {
+      uint64_t* dst = L0.bits + (int64_t)b * nw0;
+      for (int w = t; w < nw0; w += 64) dst[w] = in[w];
+    }
+  } else {
+    const uint64_t* src = L0.bits + (int64_t)b * nw0;
+    for (int w0 = t; w0 < nw0; w0 += 4 * 64) {  // four words per lane in flight
+      uint64_t v[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = src[min(w0 + u * 64, nw0 - 1)];
+      for (int u = 0; u < 4; ++u) v[u] = src[min(w0 + u * 64, nw0 - 1)];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (w0 + u * 64 < nw0) in[w0 + u * 64] = v[u];
+      for (int u = 0; u < 4; ++u)
+        if (w0 + u * 64 < nw0) in[w0 + u * 64] = v[u];
+    }
+    __syncthreads();
   }
-  __syncthreads();
   if (s == 0) {  // the input layer: its prefix and count only
     const int tot = wave_popcount_scan(in, nw0, L0.wpre + (int64_t)b * nw0);
     if (t == 0) L0.scount[b] = tot;
@@ -563,7 +626,7 @@ __global__ void __launch_bounds__(256) k_rb_lists(RulebookArgs a, ListsWork lw) 
 
 hipError_t launch_rulebook(const RulebookArgs& a, const ListsWork& lw, int32_t max_words, hipStream_t st) {
   const LayerBits& L0 = a.L[0];
-  if (a.n > 0)
+  if (a.n > 0 && !a.sample_begin)  // grouped sites: the bitmap kernel inserts them
     hipLaunchKernelGGL(k_rb_insert, dim3((a.n + 255) / 256), dim3(256), 0, st, a.coords, a.n, a.batch, L0.S, L0.Wd,
                        L0.bits, a.err);
   const size_t lds = (size_t)(2 * max_words + 64 * L0.Wd) * sizeof(uint64_t);

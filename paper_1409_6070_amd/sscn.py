@@ -31,7 +31,7 @@ STATUS = {
 }
 EXPORTED = [
     "sscn_net_create", "sscn_net_destroy", "sscn_status_string", "sscn_net_num_params", "sscn_net_param_shape",
-    "sscn_net_workspace_bytes", "sscn_rulebook_build", "sscn_layer_sizes", "sscn_forward", "sscn_backward",
+    "sscn_net_workspace_bytes", "sscn_rulebook_build", "sscn_rulebook_build_grouped", "sscn_layer_sizes", "sscn_forward", "sscn_backward",
     "sscn_forward_stage", "sscn_backward_stage", "sscn_layer_view_get", "sscn_timing_enable", "sscn_timing_collect",
     "sscn_timing_launches",
     "sscn_set_dropout", "sscn_philox4x32_10", "sscn_sgd_step", "sscn_encode_workspace_bytes", "sscn_encode_strokes",
@@ -83,6 +83,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sscn_net_param_shape": (I32, [VP, I32, P(ctypes.c_int64), P(ctypes.c_int64)]),
         "sscn_net_workspace_bytes": (I32, [VP, P(SZ)]),
         "sscn_rulebook_build": (I32, [VP, VP, I32, I32, VP, SZ, VP]),
+        "sscn_rulebook_build_grouped": (I32, [VP, VP, VP, I32, I32, VP, SZ, VP]),
         "sscn_layer_sizes": (I32, [VP, P(I32), VP]),
         "sscn_forward": (I32, [VP, VP, P(VP), P(VP), VP, VP, VP, VP]),
         "sscn_backward": (I32, [VP, P(VP), P(VP), VP, VP]),
@@ -153,6 +154,12 @@ def sscn_net_workspace_bytes(net: int) -> int:
 
 def sscn_rulebook_build(net: int, d_coords: int, n: int, batch: int, d_ws: int, ws_bytes: int, stream: int) -> None:
     _check(load_library().sscn_rulebook_build(net, d_coords, n, batch, d_ws, ws_bytes, stream), "sscn_rulebook_build")
+
+
+def sscn_rulebook_build_grouped(net: int, d_coords: int, d_sample_begin: int, n: int, batch: int, d_ws: int,
+                                ws_bytes: int, stream: int) -> None:
+    _check(load_library().sscn_rulebook_build_grouped(net, d_coords, d_sample_begin, n, batch, d_ws, ws_bytes, stream),
+           "sscn_rulebook_build_grouped")
 
 
 def sscn_layer_sizes(net: int, nlayers: int, stream: int) -> List[int]:
@@ -308,13 +315,22 @@ class SparseDeepCNet:
             self.handle = None
 
     # -- calls ---------------------------------------------------------------
-    def rulebook_build(self, coords: torch.Tensor, batch: int) -> None:
+    def rulebook_build(self, coords: torch.Tensor, batch: int, sample_begin: Optional[torch.Tensor] = None) -> None:
+        """coords [n][3] int32 (b, y, x); with sample_begin (int32 [batch + 1] on the device) the sites are
+        grouped by sample and the grouped build is used."""
         assert coords.dtype == torch.int32 and coords.is_contiguous() and coords.device.type == "cuda"
         self.batch = batch
         self.n = int(coords.shape[0])
         self._coords = coords
-        sscn_rulebook_build(self.handle, coords.data_ptr() if self.n else None, self.n, batch, self.ws.data_ptr(),
-                            self.ws_bytes, _stream())
+        if sample_begin is None:
+            sscn_rulebook_build(self.handle, coords.data_ptr() if self.n else None, self.n, batch, self.ws.data_ptr(),
+                                self.ws_bytes, _stream())
+        else:
+            assert sample_begin.dtype == torch.int32 and sample_begin.is_contiguous()
+            assert sample_begin.device.type == "cuda" and int(sample_begin.numel()) == batch + 1
+            self._sample_begin = sample_begin
+            sscn_rulebook_build_grouped(self.handle, coords.data_ptr() if self.n else None, sample_begin.data_ptr(),
+                                        self.n, batch, self.ws.data_ptr(), self.ws_bytes, _stream())
 
     def set_dropout(self, rates: Optional[Sequence[float]], seed: int = 0) -> None:
         """Dropout rates per level (ell + 2: each convolution that is not 1x1, then the softmax

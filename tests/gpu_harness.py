@@ -151,9 +151,14 @@ class Pair:
                            [b.double().numpy() for b in bs_t], labels)
             self.o.backward()
 
-    def run_gpu(self):
+    def run_gpu(self, sample_begin=None):
+        """sample_begin (batch + 1 offsets, the sites grouped by sample): the grouped rulebook build."""
         net = self.net
-        net.rulebook_build(self.coords_d, self.batch)
+        if sample_begin is None:
+            net.rulebook_build(self.coords_d, self.batch)
+        else:
+            sb = torch.tensor(np.asarray(sample_begin, dtype=np.int32)).cuda().contiguous()
+            net.rulebook_build(self.coords_d, self.batch, sample_begin=sb)
         self.counts = net.layer_sizes()
         logits, loss = net.forward(self.feats_d, self.Ws_d, self.bs_d, self.labels_d)
         dW, db, dfeats = net.backward(want_dfeats=self.want_dfeats)

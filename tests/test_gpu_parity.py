@@ -203,8 +203,8 @@ def test_first_layer_kernel_choice(c_in, narrow, dtype):
 
 @pytest.mark.parametrize("batch", [1, 1024, 1100])
 def test_rulebook_batch_sizes_around_offset_scan(batch):
-    """Up to 1024 samples the sites kernel scans the per-sample counts itself; above, a separate
-    offsets launch does. Both must give the oracle's rows, windows and values."""
+    """Up to 1024 samples the window-list kernel scans the per-sample counts itself; above, a
+    separate offsets launch does. Both must give the oracle's rows, windows and values."""
     coords, feats = _sparse_case(60 + batch % 7, 1, batch, 0.3, 1)
     log(f"[batch-scan] batch={batch} n={len(coords)}")
     Ws, bs = he_params(1, 3, 1, 4, 160)

@@ -80,6 +80,10 @@ def test_host_checked_errors_need_no_gpu():
         assert lib.sscn_rulebook_build(h, fake, 10, 4, fake, ws - 1, None) == 7  # too small
         assert lib.sscn_rulebook_build(h, fake + 8, 10, 4, fake + 8, ws, None) == 7  # misaligned
         assert lib.sscn_rulebook_build(h, None, 10, 4, fake, ws, None) == 1  # null coords
+        assert lib.sscn_rulebook_build_grouped(h, fake, None, 10, 4, fake, ws, None) == 1  # null sample offsets
+        assert lib.sscn_rulebook_build_grouped(h, None, fake, 10, 4, fake, ws, None) == 1  # null coords
+        assert lib.sscn_rulebook_build_grouped(h, fake, fake, 101, 4, fake, ws, None) == 4  # n > max_active
+        assert lib.sscn_rulebook_build_grouped(h, fake, fake, 10, 4, fake, ws - 1, None) == 7  # too small
         arr = (ctypes.c_int32 * 8)()
         assert lib.sscn_layer_sizes(h, arr, None) == 5  # before any build
         ptrs = (ctypes.c_void_p * 5)(*([fake] * 5))
