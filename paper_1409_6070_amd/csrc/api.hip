@@ -1000,7 +1000,7 @@ sscn_status sscn_forward(sscn_net* net, const void* d_feats, const void* const* 
   PackArgs pa;
   std::memset(&pa, 0, sizeof(pa));
   pa.sc = ScatterArgs{d_feats, net->n, net->d.c_in, net->perm, L0.X, L0.Cp, 0};
-  for (int p = 0; p < net->nparams; ++p) {
+  for (int p = net->nparams - 1; p >= 0; --p) {  // the largest (softmax layer) first: its tiles find their job at once
     const ParamPlan& P = net->P[p];
     pa.job[pa.njobs++] = PackJob{h_W[p], P.WpF, 0, P.A, P.c_in, P.c_out, P.cp_in, P.cp_out, P.NpadF, P.KpadF};
     if (train)  // the input-gradient layout is only read by the backward pass

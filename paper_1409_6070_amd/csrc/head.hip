@@ -77,6 +77,7 @@ __global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
     const int tiles_k = j.Kpad / PACK_K;
     const int t = g - pa.tile_beg[ji];
     const int n0 = (t / tiles_k) * PACK_N, k0 = (t % tiles_k) * PACK_K;
+    const float rcp_in = 1.f / (float)j.cp_in, rcp_out = 1.f / (float)j.cp_out;
     // every thread moves PACK_K * PACK_N / 256 elements; their loads are issued
     // together (clamped index, selected value), then stored
     constexpr int PER = PACK_K * PACK_N / 256;
@@ -87,7 +88,10 @@ __global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
         const int i = (int)threadIdx.x + u * 256;
         const int kk = i / PACK_N, nn = i % PACK_N;
         const int k = k0 + kk, n = n0 + nn;
-        const int f = k / j.cp_in, c = k - f * j.cp_in;
+        int f = (int)((float)k * rcp_in);  // k / cp_in: float estimate, exact correction
+        f += (f + 1) * j.cp_in <= k ? 1 : 0;
+        f -= f * j.cp_in > k ? 1 : 0;
+        const int c = k - f * j.cp_in;
         const bool ok = f < j.A && c < j.c_in && n < j.c_out;
         const T w = W[ok ? ((int64_t)f * j.c_in + c) * j.c_out + n : 0];
         v[u] = ok ? w : zero;
@@ -111,7 +115,10 @@ __global__ void __launch_bounds__(256) k_pack_all(PackArgs pa) {
         const int i = (int)threadIdx.x + u * 256;
         const int nn = i / PACK_K, kk = i % PACK_K;
         const int c = n0 + nn, k = k0 + kk;
-        const int f = k / j.cp_out, o = k - f * j.cp_out;
+        int f = (int)((float)k * rcp_out);
+        f += (f + 1) * j.cp_out <= k ? 1 : 0;
+        f -= f * j.cp_out > k ? 1 : 0;
+        const int o = k - f * j.cp_out;
         const bool ok = f < j.A && o < j.c_out && c < j.c_in;
         const T w = W[ok ? ((int64_t)f * j.c_in + c) * j.c_out + o : 0];
         v[u] = ok ? w : zero;
