@@ -98,6 +98,25 @@ def test_workload_parity_full_size(name, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_pen_stroke_net_at_batch_400(dtype):
+    """DeepCNet(5,50) on the pen-stroke generator at four times the measured batch (a point of
+    the batch sweep): more output tiles than a launch's grid holds, so the GEMM, first-layer
+    and weight-gradient kernels walk their tiles and row blocks in grid-stride loops, and
+    the first layer's weight gradient reaches the split-K chunk limit."""
+    import dataclasses
+    base = get_config("deepcnet5_50_strokes_b100")
+    cfg = dataclasses.replace(base, batch=400, name=f"{base.name}@400")
+    b, Ws, bs, labels = _config_case(cfg, dtype)
+    log(f"[batch-400] {dtype} n={b.n}")
+    pair = Pair(cfg.ell, cfg.k, cfg.c_in, cfg.n_classes, cfg.batch, b.coords, b.feats, Ws, bs, labels, dtype,
+                max_active=b.n).run_gpu()
+    check_structure(pair)
+    rep = check_values(pair)
+    worst = {k_: v for k_, v in rep.items() if not k_.startswith(("argmax", "relu"))}
+    log(f"  worst rel err {max(worst.values()):.3g} ({max(worst, key=worst.get)})")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_stage_kernels_on_oracle_inputs(dtype):
     """Each stage fed the oracle's exact input: pools bit-exact (values and argmax), convs to tolerance."""
     cfg = get_config("deepcnet4_20_strokes_b8")
