@@ -619,6 +619,76 @@ def counter_summary(group, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir,
     print("\n".join(lines))
 
 
+def traffic_table(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, trace_dir, out, title, commands):
+    """A markdown table of every kernel's HBM traffic: FETCH_SIZE and WRITE_SIZE per dispatch (scaled by
+    what the counters read for a 256 MiB device copy) averaged per kernel, launches per step (dispatches
+    relative to the weight packing's, which runs once a step; rounded), and the average duration from a
+    kernel trace of the same build, so bytes over time per launch."""
+    import csv
+    import glob
+    n_copy = 256 << 20
+
+    def per_kernel(d, counter):
+        disp = {}
+        for name, c, v, di in _counter_rows(d):
+            if c.startswith(counter):
+                key = (name, di)
+                disp[key] = disp.get(key, 0.0) + v  # summed over the counter's instances
+        out_ = {}
+        for (name, _), v in disp.items():
+            out_.setdefault(name, []).append(v)
+        return out_
+
+    cf = max(per_kernel(copy_fetch_dir, "FETCH_SIZE").items(), key=lambda kv: max(kv[1]) if "opy" in kv[0] else 0)
+    cw = max(per_kernel(copy_write_dir, "WRITE_SIZE").items(), key=lambda kv: max(kv[1]) if "opy" in kv[0] else 0)
+    fs, ws = n_copy / (max(cf[1]) * 1024.0), n_copy / (max(cw[1]) * 1024.0)
+    fetch, write = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+    dur = {}
+    for path in glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                dur[r["Name"]] = float(r["AverageNs"]) / 1e3
+    ref = [k for k in fetch if "k_pack_all" in k]
+    steps = len(fetch[ref[0]]) if ref else 1
+    rows = []
+    for name in fetch:
+        if name not in write or "rocclr" in name or "at::native" in name:
+            continue
+        per_step = len(fetch[name]) // steps  # (the rulebook also runs once per resident batch to size them)
+        if per_step < 1:
+            continue
+        rd = float(np.mean(fetch[name])) * 1024 * fs
+        wr = float(np.mean(write[name])) * 1024 * ws
+        us = dur.get(name)
+        rows.append((name, per_step, rd, wr, us))
+    tot = sum(n * (rd + wr) for _, n, rd, wr, _ in rows)
+    rows.sort(key=lambda r: -r[1] * (r[2] + r[3]))
+    lines = [f"# {title}", "", "Commands (repository root):", "```"] + list(commands) + ["```", "",
+             f"FETCH_SIZE scale {fs:.4f}, WRITE_SIZE scale {ws:.4f} (bytes per KiB-count x 1024 that a 256 MiB "
+             f"device copy reads and writes); {steps} steps in the counter runs; durations from the kernel "
+             "trace of the same build (every launch of the kernel averaged).", "",
+             "| kernel | launches per step | MB read per launch | MB written per launch | MB per step | "
+             "avg us | GB/s | % of step traffic |", "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for name, n, rd, wr, us in rows:
+        nm = name.replace("|", "/")
+        if len(nm) > 90:
+            nm = nm[:34] + "..." + nm[-53:]
+        gbs = f"{(rd + wr) / (us * 1e3):.0f}" if us else "–"
+        lines.append(f"| `{nm}` | {n} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | {n * (rd + wr) / 1e6:.2f} | "
+                     f"{us:.2f} | {gbs} | {100 * n * (rd + wr) / tot:.1f} |" if us else
+                     f"| `{nm}` | {n} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | {n * (rd + wr) / 1e6:.2f} | – | – | "
+                     f"{100 * n * (rd + wr) / tot:.1f} |")
+    lines += ["", f"Total per step: {tot / 1e6:.1f} MB.", "",
+              "Names: `k_gemm_gather` modes -1 plain, -2 with the pooling forward, 0 and 4 with the pooling "
+              "backward (4: the children's ground pattern from the rulebook's masks); `GCfg<T, WM, WN, TM, TN>` "
+              "is a (16 WM TM) x (16 WN TN) tile, `k_gemm_direct<SK, mode>` the 32 x 64 direct kernel with SK "
+              "waves per tile; the demangler drops the template values of the two routed 64 x 64 "
+              "`k_gemm_gather` instantiations, which differ in their last value (the mode)."]
+    with open(out, "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def trace_summary(trace_dir, out, title, command, top=30):
     """A markdown table of a rocprofv3 --kernel-trace --stats run's per-kernel statistics."""
     import csv
@@ -769,6 +839,9 @@ def main():
                          "this benchmark and of --calibrate-copy (no GPU needed)")
     ap.add_argument("--group", default="k_gemm_direct 32x64: input gradient + pooling backward")
     ap.add_argument("--commands", nargs="*", default=[], help="the commands that made the counter runs")
+    ap.add_argument("--traffic-table", nargs=6,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR", "TRACE_DIR", "OUT_MD"),
+                    help="per-kernel HBM traffic of a step from rocprofv3 FETCH_SIZE / WRITE_SIZE runs")
     ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "OUT_MD"),
                     help="a markdown table of a rocprofv3 --kernel-trace --stats run (no GPU needed)")
     ap.add_argument("--title", default="Kernel trace")
@@ -783,6 +856,9 @@ def main():
         return
     if args.counter_summary:
         counter_summary(args.group, *args.counter_summary, args.workload, args.dtype, args.commands)
+        return
+    if args.traffic_table:
+        traffic_table(*args.traffic_table, args.title, args.commands)
         return
     if args.trace_summary:
         trace_summary(args.trace_summary[0], args.trace_summary[1], args.title,
